@@ -1,0 +1,229 @@
+"""CPU oracle for the ECOKV eviction pass -- TEST INFRASTRUCTURE ONLY.
+
+Python marshalling around ``ecokv_oracle.c`` (plain C, double precision).  Only
+``tests/``, ``__graft_entry__.smoke()`` and the benchmark's ``cpu_baseline`` leg
+may import this package; the HIP product path never does.  Nothing here
+imports the HIP package, and the C source shares nothing with it.
+
+Functions follow the paper's steps (see ``ecokv_oracle.c`` for citations):
+``score_unit`` (Sec. 3 and Sec. 5, Eqs. (1)-(7), Algorithm 1), ``score`` (all
+units of a tensor), ``select`` (Sec. 3 selection; AdaKV layer-flat budget,
+Appendix A.1) and ``compact`` (gather of the kept rows).
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import math
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ecokv_oracle.c")
+_LIB = os.path.join(_HERE, "libecokv_oracle.so")
+
+NSTATS = 12
+STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7,
+            imp_mean=8, sbar_mean=9, mu_norm2=10, scale=11)
+PER_HEAD, LAYER_FLAT = 0, 1
+BF16, F32 = 0, 1
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (double precision, no fast-math)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fopenmp",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("alpha", ctypes.c_double), ("beta", ctypes.c_double), ("eps", ctypes.c_double),
+                ("tau", ctypes.c_double), ("pool_kernel", ctypes.c_int), ("causal", ctypes.c_int),
+                ("lambda_override", ctypes.c_double)]
+
+
+_TRACE_FIELDS = ["a", "imp", "dE", "cosmu", "sC", "sE", "sdiv", "sbar", "stilde", "kbar", "mu", "rowmass"]
+
+
+class _Trace(ctypes.Structure):
+    _fields_ = [(n, ctypes.POINTER(ctypes.c_double)) for n in _TRACE_FIELDS]
+
+
+@dataclasses.dataclass
+class Params:
+    alpha: float = 0.8            # Table 6
+    beta: float = 0.6             # Table 6
+    eps: float = 1e-6
+    tau: float = 0.0              # <= 0 -> sqrt(D)  (Sec. 5.2)
+    pool_kernel: int = 5          # Table 6
+    causal: bool = True
+    lambda_override: float = math.nan
+
+    def c(self) -> _Params:
+        return _Params(self.alpha, self.beta, self.eps, self.tau, int(self.pool_kernel),
+                       int(bool(self.causal)), self.lambda_override)
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        L = ctypes.CDLL(_LIB)
+        vp, i32p, dp = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)
+        L.ora_score_unit.argtypes = [vp, vp, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                     ctypes.c_int, ctypes.c_int, ctypes.POINTER(_Params), dp, dp,
+                                     ctypes.POINTER(_Trace)]
+        L.ora_score.argtypes = [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                i32p, ctypes.c_int, ctypes.c_int, ctypes.POINTER(_Params), dp, dp, ctypes.c_int]
+        L.ora_select_unit.argtypes = [dp, ctypes.c_int, ctypes.c_int, ctypes.c_int, i32p]
+        L.ora_select_flat.argtypes = [dp, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                      ctypes.c_int, i32p, i32p]
+        L.ora_select.argtypes = [dp, ctypes.c_int, ctypes.c_int, ctypes.c_int, i32p, ctypes.c_int, i32p,
+                                 ctypes.c_int, i32p, i32p, i32p, ctypes.c_int]
+        L.ora_compact.argtypes = [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, i32p,
+                                  ctypes.c_int, i32p, i32p, i32p, vp, vp]
+        _lib = L
+    return _lib
+
+
+def _dp(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _ip(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _dtype_code(a: np.ndarray) -> int:
+    if a.dtype == np.uint16:
+        return BF16
+    if a.dtype == np.float32:
+        return F32
+    raise TypeError("oracle inputs are bf16 bit patterns (uint16) or float32")
+
+
+def score_unit(K: np.ndarray, Q: np.ndarray, w: int, params: Optional[Params] = None,
+               trace: bool = False) -> dict:
+    """Score one (layer, KV head, sequence) unit.
+
+    K: [T, D] keys (uint16 bf16 bits or float32).  Q: [G, w, D] window queries of
+    the G query heads sharing this KV head.  Returns ``S`` [P] (float64),
+    ``stats`` [NSTATS] and, with ``trace``, every intermediate of the paper's
+    steps (a, imp, dE, cosmu, sC, sE, sdiv, sbar, stilde, kbar, mu, rowmass).
+    """
+    p = params or Params()
+    K = np.ascontiguousarray(K)
+    Q = np.ascontiguousarray(Q)
+    code = _dtype_code(K)
+    assert _dtype_code(Q) == code and K.ndim == 2 and Q.ndim == 3
+    T, D = K.shape
+    G = Q.shape[0]
+    assert Q.shape[1] == w and Q.shape[2] == D
+    P = T - w
+    S = np.zeros(max(P, 0), np.float64)
+    stats = np.zeros(NSTATS, np.float64)
+    out = {"S": S, "stats": stats}
+    tr_ptr = None
+    if trace:
+        sizes = dict(a=P, imp=P, dE=T, cosmu=P, sC=P, sE=P, sdiv=P, sbar=P, stilde=P, kbar=D, mu=D,
+                     rowmass=G * w)
+        arrs = {k: np.zeros(v, np.float64) for k, v in sizes.items()}
+        tr = _Trace(*[_dp(arrs[n]) for n in _TRACE_FIELDS])
+        tr_ptr = ctypes.byref(tr)
+        out.update(arrs)
+    pc = p.c()
+    rc = lib().ora_score_unit(K.ctypes.data, Q.ctypes.data, w * D, code, T, D, G, w, ctypes.byref(pc),
+                              _dp(S), _dp(stats), tr_ptr)
+    if rc != 0:
+        raise ValueError(f"oracle rejected the unit (rc={rc})")
+    return out
+
+
+def score(K, Q, L, Hq, Hkv, cu_seqlens, D, w, params: Optional[Params] = None, nthreads: int = 1):
+    """Score every unit.  K [L][Hkv][Ttot][D], Q [L][Hq][B][w][D].
+
+    Returns S [L][Hkv][Ptot] (float64) and stats [L][Hkv][B][NSTATS]."""
+    p = params or Params()
+    K = np.ascontiguousarray(K)
+    Q = np.ascontiguousarray(Q)
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    B = len(cu) - 1
+    Ptot = int(cu[-1]) - B * w
+    S = np.zeros((L, Hkv, Ptot), np.float64)
+    stats = np.zeros((L, Hkv, B, NSTATS), np.float64)
+    pc = p.c()
+    rc = lib().ora_score(K.ctypes.data, Q.ctypes.data, _dtype_code(K), L, Hq, Hkv, B, _ip(cu), D, w,
+                         ctypes.byref(pc), _dp(S), _dp(stats), nthreads)
+    if rc != 0:
+        raise ValueError(f"oracle rejected the shape (rc={rc})")
+    return S, stats
+
+
+def select_unit(S: np.ndarray, T: int, w: int, b: int) -> np.ndarray:
+    S = np.ascontiguousarray(S, dtype=np.float64)
+    out = np.zeros(min(b, T), np.int32)
+    n = lib().ora_select_unit(_dp(S), T, w, b, _ip(out))
+    if n < 0:
+        raise ValueError("invalid selection arguments")
+    return out
+
+
+def select_flat(S_heads: np.ndarray, T: int, w: int, b: int):
+    """S_heads [H][P]: returns (idx packed head-major, counts [H])."""
+    S_heads = np.ascontiguousarray(S_heads, dtype=np.float64)
+    H = S_heads.shape[0]
+    out = np.zeros(H * min(b, T), np.int32)
+    counts = np.zeros(H, np.int32)
+    n = lib().ora_select_flat(_dp(S_heads), S_heads.shape[1], H, T, w, b, _ip(out), _ip(counts))
+    if n < 0:
+        raise ValueError("invalid selection arguments")
+    return out, counts
+
+
+def index_count(L, Hkv, cu_seqlens, budget) -> int:
+    B = len(cu_seqlens) - 1
+    return L * Hkv * sum(min(int(budget[s]), int(cu_seqlens[s + 1] - cu_seqlens[s])) for s in range(B))
+
+
+def select(S, L, Hkv, cu_seqlens, w, budget, mode=PER_HEAD, nthreads: int = 1):
+    """Select over every unit; returns idx (packed), counts [L][Hkv][B], offsets [L][Hkv][B]."""
+    S = np.ascontiguousarray(S, dtype=np.float64)
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    bud = np.ascontiguousarray(budget, dtype=np.int32)
+    B = len(cu) - 1
+    idx = np.zeros(index_count(L, Hkv, cu, bud), np.int32)
+    counts = np.zeros((L, Hkv, B), np.int32)
+    offsets = np.zeros((L, Hkv, B), np.int32)
+    rc = lib().ora_select(_dp(S), L, Hkv, B, _ip(cu), w, _ip(bud), mode, _ip(idx), _ip(counts),
+                          _ip(offsets), nthreads)
+    if rc != 0:
+        raise ValueError("invalid selection arguments")
+    return idx, counts, offsets
+
+
+def compact(K, V, L, Hkv, cu_seqlens, D, idx, counts, offsets):
+    """Gather the kept rows of K and V (exact byte copies)."""
+    K = np.ascontiguousarray(K)
+    V = np.ascontiguousarray(V)
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    B = len(cu) - 1
+    n = int(np.asarray(idx).size)
+    Kc = np.zeros((n, D), K.dtype)
+    Vc = np.zeros((n, D), V.dtype)
+    rc = lib().ora_compact(K.ctypes.data, V.ctypes.data, K.dtype.itemsize, L, Hkv, B, _ip(cu), D,
+                           _ip(np.ascontiguousarray(idx, np.int32)),
+                           _ip(np.ascontiguousarray(counts, np.int32)),
+                           _ip(np.ascontiguousarray(offsets, np.int32)), Kc.ctypes.data, Vc.ctypes.data)
+    if rc != 0:
+        raise ValueError("index out of range")
+    return Kc, Vc
