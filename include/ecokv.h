@@ -1,0 +1,167 @@
+/*
+ * ecokv.h -- C ABI of libecokv.so, the gfx950 (MI355X) implementation of the
+ * prefill-time KV-cache eviction pass of ECOKV ("Geometry-Aware KV Cache
+ * Eviction via Complementary Diversity Metrics", arXiv 2609.06663).
+ *
+ * The pass, for every (layer, KV head, sequence) "unit":
+ *   ecokv_score   importance of each non-window key from the observation window
+ *                 (Sec. 3; SnapKV, Appendix A.1; mean over the window, Sec. 5.2;
+ *                 average pool, Table 6), composite diversity (Sec. 5.1,
+ *                 Eqs. (1)-(3)), head redundancy weight lambda (Sec. 5.2,
+ *                 Eqs. (4)-(6)) and the final score S (Sec. 5.2, Eq. (7)).
+ *   ecokv_select  top-k of S over the non-window keys plus the whole window
+ *                 (Sec. 3), per head or shared across the heads of a layer
+ *                 (AdaKV budget sharing, Appendix A.1).
+ *   ecokv_compact gather of the kept K/V rows into the compressed cache
+ *                 (Sec. 3, selected subset).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All tensor pointers are DEVICE pointers unless stated; the caller
+ *    allocates and owns every buffer (inputs, outputs, workspace).  The library
+ *    never allocates or frees device memory, never synchronises, and keeps no
+ *    mutable global state: calls on different streams with different
+ *    workspaces may run concurrently.
+ *  - `stream` is a hipStream_t passed as void*; NULL means the null stream.
+ *    Work is enqueued asynchronously; results are valid once the stream has
+ *    been synchronised.
+ *  - Return value: ECOKV_OK, or a negative error code.  Every argument check
+ *    runs on the host before anything is enqueued, so an error leaves every
+ *    output untouched.  ecokv_last_error() describes the last failure of the
+ *    calling thread.  Device faults surface at the caller's next synchronise.
+ *  - Layouts are row-major and contiguous:
+ *      K, V   [L][H_kv][Ttot][D]   sequence s of a (varlen) batch occupies
+ *                                  rows cu_seqlens[s] .. cu_seqlens[s+1]-1
+ *      Q_win  [L][H_q][B][w][D]    the last w query rows of every query head;
+ *                                  query head q belongs to KV head q / (H_q/H_kv)
+ *      scores [L][H_kv][Ptot]      Ptot = Ttot - B*w; sequence s starts at
+ *                                  cu_seqlens[s] - s*w (non-window keys only)
+ *      per-unit arrays [L][H_kv][B] (unit u = (l*H_kv + h)*B + s)
+ *  - Positions stored in idx are relative to the start of their sequence.
+ */
+#ifndef ECOKV_H
+#define ECOKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ECOKV_OK 0
+#define ECOKV_EINVAL (-1)       /* bad shape, parameter or NULL pointer          */
+#define ECOKV_EWORKSPACE (-2)   /* workspace smaller than ecokv_workspace_size   */
+#define ECOKV_EUNSUPPORTED (-3) /* valid request this build does not implement   */
+#define ECOKV_EHIP (-4)         /* the HIP runtime refused a launch              */
+
+#define ECOKV_BF16 0 /* bfloat16 elements (2 bytes) */
+#define ECOKV_F32 1  /* float32 elements  (4 bytes) */
+
+#define ECOKV_PER_HEAD 0   /* each unit keeps exactly min(b_s, T_s) tokens    */
+#define ECOKV_LAYER_FLAT 1 /* the H_kv heads of (layer, sequence) share       */
+                           /* H_kv*min(b_s, T_s) places (AdaKV, App. A.1)     */
+
+#define ECOKV_MAX_SEQS 64   /* sequences per call                              */
+#define ECOKV_MAX_ROWS 64   /* window rows per KV head, (H_q/H_kv)*w           */
+
+/* Per-unit statistics written by ecokv_score when `stats` is non-NULL. */
+#define ECOKV_STAT_LAMBDA 0    /* lambda = beta r_E + (1-beta) r_C, Eq. (6)      */
+#define ECOKV_STAT_RC 1        /* cosine redundancy (T|mu|^2-1)/(T-1), App. A.1  */
+#define ECOKV_STAT_RE 2        /* 2 - 2 sigmoid(D_E/tau), Eq. (5)                */
+#define ECOKV_STAT_DE 3        /* mean distance to the centroid, Eq. (4)         */
+#define ECOKV_STAT_DMIN 4      /* min / max of d_E over the non-window keys      */
+#define ECOKV_STAT_DMAX 5
+#define ECOKV_STAT_SDIV_MIN 6  /* min / max of S_div, Eq. (3)                    */
+#define ECOKV_STAT_SDIV_MAX 7
+#define ECOKV_STAT_IMP_MEAN 8  /* mean of the pooled importance S_imp            */
+#define ECOKV_STAT_SBAR_MEAN 9 /* mean of the min-max normalised S_div           */
+#define ECOKV_STAT_MU_NORM2 10 /* |mu|^2                                         */
+#define ECOKV_STAT_SCALE 11    /* mean(S_imp) / (mean(S_bar) + eps)              */
+#define ECOKV_NSTATS 12
+
+/* Shape of one call.  cu_seqlens is a HOST array of num_seqs+1 nondecreasing
+ * offsets with cu_seqlens[0] = 0; a fixed-length batch of one sequence of T
+ * tokens is {0, T}.  Every sequence needs 1 <= window < T_s. */
+typedef struct ecokv_shape {
+    int32_t num_layers;         /* L >= 0 (0: nothing to do)                     */
+    int32_t num_q_heads;        /* H_q, a multiple of H_kv                       */
+    int32_t num_kv_heads;       /* H_kv >= 1                                     */
+    int32_t head_dim;           /* D: 64 or 128                                  */
+    int32_t window;             /* w >= 1, the observation window (Sec. 5.3)     */
+    int32_t num_seqs;           /* B in [1, ECOKV_MAX_SEQS]                      */
+    const int32_t *cu_seqlens;  /* host, [B+1]                                   */
+} ecokv_shape;
+
+/* Hyper-parameters (Table 6 defaults via ecokv_default_params). */
+typedef struct ecokv_params {
+    float alpha;            /* Euclidean weight of S_div, Eq. (3); 0.8            */
+    float beta;             /* Euclidean weight of lambda, Eq. (6); 0.6           */
+    float eps;              /* guard of the min-max and mean ratios; 1e-6         */
+    float tau;              /* temperature of Eq. (5); <= 0 selects sqrt(D)       */
+    int32_t pool_kernel;    /* odd average-pool width for S_imp; 5                */
+    int32_t causal;         /* 1: window row j sees keys <= T-w+j; 0: all keys    */
+    float lambda_override;  /* NaN: lambda from Eq. (6); else this fixed value    */
+} ecokv_params;
+
+/* Fills *p with the paper's defaults: alpha 0.8, beta 0.6, eps 1e-6,
+ * tau sqrt(D), pool 5, causal, no override.  Returns ECOKV_OK. */
+int ecokv_default_params(ecokv_params *p);
+
+/* Bytes of device workspace ecokv_score needs for this shape (select and
+ * compact need none).  The workspace is scratch: its contents are undefined
+ * between calls and it must not be shared by calls that may overlap. */
+int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, size_t *bytes);
+
+/* Score every unit (Sec. 3 and Sec. 5, Eqs. (1)-(7)).
+ *   K      [L][H_kv][Ttot][D]  keys, element type `dtype`
+ *   Q_win  [L][H_q][B][w][D]   window queries, element type `dtype`
+ *   scores [L][H_kv][Ptot]     float32 output S for the non-window keys
+ *   lambda [L][H_kv][B]        float32 output, may be NULL
+ *   stats  [L][H_kv][B][ECOKV_NSTATS] float32 output, may be NULL
+ *   workspace, workspace_bytes: device scratch of ecokv_workspace_size bytes,
+ *   256-byte aligned.
+ * Arithmetic: fp32 accumulation of bf16/fp32 inputs. */
+int ecokv_score(const void *K, const void *Q_win, int dtype, const ecokv_shape *shape,
+                const ecokv_params *params, float *scores, float *lambda, float *stats,
+                void *workspace, size_t workspace_bytes, void *stream);
+
+/* Number of int32 entries ecokv_select writes to idx:
+ * L * H_kv * sum_s min(budget[s], T_s) (both modes). */
+int ecokv_index_count(const ecokv_shape *shape, const int32_t *budget, int64_t *count);
+
+/* Select the kept positions (Sec. 3; AdaKV, Appendix A.1).
+ *   scores  [L][H_kv][Ptot] float32, as written by ecokv_score
+ *   budget  HOST [B]: b_s = tokens kept per head for sequence s, window
+ *           included, b_s >= w.  b_s >= T_s keeps every token.
+ *   mode    ECOKV_PER_HEAD: unit (l,h,s) keeps the b_s - w highest scores
+ *           (equal scores: smaller position first), listed ascending, then the
+ *           window T_s-w .. T_s-1.  Units are laid out in (l, h, s) order.
+ *           ECOKV_LAYER_FLAT: the H_kv heads of (l, s) compete for
+ *           H_kv*(b_s - w) places (equal scores: smaller (head, position)
+ *           first); each head lists its chosen positions ascending, then its
+ *           window.  Groups are laid out in (l, s) order, heads in order.
+ *   idx     output, ecokv_index_count entries
+ *   counts  [L][H_kv][B] output: entries of each unit (may be NULL in PER_HEAD)
+ *   offsets [L][H_kv][B] output: start of each unit in idx (may be NULL in
+ *           PER_HEAD)
+ * NaN scores rank below every number; -0 ranks equal to +0. */
+int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const int32_t *budget,
+                 int32_t *idx, int32_t *counts, int32_t *offsets, void *stream);
+
+/* Gather Kc[e] = K[row of entry e], Vc[e] = V[row of entry e] for every idx
+ * entry e, bit-exact (Sec. 3).  `mode` and `budget` as given to ecokv_select;
+ * counts and offsets are required for ECOKV_LAYER_FLAT (device arrays written
+ * by ecokv_select) and ignored for ECOKV_PER_HEAD.  Kc, Vc have
+ * ecokv_index_count rows of D elements. */
+int ecokv_compact(const void *K, const void *V, int dtype, const ecokv_shape *shape, int mode,
+                  const int32_t *budget, const int32_t *idx, const int32_t *counts,
+                  const int32_t *offsets, void *Kc, void *Vc, void *stream);
+
+/* Message for the calling thread's last failed call ("" if none). */
+const char *ecokv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ECOKV_H */

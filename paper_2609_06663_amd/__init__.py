@@ -1,0 +1,11 @@
+"""ECOKV prefill-time KV-cache eviction pass on AMD MI355X (gfx950).
+
+The product is ``libecokv.so`` (C ABI in ``include/ecokv.h``); ``ecokv`` is
+its thin Python binding.  ``pipeline`` strings the three calls together for
+torch tensors.
+"""
+from .ecokv import (  # noqa: F401
+    BF16, F32, PER_HEAD, LAYER_FLAT, NSTATS, STAT, EcoKVError, Params, Shape,
+    ecokv_compact, ecokv_default_params, ecokv_index_count, ecokv_last_error, ecokv_score,
+    ecokv_select, ecokv_workspace_size,
+)

@@ -1,0 +1,280 @@
+// C entry points of libecokv: host-side argument checks, workspace layout and
+// launches.  Every check completes before anything is enqueued.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "ecokv_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+struct ShapeInfo {
+    int L, Hq, Hkv, G, D, w, B, R;
+    int64_t Ttot, Ptot;
+    int maxT, maxP;
+};
+
+int check_shape(const ecokv_shape *sh, ShapeInfo *o)
+{
+    if (!sh) return fail(ECOKV_EINVAL, "shape is NULL");
+    if (sh->num_layers < 0) return fail(ECOKV_EINVAL, "num_layers %d < 0", sh->num_layers);
+    if (sh->num_kv_heads < 1) return fail(ECOKV_EINVAL, "num_kv_heads %d < 1", sh->num_kv_heads);
+    if (sh->num_q_heads < sh->num_kv_heads || sh->num_q_heads % sh->num_kv_heads != 0)
+        return fail(ECOKV_EINVAL, "num_q_heads %d is not a positive multiple of num_kv_heads %d", sh->num_q_heads,
+                    sh->num_kv_heads);
+    if (sh->head_dim != 64 && sh->head_dim != 128)
+        return fail(ECOKV_EUNSUPPORTED, "head_dim %d (supported: 64, 128)", sh->head_dim);
+    if (sh->window < 1) return fail(ECOKV_EINVAL, "window %d < 1", sh->window);
+    if (sh->num_seqs < 1 || sh->num_seqs > ECOKV_MAX_SEQS)
+        return fail(ECOKV_EINVAL, "num_seqs %d outside [1, %d]", sh->num_seqs, ECOKV_MAX_SEQS);
+    if (!sh->cu_seqlens) return fail(ECOKV_EINVAL, "cu_seqlens is NULL");
+    if (sh->cu_seqlens[0] != 0) return fail(ECOKV_EINVAL, "cu_seqlens[0] = %d, must be 0", sh->cu_seqlens[0]);
+    o->maxT = 0;
+    for (int s = 0; s < sh->num_seqs; ++s) {
+        const int64_t T = (int64_t)sh->cu_seqlens[s + 1] - sh->cu_seqlens[s];
+        if (T <= sh->window)
+            return fail(ECOKV_EINVAL, "sequence %d has %lld tokens; the window %d must be shorter", s, (long long)T,
+                        sh->window);
+        if (T > o->maxT) o->maxT = (int)T;
+    }
+    o->L = sh->num_layers;
+    o->Hq = sh->num_q_heads;
+    o->Hkv = sh->num_kv_heads;
+    o->G = o->Hq / o->Hkv;
+    o->D = sh->head_dim;
+    o->w = sh->window;
+    o->B = sh->num_seqs;
+    o->R = o->G * o->w;
+    o->Ttot = sh->cu_seqlens[o->B];
+    o->Ptot = o->Ttot - (int64_t)o->B * o->w;
+    o->maxP = o->maxT - o->w;
+    if ((int64_t)o->L * o->Hkv * o->B > (int64_t)INT32_MAX / 8)
+        return fail(ECOKV_EINVAL, "too many (layer, head, sequence) units");
+    return ECOKV_OK;
+}
+
+int check_params(const ecokv_params *p)
+{
+    if (!p) return fail(ECOKV_EINVAL, "params is NULL");
+    if (!(isfinite(p->alpha) && isfinite(p->beta) && isfinite(p->eps) && isfinite(p->tau)))
+        return fail(ECOKV_EINVAL, "alpha, beta, eps and tau must be finite");
+    if (p->eps < 0.f) return fail(ECOKV_EINVAL, "eps %g < 0", (double)p->eps);
+    if (p->pool_kernel < 1 || p->pool_kernel % 2 == 0)
+        return fail(ECOKV_EINVAL, "pool_kernel %d must be odd and >= 1", p->pool_kernel);
+    if (p->causal != 0 && p->causal != 1) return fail(ECOKV_EINVAL, "causal must be 0 or 1");
+    if (isinf(p->lambda_override)) return fail(ECOKV_EINVAL, "lambda_override must be NaN or finite");
+    return ECOKV_OK;
+}
+
+int fill_seqtab(const ecokv_shape *sh, const int32_t *budget, int w, ecokv::SeqTab *t, int64_t *per_lh)
+{
+    memset(t, 0, sizeof *t);
+    t->nseq = sh->num_seqs;
+    for (int s = 0; s <= sh->num_seqs; ++s) t->cu[s] = sh->cu_seqlens[s];
+    int64_t acc = 0;
+    t->boff[0] = 0;
+    for (int s = 0; s < sh->num_seqs; ++s) {
+        const int T = sh->cu_seqlens[s + 1] - sh->cu_seqlens[s];
+        int b = T;
+        if (budget) {
+            if (budget[s] < w)
+                return fail(ECOKV_EINVAL, "budget[%d] = %d is below the window %d", s, budget[s], w);
+            b = budget[s] < T ? budget[s] : T;
+        }
+        t->beff[s] = b;
+        acc += b;
+        if (acc > INT32_MAX) return fail(ECOKV_EINVAL, "budget sum overflows");
+        t->boff[s + 1] = (int)acc;
+    }
+    if (per_lh) *per_lh = acc;
+    return ECOKV_OK;
+}
+
+int hip_fail(hipError_t e, const char *what)
+{
+    return fail(ECOKV_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+int ecokv_default_params(ecokv_params *p)
+{
+    if (!p) return fail(ECOKV_EINVAL, "params is NULL");
+    p->alpha = 0.8f;
+    p->beta = 0.6f;
+    p->eps = 1e-6f;
+    p->tau = 0.f;
+    p->pool_kernel = 5;
+    p->causal = 1;
+    p->lambda_override = NAN;
+    return ECOKV_OK;
+}
+
+int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, size_t *bytes)
+{
+    ShapeInfo si;
+    int rc = check_shape(shape, &si);
+    if (rc) return rc;
+    if ((rc = check_params(params))) return rc;
+    if (!bytes) return fail(ECOKV_EINVAL, "bytes is NULL");
+    if (si.R > ECOKV_MAX_ROWS)
+        return fail(ECOKV_EUNSUPPORTED, "(H_q/H_kv)*window = %d exceeds %d", si.R, ECOKV_MAX_ROWS);
+    *bytes = ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, si.maxP).total;
+    return ECOKV_OK;
+}
+
+int ecokv_score(const void *K, const void *Q_win, int dtype, const ecokv_shape *shape, const ecokv_params *params,
+                float *scores, float *lambda, float *stats, void *workspace, size_t workspace_bytes, void *stream)
+{
+    ShapeInfo si;
+    int rc = check_shape(shape, &si);
+    if (rc) return rc;
+    if ((rc = check_params(params))) return rc;
+    if (dtype != ECOKV_BF16 && dtype != ECOKV_F32) return fail(ECOKV_EUNSUPPORTED, "dtype %d", dtype);
+    if (si.R > ECOKV_MAX_ROWS)
+        return fail(ECOKV_EUNSUPPORTED, "(H_q/H_kv)*window = %d exceeds %d", si.R, ECOKV_MAX_ROWS);
+    if (si.L == 0) return ECOKV_OK;
+    if (!K || !Q_win || !scores) return fail(ECOKV_EINVAL, "K, Q_win and scores must be non-NULL");
+    const ecokv::WsLayout lay = ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, si.maxP);
+    if (!workspace) return fail(ECOKV_EINVAL, "workspace is NULL");
+    if (((uintptr_t)workspace & 255u) != 0) return fail(ECOKV_EINVAL, "workspace must be 256-byte aligned");
+    if (workspace_bytes < lay.total)
+        return fail(ECOKV_EWORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
+
+    ecokv::ScoreArgs a;
+    memset(&a, 0, sizeof a);
+    a.K = K;
+    a.Q = Q_win;
+    a.scores = scores;
+    a.lambda = lambda;
+    a.stats = stats;
+    a.L = si.L;
+    a.Hq = si.Hq;
+    a.Hkv = si.Hkv;
+    a.G = si.G;
+    a.D = si.D;
+    a.w = si.w;
+    a.R = si.R;
+    a.B = si.B;
+    a.Ttot = si.Ttot;
+    a.Ptot = si.Ptot;
+    a.alpha = params->alpha;
+    a.beta = params->beta;
+    a.eps = params->eps;
+    a.tau = params->tau > 0.f ? params->tau : sqrtf((float)si.D);
+    a.inv_sqrt_d = 1.f / sqrtf((float)si.D);
+    a.use_override = isnan(params->lambda_override) ? 0 : 1;
+    a.lambda_override = a.use_override ? params->lambda_override : 0.f;
+    a.pool_half = params->pool_kernel / 2;
+    a.causal = params->causal;
+    if ((rc = fill_seqtab(shape, nullptr, si.w, &a.seq, nullptr))) return rc;
+    const hipError_t e = ecokv::score_launch(a, static_cast<char *>(workspace), lay, si.maxT, si.maxP,
+                                             static_cast<hipStream_t>(stream), dtype == ECOKV_BF16);
+    if (e != hipSuccess) return hip_fail(e, "ecokv_score launch");
+    return ECOKV_OK;
+}
+
+int ecokv_index_count(const ecokv_shape *shape, const int32_t *budget, int64_t *count)
+{
+    ShapeInfo si;
+    int rc = check_shape(shape, &si);
+    if (rc) return rc;
+    if (!budget || !count) return fail(ECOKV_EINVAL, "budget and count must be non-NULL");
+    ecokv::SeqTab t;
+    int64_t per_lh = 0;
+    if ((rc = fill_seqtab(shape, budget, si.w, &t, &per_lh))) return rc;
+    *count = (int64_t)si.L * si.Hkv * per_lh;
+    return ECOKV_OK;
+}
+
+int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const int32_t *budget, int32_t *idx,
+                 int32_t *counts, int32_t *offsets, void *stream)
+{
+    ShapeInfo si;
+    int rc = check_shape(shape, &si);
+    if (rc) return rc;
+    if (mode != ECOKV_PER_HEAD && mode != ECOKV_LAYER_FLAT) return fail(ECOKV_EINVAL, "mode %d", mode);
+    if (!budget) return fail(ECOKV_EINVAL, "budget is NULL");
+    ecokv::SelectArgs a;
+    memset(&a, 0, sizeof a);
+    int64_t per_lh = 0;
+    if ((rc = fill_seqtab(shape, budget, si.w, &a.seq, &per_lh))) return rc;
+    if ((int64_t)si.L * si.Hkv * per_lh > INT32_MAX) return fail(ECOKV_EINVAL, "index count overflows int32");
+    if (mode == ECOKV_LAYER_FLAT) {
+        if (!counts || !offsets) return fail(ECOKV_EINVAL, "LAYER_FLAT needs counts and offsets");
+        if (si.Hkv > ecokv::select_max_flat_heads())
+            return fail(ECOKV_EUNSUPPORTED, "LAYER_FLAT supports at most %d KV heads", ecokv::select_max_flat_heads());
+    }
+    if (si.L == 0) return ECOKV_OK;
+    if (!scores || !idx) return fail(ECOKV_EINVAL, "scores and idx must be non-NULL");
+    a.scores = scores;
+    a.idx = idx;
+    a.counts = counts;
+    a.offsets = offsets;
+    a.L = si.L;
+    a.Hkv = si.Hkv;
+    a.B = si.B;
+    a.w = si.w;
+    a.Ptot = si.Ptot;
+    a.per_lh = per_lh;
+    a.flat = mode == ECOKV_LAYER_FLAT;
+    const hipError_t e = ecokv::select_launch(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "ecokv_select launch");
+    return ECOKV_OK;
+}
+
+int ecokv_compact(const void *K, const void *V, int dtype, const ecokv_shape *shape, int mode, const int32_t *budget,
+                  const int32_t *idx, const int32_t *counts, const int32_t *offsets, void *Kc, void *Vc,
+                  void *stream)
+{
+    ShapeInfo si;
+    int rc = check_shape(shape, &si);
+    if (rc) return rc;
+    if (dtype != ECOKV_BF16 && dtype != ECOKV_F32) return fail(ECOKV_EUNSUPPORTED, "dtype %d", dtype);
+    if (mode != ECOKV_PER_HEAD && mode != ECOKV_LAYER_FLAT) return fail(ECOKV_EINVAL, "mode %d", mode);
+    if (!budget) return fail(ECOKV_EINVAL, "budget is NULL");
+    ecokv::CompactArgs a;
+    memset(&a, 0, sizeof a);
+    int64_t per_lh = 0;
+    if ((rc = fill_seqtab(shape, budget, si.w, &a.seq, &per_lh))) return rc;
+    if (mode == ECOKV_LAYER_FLAT && !offsets) return fail(ECOKV_EINVAL, "LAYER_FLAT needs offsets");
+    (void)counts;
+    if (si.L == 0) return ECOKV_OK;
+    if (!K || !V || !idx || !Kc || !Vc) return fail(ECOKV_EINVAL, "K, V, idx, Kc and Vc must be non-NULL");
+    a.K = static_cast<const char *>(K);
+    a.V = static_cast<const char *>(V);
+    a.Kc = static_cast<char *>(Kc);
+    a.Vc = static_cast<char *>(Vc);
+    a.idx = idx;
+    a.offsets = offsets;
+    a.L = si.L;
+    a.Hkv = si.Hkv;
+    a.B = si.B;
+    a.flat = mode == ECOKV_LAYER_FLAT;
+    a.Ttot = si.Ttot;
+    a.row_bytes = si.D * (dtype == ECOKV_BF16 ? 2 : 4);
+    a.segs = a.row_bytes / 16;
+    a.total = (int64_t)si.L * si.Hkv * per_lh;
+    a.per_lh = per_lh;
+    const hipError_t e = ecokv::compact_launch(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "ecokv_compact launch");
+    return ECOKV_OK;
+}
+
+const char *ecokv_last_error(void) { return g_err; }
+
+}  // extern "C"

@@ -1,0 +1,61 @@
+// ecokv_compact kernel (gfx950): gather of the kept K/V rows (Sec. 3).
+//
+// A flat grid over (entry, 16-byte segment): consecutive threads copy
+// consecutive 16-byte pieces of one row, so both the row read and the
+// compacted write are coalesced streams.  The unit of an entry follows from
+// the documented idx layout (PER_HEAD: arithmetic; LAYER_FLAT: the group by
+// arithmetic, the head from the offsets written by ecokv_select).  Entries
+// whose position lies outside [0, T_s) are skipped.
+#include "ecokv_internal.h"
+
+namespace ecokv {
+
+
+
+constexpr int kCompactThreads = 256;
+
+__global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a)
+{
+    const int64_t t = (int64_t)blockIdx.x * kCompactThreads + threadIdx.x;
+    const int64_t e = t / a.segs;
+    if (e >= a.total) return;
+    const int seg = (int)(t - e * a.segs);
+    int l, h, s;
+    if (!a.flat) {
+        const int64_t lh = e / a.per_lh;
+        const int64_t r = e - lh * a.per_lh;
+        s = 0;
+        while (s + 1 < a.B && a.seq.boff[s + 1] <= r) ++s;
+        l = (int)(lh / a.Hkv);
+        h = (int)(lh - (int64_t)l * a.Hkv);
+    } else {
+        const int64_t gl = (int64_t)a.Hkv * a.per_lh;
+        l = (int)(e / gl);
+        const int64_t r = e - (int64_t)l * gl;
+        s = 0;
+        while (s + 1 < a.B && (int64_t)a.Hkv * a.seq.boff[s + 1] <= r) ++s;
+        h = 0;
+        while (h + 1 < a.Hkv && a.offsets[((int64_t)l * a.Hkv + h + 1) * a.B + s] <= e) ++h;
+    }
+    const int T = a.seq.cu[s + 1] - a.seq.cu[s];
+    const int32_t pos = a.idx[e];
+    if (pos < 0 || pos >= T) return;
+    const int64_t src = ((int64_t)l * a.Hkv + h) * a.Ttot + a.seq.cu[s] + pos;
+    const int64_t so = src * a.row_bytes + (int64_t)seg * 16;
+    const int64_t d = e * a.row_bytes + (int64_t)seg * 16;
+    const uint4 kv = *reinterpret_cast<const uint4 *>(a.K + so);
+    const uint4 vv = *reinterpret_cast<const uint4 *>(a.V + so);
+    *reinterpret_cast<uint4 *>(a.Kc + d) = kv;
+    *reinterpret_cast<uint4 *>(a.Vc + d) = vv;
+}
+
+hipError_t compact_launch(const CompactArgs &a, hipStream_t st)
+{
+    const int64_t threads = a.total * a.segs;
+    if (threads == 0) return hipSuccess;
+    const int64_t blocks = (threads + kCompactThreads - 1) / kCompactThreads;
+    hipLaunchKernelGGL(k_compact, dim3((unsigned)blocks), dim3(kCompactThreads), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace ecokv

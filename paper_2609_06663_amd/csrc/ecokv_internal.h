@@ -1,0 +1,198 @@
+// Internal definitions of libecokv (gfx950).  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ecokv.h"
+
+namespace ecokv {
+
+constexpr int kWave = 64;
+
+// Per-call table of sequence boundaries and budgets, passed by value as a
+// kernel argument so that no device copy of host arrays is needed.
+struct SeqTab {
+    int nseq;
+    int cu[ECOKV_MAX_SEQS + 1];    // token offsets (prefix of T_s)
+    int beff[ECOKV_MAX_SEQS];      // min(b_s, T_s)
+    int boff[ECOKV_MAX_SEQS + 1];  // prefix of beff
+};
+
+// Decode unit u = (l*Hkv + h)*B + s.
+struct Unit {
+    int l, h, s;
+};
+__device__ __forceinline__ Unit unit_of(int u, int Hkv, int B)
+{
+    Unit r;
+    r.s = u % B;
+    const int lh = u / B;
+    r.h = lh % Hkv;
+    r.l = lh / Hkv;
+    return r;
+}
+
+// Internal per-unit statistics kept in the workspace (superset of the ABI stats).
+enum {
+    HS_LAMBDA = 0, HS_RC, HS_RE, HS_DE, HS_DMIN, HS_DMAX, HS_SDMIN, HS_SDMAX, HS_IMPMEAN,
+    HS_SBARMEAN, HS_MU2, HS_SCALE, HS_COUNT = 16
+};
+static_assert(ECOKV_NSTATS <= HS_COUNT, "stat layout");
+
+struct ScoreArgs {
+    const void *K;
+    const void *Q;
+    float *scores;
+    float *lambda;
+    float *stats;
+    // workspace regions
+    float *part1;    // [U][nch1][2D + 2R]  column sums, row max / sum-exp per chunk
+    float *anchors;  // [U][2D + 2R]        kbar, mu, row max, row sum
+    float *part2;    // [U][nch1][4]        sum d_E, min d_E, max d_E
+    float *hstat;    // [U][HS_COUNT]
+    float *bufA;     // [L][Hkv][Ptot]      d_E, then S_div
+    float *bufB;     // [L][Hkv][Ptot]      khat.mu, then S_imp
+    float *bufC;     // [L][Hkv][Ptot]      window-mean attention a
+    float *part3;    // [U][nch3][4]        min/max/sum S_div, sum S_imp
+    unsigned *counters;  // [U][4]
+    int L, Hq, Hkv, G, D, w, R, B;
+    int64_t Ttot, Ptot;
+    int nch1, nch3;
+    float alpha, beta, eps, tau, inv_sqrt_d, lambda_override;
+    int use_override, pool_half, causal;
+    SeqTab seq;
+};
+
+struct SelectArgs {
+    const float *scores;
+    int32_t *idx;
+    int32_t *counts;
+    int32_t *offsets;
+    int L, Hkv, B, w;
+    int64_t Ptot;
+    int64_t per_lh;  // sum over s of min(b_s, T_s)
+    int flat;
+    SeqTab seq;
+};
+
+struct CompactArgs {
+    const char *K;
+    const char *V;
+    char *Kc;
+    char *Vc;
+    const int32_t *idx;
+    const int32_t *offsets;
+    int L, Hkv, B, flat;
+    int64_t Ttot;
+    int row_bytes;
+    int segs;          // row_bytes / 16
+    int64_t total;     // entries
+    int64_t per_lh;
+    SeqTab seq;
+};
+
+// Workspace layout, shared by the size query and the launcher.
+struct WsLayout {
+    size_t part1, anchors, part2, hstat, bufA, bufB, bufC, part3, counters, total;
+};
+
+WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, int maxP);
+hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, int maxP, hipStream_t st,
+                        bool bf16);
+hipError_t select_launch(const SelectArgs &a, hipStream_t st);
+int select_max_flat_heads();
+hipError_t compact_launch(const CompactArgs &a, hipStream_t st);
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t x) { return __uint_as_float((uint32_t)x << 16); }
+
+// Sum over the 16 lanes of an aligned 16-lane segment; every lane gets the total.
+__device__ __forceinline__ float seg16_sum(float x)
+{
+    x += __shfl_xor(x, 8, 16);
+    x += __shfl_xor(x, 4, 16);
+    x += __shfl_xor(x, 2, 16);
+    x += __shfl_xor(x, 1, 16);
+    return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x)
+{
+    for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, kWave);
+    return x;
+}
+__device__ __forceinline__ float wave_min(float x)
+{
+    for (int m = 32; m >= 1; m >>= 1) x = fminf(x, __shfl_xor(x, m, kWave));
+    return x;
+}
+__device__ __forceinline__ float wave_max(float x)
+{
+    for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m, kWave));
+    return x;
+}
+
+// Load the VEC = D/16 elements of segment c of a key row as float.
+template <int D, bool BF>
+__device__ __forceinline__ void load_seg(const void *row, int c, float *v)
+{
+    constexpr int VEC = D / 16;
+    if constexpr (BF) {
+        const uint16_t *p = static_cast<const uint16_t *>(row) + c * VEC;
+        if constexpr (VEC == 8) {
+            const uint4 q = *reinterpret_cast<const uint4 *>(p);
+            const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                v[2 * e] = __uint_as_float(w4[e] << 16);
+                v[2 * e + 1] = __uint_as_float(w4[e] & 0xffff0000u);
+            }
+        } else {
+            const uint2 q = *reinterpret_cast<const uint2 *>(p);
+            v[0] = __uint_as_float(q.x << 16);
+            v[1] = __uint_as_float(q.x & 0xffff0000u);
+            v[2] = __uint_as_float(q.y << 16);
+            v[3] = __uint_as_float(q.y & 0xffff0000u);
+        }
+    } else {
+        const float *p = static_cast<const float *>(row) + c * VEC;
+        if constexpr (VEC == 8) {
+            const float4 a = reinterpret_cast<const float4 *>(p)[0];
+            const float4 b = reinterpret_cast<const float4 *>(p)[1];
+            v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+            v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+        } else {
+            const float4 a = reinterpret_cast<const float4 *>(p)[0];
+            v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        }
+    }
+}
+
+// Release this block's global writes and count it in; returns true (to every
+// thread) in the last block of `expected` to arrive, after an acquire fence.
+// The last block resets the counter to zero for the next call.
+__device__ __forceinline__ bool last_block_arrives(unsigned *counter, unsigned expected, int *flag_lds)
+{
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const unsigned prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        *flag_lds = (prev == expected - 1) ? 1 : 0;
+    }
+    __syncthreads();
+    const bool last = *flag_lds != 0;
+    if (last) __threadfence();
+    return last;
+}
+
+// Order-preserving map of a float score to an unsigned radix key: larger
+// score -> larger key; -0 maps like +0; NaN maps below every number.
+__device__ __forceinline__ uint32_t score_key(float f)
+{
+    uint32_t b = __float_as_uint(f);
+    if (f != f) return 0u;
+    if (b == 0x80000000u) b = 0u;
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+}  // namespace ecokv

@@ -1,0 +1,177 @@
+"""Thin Python binding of libecokv.so (argument marshalling only).
+
+Every step of the eviction pass runs in the HIP kernels behind the C ABI
+declared in ``include/ecokv.h``; this module turns torch tensors into device
+pointers, the current HIP stream into a handle, and error codes into
+exceptions.  PyTorch provides device memory and streams only.  If the built
+library is missing, importing this module raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libecokv.so")
+
+OK, EINVAL, EWORKSPACE, EUNSUPPORTED, EHIP = 0, -1, -2, -3, -4
+BF16, F32 = 0, 1
+PER_HEAD, LAYER_FLAT = 0, 1
+MAX_SEQS, MAX_ROWS = 64, 64
+NSTATS = 12
+STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7, imp_mean=8, sbar_mean=9,
+            mu_norm2=10, scale=11)
+
+EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_score", "ecokv_index_count",
+           "ecokv_select", "ecokv_compact", "ecokv_last_error"]
+
+
+class EcoKVError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libecokv error {code}: {msg}")
+        self.code = code
+
+
+class _Shape(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("window", ctypes.c_int32), ("num_seqs", ctypes.c_int32),
+                ("cu_seqlens", ctypes.POINTER(ctypes.c_int32))]
+
+
+class Params(ctypes.Structure):
+    """ecokv_params; defaults are the paper's (Table 6)."""
+    _fields_ = [("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("eps", ctypes.c_float),
+                ("tau", ctypes.c_float), ("pool_kernel", ctypes.c_int32), ("causal", ctypes.c_int32),
+                ("lambda_override", ctypes.c_float)]
+
+    def __init__(self, alpha=0.8, beta=0.6, eps=1e-6, tau=0.0, pool_kernel=5, causal=True,
+                 lambda_override=math.nan):
+        super().__init__(alpha, beta, eps, tau, int(pool_kernel), int(bool(causal)), lambda_override)
+
+
+class Shape:
+    """ecokv_shape plus the host array of sequence offsets it points to."""
+
+    def __init__(self, num_layers: int, num_q_heads: int, num_kv_heads: int, head_dim: int, window: int,
+                 cu_seqlens: Sequence[int]):
+        self.cu = (ctypes.c_int32 * len(cu_seqlens))(*[int(x) for x in cu_seqlens])
+        self.c = _Shape(num_layers, num_q_heads, num_kv_heads, head_dim, window, len(cu_seqlens) - 1,
+                        ctypes.cast(self.cu, ctypes.POINTER(ctypes.c_int32)))
+
+    @property
+    def cu_seqlens(self):
+        return list(self.cu)
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2609_06663_amd.build`")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, sp, pp = ctypes.c_void_p, ctypes.POINTER(_Shape), ctypes.POINTER(Params)
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    lib.ecokv_default_params.argtypes = [pp]
+    lib.ecokv_workspace_size.argtypes = [sp, pp, ctypes.POINTER(ctypes.c_size_t)]
+    lib.ecokv_score.argtypes = [vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.ecokv_index_count.argtypes = [sp, i32p, ctypes.POINTER(ctypes.c_int64)]
+    lib.ecokv_select.argtypes = [vp, sp, ctypes.c_int, i32p, vp, vp, vp, vp]
+    lib.ecokv_compact.argtypes = [vp, vp, ctypes.c_int, sp, ctypes.c_int, i32p, vp, vp, vp, vp, vp, vp]
+    lib.ecokv_last_error.restype = ctypes.c_char_p
+    for name in EXPORTS:
+        if name != "ecokv_last_error":
+            getattr(lib, name).restype = ctypes.c_int
+    return lib
+
+
+lib = _load()
+
+
+def _check(rc: int):
+    if rc != OK:
+        raise EcoKVError(rc, lib.ecokv_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libecokv must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported element type {t.dtype} (bf16 or fp32)")
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _budget(shape: Shape, budget: Sequence[int]):
+    if len(budget) != shape.c.num_seqs:
+        raise ValueError("one budget per sequence")
+    return (ctypes.c_int32 * len(budget))(*[int(b) for b in budget])
+
+
+def ecokv_default_params() -> Params:
+    p = Params()
+    _check(lib.ecokv_default_params(ctypes.byref(p)))
+    return p
+
+
+def ecokv_workspace_size(shape: Shape, params: Optional[Params] = None) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib.ecokv_workspace_size(ctypes.byref(shape.c), ctypes.byref(params or Params()), ctypes.byref(n)))
+    return n.value
+
+
+def ecokv_score(K: torch.Tensor, Q_win: torch.Tensor, shape: Shape, params: Optional[Params],
+                scores: torch.Tensor, lambda_: Optional[torch.Tensor] = None,
+                stats: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                stream=None) -> None:
+    """Enqueue ecokv_score.  `workspace` (uint8, >= ecokv_workspace_size bytes) is
+    allocated here with torch when not given."""
+    p = params or Params()
+    if workspace is None:
+        workspace = torch.empty(ecokv_workspace_size(shape, p), dtype=torch.uint8, device=K.device)
+    if Q_win.dtype != K.dtype:
+        raise TypeError("K and Q_win must have the same element type")
+    _check(lib.ecokv_score(_ptr(K), _ptr(Q_win), _dtype_code(K), ctypes.byref(shape.c), ctypes.byref(p),
+                           _ptr(scores), _ptr(lambda_), _ptr(stats), _ptr(workspace),
+                           workspace.numel(), _stream(stream)))
+
+
+def ecokv_index_count(shape: Shape, budget: Sequence[int]) -> int:
+    n = ctypes.c_int64(0)
+    _check(lib.ecokv_index_count(ctypes.byref(shape.c), _budget(shape, budget), ctypes.byref(n)))
+    return n.value
+
+
+def ecokv_select(scores: torch.Tensor, shape: Shape, mode: int, budget: Sequence[int], idx: torch.Tensor,
+                 counts: Optional[torch.Tensor] = None, offsets: Optional[torch.Tensor] = None,
+                 stream=None) -> None:
+    _check(lib.ecokv_select(_ptr(scores), ctypes.byref(shape.c), int(mode), _budget(shape, budget), _ptr(idx),
+                            _ptr(counts), _ptr(offsets), _stream(stream)))
+
+
+def ecokv_compact(K: torch.Tensor, V: torch.Tensor, shape: Shape, mode: int, budget: Sequence[int],
+                  idx: torch.Tensor, counts: Optional[torch.Tensor], offsets: Optional[torch.Tensor],
+                  Kc: torch.Tensor, Vc: torch.Tensor, stream=None) -> None:
+    if V.dtype != K.dtype or Kc.dtype != K.dtype or Vc.dtype != K.dtype:
+        raise TypeError("K, V, Kc and Vc must share one element type")
+    _check(lib.ecokv_compact(_ptr(K), _ptr(V), _dtype_code(K), ctypes.byref(shape.c), int(mode),
+                             _budget(shape, budget), _ptr(idx), _ptr(counts), _ptr(offsets), _ptr(Kc),
+                             _ptr(Vc), _stream(stream)))
+
+
+def ecokv_last_error() -> str:
+    return lib.ecokv_last_error().decode()

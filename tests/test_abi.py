@@ -1,0 +1,130 @@
+"""The C ABI library loads and exports every entry point of include/ecokv.h,
+and its host-side argument checks reject bad calls before any device work.
+No GPU needed: every call here returns from host validation."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = []
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            names += re.findall(r"^(?:int|const char \*|size_t)\s*\*?\s*(ecokv_\w+)\s*\(", text, re.M)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def P():
+    import paper_2609_06663_amd as P
+    return P
+
+
+def test_header_declares_the_three_calls():
+    names = declared_functions()
+    for n in ("ecokv_score", "ecokv_select", "ecokv_compact", "ecokv_workspace_size", "ecokv_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(P):
+    from paper_2609_06663_amd import ecokv
+    lib = ctypes.CDLL(ecokv._LIB_PATH)
+    for n in declared_functions():
+        assert hasattr(lib, n), f"{n} is declared but not exported"
+    assert set(declared_functions()) == set(ecokv.EXPORTS)
+
+
+def test_default_params(P):
+    p = P.ecokv_default_params()
+    assert p.alpha == pytest.approx(0.8) and p.beta == pytest.approx(0.6)
+    assert p.pool_kernel == 5 and p.causal == 1 and p.lambda_override != p.lambda_override
+
+
+def test_workspace_and_index_count(P):
+    s = P.Shape(28, 28, 4, 128, 4, [0, 32768])
+    assert P.ecokv_workspace_size(s) > 0
+    assert P.ecokv_index_count(s, [6553]) == 28 * 4 * 6553
+    s2 = P.Shape(2, 8, 2, 64, 3, [0, 10, 15])
+    assert P.ecokv_index_count(s2, [4, 100]) == 2 * 2 * (4 + 5)
+
+
+@pytest.mark.parametrize("args,code", [
+    ((1, 4, 2, 96, 4, [0, 100]), -3),      # head_dim unsupported
+    ((1, 5, 2, 128, 4, [0, 100]), -1),     # H_q not a multiple of H_kv
+    ((1, 4, 2, 128, 0, [0, 100]), -1),     # window < 1
+    ((1, 4, 2, 128, 100, [0, 100]), -1),   # window >= T
+    ((1, 4, 2, 128, 4, [1, 100]), -1),     # cu_seqlens[0] != 0
+    ((1, 4, 2, 128, 4, [0, 50, 52]), -1),  # a sequence not longer than the window
+    ((-1, 4, 2, 128, 4, [0, 100]), -1),    # negative layers
+    ((1, 64, 2, 128, 4, [0, 100]), -3),    # (H_q/H_kv)*w = 128 rows > max
+])
+def test_bad_shapes_rejected(P, args, code):
+    with pytest.raises(P.EcoKVError) as e:
+        P.ecokv_workspace_size(P.Shape(*args))
+    assert e.value.code == code
+    assert P.ecokv_last_error()
+
+
+def test_too_many_sequences(P):
+    cu = list(range(0, 10 * 66, 10))
+    with pytest.raises(P.EcoKVError):
+        P.ecokv_workspace_size(P.Shape(1, 4, 2, 128, 4, cu))
+
+
+@pytest.mark.parametrize("field,value", [("pool_kernel", 4), ("pool_kernel", 0), ("eps", -1.0),
+                                         ("causal", 2), ("alpha", float("inf"))])
+def test_bad_params_rejected(P, field, value):
+    p = P.Params()
+    setattr(p, field, value)
+    with pytest.raises(P.EcoKVError) as e:
+        P.ecokv_workspace_size(P.Shape(1, 4, 2, 128, 4, [0, 100]), p)
+    assert e.value.code == -1
+
+
+def test_calls_fail_before_device_work(P):
+    """Null pointers, a short workspace, budgets below the window: rejected on the host."""
+    from paper_2609_06663_amd import ecokv as E
+    s = P.Shape(1, 4, 2, 128, 4, [0, 100])
+    p = P.Params()
+    ws = P.ecokv_workspace_size(s, p)
+    lib = E.lib
+    fake = ctypes.c_void_p(256)
+    # NULL K
+    rc = lib.ecokv_score(None, fake, 0, ctypes.byref(s.c), ctypes.byref(p), fake, None, None, fake, ws, None)
+    assert rc == -1
+    # workspace too small
+    rc = lib.ecokv_score(fake, fake, 0, ctypes.byref(s.c), ctypes.byref(p), fake, None, None, fake, ws - 1, None)
+    assert rc == -2
+    # misaligned workspace
+    rc = lib.ecokv_score(fake, fake, 0, ctypes.byref(s.c), ctypes.byref(p), fake, None, None,
+                         ctypes.c_void_p(260), ws, None)
+    assert rc == -1
+    # unsupported dtype
+    rc = lib.ecokv_score(fake, fake, 7, ctypes.byref(s.c), ctypes.byref(p), fake, None, None, fake, ws, None)
+    assert rc == -3
+    bud = (ctypes.c_int32 * 1)(3)   # below the window
+    rc = lib.ecokv_select(fake, ctypes.byref(s.c), 0, bud, fake, None, None, None)
+    assert rc == -1
+    bud = (ctypes.c_int32 * 1)(10)
+    rc = lib.ecokv_select(fake, ctypes.byref(s.c), 1, bud, fake, None, None, None)   # flat without counts
+    assert rc == -1
+    rc = lib.ecokv_select(fake, ctypes.byref(s.c), 5, bud, fake, None, None, None)   # bad mode
+    assert rc == -1
+    rc = lib.ecokv_compact(fake, None, 0, ctypes.byref(s.c), 0, bud, fake, None, None, fake, fake, None)
+    assert rc == -1
+    rc = lib.ecokv_compact(fake, fake, 0, ctypes.byref(s.c), 1, bud, fake, None, None, fake, fake, None)
+    assert rc == -1   # flat without offsets
+
+
+def test_empty_call_is_ok_without_device(P):
+    # L = 0: nothing to enqueue, success, no device access.
+    from paper_2609_06663_amd import ecokv as E
+    s = P.Shape(0, 4, 2, 128, 4, [0, 100])
+    p = P.Params()
+    rc = E.lib.ecokv_score(None, None, 0, ctypes.byref(s.c), ctypes.byref(p), None, None, None, None, 0, None)
+    assert rc == 0

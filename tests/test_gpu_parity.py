@@ -1,0 +1,303 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Every case draws seeded synthetic inputs (workloads/), runs score -> select ->
+compact on the GPU and compares with the oracle on the same bytes, to the
+tolerances stated in parity_utils.  Small and medium shapes are checked in
+full; the full-size shapes (28 layers x 32k tokens, 32 heads x 64k tokens)
+are checked on sampled units plus properties that hold everywhere.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from parity_utils import (check_scores, check_stats, check_unit_selection, dev, gpu_pass, oracle_params,
+                          oracle_unit, topk_rule, unit_slices, RTOL)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_06663_amd  # noqa: F401  (fails loudly if the library is not built)
+    oracle.build(force=False)
+
+
+def say(msg):
+    print(f"[gpu-parity] {msg}", file=sys.stderr, flush=True)
+
+
+def check_compact(wl, g):
+    cu = wl.cu_seqlens
+    for l in range(wl.L):
+        for h in range(wl.Hkv):
+            for s in range(wl.B):
+                o, n = int(g["offsets"][l, h, s]), int(g["counts"][l, h, s])
+                rows = g["idx"][o:o + n]
+                np.testing.assert_array_equal(g["Kc"][o:o + n], wl.K[l, h, cu[s] + rows])
+                np.testing.assert_array_equal(g["Vc"][o:o + n], wl.V[l, h, cu[s] + rows])
+
+
+def check_per_head(wl, g, units=None, params=None, stat_skip=()):
+    if units is None:
+        units = [(l, h, s) for l in range(wl.L) for h in range(wl.Hkv) for s in range(wl.B)]
+    ties = 0
+    for (l, h, s) in units:
+        T, off = unit_slices(wl, s)
+        P = T - wl.w
+        r = oracle_unit(wl, l, h, s, params)
+        Sg = g["scores"][l, h, off:off + P]
+        what = f"{wl.name} unit (l={l}, h={h}, s={s})"
+        floor = check_scores(Sg, r["S"], r["stats"][8], what)
+        check_stats(g["stats"][l, h, s], r["stats"], what, skip=stat_skip)
+        assert g["lambda_"][l, h, s] == g["stats"][l, h, s, 0]
+        o, n = int(g["offsets"][l, h, s]), int(g["counts"][l, h, s])
+        ties += check_unit_selection(g["idx"][o:o + n], Sg, r["S"], T, wl.w, wl.budget[s], floor, what)
+    return ties
+
+
+def check_all_selections_valid(wl, g):
+    """Properties that hold for every unit: count, window, order, range, top-k of the GPU scores."""
+    for l in range(wl.L):
+        for h in range(wl.Hkv):
+            for s in range(wl.B):
+                T, off = unit_slices(wl, s)
+                P, b = T - wl.w, wl.budget[s]
+                o, n = int(g["offsets"][l, h, s]), int(g["counts"][l, h, s])
+                assert n == min(b, T)
+                idx = g["idx"][o:o + n]
+                if b >= T:
+                    np.testing.assert_array_equal(idx, np.arange(T))
+                    continue
+                k = b - wl.w
+                np.testing.assert_array_equal(idx[k:], np.arange(P, T))
+                Sg = g["scores"][l, h, off:off + P]
+                np.testing.assert_array_equal(idx[:k], topk_rule(Sg, k))
+
+
+def test_tiny_full():
+    wl = W.tiny()
+    say("tiny: 1 layer, 2 heads, T=512, fp32")
+    g = gpu_pass(wl)
+    check_per_head(wl, g)
+    check_compact(wl, g)
+
+
+def test_layer7b_full():
+    wl = W.layer7b()
+    say("layer7b: 28q/4kv, T=8192, bf16, w=8, b=1638")
+    g = gpu_pass(wl)
+    check_per_head(wl, g)
+    check_compact(wl, g)
+
+
+def test_stack28_full_size_sampled():
+    wl = W.stack28()
+    say("stack28: 28 layers, 28q/4kv, T=32768, bf16, w=4, b=6553 (sampled oracle units)")
+    g = gpu_pass(wl)
+    check_all_selections_valid(wl, g)
+    check_compact(wl, g)
+    check_per_head(wl, g, units=[(0, 0, 0), (13, 2, 0), (27, 3, 0)])
+    # every lambda is a blend of two redundancies in [-1/(T-1), 1]
+    assert np.all(g["lambda_"] <= 1.0 + 1e-6) and np.all(g["lambda_"] > -1e-3)
+
+
+def test_mha64k_full_size_sampled():
+    wl = W.mha64k()
+    say("mha64k: 32 MHA heads, T=65536, bf16, w=8, b=2048 (sampled oracle units)")
+    g = gpu_pass(wl)
+    check_all_selections_valid(wl, g)
+    check_compact(wl, g)
+    check_per_head(wl, g, units=[(0, 0, 0), (0, 17, 0), (0, 31, 0)])
+
+
+def check_layer_flat(wl, g, params=None):
+    cu = wl.cu_seqlens
+    for l in range(wl.L):
+        for s in range(wl.B):
+            T, off = unit_slices(wl, s)
+            P, b = T - wl.w, wl.budget[s]
+            H = wl.Hkv
+            So = np.zeros((H, P))
+            Sg = g["scores"][l, :, off:off + P]
+            floor = 0.0
+            for h in range(H):
+                r = oracle_unit(wl, l, h, s, params)
+                So[h] = r["S"]
+                f = check_scores(Sg[h], r["S"], r["stats"][8], f"{wl.name} (l={l}, h={h}, s={s})")
+                check_stats(g["stats"][l, h, s], r["stats"], f"{wl.name} (l={l}, h={h}, s={s})")
+                floor = max(floor, f)
+            counts = g["counts"][l, :, s]
+            offs = g["offsets"][l, :, s]
+            assert counts.sum() == H * min(b, T)
+            if b >= T:
+                for h in range(H):
+                    np.testing.assert_array_equal(g["idx"][offs[h]:offs[h] + counts[h]], np.arange(T))
+                continue
+            assert np.all(offs[1:] == offs[:-1] + counts[:-1])
+            chosen_g = []
+            for h in range(H):
+                ent = g["idx"][offs[h]:offs[h] + counts[h]]
+                np.testing.assert_array_equal(ent[-wl.w:], np.arange(P, T))
+                sel = ent[:-wl.w]
+                assert np.all(np.diff(sel) > 0)
+                chosen_g += [h * P + i for i in sel]
+            ktot = H * (b - wl.w)
+            chosen_g = np.array(sorted(chosen_g), dtype=np.int64)
+            np.testing.assert_array_equal(chosen_g, topk_rule(Sg.reshape(-1), ktot))
+            flat_o = So.reshape(-1)
+            chosen_o = topk_rule(flat_o, ktot)
+            if ktot:
+                theta = np.sort(flat_o)[::-1][ktot - 1]
+                band = 2 * RTOL * max(abs(theta), floor) * (1 + 1e-6)
+                far = [v for v in np.setxor1d(chosen_g, chosen_o) if abs(flat_o[v] - theta) > band]
+                assert not far, f"layer-flat (l={l}, s={s}): {len(far)} disagreements outside the band"
+
+
+def test_varlen_layer_flat_full():
+    wl = W.varlen()
+    say(f"varlen layer-flat: 8 sequences {wl.seqlens}, 28q/4kv, bf16, w=4")
+    g = gpu_pass(wl)
+    check_layer_flat(wl, g)
+    check_compact(wl, g)
+
+
+# ---------------------------------------------------------------------------
+# edge cases
+# ---------------------------------------------------------------------------
+
+def test_ragged_varlen_per_head():
+    wl = W.custom(11, L=2, Hq=6, Hkv=2, D=128, w=3, seqlens=[129, 1000, 257, 4, 130], dtype="bf16",
+                  budget=[40, 300, 400, 3, 3 + 127], group=64)
+    say("ragged varlen per-head: seqlens [129, 1000, 257, 4, 130]")
+    g = gpu_pass(wl)
+    check_per_head(wl, g)
+    check_compact(wl, g)
+
+
+def test_head_dim_64_fp32_window_1():
+    wl = W.custom(12, L=1, Hq=8, Hkv=2, D=64, w=1, seqlens=[700], dtype="f32", budget=[97], group=32)
+    say("D=64 fp32 w=1 G=4")
+    g = gpu_pass(wl)
+    check_per_head(wl, g)
+    check_compact(wl, g)
+
+
+def test_max_window_rows():
+    wl = W.custom(13, L=1, Hq=16, Hkv=2, D=128, w=8, seqlens=[300], dtype="bf16", budget=[60], group=16)
+    say("G*w = 64 window rows")
+    g = gpu_pass(wl)
+    check_per_head(wl, g)
+
+
+def test_long_ragged_single_sequence():
+    wl = W.custom(14, L=1, Hq=4, Hkv=1, D=128, w=4, seqlens=[5003], dtype="bf16", budget=[777], group=128)
+    say("T=5003 single head")
+    g = gpu_pass(wl)
+    check_per_head(wl, g)
+    check_compact(wl, g)
+
+
+def test_identical_and_zero_keys():
+    # head 0: every key identical (zero diversity, lambda = 1); head 1: some zero keys.
+    wl = W.custom(15, L=1, Hq=4, Hkv=2, D=128, w=4, seqlens=[600], dtype="bf16", budget=[100], group=32)
+    wl.K[0, 0, :] = wl.K[0, 0, 17]
+    wl.K[0, 1, 5:9] = 0
+    wl.K[0, 1, 300] = 0
+    say("identical keys in head 0, zero keys in head 1")
+    g = gpu_pass(wl)
+    check_per_head(wl, g, units=[(0, 0, 0)], stat_skip=("dmin", "dmax", "D_E", "sdiv_min", "sdiv_max",
+                                                       "sbar_mean", "scale"))
+    check_per_head(wl, g, units=[(0, 1, 0)])
+    check_compact(wl, g)
+
+
+@pytest.mark.parametrize("variant", ["noncausal", "lambda0", "lambda1_alpha1", "mixkv", "pool1", "pool7",
+                                     "tau"])
+def test_parameter_variants(variant):
+    import paper_2609_06663_amd as P
+    p = {
+        "noncausal": P.Params(causal=False),
+        "lambda0": P.Params(lambda_override=0.0),
+        "lambda1_alpha1": P.Params(lambda_override=1.0, alpha=1.0),
+        "mixkv": P.Params(alpha=0.0, beta=0.0),
+        "pool1": P.Params(pool_kernel=1),
+        "pool7": P.Params(pool_kernel=7),
+        "tau": P.Params(tau=3.0),
+    }[variant]
+    wl = W.custom(16, L=1, Hq=8, Hkv=2, D=128, w=4, seqlens=[900, 333], dtype="bf16", budget=[150, 60],
+                  group=64)
+    say(f"parameter variant {variant}")
+    g = gpu_pass(wl, params=p)
+    check_per_head(wl, g, params=p)
+
+
+def test_budget_edges_per_head_and_flat():
+    import paper_2609_06663_amd as P
+    wl = W.custom(17, L=2, Hq=4, Hkv=2, D=128, w=5, seqlens=[300, 200, 150], dtype="bf16",
+                  budget=[5, 400, 149], group=32)
+    say("budgets b == w, b >= T, b = T - 1")
+    g = gpu_pass(wl, mode=P.PER_HEAD)
+    check_per_head(wl, g)
+    check_compact(wl, g)
+    wl.mode = "layer_flat"
+    g = gpu_pass(wl, mode=P.LAYER_FLAT)
+    check_layer_flat(wl, g)
+    check_compact(wl, g)
+
+
+def test_empty_layers_is_a_noop():
+    import paper_2609_06663_amd as P
+    shape = P.Shape(0, 4, 2, 128, 4, [0, 100])
+    x = torch.zeros(16, device="cuda")
+    P.ecokv_score(x, x, shape, None, x, workspace=torch.empty(256, dtype=torch.uint8, device="cuda"))
+    P.ecokv_select(x, shape, P.PER_HEAD, [10], x)
+    torch.cuda.synchronize()
+    assert torch.all(x == 0)
+
+
+def test_deterministic():
+    wl = W.layer7b(seed=21, T=4096)
+    say("determinism: two identical runs")
+    g1 = gpu_pass(wl)
+    g2 = gpu_pass(wl)
+    for k in ("scores", "stats", "idx", "Kc"):
+        np.testing.assert_array_equal(g1[k], g2[k])
+
+
+# ---------------------------------------------------------------------------
+# selection alone: bit-exact against the oracle on identical fp32 scores
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("mode", ["per_head", "layer_flat"])
+def test_select_bit_exact_with_ties(mode):
+    import paper_2609_06663_amd as P
+    rng = np.random.default_rng(5)
+    seqlens = [3000, 70, 1025, 9]
+    cu = np.concatenate([[0], np.cumsum(seqlens)]).tolist()
+    L, Hkv, w = 3, 4, 3
+    budget = [500, 71, 1025 // 2, 3]
+    Ptot = cu[-1] - len(seqlens) * w
+    S = rng.integers(0, 40, size=(L, Hkv, Ptot)).astype(np.float32) * np.float32(0.25) - np.float32(2.0)
+    S[0, 0, :50] = np.nan
+    S[1, 2, 10:20] = -0.0
+    S[1, 2, 20:30] = 0.0
+    m = P.PER_HEAD if mode == "per_head" else P.LAYER_FLAT
+    shape = P.Shape(L, 4 * Hkv, Hkv, 128, w, cu)
+    n = P.ecokv_index_count(shape, budget)
+    idx = torch.empty(n, dtype=torch.int32, device="cuda")
+    counts = torch.empty(L * Hkv * len(seqlens), dtype=torch.int32, device="cuda")
+    offsets = torch.empty_like(counts)
+    say(f"select-only bit-exact ({mode})")
+    P.ecokv_select(torch.from_numpy(S).cuda(), shape, m, budget, idx, counts, offsets)
+    torch.cuda.synchronize()
+    ref_idx, ref_c, ref_o = oracle.select(S.astype(np.float64), L, Hkv, cu, w, budget,
+                                          oracle.PER_HEAD if m == P.PER_HEAD else oracle.LAYER_FLAT)
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
+    np.testing.assert_array_equal(counts.cpu().numpy(), ref_c.reshape(-1))
+    np.testing.assert_array_equal(offsets.cpu().numpy(), ref_o.reshape(-1))
