@@ -133,7 +133,12 @@ int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, s
     if (!bytes) return fail(ECOKV_EINVAL, "bytes is NULL");
     if (si.R > ECOKV_MAX_ROWS)
         return fail(ECOKV_EUNSUPPORTED, "(H_q/H_kv)*window = %d exceeds %d", si.R, ECOKV_MAX_ROWS);
-    *bytes = ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, si.maxP).total;
+    *bytes = 0;  // the size depends on the element type; report the larger layout
+    {
+        const size_t b0 = ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, true).total;
+        const size_t b1 = ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, false).total;
+        *bytes = b0 > b1 ? b0 : b1;
+    }
     return ECOKV_OK;
 }
 
@@ -149,7 +154,8 @@ int ecokv_score(const void *K, const void *Q_win, int dtype, const ecokv_shape *
         return fail(ECOKV_EUNSUPPORTED, "(H_q/H_kv)*window = %d exceeds %d", si.R, ECOKV_MAX_ROWS);
     if (si.L == 0) return ECOKV_OK;
     if (!K || !Q_win || !scores) return fail(ECOKV_EINVAL, "K, Q_win and scores must be non-NULL");
-    const ecokv::WsLayout lay = ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, si.maxP);
+    const ecokv::WsLayout lay =
+        ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, dtype == ECOKV_BF16);
     if (!workspace) return fail(ECOKV_EINVAL, "workspace is NULL");
     if (((uintptr_t)workspace & 255u) != 0) return fail(ECOKV_EINVAL, "workspace must be 256-byte aligned");
     if (workspace_bytes < lay.total)
@@ -182,7 +188,7 @@ int ecokv_score(const void *K, const void *Q_win, int dtype, const ecokv_shape *
     a.pool_half = params->pool_kernel / 2;
     a.causal = params->causal;
     if ((rc = fill_seqtab(shape, nullptr, si.w, &a.seq, nullptr))) return rc;
-    const hipError_t e = ecokv::score_launch(a, static_cast<char *>(workspace), lay, si.maxT, si.maxP,
+    const hipError_t e = ecokv::score_launch(a, static_cast<char *>(workspace), lay, si.maxT,
                                              static_cast<hipStream_t>(stream), dtype == ECOKV_BF16);
     if (e != hipSuccess) return hip_fail(e, "ecokv_score launch");
     return ECOKV_OK;

@@ -33,13 +33,6 @@ __device__ __forceinline__ Unit unit_of(int u, int Hkv, int B)
     return r;
 }
 
-// Internal per-unit statistics kept in the workspace (superset of the ABI stats).
-enum {
-    HS_LAMBDA = 0, HS_RC, HS_RE, HS_DE, HS_DMIN, HS_DMAX, HS_SDMIN, HS_SDMAX, HS_IMPMEAN,
-    HS_SBARMEAN, HS_MU2, HS_SCALE, HS_COUNT = 16
-};
-static_assert(ECOKV_NSTATS <= HS_COUNT, "stat layout");
-
 struct ScoreArgs {
     const void *K;
     const void *Q;
@@ -47,18 +40,18 @@ struct ScoreArgs {
     float *lambda;
     float *stats;
     // workspace regions
-    float *part1;    // [U][nch1][2D + 2R]  column sums, row max / sum-exp per chunk
-    float *anchors;  // [U][2D + 2R]        kbar, mu, row max, row sum
-    float *part2;    // [U][nch1][4]        sum d_E, min d_E, max d_E
-    float *hstat;    // [U][HS_COUNT]
-    float *bufA;     // [L][Hkv][Ptot]      d_E, then S_div
-    float *bufB;     // [L][Hkv][Ptot]      khat.mu, then S_imp
+    float *part1;    // [U][nch1][2D + 2R]  column sums, row max / sum-exp per block
+    float *anchors;  // [U][2D + 2R]        kbar, mu, row max, row normaliser
+    float *part2;    // [U][nch1][4]        sum d_E, min d_E, max d_E per block
+    float *part3;    // [U][nch3][4]        sum S_div, sum S_imp, min/max S_div per block
+    float *bufA;     // [L][Hkv][Ptot]      d_E
+    float *bufB;     // [L][Hkv][Ptot]      khat.mu
     float *bufC;     // [L][Hkv][Ptot]      window-mean attention a
-    float *part3;    // [U][nch3][4]        min/max/sum S_div, sum S_imp
-    unsigned *counters;  // [U][4]
     int L, Hq, Hkv, G, D, w, R, B;
     int64_t Ttot, Ptot;
-    int nch1, nch3;
+    int nch1;        // sweep blocks per unit (for the longest sequence)
+    int nch3;        // epilogue blocks per unit
+    int rpb1;        // key rows per sweep block
     float alpha, beta, eps, tau, inv_sqrt_d, lambda_override;
     int use_override, pool_half, causal;
     SeqTab seq;
@@ -94,15 +87,24 @@ struct CompactArgs {
 
 // Workspace layout, shared by the size query and the launcher.
 struct WsLayout {
-    size_t part1, anchors, part2, hstat, bufA, bufB, bufC, part3, counters, total;
+    size_t part1, anchors, part2, part3, bufA, bufB, bufC, total;
 };
 
-WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, int maxP);
-hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, int maxP, hipStream_t st,
-                        bool bf16);
+WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16);
+hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hipStream_t st, bool bf16);
 hipError_t select_launch(const SelectArgs &a, hipStream_t st);
 int select_max_flat_heads();
 hipError_t compact_launch(const CompactArgs &a, hipStream_t st);
+
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() also
+// orders global memory, which makes every barrier wait for all outstanding
+// global loads; this one leaves prefetched loads in flight.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t x) { return __uint_as_float((uint32_t)x << 16); }
 
@@ -166,23 +168,6 @@ __device__ __forceinline__ void load_seg(const void *row, int c, float *v)
             v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
         }
     }
-}
-
-// Release this block's global writes and count it in; returns true (to every
-// thread) in the last block of `expected` to arrive, after an acquire fence.
-// The last block resets the counter to zero for the next call.
-__device__ __forceinline__ bool last_block_arrives(unsigned *counter, unsigned expected, int *flag_lds)
-{
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const unsigned prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        *flag_lds = (prev == expected - 1) ? 1 : 0;
-    }
-    __syncthreads();
-    const bool last = *flag_lds != 0;
-    if (last) __threadfence();
-    return last;
 }
 
 // Order-preserving map of a float score to an unsigned radix key: larger

@@ -2,45 +2,77 @@
 // final score of every (layer, KV head, sequence) unit.
 //
 // Stages, in stream order:
-//   pass1  one sweep over K: column sums of k and of k/|k| (anchors kbar, mu,
-//          Eq. (1) and the MixKV cosine anchor of Appendix A.1) and, per
-//          window row, the chunk's softmax max and sum of exponentials
-//          (Sec. 3 attention).  The last block of a unit combines the chunks.
-//   pass2  second sweep over K: per key d_E = |k - kbar| (Eq. (1)), khat.mu,
-//          and the window-mean attention a_i (Sec. 5.2, "average attention
-//          score").  The last block forms D_E (Eq. (4)), r_E (Eq. (5)),
-//          r_C (Appendix A.1) and lambda (Eq. (6)).
-//   epi1   per non-window key: pooled S_imp (Table 6), s_E (Eq. (2)),
-//          s_C, S_div (Eq. (3)); block min/max/sums, last block forms the
-//          rescale of Sec. 5.2.
-//   epi2   S = lambda * S_tilde + (1 - lambda) * S_imp (Eq. (7)).
+//   sweep1   one pass over K per block of rows: column sums of k and of k/|k|
+//            (centroid kbar, Eq. (1); mean normalised key mu, Appendix A.1)
+//            and, for every window row, the block's softmax maximum and sum of
+//            exponentials of q.k/sqrt(d_k) (Sec. 3 attention, causal window).
+//   reduce1  per unit: combine the block partials into kbar, mu and the
+//            per-row softmax maximum and normaliser.
+//   sweep2   second pass over K: per key d_E = |k - kbar| (Eq. (1)), khat.mu
+//            and the window-mean attention a_i (Sec. 5.2: average attention
+//            score over the window); block partials of sum/min/max d_E.
+//   epilogue per unit: D_E (Eq. (4)), r_E (Eq. (5)), r_C (Appendix A.1),
+//            lambda (Eq. (6)); pooled S_imp (Table 6), s_E (Eq. (2)), s_C,
+//            S_div (Eq. (3)); the rescale of Sec. 5.2 and S (Eq. (7)).
 //
-// Lane layout of the sweeps: 16 lanes per key row, each lane holding D/16
-// consecutive elements, so one wave reads 4 whole rows per instruction
-// (coalesced 1 KiB for bf16, D = 128) and row reductions stay inside a
-// 16-lane segment.
+// Two implementations of the sweeps:
+//   * bf16 with head_dim 128 (the shapes of the paper's models): a 128-key
+//     tile is staged through LDS (XOR-swizzled 16-byte chunks, conflict free
+//     for both read patterns).  Geometry runs on the VALU with 16 lanes per
+//     key row (DPP row reductions); the window logits run on the matrix
+//     cores, v_mfma_f32_32x32x16_bf16 with the window rows as the 32-row A
+//     operand and 32 keys per wave as the B operand.
+//   * any other case (fp32 inputs, head_dim 64): a plain VALU sweep with 16
+//     lanes per key row and window dot products reduced across the row.
 #include "ecokv_internal.h"
 
 namespace ecokv {
 
 constexpr int kThreads = 256;
-constexpr int kCh = 128;       // key rows per block in the sweeps
-constexpr int kEpi = 256;      // non-window keys per block in the epilogues
+constexpr int kCh = 128;        // key rows per block, generic sweeps
 
-__device__ __forceinline__ const char *unit_krow0(const ScoreArgs &a, const Unit &un, int esz)
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ int64_t unit_out_base(const ScoreArgs &a, const Unit &un)
 {
-    const int64_t row = ((int64_t)un.l * a.Hkv + un.h) * a.Ttot + a.seq.cu[un.s];
-    return static_cast<const char *>(a.K) + row * (int64_t)a.D * esz;
+    return ((int64_t)un.l * a.Hkv + un.h) * a.Ptot + (a.seq.cu[un.s] - un.s * a.w);
 }
 
-// Window row r = (g, j) of unit `un` as float into LDS q[r][D].
+__device__ __forceinline__ int64_t unit_row0(const ScoreArgs &a, const Unit &un)
+{
+    return ((int64_t)un.l * a.Hkv + un.h) * a.Ttot + a.seq.cu[un.s];
+}
+
+// Global row index of window row r = (g, j) of unit `un` in Q_win.
+__device__ __forceinline__ int64_t window_row(const ScoreArgs &a, const Unit &un, int r)
+{
+    const int g = r / a.w, j = r % a.w;
+    return (((int64_t)un.l * a.Hq + (int64_t)un.h * a.G + g) * a.B + un.s) * a.w + j;
+}
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Combine two softmax partials (max, sum of 2^(x - max)), x in log2 units.
+__device__ __forceinline__ void softmax_merge2(float &m, float &s, float m2, float s2)
+{
+    const float nm = fmaxf(m, m2);
+    const float a = (m == -INFINITY) ? 0.f : s * __builtin_amdgcn_exp2f(m - nm);
+    const float b = (m2 == -INFINITY) ? 0.f : s2 * __builtin_amdgcn_exp2f(m2 - nm);
+    m = nm;
+    s = a + b;
+}
+
+// ---------------------------------------------------------------------------
+// Generic sweeps (fp32 or head_dim 64): 16 lanes per key row.
+// ---------------------------------------------------------------------------
 template <int D, bool BF>
 __device__ void load_window_rows(const ScoreArgs &a, const Unit &un, float *q)
 {
     for (int idx = threadIdx.x; idx < a.R * D; idx += blockDim.x) {
         const int r = idx / D, d = idx % D;
-        const int g = r / a.w, j = r % a.w;
-        const int64_t qrow = (((int64_t)un.l * a.Hq + (int64_t)un.h * a.G + g) * a.B + un.s) * a.w + j;
+        const int64_t qrow = window_row(a, un, r);
         float v;
         if constexpr (BF)
             v = bf16_to_f32(static_cast<const uint16_t *>(a.Q)[qrow * D + d]);
@@ -58,7 +90,6 @@ __global__ __launch_bounds__(kThreads) void k_pass1(ScoreArgs a)
     __shared__ float q_lds[ECOKV_MAX_ROWS * D];
     __shared__ float lg[ECOKV_MAX_ROWS * (kCh + 1)];
     __shared__ float red[2][16][D];
-    __shared__ int flag;
 
     const int u = blockIdx.y;
     const Unit un = unit_of(u, a.Hkv, a.B);
@@ -66,14 +97,13 @@ __global__ __launch_bounds__(kThreads) void k_pass1(ScoreArgs a)
     const int P = T - a.w;
     const int row0 = blockIdx.x * kCh;
     if (row0 >= T) return;
-    const int nch = (T + kCh - 1) / kCh;
 
     load_window_rows<D, BF>(a, un, q_lds);
     __syncthreads();
 
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int c = lane & 15, sub = lane >> 4;
-    const char *k0 = unit_krow0(a, un, ESZ);
+    const char *k0 = static_cast<const char *>(a.K) + unit_row0(a, un) * D * ESZ;
     float sk[VEC], skh[VEC];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) sk[e] = skh[e] = 0.f;
@@ -107,7 +137,7 @@ __global__ __launch_bounds__(kThreads) void k_pass1(ScoreArgs a)
             d = seg16_sum(d);
             const int j = r % a.w;
             const bool vis = valid && (!a.causal || i <= P + j);
-            if (c == 0) lg[r * (kCh + 1) + rl] = vis ? d * a.inv_sqrt_d : -INFINITY;
+            if (c == 0) lg[r * (kCh + 1) + rl] = vis ? d * (a.inv_sqrt_d * kLog2e) : -INFINITY;
         }
     }
 #pragma unroll
@@ -124,7 +154,7 @@ __global__ __launch_bounds__(kThreads) void k_pass1(ScoreArgs a)
         for (int t = 0; t < kCh; ++t) m = fmaxf(m, lg[r * (kCh + 1) + t]);
         float s = 0.f;
         if (m > -INFINITY)
-            for (int t = 0; t < kCh; ++t) s += __expf(lg[r * (kCh + 1) + t] - m);
+            for (int t = 0; t < kCh; ++t) s += exp2f(lg[r * (kCh + 1) + t] - m);
         part[2 * D + r] = m;
         part[2 * D + a.R + r] = s;
     }
@@ -137,28 +167,6 @@ __global__ __launch_bounds__(kThreads) void k_pass1(ScoreArgs a)
         part[d] = s0;
         part[D + d] = s1;
     }
-
-    if (!last_block_arrives(a.counters + u * 4 + 0, nch, &flag)) return;
-
-    const float* pu = a.part1 + (int64_t)u * a.nch1 * stride;
-    float *anc = a.anchors + (int64_t)u * stride;
-    for (int d = threadIdx.x; d < 2 * D; d += blockDim.x) {
-        float s = 0.f;
-        for (int ch = 0; ch < nch; ++ch) s += pu[(int64_t)ch * stride + d];
-        anc[d] = s / (float)T;
-    }
-    for (int r = threadIdx.x; r < a.R; r += blockDim.x) {
-        float m = -INFINITY;
-        for (int ch = 0; ch < nch; ++ch) m = fmaxf(m, pu[(int64_t)ch * stride + 2 * D + r]);
-        float s = 0.f;
-        for (int ch = 0; ch < nch; ++ch) {
-            const float pm = pu[(int64_t)ch * stride + 2 * D + r];
-            if (pm > -INFINITY) s += pu[(int64_t)ch * stride + 2 * D + a.R + r] * __expf(pm - m);
-        }
-        anc[2 * D + r] = m;
-        anc[2 * D + a.R + r] = s;
-    }
-    if (threadIdx.x == 0) a.counters[u * 4 + 0] = 0;
 }
 
 template <int D, bool BF>
@@ -169,7 +177,6 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
     __shared__ float q_lds[ECOKV_MAX_ROWS * D];
     __shared__ float kb[D], mu[D], rm[ECOKV_MAX_ROWS], rs_inv[ECOKV_MAX_ROWS];
     __shared__ float wred[3][kThreads / kWave];
-    __shared__ int flag;
 
     const int u = blockIdx.y;
     const Unit un = unit_of(u, a.Hkv, a.B);
@@ -177,7 +184,6 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
     const int P = T - a.w;
     const int row0 = blockIdx.x * kCh;
     if (row0 >= T) return;
-    const int nch = (T + kCh - 1) / kCh;
     const int stride = 2 * D + 2 * a.R;
     const float *anc = a.anchors + (int64_t)u * stride;
 
@@ -194,8 +200,8 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
 
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int c = lane & 15, sub = lane >> 4;
-    const char *k0 = unit_krow0(a, un, ESZ);
-    const int64_t obase = ((int64_t)un.l * a.Hkv + un.h) * a.Ptot + (a.seq.cu[un.s] - un.s * a.w);
+    const char *k0 = static_cast<const char *>(a.K) + unit_row0(a, un) * D * ESZ;
+    const int64_t obase = unit_out_base(a, un);
     const float inv_r = 1.f / (float)a.R;
     float dsum = 0.f, dmin = INFINITY, dmax = -INFINITY;
 
@@ -229,7 +235,7 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
 #pragma unroll
             for (int e = 0; e < VEC; ++e) d += qr[e] * v[e];
             d = seg16_sum(d);
-            att += __expf(d * a.inv_sqrt_d - rm[r]) * rs_inv[r];
+            if (i < P) att += exp2f(d * (a.inv_sqrt_d * kLog2e) - rm[r]) * rs_inv[r];
         }
         if (valid) {
             dsum += (c == 0) ? dE : 0.f;
@@ -264,210 +270,773 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
         pp[0] = s;
         pp[1] = mn;
         pp[2] = mx;
-    }
-
-    if (!last_block_arrives(a.counters + u * 4 + 1, nch, &flag)) return;
-    if (threadIdx.x == 0) {
-        const float *pp = a.part2 + (int64_t)u * a.nch1 * 4;
-        float s = 0.f, mn = INFINITY, mx = -INFINITY;
-        for (int ch = 0; ch < nch; ++ch) {
-            s += pp[ch * 4 + 0];
-            mn = fminf(mn, pp[ch * 4 + 1]);
-            mx = fmaxf(mx, pp[ch * 4 + 2]);
-        }
-        float mu2 = 0.f;
-        for (int d = 0; d < D; ++d) mu2 += mu[d] * mu[d];
-        const float DE = s / (float)T;
-        const float rE = 2.f - 2.f / (1.f + expf(-DE / a.tau));
-        const float rC = ((float)T * mu2 - 1.f) / ((float)T - 1.f);
-        const float lam = a.use_override ? a.lambda_override : a.beta * rE + (1.f - a.beta) * rC;
-        float *hs = a.hstat + (int64_t)u * HS_COUNT;
-        hs[HS_LAMBDA] = lam;
-        hs[HS_RC] = rC;
-        hs[HS_RE] = rE;
-        hs[HS_DE] = DE;
-        hs[HS_DMIN] = mn;
-        hs[HS_DMAX] = mx;
-        hs[HS_MU2] = mu2;
-        a.counters[u * 4 + 1] = 0;
+        pp[3] = 0.f;
     }
 }
 
-__global__ __launch_bounds__(kEpi) void k_epi1(ScoreArgs a)
+// ---------------------------------------------------------------------------
+// bf16, head_dim 128: LDS-staged tiles, matrix-core window logits and
+// projections.
+// ---------------------------------------------------------------------------
+namespace fast {
+
+// Hot-loop transcendentals as single instructions (v_exp_f32, v_rsq_f32,
+// v_sqrt_f32, about 1 ulp).  Every exponent argument here is <= 0, so results
+// below 2^-126 (flushed to zero) are negligible next to the softmax terms of
+// size 1 they are added to.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+constexpr int kD = 128;
+constexpr int kChunks = 16;           // 16-byte chunks per key row
+constexpr int kTile = 128;            // keys per LDS tile (4 waves x 32 keys)
+#ifndef ECOKV_SWEEP_TILES
+#define ECOKV_SWEEP_TILES 8
+#endif
+#ifndef ECOKV_SWEEP1_DEPTH
+#define ECOKV_SWEEP1_DEPTH 2
+#endif
+#ifndef ECOKV_SWEEP2_DEPTH
+#define ECOKV_SWEEP2_DEPTH 2
+#endif
+constexpr int kTilesPerBlock = ECOKV_SWEEP_TILES;  // tiles per block (1024 keys by default)
+constexpr int kRows = kTile * kTilesPerBlock;
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x)
 {
-    __shared__ float wred[4][kEpi / kWave];
-    __shared__ int flag;
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over an aligned 16-lane row; every lane of the row gets the total.
+__device__ __forceinline__ float row16_sum(float x)
+{
+    x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+    x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+    x += dpp<0x141>(x);  // row_half_mirror
+    x += dpp<0x140>(x);  // row_mirror
+    return x;
+}
+
+__device__ __forceinline__ void unpack8(u32x4 q, float *v)
+{
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        v[2 * e] = __uint_as_float(q[e] << 16);
+        v[2 * e + 1] = __uint_as_float(q[e] & 0xffff0000u);
+    }
+}
+
+// acc + lo*lo + hi*hi of the two bf16 halves of w (v_dot2c_f32_bf16).
+__device__ __forceinline__ float dot2sq(unsigned w, float acc)
+{
+    const bf16x2 v = __builtin_bit_cast(bf16x2, w);
+    return __builtin_amdgcn_fdot2_f32_bf16(v, v, acc, false);
+}
+
+// Round-to-nearest-even bf16 of a finite float (bit pattern in the low half).
+__device__ __forceinline__ unsigned bf16_rne(float f)
+{
+    unsigned u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+// Swizzled position of 16-byte chunk c of tile row r.
+__device__ __forceinline__ int sw(int r, int c) { return r * kChunks + (c ^ (r & 15)); }
+
+// Buffer descriptor over the key rows [0, rows) of a unit (raw buffer, no
+// stride): loads at or past the end return zero without touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t key_rows_rsrc(const uint16_t *krow0, int rows)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(krow0), (short)0, rows * (kD * 2), 0x00020000);
+}
+
+// One 128-key tile into registers: 16 lanes per 256-byte row, coalesced.
+// Rows outside the descriptor's range come back as zero.
+__device__ __forceinline__ void tile_load(u32x4 (&pf)[8], __amdgpu_buffer_rsrc_t rs, int tr0, int g, int c)
+{
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        pf[j] = __builtin_amdgcn_raw_buffer_load_b128(rs, (tr0 + j * 16 + g) * (kD * 2) + c * 16, 0, 0);
+}
+
+__device__ __forceinline__ void tile_store(u32x4 *kt, const u32x4 (&pf)[8], int g, int c)
+{
+#pragma unroll
+    for (int j = 0; j < 8; ++j) kt[sw(j * 16 + g, c)] = pf[j];
+}
+
+// Calls body(tr0) for each of the block's `ntiles` 128-key tiles with the tile
+// in kt.  DEPTH tiles are in flight in registers while one is processed.  The
+// prefetch is unconditional (the descriptor ends at the block's last row), so
+// every barrier waits only for LDS and the oldest tile.
+template <int DEPTH, class F>
+__device__ __forceinline__ void tile_pipeline(u32x4 *kt, __amdgpu_buffer_rsrc_t rs, int row_base, int ntiles, int g,
+                                              int c, F &&body)
+{
+    // The loop over groups of DEPTH tiles is kept rolled (code size); the
+    // loads are unconditional, so the outstanding-load count is the same on
+    // every path and each barrier waits only for the oldest tile.
+    u32x4 pf[DEPTH][8];
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) tile_load(pf[d], rs, row_base + d * kTile, g, c);
+    // Whole groups only: a tile past the block's range reads as zeros from the
+    // descriptor and adds nothing (callers mask keys at or past T), so every
+    // iteration is identical and no path re-enters the loop with fewer loads
+    // in flight.
+    const int ngroups = (ntiles + DEPTH - 1) / DEPTH;
+#pragma unroll 1
+    for (int grp = 0; grp < ngroups; ++grp) {
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            const int tile = grp * DEPTH + d;
+            tile_store(kt, pf[d], g, c);
+            lds_barrier();
+            tile_load(pf[d], rs, row_base + (tile + DEPTH) * kTile, g, c);
+            body(row_base + tile * kTile);
+            lds_barrier();
+        }
+    }
+}
+
+// Window rows 32t + (lane & 31) as MFMA A operands (zero beyond R): for k-step
+// s the lane holds elements 8*(2s + lane/32) .. +7.
+template <int MT>
+__device__ __forceinline__ void load_query_operands(const ScoreArgs &a, const Unit &un, int lane, bf16x8 (&aq)[MT][8])
+{
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+        const int r = 32 * t + (lane & 31);
+        const bool ok = r < a.R;
+        const uint16_t *qp = static_cast<const uint16_t *>(a.Q) + window_row(a, un, ok ? r : 0) * kD;
+        u32x4 q[8];
+#pragma unroll
+        for (int s = 0; s < 8; ++s) q[s] = *reinterpret_cast<const u32x4 *>(qp + 8 * (2 * s + (lane >> 5)));
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            aq[t][s] = __builtin_bit_cast(bf16x8, ok ? q[s] : z);
+        }
+    }
+}
+
+// Sweep 1, per block of kRows keys:
+//  * window logits on the matrix cores (window rows x 32 keys per wave) with
+//    per-row online softmax statistics, x = log2(e) q.k / sqrt(d_k);
+//  * |k|^2 from v_dot2 on the same B registers, and 1/|k| per key;
+//  * the column sums sum_k k and sum_k k/|k| also on the matrix cores: the
+//    A operand rows are (1, 1/|k| high bf16, 1/|k| remainder) over 16 keys and
+//    the B operand is 16 keys x 32 dimensions, read transposed from the LDS
+//    tile with ds_read_b64_tr_b16 (each 16-lane group returns the 4 x 4
+//    transpose of the 8-byte pieces its lanes address).
+template <int MT>
+__global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
+{
+    __shared__ u32x4 kt[kTile * kChunks];                   // 32 KiB key tile
+    __shared__ __attribute__((aligned(16))) uint16_t aw[4][kTile];  // ones, 1/|k| high, remainder, zeros
+    __shared__ float wm[4][32 * MT], wsm[4][32 * MT];
+
     const int u = blockIdx.y;
     const Unit un = unit_of(u, a.Hkv, a.B);
     const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
     const int P = T - a.w;
-    const int i0 = blockIdx.x * kEpi;
-    if (i0 >= P) return;
-    const int nblk = (P + kEpi - 1) / kEpi;
-    const int64_t obase = ((int64_t)un.l * a.Hkv + un.h) * a.Ptot + (a.seq.cu[un.s] - un.s * a.w);
-    const float *hs = a.hstat + (int64_t)u * HS_COUNT;
-    const float dmin = hs[HS_DMIN], dden = hs[HS_DMAX] - hs[HS_DMIN] + a.eps;
-    const int i = i0 + threadIdx.x;
-    float sdiv = 0.f, imp = 0.f, mn = INFINITY, mx = -INFINITY;
-    if (i < P) {
-        float acc = 0.f;
-        for (int t = -a.pool_half; t <= a.pool_half; ++t) {
-            const int k = i + t;
-            if (k >= 0 && k < P) acc += a.bufC[obase + k];
-        }
-        imp = acc / (float)(2 * a.pool_half + 1);
-        const float sE = (a.bufA[obase + i] - dmin) / dden;
-        const float sC = (1.f - a.bufB[obase + i]) * 0.5f;
-        sdiv = a.alpha * sE + (1.f - a.alpha) * sC;
-        mn = mx = sdiv;
-        a.bufA[obase + i] = sdiv;
-        a.bufB[obase + i] = imp;
+    const int row_base = blockIdx.x * kRows;
+    if (row_base >= T) return;
+
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int c = tid & 15, g = tid >> 4, h = lane >> 5;
+    const uint16_t *krow0 = static_cast<const uint16_t *>(a.K) + unit_row0(a, un) * kD;
+    const float sc = a.inv_sqrt_d * kLog2e;
+
+    bf16x8 aq[MT][8];
+    load_query_operands<MT>(a, un, lane, aq);
+    for (int i = tid; i < kTile; i += blockDim.x) {
+        aw[0][i] = 0x3f80;  // 1.0
+        aw[3][i] = 0;
     }
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const float s1 = wave_sum(sdiv), s2 = wave_sum(imp);
-    mn = wave_min(mn);
-    mx = wave_max(mx);
+
+    // Per-lane addresses of the transposed reads (constant over the block):
+    // lane X reads 4 dimensions 32 wv + 16 ((X/16) % 2) + 4 (X % 4) of key
+    // 8 (X/32) + ((X % 16) / 4) (+4 for the second read) of each 16-key step.
+    const int tr_key = 8 * (lane >> 5) + ((lane & 15) >> 2);
+    const int tr_dim = 32 * wv + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    const int aw_row = (lane & 31) < 3 ? (lane & 31) : 3;
+
+    float ms[MT][16], ss[MT][16];
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            ms[t][i] = -INFINITY;
+            ss[t][i] = 0.f;
+        }
+    f32x16 csum = (f32x16){};
+
+    const int ntiles = min(kTilesPerBlock, (T - row_base + kTile - 1) / kTile);
+    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + kRows));
+    tile_pipeline<ECOKV_SWEEP1_DEPTH>(kt, rs, row_base, ntiles, g, c, [&](int tr0) {
+        // window logits and |k|^2 of this wave's 32 keys
+        f32x16 acc[MT];
+#pragma unroll
+        for (int t = 0; t < MT; ++t) acc[t] = (f32x16){};
+        float n2 = 0.f;
+        {
+            const int r = 32 * wv + (lane & 31);
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+                const u32x4 bq = kt[sw(r, 2 * s + h)];
+                n2 = dot2sq(bq[0], dot2sq(bq[1], dot2sq(bq[2], dot2sq(bq[3], n2))));
+                const bf16x8 b = __builtin_bit_cast(bf16x8, bq);
+#pragma unroll
+                for (int t = 0; t < MT; ++t)
+                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq[t][s], b, acc[t], 0, 0, 0);
+            }
+        }
+        n2 += __shfl_xor(n2, 32, kWave);
+        if (h == 0) {
+            const float inv = __builtin_amdgcn_rsqf(fmaxf(n2, 1e-24f));
+            const unsigned hi = bf16_rne(inv);
+            aw[1][32 * wv + lane] = (uint16_t)hi;
+            aw[2][32 * wv + lane] = (uint16_t)bf16_rne(inv - __uint_as_float(hi << 16));
+        }
+
+        // online softmax statistics
+        const int gi = tr0 + 32 * wv + (lane & 31);
+        if (tr0 + kTile <= P) {
+            // every key of the tile is a non-window key, visible to every row
+            float dmax = -INFINITY;
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) dmax = fmaxf(dmax, fmaf(acc[t][i], sc, -ms[t][i]));
+            if (!__any(dmax > 0.f)) {
+                // no new maximum in the wave: one exponential per value
+#pragma unroll
+                for (int t = 0; t < MT; ++t)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) ss[t][i] += fast_exp2(fmaf(acc[t][i], sc, -ms[t][i]));
+            } else {
+#pragma unroll
+                for (int t = 0; t < MT; ++t)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const float d = fmaf(acc[t][i], sc, -ms[t][i]);
+                        const float e = fast_exp2(-fabsf(d));
+                        ss[t][i] = d > 0.f ? fmaf(ss[t][i], e, 1.f) : ss[t][i] + e;
+                        ms[t][i] = fmaxf(ms[t][i], acc[t][i] * sc);
+                    }
+            }
+        } else {
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int m = 32 * t + 8 * (i >> 2) + 4 * h + (i & 3);
+                    const bool ok = gi < T && (!a.causal || gi <= P + (m % a.w));
+                    const float x = acc[t][i] * sc;
+                    const float dd = x - ms[t][i];
+                    const float e = fast_exp2(-fabsf(dd));
+                    const float s_new = dd > 0.f ? fmaf(ss[t][i], e, 1.f) : ss[t][i] + e;
+                    if (ok) {
+                        ss[t][i] = s_new;
+                        ms[t][i] = fmaxf(ms[t][i], x);
+                    }
+                }
+        }
+        lds_barrier();  // 1/|k| of the tile is in aw
+
+        // column sums on the matrix cores: this wave's 32 dimensions, 8 steps of 16 keys
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+            const bf16x8 wa = *reinterpret_cast<const bf16x8 *>(&aw[aw_row][16 * ks + 8 * h]);
+            const int key0 = 16 * ks + tr_key;
+            typedef short s16x4 __attribute__((ext_vector_type(4)));
+            const uint16_t *p0 = reinterpret_cast<const uint16_t *>(kt) + key0 * kD +
+                                 (((tr_dim >> 3) ^ (key0 & 15)) << 3) + (tr_dim & 7);
+            const uint16_t *p1 = reinterpret_cast<const uint16_t *>(kt) + (key0 + 4) * kD +
+                                 (((tr_dim >> 3) ^ ((key0 + 4) & 15)) << 3) + (tr_dim & 7);
+            const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4 *)(const_cast<uint16_t *>(p0)));
+            const s16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4 *)(const_cast<uint16_t *>(p1)));
+            const short __attribute__((ext_vector_type(8))) kb8 = {lo[0], lo[1], lo[2], lo[3],
+                                                                    hi4[0], hi4[1], hi4[2], hi4[3]};
+            csum = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa, __builtin_bit_cast(bf16x8, kb8), csum, 0, 0, 0);
+        }
+    });
+
+    const int stride = 2 * kD + 2 * a.R;
+    float *part = a.part1 + ((int64_t)u * a.nch1 + blockIdx.x) * stride;
+    if (h == 0) {
+        part[32 * wv + lane] = csum[0];              // sum of k
+        part[kD + 32 * wv + lane] = csum[1] + csum[2];  // sum of k / |k|
+    }
+    // per-row softmax partials: merge over the 32 lanes that hold the row
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            float m = ms[t][i], s = ss[t][i];
+#pragma unroll
+            for (int mask = 1; mask < 32; mask <<= 1) {
+                const float m2 = __shfl_xor(m, mask, kWave);
+                const float s2 = __shfl_xor(s, mask, kWave);
+                softmax_merge2(m, s, m2, s2);
+            }
+            if ((lane & 31) == 0) {
+                const int row = 32 * t + 8 * (i >> 2) + 4 * h + (i & 3);
+                wm[wv][row] = m;
+                wsm[wv][row] = s;
+            }
+        }
+    lds_barrier();
+    if (tid < a.R) {
+        float m = wm[0][tid], s = wsm[0][tid];
+        for (int w2 = 1; w2 < 4; ++w2) softmax_merge2(m, s, wm[w2][tid], wsm[w2][tid]);
+        part[2 * kD + tid] = m;
+        part[2 * kD + a.R + tid] = s;
+    }
+}
+
+// Sweep 2.  The A operand carries the window rows and, in its last four rows,
+// mu and kbar each split into a bf16 high part and a bf16 remainder, so that
+// one MFMA chain gives q.k for the window rows together with k.mu and k.kbar
+// to about 2^-17 relative.  |k|^2 comes from v_dot2 on the same B registers;
+// d_E = sqrt(|k|^2 - 2 k.kbar + |kbar|^2), khat.mu = k.mu / |k|.
+template <int MT>
+__global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
+{
+    constexpr int kAnc = 32 * MT - 4;  // first anchor row of the A operand
+    __shared__ u32x4 kt[kTile * kChunks];
+    __shared__ float rowM[32 * MT], rowIS[32 * MT];
+    __shared__ float wred[3][4];
+    __shared__ float kb2_lds;
+
+    const int u = blockIdx.y;
+    const Unit un = unit_of(u, a.Hkv, a.B);
+    const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
+    const int P = T - a.w;
+    const int row_base = blockIdx.x * kRows;
+    if (row_base >= T) return;
+
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int c = tid & 15, g = tid >> 4, h = lane >> 5;
+    const uint16_t *krow0 = static_cast<const uint16_t *>(a.K) + unit_row0(a, un) * kD;
+    const int64_t obase = unit_out_base(a, un);
+    const int stride = 2 * kD + 2 * a.R;
+    const float *anc = a.anchors + (int64_t)u * stride;
+    const float sc = a.inv_sqrt_d * kLog2e;
+
+    bf16x8 aq[MT][8];
+    load_query_operands<MT>(a, un, lane, aq);
+    {
+        // anchor rows: kAnc + 0: mu high, +1: mu remainder, +2: kbar high, +3: kbar remainder
+        const int rr = 32 * (MT - 1) + (lane & 31);
+        if (rr >= kAnc) {
+            const int which = rr - kAnc;
+            const float4 *src = reinterpret_cast<const float4 *>((which < 2) ? anc + kD : anc);
+            float4 fv[16];
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+                fv[2 * s] = src[2 * (2 * s + h)];
+                fv[2 * s + 1] = src[2 * (2 * s + h) + 1];
+            }
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+                const float f8[8] = {fv[2 * s].x, fv[2 * s].y, fv[2 * s].z, fv[2 * s].w,
+                                     fv[2 * s + 1].x, fv[2 * s + 1].y, fv[2 * s + 1].z, fv[2 * s + 1].w};
+                u32x4 q;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    unsigned half2[2];
+#pragma unroll
+                    for (int z = 0; z < 2; ++z) {
+                        const float f = f8[2 * e + z];
+                        const unsigned hi = bf16_rne(f);
+                        half2[z] = (which & 1) ? bf16_rne(f - __uint_as_float(hi << 16)) : hi;
+                    }
+                    q[e] = half2[0] | (half2[1] << 16);
+                }
+                aq[MT - 1][s] = __builtin_bit_cast(bf16x8, q);
+            }
+        }
+    }
+    if (tid < 64) {
+        // |kbar'|^2 of the centroid as represented (high + remainder)
+        float acc2 = 0.f;
+#pragma unroll
+        for (int z = 0; z < 2; ++z) {
+            const float f = anc[2 * tid + z];
+            const float hi = __uint_as_float(bf16_rne(f) << 16);
+            const float lo = __uint_as_float(bf16_rne(f - hi) << 16);
+            const float kb = hi + lo;
+            acc2 = fmaf(kb, kb, acc2);
+        }
+        acc2 = wave_sum(acc2);
+        if (tid == 0) kb2_lds = acc2;
+    }
+    if (tid < 32 * MT) {
+        const bool ok = tid < a.R;
+        rowM[tid] = ok ? anc[2 * kD + tid] : 0.f;
+        rowIS[tid] = ok ? 1.f / anc[2 * kD + a.R + tid] : 0.f;
+    }
+
+    float dsum = 0.f, dmn = INFINITY, dmx = -INFINITY;
+    const float inv_r = 1.f / (float)a.R;
+    const int ntiles = min(kTilesPerBlock, (T - row_base + kTile - 1) / kTile);
+    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + kRows));
+    tile_pipeline<ECOKV_SWEEP2_DEPTH>(kt, rs, row_base, ntiles, g, c, [&](int tr0) {
+
+        f32x16 acc[MT];
+#pragma unroll
+        for (int t = 0; t < MT; ++t) acc[t] = (f32x16){};
+        float n2 = 0.f;
+        {
+            const int r = 32 * wv + (lane & 31);
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+                const u32x4 bq = kt[sw(r, 2 * s + h)];
+                n2 = dot2sq(bq[0], dot2sq(bq[1], dot2sq(bq[2], dot2sq(bq[3], n2))));
+                const bf16x8 b = __builtin_bit_cast(bf16x8, bq);
+#pragma unroll
+                for (int t = 0; t < MT; ++t)
+                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq[t][s], b, acc[t], 0, 0, 0);
+            }
+        }
+        float att = 0.f;
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int m = 32 * t + 8 * (i >> 2) + 4 * h + (i & 3);
+                if (m < a.R) att = fmaf(fast_exp2(fmaf(acc[t][i], sc, -rowM[m])), rowIS[m], att);
+            }
+        float kmu = h ? acc[MT - 1][12] + acc[MT - 1][13] : 0.f;
+        float kk = h ? acc[MT - 1][14] + acc[MT - 1][15] : 0.f;
+        n2 += __shfl_xor(n2, 32, kWave);
+        att += __shfl_xor(att, 32, kWave);
+        kmu += __shfl_xor(kmu, 32, kWave);
+        kk += __shfl_xor(kk, 32, kWave);
+        const float dE = __builtin_amdgcn_sqrtf(fmaxf(n2 - 2.f * kk + kb2_lds, 0.f));
+        const float cm = kmu * __builtin_amdgcn_rsqf(fmaxf(n2, 1e-24f));
+        const int gi = tr0 + 32 * wv + (lane & 31);
+        if (h == 0) {
+            if (gi < T) dsum += dE;
+            if (gi < P) {
+                dmn = fminf(dmn, dE);
+                dmx = fmaxf(dmx, dE);
+                a.bufA[obase + gi] = dE;
+                a.bufB[obase + gi] = cm;
+                a.bufC[obase + gi] = att * inv_r;
+            }
+        }
+    });
+
+    dsum = wave_sum(dsum);
+    dmn = wave_min(dmn);
+    dmx = wave_max(dmx);
     if (lane == 0) {
-        wred[0][wv] = mn;
-        wred[1][wv] = mx;
-        wred[2][wv] = s1;
-        wred[3][wv] = s2;
+        wred[0][wv] = dsum;
+        wred[1][wv] = dmn;
+        wred[2][wv] = dmx;
+    }
+    lds_barrier();
+    if (tid == 0) {
+        float s = 0.f, mn = INFINITY, mx = -INFINITY;
+        for (int k = 0; k < 4; ++k) {
+            s += wred[0][k];
+            mn = fminf(mn, wred[1][k]);
+            mx = fmaxf(mx, wred[2][k]);
+        }
+        float *pp = a.part2 + ((int64_t)u * a.nch1 + blockIdx.x) * 4;
+        pp[0] = s;
+        pp[1] = mn;
+        pp[2] = mx;
+        pp[3] = 0.f;
+    }
+}
+
+}  // namespace fast
+
+// ---------------------------------------------------------------------------
+// Per-unit reduction of the sweep-1 partials.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_reduce1(ScoreArgs a)
+{
+    const int u = blockIdx.x;
+    const Unit un = unit_of(u, a.Hkv, a.B);
+    const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
+    const int nb = (T + a.rpb1 - 1) / a.rpb1;
+    const int stride = 2 * a.D + 2 * a.R;
+    const float *p = a.part1 + (int64_t)u * a.nch1 * stride;
+    float *anc = a.anchors + (int64_t)u * stride;
+    for (int d = threadIdx.x; d < 2 * a.D; d += blockDim.x) {
+        float s = 0.f;
+#pragma unroll 8
+        for (int b = 0; b < nb; ++b) s += p[(int64_t)b * stride + d];
+        anc[d] = s / (float)T;
+    }
+    for (int r = threadIdx.x; r < a.R; r += blockDim.x) {
+        float m = -INFINITY, s = 0.f;
+        for (int b = 0; b < nb; ++b)
+            softmax_merge2(m, s, p[(int64_t)b * stride + 2 * a.D + r], p[(int64_t)b * stride + 2 * a.D + a.R + r]);
+        anc[2 * a.D + r] = m;
+        anc[2 * a.D + a.R + r] = s;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Epilogue, two launches over (key blocks, units):
+//   epi1: pooled S_imp and S_div of each non-window key; block sums/extrema.
+//   epi2: every block derives the unit constants from the partials (same
+//         order in every block) and writes S; block 0 writes the statistics.
+// ---------------------------------------------------------------------------
+constexpr int kEpiThreads = 256;
+constexpr int kEpiKeys = 2048;
+
+struct Red4 {
+    float s0, s1, mn, mx;
+};
+
+__device__ Red4 block_red4(Red4 v, Red4 *lds)
+{
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    v.s0 = wave_sum(v.s0);
+    v.s1 = wave_sum(v.s1);
+    v.mn = wave_min(v.mn);
+    v.mx = wave_max(v.mx);
+    if (lane == 0) lds[wv] = v;
+    __syncthreads();
+    Red4 r = lds[0];
+    for (int k = 1; k < nw; ++k) {
+        r.s0 += lds[k].s0;
+        r.s1 += lds[k].s1;
+        r.mn = fminf(r.mn, lds[k].mn);
+        r.mx = fmaxf(r.mx, lds[k].mx);
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-        float a0 = INFINITY, a1 = -INFINITY, a2 = 0.f, a3 = 0.f;
-        for (int k = 0; k < kEpi / kWave; ++k) {
-            a0 = fminf(a0, wred[0][k]);
-            a1 = fmaxf(a1, wred[1][k]);
-            a2 += wred[2][k];
-            a3 += wred[3][k];
-        }
-        float *pp = a.part3 + ((int64_t)u * a.nch3 + blockIdx.x) * 4;
-        pp[0] = a0;
-        pp[1] = a1;
-        pp[2] = a2;
-        pp[3] = a3;
-    }
-    if (!last_block_arrives(a.counters + u * 4 + 2, nblk, &flag)) return;
-    if (threadIdx.x == 0) {
-        const float *pp = a.part3 + (int64_t)u * a.nch3 * 4;
-        float a0 = INFINITY, a1 = -INFINITY, a2 = 0.f, a3 = 0.f;
-        for (int k = 0; k < nblk; ++k) {
-            a0 = fminf(a0, pp[k * 4 + 0]);
-            a1 = fmaxf(a1, pp[k * 4 + 1]);
-            a2 += pp[k * 4 + 2];
-            a3 += pp[k * 4 + 3];
-        }
-        float *h = a.hstat + (int64_t)u * HS_COUNT;
-        const float sdmean = a2 / (float)P;
-        const float impmean = a3 / (float)P;
-        const float sbarmean = (sdmean - a0) / (a1 - a0 + a.eps);
-        h[HS_SDMIN] = a0;
-        h[HS_SDMAX] = a1;
-        h[HS_IMPMEAN] = impmean;
-        h[HS_SBARMEAN] = sbarmean;
-        h[HS_SCALE] = impmean / (sbarmean + a.eps);
-        a.counters[u * 4 + 2] = 0;
-    }
+    return r;
 }
 
-__global__ __launch_bounds__(kEpi) void k_epi2(ScoreArgs a)
+__device__ __forceinline__ float pooled(const float *abuf, int i, int P, int half)
 {
+    float acc = 0.f;
+    for (int t = -half; t <= half; ++t) {
+        const int k = i + t;
+        if (k >= 0 && k < P) acc += abuf[k];
+    }
+    return acc / (float)(2 * half + 1);
+}
+
+// Sum, min and max of d_E over the unit, from the sweep-2 partials.
+__device__ Red4 unit_distance_stats(const ScoreArgs &a, int u, int T, Red4 *lds)
+{
+    const int nb = (T + a.rpb1 - 1) / a.rpb1;
+    Red4 v{0.f, 0.f, INFINITY, -INFINITY};
+    for (int b = threadIdx.x; b < nb; b += blockDim.x) {
+        const float *pp = a.part2 + ((int64_t)u * a.nch1 + b) * 4;
+        v.s0 += pp[0];
+        v.mn = fminf(v.mn, pp[1]);
+        v.mx = fmaxf(v.mx, pp[2]);
+    }
+    return block_red4(v, lds);
+}
+
+__global__ __launch_bounds__(kEpiThreads) void k_epi1(ScoreArgs a)
+{
+    __shared__ Red4 lds[kEpiThreads / kWave];
     const int u = blockIdx.y;
     const Unit un = unit_of(u, a.Hkv, a.B);
     const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
     const int P = T - a.w;
-    const int i0 = blockIdx.x * kEpi;
+    const int i0 = blockIdx.x * kEpiKeys;
     if (i0 >= P) return;
-    const int64_t obase = ((int64_t)un.l * a.Hkv + un.h) * a.Ptot + (a.seq.cu[un.s] - un.s * a.w);
-    const float *hs = a.hstat + (int64_t)u * HS_COUNT;
-    const float lam = hs[HS_LAMBDA], smin = hs[HS_SDMIN];
-    const float sden = hs[HS_SDMAX] - smin + a.eps, scale = hs[HS_SCALE];
-    const int i = i0 + threadIdx.x;
-    if (i < P) {
-        const float sbar = (a.bufA[obase + i] - smin) / sden;
-        a.scores[obase + i] = lam * (sbar * scale) + (1.f - lam) * a.bufB[obase + i];
+    const int i1 = min(i0 + kEpiKeys, P);
+    const int64_t ob = unit_out_base(a, un);
+    const float *dbuf = a.bufA + ob, *cbuf = a.bufB + ob, *abuf = a.bufC + ob;
+    const Red4 dst = unit_distance_stats(a, u, T, lds);
+    const float dmin = dst.mn, dden = dst.mx - dst.mn + a.eps;
+
+    Red4 w{0.f, 0.f, INFINITY, -INFINITY};
+    for (int i = i0 + threadIdx.x; i < i1; i += blockDim.x) {
+        const float imp = pooled(abuf, i, P, a.pool_half);
+        const float sE = (dbuf[i] - dmin) / dden;
+        const float sC = (1.f - cbuf[i]) * 0.5f;
+        const float sdiv = a.alpha * sE + (1.f - a.alpha) * sC;
+        w.s0 += sdiv;
+        w.s1 += imp;
+        w.mn = fminf(w.mn, sdiv);
+        w.mx = fmaxf(w.mx, sdiv);
     }
-    if (blockIdx.x == 0 && threadIdx.x < ECOKV_NSTATS) {
-        if (a.stats) a.stats[(int64_t)u * ECOKV_NSTATS + threadIdx.x] = hs[threadIdx.x];
-        if (a.lambda && threadIdx.x == 0) a.lambda[u] = lam;
+    const Red4 r = block_red4(w, lds);
+    if (threadIdx.x == 0) {
+        float *pp = a.part3 + ((int64_t)u * a.nch3 + blockIdx.x) * 4;
+        pp[0] = r.s0;
+        pp[1] = r.s1;
+        pp[2] = r.mn;
+        pp[3] = r.mx;
     }
 }
 
-__global__ void k_zero_u32(unsigned *p, int64_t n)
+__global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
 {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) p[i] = 0u;
+    __shared__ Red4 lds[kEpiThreads / kWave];
+    const int u = blockIdx.y;
+    const Unit un = unit_of(u, a.Hkv, a.B);
+    const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
+    const int P = T - a.w;
+    const int i0 = blockIdx.x * kEpiKeys;
+    if (i0 >= P) return;
+    const int i1 = min(i0 + kEpiKeys, P);
+    const int64_t ob = unit_out_base(a, un);
+    const float *dbuf = a.bufA + ob, *cbuf = a.bufB + ob, *abuf = a.bufC + ob;
+    const int stride = 2 * a.D + 2 * a.R;
+    const float *mu = a.anchors + (int64_t)u * stride + a.D;
+
+    const Red4 dst = unit_distance_stats(a, u, T, lds);
+    Red4 v{0.f, 0.f, INFINITY, -INFINITY};
+    const int nb3 = (P + kEpiKeys - 1) / kEpiKeys;
+    for (int b = threadIdx.x; b < nb3; b += blockDim.x) {
+        const float *pp = a.part3 + ((int64_t)u * a.nch3 + b) * 4;
+        v.s0 += pp[0];
+        v.s1 += pp[1];
+        v.mn = fminf(v.mn, pp[2]);
+        v.mx = fmaxf(v.mx, pp[3]);
+    }
+    const Red4 sd = block_red4(v, lds);
+    Red4 m2{0.f, 0.f, 0.f, 0.f};
+    for (int d = threadIdx.x; d < a.D; d += blockDim.x) m2.s0 += mu[d] * mu[d];
+    const float mu2 = block_red4(m2, lds).s0;
+
+    const float DE = dst.s0 / (float)T;
+    const float dmin = dst.mn, dden = dst.mx - dst.mn + a.eps;
+    const float rE = 2.f - 2.f / (1.f + expf(-DE / a.tau));
+    const float rC = ((float)T * mu2 - 1.f) / ((float)T - 1.f);
+    const float lam = a.use_override ? a.lambda_override : a.beta * rE + (1.f - a.beta) * rC;
+    const float smin = sd.mn, sden = sd.mx - sd.mn + a.eps;
+    const float impmean = sd.s1 / (float)P;
+    const float sbarmean = (sd.s0 / (float)P - smin) / sden;
+    const float scale = impmean / (sbarmean + a.eps);
+
+    float *out = a.scores + ob;
+    for (int i = i0 + threadIdx.x; i < i1; i += blockDim.x) {
+        const float imp = pooled(abuf, i, P, a.pool_half);
+        const float sE = (dbuf[i] - dmin) / dden;
+        const float sC = (1.f - cbuf[i]) * 0.5f;
+        const float sdiv = a.alpha * sE + (1.f - a.alpha) * sC;
+        out[i] = lam * (((sdiv - smin) / sden) * scale) + (1.f - lam) * imp;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        float st[ECOKV_NSTATS];
+        st[ECOKV_STAT_LAMBDA] = lam;
+        st[ECOKV_STAT_RC] = rC;
+        st[ECOKV_STAT_RE] = rE;
+        st[ECOKV_STAT_DE] = DE;
+        st[ECOKV_STAT_DMIN] = dst.mn;
+        st[ECOKV_STAT_DMAX] = dst.mx;
+        st[ECOKV_STAT_SDIV_MIN] = sd.mn;
+        st[ECOKV_STAT_SDIV_MAX] = sd.mx;
+        st[ECOKV_STAT_IMP_MEAN] = impmean;
+        st[ECOKV_STAT_SBAR_MEAN] = sbarmean;
+        st[ECOKV_STAT_MU_NORM2] = mu2;
+        st[ECOKV_STAT_SCALE] = scale;
+        if (a.stats)
+            for (int k = 0; k < ECOKV_NSTATS; ++k) a.stats[(int64_t)u * ECOKV_NSTATS + k] = st[k];
+        if (a.lambda) a.lambda[u] = lam;
+    }
 }
 
-template <int D, bool BF>
-static hipError_t launch_sweeps(const ScoreArgs &a, int U, int maxT, hipStream_t st)
-{
-    const dim3 g1((maxT + kCh - 1) / kCh, U);
-    hipLaunchKernelGGL((k_pass1<D, BF>), g1, dim3(kThreads), 0, st, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_pass2<D, BF>), g1, dim3(kThreads), 0, st, a);
-    return hipGetLastError();
-}
-
-
-
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, int maxP)
+bool score_fast_path(int D, bool bf16) { return bf16 && D == fast::kD; }
+
+static int rows_per_block(int D, bool bf16) { return score_fast_path(D, bf16) ? fast::kRows : kCh; }
+
+WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16)
 {
     WsLayout w{};
     const int64_t U = (int64_t)L * Hkv * B;
-    const int64_t nch1 = (maxT + kCh - 1) / kCh;
-    const int64_t nch3 = (maxP + kEpi - 1) / kEpi;
+    const int rpb = rows_per_block(D, bf16);
+    const int64_t nch1 = (maxT + rpb - 1) / rpb;
+    const int64_t nch3 = (maxT + kEpiKeys - 1) / kEpiKeys;
     const int64_t stride = 2 * D + 2 * R;
     size_t o = 0;
     w.part1 = o; o = align256(o + sizeof(float) * U * nch1 * stride);
     w.anchors = o; o = align256(o + sizeof(float) * U * stride);
     w.part2 = o; o = align256(o + sizeof(float) * U * nch1 * 4);
-    w.hstat = o; o = align256(o + sizeof(float) * U * HS_COUNT);
+    w.part3 = o; o = align256(o + sizeof(float) * U * nch3 * 4);
     w.bufA = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
     w.bufB = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
     w.bufC = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
-    w.part3 = o; o = align256(o + sizeof(float) * U * nch3 * 4);
-    w.counters = o; o = align256(o + sizeof(unsigned) * U * 4);
     w.total = o;
     return w;
 }
 
-hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, int maxP, hipStream_t st,
-                        bool bf16)
+template <int MT1, int MT2>
+static void launch_fast_sweep(int pass, const ScoreArgs &a, dim3 grid, hipStream_t st)
+{
+    if (pass == 1)
+        hipLaunchKernelGGL((fast::k_fs1<MT1>), grid, dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL((fast::k_fs2<MT2>), grid, dim3(256), 0, st, a);
+}
+
+static void launch_sweep(int pass, const ScoreArgs &a, dim3 grid, hipStream_t st, bool bf16)
+{
+    if (score_fast_path(a.D, bf16)) {
+        // MT1 = ceil(R / 32) tiles of window rows; MT2 also holds 4 anchor rows.
+        const int mt1 = (a.R + 31) / 32, mt2 = (a.R + 4 + 31) / 32;
+        if (pass == 1) {
+            if (mt1 == 1) launch_fast_sweep<1, 1>(1, a, grid, st);
+            else launch_fast_sweep<2, 1>(1, a, grid, st);
+        } else {
+            if (mt2 == 1) launch_fast_sweep<1, 1>(2, a, grid, st);
+            else if (mt2 == 2) launch_fast_sweep<1, 2>(2, a, grid, st);
+            else launch_fast_sweep<1, 3>(2, a, grid, st);
+        }
+        return;
+    }
+    if (pass == 1) {
+        if (bf16) hipLaunchKernelGGL((k_pass1<64, true>), grid, dim3(kThreads), 0, st, a);
+        else if (a.D == 128) hipLaunchKernelGGL((k_pass1<128, false>), grid, dim3(kThreads), 0, st, a);
+        else hipLaunchKernelGGL((k_pass1<64, false>), grid, dim3(kThreads), 0, st, a);
+    } else {
+        if (bf16) hipLaunchKernelGGL((k_pass2<64, true>), grid, dim3(kThreads), 0, st, a);
+        else if (a.D == 128) hipLaunchKernelGGL((k_pass2<128, false>), grid, dim3(kThreads), 0, st, a);
+        else hipLaunchKernelGGL((k_pass2<64, false>), grid, dim3(kThreads), 0, st, a);
+    }
+}
+
+hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hipStream_t st, bool bf16)
 {
     const int U = a.L * a.Hkv * a.B;
     a.part1 = reinterpret_cast<float *>(ws + lay.part1);
     a.anchors = reinterpret_cast<float *>(ws + lay.anchors);
     a.part2 = reinterpret_cast<float *>(ws + lay.part2);
-    a.hstat = reinterpret_cast<float *>(ws + lay.hstat);
+    a.part3 = reinterpret_cast<float *>(ws + lay.part3);
     a.bufA = reinterpret_cast<float *>(ws + lay.bufA);
     a.bufB = reinterpret_cast<float *>(ws + lay.bufB);
     a.bufC = reinterpret_cast<float *>(ws + lay.bufC);
-    a.part3 = reinterpret_cast<float *>(ws + lay.part3);
-    a.counters = reinterpret_cast<unsigned *>(ws + lay.counters);
-    a.nch1 = (maxT + kCh - 1) / kCh;
-    a.nch3 = (maxP + kEpi - 1) / kEpi;
-
-    const int64_t ncnt = (int64_t)U * 4;
-    hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)((ncnt + 255) / 256)), dim3(256), 0, st, a.counters, ncnt);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-
-    if (bf16) {
-        e = a.D == 128 ? launch_sweeps<128, true>(a, U, maxT, st) : launch_sweeps<64, true>(a, U, maxT, st);
-    } else {
-        e = a.D == 128 ? launch_sweeps<128, false>(a, U, maxT, st) : launch_sweeps<64, false>(a, U, maxT, st);
-    }
-    if (e != hipSuccess) return e;
-    const dim3 ge((maxP + kEpi - 1) / kEpi, U);
-    hipLaunchKernelGGL(k_epi1, ge, dim3(kEpi), 0, st, a);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_epi2, ge, dim3(kEpi), 0, st, a);
+    a.rpb1 = rows_per_block(a.D, bf16);
+    a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
+    a.nch3 = (maxT + kEpiKeys - 1) / kEpiKeys;
+    const dim3 grid(a.nch1, U);
+    const dim3 grid_e(a.nch3, U);
+    hipError_t e;
+    launch_sweep(1, a, grid, st, bf16);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kThreads), 0, st, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    launch_sweep(2, a, grid, st, bf16);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_epi1, grid_e, dim3(kEpiThreads), 0, st, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_epi2, grid_e, dim3(kEpiThreads), 0, st, a);
     return hipGetLastError();
 }
 

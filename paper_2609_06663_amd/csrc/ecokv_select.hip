@@ -18,41 +18,59 @@ constexpr int kMaxFlatHeads = 256;
 
 
 
-// Exclusive block-wide scan of one uint32 per thread; returns the exclusive
-// prefix and writes the block total to *total (all threads).
-__device__ __forceinline__ uint32_t block_exscan(uint32_t x, uint32_t *wsum, uint32_t *total)
+// Exclusive block-wide scan of two uint32 per thread (independent sums);
+// returns the exclusive prefixes and the block totals.
+__device__ __forceinline__ void block_exscan2(uint32_t x0, uint32_t x1, uint32_t *wsum, uint32_t &e0, uint32_t &e1,
+                                              uint32_t &t0, uint32_t &t1)
 {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    uint32_t inc = x;
+    uint32_t i0 = x0, i1 = x1;
 #pragma unroll
     for (int d = 1; d < kWave; d <<= 1) {
-        const uint32_t y = __shfl_up(inc, d, kWave);
-        if (lane >= d) inc += y;
+        const uint32_t y0 = __shfl_up(i0, d, kWave), y1 = __shfl_up(i1, d, kWave);
+        if (lane >= d) {
+            i0 += y0;
+            i1 += y1;
+        }
     }
-    if (lane == kWave - 1) wsum[wv] = inc;
+    if (lane == kWave - 1) {
+        wsum[wv] = i0;
+        wsum[kSelWaves + 1 + wv] = i1;
+    }
     __syncthreads();
     if (wv == 0) {
-        uint32_t t = lane < kSelWaves ? wsum[lane] : 0u;
-        uint32_t ti = t;
+        uint32_t a0 = lane < kSelWaves ? wsum[lane] : 0u;
+        uint32_t a1 = lane < kSelWaves ? wsum[kSelWaves + 1 + lane] : 0u;
+        uint32_t c0 = a0, c1 = a1;
 #pragma unroll
         for (int d = 1; d < kSelWaves; d <<= 1) {
-            const uint32_t y = __shfl_up(ti, d, kWave);
-            if (lane >= d) ti += y;
+            const uint32_t y0 = __shfl_up(c0, d, kWave), y1 = __shfl_up(c1, d, kWave);
+            if (lane >= d) {
+                c0 += y0;
+                c1 += y1;
+            }
         }
-        if (lane < kSelWaves) wsum[lane] = ti - t;  // exclusive wave offsets
-        if (lane == kSelWaves - 1) wsum[kSelWaves] = ti;
+        if (lane < kSelWaves) {
+            wsum[lane] = c0 - a0;
+            wsum[kSelWaves + 1 + lane] = c1 - a1;
+        }
+        if (lane == kSelWaves - 1) {
+            wsum[kSelWaves] = c0;
+            wsum[2 * kSelWaves + 1] = c1;
+        }
     }
     __syncthreads();
-    const uint32_t r = wsum[wv] + inc - x;
-    *total = wsum[kSelWaves];
+    e0 = wsum[wv] + i0 - x0;
+    e1 = wsum[kSelWaves + 1 + wv] + i1 - x1;
+    t0 = wsum[kSelWaves];
+    t1 = wsum[2 * kSelWaves + 1];
     __syncthreads();
-    return r;
 }
 
-// Score of virtual element v of the group.
+// Scores of one selection group: head h's non-window scores at base + h * hstride.
 struct GroupView {
-    const float *base;  // first score of head 0
-    int64_t hstride;    // distance between heads (Ptot)
+    const float *base;
+    int64_t hstride;
     int P;
     __device__ __forceinline__ float get(int64_t v) const
     {
@@ -61,24 +79,82 @@ struct GroupView {
     }
 };
 
-// Radix select: the key of the k-th largest element (k >= 1) and how many
-// elements equal to it must be taken.
-__device__ void radix_threshold(const GroupView &g, int64_t n, int64_t k, uint32_t *hist, uint32_t *bc,
-                                uint32_t *thr_out, int64_t *need_eq_out)
+constexpr int kLdsKeys = 38912;  // keys kept in LDS by the resident variant (152 KiB)
+
+template <bool RESIDENT>
+struct KeySource {
+    const GroupView &g;
+    const uint32_t *lds;
+    __device__ __forceinline__ uint32_t operator()(int64_t v) const
+    {
+        if constexpr (RESIDENT)
+            return lds[v];
+        else
+            return score_key(g.get(v));
+    }
+};
+
+// f(v, key) for every v in [0, n) with v = tid (mod blockDim.x); eight keys
+// are fetched before any is used so that loads overlap.
+template <class Src, class F>
+__device__ __forceinline__ void for_each_key(const Src &key, int64_t n, F &&f)
 {
-    uint32_t prefix = 0, mask = 0;
+    const int64_t step = blockDim.x;
+    for (int64_t base = threadIdx.x; base < n; base += 8 * step) {
+        uint32_t kk[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int64_t v = base + q * step;
+            kk[q] = v < n ? key(v) : 0u;
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int64_t v = base + q * step;
+            if (v < n) f(v, kk[q]);
+        }
+    }
+}
+
+__device__ __forceinline__ uint32_t wave_min_u(uint32_t x)
+{
+    for (int m = 32; m >= 1; m >>= 1) x = min(x, (uint32_t)__shfl_xor(x, m, kWave));
+    return x;
+}
+__device__ __forceinline__ uint32_t wave_max_u(uint32_t x)
+{
+    for (int m = 32; m >= 1; m >>= 1) x = max(x, (uint32_t)__shfl_xor(x, m, kWave));
+    return x;
+}
+
+// Exact radix select of the k-th largest key (k >= 1) among n keys whose
+// extremes are kmin, kmax: digits of up to 8 bits, starting just below the
+// common prefix of kmin and kmax so that the first histogram is spread out.
+// Returns the threshold key and how many keys equal to it are taken.
+template <class Src>
+__device__ void radix_threshold(const Src &key, int64_t n, int64_t k, uint32_t kmin, uint32_t kmax, uint32_t *hist,
+                                uint32_t *bc, uint32_t *thr_out, int64_t *need_eq_out)
+{
+    const uint32_t diff = kmin ^ kmax;
+    if (diff == 0) {
+        *thr_out = kmin;
+        *need_eq_out = k;
+        return;
+    }
+    int hi = 31 - __clz(diff);
+    uint32_t mask = hi == 31 ? 0u : ~((2u << hi) - 1u);
+    uint32_t prefix = kmin & mask;
     int64_t rem = k;
-    for (int shift = 24; shift >= 0; shift -= 8) {
+    while (hi >= 0) {
+        const int lo = hi >= 7 ? hi - 7 : 0;
+        const uint32_t nb = 1u << (hi - lo + 1);
         for (int b = threadIdx.x; b < 256; b += blockDim.x) hist[b] = 0;
         __syncthreads();
-        for (int64_t v = threadIdx.x; v < n; v += blockDim.x) {
-            const uint32_t key = score_key(g.get(v));
-            if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
-        }
+        for_each_key(key, n, [&](int64_t, uint32_t kk) {
+            if ((kk & mask) == prefix) atomicAdd(&hist[(kk >> lo) & (nb - 1u)], 1u);
+        });
         __syncthreads();
         if (threadIdx.x < kWave) {
-            // lane l owns bins 255-4l .. 252-4l (descending); suffix counts in
-            // descending digit order locate the bin holding the rem-th key.
+            // lane l owns bins 255-4l .. 252-4l (descending order of digit)
             const int lane = threadIdx.x;
             uint32_t c4[4], loc = 0;
 #pragma unroll
@@ -92,7 +168,7 @@ __device__ void radix_threshold(const GroupView &g, int64_t n, int64_t k, uint32
                 const uint32_t y = __shfl_up(inc, d, kWave);
                 if (lane >= d) inc += y;
             }
-            const uint32_t before = inc - loc;  // keys in higher digits than this lane's bins
+            const uint32_t before = inc - loc;
             if ((int64_t)before < rem && rem <= (int64_t)inc) {
                 uint32_t cum = before;
                 for (int q = 0; q < 4; ++q) {
@@ -108,19 +184,23 @@ __device__ void radix_threshold(const GroupView &g, int64_t n, int64_t k, uint32
         __syncthreads();
         const uint32_t digit = bc[0];
         rem -= bc[1];
-        prefix |= digit << shift;
-        mask |= 255u << shift;
+        prefix |= digit << lo;
+        mask |= (nb - 1u) << lo;
+        hi = lo - 1;
         __syncthreads();
     }
     *thr_out = prefix;
     *need_eq_out = rem;
 }
 
+template <bool RESIDENT>
 __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a)
 {
+    __shared__ uint32_t keys_lds[RESIDENT ? kLdsKeys : 1];
     __shared__ uint32_t hist[256];
     __shared__ uint32_t bc[2];
-    __shared__ uint32_t wsum[kSelWaves + 1];
+    __shared__ uint32_t wsum[2 * kSelWaves + 2];
+    __shared__ uint32_t mm[2][kSelWaves];
     __shared__ int64_t through[kMaxFlatHeads];
 
     int l, h0, s, nh;
@@ -159,45 +239,79 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a)
     g.P = P;
     const int64_t n = (int64_t)nh * P;
     const int64_t k = (int64_t)nh * (beff - a.w);
+    const KeySource<RESIDENT> key{g, keys_lds};
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
 
-    for (int h = threadIdx.x; h < nh; h += blockDim.x) through[h] = 0;
+    for (int h = tid; h < nh; h += blockDim.x) through[h] = 0;
     uint32_t thr = 0xffffffffu;
     int64_t need_eq = 0;
-    if (k > 0) radix_threshold(g, n, k, hist, bc, &thr, &need_eq);
+    if (k > 0) {
+        // keys (kept in LDS by the resident variant) and their extremes
+        uint32_t kmin = 0xffffffffu, kmax = 0u;
+        const KeySource<false> from_scores{g, nullptr};
+        for_each_key(from_scores, n, [&](int64_t v, uint32_t kk) {
+            if constexpr (RESIDENT) keys_lds[v] = kk;
+            kmin = min(kmin, kk);
+            kmax = max(kmax, kk);
+        });
+        kmin = wave_min_u(kmin);
+        kmax = wave_max_u(kmax);
+        if (lane == 0) {
+            mm[0][wv] = kmin;
+            mm[1][wv] = kmax;
+        }
+        __syncthreads();
+        kmin = mm[0][0];
+        kmax = mm[1][0];
+        for (int q = 1; q < kSelWaves; ++q) {
+            kmin = min(kmin, mm[0][q]);
+            kmax = max(kmax, mm[1][q]);
+        }
+        radix_threshold(key, n, k, kmin, kmax, hist, bc, &thr, &need_eq);
+    }
     __syncthreads();
 
     if (k > 0) {
-        int64_t run_gt = 0, run_eq = 0;
-        for (int64_t b0 = 0; b0 < n; b0 += blockDim.x) {
-            const int64_t v = b0 + threadIdx.x;
-            uint32_t key = 0;
-            if (v < n) key = score_key(g.get(v));
-            const bool gt = v < n && key > thr;
-            const bool eq = v < n && key == thr;
-            uint32_t total;
-            const uint32_t ex = block_exscan((gt ? 1u : 0u) | (eq ? 0x10000u : 0u), wsum, &total);
-            const int64_t gt_before = run_gt + (ex & 0xffffu);
-            const int64_t eq_before = run_eq + (ex >> 16);
-            const bool take = gt || (eq && eq_before < need_eq);
-            const int64_t pos = gt_before + (eq_before < need_eq ? eq_before : need_eq);
-            if (v < n) {
-                const int64_t h = v / P;
-                if (take) out[pos + h * a.w] = (int32_t)(v - h * P);
-                if (nh > 1 && v - h * P == P - 1) through[h] = pos + (take ? 1 : 0);
-            }
-            run_gt += total & 0xffffu;
-            run_eq += total >> 16;
+        // ordered emission: thread t owns the contiguous run [v0, v1)
+        const int64_t per = (n + blockDim.x - 1) / blockDim.x;
+        const int64_t v0 = min((int64_t)tid * per, n), v1 = min(v0 + per, n);
+        uint32_t cg = 0, ce = 0;
+        for (int64_t b = v0; b < v1; b += 8) {
+            uint32_t kk[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) kk[q] = b + q < v1 ? key(b + q) : 0u;
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                if (b + q < v1) {
+                    cg += kk[q] > thr;
+                    ce += kk[q] == thr;
+                }
         }
-        if (nh == 1 && threadIdx.x == 0) through[0] = k;
+        uint32_t eg, ee, tg, te;
+        block_exscan2(cg, ce, wsum, eg, ee, tg, te);
+        (void)tg;
+        (void)te;
+        int64_t gt_before = eg, eq_before = ee;
+        for (int64_t v = v0; v < v1; ++v) {
+            const uint32_t kk = key(v);  // second read of the run (LDS, or cache-resident scores)
+            const bool gt = kk > thr, eq = kk == thr;
+            const bool take = gt || (eq && eq_before < need_eq);
+            const int64_t h = v / P;
+            if (take) out[gt_before + min(eq_before, need_eq) + h * a.w] = (int32_t)(v - h * P);
+            gt_before += gt;
+            eq_before += eq;
+            if (nh > 1 && v - h * P == P - 1) through[h] = gt_before + min(eq_before, need_eq);
+        }
+        if (nh == 1 && tid == 0) through[0] = k;
     }
     __syncthreads();
     // windows, counts and offsets
-    for (int e = threadIdx.x; e < nh * a.w; e += blockDim.x) {
+    for (int e = tid; e < nh * a.w; e += blockDim.x) {
         const int h = e / a.w, j = e % a.w;
         out[through[h] + (int64_t)h * a.w + j] = P + j;
     }
-    if (threadIdx.x < nh && (a.counts || a.offsets)) {
-        const int h = threadIdx.x;
+    if (tid < nh && (a.counts || a.offsets)) {
+        const int h = tid;
         const int64_t prev = h > 0 ? through[h - 1] : 0;
         const int64_t u = ((int64_t)l * a.Hkv + h0 + h) * a.B + s;
         if (a.counts) a.counts[u] = (int32_t)(through[h] - prev + a.w);
@@ -208,7 +322,16 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a)
 hipError_t select_launch(const SelectArgs &a, hipStream_t st)
 {
     const unsigned groups = a.flat ? (unsigned)(a.L * a.B) : (unsigned)(a.L * a.Hkv * a.B);
-    hipLaunchKernelGGL(k_select, dim3(groups), dim3(kSelThreads), 0, st, a);
+    // largest group: every head's non-window keys in layer-flat mode
+    int64_t maxn = 0;
+    for (int s = 0; s < a.B; ++s) {
+        const int64_t P = (int64_t)(a.seq.cu[s + 1] - a.seq.cu[s]) - a.w;
+        maxn = P * (a.flat ? a.Hkv : 1) > maxn ? P * (a.flat ? a.Hkv : 1) : maxn;
+    }
+    if (maxn <= kLdsKeys)
+        hipLaunchKernelGGL(k_select<true>, dim3(groups), dim3(kSelThreads), 0, st, a);
+    else
+        hipLaunchKernelGGL(k_select<false>, dim3(groups), dim3(kSelThreads), 0, st, a);
     return hipGetLastError();
 }
 

@@ -188,6 +188,14 @@ def test_head_dim_64_fp32_window_1():
     check_compact(wl, g)
 
 
+def test_head_dim_64_bf16_gqa():
+    wl = W.custom(18, L=2, Hq=12, Hkv=3, D=64, w=5, seqlens=[611, 90], dtype="bf16", budget=[120, 40], group=32)
+    say("D=64 bf16 G=4 w=5 (generic sweep)")
+    g = gpu_pass(wl)
+    check_per_head(wl, g)
+    check_compact(wl, g)
+
+
 def test_max_window_rows():
     wl = W.custom(13, L=1, Hq=16, Hkv=2, D=128, w=8, seqlens=[300], dtype="bf16", budget=[60], group=16)
     say("G*w = 64 window rows")
