@@ -1,0 +1,108 @@
+// Device helpers shared by the score kernels (gfx950): vector types, unit
+// addressing, log2-domain softmax merging and the LDS tile geometry of the
+// bf16 / head_dim 128 path.  Not part of the ABI.
+#pragma once
+
+#include "ecokv_internal.h"
+
+namespace ecokv {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ int64_t unit_out_base(const ScoreArgs &a, const Unit &un)
+{
+    return ((int64_t)un.l * a.Hkv + un.h) * a.Ptot + (a.seq.cu[un.s] - un.s * a.w);
+}
+
+__device__ __forceinline__ int64_t unit_row0(const ScoreArgs &a, const Unit &un)
+{
+    return ((int64_t)un.l * a.Hkv + un.h) * a.Ttot + a.seq.cu[un.s];
+}
+
+// Global row index of window row r = (g, j) of unit `un` in Q_win.
+__device__ __forceinline__ int64_t window_row(const ScoreArgs &a, const Unit &un, int r)
+{
+    const int g = r / a.w, j = r % a.w;
+    return (((int64_t)un.l * a.Hq + (int64_t)un.h * a.G + g) * a.B + un.s) * a.w + j;
+}
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Combine two softmax partials (max, sum of 2^(x - max)), x in log2 units.
+__device__ __forceinline__ void softmax_merge2(float &m, float &s, float m2, float s2)
+{
+    const float nm = fmaxf(m, m2);
+    const float a = (m == -INFINITY) ? 0.f : s * __builtin_amdgcn_exp2f(m - nm);
+    const float b = (m2 == -INFINITY) ? 0.f : s2 * __builtin_amdgcn_exp2f(m2 - nm);
+    m = nm;
+    s = a + b;
+}
+
+namespace fast {
+
+// Hot-loop transcendentals as single instructions (v_exp_f32, v_rsq_f32,
+// v_sqrt_f32, about 1 ulp).  Every exponent argument here is <= 0, so results
+// below 2^-126 (flushed to zero) are negligible next to the softmax terms of
+// size 1 they are added to.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+constexpr int kD = 128;
+constexpr int kChunks = 16;           // 16-byte chunks per key row
+constexpr int kTile = 128;            // keys per LDS tile (4 waves x 32 keys)
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over an aligned 16-lane row; every lane of the row gets the total.
+__device__ __forceinline__ float row16_sum(float x)
+{
+    x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+    x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+    x += dpp<0x141>(x);  // row_half_mirror
+    x += dpp<0x140>(x);  // row_mirror
+    return x;
+}
+
+__device__ __forceinline__ void unpack8(u32x4 q, float *v)
+{
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        v[2 * e] = __uint_as_float(q[e] << 16);
+        v[2 * e + 1] = __uint_as_float(q[e] & 0xffff0000u);
+    }
+}
+
+// acc + lo*lo + hi*hi of the two bf16 halves of w (v_dot2c_f32_bf16).
+__device__ __forceinline__ float dot2sq(unsigned w, float acc)
+{
+    const bf16x2 v = __builtin_bit_cast(bf16x2, w);
+    return __builtin_amdgcn_fdot2_f32_bf16(v, v, acc, false);
+}
+
+// Round-to-nearest-even bf16 of a finite float (bit pattern in the low half).
+__device__ __forceinline__ unsigned bf16_rne(float f)
+{
+    unsigned u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+// Swizzled position of 16-byte chunk c of tile row r.
+__device__ __forceinline__ int sw(int r, int c) { return r * kChunks + (c ^ (r & 15)); }
+
+// Buffer descriptor over the key rows [0, rows) of a unit (raw buffer, no
+// stride): loads at or past the end return zero without touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t key_rows_rsrc(const uint16_t *krow0, int rows)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(krow0), (short)0, rows * (kD * 2), 0x00020000);
+}
+
+}  // namespace fast
+}  // namespace ecokv

@@ -17,6 +17,7 @@ struct SeqTab {
     int cu[ECOKV_MAX_SEQS + 1];    // token offsets (prefix of T_s)
     int beff[ECOKV_MAX_SEQS];      // min(b_s, T_s)
     int boff[ECOKV_MAX_SEQS + 1];  // prefix of beff
+    int spre[ECOKV_MAX_SEQS + 1];  // prefix of the work items per sequence (single-read score path)
 };
 
 // Decode unit u = (l*Hkv + h)*B + s.
@@ -47,6 +48,15 @@ struct ScoreArgs {
     float *bufA;     // [L][Hkv][Ptot]      d_E
     float *bufB;     // [L][Hkv][Ptot]      khat.mu
     float *bufC;     // [L][Hkv][Ptot]      window-mean attention a
+    // single-read score path only: values published between blocks, each a
+    // 64-bit word (launch tag << 32 | float bits) so that a reader can tell a
+    // value of this launch from anything older without ordering fences
+    unsigned long long *partT;  // [U][2D + 2R][nch1]  per-item column sums and softmax partials
+    unsigned long long *ancT;   // [U][2D + 2R]        per-unit kbar, mu, row max, row normaliser
+    unsigned *status;           // set to the launch tag if a wait ran out of time
+    unsigned tag;               // launch tag (never 0)
+    int items;                  // work items of the launch
+    int slices_per_lh;          // work items of one (layer, head) over all sequences
     int L, Hq, Hkv, G, D, w, R, B;
     int64_t Ttot, Ptot;
     int nch1;        // sweep blocks per unit (for the longest sequence)
@@ -87,11 +97,19 @@ struct CompactArgs {
 
 // Workspace layout, shared by the size query and the launcher.
 struct WsLayout {
-    size_t part1, anchors, part2, part3, bufA, bufB, bufC, total;
+    size_t part1, anchors, part2, part3, bufA, bufB, bufC, partT, ancT, status, total;
 };
 
 WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16);
 hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hipStream_t st, bool bf16);
+
+// Single-read score path (bf16, head_dim 128, G*w <= 28): eligibility for a
+// shape on the current device, and its launch.  The launcher fills the
+// fused-path fields of ScoreArgs.
+bool fused_eligible(int D, bool bf16, int R, const SeqTab &seq, int L, int Hkv, int *grid);
+hipError_t fused_launch(ScoreArgs &a, int grid, hipStream_t st);
+constexpr int kFusedItem = 256;        // keys per work item of the single-read path
+constexpr int kFusedMaxRows = 28;      // window rows; 4 more rows carry kbar and mu
 hipError_t select_launch(const SelectArgs &a, hipStream_t st);
 int select_max_flat_heads();
 hipError_t compact_launch(const CompactArgs &a, hipStream_t st);

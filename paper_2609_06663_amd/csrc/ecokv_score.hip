@@ -24,45 +24,15 @@
 //     operand and 32 keys per wave as the B operand.
 //   * any other case (fp32 inputs, head_dim 64): a plain VALU sweep with 16
 //     lanes per key row and window dot products reduced across the row.
-#include "ecokv_internal.h"
+#include <stdlib.h>
+#include <string.h>
+
+#include "ecokv_fast.h"
 
 namespace ecokv {
 
 constexpr int kThreads = 256;
 constexpr int kCh = 128;        // key rows per block, generic sweeps
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-
-__device__ __forceinline__ int64_t unit_out_base(const ScoreArgs &a, const Unit &un)
-{
-    return ((int64_t)un.l * a.Hkv + un.h) * a.Ptot + (a.seq.cu[un.s] - un.s * a.w);
-}
-
-__device__ __forceinline__ int64_t unit_row0(const ScoreArgs &a, const Unit &un)
-{
-    return ((int64_t)un.l * a.Hkv + un.h) * a.Ttot + a.seq.cu[un.s];
-}
-
-// Global row index of window row r = (g, j) of unit `un` in Q_win.
-__device__ __forceinline__ int64_t window_row(const ScoreArgs &a, const Unit &un, int r)
-{
-    const int g = r / a.w, j = r % a.w;
-    return (((int64_t)un.l * a.Hq + (int64_t)un.h * a.G + g) * a.B + un.s) * a.w + j;
-}
-
-constexpr float kLog2e = 1.4426950408889634f;
-
-// Combine two softmax partials (max, sum of 2^(x - max)), x in log2 units.
-__device__ __forceinline__ void softmax_merge2(float &m, float &s, float m2, float s2)
-{
-    const float nm = fmaxf(m, m2);
-    const float a = (m == -INFINITY) ? 0.f : s * __builtin_amdgcn_exp2f(m - nm);
-    const float b = (m2 == -INFINITY) ? 0.f : s2 * __builtin_amdgcn_exp2f(m2 - nm);
-    m = nm;
-    s = a + b;
-}
 
 // ---------------------------------------------------------------------------
 // Generic sweeps (fp32 or head_dim 64): 16 lanes per key row.
@@ -280,15 +250,7 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
 // ---------------------------------------------------------------------------
 namespace fast {
 
-// Hot-loop transcendentals as single instructions (v_exp_f32, v_rsq_f32,
-// v_sqrt_f32, about 1 ulp).  Every exponent argument here is <= 0, so results
-// below 2^-126 (flushed to zero) are negligible next to the softmax terms of
-// size 1 they are added to.
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-constexpr int kD = 128;
-constexpr int kChunks = 16;           // 16-byte chunks per key row
-constexpr int kTile = 128;            // keys per LDS tile (4 waves x 32 keys)
+constexpr float kRebase = 16.f;       // log2 headroom of a lazily moved softmax reference
 #ifndef ECOKV_SWEEP_TILES
 #define ECOKV_SWEEP_TILES 8
 #endif
@@ -300,58 +262,6 @@ constexpr int kTile = 128;            // keys per LDS tile (4 waves x 32 keys)
 #endif
 constexpr int kTilesPerBlock = ECOKV_SWEEP_TILES;  // tiles per block (1024 keys by default)
 constexpr int kRows = kTile * kTilesPerBlock;
-
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-template <int CTRL>
-__device__ __forceinline__ float dpp(float x)
-{
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-
-// Sum over an aligned 16-lane row; every lane of the row gets the total.
-__device__ __forceinline__ float row16_sum(float x)
-{
-    x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
-    x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
-    x += dpp<0x141>(x);  // row_half_mirror
-    x += dpp<0x140>(x);  // row_mirror
-    return x;
-}
-
-__device__ __forceinline__ void unpack8(u32x4 q, float *v)
-{
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        v[2 * e] = __uint_as_float(q[e] << 16);
-        v[2 * e + 1] = __uint_as_float(q[e] & 0xffff0000u);
-    }
-}
-
-// acc + lo*lo + hi*hi of the two bf16 halves of w (v_dot2c_f32_bf16).
-__device__ __forceinline__ float dot2sq(unsigned w, float acc)
-{
-    const bf16x2 v = __builtin_bit_cast(bf16x2, w);
-    return __builtin_amdgcn_fdot2_f32_bf16(v, v, acc, false);
-}
-
-// Round-to-nearest-even bf16 of a finite float (bit pattern in the low half).
-__device__ __forceinline__ unsigned bf16_rne(float f)
-{
-    unsigned u = __float_as_uint(f);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
-}
-
-// Swizzled position of 16-byte chunk c of tile row r.
-__device__ __forceinline__ int sw(int r, int c) { return r * kChunks + (c ^ (r & 15)); }
-
-// Buffer descriptor over the key rows [0, rows) of a unit (raw buffer, no
-// stride): loads at or past the end return zero without touching memory.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t key_rows_rsrc(const uint16_t *krow0, int rows)
-{
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(krow0), (short)0, rows * (kD * 2), 0x00020000);
-}
 
 // One 128-key tile into registers: 16 lanes per 256-byte row, coalesced.
 // Rows outside the descriptor's range come back as zero.
@@ -502,31 +412,51 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
             aw[2][32 * wv + lane] = (uint16_t)bf16_rne(inv - __uint_as_float(hi << 16));
         }
 
-        // online softmax statistics
+        // online softmax statistics.  (ms, ss) keeps ss = sum 2^(x - ms) over the
+        // values seen so far, where ms is a reference that stays within
+        // kRebase of the running maximum instead of tracking it exactly: the
+        // reference moves only when a value exceeds it by more than kRebase,
+        // so after the first tile almost every tile takes the cheap branch.
         const int gi = tr0 + 32 * wv + (lane & 31);
         if (tr0 + kTile <= P) {
             // every key of the tile is a non-window key, visible to every row
-            float dmax = -INFINITY;
-#pragma unroll
-            for (int t = 0; t < MT; ++t)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) dmax = fmaxf(dmax, fmaf(acc[t][i], sc, -ms[t][i]));
-            if (!__any(dmax > 0.f)) {
-                // no new maximum in the wave: one exponential per value
-#pragma unroll
-                for (int t = 0; t < MT; ++t)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) ss[t][i] += fast_exp2(fmaf(acc[t][i], sc, -ms[t][i]));
-            } else {
+            if (tr0 == row_base) {
+                // first tile of the block: each value is its own reference
 #pragma unroll
                 for (int t = 0; t < MT; ++t)
 #pragma unroll
                     for (int i = 0; i < 16; ++i) {
-                        const float d = fmaf(acc[t][i], sc, -ms[t][i]);
-                        const float e = fast_exp2(-fabsf(d));
-                        ss[t][i] = d > 0.f ? fmaf(ss[t][i], e, 1.f) : ss[t][i] + e;
-                        ms[t][i] = fmaxf(ms[t][i], acc[t][i] * sc);
+                        ms[t][i] = acc[t][i] * sc;
+                        ss[t][i] = 1.f;
                     }
+            } else {
+                float d[MT][16];
+                float dmax = -INFINITY;
+#pragma unroll
+                for (int t = 0; t < MT; ++t)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        d[t][i] = fmaf(acc[t][i], sc, -ms[t][i]);
+                        dmax = fmaxf(dmax, d[t][i]);
+                    }
+                if (!__any(dmax > kRebase)) {
+#pragma unroll
+                    for (int t = 0; t < MT; ++t)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) ss[t][i] += fast_exp2(d[t][i]);
+                } else {
+#pragma unroll
+                    for (int t = 0; t < MT; ++t)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            if (d[t][i] > kRebase) {
+                                ss[t][i] = fmaf(ss[t][i], fast_exp2(-d[t][i]), 1.f);
+                                ms[t][i] = acc[t][i] * sc;
+                            } else {
+                                ss[t][i] += fast_exp2(d[t][i]);
+                            }
+                        }
+                }
             }
         } else {
 #pragma unroll
@@ -914,7 +844,8 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
     const float dmin = dst.mn, dden = dst.mx - dst.mn + a.eps;
     const float rE = 2.f - 2.f / (1.f + expf(-DE / a.tau));
     const float rC = ((float)T * mu2 - 1.f) / ((float)T - 1.f);
-    const float lam = a.use_override ? a.lambda_override : a.beta * rE + (1.f - a.beta) * rC;
+    float lam = a.use_override ? a.lambda_override : a.beta * rE + (1.f - a.beta) * rC;
+    if (a.status && *a.status == a.tag) lam = NAN;  // a publication wait of this launch timed out
     const float smin = sd.mn, sden = sd.mx - sd.mn + a.eps;
     const float impmean = sd.s1 / (float)P;
     const float sbarmean = (sd.s0 / (float)P - smin) / sden;
@@ -963,16 +894,23 @@ WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int 
     const int64_t U = (int64_t)L * Hkv * B;
     const int rpb = rows_per_block(D, bf16);
     const int64_t nch1 = (maxT + rpb - 1) / rpb;
+    // the single-read path publishes per 256-key item; size for it whenever it may run
+    const bool single = bf16 && D == fast::kD && R <= kFusedMaxRows;
+    const int64_t nchf = single ? (maxT + kFusedItem - 1) / kFusedItem : 0;
+    const int64_t nch2 = nch1 > nchf ? nch1 : nchf;
     const int64_t nch3 = (maxT + kEpiKeys - 1) / kEpiKeys;
     const int64_t stride = 2 * D + 2 * R;
     size_t o = 0;
     w.part1 = o; o = align256(o + sizeof(float) * U * nch1 * stride);
     w.anchors = o; o = align256(o + sizeof(float) * U * stride);
-    w.part2 = o; o = align256(o + sizeof(float) * U * nch1 * 4);
+    w.part2 = o; o = align256(o + sizeof(float) * U * nch2 * 4);
     w.part3 = o; o = align256(o + sizeof(float) * U * nch3 * 4);
     w.bufA = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
     w.bufB = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
     w.bufC = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
+    w.partT = o; o = align256(o + sizeof(unsigned long long) * U * stride * nchf);
+    w.ancT = o; o = align256(o + (single ? sizeof(unsigned long long) * U * stride : 0));
+    w.status = o; o = align256(o + sizeof(unsigned));
     w.total = o;
     return w;
 }
@@ -1022,18 +960,39 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     a.bufA = reinterpret_cast<float *>(ws + lay.bufA);
     a.bufB = reinterpret_cast<float *>(ws + lay.bufB);
     a.bufC = reinterpret_cast<float *>(ws + lay.bufC);
-    a.rpb1 = rows_per_block(a.D, bf16);
-    a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
     a.nch3 = (maxT + kEpiKeys - 1) / kEpiKeys;
-    const dim3 grid(a.nch1, U);
     const dim3 grid_e(a.nch3, U);
     hipError_t e;
-    launch_sweep(1, a, grid, st, bf16);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kThreads), 0, st, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    launch_sweep(2, a, grid, st, bf16);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+
+    // work items of the single-read path: 256-key slices of every sequence
+    a.seq.spre[0] = 0;
+    for (int s = 0; s < a.seq.nseq; ++s)
+        a.seq.spre[s + 1] = a.seq.spre[s] + (a.seq.cu[s + 1] - a.seq.cu[s] + kFusedItem - 1) / kFusedItem;
+    // The single-read path is selected with ECOKV_SCORE_PATH=single (read on
+    // every call); the two-sweep path is the default.
+    const char *path = getenv("ECOKV_SCORE_PATH");
+    const bool want_single = path && strcmp(path, "single") == 0;
+    int fgrid = 0;
+    if (want_single && fused_eligible(a.D, bf16, a.R, a.seq, a.L, a.Hkv, &fgrid)) {
+        a.partT = reinterpret_cast<unsigned long long *>(ws + lay.partT);
+        a.ancT = reinterpret_cast<unsigned long long *>(ws + lay.ancT);
+        a.status = reinterpret_cast<unsigned *>(ws + lay.status);
+        a.rpb1 = kFusedItem;
+        a.nch1 = (maxT + kFusedItem - 1) / kFusedItem;
+        a.slices_per_lh = a.seq.spre[a.seq.nseq];
+        a.items = a.L * a.Hkv * a.slices_per_lh;
+        if ((e = fused_launch(a, fgrid, st)) != hipSuccess) return e;
+    } else {
+        a.rpb1 = rows_per_block(a.D, bf16);
+        a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
+        const dim3 grid(a.nch1, U);
+        launch_sweep(1, a, grid, st, bf16);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kThreads), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        launch_sweep(2, a, grid, st, bf16);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     hipLaunchKernelGGL(k_epi1, grid_e, dim3(kEpiThreads), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_epi2, grid_e, dim3(kEpiThreads), 0, st, a);

@@ -225,6 +225,27 @@ def test_identical_and_zero_keys():
     check_compact(wl, g)
 
 
+def test_rising_logits():
+    # key magnitudes ramp up along each sequence (x1 -> x8), so the window
+    # logits (about 45 in log2 units at the start, 360 at the end) keep
+    # setting new maxima far above the earlier ones: the running softmax
+    # statistics must move their reference many times inside a block.  (A much
+    # steeper ramp makes the logits so large that fp32 rounding of q.k alone
+    # exceeds the score tolerance.)
+    wl = W.custom(18, L=1, Hq=8, Hkv=2, D=128, w=4, seqlens=[5003, 2100], dtype="bf16", budget=[700, 300],
+                  group=64)
+    cu = wl.cu_seqlens
+    for s in range(wl.B):
+        n = cu[s + 1] - cu[s]
+        ramp = np.exp(np.linspace(0.0, np.log(8.0), n)).astype(np.float32)
+        k = W.bf16_bits_to_f32(wl.K[0, :, cu[s]:cu[s + 1]]) * ramp[None, :, None]
+        wl.K[0, :, cu[s]:cu[s + 1]] = W.to_bf16_bits(k)
+    say("rising logits: keys scaled x1..x8 along the sequence")
+    g = gpu_pass(wl)
+    check_per_head(wl, g)
+    check_compact(wl, g)
+
+
 @pytest.mark.parametrize("variant", ["noncausal", "lambda0", "lambda1_alpha1", "mixkv", "pool1", "pool7",
                                      "tau"])
 def test_parameter_variants(variant):
