@@ -67,15 +67,19 @@ __device__ __forceinline__ void block_exscan2(uint32_t x0, uint32_t x1, uint32_t
     __syncthreads();
 }
 
-// Scores of one selection group: head h's non-window scores at base + h * hstride.
+// Scores of one selection group: head h's non-window scores at base + h * hstride
+// (a single head in per-head mode: no division on that path; a group has at
+// most kMaxFlatHeads * 2^31 keys, so the head index fits 32 bits).
 struct GroupView {
     const float *base;
     int64_t hstride;
     int P;
+    int nh;
     __device__ __forceinline__ float get(int64_t v) const
     {
-        const int64_t h = v / P;
-        return base[h * hstride + (v - h * P)];
+        if (nh == 1) return base[v];
+        const int h = v < 0x7fffffff ? (int)((uint32_t)v / (uint32_t)P) : (int)(v / P);
+        return base[(int64_t)h * hstride + (v - (int64_t)h * P)];
     }
 };
 
@@ -237,6 +241,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a)
     g.base = a.scores + ((int64_t)l * a.Hkv + h0) * a.Ptot + (a.seq.cu[s] - s * a.w);
     g.hstride = a.Ptot;
     g.P = P;
+    g.nh = nh;
     const int64_t n = (int64_t)nh * P;
     const int64_t k = (int64_t)nh * (beff - a.w);
     const KeySource<RESIDENT> key{g, keys_lds};
@@ -292,15 +297,21 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a)
         (void)tg;
         (void)te;
         int64_t gt_before = eg, eq_before = ee;
+        // head and position of v0, then stepped along the run
+        int h = nh == 1 ? 0 : (int)(v0 / P);
+        int pos = (int)(v0 - (int64_t)h * P);
         for (int64_t v = v0; v < v1; ++v) {
             const uint32_t kk = key(v);  // second read of the run (LDS, or cache-resident scores)
             const bool gt = kk > thr, eq = kk == thr;
             const bool take = gt || (eq && eq_before < need_eq);
-            const int64_t h = v / P;
-            if (take) out[gt_before + min(eq_before, need_eq) + h * a.w] = (int32_t)(v - h * P);
+            if (take) out[gt_before + min(eq_before, need_eq) + (int64_t)h * a.w] = (int32_t)pos;
             gt_before += gt;
             eq_before += eq;
-            if (nh > 1 && v - h * P == P - 1) through[h] = gt_before + min(eq_before, need_eq);
+            if (++pos == P) {
+                if (nh > 1) through[h] = gt_before + min(eq_before, need_eq);
+                pos = 0;
+                ++h;
+            }
         }
         if (nh == 1 && tid == 0) through[0] = k;
     }
@@ -319,6 +330,216 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a)
     }
 }
 
+// ---------------------------------------------------------------------------
+// Register-resident variant for groups of up to 64 Ki keys: thread t owns the
+// contiguous run [t*KPT, t*KPT + KPT) of the group's keys in registers
+// (16-byte loads in per-head mode), the radix passes histogram them into one
+// LDS copy per wave, and the ordered emission walks the registers.
+// ---------------------------------------------------------------------------
+constexpr int kRegMaxKeys = 64 * kSelThreads;
+
+template <int KPT>
+__global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
+{
+    __shared__ uint32_t hist[kSelWaves][256];
+    __shared__ uint32_t hsum[256];
+    __shared__ uint32_t bc[2];
+    __shared__ uint32_t wsum[2 * kSelWaves + 2];
+    __shared__ uint32_t mm[2][kSelWaves];
+    __shared__ int64_t through[kMaxFlatHeads];
+
+    int l, h0, s, nh;
+    if (a.flat) {
+        l = blockIdx.x / a.B;
+        s = blockIdx.x % a.B;
+        h0 = 0;
+        nh = a.Hkv;
+    } else {
+        const Unit un = unit_of(blockIdx.x, a.Hkv, a.B);
+        l = un.l;
+        s = un.s;
+        h0 = un.h;
+        nh = 1;
+    }
+    const int T = a.seq.cu[s + 1] - a.seq.cu[s];
+    const int P = T - a.w;
+    const int beff = a.seq.beff[s];
+    const int64_t out_base = a.flat ? ((int64_t)l * a.Hkv * a.per_lh + (int64_t)a.Hkv * a.seq.boff[s])
+                                    : (((int64_t)l * a.Hkv + h0) * a.per_lh + a.seq.boff[s]);
+    int32_t *out = a.idx + out_base;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+
+    if (beff >= T) {  // keep every token
+        for (int64_t e = tid; e < (int64_t)nh * T; e += blockDim.x) out[e] = (int32_t)(e % T);
+        if (tid < nh && (a.counts || a.offsets)) {
+            const int64_t u = ((int64_t)l * a.Hkv + h0 + tid) * a.B + s;
+            if (a.counts) a.counts[u] = T;
+            if (a.offsets) a.offsets[u] = (int32_t)(out_base + (int64_t)tid * T);
+        }
+        return;
+    }
+
+    GroupView g;
+    g.base = a.scores + ((int64_t)l * a.Hkv + h0) * a.Ptot + (a.seq.cu[s] - s * a.w);
+    g.hstride = a.Ptot;
+    g.P = P;
+    g.nh = nh;
+    const int n = nh * P;  // <= kRegMaxKeys (checked on the host)
+    const int k = nh * (beff - a.w);
+    const int v0 = tid * KPT;
+
+    for (int h = tid; h < nh; h += blockDim.x) through[h] = 0;
+    uint32_t kk[KPT];
+    if (nh == 1) {
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(g.base), (short)0, n * 4, 0x00020000);
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q) {
+            typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+            const u32x4_t x = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (v0 + 4 * q) * 4, 0, 0));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) kk[4 * q + e] = score_key(__uint_as_float(x[e]));
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < KPT; ++q) kk[q] = v0 + q < n ? score_key(g.get(v0 + q)) : 0u;
+    }
+
+    uint32_t thr = 0xffffffffu;
+    int need_eq = 0;
+    if (k > 0) {
+        uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q)
+            if (v0 + q < n) {
+                kmin = min(kmin, kk[q]);
+                kmax = max(kmax, kk[q]);
+            }
+        kmin = wave_min_u(kmin);
+        kmax = wave_max_u(kmax);
+        if (lane == 0) {
+            mm[0][wv] = kmin;
+            mm[1][wv] = kmax;
+        }
+        __syncthreads();
+        kmin = mm[0][0];
+        kmax = mm[1][0];
+        for (int q = 1; q < kSelWaves; ++q) {
+            kmin = min(kmin, mm[0][q]);
+            kmax = max(kmax, mm[1][q]);
+        }
+        // radix select of the k-th largest key, digits of up to 8 bits below
+        // the common prefix of kmin and kmax
+        const uint32_t diff = kmin ^ kmax;
+        if (diff == 0) {
+            thr = kmin;
+            need_eq = k;
+        } else {
+            int hi = 31 - __clz(diff);
+            uint32_t mask = hi == 31 ? 0u : ~((2u << hi) - 1u);
+            uint32_t prefix = kmin & mask;
+            int rem = k;
+            while (hi >= 0) {
+                const int lo = hi >= 7 ? hi - 7 : 0;
+                const uint32_t nb = 1u << (hi - lo + 1);
+                for (int b = tid; b < kSelWaves * 256; b += blockDim.x) (&hist[0][0])[b] = 0;
+                __syncthreads();
+#pragma unroll
+                for (int q = 0; q < KPT; ++q)
+                    if (v0 + q < n && (kk[q] & mask) == prefix) atomicAdd(&hist[wv][(kk[q] >> lo) & (nb - 1u)], 1u);
+                __syncthreads();
+                if (tid < 256) {
+                    uint32_t c = 0;
+#pragma unroll
+                    for (int w2 = 0; w2 < kSelWaves; ++w2) c += hist[w2][tid];
+                    hsum[tid] = c;
+                }
+                __syncthreads();
+                if (tid < kWave) {
+                    // lane owns bins 255-4l .. 252-4l (descending digit order)
+                    uint32_t c4[4], loc = 0;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        c4[q] = hsum[255 - 4 * lane - q];
+                        loc += c4[q];
+                    }
+                    uint32_t inc = loc;
+#pragma unroll
+                    for (int d = 1; d < kWave; d <<= 1) {
+                        const uint32_t y = __shfl_up(inc, d, kWave);
+                        if (lane >= d) inc += y;
+                    }
+                    const uint32_t before = inc - loc;
+                    if ((int)before < rem && rem <= (int)inc) {
+                        uint32_t cum = before;
+                        for (int q = 0; q < 4; ++q) {
+                            if ((int)(cum + c4[q]) >= rem) {
+                                bc[0] = 255u - 4u * lane - q;
+                                bc[1] = cum;
+                                break;
+                            }
+                            cum += c4[q];
+                        }
+                    }
+                }
+                __syncthreads();
+                prefix |= bc[0] << lo;
+                rem -= (int)bc[1];
+                mask |= (nb - 1u) << lo;
+                hi = lo - 1;
+                __syncthreads();
+            }
+            thr = prefix;
+            need_eq = rem;
+        }
+
+        // ordered emission from the registers
+        uint32_t cg = 0, ce = 0;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q)
+            if (v0 + q < n) {
+                cg += kk[q] > thr;
+                ce += kk[q] == thr;
+            }
+        uint32_t eg, ee, tg, te;
+        block_exscan2(cg, ce, wsum, eg, ee, tg, te);
+        (void)tg;
+        (void)te;
+        int gt_before = (int)eg, eq_before = (int)ee;
+        int h = nh == 1 ? 0 : (v0 < n ? v0 / P : nh);
+        int pos = v0 - h * P;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q) {
+            if (v0 + q < n) {
+                const bool gt = kk[q] > thr, eq = kk[q] == thr;
+                const bool take = gt || (eq && eq_before < need_eq);
+                if (take) out[gt_before + min(eq_before, need_eq) + (int64_t)h * a.w] = pos;
+                gt_before += gt;
+                eq_before += eq;
+                if (++pos == P) {
+                    if (nh > 1) through[h] = gt_before + min(eq_before, need_eq);
+                    pos = 0;
+                    ++h;
+                }
+            }
+        }
+        if (nh == 1 && tid == 0) through[0] = k;
+    }
+    __syncthreads();
+    // windows, counts and offsets
+    for (int e = tid; e < nh * a.w; e += blockDim.x) {
+        const int hh = e / a.w, j = e % a.w;
+        out[through[hh] + (int64_t)hh * a.w + j] = P + j;
+    }
+    if (tid < nh && (a.counts || a.offsets)) {
+        const int hh = tid;
+        const int64_t prev = hh > 0 ? through[hh - 1] : 0;
+        const int64_t u = ((int64_t)l * a.Hkv + h0 + hh) * a.B + s;
+        if (a.counts) a.counts[u] = (int32_t)(through[hh] - prev + a.w);
+        if (a.offsets) a.offsets[u] = (int32_t)(out_base + prev + (int64_t)hh * a.w);
+    }
+}
+
 hipError_t select_launch(const SelectArgs &a, hipStream_t st)
 {
     const unsigned groups = a.flat ? (unsigned)(a.L * a.B) : (unsigned)(a.L * a.Hkv * a.B);
@@ -328,7 +549,11 @@ hipError_t select_launch(const SelectArgs &a, hipStream_t st)
         const int64_t P = (int64_t)(a.seq.cu[s + 1] - a.seq.cu[s]) - a.w;
         maxn = P * (a.flat ? a.Hkv : 1) > maxn ? P * (a.flat ? a.Hkv : 1) : maxn;
     }
-    if (maxn <= kLdsKeys)
+    if (maxn <= 32 * kSelThreads)
+        hipLaunchKernelGGL(k_select_reg<32>, dim3(groups), dim3(kSelThreads), 0, st, a);
+    else if (maxn <= kRegMaxKeys)
+        hipLaunchKernelGGL(k_select_reg<64>, dim3(groups), dim3(kSelThreads), 0, st, a);
+    else if (maxn <= kLdsKeys)
         hipLaunchKernelGGL(k_select<true>, dim3(groups), dim3(kSelThreads), 0, st, a);
     else
         hipLaunchKernelGGL(k_select<false>, dim3(groups), dim3(kSelThreads), 0, st, a);
