@@ -722,9 +722,14 @@ __global__ __launch_bounds__(kThreads) void k_reduce1(ScoreArgs a)
 //   epi1: pooled S_imp and S_div of each non-window key; block sums/extrema.
 //   epi2: every block derives the unit constants from the partials (same
 //         order in every block) and writes S; block 0 writes the statistics.
+// Each thread takes 16 consecutive keys with 16-byte buffer loads; the
+// descriptors span exactly the unit's P non-window keys, so the pooling halo
+// reads zero outside [0, P) (the zero padding of the average pool).
 // ---------------------------------------------------------------------------
 constexpr int kEpiThreads = 256;
-constexpr int kEpiKeys = 2048;
+constexpr int kEpiPer = 16;                      // consecutive keys per thread
+constexpr int kEpiKeys = kEpiThreads * kEpiPer;  // keys per block
+constexpr int kPoolHalfMax = 4;                  // vector pooling for kernels up to 9
 
 struct Red4 {
     float s0, s1, mn, mx;
@@ -757,7 +762,56 @@ __device__ __forceinline__ float pooled(const float *abuf, int i, int P, int hal
         const int k = i + t;
         if (k >= 0 && k < P) acc += abuf[k];
     }
-    return acc / (float)(2 * half + 1);
+    return acc * (1.f / (float)(2 * half + 1));
+}
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t float_rsrc(const float *p, int n)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p), (short)0, n * 4, 0x00020000);
+}
+
+// d_E, khat.mu and pooled window attention of keys i0 .. i0+15 (zero past P).
+__device__ __forceinline__ void epi_keys(const ScoreArgs &a, const float *dbuf, const float *cbuf, const float *abuf,
+                                         int P, int i0, float (&d)[kEpiPer], float (&c)[kEpiPer],
+                                         float (&imp)[kEpiPer])
+{
+    const __amdgpu_buffer_rsrc_t rd = float_rsrc(dbuf, P), rc = float_rsrc(cbuf, P), ra = float_rsrc(abuf, P);
+#pragma unroll
+    for (int q = 0; q < kEpiPer / 4; ++q) {
+        const f32x4 x = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rd, (i0 + 4 * q) * 4, 0, 0));
+        const f32x4 y = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rc, (i0 + 4 * q) * 4, 0, 0));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            d[4 * q + e] = x[e];
+            c[4 * q + e] = y[e];
+        }
+    }
+    const int half = a.pool_half;
+    const float inv_k = 1.f / (float)(2 * half + 1);
+    if (half <= kPoolHalfMax) {
+        // av[j] = a[i0 - 4 + j]; a negative offset wraps past the range and reads zero
+        float av[kEpiPer + 2 * kPoolHalfMax];
+#pragma unroll
+        for (int q = 0; q < (kEpiPer + 2 * kPoolHalfMax) / 4; ++q) {
+            const f32x4 x = __builtin_bit_cast(
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, (unsigned)(i0 - kPoolHalfMax + 4 * q) * 4u, 0, 0));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) av[4 * q + e] = x[e];
+        }
+#pragma unroll
+        for (int j = 0; j < kEpiPer; ++j) {
+            float acc = 0.f;
+#pragma unroll
+            for (int t = -kPoolHalfMax; t <= kPoolHalfMax; ++t)
+                if (t >= -half && t <= half) acc += av[j + kPoolHalfMax + t];
+            imp[j] = acc * inv_k;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kEpiPer; ++j) imp[j] = i0 + j < P ? pooled(abuf, i0 + j, P, half) : 0.f;
+    }
 }
 
 // Sum, min and max of d_E over the unit, from the sweep-2 partials.
@@ -790,15 +844,21 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi1(ScoreArgs a)
     const float dmin = dst.mn, dden = dst.mx - dst.mn + a.eps;
 
     Red4 w{0.f, 0.f, INFINITY, -INFINITY};
-    for (int i = i0 + threadIdx.x; i < i1; i += blockDim.x) {
-        const float imp = pooled(abuf, i, P, a.pool_half);
-        const float sE = (dbuf[i] - dmin) / dden;
-        const float sC = (1.f - cbuf[i]) * 0.5f;
-        const float sdiv = a.alpha * sE + (1.f - a.alpha) * sC;
-        w.s0 += sdiv;
-        w.s1 += imp;
-        w.mn = fminf(w.mn, sdiv);
-        w.mx = fmaxf(w.mx, sdiv);
+    {
+        const int k0 = i0 + kEpiPer * threadIdx.x;
+        float d[kEpiPer], c[kEpiPer], imp[kEpiPer];
+        epi_keys(a, dbuf, cbuf, abuf, P, k0, d, c, imp);
+#pragma unroll
+        for (int j = 0; j < kEpiPer; ++j)
+            if (k0 + j < i1) {
+                const float sE = (d[j] - dmin) / dden;
+                const float sC = (1.f - c[j]) * 0.5f;
+                const float sdiv = a.alpha * sE + (1.f - a.alpha) * sC;
+                w.s0 += sdiv;
+                w.s1 += imp[j];
+                w.mn = fminf(w.mn, sdiv);
+                w.mx = fmaxf(w.mx, sdiv);
+            }
     }
     const Red4 r = block_red4(w, lds);
     if (threadIdx.x == 0) {
@@ -852,12 +912,29 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
     const float scale = impmean / (sbarmean + a.eps);
 
     float *out = a.scores + ob;
-    for (int i = i0 + threadIdx.x; i < i1; i += blockDim.x) {
-        const float imp = pooled(abuf, i, P, a.pool_half);
-        const float sE = (dbuf[i] - dmin) / dden;
-        const float sC = (1.f - cbuf[i]) * 0.5f;
-        const float sdiv = a.alpha * sE + (1.f - a.alpha) * sC;
-        out[i] = lam * (((sdiv - smin) / sden) * scale) + (1.f - lam) * imp;
+    {
+        const int k0 = i0 + kEpiPer * threadIdx.x;
+        float d[kEpiPer], c[kEpiPer], imp[kEpiPer], sv[kEpiPer];
+        epi_keys(a, dbuf, cbuf, abuf, P, k0, d, c, imp);
+#pragma unroll
+        for (int j = 0; j < kEpiPer; ++j) {
+            const float sE = (d[j] - dmin) / dden;
+            const float sC = (1.f - c[j]) * 0.5f;
+            const float sdiv = a.alpha * sE + (1.f - a.alpha) * sC;
+            sv[j] = lam * (((sdiv - smin) / sden) * scale) + (1.f - lam) * imp[j];
+        }
+        if (k0 + kEpiPer <= i1) {
+            const __amdgpu_buffer_rsrc_t ro = float_rsrc(out, P);
+#pragma unroll
+            for (int q = 0; q < kEpiPer / 4; ++q) {
+                const f32x4 x = {sv[4 * q], sv[4 * q + 1], sv[4 * q + 2], sv[4 * q + 3]};
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, x), ro, (k0 + 4 * q) * 4, 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < kEpiPer; ++j)
+                if (k0 + j < i1) out[k0 + j] = sv[j];
+        }
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         float st[ECOKV_NSTATS];
