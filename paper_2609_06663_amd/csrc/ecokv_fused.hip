@@ -704,7 +704,7 @@ __global__ __launch_bounds__(kFThreads, 1) void k_fused(ScoreArgs a)
                 mn = fminf(mn, S.dred[w2][1]);
                 mx = fmaxf(mx, S.dred[w2][2]);
             }
-            float *pp = a.part2 + ((int64_t)i2.u * a.nch1 + i2.j) * 4;
+            float *pp = a.part2 + ((int64_t)i2.u * a.nch2 + i2.j) * 4;
             pp[0] = s;
             pp[1] = mn;
             pp[2] = mx;

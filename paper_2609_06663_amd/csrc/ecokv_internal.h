@@ -43,7 +43,7 @@ struct ScoreArgs {
     // workspace regions
     float *part1;    // [U][nch1][2D + 2R]  column sums, row max / sum-exp per block
     float *anchors;  // [U][2D + 2R]        kbar, mu, row max, row normaliser
-    float *part2;    // [U][nch1][4]        sum d_E, min d_E, max d_E per block
+    float *part2;    // [U][nch2][4]        sum d_E, min d_E, max d_E per block
     float *part3;    // [U][nch3][4]        sum S_div, sum S_imp, min/max S_div per block
     float *bufA;     // [L][Hkv][Ptot]      d_E
     float *bufB;     // [L][Hkv][Ptot]      khat.mu
@@ -61,7 +61,9 @@ struct ScoreArgs {
     int64_t Ttot, Ptot;
     int nch1;        // sweep blocks per unit (for the longest sequence)
     int nch3;        // epilogue blocks per unit
-    int rpb1;        // key rows per sweep block
+    int rpb1;        // key rows per sweep-1 block
+    int nch2;        // sweep-2 blocks per unit (d_E partials in part2)
+    int rpb2;        // key rows per sweep-2 block
     float alpha, beta, eps, tau, inv_sqrt_d, lambda_override;
     int use_override, pool_half, causal;
     SeqTab seq;

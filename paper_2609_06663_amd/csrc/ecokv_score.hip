@@ -236,7 +236,7 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
             mn = fminf(mn, wred[1][k]);
             mx = fmaxf(mx, wred[2][k]);
         }
-        float *pp = a.part2 + ((int64_t)u * a.nch1 + blockIdx.x) * 4;
+        float *pp = a.part2 + ((int64_t)u * a.nch2 + blockIdx.x) * 4;
         pp[0] = s;
         pp[1] = mn;
         pp[2] = mx;
@@ -680,8 +680,212 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
             mn = fminf(mn, wred[1][k]);
             mx = fmaxf(mx, wred[2][k]);
         }
-        float *pp = a.part2 + ((int64_t)u * a.nch1 + blockIdx.x) * 4;
+        float *pp = a.part2 + ((int64_t)u * a.nch2 + blockIdx.x) * 4;
         pp[0] = s;
+        pp[1] = mn;
+        pp[2] = mx;
+        pp[3] = 0.f;
+    }
+}
+
+// Sweep 2, streaming form (window rows + 4 anchor rows in one 32-row operand,
+// i.e. G*w <= 28): no LDS tile and no barrier in the key loop.  Each wave
+// streams its own groups of 32 keys straight from HBM into MFMA B-operand
+// registers (lane l: key l % 32, 16-byte chunks 2s + l / 32), double
+// buffered, so the loads of group g+1 are in flight while group g is used.
+// The attention of row m is 2^(x - M'_m) with M'_m = M_m + log2(S_m), the
+// normaliser folded into the shift.
+constexpr int kS2Waves = 4;
+#ifndef ECOKV_S2_KEYS
+#define ECOKV_S2_KEYS 4096
+#endif
+constexpr int kS2Keys = ECOKV_S2_KEYS;            // keys per block
+constexpr int kS2Groups = kS2Keys / (32 * kS2Waves);  // 32-key groups per wave
+
+// Coalesced load of 32 key rows: instruction i covers rows 4i .. 4i+3, lane l
+// chunk l % 16 of row 4i + l / 16 (four whole 256-byte rows per instruction).
+__device__ __forceinline__ void group_load(u32x4 (&b)[8], __amdgpu_buffer_rsrc_t rs, int key0, int lane)
+{
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        b[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (key0 + 4 * i + (lane >> 4)) * (kD * 2) + (lane & 15) * 16, 0, 0);
+}
+
+__global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
+{
+    __shared__ float wred[3][kS2Waves];
+    __shared__ u32x4 stage[kS2Waves][32 * kChunks];  // per wave: 32 rows, swizzled 16-byte chunks
+    const int u = blockIdx.y;
+    const Unit un = unit_of(u, a.Hkv, a.B);
+    const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
+    const int P = T - a.w;
+    const int row_base = blockIdx.x * kS2Keys;
+    if (row_base >= T) return;
+    const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, kl = lane & 31;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint16_t *krow0 = static_cast<const uint16_t *>(a.K) + unit_row0(a, un) * kD;
+    const int64_t obase = unit_out_base(a, un);
+    const int stride = 2 * kD + 2 * a.R;
+    const float *anc = a.anchors + (int64_t)u * stride;
+    const float sc = a.inv_sqrt_d * kLog2e;
+    constexpr int kAnc = 28;
+
+    // A operand: window rows (zero beyond R), rows 28..31 mu high/remainder, kbar high/remainder
+    bf16x8 aq[1][8];
+    load_query_operands<1>(a, un, lane, aq);
+    if (kl >= kAnc) {
+        const int which = kl - kAnc;
+        const float4 *src = reinterpret_cast<const float4 *>((which < 2) ? anc + kD : anc);
+        float4 fv[16];
+#pragma unroll
+        for (int st = 0; st < 8; ++st) {
+            fv[2 * st] = src[2 * (2 * st + h)];
+            fv[2 * st + 1] = src[2 * (2 * st + h) + 1];
+        }
+#pragma unroll
+        for (int st = 0; st < 8; ++st) {
+            const float f8[8] = {fv[2 * st].x,     fv[2 * st].y,     fv[2 * st].z,     fv[2 * st].w,
+                                 fv[2 * st + 1].x, fv[2 * st + 1].y, fv[2 * st + 1].z, fv[2 * st + 1].w};
+            u32x4 q;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                unsigned half2[2];
+#pragma unroll
+                for (int z = 0; z < 2; ++z) {
+                    const float f = f8[2 * e + z];
+                    const unsigned hb = bf16_rne(f);
+                    half2[z] = (which & 1) ? bf16_rne(f - __uint_as_float(hb << 16)) : hb;
+                }
+                q[e] = half2[0] | (half2[1] << 16);
+            }
+            aq[0][st] = __builtin_bit_cast(bf16x8, q);
+        }
+    }
+    // |kbar'|^2 (each wave on its own)
+    float kb2 = 0.f;
+#pragma unroll
+    for (int z = 0; z < 2; ++z) {
+        const float f = anc[2 * lane + z];
+        const float fh = __uint_as_float(bf16_rne(f) << 16);
+        const float fl = __uint_as_float(bf16_rne(f - fh) << 16);
+        kb2 = fmaf(fh + fl, fh + fl, kb2);
+    }
+    kb2 = wave_sum(kb2);
+    // per-lane row shifts M'_m for the rows m = 8(r/4) + 4h + r%4 of accumulator r
+    float rsh[16];
+    {
+        float mv[16], sv[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int m = min(8 * (r >> 2) + 4 * h + (r & 3), a.R - 1);
+            mv[r] = anc[2 * kD + m];
+            sv[r] = anc[2 * kD + a.R + m];
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int m = 8 * (r >> 2) + 4 * h + (r & 3);
+            rsh[r] = m < a.R ? mv[r] + __log2f(sv[r]) : INFINITY;
+        }
+    }
+
+    // this wave's keys [wbase, wbase + 32 kS2Groups) only: loads past them read zero, no traffic
+    const int wbase = row_base + wv * (32 * kS2Groups);
+    const int wkeys = __builtin_amdgcn_readfirstlane(max(0, min(32 * kS2Groups, T - wbase)));
+    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0 + (int64_t)wbase * kD, wkeys);
+    float dsum = 0.f, dmn = INFINITY, dmx = -INFINITY;
+    const float inv_r = 1.f / (float)a.R;
+
+    u32x4 *wst = stage[wv];
+    auto group = [&](const u32x4 (&ld)[8], int key0, bool valid) {
+        // through this wave's LDS stage into the B-operand layout (lane l: key
+        // l % 32, chunks 2s + l / 32); a wave's own LDS accesses are ordered
+#pragma unroll
+        for (int i = 0; i < 8; ++i) wst[sw(4 * i + (lane >> 4), lane & 15)] = ld[i];
+        u32x4 b[8];
+#pragma unroll
+        for (int st = 0; st < 8; ++st) b[st] = wst[sw(kl, 2 * st + h)];
+        f32x16 acc = (f32x16){};
+        float n2 = 0.f;
+#pragma unroll
+        for (int st = 0; st < 8; ++st) {
+            n2 = dot2sq(b[st][0], dot2sq(b[st][1], dot2sq(b[st][2], dot2sq(b[st][3], n2))));
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq[0][st], __builtin_bit_cast(bf16x8, b[st]), acc, 0, 0, 0);
+        }
+        float att = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) att += fast_exp2(fmaf(acc[r], sc, -rsh[r]));
+        float kmu = h ? acc[12] + acc[13] : 0.f;
+        float kk = h ? acc[14] + acc[15] : 0.f;
+        n2 += __shfl_xor(n2, 32, kWave);
+        att += __shfl_xor(att, 32, kWave);
+        kmu += __shfl_xor(kmu, 32, kWave);
+        kk += __shfl_xor(kk, 32, kWave);
+        const float dE = __builtin_amdgcn_sqrtf(fmaxf(n2 - 2.f * kk + kb2, 0.f));
+        const float cm = kmu * __builtin_amdgcn_rsqf(fmaxf(n2, 1e-24f));
+        const int gi = key0 + kl;
+        if (valid && h == 0) {
+            if (gi < T) dsum += dE;
+            if (gi < P) {
+                dmn = fminf(dmn, dE);
+                dmx = fmaxf(dmx, dE);
+                a.bufA[obase + gi] = dE;
+                a.bufB[obase + gi] = cm;
+                a.bufC[obase + gi] = att * inv_r;
+            }
+        }
+    };
+
+    // Four register buffers in a ring: three groups (24 KiB per wave) stay in
+    // flight while one is used.  Every load is unconditional (the descriptor
+    // zero-fills past the wave's keys), so the outstanding-load count is the
+    // same on every path and each wait covers only the group about to be used.
+    const int ng = (wkeys + 31) >> 5;
+    // Waves start at different groups of their range (rotation rot), so that
+    // at any moment they read different offsets rather than the same offset
+    // of equally sized, equally aligned ranges (which would crowd the same
+    // memory channels).  Slot g >= ng reads past the range: zeros, skipped.
+    const int rot = ng > 0 ? __builtin_amdgcn_readfirstlane(
+                                 (int)(((unsigned)(blockIdx.x * kS2Waves + wv) * 2654435761u + blockIdx.y * 40503u) % (unsigned)ng))
+                           : 0;
+    auto goff = [&](int g) { return g < ng ? 32 * (g + rot < ng ? g + rot : g + rot - ng) : 32 * ng; };
+    u32x4 b0[8], b1[8], b2[8], b3[8];
+    group_load(b0, rs, goff(0), lane);
+    group_load(b1, rs, goff(1), lane);
+    group_load(b2, rs, goff(2), lane);
+#pragma unroll 1
+    for (int g = 0; g < ng; g += 4) {
+        group_load(b3, rs, goff(g + 3), lane);
+        __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the use
+        group(b0, wbase + goff(g), g < ng);
+        group_load(b0, rs, goff(g + 4), lane);
+        __builtin_amdgcn_sched_barrier(0);
+        group(b1, wbase + goff(g + 1), g + 1 < ng);
+        group_load(b1, rs, goff(g + 5), lane);
+        __builtin_amdgcn_sched_barrier(0);
+        group(b2, wbase + goff(g + 2), g + 2 < ng);
+        group_load(b2, rs, goff(g + 6), lane);
+        __builtin_amdgcn_sched_barrier(0);
+        group(b3, wbase + goff(g + 3), g + 3 < ng);
+    }
+
+    dsum = wave_sum(dsum);
+    dmn = wave_min(dmn);
+    dmx = wave_max(dmx);
+    if (lane == 0) {
+        wred[0][wv] = dsum;
+        wred[1][wv] = dmn;
+        wred[2][wv] = dmx;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        float s2 = 0.f, mn = INFINITY, mx = -INFINITY;
+        for (int k = 0; k < kS2Waves; ++k) {
+            s2 += wred[0][k];
+            mn = fminf(mn, wred[1][k]);
+            mx = fmaxf(mx, wred[2][k]);
+        }
+        float *pp = a.part2 + ((int64_t)u * a.nch2 + blockIdx.x) * 4;
+        pp[0] = s2;
         pp[1] = mn;
         pp[2] = mx;
         pp[3] = 0.f;
@@ -817,10 +1021,10 @@ __device__ __forceinline__ void epi_keys(const ScoreArgs &a, const float *dbuf, 
 // Sum, min and max of d_E over the unit, from the sweep-2 partials.
 __device__ Red4 unit_distance_stats(const ScoreArgs &a, int u, int T, Red4 *lds)
 {
-    const int nb = (T + a.rpb1 - 1) / a.rpb1;
+    const int nb = (T + a.rpb2 - 1) / a.rpb2;
     Red4 v{0.f, 0.f, INFINITY, -INFINITY};
     for (int b = threadIdx.x; b < nb; b += blockDim.x) {
-        const float *pp = a.part2 + ((int64_t)u * a.nch1 + b) * 4;
+        const float *pp = a.part2 + ((int64_t)u * a.nch2 + b) * 4;
         v.s0 += pp[0];
         v.mn = fminf(v.mn, pp[1]);
         v.mx = fmaxf(v.mx, pp[2]);
@@ -1056,6 +1260,8 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         a.status = reinterpret_cast<unsigned *>(ws + lay.status);
         a.rpb1 = kFusedItem;
         a.nch1 = (maxT + kFusedItem - 1) / kFusedItem;
+        a.rpb2 = a.rpb1;
+        a.nch2 = a.nch1;
         a.slices_per_lh = a.seq.spre[a.seq.nseq];
         a.items = a.L * a.Hkv * a.slices_per_lh;
         if ((e = fused_launch(a, fgrid, st)) != hipSuccess) return e;
@@ -1067,7 +1273,16 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         if ((e = hipGetLastError()) != hipSuccess) return e;
         hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kThreads), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        launch_sweep(2, a, grid, st, bf16);
+        if (score_fast_path(a.D, bf16) && a.R <= kFusedMaxRows) {
+            // streaming sweep 2: window rows and the four anchor rows in one operand
+            a.rpb2 = fast::kS2Keys;
+            a.nch2 = (maxT + a.rpb2 - 1) / a.rpb2;
+            hipLaunchKernelGGL(fast::k_fs2s, dim3(a.nch2, U), dim3(256), 0, st, a);
+        } else {
+            a.rpb2 = a.rpb1;
+            a.nch2 = a.nch1;
+            launch_sweep(2, a, grid, st, bf16);
+        }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL(k_epi1, grid_e, dim3(kEpiThreads), 0, st, a);
