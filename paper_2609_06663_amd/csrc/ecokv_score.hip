@@ -892,6 +892,183 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
     }
 }
 
+// Sweep 1, streaming form (bf16, head_dim 128, G*w <= 32): like the streaming
+// sweep 2, each wave streams its own 1024 keys in 32-key groups (coalesced
+// loads, three register buffers in flight, a wave-private LDS stage) and no
+// barrier is needed until the final merge of the four waves.
+//  * window logits: v_mfma_f32_32x32x16_bf16 with the keys as the A operand and
+//    the window rows as B, so each lane holds one window row against 16 keys
+//    and keeps that row's running softmax maximum and sum on its own (the
+//    reference moves only when a group exceeds it by more than 2^16);
+//  * column sums of k and of k/|k|: v_mfma_f32_16x16x32_bf16 per 16-dimension
+//    block with rows (1, 1/|k| high, remainder, 0...) over the wave's 32 keys
+//    as A, and the keys transposed out of the stage with ds_read_b64_tr_b16
+//    as B.
+constexpr float kRebase1 = 16.f;  // log2 headroom of the lazily moved row reference
+
+__global__ __launch_bounds__(256, 2) void k_fs1s(ScoreArgs a)
+{
+    __shared__ u32x4 stage[kS2Waves][32 * kChunks];
+    __shared__ __attribute__((aligned(16))) uint16_t wts[kS2Waves][4][32];  // 1, 1/|k| hi, remainder, 0
+    __shared__ float wcs[kS2Waves][2][kD];                                 // per-wave column sums
+    __shared__ float wm[kS2Waves][32], wsm[kS2Waves][32];                  // per-wave row max / sum
+
+    const int u = blockIdx.y;
+    const Unit un = unit_of(u, a.Hkv, a.B);
+    const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
+    const int P = T - a.w;
+    const int row_base = blockIdx.x * kS2Keys;
+    if (row_base >= T) return;
+    const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, kl = lane & 31;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint16_t *krow0 = static_cast<const uint16_t *>(a.K) + unit_row0(a, un) * kD;
+    const float sc = a.inv_sqrt_d * kLog2e;
+    const int lim = a.causal ? P + kl % a.w : T - 1;  // last key visible to window row kl
+
+    bf16x8 aq[1][8];
+    load_query_operands<1>(a, un, lane, aq);
+    if (lane < 32) {
+        wts[wv][0][lane] = 0x3f80;
+        wts[wv][3][lane] = 0;
+    }
+
+    const int wbase = row_base + wv * (32 * kS2Groups);
+    const int wkeys = __builtin_amdgcn_readfirstlane(max(0, min(32 * kS2Groups, T - wbase)));
+    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0 + (int64_t)wbase * kD, wkeys);
+    u32x4 *wst = stage[wv];
+
+    float ms = -INFINITY, ss = 0.f;  // window row kl over this lane's keys
+    typedef float f32x4v __attribute__((ext_vector_type(4)));
+    f32x4v cs[8];
+#pragma unroll
+    for (int b = 0; b < 8; ++b) cs[b] = (f32x4v){0.f, 0.f, 0.f, 0.f};
+    // transposed-read addressing: lane 16G + 4a + b reads key row 8G + a (+4),
+    // dimensions 16 blk + 4b .. +3; the read returns dimension 16 blk + lane % 16
+    // of keys 8G + 0..3 (then 4..7)
+    const int tr_row = 8 * (lane >> 4) + ((lane & 15) >> 2), tr_b = lane & 3;
+    const int w_row = (lane & 15) < 3 ? (lane & 15) : 3;
+
+    auto group = [&](const u32x4 (&ld)[8], int key0, bool valid) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) wst[sw(4 * i + (lane >> 4), lane & 15)] = ld[i];
+        u32x4 b[8];
+#pragma unroll
+        for (int st = 0; st < 8; ++st) b[st] = wst[sw(kl, 2 * st + h)];
+        f32x16 acc = (f32x16){};
+        float n2 = 0.f;
+#pragma unroll
+        for (int st = 0; st < 8; ++st) {
+            n2 = dot2sq(b[st][0], dot2sq(b[st][1], dot2sq(b[st][2], dot2sq(b[st][3], n2))));
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, b[st]), aq[0][st], acc, 0, 0, 0);
+        }
+        n2 += __shfl_xor(n2, 32, kWave);
+        const float inv = __builtin_amdgcn_rsqf(fmaxf(n2, 1e-24f));
+        if (h == 0) {
+            const unsigned hi = bf16_rne(inv);
+            wts[wv][1][kl] = (uint16_t)hi;
+            wts[wv][2][kl] = (uint16_t)bf16_rne(inv - __uint_as_float(hi << 16));
+        }
+        // softmax statistics of row kl over keys key0 + 8(r/4) + 4h + r%4
+        if (valid) {
+            float x[16];
+            float mx = -INFINITY;
+            if (key0 + 32 <= P) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    x[r] = acc[r] * sc;
+                    mx = fmaxf(mx, x[r]);
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int gk = key0 + 8 * (r >> 2) + 4 * h + (r & 3);
+                    x[r] = (gk < T && gk <= lim) ? acc[r] * sc : -INFINITY;
+                    mx = fmaxf(mx, x[r]);
+                }
+            }
+            const bool move = mx > ms + kRebase1 || (ms == -INFINITY && mx != -INFINITY);
+            const float nm = move ? mx : ms;
+            if (nm != -INFINITY) {
+                float add = 0.f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) add += fast_exp2(x[r] - nm);
+                ss = (move ? ss * fast_exp2(ms - nm) : ss) + add;
+                ms = nm;
+            }
+        }
+        // column sums over the wave's 32 keys (zero rows past T add nothing)
+        const bf16x8 wa = *reinterpret_cast<const bf16x8 *>(&wts[wv][w_row][8 * (lane >> 4)]);
+        typedef short s16x4 __attribute__((ext_vector_type(4)));
+        const uint16_t *st16 = reinterpret_cast<const uint16_t *>(wst);
+#pragma unroll
+        for (int blk = 0; blk < 8; ++blk) {
+            const int c = 2 * blk + (tr_b >> 1), off = (tr_b & 1) * 4;
+            const uint16_t *p0 = st16 + tr_row * kD + ((c ^ (tr_row & 15)) << 3) + off;
+            const uint16_t *p1 = st16 + (tr_row + 4) * kD + ((c ^ ((tr_row + 4) & 15)) << 3) + off;
+            const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4 *)(const_cast<uint16_t *>(p0)));
+            const s16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4 *)(const_cast<uint16_t *>(p1)));
+            const short __attribute__((ext_vector_type(8))) kb8 = {lo[0], lo[1], lo[2], lo[3],
+                                                                    hi4[0], hi4[1], hi4[2], hi4[3]};
+            cs[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, __builtin_bit_cast(bf16x8, kb8), cs[blk], 0, 0, 0);
+        }
+    };
+
+    const int ng = (wkeys + 31) >> 5;
+    const int rot = ng > 0 ? __builtin_amdgcn_readfirstlane(
+                                 (int)(((unsigned)(blockIdx.x * kS2Waves + wv) * 2654435761u + blockIdx.y * 40503u) % (unsigned)ng))
+                           : 0;
+    auto goff = [&](int g) { return g < ng ? 32 * (g + rot < ng ? g + rot : g + rot - ng) : 32 * ng; };
+    u32x4 b0[8], b1[8], b2[8];
+    group_load(b0, rs, goff(0), lane);
+    group_load(b1, rs, goff(1), lane);
+#pragma unroll 1
+    for (int g = 0; g < ng; g += 3) {
+        group_load(b2, rs, goff(g + 2), lane);
+        __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the use
+        group(b0, wbase + goff(g), g < ng);
+        group_load(b0, rs, goff(g + 3), lane);
+        __builtin_amdgcn_sched_barrier(0);
+        group(b1, wbase + goff(g + 1), g + 1 < ng);
+        group_load(b1, rs, goff(g + 4), lane);
+        __builtin_amdgcn_sched_barrier(0);
+        group(b2, wbase + goff(g + 2), g + 2 < ng);
+    }
+
+    // merge: halves of a row, then the four waves (fixed order)
+    {
+        const float m2 = __shfl_xor(ms, 32, kWave), s2 = __shfl_xor(ss, 32, kWave);
+        softmax_merge2(ms, ss, m2, s2);
+    }
+    if (lane < 32) {
+        wm[wv][lane] = ms;
+        wsm[wv][lane] = ss;
+    }
+    if (lane < 16) {
+#pragma unroll
+        for (int blk = 0; blk < 8; ++blk) {
+            wcs[wv][0][16 * blk + lane] = cs[blk][0];
+            wcs[wv][1][16 * blk + lane] = cs[blk][1] + cs[blk][2];
+        }
+    }
+    __syncthreads();
+    const int stride = 2 * kD + 2 * a.R;
+    float *part = a.part1 + ((int64_t)u * a.nch1 + blockIdx.x) * stride;
+    for (int i = tid; i < 2 * kD; i += blockDim.x) {
+        const int which = i / kD, d = i % kD;
+        float s = 0.f;
+        for (int w2 = 0; w2 < kS2Waves; ++w2) s += wcs[w2][which][d];
+        part[i] = s;
+    }
+    if (tid < a.R) {
+        float m = wm[0][tid], s = wsm[0][tid];
+        for (int w2 = 1; w2 < kS2Waves; ++w2) softmax_merge2(m, s, wm[w2][tid], wsm[w2][tid]);
+        part[2 * kD + tid] = m;
+        part[2 * kD + a.R + tid] = s;
+    }
+}
+
 }  // namespace fast
 
 // ---------------------------------------------------------------------------
@@ -1269,7 +1446,14 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         a.rpb1 = rows_per_block(a.D, bf16);
         a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
         const dim3 grid(a.nch1, U);
-        launch_sweep(1, a, grid, st, bf16);
+        if (score_fast_path(a.D, bf16) && a.R <= 32) {
+            // streaming sweep 1: one 32-row window operand
+            a.rpb1 = fast::kS2Keys;
+            a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
+            hipLaunchKernelGGL(fast::k_fs1s, dim3(a.nch1, U), dim3(256), 0, st, a);
+        } else {
+            launch_sweep(1, a, grid, st, bf16);
+        }
         if ((e = hipGetLastError()) != hipSuccess) return e;
         hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kThreads), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1279,8 +1463,9 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
             a.nch2 = (maxT + a.rpb2 - 1) / a.rpb2;
             hipLaunchKernelGGL(fast::k_fs2s, dim3(a.nch2, U), dim3(256), 0, st, a);
         } else {
-            a.rpb2 = a.rpb1;
-            a.nch2 = a.nch1;
+            // block sweep 2: the chunking of the block sweeps (grid)
+            a.rpb2 = rows_per_block(a.D, bf16);
+            a.nch2 = (maxT + a.rpb2 - 1) / a.rpb2;
             launch_sweep(2, a, grid, st, bf16);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
