@@ -36,6 +36,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-layers", type=int, default=28)
     ap.add_argument("--extras", action="store_true", help="also time 10/40 % budgets and per-layer calls")
+    ap.add_argument("--counter-run", action="store_true",
+                    help="run a few passes and a 1 GiB copy for rocprofv3 --pmc, then exit")
+    ap.add_argument("--traffic-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "COMMAND"),
+                    help="turn two rocprofv3 --pmc outputs (FETCH_SIZE, WRITE_SIZE) of --counter-run into "
+                         "the traffic summary text (CPU only)")
     return ap.parse_args()
 
 
@@ -43,8 +48,64 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+# Stage names the library times (ECOKV_STAGE_TIMING=1) and the kernels behind them.
+STAGE_KERNELS = {
+    "sweep1_stream": ["k_fs1s"], "sweep1_block": ["k_fs1", "k_pass1"], "reduce1": ["k_reduce1"],
+    "sweep2_stream": ["k_fs2s"], "sweep2_block": ["k_fs2", "k_pass2"], "epilogue1": ["k_epi1"],
+    "epilogue2": ["k_epi2"], "single_read": ["k_fused"], "select": ["k_select_reg", "k_select"],
+    "compact": ["k_compact"],
+}
+COPY_BYTES = 1 << 30  # size of the calibration copy in --counter-run
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_stack28.txt")
+
+
+def stage_of_kernel(kname):
+    import re
+    m = re.search(r"::(k_\w+?)(<|\()", kname)
+    if not m:
+        return None
+    for st, ks in STAGE_KERNELS.items():
+        if m.group(1) in ks:
+            return st
+    return None
+
+
+def source_digest():
+    """sha256 over the library sources; stored traffic figures are valid only for this digest."""
+    import hashlib
+    h = hashlib.sha256()
+    for d in (os.path.join(ROOT, "paper_2609_06663_amd", "csrc"), os.path.join(ROOT, "include")):
+        for f in sorted(os.listdir(d)):
+            if f.endswith((".hip", ".h")):
+                h.update(f.encode())
+                with open(os.path.join(d, f), "rb") as fh:
+                    h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(stage):
+    """HBM bytes per launch of `stage` from the committed counter summary, or None if the
+    summary is missing or the sources changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    digest, val = None, None
+    with open(TRAFFIC_FILE) as fh:
+        for line in fh:
+            parts = line.split()
+            if len(parts) >= 2 and parts[0] == "source_digest:":
+                digest = parts[1]
+            if len(parts) >= 6 and parts[0] == "stage:" and parts[1] == stage:
+                val = float(parts[5])
+    if digest != source_digest():
+        return None
+    return val
+
+
 def main():
     args = parse()
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the eviction pass is per (layer, KV head) and this "
               "build has no multi-GPU path; run with --gpus 1", file=sys.stderr)
@@ -73,6 +134,10 @@ def main():
     b = wl.budget[0]
     ep = EvictionPass(shape, [b], P.PER_HEAD, P.Params(), torch.bfloat16, "cuda")
     stream = torch.cuda.current_stream()
+
+    if args.counter_run:
+        counter_run(ep, K, V, Q)
+        return
 
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
@@ -106,6 +171,17 @@ def main():
         torch.cuda.synchronize()
         per_call_ms[name] = e0.elapsed_time(e1) / args.steps
 
+    # Per-kernel durations: a second timed region with the library's own HIP events
+    # around every launch, recorded on the stream the kernel runs on.
+    log("per-kernel timing")
+    os.environ["ECOKV_STAGE_TIMING"] = "1"
+    P.ecokv_stage_times()  # drop anything recorded before
+    for _ in range(args.steps):
+        ep.run(K, V, Q)
+    torch.cuda.synchronize()
+    stages = P.ecokv_stage_times()
+    os.environ["ECOKV_STAGE_TIMING"] = "0"
+
     e = 2
     Hkv, Hq, D, w = wl.Hkv, wl.Hq, wl.D, wl.w
     n_idx = ep.n_idx
@@ -121,17 +197,34 @@ def main():
         "select": bytes_scores + bytes_idx,
         "compact": bytes_gather + bytes_idx,
     }
+    # what each kernel must move at minimum (scratch between kernels is not counted)
+    stage_algo = {
+        "sweep1_stream": bytes_k + bytes_q, "sweep1_block": bytes_k + bytes_q,
+        "sweep2_stream": bytes_k + bytes_q, "sweep2_block": bytes_k + bytes_q,
+        "single_read": bytes_k + bytes_q + bytes_scores, "reduce1": 0, "epilogue1": 0,
+        "epilogue2": bytes_scores, "select": bytes_scores + bytes_idx, "compact": bytes_gather + bytes_idx,
+    }
     pass_bytes = bytes_k + bytes_q + bytes_gather + bytes_idx  # per-layer formula x L
-    dom = max(per_call_ms, key=per_call_ms.get)
-    dom_gbs = algo[dom] / (per_call_ms[dom] / 1e3) / 1e9
+    kernels = {}
+    for name, (ms, n) in stages.items():
+        avg_s = ms / n / 1e3
+        ab = stage_algo.get(name, 0)
+        kernels[name] = {"avg_us": round(avg_s * 1e6, 2), "launches": n, "algorithmic_bytes": ab,
+                         "GBs": round(ab / avg_s / 1e9, 1) if ab else None}
+    dom = max(kernels, key=lambda k: kernels[k]["avg_us"])
+    dom_s = kernels[dom]["avg_us"] / 1e6
+    dom_gbs = stage_algo[dom] / dom_s / 1e9
+    traffic = stored_traffic(dom)
     roofline = {
         "bound": "hbm",
-        "kernel": f"ecokv_{dom}",
+        "kernel": dom,
         "achieved": round(dom_gbs, 1),
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
         "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
-        "traffic": None,
+        "traffic": None if traffic is None else int(traffic),
+        "algorithmic_bytes": stage_algo[dom],
+        "avg_launch_us": kernels[dom]["avg_us"],
     }
     pass_gbs = pass_bytes / (ms_per_step / 1e3) / 1e9
 
@@ -199,10 +292,77 @@ def main():
                  "t_layer_us": round(t_layer_s * 1e6, 3)},
         "per_call_ms": {k: round(v, 4) for k, v in per_call_ms.items()},
         "per_call_algorithmic_bytes": algo,
+        "kernels": kernels,
     }
     if extras:
         out["extras"] = extras
     print(json.dumps(out), flush=True)
+
+
+def counter_run(ep, K, V, Q):
+    """Workload for rocprofv3 --pmc: three passes, then three copies of COPY_BYTES."""
+    import torch
+    for _ in range(3):
+        ep.run(K, V, Q)
+    torch.cuda.synchronize()
+    src = torch.ones(COPY_BYTES // 2, dtype=torch.bfloat16, device=K.device)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)  # reads and writes COPY_BYTES each
+    torch.cuda.synchronize()
+    log("counter run done")
+
+
+def _counter_rows(d):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    rows = []
+    for f in files:
+        with open(f, newline="") as fh:
+            rows.extend(csv.DictReader(fh))
+    return rows
+
+
+def traffic_summary(fetch_dir, write_dir, command):
+    """FETCH_SIZE and WRITE_SIZE (KiB per dispatch) per stage, scaled by the same counters
+    on a plain copy of COPY_BYTES, into the text that stored_traffic() reads."""
+    per = {}
+    for ctr, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        copies = []
+        for r in _counter_rows(d):
+            if r.get("Counter_Name") != ctr:
+                continue
+            kname = r.get("Kernel_Name", "")
+            val = float(r["Counter_Value"]) * 1024.0
+            if "neg" in kname and "kernel" in kname:
+                copies.append(val)
+                continue
+            st = stage_of_kernel(kname)
+            if st:
+                per.setdefault(st, {}).setdefault(ctr, []).append(val)
+        if not copies:
+            raise SystemExit(f"{ctr}: copy kernel not found")
+        per.setdefault("_copy", {})[ctr] = copies
+    cf = COPY_BYTES / (sum(per["_copy"]["FETCH_SIZE"]) / len(per["_copy"]["FETCH_SIZE"]))
+    cw = COPY_BYTES / (sum(per["_copy"]["WRITE_SIZE"]) / len(per["_copy"]["WRITE_SIZE"]))
+    print("HBM traffic per launch from rocprofv3 counters: 28-layer stack, 28 query / 4 KV heads, "
+          "head_dim 128, bf16, N=32768, window 4, budget 6553 per head (20 %)")
+    print(f"command: {command}")
+    print("FETCH_SIZE and WRITE_SIZE are KiB per dispatch; each is scaled by copy_bytes / counter "
+          f"on torch.neg over {COPY_BYTES} bytes (reads and writes that many bytes)")
+    print(f"copy_factor_fetch: {cf:.4f}")
+    print(f"copy_factor_write: {cw:.4f}")
+    print(f"source_digest: {source_digest()}")
+    print("# stage: name  fetch_bytes  write_bytes  =  scaled_total_bytes  (averages over dispatches)")
+    for st in STAGE_KERNELS:
+        if st not in per or "FETCH_SIZE" not in per[st] or "WRITE_SIZE" not in per[st]:
+            continue
+        f = sum(per[st]["FETCH_SIZE"]) / len(per[st]["FETCH_SIZE"]) * cf
+        w = sum(per[st]["WRITE_SIZE"]) / len(per[st]["WRITE_SIZE"]) * cw
+        print(f"stage: {st} {f:.0f} {w:.0f} = {f + w:.0f}")
 
 
 def cpu_baseline(wl, sample_layers):
@@ -217,18 +377,21 @@ def cpu_baseline(wl, sample_layers):
     threads = max(1, min(16, ncpu))
     Ls = min(sample_layers, wl.L)
     K, V, Q = wl.K[:Ls], wl.V[:Ls], wl.Q[:Ls]
-    log(f"cpu baseline: oracle on {Ls} layers x {wl.Hkv} heads with {threads} threads")
-    t0 = time.perf_counter()
-    S, _ = oracle.score(K, Q, Ls, wl.Hq, wl.Hkv, wl.cu_seqlens, wl.D, wl.w, nthreads=threads)
-    idx, counts, offsets = oracle.select(S, Ls, wl.Hkv, wl.cu_seqlens, wl.w, wl.budget, oracle.PER_HEAD,
-                                         nthreads=threads)
-    oracle.compact(K, V, Ls, wl.Hkv, wl.cu_seqlens, wl.D, idx, counts, offsets)
-    dt = time.perf_counter() - t0
+    log(f"cpu baseline: oracle on {Ls} layers x {wl.Hkv} heads with {threads} threads, repeated for >= 10 s")
+    reps, dt = 0, 0.0
+    while dt < 10.0 and reps < 64:
+        t0 = time.perf_counter()
+        S, _ = oracle.score(K, Q, Ls, wl.Hq, wl.Hkv, wl.cu_seqlens, wl.D, wl.w, nthreads=threads)
+        idx, counts, offsets = oracle.select(S, Ls, wl.Hkv, wl.cu_seqlens, wl.w, wl.budget, oracle.PER_HEAD,
+                                             nthreads=threads)
+        oracle.compact(K, V, Ls, wl.Hkv, wl.cu_seqlens, wl.D, idx, counts, offsets)
+        dt += time.perf_counter() - t0
+        reps += 1
     T = wl.cu_seqlens[-1]
     used = min(threads, Ls * wl.Hkv)
-    return {"value": round(T / (dt / Ls), 1), "unit": "tokens/s per layer", "cores": used, "kind": "oracle",
+    return {"value": round(T * reps / (dt / Ls), 1), "unit": "tokens/s per layer", "cores": used, "kind": "oracle",
             "sample": f"first {Ls} of {wl.L} layers ({Ls * wl.Hkv} (layer, head) units of {T} tokens), "
-                      f"score+select+compact, fp64, {dt:.2f}s wall"}
+                      f"score+select+compact, fp64, {reps} repetitions, {dt:.2f}s wall"}
 
 
 if __name__ == "__main__":

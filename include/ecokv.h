@@ -19,9 +19,11 @@
  * ---------------------------------------
  *  - All tensor pointers are DEVICE pointers unless stated; the caller
  *    allocates and owns every buffer (inputs, outputs, workspace).  The library
- *    never allocates or frees device memory, never synchronises, and keeps no
- *    mutable global state: calls on different streams with different
- *    workspaces may run concurrently.
+ *    never allocates or frees device memory and never synchronises outside
+ *    ecokv_stage_times().  Its only process-wide state is a launch counter, a
+ *    per-device cache of the compute-unit count and the optional stage timer;
+ *    calls on different streams with different workspaces may run
+ *    concurrently (see ecokv_score for the single-read path).
  *  - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *    Work is enqueued asynchronously; results are valid once the stream has
  *    been synchronised.
@@ -121,7 +123,14 @@ int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, s
  *   stats  [L][H_kv][B][ECOKV_NSTATS] float32 output, may be NULL
  *   workspace, workspace_bytes: device scratch of ecokv_workspace_size bytes,
  *   256-byte aligned.
- * Arithmetic: fp32 accumulation of bf16/fp32 inputs. */
+ * Arithmetic: fp32 accumulation of bf16/fp32 inputs.
+ * Paths: two sweeps over K (default), or, with the environment variable
+ * ECOKV_SCORE_PATH=single (bf16, head_dim 128, (H_q/H_kv)*w <= 28), one
+ * persistent kernel that reads K once and exchanges per-unit sums between its
+ * blocks.  That kernel needs all of its blocks resident at once (one per
+ * compute unit): it must not share the device with another running launch of
+ * it.  If a wait between its blocks ever times out, lambda and the scores of
+ * the launch come out NaN. */
 int ecokv_score(const void *K, const void *Q_win, int dtype, const ecokv_shape *shape,
                 const ecokv_params *params, float *scores, float *lambda, float *stats,
                 void *workspace, size_t workspace_bytes, void *stream);
@@ -160,6 +169,24 @@ int ecokv_compact(const void *K, const void *V, int dtype, const ecokv_shape *sh
 
 /* Message for the calling thread's last failed call ("" if none). */
 const char *ecokv_last_error(void);
+
+/*
+ * Optional per-kernel timing, for benchmarks.  While the environment variable
+ * ECOKV_STAGE_TIMING is set to 1 at the time of a call, ecokv_score,
+ * ecokv_select and ecokv_compact bracket every kernel they launch with HIP
+ * events on the call's stream (which adds a little launch overhead).
+ * ecokv_stage_times() waits for the recorded events, writes up to `max`
+ * entries (one per kernel name, in order of first launch) to `out` and their
+ * number to `*count`, and clears the record.  Host arrays; returns ECOKV_OK or
+ * ECOKV_EINVAL / ECOKV_EHIP.
+ */
+typedef struct {
+    char name[48];    /* kernel name                                      */
+    double ms;        /* summed duration of its launches, milliseconds     */
+    int64_t launches; /* number of launches                               */
+} ecokv_stage_time;
+
+int ecokv_stage_times(ecokv_stage_time *out, int max, int *count);
 
 #ifdef __cplusplus
 }

@@ -1,6 +1,8 @@
 """Build libecokv.so (HIP, gfx950) in-tree with hipcc.
 
-    python -m paper_2609_06663_amd.build
+    python paper_2609_06663_amd/build.py
+
+Run it as a script (not with -m): importing the package loads the library.
 """
 from __future__ import annotations
 

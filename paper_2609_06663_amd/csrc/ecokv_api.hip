@@ -1,9 +1,13 @@
 // C entry points of libecokv: host-side argument checks, workspace layout and
 // launches.  Every check completes before anything is enqueued.
 #include <math.h>
+#include <stdlib.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
+
+#include <mutex>
+#include <vector>
 
 #include "ecokv_internal.h"
 
@@ -107,9 +111,89 @@ int hip_fail(hipError_t e, const char *what)
     return fail(ECOKV_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+struct StageRec {
+    const char *name;
+    hipEvent_t start, stop;
+};
+std::mutex g_stage_mu;
+std::vector<StageRec> g_stages;
+thread_local const char *g_stage_name = nullptr;
+thread_local hipEvent_t g_stage_start = nullptr;
+
 }  // namespace
 
+namespace ecokv {
+
+bool stage_timing_on()
+{
+    const char *v = getenv("ECOKV_STAGE_TIMING");
+    return v && v[0] == '1' && v[1] == 0;
+}
+
+void stage_begin(const char *name, hipStream_t st)
+{
+    g_stage_name = nullptr;
+    if (!stage_timing_on()) return;
+    if (hipEventCreate(&g_stage_start) != hipSuccess) return;
+    if (hipEventRecord(g_stage_start, st) != hipSuccess) {
+        (void)hipEventDestroy(g_stage_start);
+        return;
+    }
+    g_stage_name = name;
+}
+
+void stage_end(hipStream_t st)
+{
+    if (!g_stage_name) return;
+    hipEvent_t stop;
+    if (hipEventCreate(&stop) != hipSuccess || hipEventRecord(stop, st) != hipSuccess) {
+        (void)hipEventDestroy(g_stage_start);
+        g_stage_name = nullptr;
+        return;
+    }
+    std::lock_guard<std::mutex> lk(g_stage_mu);
+    g_stages.push_back({g_stage_name, g_stage_start, stop});
+    g_stage_name = nullptr;
+}
+
+}  // namespace ecokv
+
 extern "C" {
+
+int ecokv_stage_times(ecokv_stage_time *out, int max, int *count)
+{
+    if (!count || (max > 0 && !out) || max < 0) return fail(ECOKV_EINVAL, "ecokv_stage_times: bad arguments");
+    std::vector<StageRec> recs;
+    {
+        std::lock_guard<std::mutex> lk(g_stage_mu);
+        recs.swap(g_stages);
+    }
+    int n = 0, rc = ECOKV_OK;
+    for (const StageRec &r : recs) {
+        float ms = 0.f;
+        hipError_t e = hipEventSynchronize(r.stop);
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.start, r.stop);
+        (void)hipEventDestroy(r.start);
+        (void)hipEventDestroy(r.stop);
+        if (e != hipSuccess) {
+            rc = hip_fail(e, "ecokv_stage_times");
+            continue;
+        }
+        int k = 0;
+        while (k < n && strcmp(out[k].name, r.name) != 0) ++k;
+        if (k == n) {
+            if (n >= max) continue;
+            memset(&out[n], 0, sizeof out[n]);
+            strncpy(out[n].name, r.name, sizeof out[n].name - 1);
+            ++n;
+        }
+        out[k].ms += ms;
+        out[k].launches += 1;
+    }
+    *count = n;
+    return rc;
+}
+
 
 int ecokv_default_params(ecokv_params *p)
 {

@@ -54,7 +54,7 @@ hipError_t compact_launch(const CompactArgs &a, hipStream_t st)
     const int64_t threads = a.total * a.segs;
     if (threads == 0) return hipSuccess;
     const int64_t blocks = (threads + kCompactThreads - 1) / kCompactThreads;
-    hipLaunchKernelGGL(k_compact, dim3((unsigned)blocks), dim3(kCompactThreads), 0, st, a);
+    ECOKV_TIMED("compact", st, hipLaunchKernelGGL(k_compact, dim3((unsigned)blocks), dim3(kCompactThreads), 0, st, a));
     return hipGetLastError();
 }
 

@@ -116,6 +116,19 @@ hipError_t select_launch(const SelectArgs &a, hipStream_t st);
 int select_max_flat_heads();
 hipError_t compact_launch(const CompactArgs &a, hipStream_t st);
 
+// Optional per-kernel timing (ECOKV_STAGE_TIMING=1): every launch site calls
+// stage_begin before and stage_end after its launch; both are no-ops unless
+// the variable is set.
+bool stage_timing_on();
+void stage_begin(const char *name, hipStream_t st);
+void stage_end(hipStream_t st);
+#define ECOKV_TIMED(name, st, ...)          \
+    do {                                    \
+        ::ecokv::stage_begin((name), (st)); \
+        __VA_ARGS__;                        \
+        ::ecokv::stage_end((st));           \
+    } while (0)
+
 // Workgroup barrier that orders LDS accesses only.  __syncthreads() also
 // orders global memory, which makes every barrier wait for all outstanding
 // global loads; this one leaves prefetched loads in flight.

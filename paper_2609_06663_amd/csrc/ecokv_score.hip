@@ -1441,7 +1441,8 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         a.nch2 = a.nch1;
         a.slices_per_lh = a.seq.spre[a.seq.nseq];
         a.items = a.L * a.Hkv * a.slices_per_lh;
-        if ((e = fused_launch(a, fgrid, st)) != hipSuccess) return e;
+        ECOKV_TIMED("single_read", st, e = fused_launch(a, fgrid, st));
+        if (e != hipSuccess) return e;
     } else {
         a.rpb1 = rows_per_block(a.D, bf16);
         a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
@@ -1450,29 +1451,29 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
             // streaming sweep 1: one 32-row window operand
             a.rpb1 = fast::kS2Keys;
             a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
-            hipLaunchKernelGGL(fast::k_fs1s, dim3(a.nch1, U), dim3(256), 0, st, a);
+            ECOKV_TIMED("sweep1_stream", st, hipLaunchKernelGGL(fast::k_fs1s, dim3(a.nch1, U), dim3(256), 0, st, a));
         } else {
-            launch_sweep(1, a, grid, st, bf16);
+            ECOKV_TIMED("sweep1_block", st, launch_sweep(1, a, grid, st, bf16));
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kThreads), 0, st, a);
+        ECOKV_TIMED("reduce1", st, hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kThreads), 0, st, a));
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (score_fast_path(a.D, bf16) && a.R <= kFusedMaxRows) {
             // streaming sweep 2: window rows and the four anchor rows in one operand
             a.rpb2 = fast::kS2Keys;
             a.nch2 = (maxT + a.rpb2 - 1) / a.rpb2;
-            hipLaunchKernelGGL(fast::k_fs2s, dim3(a.nch2, U), dim3(256), 0, st, a);
+            ECOKV_TIMED("sweep2_stream", st, hipLaunchKernelGGL(fast::k_fs2s, dim3(a.nch2, U), dim3(256), 0, st, a));
         } else {
             // block sweep 2: the chunking of the block sweeps (grid)
             a.rpb2 = rows_per_block(a.D, bf16);
             a.nch2 = (maxT + a.rpb2 - 1) / a.rpb2;
-            launch_sweep(2, a, grid, st, bf16);
+            ECOKV_TIMED("sweep2_block", st, launch_sweep(2, a, grid, st, bf16));
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(k_epi1, grid_e, dim3(kEpiThreads), 0, st, a);
+    ECOKV_TIMED("epilogue1", st, hipLaunchKernelGGL(k_epi1, grid_e, dim3(kEpiThreads), 0, st, a));
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_epi2, grid_e, dim3(kEpiThreads), 0, st, a);
+    ECOKV_TIMED("epilogue2", st, hipLaunchKernelGGL(k_epi2, grid_e, dim3(kEpiThreads), 0, st, a));
     return hipGetLastError();
 }
 

@@ -550,13 +550,13 @@ hipError_t select_launch(const SelectArgs &a, hipStream_t st)
         maxn = P * (a.flat ? a.Hkv : 1) > maxn ? P * (a.flat ? a.Hkv : 1) : maxn;
     }
     if (maxn <= 32 * kSelThreads)
-        hipLaunchKernelGGL(k_select_reg<32>, dim3(groups), dim3(kSelThreads), 0, st, a);
+        ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select_reg<32>, dim3(groups), dim3(kSelThreads), 0, st, a));
     else if (maxn <= kRegMaxKeys)
-        hipLaunchKernelGGL(k_select_reg<64>, dim3(groups), dim3(kSelThreads), 0, st, a);
+        ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select_reg<64>, dim3(groups), dim3(kSelThreads), 0, st, a));
     else if (maxn <= kLdsKeys)
-        hipLaunchKernelGGL(k_select<true>, dim3(groups), dim3(kSelThreads), 0, st, a);
+        ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select<true>, dim3(groups), dim3(kSelThreads), 0, st, a));
     else
-        hipLaunchKernelGGL(k_select<false>, dim3(groups), dim3(kSelThreads), 0, st, a);
+        ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select<false>, dim3(groups), dim3(kSelThreads), 0, st, a));
     return hipGetLastError();
 }
 

@@ -26,7 +26,11 @@ STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7, imp_m
             mu_norm2=10, scale=11)
 
 EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_score", "ecokv_index_count",
-           "ecokv_select", "ecokv_compact", "ecokv_last_error"]
+           "ecokv_select", "ecokv_compact", "ecokv_last_error", "ecokv_stage_times"]
+
+
+class _StageTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("ms", ctypes.c_double), ("launches", ctypes.c_int64)]
 
 
 class EcoKVError(RuntimeError):
@@ -69,7 +73,7 @@ class Shape:
 
 def _load():
     if not os.path.exists(_LIB_PATH):
-        raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2609_06663_amd.build`")
+        raise ImportError(f"{_LIB_PATH} is not built; run `python paper_2609_06663_amd/build.py`")
     lib = ctypes.CDLL(_LIB_PATH)
     vp, sp, pp = ctypes.c_void_p, ctypes.POINTER(_Shape), ctypes.POINTER(Params)
     i32p = ctypes.POINTER(ctypes.c_int32)
@@ -80,6 +84,7 @@ def _load():
     lib.ecokv_select.argtypes = [vp, sp, ctypes.c_int, i32p, vp, vp, vp, vp]
     lib.ecokv_compact.argtypes = [vp, vp, ctypes.c_int, sp, ctypes.c_int, i32p, vp, vp, vp, vp, vp, vp]
     lib.ecokv_last_error.restype = ctypes.c_char_p
+    lib.ecokv_stage_times.argtypes = [ctypes.POINTER(_StageTime), ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
     for name in EXPORTS:
         if name != "ecokv_last_error":
             getattr(lib, name).restype = ctypes.c_int
@@ -175,3 +180,11 @@ def ecokv_compact(K: torch.Tensor, V: torch.Tensor, shape: Shape, mode: int, bud
 
 def ecokv_last_error() -> str:
     return lib.ecokv_last_error().decode()
+
+
+def ecokv_stage_times(max_entries: int = 32) -> dict:
+    """Per-kernel times recorded while ECOKV_STAGE_TIMING=1: {name: (ms, launches)}; clears the record."""
+    arr = (_StageTime * max_entries)()
+    n = ctypes.c_int(0)
+    _check(lib.ecokv_stage_times(arr, int(max_entries), ctypes.byref(n)))
+    return {arr[i].name.decode(): (arr[i].ms, int(arr[i].launches)) for i in range(n.value)}
