@@ -10,7 +10,7 @@
 
 namespace ecokv {
 
-
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kCompactThreads = 256;
 
@@ -43,10 +43,14 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a)
     const int64_t src = ((int64_t)l * a.Hkv + h) * a.Ttot + a.seq.cu[s] + pos;
     const int64_t so = src * a.row_bytes + (int64_t)seg * 16;
     const int64_t d = e * a.row_bytes + (int64_t)seg * 16;
-    const uint4 kv = *reinterpret_cast<const uint4 *>(a.K + so);
-    const uint4 vv = *reinterpret_cast<const uint4 *>(a.V + so);
-    *reinterpret_cast<uint4 *>(a.Kc + d) = kv;
-    *reinterpret_cast<uint4 *>(a.Vc + d) = vv;
+    // Nontemporal in both directions: the rows are read once here, and the
+    // compacted copy is not read again by this pass.  Without the streaming
+    // hint the written lines stay dirty in the caches and are written back
+    // while the next pass streams K, taking bandwidth from it.
+    const u32x4 kv = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(a.K + so));
+    const u32x4 vv = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(a.V + so));
+    __builtin_nontemporal_store(kv, reinterpret_cast<u32x4 *>(a.Kc + d));
+    __builtin_nontemporal_store(vv, reinterpret_cast<u32x4 *>(a.Vc + d));
 }
 
 hipError_t compact_launch(const CompactArgs &a, hipStream_t st)

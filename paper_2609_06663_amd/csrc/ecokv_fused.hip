@@ -6,39 +6,35 @@
 // persistent kernel reads every key from HBM once and keeps it on chip until
 // the constants of its unit are known:
 //
-//   * work item = 256 consecutive keys of one (layer, KV head, sequence)
-//     unit; block b takes items b, b + G, b + 2G, ... (G = grid size, one
-//     block per CU, all co-resident);
-//   * 4 loader waves stream the next item's keys and window rows from HBM
-//     into registers and swap them into LDS once per iteration;
-//   * 8 compute waves run sweep 1 on the item in LDS (window logits on the
-//     matrix cores with the keys as the A operand, so each lane holds one
-//     window row and the softmax statistics need no cross-lane work; |k|; the
-//     column sums of k and k/|k| on the matrix cores from transposed LDS
-//     reads) and keep each wave's 32 keys as MFMA operands in registers;
-//   * two iterations later, once the unit's constants are published, they
-//     run sweep 2 on those registers (window attention a_i, d_E, khat.mu).
+//   * work item ("slice") = 224 consecutive keys of one (layer, KV head,
+//     sequence) unit; block b takes slices b, b + G, b + 2G, ... (G = grid
+//     size, two blocks per CU so that one computes while the other waits,
+//     all co-resident);
+//   * 7 compute waves own 32 keys each.  A wave's keys arrive in its own 32
+//     LDS rows by direct-to-LDS buffer loads (rows past the unit read as
+//     zero), are read once into MFMA operand registers and stay there until
+//     sweep 2; as soon as they are in registers the wave issues the loads of
+//     its rows of the next slice, so HBM traffic continues through the
+//     publication wait;
+//   * sweep 1 in registers: window logits on the matrix cores (keys as the A
+//     operand, so each lane holds one window row and its softmax statistics
+//     need no cross-lane work), |k|, and the column sums of k and k/|k| on the
+//     matrix cores from transposed LDS reads of the wave's rows;
+//   * wave 7 runs the publication protocol alone, so that its waits never
+//     queue behind the key loads in flight in the compute waves;
+//   * sweep 2 from the same registers: window attention a_i, d_E, khat.mu.
 //
-// Publication between blocks.  Item partials (column sums, softmax max and
+// Publication between blocks.  Slice partials (column sums, softmax max and
 // sum per window row) and unit constants are 64-bit words (launch tag << 32 |
 // float bits), written and read as relaxed device-scope atomics.  A reader
 // accepts a word only if it carries this launch's tag, so no release/acquire
 // fence (an L2 write-back / invalidate on this GPU) is ever needed.  Every
-// block that holds an item of a unit reduces a fixed slice of the unit's
-// columns over all of the unit's items (in item order: deterministic), and
-// every block then reads the whole record.  Per iteration k of a block:
-//   phase 0   issue loads: partial slices of item k-1's unit, constants of
-//             item k-2's unit; loaders issue item k+1.  Sweep 1 logits.
-//   phase 1-2 sweep 1 column sums; item partial assembled in LDS.
-//   phase 3   check the loads of phase 0 (retry until tagged), publish the
-//             item partial, reduce and publish the column slice, stage the
-//             constants for sweep 2.
-//   phase 4   sweep 2 of item k-2; keep item k's keys in registers.
-//   phase 5   loaders swap item k+1 into LDS; item k-2's d_E extrema out.
-// Deadlock freedom: a block waits only for partials of a unit whose items
-// are all claimed by steps <= k (a unit has at most G items, so it spans at
-// most two steps) and for slices reduced by blocks that only wait on older
-// units; the block furthest behind never waits on a later one.  Every wait
+// block that holds a slice of a unit reduces a fixed part of the unit's
+// columns over all of the unit's slices (in slice order: deterministic), and
+// every block then reads the whole record.
+// Deadlock freedom: a block waits only for slices of the unit it holds; a
+// unit has at most G slices, so they sit in at most two consecutive steps,
+// and the earliest unfinished unit never waits for a later one.  Every wait
 // is bounded; a timeout marks the launch failed (status = tag) and the
 // epilogue then writes NaN.
 #include "ecokv_fast.h"
@@ -48,28 +44,26 @@
 namespace ecokv {
 namespace fast {
 
-constexpr int kItem = kFusedItem;                  // 256 keys
-constexpr int kCWaves = 8;                         // compute waves (32 keys each)
-constexpr int kLWaves = 4;                         // loader waves
-constexpr int kPWaves = kCWaves;                   // waves that run the publication protocol
-constexpr int kFThreads = (kCWaves + kLWaves) * kWave;
-constexpr int kPThreads = kPWaves * kWave;         // 512
-constexpr int kLThreads = kLWaves * kWave;         // 256
+constexpr int kItem = kFusedItem;                  // keys per slice
+constexpr int kCW = kItem / 32;                    // compute waves, 32 keys each
+constexpr int kFThreads = (kCW + 1) * kWave;       // plus the protocol wave
+constexpr int kFBlocksPerCU = 2;                   // two blocks per CU: one computes while the other waits
+// (the second launch bound is the minimum number of waves per SIMD)
 constexpr int kCols = 2 * kD + 2 * kFusedMaxRows;  // record width for the largest R
-constexpr int kChunkPerLane = 2;                   // tagged loads per protocol lane for one column slice
-constexpr int kQSlots = 4;                         // window-row tiles of items k+1, k, k-1, k-2
-constexpr int kChunkMax = kChunkPerLane * kPThreads;
+constexpr int kChunkPerLane = 12;                  // tagged loads per protocol lane for one column part
+constexpr int kChunkMax = kChunkPerLane * kWave;
 constexpr int kSpinLimit = 1 << 14;                // retries of a wait (each at least one memory round trip)
+static_assert(kCW * 32 == kItem && kFThreads <= 1024, "slice = 32 keys per compute wave");
 
 struct Item {
     int valid;
-    int u, j, n;  // unit, index of the item in the unit, items of the unit
+    int u, j, n;  // unit, index of the slice in the unit, slices of the unit
     int T, P;     // keys and non-window keys of the unit
-    int base;     // first key of the item in the unit
+    int base;     // first key of the slice in the unit
 };
 
-// Items of one block in order (b, b + G, b + 2G, ...) as (lh, rem): lh the
-// (layer, head) group, rem the item within it; one step adds G with 32-bit
+// Slices of one block in order (b, b + G, b + 2G, ...) as (lh, rem): lh the
+// (layer, head) group, rem the slice within it; one step adds G with 32-bit
 // arithmetic only (the division of G by the group size happens once).
 struct ItemGen {
     int lh, rem, qG, rG;
@@ -115,10 +109,10 @@ __device__ __forceinline__ Item item_of(const ScoreArgs &a, const ItemGen &g)
     return r;
 }
 
-// The column slice reduced by item j of a unit with n items: logical columns
+// The column part reduced by slice j of a unit with n slices: logical columns
 // [j*Cc/n, (j+1)*Cc/n) of Cc = 2D + R (2D sums, then R (max, normaliser)
 // pairs).  Its load list: ns sum columns, then np max columns, then np
-// normaliser columns, each over the unit's n items.
+// normaliser columns, each over the unit's n slices.
 struct Chunk {
     int cs0, ns, r0, np, nl;
 };
@@ -159,74 +153,62 @@ __device__ __forceinline__ bool tag_ok(unsigned long long x, unsigned tag) { ret
 __device__ __forceinline__ float tag_val(unsigned long long x) { return __uint_as_float((unsigned)x); }
 
 struct __attribute__((aligned(16))) FusedLds {
-    u32x4 kt[kItem * kChunks];            // keys of the item in sweep 1 (swizzled 16-byte chunks)
-    u32x4 qs[kQSlots][32 * kChunks];      // window rows of item k in slot k % 4 (rows >= R zero); rows
-                                          // 28..31 take mu and kbar before the item's sweep 2
-    uint16_t aw[2][4][kTile];             // per 128-key tile: 1, 1/|k| high, 1/|k| remainder, 0
-    float sm[kCWaves][2][32], ss[kCWaves][2][32];  // per wave and half: row max and sum of 2^(x - max)
-    float cx[4][2][32];                   // column sums of the second tile
-    float part[kCols];                    // partial record of the sweep-1 item
-    float anc[kCols];                     // constants of the sweep-2 item's unit
-    float cv[kChunkMax];                  // validated partial values of the column slice
-    float rowM[32], rowIS[32];
-    float kb2;
-    float dred[kCWaves][3];
-    int flag[2][2][kPWaves];              // [retry parity][slice, constants][wave]
-    int dead;                             // a wait of this block timed out: skip the remaining waits
+    u32x4 kt[kItem * kChunks];  // the slice's keys: rows 32w .. 32w+31 belong to compute wave w
+                                // (16-byte chunks swizzled by row)
+    uint16_t wts[kCW][4][32];   // per wave: 1, 1/|k| high, 1/|k| remainder, 0
+    float wcs[kCW][2][kD];      // per wave: column sums of k and of k/|k|; the protocol wave
+                                // reuses the space for the values of its column part
+    float wm[kCW][32], wsm[kCW][32];  // per wave: row max and sum of 2^(x - max)
+    float anc[kCols];           // constants of the slice's unit
+    u32x4 arow[4][kChunks];     // operand rows mu high, mu remainder, kbar high, kbar remainder (bf16)
+    float rsh[32];              // per window row: max + log2(normaliser); +inf past R
+    float kb2;                  // |kbar|^2 as the operand rows represent kbar
+    float dred[kCW][3];         // per wave: sum, min, max of d_E
 };
+static_assert(sizeof(float) * kCW * 2 * kD >= sizeof(float) * kChunkMax, "column part fits the wcs space");
 
-// Loader: one item's keys (16 lanes per 256-byte row) and window rows.
-__device__ __forceinline__ void issue_keys(const ScoreArgs &a, const Item &it, int ltid, u32x4 (&lk)[16])
+// A compute wave's 32 rows of slice `it` into its LDS rows: 8 direct-to-LDS
+// 16-byte buffer loads; instruction i fills rows 4i .. 4i+3, lane l takes
+// physical chunk l % 16 of row 4i + l / 16, which holds logical chunk
+// (l % 16) ^ row.  The descriptor spans the unit's T rows, so rows past T
+// land as zeros.
+__device__ __forceinline__ void dma_keys(const ScoreArgs &a, const Item &it, int cw, int lane, u32x4 *dst)
 {
     if (!it.valid) return;
     const Unit un = unit_of(it.u, a.Hkv, a.B);
     const uint16_t *krow0 = static_cast<const uint16_t *>(a.K) + unit_row0(a, un) * kD;
     const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, it.T);
-    const int c = ltid & 15, g = ltid >> 4;
+    const int r0 = it.base + 32 * cw;
 #pragma unroll
-    for (int jj = 0; jj < 16; ++jj)
-        lk[jj] = __builtin_amdgcn_raw_buffer_load_b128(rs, (it.base + g + 16 * jj) * (kD * 2) + c * 16, 0, 0);
-}
-
-// Loader: the window rows of an item straight into a row tile (no
-// registers).  Each direct-to-LDS 16-byte load of a wave fills 64 consecutive
-// chunks, i.e. rows 4i .. 4i+3 of the swizzled tile; lane l takes physical
-// chunk l % 16 of row 4i + l / 16, which holds logical chunk (l % 16) ^ row.
-__device__ __forceinline__ void dma_rows(const ScoreArgs &a, const Item &it, int lw, int lane, u32x4 *q)
-{
-    if (!it.valid) return;
-    const Unit un = unit_of(it.u, a.Hkv, a.B);
-    const int ninst = (a.R + 3) >> 2;
-    for (int i = lw; i < ninst; i += kLWaves) {
+    for (int i = 0; i < 8; ++i) {
         const int r = 4 * i + (lane >> 4), c = (lane & 15) ^ (r & 15);
-        if (r < a.R)
-            __builtin_amdgcn_global_load_lds(
-                static_cast<const uint16_t *>(a.Q) + window_row(a, un, r) * kD + c * 8,
-                (__attribute__((address_space(3))) void *)(q + 64 * i), 16, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)(dst + 64 * i), 16,
+                                                 (r0 + r) * (kD * 2) + c * 16, 0, 0, 0);
     }
 }
 
-__device__ __forceinline__ void wait_all_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
-
-// Barrier for the loader waves between their load issue and their LDS
-// writes: they write no LDS in that span, so no release fence (which would
-// wait for the in-flight direct-to-LDS loads); the acquire side still orders
-// their later LDS reads (the publication flags) after the barrier.
-__device__ __forceinline__ void loader_barrier()
+// Window rows of the slice's unit as the 32-row MFMA operand (lane l: row
+// l % 32, chunks 2s + l / 32); rows >= R read as zero (offset past the range).
+__device__ __forceinline__ void load_window(const ScoreArgs &a, const Item &it, int lane, u32x4 (&aq)[8])
 {
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+    if (!it.valid) return;
+    const Unit un = unit_of(it.u, a.Hkv, a.B);
+    const int r = lane & 31;
+    const int qbytes = (int)((int64_t)a.L * a.Hq * a.B * a.w * kD * 2);
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(a.Q), (short)0, qbytes, 0x00020000);
+    const unsigned off = r < a.R ? (unsigned)(window_row(a, un, r) * (kD * 2)) + (lane >> 5) * 16u : 0x80000000u;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) aq[s] = __builtin_amdgcn_raw_buffer_load_b128(rs, off + 32u * s, 0, 0);
 }
 
-// Protocol loads: the column slice of item `ic` (partials of its unit) and
-// the constants of item `i2`'s unit.
-__device__ __forceinline__ void issue_chunk(const ScoreArgs &a, const Item &ic, const Chunk &ch, int C, int ptid,
+// Protocol wave: loads of its column part of slice `ic` (partials of the unit).
+__device__ __forceinline__ void issue_chunk(const ScoreArgs &a, const Item &ic, const Chunk &ch, int C, int lane,
                                             unsigned long long (&cl)[kChunkPerLane])
 {
-    if (!ic.valid) return;
 #pragma unroll
     for (int q = 0; q < kChunkPerLane; ++q) {
-        const int t = ptid + kPThreads * q;
+        const int t = lane + kWave * q;
         if (t < ch.nl) {
             const int i = t / ic.n, jj = t - i * ic.n;
             const int col = chunk_col(ch, i, a.R);
@@ -235,109 +217,70 @@ __device__ __forceinline__ void issue_chunk(const ScoreArgs &a, const Item &ic, 
     }
 }
 
-__device__ __forceinline__ bool chunk_ok(const ScoreArgs &a, const Item &ic, const Chunk &ch, int ptid,
+__device__ __forceinline__ bool chunk_ok(const ScoreArgs &a, const Chunk &ch, int lane,
                                          const unsigned long long (&cl)[kChunkPerLane])
 {
     bool ok = true;
-    if (ic.valid) {
 #pragma unroll
-        for (int q = 0; q < kChunkPerLane; ++q)
-            if (ptid + kPThreads * q < ch.nl) ok = ok && tag_ok(cl[q], a.tag);
-    }
+    for (int q = 0; q < kChunkPerLane; ++q)
+        if (lane + kWave * q < ch.nl) ok = ok && tag_ok(cl[q], a.tag);
     return ok;
 }
 
-__device__ __forceinline__ void issue_consts(const ScoreArgs &a, const Item &i2, int C, int ptid,
-                                             unsigned long long &al)
-{
-    if (i2.valid && ptid < C) al = tag_load(&a.ancT[(long long)i2.u * C + ptid]);
-}
+constexpr int kConstPerLane = (kCols + kWave - 1) / kWave;
 
-__device__ __forceinline__ bool consts_ok(const ScoreArgs &a, const Item &i2, int C, int ptid,
-                                          unsigned long long al)
+__device__ __forceinline__ void issue_consts(const ScoreArgs &a, const Item &it, int C, int lane,
+                                             unsigned long long (&al)[kConstPerLane])
 {
-    return !(i2.valid && ptid < C) || tag_ok(al, a.tag);
-}
-
-__device__ __forceinline__ bool all_flags(const FusedLds &S, int par, int kind)
-{
-    int ok = 1;
 #pragma unroll
-    for (int w = 0; w < kPWaves; ++w) ok &= S.flag[par][kind][w];
-    return ok != 0;
-}
-
-// Barrier skeleton of a publication wait for the loader waves, which take no
-// part in it: the same flag reads (so the same number of iterations) and
-// barriers.
-__device__ __forceinline__ void follow_flags(const FusedLds &S, int kind)
-{
-    if (S.dead) return;
-    int par = 0, tries = 0;
-    while (!all_flags(S, par, kind)) {
-        if (++tries > kSpinLimit) break;
-        par ^= 1;
-        loader_barrier();
+    for (int q = 0; q < kConstPerLane; ++q) {
+        const int c = lane + kWave * q;
+        if (c < C) al[q] = tag_load(&a.ancT[(long long)it.u * C + c]);
     }
 }
 
-// Reduce the validated column slice (S.cv) of item ic and publish it: sums /
-// T as kbar and mu, merged (max, normaliser) pairs as they are.  The order of
+__device__ __forceinline__ bool consts_ok(const ScoreArgs &a, int C, int lane,
+                                          const unsigned long long (&al)[kConstPerLane])
+{
+    bool ok = true;
+#pragma unroll
+    for (int q = 0; q < kConstPerLane; ++q)
+        if (lane + kWave * q < C) ok = ok && tag_ok(al[q], a.tag);
+    return ok;
+}
+
+// Reduce the validated column part (cv) of slice ic and publish it: sums / T
+// as kbar and mu, merged (max, normaliser) pairs as they are.  The order of
 // every sum depends only on (n, j): the result is the same in any block.
-__device__ __forceinline__ void reduce_chunk(const ScoreArgs &a, const Item &ic, const Chunk &ch, int C, int ptid,
-                                             const FusedLds &S)
+__device__ __forceinline__ void reduce_chunk(const ScoreArgs &a, const Item &ic, const Chunk &ch, int C, int lane,
+                                             const float *cv)
 {
     const int n = ic.n, ncl = ch.ns + ch.np;
     const float invT = 1.f / (float)ic.T;
     unsigned long long *outT = a.ancT + (long long)ic.u * C;
     float *outP = a.anchors + (long long)ic.u * C;
-    if (n >= 16) {
-        for (int t = ptid; t < ncl * 16; t += kPThreads) {  // 16 lanes per column; groups stay whole
-            const int lc = t >> 4, q = t & 15;
-            if (lc < ch.ns) {
-                float s = 0.f;
-                for (int jj = q; jj < n; jj += 16) s += S.cv[lc * n + jj];
-                s += __shfl_xor(s, 8, 16);
-                s += __shfl_xor(s, 4, 16);
-                s += __shfl_xor(s, 2, 16);
-                s += __shfl_xor(s, 1, 16);
-                if (q == 0) {
-                    const int col = ch.cs0 + lc;
-                    tag_store(outT + col, s * invT, a.tag);
-                    outP[col] = s * invT;
-                }
-            } else {
-                const int pr = lc - ch.ns;
-                const float *mv = S.cv + (ch.ns + pr) * n, *sv = S.cv + (ch.ns + ch.np + pr) * n;
-                float m = -INFINITY, s = 0.f;
-                for (int jj = q; jj < n; jj += 16) softmax_merge2(m, s, mv[jj], sv[jj]);
-#pragma unroll
-                for (int x = 8; x >= 1; x >>= 1) {
-                    const float m2 = __shfl_xor(m, x, 16), s2 = __shfl_xor(s, x, 16);
-                    softmax_merge2(m, s, m2, s2);
-                }
-                if (q == 0) {
-                    const int r = ch.r0 + pr;
-                    tag_store(outT + 2 * kD + r, m, a.tag);
-                    tag_store(outT + 2 * kD + a.R + r, s, a.tag);
-                    outP[2 * kD + r] = m;
-                    outP[2 * kD + a.R + r] = s;
-                }
-            }
-        }
-    } else {
-        for (int lc = ptid; lc < ncl; lc += kPThreads) {
-            if (lc < ch.ns) {
-                float s = 0.f;
-                for (int jj = 0; jj < n; ++jj) s += S.cv[lc * n + jj];
+    for (int t = lane; t < ncl * 16; t += kWave) {  // 16 lanes per column; groups stay whole
+        const int lc = t >> 4, q = t & 15;
+        if (lc < ch.ns) {
+            float s = 0.f;
+            for (int jj = q; jj < n; jj += 16) s += cv[lc * n + jj];
+            s = seg16_sum(s);
+            if (q == 0) {
                 const int col = ch.cs0 + lc;
                 tag_store(outT + col, s * invT, a.tag);
                 outP[col] = s * invT;
-            } else {
-                const int pr = lc - ch.ns;
-                const float *mv = S.cv + (ch.ns + pr) * n, *sv = S.cv + (ch.ns + ch.np + pr) * n;
-                float m = -INFINITY, s = 0.f;
-                for (int jj = 0; jj < n; ++jj) softmax_merge2(m, s, mv[jj], sv[jj]);
+            }
+        } else {
+            const int pr = lc - ch.ns;
+            const float *mv = cv + (ch.ns + pr) * n, *sv = cv + (ch.ns + ch.np + pr) * n;
+            float m = -INFINITY, s = 0.f;
+            for (int jj = q; jj < n; jj += 16) softmax_merge2(m, s, mv[jj], sv[jj]);
+#pragma unroll
+            for (int x = 8; x >= 1; x >>= 1) {
+                const float m2 = __shfl_xor(m, x, 16), s2 = __shfl_xor(s, x, 16);
+                softmax_merge2(m, s, m2, s2);
+            }
+            if (q == 0) {
                 const int r = ch.r0 + pr;
                 tag_store(outT + 2 * kD + r, m, a.tag);
                 tag_store(outT + 2 * kD + a.R + r, s, a.tag);
@@ -348,324 +291,307 @@ __device__ __forceinline__ void reduce_chunk(const ScoreArgs &a, const Item &ic,
     }
 }
 
-__global__ __launch_bounds__(kFThreads, 1) void k_fused(ScoreArgs a)
+// d_E partial of a finished slice (sum over keys < T, extrema over keys < P)
+// from the compute waves' records.
+__device__ __forceinline__ void write_dstats(const ScoreArgs &a, const Item &it, const FusedLds &S)
+{
+    float s = 0.f, mn = INFINITY, mx = -INFINITY;
+    for (int w2 = 0; w2 < kCW; ++w2) {
+        s += S.dred[w2][0];
+        mn = fminf(mn, S.dred[w2][1]);
+        mx = fmaxf(mx, S.dred[w2][2]);
+    }
+    float *pp = a.part2 + ((int64_t)it.u * a.nch2 + it.j) * 4;
+    pp[0] = s;
+    pp[1] = mn;
+    pp[2] = mx;
+    pp[3] = 0.f;
+}
+
+// The protocol wave's part of one slice: the block partial from the compute
+// waves' LDS records and its publication, the unit's column part assigned to
+// this slice, then the unit's constants into LDS.  Returns false once a wait
+// has run out of time (the caller then stops waiting for the rest of the
+// launch).
+__device__ bool protocol(const ScoreArgs &a, const Item &it, int lane, FusedLds &S, bool live)
+{
+    const int C = 2 * kD + 2 * a.R;
+    // block partial: column sums over the compute waves, softmax merges over them
+    for (int c = lane; c < 2 * kD; c += kWave) {
+        const int which = c / kD, d = c % kD;
+        float s = 0.f;
+#pragma unroll
+        for (int w = 0; w < kCW; ++w) s += S.wcs[w][which][d];
+        tag_store(&a.partT[((long long)it.u * C + c) * a.nch1 + it.j], s, a.tag);
+    }
+    if (lane < a.R) {
+        float m = -INFINITY, s = 0.f;
+#pragma unroll
+        for (int w = 0; w < kCW; ++w) softmax_merge2(m, s, S.wm[w][lane], S.wsm[w][lane]);
+        tag_store(&a.partT[((long long)it.u * C + 2 * kD + lane) * a.nch1 + it.j], m, a.tag);
+        tag_store(&a.partT[((long long)it.u * C + 2 * kD + a.R + lane) * a.nch1 + it.j], s, a.tag);
+    }
+    // the column part assigned to this slice: wait for every slice's partial
+    const Chunk ch = chunk_of(it.j, it.n, a.R);
+    unsigned long long cl[kChunkPerLane] = {};
+    issue_chunk(a, it, ch, C, lane, cl);
+    int tries = 0;
+    while (live && !__all(chunk_ok(a, ch, lane, cl))) {
+        if (++tries > kSpinLimit) {
+            live = false;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+        issue_chunk(a, it, ch, C, lane, cl);
+    }
+    float *cv = &S.wcs[0][0][0];  // the wave records were read above
+#pragma unroll
+    for (int q = 0; q < kChunkPerLane; ++q) {
+        const int t = lane + kWave * q;
+        if (t < ch.nl) cv[t] = tag_val(cl[q]);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    reduce_chunk(a, it, ch, C, lane, cv);
+    // the unit's constants
+    unsigned long long al[kConstPerLane] = {};
+    issue_consts(a, it, C, lane, al);
+    tries = 0;
+    while (live && !__all(consts_ok(a, C, lane, al))) {
+        if (++tries > kSpinLimit) {
+            live = false;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+        issue_consts(a, it, C, lane, al);
+    }
+#pragma unroll
+    for (int q = 0; q < kConstPerLane; ++q) {
+        const int c = lane + kWave * q;
+        if (c < C) S.anc[c] = tag_val(al[q]);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    if (lane < 32) {
+        const bool r_ok = lane < a.R;
+        const float M = r_ok ? S.anc[2 * kD + lane] : 0.f, Sn = r_ok ? S.anc[2 * kD + a.R + lane] : 1.f;
+        S.rsh[lane] = r_ok ? M + __log2f(Sn) : INFINITY;
+    }
+    // |kbar|^2 of the centroid as the operand rows represent it (bf16 high + remainder)
+    float acc2 = 0.f;
+#pragma unroll
+    for (int z = 0; z < 2; ++z) {
+        const float f = S.anc[2 * lane + z];
+        const float fh = __uint_as_float(bf16_rne(f) << 16);
+        const float fl = __uint_as_float(bf16_rne(f - fh) << 16);
+        acc2 = fmaf(fh + fl, fh + fl, acc2);
+    }
+    acc2 = wave_sum(acc2);
+    if (lane == 0) S.kb2 = acc2;
+    // the anchor rows of the sweep-2 operand: lane 16q + c builds chunk c of row q
+    {
+        const int which = lane >> 4, c = lane & 15;
+        const float *src = ((which < 2) ? S.anc + kD : S.anc) + 8 * c;
+        u32x4 q;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            unsigned half2[2];
+#pragma unroll
+            for (int z = 0; z < 2; ++z) {
+                const float f = src[2 * e + z];
+                const unsigned hb = bf16_rne(f);
+                half2[z] = (which & 1) ? bf16_rne(f - __uint_as_float(hb << 16)) : hb;
+            }
+            q[e] = half2[0] | (half2[1] << 16);
+        }
+        S.arow[which][c] = q;
+    }
+    return live;
+}
+
+__global__ __launch_bounds__(kFThreads, kFBlocksPerCU * kFThreads / kWave / 4) void k_fused(ScoreArgs a)
 {
     __shared__ FusedLds S;
 
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const bool comp = wv < kCWaves, loader = !comp;
+    const int lane = threadIdx.x & 63;
+    const bool comp = wv < kCW;
     const int G = gridDim.x;
-    const int C = 2 * kD + 2 * a.R;
     const float sc = a.inv_sqrt_d * kLog2e;
     const float inv_r = 1.f / (float)a.R;
     const int nsteps = (a.items + G - 1) / G;
-    const int niter = nsteps + 2;  // sweep 2 lags two iterations
+    constexpr int kAnc = kFusedMaxRows;
 
-    // window-row tiles start zero (rows >= R stay zero); tile weights rows 0 and 3
-    for (int i = threadIdx.x; i < kQSlots * 32 * kChunks; i += kFThreads)
-        (&S.qs[0][0])[i] = (u32x4){0u, 0u, 0u, 0u};
-    for (int i = threadIdx.x; i < 2 * kTile; i += kFThreads) {
-        S.aw[i / kTile][0][i % kTile] = 0x3f80;
-        S.aw[i / kTile][3][i % kTile] = 0;
-    }
-    if (threadIdx.x == 0) S.dead = 0;
-
-    // One register array serves both roles (the allocator cannot see that the
-    // roles are exclusive): loader waves stage the next item's keys in it,
-    // compute waves keep the keys of the two items waiting for sweep 2 as MFMA
-    // operands (elements 0..7: item k-2, 8..15: item k-1 at iteration k).
-    u32x4 lk[16];
-    float sn2[2] = {0.f, 0.f}, sinv[2] = {0.f, 0.f};
-    unsigned long long cl[kChunkPerLane] = {}, al = 0;
-    lds_barrier();  // zero fill done before the first item lands
-    // items k+1, k, k-1, k-2 of this block, shifted once per iteration
     ItemGen gen = item_gen(a, blockIdx.x, G);
-    Item in = item_of(a, gen), i1{}, ic{}, i2{};
-    if (loader) {
-        const int ltid = threadIdx.x - kCWaves * kWave;
-        const Item &i0 = in;
-        dma_rows(a, i0, wv - kCWaves, threadIdx.x & 63, S.qs[0]);
-        issue_keys(a, i0, ltid, lk);
-        if (i0.valid) {
-            const int c = ltid & 15, g = ltid >> 4;
-#pragma unroll
-            for (int jj = 0; jj < 16; ++jj) S.kt[sw(g + 16 * jj, c)] = lk[jj];
+    Item it = item_of(a, gen);
+    Item prev{};
+
+    if (!comp) {
+        // the protocol wave: the same barrier sequence as the compute waves
+        bool live = true;
+#pragma unroll 1
+        for (int k = 0; k < nsteps; ++k) {
+            item_next(a, gen);
+            const Item nx = item_of(a, gen);
+            lds_barrier();  // B1: the slice's wave records (and the last slice's d_E records) are in
+            if (prev.valid && lane == 0) write_dstats(a, prev, S);
+            if (it.valid) {
+                const bool ok = protocol(a, it, lane, S, live);
+                if (live && !ok && lane == 0)
+                    __hip_atomic_store(a.status, a.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                live = ok;
+            }
+            lds_barrier();  // B2: the unit's constants are in
+            prev = it;
+            it = nx;
         }
-        wait_all_loads();
+        lds_barrier();
+        if (prev.valid && lane == 0) write_dstats(a, prev, S);
+        return;
     }
+
+    u32x4 *wkt = S.kt + 32 * kChunks * wv;
+    u32x4 aq[8];  // window operand; rows kAnc .. kAnc+3 take mu and kbar before sweep 2
+    if (lane < 32) {
+        S.wts[wv][0][lane] = 0x3f80;  // 1.0
+        S.wts[wv][3][lane] = 0;
+    }
+    dma_keys(a, it, wv, lane, wkt);
+    load_window(a, it, lane, aq);
 
 #pragma unroll 1
-    for (int k = 0; k < niter; ++k) {
+    for (int k = 0; k < nsteps; ++k) {
         // lane-derived indices are recomputed every iteration: kept out of the
         // loop-invariant set, which would otherwise pin them in registers
         int tv = threadIdx.x;
         asm volatile("" : "+v"(tv));
-        const int tid = tv, lane = tv & 63, h = lane >> 5, qr = lane & 31;
-        i2 = ic;  // sweep 2
-        ic = i1;  // column slice to reduce
-        i1 = in;  // sweep 1
+        const int lane = tv & 63, h = lane >> 5, kl = lane & 31;
+        const int tr_row = 8 * (lane >> 4) + ((lane & 15) >> 2), tr_b = lane & 3;
+        const int w_row = (lane & 15) < 3 ? (lane & 15) : 3;
         item_next(a, gen);
-        in = item_of(a, gen);  // loaded during this iteration
-        const Chunk ch = ic.valid ? chunk_of(ic.j, ic.n, a.R) : Chunk{};
-        const u32x4 *q1 = S.qs[k & 3];
-        u32x4 *q2 = S.qs[(k + 2) & 3];
-        lds_barrier();  // item k in kt and q1; item k-2's rows in q2
-
-        if (loader) {
-            // item k+1: window rows into slot (k+1) % 4 (free since the sweep 2
-            // of item k-3), keys into registers; the same barrier sequence as
-            // the compute waves, with the keys consumed only at its end
-            const int ltid = tid - kCWaves * kWave;
-            dma_rows(a, in, wv - kCWaves, lane, S.qs[(k + 1) & 3]);
-            issue_keys(a, in, ltid, lk);
-            loader_barrier();  // phase 0 | 1
-            loader_barrier();  // phase 1 | 2
-            loader_barrier();  // phase 2 | 3
-            loader_barrier();  // publication flags
-            follow_flags(S, 0);
-            loader_barrier();  // slice values staged
-            follow_flags(S, 1);
-            loader_barrier();  // constants staged
-            loader_barrier();  // phase 3 | 4
-            loader_barrier();  // phase 4 | 5
-            if (in.valid) {
-                const int c = ltid & 15, g = ltid >> 4;
+        const Item nx = item_of(a, gen);
+        u32x4 kb[8];
+        float n2 = 0.f, inv = 0.f;
+        if (it.valid) {
+            __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's rows and window operand are in
+            // keys into the operand layout (lane l: key l % 32, chunks 2s + l / 32)
 #pragma unroll
-                for (int jj = 0; jj < 16; ++jj) S.kt[sw(g + 16 * jj, c)] = lk[jj];
-            }
-            wait_all_loads();  // the row tile's direct-to-LDS loads too
-            continue;
-        }
-        // ---- phase 0: protocol and loader requests; sweep-1 logits ----
-        issue_chunk(a, ic, ch, C, tid, cl);
-        issue_consts(a, i2, C, tid, al);
-        float n2c = 0.f, invc = 0.f;
-        if (i1.valid) {
-            const int kr = 32 * wv + qr;
-            f32x16 acc = (f32x16){};
-            float n2 = 0.f;
+            for (int st = 0; st < 8; ++st) kb[st] = wkt[sw(kl, 2 * st + h)];
 #pragma unroll
-            for (int s = 0; s < 8; ++s) {
-                const u32x4 kq = S.kt[sw(kr, 2 * s + h)];
-                const u32x4 qq = q1[sw(qr, 2 * s + h)];
-                n2 = dot2sq(kq[0], dot2sq(kq[1], dot2sq(kq[2], dot2sq(kq[3], n2))));
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kq),
-                                                              __builtin_bit_cast(bf16x8, qq), acc, 0, 0, 0);
-            }
+            for (int st = 0; st < 8; ++st)
+                n2 = dot2sq(kb[st][0], dot2sq(kb[st][1], dot2sq(kb[st][2], dot2sq(kb[st][3], n2))));
             n2 += __shfl_xor(n2, 32, kWave);
-            const float inv = __builtin_amdgcn_rsqf(fmaxf(n2, 1e-24f));
-            n2c = n2;
-            invc = inv;
+            inv = __builtin_amdgcn_rsqf(fmaxf(n2, 1e-24f));
             if (h == 0) {
                 const unsigned hi = bf16_rne(inv);
-                S.aw[wv >> 2][1][32 * (wv & 3) + lane] = (uint16_t)hi;
-                S.aw[wv >> 2][2][32 * (wv & 3) + lane] = (uint16_t)bf16_rne(inv - __uint_as_float(hi << 16));
+                S.wts[wv][1][kl] = (uint16_t)hi;
+                S.wts[wv][2][kl] = (uint16_t)bf16_rne(inv - __uint_as_float(hi << 16));
             }
-            // this lane: window row qr against keys 8(r/4) + 4h + r%4 of the wave, r < 16
-            float mloc, sloc = 0.f;
-            if (i1.base + kItem <= i1.P) {
-                float mx = acc[0];
-#pragma unroll
-                for (int r = 1; r < 16; ++r) mx = fmaxf(mx, acc[r]);
-                mloc = mx * sc;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) sloc += fast_exp2(fmaf(acc[r], sc, -mloc));
-            } else {
-                const int kb = i1.base + 32 * wv + 4 * h;
-                const int lim = a.causal ? i1.P + qr % a.w : i1.T - 1;  // last visible key of row qr
-                float x[16];
-                mloc = -INFINITY;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int gk = kb + 8 * (r >> 2) + (r & 3);
-                    x[r] = (gk < i1.T && gk <= lim) ? acc[r] * sc : -INFINITY;
-                    mloc = fmaxf(mloc, x[r]);
-                }
-                if (mloc != -INFINITY)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) sloc += fast_exp2(x[r] - mloc);
-            }
-            S.sm[wv][h][qr] = mloc;
-            S.ss[wv][h][qr] = sloc;
-        }
-        lds_barrier();
-
-        // ---- phase 1: column sums of the two 128-key tiles; softmax fold ----
-        f32x16 cs = (f32x16){};
-        if (i1.valid) {
-            const int ti = wv >> 2, wq = wv & 3;
-            const int tr_key = 8 * h + ((lane & 15) >> 2);
-            const int tr_dim = 32 * wq + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-            const int aw_row = qr < 3 ? qr : 3;
+            // column sums over the wave's 32 keys (zero rows past T add nothing); a
+            // wave's own LDS accesses are ordered.  Transposed reads: lane 16G + 4a + b
+            // reads key row 8G + a (+4), dimensions 16 blk + 4b .. +3; the read returns
+            // dimension 16 blk + lane % 16 of keys 8G + 0..3 (then 4..7)
+            typedef float f32x4v __attribute__((ext_vector_type(4)));
             typedef short s16x4 __attribute__((ext_vector_type(4)));
+            const bf16x8 wa = *reinterpret_cast<const bf16x8 *>(&S.wts[wv][w_row][8 * (lane >> 4)]);
+            const uint16_t *st16 = reinterpret_cast<const uint16_t *>(wkt);
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks) {
-                const bf16x8 wa = *reinterpret_cast<const bf16x8 *>(&S.aw[ti][aw_row][16 * ks + 8 * h]);
-                const int key0 = kTile * ti + 16 * ks + tr_key;
-                const uint16_t *kt16 = reinterpret_cast<const uint16_t *>(S.kt);
-                const uint16_t *p0 = kt16 + key0 * kD + (((tr_dim >> 3) ^ (key0 & 15)) << 3) + (tr_dim & 7);
-                const uint16_t *p1 =
-                    kt16 + (key0 + 4) * kD + (((tr_dim >> 3) ^ ((key0 + 4) & 15)) << 3) + (tr_dim & 7);
+            for (int blk = 0; blk < 8; ++blk) {
+                const int c = 2 * blk + (tr_b >> 1), off = (tr_b & 1) * 4;
+                const uint16_t *p0 = st16 + tr_row * kD + ((c ^ (tr_row & 15)) << 3) + off;
+                const uint16_t *p1 = st16 + (tr_row + 4) * kD + ((c ^ ((tr_row + 4) & 15)) << 3) + off;
                 const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                     (__attribute__((address_space(3))) s16x4 *)(const_cast<uint16_t *>(p0)));
                 const s16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                     (__attribute__((address_space(3))) s16x4 *)(const_cast<uint16_t *>(p1)));
                 const short __attribute__((ext_vector_type(8))) kb8 = {lo[0],  lo[1],  lo[2],  lo[3],
                                                                         hi4[0], hi4[1], hi4[2], hi4[3]};
-                cs = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa, __builtin_bit_cast(bf16x8, kb8), cs, 0, 0, 0);
-            }
-            if (ti == 1 && h == 0) {
-                S.cx[wq][0][lane] = cs[0];
-                S.cx[wq][1][lane] = cs[1] + cs[2];
-            }
-            if (wv == 0 && lane < a.R) {
-                float m = -INFINITY, s = 0.f;
-#pragma unroll
-                for (int w2 = 0; w2 < kCWaves; ++w2)
-#pragma unroll
-                    for (int hh = 0; hh < 2; ++hh) softmax_merge2(m, s, S.sm[w2][hh][lane], S.ss[w2][hh][lane]);
-                S.part[2 * kD + lane] = m;
-                S.part[2 * kD + a.R + lane] = s;
-            }
-        }
-        lds_barrier();
-
-        // ---- phase 2: item partial column sums (tile 0 + tile 1) ----
-        if (i1.valid && wv < 4 && h == 0) {
-            S.part[32 * wv + lane] = cs[0] + S.cx[wv][0][lane];
-            S.part[kD + 32 * wv + lane] = (cs[1] + cs[2]) + S.cx[wv][1][lane];
-        }
-        lds_barrier();
-
-        // ---- phase 3: publication ----
-        {
-            const bool okc = __all(chunk_ok(a, ic, ch, tid, cl));
-            const bool oka = __all(consts_ok(a, i2, C, tid, al));
-            if (lane == 0) {
-                S.flag[0][0][wv] = okc;
-                S.flag[0][1][wv] = oka;
-            }
-            if (i1.valid && tid < C) tag_store(&a.partT[((long long)i1.u * C + tid) * a.nch1 + i1.j], S.part[tid], a.tag);
-        }
-        lds_barrier();
-        // column slice: wait until every partial of item ic's unit is published
-        if (!S.dead) {
-            int par = 0, tries = 0;
-            while (!all_flags(S, par, 0)) {
-                if (++tries > kSpinLimit) {
-                    if (tid == 0) {
-                        __hip_atomic_store(a.status, a.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        S.dead = 1;  // read by every wave only after the next barrier
-                    }
-                    break;
+                const f32x4v cs = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    wa, __builtin_bit_cast(bf16x8, kb8), (f32x4v){0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                if (lane < 16) {
+                    S.wcs[wv][0][16 * blk + lane] = cs[0];
+                    S.wcs[wv][1][16 * blk + lane] = cs[1] + cs[2];
                 }
-                par ^= 1;
-                {
-                    __builtin_amdgcn_s_sleep(2);
-                    issue_chunk(a, ic, ch, C, tid, cl);
-                    const bool okc = __all(chunk_ok(a, ic, ch, tid, cl));
-                    if (lane == 0) S.flag[par][0][wv] = okc;
-                }
-                lds_barrier();
             }
         }
-        if (ic.valid) {
-#pragma unroll
-            for (int q = 0; q < kChunkPerLane; ++q) {
-                const int t = tid + kPThreads * q;
-                if (t < ch.nl) S.cv[t] = tag_val(cl[q]);
-            }
-        }
-        lds_barrier();
-        if (ic.valid) reduce_chunk(a, ic, ch, C, tid, S);
-        // constants of item i2's unit
-        if (!S.dead) {
-            int par = 0, tries = 0;
-            while (!all_flags(S, par, 1)) {
-                if (++tries > kSpinLimit) {
-                    if (tid == 0) {
-                        __hip_atomic_store(a.status, a.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        S.dead = 1;  // read by every wave only after the next barrier
-                    }
-                    break;
-                }
-                par ^= 1;
-                {
-                    __builtin_amdgcn_s_sleep(2);
-                    issue_consts(a, i2, C, tid, al);
-                    const bool oka = __all(consts_ok(a, i2, C, tid, al));
-                    if (lane == 0) S.flag[par][1][wv] = oka;
-                }
-                lds_barrier();
-            }
-        }
-        if (i2.valid && tid < C) S.anc[tid] = tag_val(al);
-        lds_barrier();
-        if (wv == 0 && i2.valid) {
-            if (lane < a.R) {
-                S.rowM[lane] = S.anc[2 * kD + lane];
-                S.rowIS[lane] = 1.f / S.anc[2 * kD + a.R + lane];
-            }
-            // |kbar'|^2 of the centroid as the operand rows represent it
-            float acc2 = 0.f;
-#pragma unroll
-            for (int z = 0; z < 2; ++z) {
-                const float f = S.anc[2 * lane + z];
-                const float fh = __uint_as_float(bf16_rne(f) << 16);
-                const float fl = __uint_as_float(bf16_rne(f - fh) << 16);
-                acc2 = fmaf(fh + fl, fh + fl, acc2);
-            }
-            acc2 = wave_sum(acc2);
-            if (lane == 0) S.kb2 = acc2;
-            // rows 28..31 of the sweep-2 operand: mu high, mu remainder, kbar high, kbar remainder
-            const int which = lane >> 4, c = lane & 15;
-            const float *src = (which < 2) ? S.anc + kD : S.anc;
-            u32x4 q;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                unsigned half2[2];
-#pragma unroll
-                for (int z = 0; z < 2; ++z) {
-                    const float f = src[8 * c + 2 * e + z];
-                    const unsigned hb = bf16_rne(f);
-                    half2[z] = (which & 1) ? bf16_rne(f - __uint_as_float(hb << 16)) : hb;
-                }
-                q[e] = half2[0] | (half2[1] << 16);
-            }
-            q2[sw(kFusedMaxRows + which, c)] = q;
-        }
-        lds_barrier();
-
-        // ---- phase 4: sweep 2 of item k-2 from registers; shift the key slots ----
-        if (i2.valid) {
+        // every read of this wave's rows has completed: its rows of the next slice may land
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+        __builtin_amdgcn_sched_barrier(0);
+        dma_keys(a, nx, wv, lane, wkt);
+        __builtin_amdgcn_sched_barrier(0);
+        if (it.valid) {
+            // window logits: keys as A, window rows as B; lane holds row kl against
+            // keys 8(r/4) + 4h + r%4 of the wave
             f32x16 acc = (f32x16){};
 #pragma unroll
-            for (int s = 0; s < 8; ++s) {
-                const u32x4 qa = q2[sw(qr, 2 * s + h)];
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, qa),
-                                                              __builtin_bit_cast(bf16x8, lk[s]), acc, 0, 0, 0);
+            for (int st = 0; st < 8; ++st)
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kb[st]),
+                                                              __builtin_bit_cast(bf16x8, aq[st]), acc, 0, 0, 0);
+            float mx = -INFINITY;
+            if (it.base + 32 * (wv + 1) <= it.P) {
+                // every key of the wave precedes the window: visible to every row
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    acc[r] *= sc;
+                    mx = fmaxf(mx, acc[r]);
+                }
+            } else {
+                const int kb0 = it.base + 32 * wv + 4 * h;
+                const int lim = a.causal ? it.P + kl % a.w : it.T - 1;  // last key visible to row kl
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int gk = kb0 + 8 * (r >> 2) + (r & 3);
+                    acc[r] = (gk < it.T && gk <= lim) ? acc[r] * sc : -INFINITY;
+                    mx = fmaxf(mx, acc[r]);
+                }
             }
+            float s = 0.f;
+            if (mx != -INFINITY)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) s += fast_exp2(acc[r] - mx);
+            const float m2 = __shfl_xor(mx, 32, kWave), s2 = __shfl_xor(s, 32, kWave);
+            softmax_merge2(mx, s, m2, s2);
+            if (h == 0) {
+                S.wm[wv][kl] = mx;
+                S.wsm[wv][kl] = s;
+            }
+        }
+        lds_barrier();  // B1
+        lds_barrier();  // B2: the unit's constants are in
+        if (it.valid) {
+            // rows kAnc .. kAnc+3 of the operand: mu high, mu remainder, kbar high, kbar remainder
+            if (kl >= kAnc) {
+#pragma unroll
+                for (int st = 0; st < 8; ++st) aq[st] = S.arow[kl - kAnc][2 * st + h];
+            }
+            // sweep 2: window rows and anchors as A, keys as B; lane holds key kl
+            // against rows 8(r/4) + 4h + r%4
+            f32x16 acc = (f32x16){};
+#pragma unroll
+            for (int st = 0; st < 8; ++st)
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, aq[st]),
+                                                              __builtin_bit_cast(bf16x8, kb[st]), acc, 0, 0, 0);
             float att = 0.f;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int m = 8 * (r >> 2) + 4 * h + (r & 3);
-                if (m < a.R) att = fmaf(fast_exp2(fmaf(acc[r], sc, -S.rowM[m])), S.rowIS[m], att);
+            for (int g4 = 0; g4 < 4; ++g4) {
+                typedef float f32x4v __attribute__((ext_vector_type(4)));
+                const f32x4v sh = *reinterpret_cast<const f32x4v *>(&S.rsh[8 * g4 + 4 * h]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) att += fast_exp2(fmaf(acc[4 * g4 + e], sc, -sh[e]));
             }
             float kmu = h ? acc[12] + acc[13] : 0.f;
             float kk = h ? acc[14] + acc[15] : 0.f;
             att += __shfl_xor(att, 32, kWave);
             kmu += __shfl_xor(kmu, 32, kWave);
             kk += __shfl_xor(kk, 32, kWave);
-            const float dE = __builtin_amdgcn_sqrtf(fmaxf(sn2[0] - 2.f * kk + S.kb2, 0.f));
-            const float cm = kmu * sinv[0];
-            const int gi = i2.base + 32 * wv + qr;
+            const float dE = __builtin_amdgcn_sqrtf(fmaxf(n2 - 2.f * kk + S.kb2, 0.f));
+            const float cm = kmu * inv;
+            const int gi = it.base + 32 * wv + kl;
             float dsum = 0.f, dmn = INFINITY, dmx = -INFINITY;
             if (h == 0) {
-                if (gi < i2.T) dsum = dE;
-                if (gi < i2.P) {
+                if (gi < it.T) dsum = dE;
+                if (gi < it.P) {
                     dmn = dE;
                     dmx = dE;
-                    const Unit un = unit_of(i2.u, a.Hkv, a.B);
+                    const Unit un = unit_of(it.u, a.Hkv, a.B);
                     const int64_t ob = unit_out_base(a, un);
                     a.bufA[ob + gi] = dE;
                     a.bufB[ob + gi] = cm;
@@ -681,36 +607,10 @@ __global__ __launch_bounds__(kFThreads, 1) void k_fused(ScoreArgs a)
                 S.dred[wv][2] = dmx;
             }
         }
-        {
-            // item k-1 becomes the next sweep-2 item; item k (still in kt) follows it
-            const int kr = 32 * wv + qr;
-#pragma unroll
-            for (int s = 0; s < 8; ++s) {
-                lk[s] = lk[8 + s];
-                lk[8 + s] = S.kt[sw(kr, 2 * s + h)];
-            }
-            sn2[0] = sn2[1];
-            sinv[0] = sinv[1];
-            sn2[1] = n2c;
-            sinv[1] = invc;
-        }
-        lds_barrier();
-
-        // ---- phase 5: d_E extrema of item k-2 ----
-        if (wv == 0 && i2.valid && lane == 0) {
-            float s = 0.f, mn = INFINITY, mx = -INFINITY;
-            for (int w2 = 0; w2 < kCWaves; ++w2) {
-                s += S.dred[w2][0];
-                mn = fminf(mn, S.dred[w2][1]);
-                mx = fmaxf(mx, S.dred[w2][2]);
-            }
-            float *pp = a.part2 + ((int64_t)i2.u * a.nch2 + i2.j) * 4;
-            pp[0] = s;
-            pp[1] = mn;
-            pp[2] = mx;
-            pp[3] = 0.f;
-        }
+        load_window(a, nx, lane, aq);  // the next slice's window operand
+        it = nx;
     }
+    lds_barrier();
 }
 
 }  // namespace fast
@@ -741,7 +641,7 @@ bool dev_info(DevInfo *o)
 
 int chunk_loads_max(int n, int R)
 {
-    // largest load list of any column slice of a unit with n items
+    // largest load list of any column part of a unit with n slices
     const int Cc = 2 * fast::kD + R, D2 = 2 * fast::kD;
     int mx = 0;
     for (int j = 0; j < n; ++j) {
@@ -758,15 +658,19 @@ std::atomic<unsigned> g_tag{0};
 
 }  // namespace
 
-bool fused_eligible(int D, bool bf16, int R, const SeqTab &seq, int L, int Hkv, int *grid)
+bool fused_eligible(int D, bool bf16, int R, const SeqTab &seq, int L, int Hkv, int Hq, int w, int *grid)
 {
     if (!bf16 || D != fast::kD || R > kFusedMaxRows || R < 1) return false;
+    // window rows are addressed through one 32-bit buffer range
+    if ((long long)L * Hq * seq.nseq * w * D * 2 >= (1LL << 31)) return false;
     DevInfo di;
     if (!dev_info(&di)) return false;
     long long ns = 0;
     int nmax = 0;
     for (int s = 0; s < seq.nseq; ++s) {
-        const int n = (seq.cu[s + 1] - seq.cu[s] + kFusedItem - 1) / kFusedItem;
+        const int T = seq.cu[s + 1] - seq.cu[s];
+        if ((long long)(T + kFusedItem) * D * 2 >= (1LL << 31)) return false;  // 32-bit key offsets
+        const int n = (T + kFusedItem - 1) / kFusedItem;
         ns += n;
         if (n > nmax) nmax = n;
         if (chunk_loads_max(n, R) > fast::kChunkMax) return false;
@@ -774,7 +678,7 @@ bool fused_eligible(int D, bool bf16, int R, const SeqTab &seq, int L, int Hkv, 
     const long long items = (long long)L * Hkv * ns;
     if (items < 1 || items > (1LL << 30)) return false;
     const long long g = items < (long long)di.ncu * di.per_cu ? items : (long long)di.ncu * di.per_cu;
-    // every unit must span at most G items (two consecutive steps)
+    // every unit must span at most G slices (two consecutive steps)
     if (nmax > g) return false;
     *grid = (int)g;
     return true;

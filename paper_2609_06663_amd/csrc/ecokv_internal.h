@@ -108,9 +108,9 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
 // Single-read score path (bf16, head_dim 128, G*w <= 28): eligibility for a
 // shape on the current device, and its launch.  The launcher fills the
 // fused-path fields of ScoreArgs.
-bool fused_eligible(int D, bool bf16, int R, const SeqTab &seq, int L, int Hkv, int *grid);
+bool fused_eligible(int D, bool bf16, int R, const SeqTab &seq, int L, int Hkv, int Hq, int w, int *grid);
 hipError_t fused_launch(ScoreArgs &a, int grid, hipStream_t st);
-constexpr int kFusedItem = 256;        // keys per work item of the single-read path
+constexpr int kFusedItem = 224;        // keys per work item (slice) of the single-read path
 constexpr int kFusedMaxRows = 28;      // window rows; 4 more rows carry kbar and mu
 hipError_t select_launch(const SelectArgs &a, hipStream_t st);
 int select_max_flat_heads();

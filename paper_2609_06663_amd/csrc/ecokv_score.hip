@@ -697,7 +697,7 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
 // normaliser folded into the shift.
 constexpr int kS2Waves = 4;
 #ifndef ECOKV_S2_KEYS
-#define ECOKV_S2_KEYS 4096
+#define ECOKV_S2_KEYS 2048
 #endif
 constexpr int kS2Keys = ECOKV_S2_KEYS;            // keys per block
 constexpr int kS2Groups = kS2Keys / (32 * kS2Waves);  // 32-key groups per wave
@@ -1074,7 +1074,13 @@ __global__ __launch_bounds__(256, 2) void k_fs1s(ScoreArgs a)
 // ---------------------------------------------------------------------------
 // Per-unit reduction of the sweep-1 partials.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void k_reduce1(ScoreArgs a)
+// Four lanes per column, each over every fourth block partial, so that a
+// unit's partials are all requested at once; the four sums and the four
+// (max, normaliser) pairs are combined by commutative steps, so every lane
+// ends with the same value.
+constexpr int kReduceThreads = 1024;
+
+__global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
 {
     const int u = blockIdx.x;
     const Unit un = unit_of(u, a.Hkv, a.B);
@@ -1083,18 +1089,31 @@ __global__ __launch_bounds__(kThreads) void k_reduce1(ScoreArgs a)
     const int stride = 2 * a.D + 2 * a.R;
     const float *p = a.part1 + (int64_t)u * a.nch1 * stride;
     float *anc = a.anchors + (int64_t)u * stride;
-    for (int d = threadIdx.x; d < 2 * a.D; d += blockDim.x) {
-        float s = 0.f;
-#pragma unroll 8
-        for (int b = 0; b < nb; ++b) s += p[(int64_t)b * stride + d];
-        anc[d] = s / (float)T;
-    }
-    for (int r = threadIdx.x; r < a.R; r += blockDim.x) {
-        float m = -INFINITY, s = 0.f;
-        for (int b = 0; b < nb; ++b)
-            softmax_merge2(m, s, p[(int64_t)b * stride + 2 * a.D + r], p[(int64_t)b * stride + 2 * a.D + a.R + r]);
-        anc[2 * a.D + r] = m;
-        anc[2 * a.D + a.R + r] = s;
+    const int q = threadIdx.x & 3;
+    for (int c = threadIdx.x >> 2; c < 2 * a.D + a.R; c += kReduceThreads / 4) {
+        if (c < 2 * a.D) {
+            float s = 0.f;
+#pragma unroll 4
+            for (int b = q; b < nb; b += 4) s += p[(int64_t)b * stride + c];
+            s += __shfl_xor(s, 1, 4);
+            s += __shfl_xor(s, 2, 4);
+            if (q == 0) anc[c] = s / (float)T;
+        } else {
+            const int r = c - 2 * a.D;
+            float m = -INFINITY, s = 0.f;
+#pragma unroll 4
+            for (int b = q; b < nb; b += 4)
+                softmax_merge2(m, s, p[(int64_t)b * stride + 2 * a.D + r], p[(int64_t)b * stride + 2 * a.D + a.R + r]);
+#pragma unroll
+            for (int x = 1; x <= 2; x <<= 1) {
+                const float m2 = __shfl_xor(m, x, 4), s2 = __shfl_xor(s, x, 4);
+                softmax_merge2(m, s, m2, s2);
+            }
+            if (q == 0) {
+                anc[2 * a.D + r] = m;
+                anc[2 * a.D + a.R + r] = s;
+            }
+        }
     }
 }
 
@@ -1431,7 +1450,7 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     const char *path = getenv("ECOKV_SCORE_PATH");
     const bool want_single = path && strcmp(path, "single") == 0;
     int fgrid = 0;
-    if (want_single && fused_eligible(a.D, bf16, a.R, a.seq, a.L, a.Hkv, &fgrid)) {
+    if (want_single && fused_eligible(a.D, bf16, a.R, a.seq, a.L, a.Hkv, a.Hq, a.w, &fgrid)) {
         a.partT = reinterpret_cast<unsigned long long *>(ws + lay.partT);
         a.ancT = reinterpret_cast<unsigned long long *>(ws + lay.ancT);
         a.status = reinterpret_cast<unsigned *>(ws + lay.status);
@@ -1456,7 +1475,7 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
             ECOKV_TIMED("sweep1_block", st, launch_sweep(1, a, grid, st, bf16));
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        ECOKV_TIMED("reduce1", st, hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kThreads), 0, st, a));
+        ECOKV_TIMED("reduce1", st, hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kReduceThreads), 0, st, a));
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (score_fast_path(a.D, bf16) && a.R <= kFusedMaxRows) {
             // streaming sweep 2: window rows and the four anchor rows in one operand

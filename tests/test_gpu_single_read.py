@@ -1,8 +1,8 @@
 """GPU parity of the single-read score path (ECOKV_SCORE_PATH=single).
 
 The single-read kernel keeps every key on chip between the two sweeps and
-publishes per-item partials and per-unit constants between blocks (bf16,
-head_dim 128, G*w <= 28).  The cases below run it against the CPU oracle with
+publishes per-slice partials (224-key slices) and per-unit constants between
+blocks (bf16, head_dim 128, G*w <= 28).  The cases below run it against the CPU oracle with
 the tolerances of parity_utils, plus: it is bit-reproducible, and it agrees
 with the two-sweep path to the score tolerance.
 """
@@ -48,7 +48,7 @@ def test_stack28_full_size_sampled():
 
 def test_mha64k_full_size_sampled():
     wl = W.mha64k()
-    say("mha64k: 32 MHA heads, T=65536, w=8 (single-read path, 256 items per unit)")
+    say("mha64k: 32 MHA heads, T=65536, w=8 (single-read path, 293 slices per unit)")
     g = gpu_pass(wl)
     check_all_selections_valid(wl, g)
     check_per_head(wl, g, units=[(0, 0, 0), (0, 31, 0)])
@@ -62,9 +62,9 @@ def test_varlen_layer_flat():
     check_compact(wl, g)
 
 
-@pytest.mark.parametrize("seqlens", [[5003], [300, 2100, 257, 4096], [40, 256, 511, 513]])
+@pytest.mark.parametrize("seqlens", [[5003], [300, 2100, 257, 4096], [40, 224, 223, 225, 449]])
 def test_ragged_lengths(seqlens):
-    # item boundaries: shorter than one item, exactly one, one key over, many
+    # slice boundaries: shorter than one slice, exactly one, one key short, one over, many
     wl = W.custom(21, L=2, Hq=8, Hkv=2, D=128, w=4, seqlens=seqlens, dtype="bf16", group=64)
     say(f"ragged sequences {seqlens} (single-read path)")
     g = gpu_pass(wl)
