@@ -1172,14 +1172,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t float_rsrc(const float *p, int
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p), (short)0, n * 4, 0x00020000);
 }
 
-// d_E, khat.mu and pooled window attention of keys i0 .. i0+15 (zero past P).
-__device__ __forceinline__ void epi_keys(const ScoreArgs &a, const float *dbuf, const float *cbuf, const float *abuf,
-                                         int P, int i0, float (&d)[kEpiPer], float (&c)[kEpiPer],
-                                         float (&imp)[kEpiPer])
+// d_E and khat.mu of keys i0 .. i0+PER-1 (zero past P).
+template <int PER>
+__device__ __forceinline__ void load_dc(const float *dbuf, const float *cbuf, int P, int i0, float (&d)[PER],
+                                        float (&c)[PER])
 {
-    const __amdgpu_buffer_rsrc_t rd = float_rsrc(dbuf, P), rc = float_rsrc(cbuf, P), ra = float_rsrc(abuf, P);
+    const __amdgpu_buffer_rsrc_t rd = float_rsrc(dbuf, P), rc = float_rsrc(cbuf, P);
 #pragma unroll
-    for (int q = 0; q < kEpiPer / 4; ++q) {
+    for (int q = 0; q < PER / 4; ++q) {
         const f32x4 x = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rd, (i0 + 4 * q) * 4, 0, 0));
         const f32x4 y = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rc, (i0 + 4 * q) * 4, 0, 0));
 #pragma unroll
@@ -1188,20 +1188,27 @@ __device__ __forceinline__ void epi_keys(const ScoreArgs &a, const float *dbuf, 
             c[4 * q + e] = y[e];
         }
     }
+}
+
+// Pooled window attention S_imp of keys i0 .. i0+PER-1 (zero past P).
+template <int PER>
+__device__ __forceinline__ void load_imp(const ScoreArgs &a, const float *abuf, int P, int i0, float (&imp)[PER])
+{
+    const __amdgpu_buffer_rsrc_t ra = float_rsrc(abuf, P);
     const int half = a.pool_half;
     const float inv_k = 1.f / (float)(2 * half + 1);
     if (half <= kPoolHalfMax) {
         // av[j] = a[i0 - 4 + j]; a negative offset wraps past the range and reads zero
-        float av[kEpiPer + 2 * kPoolHalfMax];
+        float av[PER + 2 * kPoolHalfMax];
 #pragma unroll
-        for (int q = 0; q < (kEpiPer + 2 * kPoolHalfMax) / 4; ++q) {
+        for (int q = 0; q < (PER + 2 * kPoolHalfMax) / 4; ++q) {
             const f32x4 x = __builtin_bit_cast(
                 f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, (unsigned)(i0 - kPoolHalfMax + 4 * q) * 4u, 0, 0));
 #pragma unroll
             for (int e = 0; e < 4; ++e) av[4 * q + e] = x[e];
         }
 #pragma unroll
-        for (int j = 0; j < kEpiPer; ++j) {
+        for (int j = 0; j < PER; ++j) {
             float acc = 0.f;
 #pragma unroll
             for (int t = -kPoolHalfMax; t <= kPoolHalfMax; ++t)
@@ -1210,8 +1217,64 @@ __device__ __forceinline__ void epi_keys(const ScoreArgs &a, const float *dbuf, 
         }
     } else {
 #pragma unroll
-        for (int j = 0; j < kEpiPer; ++j) imp[j] = i0 + j < P ? pooled(abuf, i0 + j, P, half) : 0.f;
+        for (int j = 0; j < PER; ++j) imp[j] = i0 + j < P ? pooled(abuf, i0 + j, P, half) : 0.f;
     }
+}
+
+// d_E, khat.mu and pooled window attention of keys i0 .. i0+15 (zero past P).
+__device__ __forceinline__ void epi_keys(const ScoreArgs &a, const float *dbuf, const float *cbuf, const float *abuf,
+                                         int P, int i0, float (&d)[kEpiPer], float (&c)[kEpiPer],
+                                         float (&imp)[kEpiPer])
+{
+    load_dc<kEpiPer>(dbuf, cbuf, P, i0, d, c);
+    load_imp<kEpiPer>(a, abuf, P, i0, imp);
+}
+
+// The per-unit constants of Eq. (2)-(7) from the unit's reductions: d_E
+// (sum over T, min / max over P), S_div (sum, min, max over P) and S_imp
+// (sum over P), and |mu|^2.
+struct EpiConsts {
+    float lam, rE, rC, DE, dmin, dden, smin, sden, impmean, sbarmean, scale;
+};
+
+__device__ __forceinline__ EpiConsts epi_consts(const ScoreArgs &a, const Red4 &dst, const Red4 &sd, float mu2, int T,
+                                                int P)
+{
+    EpiConsts k;
+    k.DE = dst.s0 / (float)T;
+    k.dmin = dst.mn;
+    k.dden = dst.mx - dst.mn + a.eps;
+    k.rE = 2.f - 2.f / (1.f + expf(-k.DE / a.tau));
+    k.rC = ((float)T * mu2 - 1.f) / ((float)T - 1.f);
+    k.lam = a.use_override ? a.lambda_override : a.beta * k.rE + (1.f - a.beta) * k.rC;
+    if (a.status && *a.status == a.tag) k.lam = NAN;  // a publication wait of this launch timed out
+    k.smin = sd.mn;
+    k.sden = sd.mx - sd.mn + a.eps;
+    k.impmean = sd.s1 / (float)P;
+    k.sbarmean = (sd.s0 / (float)P - k.smin) / k.sden;
+    k.scale = k.impmean / (k.sbarmean + a.eps);
+    return k;
+}
+
+__device__ __forceinline__ void epi_write_stats(const ScoreArgs &a, int u, const EpiConsts &k, const Red4 &dst,
+                                                const Red4 &sd, float mu2)
+{
+    float st[ECOKV_NSTATS];
+    st[ECOKV_STAT_LAMBDA] = k.lam;
+    st[ECOKV_STAT_RC] = k.rC;
+    st[ECOKV_STAT_RE] = k.rE;
+    st[ECOKV_STAT_DE] = k.DE;
+    st[ECOKV_STAT_DMIN] = dst.mn;
+    st[ECOKV_STAT_DMAX] = dst.mx;
+    st[ECOKV_STAT_SDIV_MIN] = sd.mn;
+    st[ECOKV_STAT_SDIV_MAX] = sd.mx;
+    st[ECOKV_STAT_IMP_MEAN] = k.impmean;
+    st[ECOKV_STAT_SBAR_MEAN] = k.sbarmean;
+    st[ECOKV_STAT_MU_NORM2] = mu2;
+    st[ECOKV_STAT_SCALE] = k.scale;
+    if (a.stats)
+        for (int q = 0; q < ECOKV_NSTATS; ++q) a.stats[(int64_t)u * ECOKV_NSTATS + q] = st[q];
+    if (a.lambda) a.lambda[u] = k.lam;
 }
 
 // Sum, min and max of d_E over the unit, from the sweep-2 partials.
@@ -1299,17 +1362,8 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
     Red4 m2{0.f, 0.f, 0.f, 0.f};
     for (int d = threadIdx.x; d < a.D; d += blockDim.x) m2.s0 += mu[d] * mu[d];
     const float mu2 = block_red4(m2, lds).s0;
-
-    const float DE = dst.s0 / (float)T;
-    const float dmin = dst.mn, dden = dst.mx - dst.mn + a.eps;
-    const float rE = 2.f - 2.f / (1.f + expf(-DE / a.tau));
-    const float rC = ((float)T * mu2 - 1.f) / ((float)T - 1.f);
-    float lam = a.use_override ? a.lambda_override : a.beta * rE + (1.f - a.beta) * rC;
-    if (a.status && *a.status == a.tag) lam = NAN;  // a publication wait of this launch timed out
-    const float smin = sd.mn, sden = sd.mx - sd.mn + a.eps;
-    const float impmean = sd.s1 / (float)P;
-    const float sbarmean = (sd.s0 / (float)P - smin) / sden;
-    const float scale = impmean / (sbarmean + a.eps);
+    const EpiConsts k = epi_consts(a, dst, sd, mu2, T, P);
+    const float lam = k.lam, dmin = k.dmin, dden = k.dden, smin = k.smin, sden = k.sden, scale = k.scale;
 
     float *out = a.scores + ob;
     {
@@ -1336,24 +1390,190 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
                 if (k0 + j < i1) out[k0 + j] = sv[j];
         }
     }
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        float st[ECOKV_NSTATS];
-        st[ECOKV_STAT_LAMBDA] = lam;
-        st[ECOKV_STAT_RC] = rC;
-        st[ECOKV_STAT_RE] = rE;
-        st[ECOKV_STAT_DE] = DE;
-        st[ECOKV_STAT_DMIN] = dst.mn;
-        st[ECOKV_STAT_DMAX] = dst.mx;
-        st[ECOKV_STAT_SDIV_MIN] = sd.mn;
-        st[ECOKV_STAT_SDIV_MAX] = sd.mx;
-        st[ECOKV_STAT_IMP_MEAN] = impmean;
-        st[ECOKV_STAT_SBAR_MEAN] = sbarmean;
-        st[ECOKV_STAT_MU_NORM2] = mu2;
-        st[ECOKV_STAT_SCALE] = scale;
-        if (a.stats)
-            for (int k = 0; k < ECOKV_NSTATS; ++k) a.stats[(int64_t)u * ECOKV_NSTATS + k] = st[k];
-        if (a.lambda) a.lambda[u] = lam;
+    if (blockIdx.x == 0 && threadIdx.x == 0) epi_write_stats(a, u, k, dst, sd, mu2);
+}
+
+// Epilogue in one launch when a unit's P non-window keys fit one block: every
+// per-unit reduction is block-local, so each key's d_E, khat.mu and attention
+// is read once.  Wave w holds keys 2048 w .. 2048 w + 2047 as 8 chunks of 256;
+// lane l of chunk j holds keys 2048 w + 256 j + 4 l .. +3, so each load
+// instruction covers 1 KiB of consecutive keys.  The pooling window (up to 4
+// keys on each side) comes from the neighbouring lanes' registers (or the
+// neighbouring chunk's end lane); the wave's outermost neighbours come from
+// the neighbouring waves through LDS.
+constexpr int kUThreads = 1024;
+constexpr int kUVec = 8;                      // chunks (float4 per thread and array)
+constexpr int kUWaveKeys = 256 * kUVec;       // keys per wave
+constexpr int kUKeys = kUThreads / kWave * kUWaveKeys;  // 32768
+
+// Block sum / min / max whose barriers order LDS only, so that global loads
+// issued before it stay in flight.
+__device__ Red4 block_red4_lds(Red4 v, Red4 *lds)
+{
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    v.s0 = wave_sum(v.s0);
+    v.s1 = wave_sum(v.s1);
+    v.mn = wave_min(v.mn);
+    v.mx = wave_max(v.mx);
+    if (lane == 0) lds[wv] = v;
+    lds_barrier();
+    Red4 r = lds[0];
+    for (int k = 1; k < nw; ++k) {
+        r.s0 += lds[k].s0;
+        r.s1 += lds[k].s1;
+        r.mn = fminf(r.mn, lds[k].mn);
+        r.mx = fmaxf(r.mx, lds[k].mx);
     }
+    lds_barrier();
+    return r;
+}
+
+// Whole-wave shifts by one lane (DPP wave_shr:1 / wave_shl:1): lane l gets
+// lane l - 1's (resp. l + 1's) value; the lane shifted in gets zero.
+__device__ __forceinline__ f32x4 from_prev_lane(f32x4 x)
+{
+    f32x4 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x[e]), 0x138, 0xF, 0xF, false));
+    return r;
+}
+__device__ __forceinline__ f32x4 from_next_lane(f32x4 x)
+{
+    f32x4 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x[e]), 0x130, 0xF, 0xF, false));
+    return r;
+}
+__device__ __forceinline__ f32x4 lane_value(f32x4 x, int l)
+{
+    f32x4 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x[e]), l));
+    return r;
+}
+
+__global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
+{
+    constexpr int kUW = kUThreads / kWave;
+    __shared__ Red4 lds[kUW];
+    __shared__ f32x4 svl[kUVec][kUThreads];  // S_div of every thread's keys (128 KiB)
+    __shared__ f32x4 edge[kUW][2];           // per wave: its first and last four attention values
+    const int u = blockIdx.x;
+    const Unit un = unit_of(u, a.Hkv, a.B);
+    const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
+    const int P = T - a.w;
+    const int64_t ob = unit_out_base(a, un);
+    const int stride = 2 * a.D + 2 * a.R;
+    const float *mu = a.anchors + (int64_t)u * stride + a.D;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int half = a.pool_half;  // <= kPoolHalfMax (checked on the host)
+    const int kw = kUWaveKeys * wv;
+
+    // every global load first, so that their latencies overlap: the sweep-2
+    // partials and mu (d_E sum / extrema and |mu|^2 in one block reduction),
+    // then d_E, khat.mu and attention of the thread's keys (zero past P)
+    Red4 v{0.f, 0.f, INFINITY, -INFINITY};
+    const int nb2 = (T + a.rpb2 - 1) / a.rpb2;
+    for (int b = threadIdx.x; b < nb2; b += blockDim.x) {
+        const float *pp = a.part2 + ((int64_t)u * a.nch2 + b) * 4;
+        v.s0 += pp[0];
+        v.mn = fminf(v.mn, pp[1]);
+        v.mx = fmaxf(v.mx, pp[2]);
+    }
+    for (int d = threadIdx.x; d < a.D; d += blockDim.x) v.s1 += mu[d] * mu[d];
+    const __amdgpu_buffer_rsrc_t rd = float_rsrc(a.bufA + ob, P), rc = float_rsrc(a.bufB + ob, P),
+                                 ra = float_rsrc(a.bufC + ob, P);
+    f32x4 xd[kUVec], xc[kUVec], xa[kUVec];
+#pragma unroll
+    for (int j = 0; j < kUVec; ++j) {
+        const int k4 = kw + 256 * j + 4 * lane;
+        xd[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rd, k4 * 4, 0, 0));
+        xc[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rc, k4 * 4, 0, 0));
+        xa[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, k4 * 4, 0, 0));
+    }
+    __builtin_amdgcn_sched_barrier(0);  // the phases below stay in order (register pressure)
+
+    const Red4 dm = block_red4_lds(v, lds);
+    const Red4 dst{dm.s0, 0.f, dm.mn, dm.mx};
+    const float mu2 = dm.s1;
+
+    // S_div, kept in LDS (each thread reads back only its own values)
+    const float dmin = dst.mn, inv_dden = 1.f / (dst.mx - dst.mn + a.eps);
+    Red4 w{0.f, 0.f, INFINITY, -INFINITY};
+#pragma unroll
+    for (int j = 0; j < kUVec; ++j) {
+        const int k4 = kw + 256 * j + 4 * lane;
+        f32x4 sv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float sE = (xd[j][e] - dmin) * inv_dden;
+            const float sC = (1.f - xc[j][e]) * 0.5f;
+            sv[e] = a.alpha * sE + (1.f - a.alpha) * sC;
+            if (k4 + e < P) {
+                w.s0 += sv[e];
+                w.mn = fminf(w.mn, sv[e]);
+                w.mx = fmaxf(w.mx, sv[e]);
+            }
+        }
+        svl[j][threadIdx.x] = sv;
+    }
+    // the wave's first and last four attention values for its neighbours
+    if (lane == 0) edge[wv][0] = xa[0];
+    if (lane == 63) edge[wv][1] = xa[kUVec - 1];
+    lds_barrier();
+    const f32x4 z4 = {0.f, 0.f, 0.f, 0.f};
+    const f32x4 hl = wv > 0 ? edge[wv - 1][1] : z4;            // the four keys before the wave's first
+    const f32x4 hr = wv < kUW - 1 ? edge[wv + 1][0] : z4;       // the four after its last
+    __builtin_amdgcn_sched_barrier(0);
+    // pooled S_imp (each chunk's attention registers die as its pooled values are made)
+    const float inv_k = 1.f / (float)(2 * half + 1);
+    f32x4 im[kUVec];
+#pragma unroll
+    for (int j = 0; j < kUVec; ++j) {
+        const f32x4 sl = from_prev_lane(xa[j]), sr = from_next_lane(xa[j]);
+        const f32x4 pl = j > 0 ? lane_value(xa[j - 1], 63) : hl;  // lane 0: previous chunk's end
+        const f32x4 nr = j < kUVec - 1 ? lane_value(xa[j + 1], 0) : hr;  // lane 63: next chunk's start
+        const f32x4 left = lane == 0 ? pl : sl;
+        const f32x4 right = lane == 63 ? nr : sr;
+        float win[12];  // keys k4 - 4 .. k4 + 7
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            win[e] = left[e];
+            win[4 + e] = xa[j][e];
+            win[8 + e] = right[e];
+        }
+        const int k4 = kw + 256 * j + 4 * lane;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            float acc = 0.f;
+#pragma unroll
+            for (int t = -kPoolHalfMax; t <= kPoolHalfMax; ++t)
+                if (t >= -half && t <= half) acc += win[4 + e + t];
+            im[j][e] = acc * inv_k;
+            if (k4 + e < P) w.s1 += im[j][e];
+        }
+    }
+    const Red4 sd = block_red4_lds(w, lds);
+    const EpiConsts k = epi_consts(a, dst, sd, mu2, T, P);
+
+    const __amdgpu_buffer_rsrc_t ro = float_rsrc(a.scores + ob, P);
+    const float gain = k.lam * k.scale / k.sden, one_m = 1.f - k.lam;
+#pragma unroll
+    for (int j = 0; j < kUVec; ++j) {
+        const f32x4 sv = svl[j][threadIdx.x];
+        f32x4 x;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = (sv[e] - k.smin) * gain + one_m * im[j][e];
+        const int k4 = kw + 256 * j + 4 * lane;
+        if (k4 + 4 <= P) {
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, x), ro, k4 * 4, 0, 0);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (k4 + e < P) a.scores[ob + k4 + e] = x[e];
+        }
+    }
+    if (threadIdx.x == 0) epi_write_stats(a, u, k, dst, sd, mu2);
 }
 
 // ---------------------------------------------------------------------------
@@ -1489,6 +1709,10 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
             ECOKV_TIMED("sweep2_block", st, launch_sweep(2, a, grid, st, bf16));
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (maxT - a.w <= kUKeys && a.pool_half <= kPoolHalfMax) {
+        ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL(k_epi_unit, dim3(U), dim3(kUThreads), 0, st, a));
+        return hipGetLastError();
     }
     ECOKV_TIMED("epilogue1", st, hipLaunchKernelGGL(k_epi1, grid_e, dim3(kEpiThreads), 0, st, a));
     if ((e = hipGetLastError()) != hipSuccess) return e;
