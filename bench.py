@@ -51,10 +51,11 @@ def log(msg):
 # Stage names the library times (ECOKV_STAGE_TIMING=1) and the kernels behind them.
 STAGE_KERNELS = {
     "sweep1_stream": ["k_fs1s"], "sweep1_block": ["k_fs1", "k_pass1"], "reduce1": ["k_reduce1"],
-    "sweep2_stream": ["k_fs2s"], "sweep2_block": ["k_fs2", "k_pass2"], "epilogue1": ["k_epi1"],
-    "epilogue2": ["k_epi2"], "single_read": ["k_fused"], "select": ["k_select_reg", "k_select"],
-    "compact": ["k_compact"],
+    "sweep2_stream": ["k_fs2s"], "sweep2_block": ["k_fs2", "k_pass2"], "epilogue": ["k_epi_unit"],
+    "epilogue1": ["k_epi1"], "epilogue2": ["k_epi2"], "single_read": ["k_fused"],
+    "select": ["k_select_reg", "k_select"], "compact": ["k_compact"],
 }
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, vendor figure
 COPY_BYTES = 1 << 30  # size of the calibration copy in --counter-run
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_stack28.txt")
 
@@ -71,15 +72,15 @@ def stage_of_kernel(kname):
 
 
 def source_digest():
-    """sha256 over the library sources; stored traffic figures are valid only for this digest."""
+    """sha256 over the kernel sources (csrc); stored traffic figures are valid only for this digest."""
     import hashlib
     h = hashlib.sha256()
-    for d in (os.path.join(ROOT, "paper_2609_06663_amd", "csrc"), os.path.join(ROOT, "include")):
-        for f in sorted(os.listdir(d)):
-            if f.endswith((".hip", ".h")):
-                h.update(f.encode())
-                with open(os.path.join(d, f), "rb") as fh:
-                    h.update(fh.read())
+    d = os.path.join(ROOT, "paper_2609_06663_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
     return h.hexdigest()[:16]
 
 
@@ -201,9 +202,12 @@ def main():
     stage_algo = {
         "sweep1_stream": bytes_k + bytes_q, "sweep1_block": bytes_k + bytes_q,
         "sweep2_stream": bytes_k + bytes_q, "sweep2_block": bytes_k + bytes_q,
-        "single_read": bytes_k + bytes_q + bytes_scores, "reduce1": 0, "epilogue1": 0,
-        "epilogue2": bytes_scores, "select": bytes_scores + bytes_idx, "compact": bytes_gather + bytes_idx,
+        "single_read": bytes_k + bytes_q + bytes_scores, "reduce1": 0, "epilogue": bytes_scores,
+        "epilogue1": 0, "epilogue2": bytes_scores, "select": bytes_scores + bytes_idx,
+        "compact": bytes_gather + bytes_idx,
     }
+    # window logits q.k for every (window row, key): the contraction the sweeps run on the matrix cores
+    window_flops = 2 * L * Hq * w * T * D
     pass_bytes = bytes_k + bytes_q + bytes_gather + bytes_idx  # per-layer formula x L
     kernels = {}
     for name, (ms, n) in stages.items():
@@ -227,6 +231,12 @@ def main():
         "avg_launch_us": kernels[dom]["avg_us"],
     }
     pass_gbs = pass_bytes / (ms_per_step / 1e3) / 1e9
+    mfma = {}
+    for name in ("sweep1_stream", "sweep2_stream", "single_read"):
+        if name in kernels:
+            tf = window_flops / (kernels[name]["avg_us"] / 1e6) / 1e12
+            mfma[name] = {"window_flops": window_flops, "achieved_tflops": round(tf, 1),
+                          "peak_tflops": BF16_MFMA_PEAK_TFLOPS, "frac": round(tf / BF16_MFMA_PEAK_TFLOPS, 4)}
 
     extras = {}
     if args.extras:
@@ -293,6 +303,7 @@ def main():
         "per_call_ms": {k: round(v, 4) for k, v in per_call_ms.items()},
         "per_call_algorithmic_bytes": algo,
         "kernels": kernels,
+        "mfma_window_gemm": mfma,
     }
     if extras:
         out["extras"] = extras

@@ -127,7 +127,7 @@ int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, s
  * Paths: two sweeps over K (default), or, with the environment variable
  * ECOKV_SCORE_PATH=single (bf16, head_dim 128, (H_q/H_kv)*w <= 28), one
  * persistent kernel that reads K once and exchanges per-unit sums between its
- * blocks.  That kernel needs all of its blocks resident at once (one per
+ * blocks.  That kernel needs all of its blocks resident at once (two per
  * compute unit): it must not share the device with another running launch of
  * it.  If a wait between its blocks ever times out, lambda and the scores of
  * the launch come out NaN. */
