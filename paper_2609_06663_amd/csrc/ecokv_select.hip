@@ -343,10 +343,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
 {
     __shared__ uint32_t hist[kSelWaves][256];
     __shared__ uint32_t hsum[256];
-    __shared__ uint32_t bc[2];
+    __shared__ uint32_t bc[2][2];
     __shared__ uint32_t wsum[2 * kSelWaves + 2];
     __shared__ uint32_t mm[2][kSelWaves];
     __shared__ int64_t through[kMaxFlatHeads];
+    typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+    // KPT == 32: the stage of the coalesced score load, then of the output
+    __shared__ u32x4_t stg[KPT == 32 ? KPT / 4 * kSelThreads : 1];
 
     int l, h0, s, nh;
     if (a.flat) {
@@ -390,12 +393,31 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
 
     for (int h = tid; h < nh; h += blockDim.x) through[h] = 0;
     uint32_t kk[KPT];
-    if (nh == 1) {
+    if (nh == 1 && KPT == 32) {
+        // Coalesced load through LDS: the block reads the group's scores as
+        // consecutive 16-byte pieces (1 KiB per wave instruction) into a
+        // swizzled stage (piece g at g ^ ((g >> 3) & 7)), then each thread takes
+        // its 32 consecutive scores from it.
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(g.base), (short)0, n * 4, 0x00020000);
+        u32x4_t x[KPT / 4];
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q)
+            x[q] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (q * kSelThreads + tid) * 16, 0, 0));
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q) stg[q * kSelThreads + (tid ^ ((tid >> 3) & 7))] = x[q];
+        lds_barrier();
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q) {
+            const u32x4_t y = stg[(KPT / 4) * tid + (q ^ (tid & 7))];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) kk[4 * q + e] = score_key(__uint_as_float(y[e]));
+        }
+    } else if (nh == 1) {
         const __amdgpu_buffer_rsrc_t rs =
             __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(g.base), (short)0, n * 4, 0x00020000);
 #pragma unroll
         for (int q = 0; q < KPT / 4; ++q) {
-            typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
             const u32x4_t x = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (v0 + 4 * q) * 4, 0, 0));
 #pragma unroll
             for (int e = 0; e < 4; ++e) kk[4 * q + e] = score_key(__uint_as_float(x[e]));
@@ -405,6 +427,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
         for (int q = 0; q < KPT; ++q) kk[q] = v0 + q < n ? score_key(g.get(v0 + q)) : 0u;
     }
 
+    // KPT == 32: the ordered output is assembled in LDS and written out in
+    // consecutive 4-byte pieces (instead of each thread's scattered stores)
+    uint32_t *ost = reinterpret_cast<uint32_t *>(stg);
+    const bool staged = KPT == 32 && k + nh * a.w <= KPT * kSelThreads;
     uint32_t thr = 0xffffffffu;
     int need_eq = 0;
     if (k > 0) {
@@ -439,11 +465,14 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
             uint32_t mask = hi == 31 ? 0u : ~((2u << hi) - 1u);
             uint32_t prefix = kmin & mask;
             int rem = k;
+            // Three barriers per pass: the histogram is cleared by the threads
+            // that fold it, and the chosen digit alternates between two slots.
+            for (int b = tid; b < kSelWaves * 256; b += blockDim.x) (&hist[0][0])[b] = 0;
+            __syncthreads();
+            int par = 0;
             while (hi >= 0) {
                 const int lo = hi >= 7 ? hi - 7 : 0;
                 const uint32_t nb = 1u << (hi - lo + 1);
-                for (int b = tid; b < kSelWaves * 256; b += blockDim.x) (&hist[0][0])[b] = 0;
-                __syncthreads();
 #pragma unroll
                 for (int q = 0; q < KPT; ++q)
                     if (v0 + q < n && (kk[q] & mask) == prefix) atomicAdd(&hist[wv][(kk[q] >> lo) & (nb - 1u)], 1u);
@@ -451,7 +480,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
                 if (tid < 256) {
                     uint32_t c = 0;
 #pragma unroll
-                    for (int w2 = 0; w2 < kSelWaves; ++w2) c += hist[w2][tid];
+                    for (int w2 = 0; w2 < kSelWaves; ++w2) {
+                        c += hist[w2][tid];
+                        hist[w2][tid] = 0;
+                    }
                     hsum[tid] = c;
                 }
                 __syncthreads();
@@ -474,8 +506,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
                         uint32_t cum = before;
                         for (int q = 0; q < 4; ++q) {
                             if ((int)(cum + c4[q]) >= rem) {
-                                bc[0] = 255u - 4u * lane - q;
-                                bc[1] = cum;
+                                bc[par][0] = 255u - 4u * lane - q;
+                                bc[par][1] = cum;
                                 break;
                             }
                             cum += c4[q];
@@ -483,11 +515,11 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
                     }
                 }
                 __syncthreads();
-                prefix |= bc[0] << lo;
-                rem -= (int)bc[1];
+                prefix |= bc[par][0] << lo;
+                rem -= (int)bc[par][1];
                 mask |= (nb - 1u) << lo;
                 hi = lo - 1;
-                __syncthreads();
+                par ^= 1;
             }
             thr = prefix;
             need_eq = rem;
@@ -513,7 +545,11 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
             if (v0 + q < n) {
                 const bool gt = kk[q] > thr, eq = kk[q] == thr;
                 const bool take = gt || (eq && eq_before < need_eq);
-                if (take) out[gt_before + min(eq_before, need_eq) + (int64_t)h * a.w] = pos;
+                if (take) {
+                    const int64_t o = gt_before + min(eq_before, need_eq) + (int64_t)h * a.w;
+                    if (staged) ost[o] = (uint32_t)pos;
+                    else out[o] = pos;
+                }
                 gt_before += gt;
                 eq_before += eq;
                 if (++pos == P) {
@@ -529,7 +565,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
     // windows, counts and offsets
     for (int e = tid; e < nh * a.w; e += blockDim.x) {
         const int hh = e / a.w, j = e % a.w;
-        out[through[hh] + (int64_t)hh * a.w + j] = P + j;
+        const int64_t o = through[hh] + (int64_t)hh * a.w + j;
+        if (staged) ost[o] = (uint32_t)(P + j);
+        else out[o] = P + j;
+    }
+    if (staged) {
+        __syncthreads();
+        for (int e = tid; e < k + nh * a.w; e += blockDim.x) out[e] = (int32_t)ost[e];
     }
     if (tid < nh && (a.counts || a.offsets)) {
         const int hh = tid;

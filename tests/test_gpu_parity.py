@@ -247,7 +247,7 @@ def test_rising_logits():
 
 
 @pytest.mark.parametrize("variant", ["noncausal", "lambda0", "lambda1_alpha1", "mixkv", "pool1", "pool7",
-                                     "tau"])
+                                     "pool9", "pool11", "tau"])
 def test_parameter_variants(variant):
     import paper_2609_06663_amd as P
     p = {
@@ -257,6 +257,8 @@ def test_parameter_variants(variant):
         "mixkv": P.Params(alpha=0.0, beta=0.0),
         "pool1": P.Params(pool_kernel=1),
         "pool7": P.Params(pool_kernel=7),
+        "pool9": P.Params(pool_kernel=9),    # widest pooling of the one-launch epilogue
+        "pool11": P.Params(pool_kernel=11),  # wider: the two-launch epilogue
         "tau": P.Params(tau=3.0),
     }[variant]
     wl = W.custom(16, L=1, Hq=8, Hkv=2, D=128, w=4, seqlens=[900, 333], dtype="bf16", budget=[150, 60],
@@ -264,6 +266,18 @@ def test_parameter_variants(variant):
     say(f"parameter variant {variant}")
     g = gpu_pass(wl, params=p)
     check_per_head(wl, g, params=p)
+
+
+@pytest.mark.parametrize("seqlens", [[32772], [32773], [100, 32772], [2052, 255]])
+def test_epilogue_unit_bounds(seqlens):
+    # P = 32768 non-window keys is the largest unit the one-launch epilogue takes
+    # (one block, 32 keys per thread); one more key selects the two-launch
+    # epilogue; short units leave most of the block's keys past P
+    wl = W.custom(24, L=1, Hq=8, Hkv=2, D=128, w=4, seqlens=seqlens, dtype="bf16", group=128)
+    say(f"epilogue bounds: sequences {seqlens}")
+    g = gpu_pass(wl)
+    check_per_head(wl, g)
+    check_compact(wl, g)
 
 
 def test_budget_edges_per_head_and_flat():
