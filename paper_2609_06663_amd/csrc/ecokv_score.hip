@@ -715,6 +715,10 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
 {
     __shared__ float wred[3][kS2Waves];
     __shared__ u32x4 stage[kS2Waves][32 * kChunks];  // per wave: 32 rows, swizzled 16-byte chunks
+    // the block's per-key outputs (d_E, khat.mu, a), written out once at the end:
+    // a few long stores instead of three 128-byte stores per 32 keys, which
+    // interleave with the read stream at a high price
+    __shared__ __attribute__((aligned(16))) float outs[3][kS2Keys];
     const int u = blockIdx.y;
     const Unit un = unit_of(u, a.Hkv, a.B);
     const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
@@ -828,10 +832,10 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
             if (gi < P) {
                 dmn = fminf(dmn, dE);
                 dmx = fmaxf(dmx, dE);
-                a.bufA[obase + gi] = dE;
-                a.bufB[obase + gi] = cm;
-                a.bufC[obase + gi] = att * inv_r;
             }
+            outs[0][gi - row_base] = dE;
+            outs[1][gi - row_base] = cm;
+            outs[2][gi - row_base] = att * inv_r;
         }
     };
 
@@ -877,6 +881,21 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
         wred[2][wv] = dmx;
     }
     __syncthreads();
+    {
+        // keys row_base .. of the unit's P non-window keys; the descriptors end at P
+        float *const dst[3] = {a.bufA + obase, a.bufB + obase, a.bufC + obase};
+        typedef float f32x4v __attribute__((ext_vector_type(4)));
+#pragma unroll
+        for (int t = 0; t < 3; ++t) {
+            const __amdgpu_buffer_rsrc_t ro =
+                __builtin_amdgcn_make_buffer_rsrc(dst[t], (short)0, P * 4, 0x00020000);
+#pragma unroll
+            for (int i = 4 * tid; i < kS2Keys; i += 4 * 256) {
+                const f32x4v v = *reinterpret_cast<const f32x4v *>(&outs[t][i]);
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), ro, (row_base + i) * 4, 0, 0);
+            }
+        }
+    }
     if (tid == 0) {
         float s2 = 0.f, mn = INFINITY, mx = -INFINITY;
         for (int k = 0; k < kS2Waves; ++k) {
