@@ -684,11 +684,16 @@ bool fused_eligible(int D, bool bf16, int R, const SeqTab &seq, int L, int Hkv, 
     return true;
 }
 
-hipError_t fused_launch(ScoreArgs &a, int grid, hipStream_t st)
+unsigned launch_tag()
 {
     unsigned t = ++g_tag;
     if (t == 0) t = ++g_tag;
-    a.tag = t;
+    return t;
+}
+
+hipError_t fused_launch(ScoreArgs &a, int grid, hipStream_t st)
+{
+    a.tag = launch_tag();
     hipLaunchKernelGGL(fast::k_fused, dim3(grid), dim3(fast::kFThreads), 0, st, a);
     return hipGetLastError();
 }

@@ -53,6 +53,7 @@ struct ScoreArgs {
     // value of this launch from anything older without ordering fences
     unsigned long long *partT;  // [U][2D + 2R][nch1]  per-item column sums and softmax partials
     unsigned long long *ancT;   // [U][2D + 2R]        per-unit kbar, mu, row max, row normaliser
+    unsigned long long *epiT;   // [U][2][4]           the one-launch epilogue's half-unit S_div / S_imp sums
     unsigned *status;           // set to the launch tag if a wait ran out of time
     unsigned tag;               // launch tag (never 0)
     int items;                  // work items of the launch
@@ -99,7 +100,7 @@ struct CompactArgs {
 
 // Workspace layout, shared by the size query and the launcher.
 struct WsLayout {
-    size_t part1, anchors, part2, part3, bufA, bufB, bufC, partT, ancT, status, total;
+    size_t part1, anchors, part2, part3, bufA, bufB, bufC, partT, ancT, epiT, status, total;
 };
 
 WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16);
@@ -110,6 +111,9 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
 // fused-path fields of ScoreArgs.
 bool fused_eligible(int D, bool bf16, int R, const SeqTab &seq, int L, int Hkv, int Hq, int w, int *grid);
 hipError_t fused_launch(ScoreArgs &a, int grid, hipStream_t st);
+// A launch tag (never 0), distinct for every launch of the process: values a
+// launch publishes between its blocks carry it.
+unsigned launch_tag();
 constexpr int kFusedItem = 224;        // keys per work item (slice) of the single-read path
 constexpr int kFusedMaxRows = 28;      // window rows; 4 more rows carry kbar and mu
 hipError_t select_launch(const SelectArgs &a, hipStream_t st);

@@ -1412,18 +1412,23 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
     if (blockIdx.x == 0 && threadIdx.x == 0) epi_write_stats(a, u, k, dst, sd, mu2);
 }
 
-// Epilogue in one launch when a unit's P non-window keys fit one block: every
-// per-unit reduction is block-local, so each key's d_E, khat.mu and attention
-// is read once.  Wave w holds keys 2048 w .. 2048 w + 2047 as 8 chunks of 256;
-// lane l of chunk j holds keys 2048 w + 256 j + 4 l .. +3, so each load
-// instruction covers 1 KiB of consecutive keys.  The pooling window (up to 4
-// keys on each side) comes from the neighbouring lanes' registers (or the
-// neighbouring chunk's end lane); the wave's outermost neighbours come from
-// the neighbouring waves through LDS.
+// Epilogue in one launch when a unit's P non-window keys fit one block
+// (SPLIT = 1) or two (SPLIT = 2, each with half of the keys).  Every per-unit
+// reduction is block-local, except that with SPLIT = 2 the two halves of a
+// unit exchange their S_div / S_imp sums and extrema once (tagged 64-bit
+// relaxed atomics, as in the single-read path; the halves are combined in a
+// fixed order, so both compute the same constants).  Each key's d_E,
+// khat.mu and attention is read once.  Wave w holds 8/SPLIT chunks of 256
+// consecutive keys; lane l of chunk j holds keys 256 j + 4 l .. +3 of the
+// wave's range, so each load instruction covers 1 KiB of consecutive keys.
+// The pooling window (up to 4 keys on each side) comes from the neighbouring
+// lanes' registers (or the neighbouring chunk's end lane); the wave's
+// outermost neighbours come from the neighbouring waves through LDS, and at
+// the ends of a block's range from memory.
 constexpr int kUThreads = 1024;
-constexpr int kUVec = 8;                      // chunks (float4 per thread and array)
-constexpr int kUWaveKeys = 256 * kUVec;       // keys per wave
-constexpr int kUKeys = kUThreads / kWave * kUWaveKeys;  // 32768
+constexpr int kUW = kUThreads / kWave;
+constexpr int kUKeys = kUThreads * 32;  // 32768 keys per unit
+constexpr int kUSpinLimit = 1 << 14;
 
 // Block sum / min / max whose barriers order LDS only, so that global loads
 // issued before it stay in flight.
@@ -1471,13 +1476,22 @@ __device__ __forceinline__ f32x4 lane_value(f32x4 x, int l)
     return r;
 }
 
+__device__ __forceinline__ void epi_tag_store(unsigned long long *p, float v, unsigned tag)
+{
+    __hip_atomic_store(p, ((unsigned long long)tag << 32) | __float_as_uint(v), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int SPLIT>
 __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
 {
-    constexpr int kUW = kUThreads / kWave;
-    __shared__ Red4 lds[kUW];
-    __shared__ f32x4 svl[kUVec][kUThreads];  // S_div of every thread's keys (128 KiB)
-    __shared__ f32x4 edge[kUW][2];           // per wave: its first and last four attention values
-    const int u = blockIdx.x;
+    constexpr int kVec = 8 / SPLIT;          // chunks (float4 per thread and array)
+    constexpr int kWaveKeys = 256 * kVec;    // keys per wave
+    constexpr int kPartKeys = kUW * kWaveKeys;
+    __shared__ Red4 lds[kUW + 1];
+    __shared__ f32x4 svl[kVec][kUThreads];  // S_div of every thread's keys
+    __shared__ f32x4 edge[kUW][2];          // per wave: its first and last four attention values
+    const int u = blockIdx.x / SPLIT, part = blockIdx.x % SPLIT;
     const Unit un = unit_of(u, a.Hkv, a.B);
     const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
     const int P = T - a.w;
@@ -1486,32 +1500,43 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
     const float *mu = a.anchors + (int64_t)u * stride + a.D;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int half = a.pool_half;  // <= kPoolHalfMax (checked on the host)
-    const int kw = kUWaveKeys * wv;
+    const int kw = kPartKeys * part + kWaveKeys * wv;
 
     // every global load first, so that their latencies overlap: the sweep-2
-    // partials and mu (d_E sum / extrema and |mu|^2 in one block reduction),
-    // then d_E, khat.mu and attention of the thread's keys (zero past P)
+    // partials and mu (d_E sum / extrema and |mu|^2 in one block reduction;
+    // one partial and one mu component per thread at most: a unit of at most
+    // 32768 + w keys has at most 257 sweep-2 blocks, and D <= 128), then
+    // d_E, khat.mu and attention of the thread's keys (zero past P), and the
+    // attention just outside the block's range (a negative offset wraps past
+    // the range and reads zero)
     Red4 v{0.f, 0.f, INFINITY, -INFINITY};
     const int nb2 = (T + a.rpb2 - 1) / a.rpb2;
-    for (int b = threadIdx.x; b < nb2; b += blockDim.x) {
-        const float *pp = a.part2 + ((int64_t)u * a.nch2 + b) * 4;
-        v.s0 += pp[0];
-        v.mn = fminf(v.mn, pp[1]);
-        v.mx = fmaxf(v.mx, pp[2]);
+    if ((int)threadIdx.x < nb2) {
+        const float *pp = a.part2 + ((int64_t)u * a.nch2 + threadIdx.x) * 4;
+        v.s0 = pp[0];
+        v.mn = pp[1];
+        v.mx = pp[2];
     }
-    for (int d = threadIdx.x; d < a.D; d += blockDim.x) v.s1 += mu[d] * mu[d];
+    const float mv = (int)threadIdx.x < a.D ? mu[threadIdx.x] : 0.f;
     const __amdgpu_buffer_rsrc_t rd = float_rsrc(a.bufA + ob, P), rc = float_rsrc(a.bufB + ob, P),
                                  ra = float_rsrc(a.bufC + ob, P);
-    f32x4 xd[kUVec], xc[kUVec], xa[kUVec];
+    f32x4 xd[kVec], xc[kVec], xa[kVec];
 #pragma unroll
-    for (int j = 0; j < kUVec; ++j) {
+    for (int j = 0; j < kVec; ++j) {
         const int k4 = kw + 256 * j + 4 * lane;
         xd[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rd, k4 * 4, 0, 0));
         xc[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rc, k4 * 4, 0, 0));
         xa[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, k4 * 4, 0, 0));
     }
+    f32x4 bl = {0.f, 0.f, 0.f, 0.f}, br = {0.f, 0.f, 0.f, 0.f};
+    if (SPLIT > 1) {
+        const int b0 = kPartKeys * part;
+        bl = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, (unsigned)(b0 - 4) * 4u, 0, 0));
+        br = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, (b0 + kPartKeys) * 4, 0, 0));
+    }
     __builtin_amdgcn_sched_barrier(0);  // the phases below stay in order (register pressure)
 
+    v.s1 = mv * mv;
     const Red4 dm = block_red4_lds(v, lds);
     const Red4 dst{dm.s0, 0.f, dm.mn, dm.mx};
     const float mu2 = dm.s1;
@@ -1520,7 +1545,7 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
     const float dmin = dst.mn, inv_dden = 1.f / (dst.mx - dst.mn + a.eps);
     Red4 w{0.f, 0.f, INFINITY, -INFINITY};
 #pragma unroll
-    for (int j = 0; j < kUVec; ++j) {
+    for (int j = 0; j < kVec; ++j) {
         const int k4 = kw + 256 * j + 4 * lane;
         f32x4 sv;
 #pragma unroll
@@ -1538,20 +1563,19 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
     }
     // the wave's first and last four attention values for its neighbours
     if (lane == 0) edge[wv][0] = xa[0];
-    if (lane == 63) edge[wv][1] = xa[kUVec - 1];
+    if (lane == 63) edge[wv][1] = xa[kVec - 1];
     lds_barrier();
-    const f32x4 z4 = {0.f, 0.f, 0.f, 0.f};
-    const f32x4 hl = wv > 0 ? edge[wv - 1][1] : z4;            // the four keys before the wave's first
-    const f32x4 hr = wv < kUW - 1 ? edge[wv + 1][0] : z4;       // the four after its last
+    const f32x4 hl = wv > 0 ? edge[wv - 1][1] : bl;       // the four keys before the wave's first
+    const f32x4 hr = wv < kUW - 1 ? edge[wv + 1][0] : br;  // the four after its last
     __builtin_amdgcn_sched_barrier(0);
     // pooled S_imp (each chunk's attention registers die as its pooled values are made)
     const float inv_k = 1.f / (float)(2 * half + 1);
-    f32x4 im[kUVec];
+    f32x4 im[kVec];
 #pragma unroll
-    for (int j = 0; j < kUVec; ++j) {
+    for (int j = 0; j < kVec; ++j) {
         const f32x4 sl = from_prev_lane(xa[j]), sr = from_next_lane(xa[j]);
         const f32x4 pl = j > 0 ? lane_value(xa[j - 1], 63) : hl;  // lane 0: previous chunk's end
-        const f32x4 nr = j < kUVec - 1 ? lane_value(xa[j + 1], 0) : hr;  // lane 63: next chunk's start
+        const f32x4 nr = j < kVec - 1 ? lane_value(xa[j + 1], 0) : hr;  // lane 63: next chunk's start
         const f32x4 left = lane == 0 ? pl : sl;
         const f32x4 right = lane == 63 ? nr : sr;
         float win[12];  // keys k4 - 4 .. k4 + 7
@@ -1572,13 +1596,45 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
             if (k4 + e < P) w.s1 += im[j][e];
         }
     }
-    const Red4 sd = block_red4_lds(w, lds);
+    Red4 sd = block_red4_lds(w, lds);
+    if (SPLIT > 1) {
+        // exchange with the other half of the unit: publish, then wait (bounded)
+        if (threadIdx.x == 0) {
+            unsigned long long *mine = a.epiT + ((int64_t)u * 2 + part) * 4;
+            epi_tag_store(mine + 0, sd.s0, a.tag);
+            epi_tag_store(mine + 1, sd.s1, a.tag);
+            epi_tag_store(mine + 2, sd.mn, a.tag);
+            epi_tag_store(mine + 3, sd.mx, a.tag);
+            const unsigned long long *other = a.epiT + ((int64_t)u * 2 + (part ^ 1)) * 4;
+            unsigned long long o[4];
+            int tries = 0;
+            bool ok;
+            do {
+                ok = true;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    o[q] = __hip_atomic_load(other + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    ok = ok && (unsigned)(o[q] >> 32) == a.tag;
+                }
+                if (!ok) __builtin_amdgcn_s_sleep(2);
+            } while (!ok && ++tries < kUSpinLimit);
+            if (!ok) __hip_atomic_store(a.status, a.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const Red4 so{__uint_as_float((unsigned)o[0]), __uint_as_float((unsigned)o[1]),
+                          __uint_as_float((unsigned)o[2]), __uint_as_float((unsigned)o[3])};
+            const Red4 h0 = part == 0 ? sd : so, h1 = part == 0 ? so : sd;  // the same order in both halves
+            Red4 c{h0.s0 + h1.s0, h0.s1 + h1.s1, fminf(h0.mn, h1.mn), fmaxf(h0.mx, h1.mx)};
+            if (!ok) c.s0 = NAN;
+            lds[kUW] = c;
+        }
+        lds_barrier();
+        sd = lds[kUW];
+    }
     const EpiConsts k = epi_consts(a, dst, sd, mu2, T, P);
 
     const __amdgpu_buffer_rsrc_t ro = float_rsrc(a.scores + ob, P);
     const float gain = k.lam * k.scale / k.sden, one_m = 1.f - k.lam;
 #pragma unroll
-    for (int j = 0; j < kUVec; ++j) {
+    for (int j = 0; j < kVec; ++j) {
         const f32x4 sv = svl[j][threadIdx.x];
         f32x4 x;
 #pragma unroll
@@ -1592,7 +1648,7 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
                 if (k4 + e < P) a.scores[ob + k4 + e] = x[e];
         }
     }
-    if (threadIdx.x == 0) epi_write_stats(a, u, k, dst, sd, mu2);
+    if (part == 0 && threadIdx.x == 0) epi_write_stats(a, u, k, dst, sd, mu2);
 }
 
 // ---------------------------------------------------------------------------
@@ -1610,7 +1666,7 @@ WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int 
     const int64_t U = (int64_t)L * Hkv * B;
     const int rpb = rows_per_block(D, bf16);
     const int64_t nch1 = (maxT + rpb - 1) / rpb;
-    // the single-read path publishes per 256-key item; size for it whenever it may run
+    // the single-read path publishes per slice; size for it whenever it may run
     const bool single = bf16 && D == fast::kD && R <= kFusedMaxRows;
     const int64_t nchf = single ? (maxT + kFusedItem - 1) / kFusedItem : 0;
     const int64_t nch2 = nch1 > nchf ? nch1 : nchf;
@@ -1626,6 +1682,7 @@ WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int 
     w.bufC = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
     w.partT = o; o = align256(o + sizeof(unsigned long long) * U * stride * nchf);
     w.ancT = o; o = align256(o + (single ? sizeof(unsigned long long) * U * stride : 0));
+    w.epiT = o; o = align256(o + sizeof(unsigned long long) * U * 2 * 4);
     w.status = o; o = align256(o + sizeof(unsigned));
     w.total = o;
     return w;
@@ -1664,6 +1721,21 @@ static void launch_sweep(int pass, const ScoreArgs &a, dim3 grid, hipStream_t st
         else if (a.D == 128) hipLaunchKernelGGL((k_pass2<128, false>), grid, dim3(kThreads), 0, st, a);
         else hipLaunchKernelGGL((k_pass2<64, false>), grid, dim3(kThreads), 0, st, a);
     }
+}
+
+// Blocks of k_epi_unit<2> that the current device holds at once (cached per device).
+static int64_t epi_split_capacity()
+{
+    static int64_t cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cache[dev] == 0) {
+        int ncu = 0, nb = 0;
+        if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_epi_unit<2>, kUThreads, 0) != hipSuccess) return 0;
+        cache[dev] = (int64_t)ncu * nb;
+    }
+    return cache[dev];
 }
 
 hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hipStream_t st, bool bf16)
@@ -1729,8 +1801,17 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    if (maxT - a.w <= kUKeys && a.pool_half <= kPoolHalfMax) {
-        ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL(k_epi_unit, dim3(U), dim3(kUThreads), 0, st, a));
+    if (maxT - a.w <= kUKeys && a.pool_half <= kPoolHalfMax && (maxT + a.rpb2 - 1) / a.rpb2 <= kUThreads && a.D <= kUThreads) {
+        // two blocks per unit when all of them can be resident at once (their
+        // exchange waits for each other), else one
+        if (2 * (int64_t)U <= epi_split_capacity()) {
+            a.epiT = reinterpret_cast<unsigned long long *>(ws + lay.epiT);
+            a.status = reinterpret_cast<unsigned *>(ws + lay.status);
+            if (a.tag == 0) a.tag = launch_tag();  // (the single-read path's tag, if it ran)
+            ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL(k_epi_unit<2>, dim3(2 * U), dim3(kUThreads), 0, st, a));
+        } else {
+            ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL(k_epi_unit<1>, dim3(U), dim3(kUThreads), 0, st, a));
+        }
         return hipGetLastError();
     }
     ECOKV_TIMED("epilogue1", st, hipLaunchKernelGGL(k_epi1, grid_e, dim3(kEpiThreads), 0, st, a));
