@@ -124,6 +124,11 @@ int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, s
  *   workspace, workspace_bytes: device scratch of ecokv_workspace_size bytes,
  *   256-byte aligned.
  * Arithmetic: fp32 accumulation of bf16/fp32 inputs.
+ * For sequences of at most 32768 + w tokens the final step runs as pairs of
+ * blocks (two per (layer, KV head, sequence)) that exchange sums once and wait
+ * for each other, when the device can hold all of them at once; if one ever
+ * waits for its partner for seconds (the device taken by other work all that
+ * time), that unit's lambda and scores come out NaN.
  * Paths: two sweeps over K (default), or, with the environment variable
  * ECOKV_SCORE_PATH=single (bf16, head_dim 128, (H_q/H_kv)*w <= 28), one
  * persistent kernel that reads K once and exchanges per-unit sums between its

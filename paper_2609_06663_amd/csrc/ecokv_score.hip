@@ -251,16 +251,9 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
 namespace fast {
 
 constexpr float kRebase = 16.f;       // log2 headroom of a lazily moved softmax reference
-#ifndef ECOKV_SWEEP_TILES
-#define ECOKV_SWEEP_TILES 8
-#endif
-#ifndef ECOKV_SWEEP1_DEPTH
-#define ECOKV_SWEEP1_DEPTH 2
-#endif
-#ifndef ECOKV_SWEEP2_DEPTH
-#define ECOKV_SWEEP2_DEPTH 2
-#endif
-constexpr int kTilesPerBlock = ECOKV_SWEEP_TILES;  // tiles per block (1024 keys by default)
+constexpr int kTilesPerBlock = 8;  // tiles per block (1024 keys)
+constexpr int kSweep1Depth = 2;    // tiles in flight ahead of the one in use
+constexpr int kSweep2Depth = 2;
 constexpr int kRows = kTile * kTilesPerBlock;
 
 // One 128-key tile into registers: 16 lanes per 256-byte row, coalesced.
@@ -386,7 +379,7 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
 
     const int ntiles = min(kTilesPerBlock, (T - row_base + kTile - 1) / kTile);
     const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + kRows));
-    tile_pipeline<ECOKV_SWEEP1_DEPTH>(kt, rs, row_base, ntiles, g, c, [&](int tr0) {
+    tile_pipeline<kSweep1Depth>(kt, rs, row_base, ntiles, g, c, [&](int tr0) {
         // window logits and |k|^2 of this wave's 32 keys
         f32x16 acc[MT];
 #pragma unroll
@@ -617,7 +610,7 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
     const float inv_r = 1.f / (float)a.R;
     const int ntiles = min(kTilesPerBlock, (T - row_base + kTile - 1) / kTile);
     const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + kRows));
-    tile_pipeline<ECOKV_SWEEP2_DEPTH>(kt, rs, row_base, ntiles, g, c, [&](int tr0) {
+    tile_pipeline<kSweep2Depth>(kt, rs, row_base, ntiles, g, c, [&](int tr0) {
 
         f32x16 acc[MT];
 #pragma unroll
@@ -690,16 +683,14 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
 
 // Sweep 2, streaming form (window rows + 4 anchor rows in one 32-row operand,
 // i.e. G*w <= 28): no LDS tile and no barrier in the key loop.  Each wave
-// streams its own groups of 32 keys straight from HBM into MFMA B-operand
-// registers (lane l: key l % 32, 16-byte chunks 2s + l / 32), double
-// buffered, so the loads of group g+1 are in flight while group g is used.
-// The attention of row m is 2^(x - M'_m) with M'_m = M_m + log2(S_m), the
-// normaliser folded into the shift.
+// streams its own 512 keys in groups of 32 from HBM into registers (three
+// groups in flight), re-lays them out through a wave-private LDS stage into
+// MFMA B operands (lane l: key l % 32, 16-byte chunks 2s + l / 32).  The
+// attention of row m is 2^(x - M'_m) with M'_m = M_m + log2(S_m), the
+// normaliser folded into the shift.  2048-key blocks: 1024 and 4096 measured
+// no better.
 constexpr int kS2Waves = 4;
-#ifndef ECOKV_S2_KEYS
-#define ECOKV_S2_KEYS 2048
-#endif
-constexpr int kS2Keys = ECOKV_S2_KEYS;            // keys per block
+constexpr int kS2Keys = 2048;                          // keys per block
 constexpr int kS2Groups = kS2Keys / (32 * kS2Waves);  // 32-key groups per wave
 
 // Coalesced load of 32 key rows: instruction i covers rows 4i .. 4i+3, lane l
@@ -912,7 +903,7 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
 }
 
 // Sweep 1, streaming form (bf16, head_dim 128, G*w <= 32): like the streaming
-// sweep 2, each wave streams its own 1024 keys in 32-key groups (coalesced
+// sweep 2, each wave streams its own 512 keys in 32-key groups (coalesced
 // loads, three register buffers in flight, a wave-private LDS stage) and no
 // barrier is needed until the final merge of the four waves.
 //  * window logits: v_mfma_f32_32x32x16_bf16 with the keys as the A operand and
@@ -1428,7 +1419,7 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
 constexpr int kUThreads = 1024;
 constexpr int kUW = kUThreads / kWave;
 constexpr int kUKeys = kUThreads * 32;  // 32768 keys per unit
-constexpr int kUSpinLimit = 1 << 14;
+constexpr int kUSpinLimit = 1 << 20;  // a few seconds: the partner block only has to be scheduled
 
 // Block sum / min / max whose barriers order LDS only, so that global loads
 // issued before it stay in flight.
@@ -1485,6 +1476,7 @@ __device__ __forceinline__ void epi_tag_store(unsigned long long *p, float v, un
 template <int SPLIT>
 __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
 {
+    static_assert(SPLIT == 1 || SPLIT == 2, "one or two blocks per unit");
     constexpr int kVec = 8 / SPLIT;          // chunks (float4 per thread and array)
     constexpr int kWaveKeys = 256 * kVec;    // keys per wave
     constexpr int kPartKeys = kUW * kWaveKeys;
@@ -1803,7 +1795,7 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     }
     if (maxT - a.w <= kUKeys && a.pool_half <= kPoolHalfMax && (maxT + a.rpb2 - 1) / a.rpb2 <= kUThreads && a.D <= kUThreads) {
         // two blocks per unit when all of them can be resident at once (their
-        // exchange waits for each other), else one
+        // exchange waits for each other; four per unit measured no faster), else one
         if (2 * (int64_t)U <= epi_split_capacity()) {
             a.epiT = reinterpret_cast<unsigned long long *>(ws + lay.epiT);
             a.status = reinterpret_cast<unsigned *>(ws + lay.status);
