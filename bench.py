@@ -238,6 +238,34 @@ def main():
             mfma[name] = {"window_flops": window_flops, "achieved_tflops": round(tf, 1),
                           "peak_tflops": BF16_MFMA_PEAK_TFLOPS, "frac": round(tf / BF16_MFMA_PEAK_TFLOPS, 4)}
 
+    # Budgets per (layer, KV head): the PyramidKV layer schedule (beta 20) with
+    # the same tokens per head over the stack, select + compact on the scores
+    # of the pass above (outputs fit the uniform-budget buffers: same total).
+    log("per-(layer, head) budgets: PyramidKV schedule")
+    per_layer = P.ecokv_pyramid_budgets(L, L * b, 20.0, w)
+    hbud = [bl for bl in per_layer for _ in range(Hkv)]
+    n_h = P.ecokv_index_count_mode(shape, P.HEAD_BUDGETS, hbud)
+    assert n_h <= ep.n_idx
+    h_calls = {
+        "select": lambda: P.ecokv_select(ep.scores, shape, P.HEAD_BUDGETS, hbud, ep.idx, ep.counts, ep.offsets),
+        "compact": lambda: P.ecokv_compact(K, V, shape, P.HEAD_BUDGETS, hbud, ep.idx, None, None, ep.Kc, ep.Vc),
+    }
+    head_budgets = {"schedule": "PyramidKV, beta 20", "budget_first_layer": per_layer[0],
+                    "budget_last_layer": per_layer[-1], "entries": n_h}
+    for name, fn in h_calls.items():
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        head_budgets[f"{name}_ms"] = round(e0.elapsed_time(e1) / args.steps, 4)
+    h_gather = 4 * n_h * D * e + 4 * n_h
+    head_budgets["compact_algorithmic_bytes"] = h_gather
+    head_budgets["compact_GBs"] = round(h_gather / (head_budgets["compact_ms"] / 1e3) / 1e9, 1)
+
     extras = {}
     if args.extras:
         for frac in (0.1, 0.4):
@@ -304,6 +332,7 @@ def main():
         "per_call_algorithmic_bytes": algo,
         "kernels": kernels,
         "mfma_window_gemm": mfma,
+        "head_budgets": head_budgets,
     }
     if extras:
         out["extras"] = extras

@@ -63,6 +63,11 @@ extern "C" {
 #define ECOKV_PER_HEAD 0   /* each unit keeps exactly min(b_s, T_s) tokens    */
 #define ECOKV_LAYER_FLAT 1 /* the H_kv heads of (layer, sequence) share       */
                            /* H_kv*min(b_s, T_s) places (AdaKV, App. A.1)     */
+#define ECOKV_HEAD_BUDGETS 2 /* head h of layer l keeps min(b^l_h, T_s) tokens */
+                             /* per sequence: a caller-chosen budget for each */
+                             /* (layer, KV head), as PyramidKV's layer        */
+                             /* schedule and SparseMM's head budgets assign   */
+                             /* them (App. A.1)                               */
 
 #define ECOKV_MAX_SEQS 64   /* sequences per call                              */
 #define ECOKV_MAX_ROWS 64   /* window rows per KV head, (H_q/H_kv)*w           */
@@ -141,13 +146,22 @@ int ecokv_score(const void *K, const void *Q_win, int dtype, const ecokv_shape *
                 void *workspace, size_t workspace_bytes, void *stream);
 
 /* Number of int32 entries ecokv_select writes to idx:
- * L * H_kv * sum_s min(budget[s], T_s) (both modes). */
+ * L * H_kv * sum_s min(budget[s], T_s) (ECOKV_PER_HEAD and ECOKV_LAYER_FLAT). */
 int ecokv_index_count(const ecokv_shape *shape, const int32_t *budget, int64_t *count);
 
-/* Select the kept positions (Sec. 3; AdaKV, Appendix A.1).
+/* The same for any mode: `budget` is laid out as ecokv_select takes it in
+ * that mode ([B], or [L][H_kv] for ECOKV_HEAD_BUDGETS, where the count is
+ * sum over (l, h, s) of min(budget[l][h], T_s)). */
+int ecokv_index_count_mode(const ecokv_shape *shape, int mode, const int32_t *budget, int64_t *count);
+
+/* Select the kept positions (Sec. 3; AdaKV, PyramidKV and SparseMM budgets,
+ * Appendix A.1).
  *   scores  [L][H_kv][Ptot] float32, as written by ecokv_score
  *   budget  HOST [B]: b_s = tokens kept per head for sequence s, window
  *           included, b_s >= w.  b_s >= T_s keeps every token.
+ *           ECOKV_HEAD_BUDGETS: HOST [L][H_kv] instead, b^l_h = tokens kept
+ *           by head h of layer l in every sequence (window included, >= w,
+ *           >= T_s keeps every token).
  *   mode    ECOKV_PER_HEAD: unit (l,h,s) keeps the b_s - w highest scores
  *           (equal scores: smaller position first), listed ascending, then the
  *           window T_s-w .. T_s-1.  Units are laid out in (l, h, s) order.
@@ -155,10 +169,13 @@ int ecokv_index_count(const ecokv_shape *shape, const int32_t *budget, int64_t *
  *           H_kv*(b_s - w) places (equal scores: smaller (head, position)
  *           first); each head lists its chosen positions ascending, then its
  *           window.  Groups are laid out in (l, s) order, heads in order.
+ *           ECOKV_HEAD_BUDGETS: as ECOKV_PER_HEAD with unit (l,h,s) keeping
+ *           min(b^l_h, T_s) tokens; units in (l, h, s) order.
  *   idx     output, ecokv_index_count entries
- *   counts  [L][H_kv][B] output: entries of each unit (may be NULL in PER_HEAD)
- *   offsets [L][H_kv][B] output: start of each unit in idx (may be NULL in
- *           PER_HEAD)
+ *   counts  [L][H_kv][B] output: entries of each unit (may be NULL, except in
+ *           LAYER_FLAT)
+ *   offsets [L][H_kv][B] output: start of each unit in idx (may be NULL,
+ *           except in LAYER_FLAT)
  * NaN scores rank below every number; -0 ranks equal to +0. */
 int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const int32_t *budget,
                  int32_t *idx, int32_t *counts, int32_t *offsets, void *stream);
@@ -166,11 +183,22 @@ int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const 
 /* Gather Kc[e] = K[row of entry e], Vc[e] = V[row of entry e] for every idx
  * entry e, bit-exact (Sec. 3).  `mode` and `budget` as given to ecokv_select;
  * counts and offsets are required for ECOKV_LAYER_FLAT (device arrays written
- * by ecokv_select) and ignored for ECOKV_PER_HEAD.  Kc, Vc have
- * ecokv_index_count rows of D elements. */
+ * by ecokv_select) and ignored for ECOKV_PER_HEAD and ECOKV_HEAD_BUDGETS.
+ * Kc, Vc have ecokv_index_count_mode rows of D elements. */
 int ecokv_compact(const void *K, const void *V, int dtype, const ecokv_shape *shape, int mode,
                   const int32_t *budget, const int32_t *idx, const int32_t *counts,
                   const int32_t *offsets, void *Kc, void *Vc, void *stream);
+
+/* PyramidKV's layer schedule (Appendix A.1), host only: for m = num_layers
+ * layers sharing `total` tokens per head, the last layer gets
+ * b^{m-1} = total / (beta m), the first b^0 = 2 total / m - b^{m-1}, and the
+ * layers between follow the straight line b^l = b^0 - (b^0 - b^{m-1}) l / (m-1)
+ * (one layer: b^0 = total).  Each value is rounded down, so the sum is at most
+ * `total`.  out: HOST [num_layers].  ECOKV_EINVAL if num_layers < 1, total or
+ * beta is not a positive finite number, or a value would fall below
+ * `window` (>= 1) or exceed INT32_MAX.  To give every KV head of a layer its
+ * layer's budget, repeat each value H_kv times for ECOKV_HEAD_BUDGETS. */
+int ecokv_pyramid_budgets(int num_layers, double total, double beta, int window, int32_t *out);
 
 /* Message for the calling thread's last failed call ("" if none). */
 const char *ecokv_last_error(void);

@@ -28,7 +28,7 @@ _LIB = os.path.join(_HERE, "libecokv_oracle.so")
 NSTATS = 12
 STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7,
             imp_mean=8, sbar_mean=9, mu_norm2=10, scale=11)
-PER_HEAD, LAYER_FLAT = 0, 1
+PER_HEAD, LAYER_FLAT, HEAD_BUDGETS = 0, 1, 2
 BF16, F32 = 0, 1
 
 
@@ -190,18 +190,39 @@ def select_flat(S_heads: np.ndarray, T: int, w: int, b: int):
     return out, counts
 
 
-def index_count(L, Hkv, cu_seqlens, budget) -> int:
+def index_count(L, Hkv, cu_seqlens, budget, mode=PER_HEAD) -> int:
+    """Entries of idx: budget[s] per sequence, or budget[l][h] with mode HEAD_BUDGETS."""
     B = len(cu_seqlens) - 1
-    return L * Hkv * sum(min(int(budget[s]), int(cu_seqlens[s + 1] - cu_seqlens[s])) for s in range(B))
+    lens = [int(cu_seqlens[s + 1] - cu_seqlens[s]) for s in range(B)]
+    if mode == HEAD_BUDGETS:
+        b = np.asarray(budget).reshape(-1)
+        return sum(min(int(b[lh]), lens[s]) for lh in range(L * Hkv) for s in range(B))
+    return L * Hkv * sum(min(int(budget[s]), lens[s]) for s in range(B))
+
+
+def pyramid_budgets(m: int, total, beta) -> list:
+    """PyramidKV's layer schedule (Appendix A.1) in exact rational arithmetic:
+    b^{m-1} = total / (beta m), b^0 = 2 total / m - b^{m-1}, the layers between
+    on the straight line from b^0 to b^{m-1}; one layer gets the total.  Each
+    value is rounded down.  `total` and `beta` are taken exactly (a float is
+    its binary value)."""
+    from fractions import Fraction
+    tot, bet = Fraction(total), Fraction(beta)
+    if m == 1:
+        return [math.floor(tot)]
+    last = tot / (bet * m)
+    first = 2 * tot / m - last
+    return [math.floor(first - (first - last) * l / (m - 1)) for l in range(m)]
 
 
 def select(S, L, Hkv, cu_seqlens, w, budget, mode=PER_HEAD, nthreads: int = 1):
-    """Select over every unit; returns idx (packed), counts [L][Hkv][B], offsets [L][Hkv][B]."""
+    """Select over every unit; returns idx (packed), counts [L][Hkv][B], offsets [L][Hkv][B].
+    `budget` has one entry per sequence, or [L][Hkv] entries with mode HEAD_BUDGETS."""
     S = np.ascontiguousarray(S, dtype=np.float64)
     cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
-    bud = np.ascontiguousarray(budget, dtype=np.int32)
+    bud = np.ascontiguousarray(np.asarray(budget).reshape(-1), dtype=np.int32)
     B = len(cu) - 1
-    idx = np.zeros(index_count(L, Hkv, cu, bud), np.int32)
+    idx = np.zeros(index_count(L, Hkv, cu, bud, mode), np.int32)
     counts = np.zeros((L, Hkv, B), np.int32)
     offsets = np.zeros((L, Hkv, B), np.int32)
     rc = lib().ora_select(_dp(S), L, Hkv, B, _ip(cu), w, _ip(bud), mode, _ip(idx), _ip(counts),

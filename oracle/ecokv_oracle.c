@@ -34,7 +34,7 @@
 #endif
 
 enum { ORA_BF16 = 0, ORA_F32 = 1 };
-enum { ORA_PER_HEAD = 0, ORA_LAYER_FLAT = 1 };
+enum { ORA_PER_HEAD = 0, ORA_LAYER_FLAT = 1, ORA_HEAD_BUDGETS = 2 };
 
 /* Per-head statistics written by ora_score_unit (indices into stats[ORA_NSTATS]). */
 enum {
@@ -423,21 +423,57 @@ int ora_score(const void *K, const void *Q, int dtype, int L, int Hq, int Hkv, i
 
 /* idx layout: PER_HEAD -- unit (l, h, s) owns min(b_s, T_s) entries, units in
  * (l, h, s) order.  LAYER_FLAT -- group (l, s) owns Hkv * min(b_s, T_s)
- * entries, groups in (l, s) order, heads in order inside a group.  counts and
- * offsets ([L][Hkv][B]) give each unit's entry count and start. */
+ * entries, groups in (l, s) order, heads in order inside a group.
+ * HEAD_BUDGETS -- budget is [L][Hkv] (a budget per layer and head, as the
+ * PyramidKV layer schedule and the SparseMM head budgets of Appendix A.1
+ * assign them): unit (l, h, s) owns min(b[l][h], T_s) entries, units in
+ * (l, h, s) order.  counts and offsets ([L][Hkv][B]) give each unit's entry
+ * count and start. */
 int ora_select(const double *S, int L, int Hkv, int B, const int32_t *cu, int w,
                const int32_t *budget, int mode, int32_t *idx, int32_t *counts,
                int32_t *offsets, int nthreads)
 {
     const int64_t Ttot = cu[B];
     const int64_t Ptot = Ttot - (int64_t)B * w;
+    int bad = 0;
+    if (mode == ORA_HEAD_BUDGETS) {
+        for (int s = 0; s < B; ++s)
+            if (w >= cu[s + 1] - cu[s]) return -1;
+        for (int64_t lh = 0; lh < (int64_t)L * Hkv; ++lh)
+            if (budget[lh] < w) return -1;
+        const int64_t U = (int64_t)L * Hkv * B;
+        int64_t *start = malloc((size_t)(U > 0 ? U : 1) * sizeof(int64_t));
+        if (!start) return -2;
+        int64_t o = 0;
+        for (int64_t u = 0; u < U; ++u) {
+            const int s = (int)(u % B);
+            const int T = cu[s + 1] - cu[s];
+            const int32_t b = budget[u / B];
+            start[u] = o;
+            o += b < T ? b : T;
+        }
+#ifdef _OPENMP
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads > 0 ? nthreads : 1) reduction(|| : bad)
+#endif
+        for (int64_t u = 0; u < U; ++u) {
+            const int s = (int)(u % B);
+            const int64_t lh = u / B;
+            const int T = cu[s + 1] - cu[s];
+            const int n = ora_select_unit(S + lh * Ptot + (cu[s] - s * w), T, w, budget[lh], idx + start[u]);
+            if (n < 0) bad = 1;
+            if (counts) counts[u] = n;
+            if (offsets) offsets[u] = (int32_t)start[u];
+        }
+        free(start);
+        (void)nthreads;
+        return bad ? -1 : 0;
+    }
     int64_t per_layer_head = 0; /* sum over s of min(b_s, T_s) */
     for (int s = 0; s < B; ++s) {
         const int T = cu[s + 1] - cu[s];
         if (budget[s] < w || w >= T) return -1;
         per_layer_head += budget[s] < T ? budget[s] : T;
     }
-    int bad = 0;
     if (mode == ORA_PER_HEAD) {
         const int64_t U = (int64_t)L * Hkv * B;
 #ifdef _OPENMP

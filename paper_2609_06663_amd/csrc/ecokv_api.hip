@@ -106,6 +106,46 @@ int fill_seqtab(const ecokv_shape *sh, const int32_t *budget, int w, ecokv::SeqT
     return ECOKV_OK;
 }
 
+// Per-(layer, KV head) budgets (ECOKV_HEAD_BUDGETS): checks every budget and
+// counts the idx entries, sum over (l, h, s) of min(b^l_h, T_s).
+int head_budget_total(const ecokv_shape *sh, const ShapeInfo &si, const int32_t *budget, int64_t *total)
+{
+    const int64_t n = (int64_t)si.L * si.Hkv;
+    int64_t acc = 0;
+    for (int64_t j = 0; j < n; ++j) {
+        if (budget[j] < si.w)
+            return fail(ECOKV_EINVAL, "budget[%lld] = %d is below the window %d", (long long)j, budget[j], si.w);
+        for (int s = 0; s < si.B; ++s) {
+            const int T = sh->cu_seqlens[s + 1] - sh->cu_seqlens[s];
+            acc += budget[j] < T ? budget[j] : T;
+        }
+        if (acc > INT32_MAX) return fail(ECOKV_EINVAL, "index count overflows int32");
+    }
+    *total = acc;
+    return ECOKV_OK;
+}
+
+// The table of pairs lh0 .. lh0+n-1 (n <= kLhChunk) whose entries start at
+// idx offset e0; returns the offset just past them.
+int64_t fill_lhtab(const ecokv_shape *sh, int B, const int32_t *budget, int64_t lh0, int n, int64_t e0,
+                   ecokv::LhTab *t)
+{
+    t->lh0 = (int)lh0;
+    t->n = n;
+    int64_t e = e0;
+    for (int j = 0; j < n; ++j) {
+        const int b = budget[lh0 + j];
+        t->b[j] = b;
+        t->start[j] = (int)e;
+        for (int s = 0; s < B; ++s) {
+            const int T = sh->cu_seqlens[s + 1] - sh->cu_seqlens[s];
+            e += b < T ? b : T;
+        }
+    }
+    t->start[n] = (int)e;
+    return e;
+}
+
 int hip_fail(hipError_t e, const char *what)
 {
     return fail(ECOKV_EHIP, "%s: %s", what, hipGetErrorString(e));
@@ -291,17 +331,60 @@ int ecokv_index_count(const ecokv_shape *shape, const int32_t *budget, int64_t *
     return ECOKV_OK;
 }
 
+int ecokv_index_count_mode(const ecokv_shape *shape, int mode, const int32_t *budget, int64_t *count)
+{
+    if (mode == ECOKV_PER_HEAD || mode == ECOKV_LAYER_FLAT) return ecokv_index_count(shape, budget, count);
+    if (mode != ECOKV_HEAD_BUDGETS) return fail(ECOKV_EINVAL, "mode %d", mode);
+    ShapeInfo si;
+    int rc = check_shape(shape, &si);
+    if (rc) return rc;
+    if ((!budget && (int64_t)si.L * si.Hkv > 0) || !count) return fail(ECOKV_EINVAL, "budget and count must be non-NULL");
+    int64_t total = 0;
+    if ((rc = head_budget_total(shape, si, budget, &total))) return rc;
+    *count = total;
+    return ECOKV_OK;
+}
+
 int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const int32_t *budget, int32_t *idx,
                  int32_t *counts, int32_t *offsets, void *stream)
 {
     ShapeInfo si;
     int rc = check_shape(shape, &si);
     if (rc) return rc;
-    if (mode != ECOKV_PER_HEAD && mode != ECOKV_LAYER_FLAT) return fail(ECOKV_EINVAL, "mode %d", mode);
-    if (!budget) return fail(ECOKV_EINVAL, "budget is NULL");
+    if (mode != ECOKV_PER_HEAD && mode != ECOKV_LAYER_FLAT && mode != ECOKV_HEAD_BUDGETS)
+        return fail(ECOKV_EINVAL, "mode %d", mode);
+    if (!budget && (mode != ECOKV_HEAD_BUDGETS || (int64_t)si.L * si.Hkv > 0))
+        return fail(ECOKV_EINVAL, "budget is NULL");
     ecokv::SelectArgs a;
     memset(&a, 0, sizeof a);
     int64_t per_lh = 0;
+    if (mode == ECOKV_HEAD_BUDGETS) {
+        int64_t total = 0;
+        if ((rc = head_budget_total(shape, si, budget, &total))) return rc;
+        if ((rc = fill_seqtab(shape, nullptr, si.w, &a.seq, &per_lh))) return rc;
+        if (si.L == 0) return ECOKV_OK;
+        if (!scores || !idx) return fail(ECOKV_EINVAL, "scores and idx must be non-NULL");
+        a.scores = scores;
+        a.idx = idx;
+        a.counts = counts;
+        a.offsets = offsets;
+        a.L = si.L;
+        a.Hkv = si.Hkv;
+        a.B = si.B;
+        a.w = si.w;
+        a.Ptot = si.Ptot;
+        a.heads = 1;
+        // one launch per kLhChunk (layer, head) pairs, each with its table
+        const int64_t npairs = (int64_t)si.L * si.Hkv;
+        int64_t e0 = 0;
+        for (int64_t lh0 = 0; lh0 < npairs; lh0 += ecokv::kLhChunk) {
+            const int n = (int)(npairs - lh0 < ecokv::kLhChunk ? npairs - lh0 : ecokv::kLhChunk);
+            e0 = fill_lhtab(shape, si.B, budget, lh0, n, e0, &a.lht);
+            const hipError_t e = ecokv::select_launch(a, static_cast<hipStream_t>(stream));
+            if (e != hipSuccess) return hip_fail(e, "ecokv_select launch");
+        }
+        return ECOKV_OK;
+    }
     if ((rc = fill_seqtab(shape, budget, si.w, &a.seq, &per_lh))) return rc;
     if ((int64_t)si.L * si.Hkv * per_lh > INT32_MAX) return fail(ECOKV_EINVAL, "index count overflows int32");
     if (mode == ECOKV_LAYER_FLAT) {
@@ -335,11 +418,42 @@ int ecokv_compact(const void *K, const void *V, int dtype, const ecokv_shape *sh
     int rc = check_shape(shape, &si);
     if (rc) return rc;
     if (dtype != ECOKV_BF16 && dtype != ECOKV_F32) return fail(ECOKV_EUNSUPPORTED, "dtype %d", dtype);
-    if (mode != ECOKV_PER_HEAD && mode != ECOKV_LAYER_FLAT) return fail(ECOKV_EINVAL, "mode %d", mode);
-    if (!budget) return fail(ECOKV_EINVAL, "budget is NULL");
+    if (mode != ECOKV_PER_HEAD && mode != ECOKV_LAYER_FLAT && mode != ECOKV_HEAD_BUDGETS)
+        return fail(ECOKV_EINVAL, "mode %d", mode);
+    if (!budget && (mode != ECOKV_HEAD_BUDGETS || (int64_t)si.L * si.Hkv > 0))
+        return fail(ECOKV_EINVAL, "budget is NULL");
     ecokv::CompactArgs a;
     memset(&a, 0, sizeof a);
     int64_t per_lh = 0;
+    if (mode == ECOKV_HEAD_BUDGETS) {
+        int64_t total = 0;
+        if ((rc = head_budget_total(shape, si, budget, &total))) return rc;
+        if ((rc = fill_seqtab(shape, nullptr, si.w, &a.seq, &per_lh))) return rc;
+        if (si.L == 0) return ECOKV_OK;
+        if (!K || !V || !idx || !Kc || !Vc) return fail(ECOKV_EINVAL, "K, V, idx, Kc and Vc must be non-NULL");
+        a.K = static_cast<const char *>(K);
+        a.V = static_cast<const char *>(V);
+        a.Kc = static_cast<char *>(Kc);
+        a.Vc = static_cast<char *>(Vc);
+        a.idx = idx;
+        a.L = si.L;
+        a.Hkv = si.Hkv;
+        a.B = si.B;
+        a.heads = 1;
+        a.Ttot = si.Ttot;
+        a.row_bytes = si.D * (dtype == ECOKV_BF16 ? 2 : 4);
+        a.segs = a.row_bytes / 16;
+        const int64_t npairs = (int64_t)si.L * si.Hkv;
+        int64_t e0 = 0;
+        for (int64_t lh0 = 0; lh0 < npairs; lh0 += ecokv::kLhChunk) {
+            const int n = (int)(npairs - lh0 < ecokv::kLhChunk ? npairs - lh0 : ecokv::kLhChunk);
+            a.e0 = e0;
+            a.total = e0 = fill_lhtab(shape, si.B, budget, lh0, n, e0, &a.lht);
+            const hipError_t e = ecokv::compact_launch(a, static_cast<hipStream_t>(stream));
+            if (e != hipSuccess) return hip_fail(e, "ecokv_compact launch");
+        }
+        return ECOKV_OK;
+    }
     if ((rc = fill_seqtab(shape, budget, si.w, &a.seq, &per_lh))) return rc;
     if (mode == ECOKV_LAYER_FLAT && !offsets) return fail(ECOKV_EINVAL, "LAYER_FLAT needs offsets");
     (void)counts;
@@ -362,6 +476,27 @@ int ecokv_compact(const void *K, const void *V, int dtype, const ecokv_shape *sh
     a.per_lh = per_lh;
     const hipError_t e = ecokv::compact_launch(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "ecokv_compact launch");
+    return ECOKV_OK;
+}
+
+int ecokv_pyramid_budgets(int num_layers, double total, double beta, int window, int32_t *out)
+{
+    if (num_layers < 1 || !out) return fail(ECOKV_EINVAL, "num_layers %d < 1 or out is NULL", num_layers);
+    if (!(isfinite(total) && total > 0.0) || !(isfinite(beta) && beta > 0.0))
+        return fail(ECOKV_EINVAL, "total %g and beta %g must be positive and finite", total, beta);
+    if (window < 1) return fail(ECOKV_EINVAL, "window %d < 1", window);
+    const int m = num_layers;
+    const double last = total / (beta * m), first = 2.0 * total / m - last;
+    // every value checked before any is written
+    for (int pass = 0; pass < 2; ++pass)
+        for (int l = 0; l < m; ++l) {
+            const double v = m == 1 ? total : first - (first - last) * l / (m - 1);
+            // rounded down; a value within 1e-9 below an integer is that integer
+            const double f = floor(v + 1e-9);
+            if (pass == 0 && !(f >= window && f <= (double)INT32_MAX))
+                return fail(ECOKV_EINVAL, "layer %d budget %g is outside [window %d, INT32_MAX]", l, v, window);
+            if (pass == 1) out[l] = (int32_t)f;
+        }
     return ECOKV_OK;
 }
 

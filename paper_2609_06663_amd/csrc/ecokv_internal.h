@@ -70,6 +70,24 @@ struct ScoreArgs {
     SeqTab seq;
 };
 
+// Budgets of up to kLhChunk (layer, KV head) pairs, passed by value to one
+// launch (ECOKV_HEAD_BUDGETS): pair lh0 + j keeps min(b[j], T_s) tokens of
+// sequence s, and its entries start at idx offset start[j] (start[n] = end).
+constexpr int kLhChunk = 256;
+struct LhTab {
+    int lh0, n;
+    int b[kLhChunk];
+    int start[kLhChunk + 1];
+};
+
+// Entries of pair j of `t` before sequence s, and min(b, T_s).
+__device__ __forceinline__ int lh_seq_offset(const LhTab &t, const SeqTab &q, int j, int s)
+{
+    int o = 0;
+    for (int r = 0; r < s; ++r) o += min(t.b[j], q.cu[r + 1] - q.cu[r]);
+    return o;
+}
+
 struct SelectArgs {
     const float *scores;
     int32_t *idx;
@@ -77,9 +95,11 @@ struct SelectArgs {
     int32_t *offsets;
     int L, Hkv, B, w;
     int64_t Ptot;
-    int64_t per_lh;  // sum over s of min(b_s, T_s)
+    int64_t per_lh;  // sum over s of min(b_s, T_s) (not ECOKV_HEAD_BUDGETS)
     int flat;
+    int heads;       // ECOKV_HEAD_BUDGETS: budgets and starts from lht
     SeqTab seq;
+    LhTab lht;
 };
 
 struct CompactArgs {
@@ -90,12 +110,15 @@ struct CompactArgs {
     const int32_t *idx;
     const int32_t *offsets;
     int L, Hkv, B, flat;
+    int heads;         // ECOKV_HEAD_BUDGETS: entries [e0, total) of the pairs in lht
     int64_t Ttot;
     int row_bytes;
     int segs;          // row_bytes / 16
-    int64_t total;     // entries
+    int64_t e0;        // first entry of this launch
+    int64_t total;     // one past its last entry
     int64_t per_lh;
     SeqTab seq;
+    LhTab lht;
 };
 
 // Workspace layout, shared by the size query and the launcher.

@@ -85,6 +85,44 @@ struct GroupView {
 
 constexpr int kLdsKeys = 38912;  // keys kept in LDS by the resident variant (152 KiB)
 
+// The selection group of this block: layer l, heads h0 .. h0+nh-1 of
+// sequence s, min(budget, T_s) entries per head, first entry at out_base.
+struct SelGroup {
+    int l, h0, s, nh, beff;
+    int64_t out_base;
+};
+__device__ __forceinline__ SelGroup sel_group(const SelectArgs &a)
+{
+    SelGroup g;
+    if (a.heads) {
+        // one unit per block, (layer, head) pair lh0 + j of the launch's table
+        const int j = blockIdx.x / a.B;
+        g.s = blockIdx.x - j * a.B;
+        const int lh = a.lht.lh0 + j;
+        g.l = lh / a.Hkv;
+        g.h0 = lh - g.l * a.Hkv;
+        g.nh = 1;
+        g.beff = min(a.lht.b[j], a.seq.cu[g.s + 1] - a.seq.cu[g.s]);
+        g.out_base = a.lht.start[j] + lh_seq_offset(a.lht, a.seq, j, g.s);
+    } else if (a.flat) {
+        g.l = blockIdx.x / a.B;
+        g.s = blockIdx.x % a.B;
+        g.h0 = 0;
+        g.nh = a.Hkv;
+        g.beff = a.seq.beff[g.s];
+        g.out_base = (int64_t)g.l * a.Hkv * a.per_lh + (int64_t)a.Hkv * a.seq.boff[g.s];
+    } else {
+        const Unit un = unit_of(blockIdx.x, a.Hkv, a.B);
+        g.l = un.l;
+        g.s = un.s;
+        g.h0 = un.h;
+        g.nh = 1;
+        g.beff = a.seq.beff[g.s];
+        g.out_base = ((int64_t)g.l * a.Hkv + g.h0) * a.per_lh + a.seq.boff[g.s];
+    }
+    return g;
+}
+
 template <bool RESIDENT>
 struct KeySource {
     const GroupView &g;
@@ -207,24 +245,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a)
     __shared__ uint32_t mm[2][kSelWaves];
     __shared__ int64_t through[kMaxFlatHeads];
 
-    int l, h0, s, nh;
-    if (a.flat) {
-        l = blockIdx.x / a.B;
-        s = blockIdx.x % a.B;
-        h0 = 0;
-        nh = a.Hkv;
-    } else {
-        const Unit un = unit_of(blockIdx.x, a.Hkv, a.B);
-        l = un.l;
-        s = un.s;
-        h0 = un.h;
-        nh = 1;
-    }
+    const SelGroup grp = sel_group(a);
+    const int l = grp.l, h0 = grp.h0, s = grp.s, nh = grp.nh;
     const int T = a.seq.cu[s + 1] - a.seq.cu[s];
     const int P = T - a.w;
-    const int beff = a.seq.beff[s];
-    const int64_t out_base = a.flat ? ((int64_t)l * a.Hkv * a.per_lh + (int64_t)a.Hkv * a.seq.boff[s])
-                                    : (((int64_t)l * a.Hkv + h0) * a.per_lh + a.seq.boff[s]);
+    const int beff = grp.beff;
+    const int64_t out_base = grp.out_base;
     int32_t *out = a.idx + out_base;
 
     if (beff >= T) {  // keep every token
@@ -351,24 +377,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
     // KPT == 32: the stage of the coalesced score load, then of the output
     __shared__ u32x4_t stg[KPT == 32 ? KPT / 4 * kSelThreads : 1];
 
-    int l, h0, s, nh;
-    if (a.flat) {
-        l = blockIdx.x / a.B;
-        s = blockIdx.x % a.B;
-        h0 = 0;
-        nh = a.Hkv;
-    } else {
-        const Unit un = unit_of(blockIdx.x, a.Hkv, a.B);
-        l = un.l;
-        s = un.s;
-        h0 = un.h;
-        nh = 1;
-    }
+    const SelGroup grp = sel_group(a);
+    const int l = grp.l, h0 = grp.h0, s = grp.s, nh = grp.nh;
     const int T = a.seq.cu[s + 1] - a.seq.cu[s];
     const int P = T - a.w;
-    const int beff = a.seq.beff[s];
-    const int64_t out_base = a.flat ? ((int64_t)l * a.Hkv * a.per_lh + (int64_t)a.Hkv * a.seq.boff[s])
-                                    : (((int64_t)l * a.Hkv + h0) * a.per_lh + a.seq.boff[s]);
+    const int beff = grp.beff;
+    const int64_t out_base = grp.out_base;
     int32_t *out = a.idx + out_base;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
 
@@ -584,7 +598,9 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
 
 hipError_t select_launch(const SelectArgs &a, hipStream_t st)
 {
-    const unsigned groups = a.flat ? (unsigned)(a.L * a.B) : (unsigned)(a.L * a.Hkv * a.B);
+    const unsigned groups = a.heads  ? (unsigned)(a.lht.n * a.B)
+                            : a.flat ? (unsigned)(a.L * a.B)
+                                     : (unsigned)(a.L * a.Hkv * a.B);
     // largest group: every head's non-window keys in layer-flat mode
     int64_t maxn = 0;
     for (int s = 0; s < a.B; ++s) {

@@ -19,14 +19,15 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libecokv.s
 
 OK, EINVAL, EWORKSPACE, EUNSUPPORTED, EHIP = 0, -1, -2, -3, -4
 BF16, F32 = 0, 1
-PER_HEAD, LAYER_FLAT = 0, 1
+PER_HEAD, LAYER_FLAT, HEAD_BUDGETS = 0, 1, 2
 MAX_SEQS, MAX_ROWS = 64, 64
 NSTATS = 12
 STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7, imp_mean=8, sbar_mean=9,
             mu_norm2=10, scale=11)
 
 EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_score", "ecokv_index_count",
-           "ecokv_select", "ecokv_compact", "ecokv_last_error", "ecokv_stage_times"]
+           "ecokv_index_count_mode", "ecokv_select", "ecokv_compact", "ecokv_pyramid_budgets",
+           "ecokv_last_error", "ecokv_stage_times"]
 
 
 class _StageTime(ctypes.Structure):
@@ -81,6 +82,8 @@ def _load():
     lib.ecokv_workspace_size.argtypes = [sp, pp, ctypes.POINTER(ctypes.c_size_t)]
     lib.ecokv_score.argtypes = [vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_index_count.argtypes = [sp, i32p, ctypes.POINTER(ctypes.c_int64)]
+    lib.ecokv_index_count_mode.argtypes = [sp, ctypes.c_int, i32p, ctypes.POINTER(ctypes.c_int64)]
+    lib.ecokv_pyramid_budgets.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_int, i32p]
     lib.ecokv_select.argtypes = [vp, sp, ctypes.c_int, i32p, vp, vp, vp, vp]
     lib.ecokv_compact.argtypes = [vp, vp, ctypes.c_int, sp, ctypes.c_int, i32p, vp, vp, vp, vp, vp, vp]
     lib.ecokv_last_error.restype = ctypes.c_char_p
@@ -121,10 +124,27 @@ def _stream(stream) -> ctypes.c_void_p:
     return ctypes.c_void_p(stream.cuda_stream)
 
 
-def _budget(shape: Shape, budget: Sequence[int]):
-    if len(budget) != shape.c.num_seqs:
-        raise ValueError("one budget per sequence")
-    return (ctypes.c_int32 * len(budget))(*[int(b) for b in budget])
+def _flat_ints(x) -> list:
+    if hasattr(x, "reshape"):  # numpy array or tensor
+        x = x.reshape(-1).tolist()
+    out = []
+    for v in x:
+        if isinstance(v, (list, tuple)):
+            out.extend(_flat_ints(v))
+        else:
+            out.append(int(v))
+    return out
+
+
+def _budget(shape: Shape, budget, mode: int = PER_HEAD):
+    """Host budget array: one per sequence, or [L][H_kv] for HEAD_BUDGETS."""
+    vals = _flat_ints(budget)
+    c = shape.c
+    n = c.num_layers * c.num_kv_heads if mode == HEAD_BUDGETS else c.num_seqs
+    if len(vals) != n:
+        raise ValueError("HEAD_BUDGETS takes one budget per (layer, KV head)" if mode == HEAD_BUDGETS
+                         else "one budget per sequence")
+    return (ctypes.c_int32 * max(n, 1))(*vals)
 
 
 def ecokv_default_params() -> Params:
@@ -161,20 +181,33 @@ def ecokv_index_count(shape: Shape, budget: Sequence[int]) -> int:
     return n.value
 
 
-def ecokv_select(scores: torch.Tensor, shape: Shape, mode: int, budget: Sequence[int], idx: torch.Tensor,
+def ecokv_index_count_mode(shape: Shape, mode: int, budget) -> int:
+    n = ctypes.c_int64(0)
+    _check(lib.ecokv_index_count_mode(ctypes.byref(shape.c), int(mode), _budget(shape, budget, mode),
+                                      ctypes.byref(n)))
+    return n.value
+
+
+def ecokv_pyramid_budgets(num_layers: int, total: float, beta: float, window: int) -> list:
+    out = (ctypes.c_int32 * max(int(num_layers), 1))()
+    _check(lib.ecokv_pyramid_budgets(int(num_layers), float(total), float(beta), int(window), out))
+    return [int(v) for v in out[:num_layers]]
+
+
+def ecokv_select(scores: torch.Tensor, shape: Shape, mode: int, budget, idx: torch.Tensor,
                  counts: Optional[torch.Tensor] = None, offsets: Optional[torch.Tensor] = None,
                  stream=None) -> None:
-    _check(lib.ecokv_select(_ptr(scores), ctypes.byref(shape.c), int(mode), _budget(shape, budget), _ptr(idx),
-                            _ptr(counts), _ptr(offsets), _stream(stream)))
+    _check(lib.ecokv_select(_ptr(scores), ctypes.byref(shape.c), int(mode), _budget(shape, budget, mode),
+                            _ptr(idx), _ptr(counts), _ptr(offsets), _stream(stream)))
 
 
-def ecokv_compact(K: torch.Tensor, V: torch.Tensor, shape: Shape, mode: int, budget: Sequence[int],
+def ecokv_compact(K: torch.Tensor, V: torch.Tensor, shape: Shape, mode: int, budget,
                   idx: torch.Tensor, counts: Optional[torch.Tensor], offsets: Optional[torch.Tensor],
                   Kc: torch.Tensor, Vc: torch.Tensor, stream=None) -> None:
     if V.dtype != K.dtype or Kc.dtype != K.dtype or Vc.dtype != K.dtype:
         raise TypeError("K, V, Kc and Vc must share one element type")
     _check(lib.ecokv_compact(_ptr(K), _ptr(V), _dtype_code(K), ctypes.byref(shape.c), int(mode),
-                             _budget(shape, budget), _ptr(idx), _ptr(counts), _ptr(offsets), _ptr(Kc),
+                             _budget(shape, budget, mode), _ptr(idx), _ptr(counts), _ptr(offsets), _ptr(Kc),
                              _ptr(Vc), _stream(stream)))
 
 

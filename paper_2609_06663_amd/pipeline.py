@@ -6,7 +6,7 @@ benchmark times.  All arithmetic happens inside libecokv.
 """
 from __future__ import annotations
 
-from typing import Optional, Sequence
+from typing import Optional
 
 import torch
 
@@ -14,10 +14,10 @@ from . import ecokv as E
 
 
 class EvictionPass:
-    def __init__(self, shape: E.Shape, budget: Sequence[int], mode: int = E.PER_HEAD,
+    def __init__(self, shape: E.Shape, budget, mode: int = E.PER_HEAD,
                  params: Optional[E.Params] = None, dtype: torch.dtype = torch.bfloat16,
                  device: str = "cuda"):
-        self.shape, self.budget, self.mode = shape, list(budget), mode
+        self.shape, self.budget, self.mode = shape, E._flat_ints(budget), mode
         self.params = params or E.Params()
         c = shape.c
         L, Hkv, D, w, B = c.num_layers, c.num_kv_heads, c.head_dim, c.window, c.num_seqs
@@ -29,7 +29,7 @@ class EvictionPass:
         self.stats = torch.empty(U * E.NSTATS, dtype=torch.float32, device=device)
         ws = E.ecokv_workspace_size(shape, self.params)
         self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
-        self.n_idx = E.ecokv_index_count(shape, self.budget)
+        self.n_idx = E.ecokv_index_count_mode(shape, mode, self.budget)
         self.idx = torch.empty(max(self.n_idx, 1), dtype=torch.int32, device=device)
         self.counts = torch.empty(max(U, 1), dtype=torch.int32, device=device)
         self.offsets = torch.empty(max(U, 1), dtype=torch.int32, device=device)

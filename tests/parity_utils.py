@@ -39,14 +39,16 @@ def host_bits(t: torch.Tensor) -> np.ndarray:
     return t.numpy()
 
 
-def gpu_pass(wl: W.Workload, params=None, mode=None):
-    """Run score -> select -> compact through the C ABI; returns numpy outputs."""
+def gpu_pass(wl: W.Workload, params=None, mode=None, budget=None):
+    """Run score -> select -> compact through the C ABI; returns numpy outputs.
+    `budget` overrides the workload's per-sequence budgets (e.g. [L][Hkv]
+    budgets with mode HEAD_BUDGETS)."""
     import paper_2609_06663_amd as P
     from paper_2609_06663_amd.pipeline import EvictionPass
     shape = P.Shape(wl.L, wl.Hq, wl.Hkv, wl.D, wl.w, wl.cu_seqlens)
     m = mode if mode is not None else (P.LAYER_FLAT if wl.mode == "layer_flat" else P.PER_HEAD)
     tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
-    ep = EvictionPass(shape, wl.budget, m, params or P.Params(), tdt)
+    ep = EvictionPass(shape, wl.budget if budget is None else budget, m, params or P.Params(), tdt)
     K, V, Q = dev(wl.K, wl.dtype), dev(wl.V, wl.dtype), dev(wl.Q, wl.dtype)
     ep.run(K, V, Q)
     torch.cuda.synchronize()

@@ -128,3 +128,57 @@ def test_empty_call_is_ok_without_device(P):
     p = P.Params()
     rc = E.lib.ecokv_score(None, None, 0, ctypes.byref(s.c), ctypes.byref(p), None, None, None, None, 0, None)
     assert rc == 0
+
+
+@pytest.mark.parametrize("m", [1, 2, 3, 4, 5, 7, 28, 32, 80])
+@pytest.mark.parametrize("total,beta", [(4096, 2.0), (1000, 4.0), (183484, 20.0), (1234.5, 2.5), (900, 1.5),
+                                        (4096, 1.0), (300, 0.75)])
+def test_pyramid_budgets_match_oracle(P, m, total, beta):
+    import oracle
+    want = oracle.pyramid_budgets(m, total, beta)
+    w = 4
+    if min(want) < w:
+        with pytest.raises(P.EcoKVError) as e:
+            P.ecokv_pyramid_budgets(m, total, beta, w)
+        assert e.value.code == -1
+    else:
+        assert P.ecokv_pyramid_budgets(m, total, beta, w) == want
+
+
+@pytest.mark.parametrize("args", [(0, 100.0, 2.0, 1), (3, 0.0, 2.0, 1), (3, 100.0, -1.0, 1), (3, float("nan"), 2.0, 1),
+                                  (3, 100.0, 2.0, 0), (2, 1e12, 2.0, 1)])
+def test_pyramid_budgets_rejects(P, args):
+    with pytest.raises(P.EcoKVError) as e:
+        P.ecokv_pyramid_budgets(*args)
+    assert e.value.code == -1
+
+
+def test_head_budget_index_count(P):
+    import oracle
+    cu = [0, 10, 25, 27]
+    s = P.Shape(2, 6, 3, 128, 1, cu)
+    bud = [[1, 5, 30], [10, 15, 2]]
+    want = oracle.index_count(2, 3, cu, bud, oracle.HEAD_BUDGETS)
+    assert want == sum(min(b, T) for row in bud for b in row for T in (10, 15, 2))
+    assert P.ecokv_index_count_mode(s, P.HEAD_BUDGETS, bud) == want
+    assert P.ecokv_index_count_mode(s, P.PER_HEAD, [3, 4, 1]) == P.ecokv_index_count(s, [3, 4, 1])
+    with pytest.raises(ValueError):
+        P.ecokv_index_count_mode(s, P.HEAD_BUDGETS, [1, 2, 3])   # one per sequence is the wrong shape
+    with pytest.raises(P.EcoKVError):
+        P.ecokv_index_count_mode(s, 7, [1, 2, 3])
+
+
+def test_head_budget_calls_fail_before_device_work(P):
+    from paper_2609_06663_amd import ecokv as E
+    s = P.Shape(2, 4, 2, 128, 4, [0, 100])
+    lib = E.lib
+    fake = ctypes.c_void_p(256)
+    bud = (ctypes.c_int32 * 4)(10, 20, 3, 50)   # pair (1, 0) below the window
+    assert lib.ecokv_select(fake, ctypes.byref(s.c), 2, bud, fake, None, None, None) == -1
+    assert "below the window" in P.ecokv_last_error()
+    assert lib.ecokv_compact(fake, fake, 0, ctypes.byref(s.c), 2, bud, fake, None, None, fake, fake, None) == -1
+    bud = (ctypes.c_int32 * 4)(10, 20, 30, 50)
+    assert lib.ecokv_select(None, ctypes.byref(s.c), 2, bud, fake, None, None, None) == -1   # NULL scores
+    assert lib.ecokv_compact(fake, None, 0, ctypes.byref(s.c), 2, bud, fake, None, None, fake, fake, None) == -1
+    s0 = P.Shape(0, 4, 2, 128, 4, [0, 100])
+    assert lib.ecokv_select(None, ctypes.byref(s0.c), 2, None, None, None, None, None) == 0   # nothing to do

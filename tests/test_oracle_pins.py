@@ -491,3 +491,78 @@ def test_tiny_regression_fixture(ora):
         np.testing.assert_allclose(st[0, h, 0], gh["stats"], rtol=1e-12)
         np.testing.assert_allclose(S[0, h, gh["score_positions"]], gh["scores"], rtol=1e-12)
         np.testing.assert_array_equal(idx[offsets[0, h, 0]:offsets[0, h, 0] + counts[0, h, 0]], gh["selected"])
+
+
+# --------------------------------------------------------------------------
+# Budgets per (layer, KV head) (PyramidKV layer schedule, SparseMM head
+# budgets, Appendix A.1)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(4))
+def test_select_head_budgets_matches_brute_force(ora, seed):
+    r = np.random.default_rng(300 + seed)
+    L, Hkv, w = int(r.integers(1, 4)), int(r.integers(1, 4)), int(r.integers(1, 3))
+    lens = [int(x) for x in r.integers(w + 1, 40, size=int(r.integers(1, 4)))]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    B = len(lens)
+    Ptot = int(cu[-1]) - B * w
+    S = r.integers(0, 6, size=(L, Hkv, Ptot)).astype(np.float64)  # many exact ties
+    bud = r.integers(w, max(lens) + 3, size=(L, Hkv)).astype(np.int32)
+    bud[0, 0] = w                       # the window only
+    idx, counts, offsets = ora.select(S, L, Hkv, cu, w, bud, ora.HEAD_BUDGETS)
+    o = 0
+    for l in range(L):
+        for h in range(Hkv):
+            for s, T in enumerate(lens):
+                b, P = int(bud[l, h]), T - w
+                n = min(b, T)
+                assert offsets[l, h, s] == o and counts[l, h, s] == n
+                got = idx[o:o + n]
+                if b >= T:
+                    np.testing.assert_array_equal(got, np.arange(T))
+                else:
+                    Su = S[l, h, cu[s] - s * w: cu[s] - s * w + P]
+                    np.testing.assert_array_equal(got, list(brute_topk(Su, b - w)) + list(range(P, T)))
+                o += n
+    assert o == len(idx) == ora.index_count(L, Hkv, cu, bud, ora.HEAD_BUDGETS)
+
+
+def test_select_head_budgets_rejects_budget_below_window(ora):
+    with pytest.raises(ValueError):
+        ora.select(np.zeros((1, 2, 8)), 1, 2, [0, 10], 2, [[3, 1]], ora.HEAD_BUDGETS)
+
+
+# Schedules worked by hand from the formulas of Appendix A.1 (PyramidKV):
+# b^{m-1} = total/(beta m), b^0 = 2 total/m - b^{m-1}, straight line between.
+#  m=4, total=4096, beta=2:  b^3 = 512, b^0 = 1536, step 1024/3:
+#                            1194.67 -> 1194, 853.33 -> 853
+#  m=5, total=1000, beta=4:  b^4 = 50, b^0 = 350, step 75 (sum exactly 1000)
+#  m=3, total=900, beta=1.5: b^2 = 200, b^0 = 400, step 100
+#  m=3, total=100, beta=3:   b^2 = 100/9 -> 11, b^0 = 500/9 -> 55, 300/9 -> 33
+#  m=1:                      the whole total
+#  beta=1:                   b^{m-1} = b^0 = total/m, a flat schedule
+PYRAMID_CASES = [
+    (4, 4096, 2.0, [1536, 1194, 853, 512]),
+    (5, 1000, 4.0, [350, 275, 200, 125, 50]),
+    (3, 900, 1.5, [400, 300, 200]),
+    (3, 100, 3.0, [55, 33, 11]),
+    (1, 777, 3.0, [777]),
+    (4, 4096, 1.0, [1024, 1024, 1024, 1024]),
+]
+
+
+@pytest.mark.parametrize("m,total,beta,want", PYRAMID_CASES)
+def test_pyramid_schedule_worked_examples(ora, m, total, beta, want):
+    assert ora.pyramid_budgets(m, total, beta) == want
+
+
+@pytest.mark.parametrize("m,total,beta", [(28, 28 * 6553, 20.0), (32, 32 * 128, 20.0), (7, 1234.5, 2.5)])
+def test_pyramid_schedule_properties(ora, m, total, beta):
+    b = ora.pyramid_budgets(m, total, beta)
+    assert len(b) == m
+    # the two ends of the schedule (before rounding down)
+    assert b[-1] == math.floor(total / (beta * m))
+    assert abs(b[0] - (2 * total / m - total / (beta * m))) < 1
+    # non-increasing for beta >= 1, the sum within m of the total, never above
+    assert all(x >= y for x, y in zip(b, b[1:]))
+    assert total - m < sum(b) <= total
