@@ -53,7 +53,7 @@ STAGE_KERNELS = {
     "sweep1_stream": ["k_fs1s"], "sweep1_block": ["k_fs1", "k_pass1"], "reduce1": ["k_reduce1"],
     "sweep2_stream": ["k_fs2s"], "sweep2_block": ["k_fs2", "k_pass2"], "epilogue": ["k_epi_unit"],
     "epilogue1": ["k_epi1"], "epilogue2": ["k_epi2"], "single_read": ["k_fused"],
-    "select": ["k_select_reg", "k_select"], "compact": ["k_compact"],
+    "select": ["k_select_reg", "k_select"], "compact": ["k_compact"], "vnorm": ["k_vnorm"],
 }
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, vendor figure
 COPY_BYTES = 1 << 30  # size of the calibration copy in --counter-run
@@ -266,6 +266,39 @@ def main():
     head_budgets["compact_algorithmic_bytes"] = h_gather
     head_budgets["compact_GBs"] = round(h_gather / (head_budgets["compact_ms"] / 1e3) / 1e9, 1)
 
+    # Value-norm importance (S_imp = pooled attention x |v_i|_2): the score
+    # call with V, on the same stack; one extra pass reads V.
+    log("value-norm importance")
+    pv = P.Params(imp_mode=P.IMP_ATTN_VNORM)
+    ws_v = torch.empty(P.ecokv_workspace_size(shape, pv), dtype=torch.uint8, device=dev)
+
+    def score_v():
+        P.ecokv_score_v(K, V, Q, shape, pv, ep.scores, ep.lambda_, ep.stats, ws_v)
+
+    score_v()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        score_v()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    os.environ["ECOKV_STAGE_TIMING"] = "1"
+    P.ecokv_stage_times()
+    for _ in range(args.steps):
+        score_v()
+    torch.cuda.synchronize()
+    vstages = P.ecokv_stage_times()
+    os.environ["ECOKV_STAGE_TIMING"] = "0"
+    del ws_v
+    bytes_v = L * Hkv * P_ * D * e  # the non-window value rows
+    vn_s = vstages["vnorm"][0] / vstages["vnorm"][1] / 1e3
+    value_norm = {"score_ms": round(e0.elapsed_time(e1) / args.steps, 4),
+                  "score_ms_attention_only": round(per_call_ms["score"], 4),
+                  "vnorm_kernel_us": round(vn_s * 1e6, 2),
+                  "vnorm_algorithmic_bytes": bytes_v + 2 * bytes_scores,
+                  "vnorm_GBs": round((bytes_v + 2 * bytes_scores) / vn_s / 1e9, 1)}
+
     extras = {}
     if args.extras:
         for frac in (0.1, 0.4):
@@ -333,6 +366,7 @@ def main():
         "kernels": kernels,
         "mfma_window_gemm": mfma,
         "head_budgets": head_budgets,
+        "value_norm": value_norm,
     }
     if extras:
         out["extras"] = extras

@@ -69,6 +69,9 @@ extern "C" {
                              /* schedule and SparseMM's head budgets assign   */
                              /* them (App. A.1)                               */
 
+#define ECOKV_IMP_ATTN 0       /* S_imp: pooled window-mean attention (SnapKV)   */
+#define ECOKV_IMP_ATTN_VNORM 1 /* S_imp: that times |v_i|_2 (Sec. 5.2; VNorm)    */
+
 #define ECOKV_MAX_SEQS 64   /* sequences per call                              */
 #define ECOKV_MAX_ROWS 64   /* window rows per KV head, (H_q/H_kv)*w           */
 
@@ -109,15 +112,18 @@ typedef struct ecokv_params {
     int32_t pool_kernel;    /* odd average-pool width for S_imp; 5                */
     int32_t causal;         /* 1: window row j sees keys <= T-w+j; 0: all keys    */
     float lambda_override;  /* NaN: lambda from Eq. (6); else this fixed value    */
+    int32_t imp_mode;       /* ECOKV_IMP_ATTN or ECOKV_IMP_ATTN_VNORM             */
 } ecokv_params;
 
 /* Fills *p with the paper's defaults: alpha 0.8, beta 0.6, eps 1e-6,
- * tau sqrt(D), pool 5, causal, no override.  Returns ECOKV_OK. */
+ * tau sqrt(D), pool 5, causal, no override, ECOKV_IMP_ATTN.  Returns ECOKV_OK. */
 int ecokv_default_params(ecokv_params *p);
 
-/* Bytes of device workspace ecokv_score needs for this shape (select and
- * compact need none).  The workspace is scratch: its contents are undefined
- * between calls and it must not be shared by calls that may overlap. */
+/* Bytes of device workspace ecokv_score / ecokv_score_v need for this shape
+ * and these parameters (select and compact need none; ECOKV_IMP_ATTN_VNORM
+ * adds one float per non-window key).  The workspace is scratch: its contents
+ * are undefined between calls and it must not be shared by calls that may
+ * overlap. */
 int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, size_t *bytes);
 
 /* Score every unit (Sec. 3 and Sec. 5, Eqs. (1)-(7)).
@@ -140,10 +146,23 @@ int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, s
  * blocks.  That kernel needs all of its blocks resident at once (two per
  * compute unit): it must not share the device with another running launch of
  * it.  If a wait between its blocks ever times out, lambda and the scores of
- * the launch come out NaN. */
+ * the launch come out NaN.
+ * params->imp_mode must be ECOKV_IMP_ATTN here (the value norm needs V:
+ * ecokv_score_v). */
 int ecokv_score(const void *K, const void *Q_win, int dtype, const ecokv_shape *shape,
                 const ecokv_params *params, float *scores, float *lambda, float *stats,
                 void *workspace, size_t workspace_bytes, void *stream);
+
+/* ecokv_score with the values V [L][H_kv][Ttot][D] (element type `dtype`).
+ * With params->imp_mode == ECOKV_IMP_ATTN_VNORM the importance of key i < P
+ * combines the l2 norm of its value vector with the window-mean attention
+ * (Sec. 5.2; VNorm, Sec. 2) as the product S_imp(i) = pool(a)(i) * |v_i|_2
+ * (the pooled attention times the norm; the norm is not pooled); V is read
+ * once, in one extra pass over the non-window rows.  With ECOKV_IMP_ATTN, V
+ * is not read and may be NULL. */
+int ecokv_score_v(const void *K, const void *V, const void *Q_win, int dtype, const ecokv_shape *shape,
+                  const ecokv_params *params, float *scores, float *lambda, float *stats,
+                  void *workspace, size_t workspace_bytes, void *stream);
 
 /* Number of int32 entries ecokv_select writes to idx:
  * L * H_kv * sum_s min(budget[s], T_s) (ECOKV_PER_HEAD and ECOKV_LAYER_FLAT). */

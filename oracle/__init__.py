@@ -29,6 +29,7 @@ NSTATS = 12
 STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7,
             imp_mean=8, sbar_mean=9, mu_norm2=10, scale=11)
 PER_HEAD, LAYER_FLAT, HEAD_BUDGETS = 0, 1, 2
+IMP_ATTN, IMP_ATTN_VNORM = 0, 1
 BF16, F32 = 0, 1
 
 
@@ -45,7 +46,7 @@ def build(force: bool = True) -> str:
 class _Params(ctypes.Structure):
     _fields_ = [("alpha", ctypes.c_double), ("beta", ctypes.c_double), ("eps", ctypes.c_double),
                 ("tau", ctypes.c_double), ("pool_kernel", ctypes.c_int), ("causal", ctypes.c_int),
-                ("lambda_override", ctypes.c_double)]
+                ("lambda_override", ctypes.c_double), ("imp_mode", ctypes.c_int)]
 
 
 _TRACE_FIELDS = ["a", "imp", "dE", "cosmu", "sC", "sE", "sdiv", "sbar", "stilde", "kbar", "mu", "rowmass"]
@@ -64,10 +65,11 @@ class Params:
     pool_kernel: int = 5          # Table 6
     causal: bool = True
     lambda_override: float = math.nan
+    imp_mode: int = IMP_ATTN       # IMP_ATTN_VNORM: times the value norm (Sec. 5.2)
 
     def c(self) -> _Params:
         return _Params(self.alpha, self.beta, self.eps, self.tau, int(self.pool_kernel),
-                       int(bool(self.causal)), self.lambda_override)
+                       int(bool(self.causal)), self.lambda_override, int(self.imp_mode))
 
 
 _lib = None
@@ -80,11 +82,12 @@ def lib():
             build(force=False)
         L = ctypes.CDLL(_LIB)
         vp, i32p, dp = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)
-        L.ora_score_unit.argtypes = [vp, vp, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-                                     ctypes.c_int, ctypes.c_int, ctypes.POINTER(_Params), dp, dp,
-                                     ctypes.POINTER(_Trace)]
-        L.ora_score.argtypes = [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-                                i32p, ctypes.c_int, ctypes.c_int, ctypes.POINTER(_Params), dp, dp, ctypes.c_int]
+        L.ora_score_unit_v.argtypes = [vp, vp, vp, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                       ctypes.c_int, ctypes.c_int, ctypes.POINTER(_Params), dp, dp,
+                                       ctypes.POINTER(_Trace)]
+        L.ora_score_v.argtypes = [vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                  ctypes.c_int, i32p, ctypes.c_int, ctypes.c_int, ctypes.POINTER(_Params), dp,
+                                  dp, ctypes.c_int]
         L.ora_select_unit.argtypes = [dp, ctypes.c_int, ctypes.c_int, ctypes.c_int, i32p]
         L.ora_select_flat.argtypes = [dp, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                       ctypes.c_int, i32p, i32p]
@@ -113,11 +116,12 @@ def _dtype_code(a: np.ndarray) -> int:
 
 
 def score_unit(K: np.ndarray, Q: np.ndarray, w: int, params: Optional[Params] = None,
-               trace: bool = False) -> dict:
+               trace: bool = False, V: Optional[np.ndarray] = None) -> dict:
     """Score one (layer, KV head, sequence) unit.
 
     K: [T, D] keys (uint16 bf16 bits or float32).  Q: [G, w, D] window queries of
-    the G query heads sharing this KV head.  Returns ``S`` [P] (float64),
+    the G query heads sharing this KV head.  V: [T, D] values of the unit's
+    tokens (needed with imp_mode IMP_ATTN_VNORM).  Returns ``S`` [P] (float64),
     ``stats`` [NSTATS] and, with ``trace``, every intermediate of the paper's
     steps (a, imp, dE, cosmu, sC, sE, sdiv, sbar, stilde, kbar, mu, rowmass).
     """
@@ -142,28 +146,35 @@ def score_unit(K: np.ndarray, Q: np.ndarray, w: int, params: Optional[Params] = 
         tr_ptr = ctypes.byref(tr)
         out.update(arrs)
     pc = p.c()
-    rc = lib().ora_score_unit(K.ctypes.data, Q.ctypes.data, w * D, code, T, D, G, w, ctypes.byref(pc),
-                              _dp(S), _dp(stats), tr_ptr)
+    if V is not None:
+        V = np.ascontiguousarray(V)
+        assert V.shape == K.shape and _dtype_code(V) == code
+    rc = lib().ora_score_unit_v(K.ctypes.data, None if V is None else V.ctypes.data, Q.ctypes.data, w * D,
+                                code, T, D, G, w, ctypes.byref(pc), _dp(S), _dp(stats), tr_ptr)
     if rc != 0:
         raise ValueError(f"oracle rejected the unit (rc={rc})")
     return out
 
 
-def score(K, Q, L, Hq, Hkv, cu_seqlens, D, w, params: Optional[Params] = None, nthreads: int = 1):
-    """Score every unit.  K [L][Hkv][Ttot][D], Q [L][Hq][B][w][D].
+def score(K, Q, L, Hq, Hkv, cu_seqlens, D, w, params: Optional[Params] = None, nthreads: int = 1, V=None):
+    """Score every unit.  K [L][Hkv][Ttot][D], Q [L][Hq][B][w][D], V like K
+    (needed with imp_mode IMP_ATTN_VNORM).
 
     Returns S [L][Hkv][Ptot] (float64) and stats [L][Hkv][B][NSTATS]."""
     p = params or Params()
     K = np.ascontiguousarray(K)
     Q = np.ascontiguousarray(Q)
+    if V is not None:
+        V = np.ascontiguousarray(V)
+        assert V.shape == K.shape and V.dtype == K.dtype
     cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
     B = len(cu) - 1
     Ptot = int(cu[-1]) - B * w
     S = np.zeros((L, Hkv, Ptot), np.float64)
     stats = np.zeros((L, Hkv, B, NSTATS), np.float64)
     pc = p.c()
-    rc = lib().ora_score(K.ctypes.data, Q.ctypes.data, _dtype_code(K), L, Hq, Hkv, B, _ip(cu), D, w,
-                         ctypes.byref(pc), _dp(S), _dp(stats), nthreads)
+    rc = lib().ora_score_v(K.ctypes.data, None if V is None else V.ctypes.data, Q.ctypes.data, _dtype_code(K),
+                           L, Hq, Hkv, B, _ip(cu), D, w, ctypes.byref(pc), _dp(S), _dp(stats), nthreads)
     if rc != 0:
         raise ValueError(f"oracle rejected the shape (rc={rc})")
     return S, stats

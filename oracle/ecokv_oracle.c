@@ -61,6 +61,7 @@ typedef struct {
     int pool_kernel;         /* average-pool width (odd), 5 in Table 6            */
     int causal;              /* window query j sees keys <= P + j                 */
     double lambda_override;  /* NaN: use Eq. (6); else use this value (tests)     */
+    int imp_mode;            /* 0: S_imp = pooled attention; 1: times |v_i|_2     */
 } ora_params;
 
 /* Optional per-unit intermediates (any pointer may be NULL). */
@@ -93,17 +94,19 @@ static double ora_get(const void *base, int dtype, size_t i)
 /*
  * Score one (layer, KV head, sequence) unit.
  *   K: T x D rows of this unit (element type dtype).
+ *   V: T x D value rows of this unit; read only when p->imp_mode == 1.
  *   Q: the window queries of the G query heads mapped to this KV head; query
  *      head g, window row j is at Q + (g * q_gstride + j * D) elements.
  *   S: [P] output scores, P = T - w.   stats: [ORA_NSTATS] output.
  * Returns 0, or -1 on invalid sizes.
  */
-int ora_score_unit(const void *K, const void *Q, size_t q_gstride, int dtype,
-                   int T, int D, int G, int w, const ora_params *p,
-                   double *S, double *stats, const ora_trace *tr)
+int ora_score_unit_v(const void *K, const void *V, const void *Q, size_t q_gstride, int dtype,
+                     int T, int D, int G, int w, const ora_params *p,
+                     double *S, double *stats, const ora_trace *tr)
 {
     if (T < 2 || w < 1 || w >= T || D < 1 || G < 1 || p->pool_kernel < 1 || (p->pool_kernel % 2) == 0)
         return -1;
+    if (p->imp_mode != 0 && (p->imp_mode != 1 || !V)) return -1;
     const int P = T - w;
     const double inv_sqrt_d = 1.0 / sqrt((double)D);
 
@@ -163,6 +166,21 @@ int ora_score_unit(const void *K, const void *Q, size_t q_gstride, int dtype,
         for (int t = -half; t <= half; ++t)
             if (i + t >= 0 && i + t < P) acc += a[i + t];
         imp[i] = acc / (double)p->pool_kernel;
+    }
+
+    /* Step 3'. Value-norm importance (imp_mode 1): the importance combines the
+     * l2 norm of the value vector with the window-mean attention (Sec. 5.2;
+     * VNorm, Sec. 2).  Reading: the product of the pooled attention and
+     * |v_i|_2; the norm is not pooled. */
+    if (p->imp_mode == 1) {
+        for (int i = 0; i < P; ++i) {
+            double n2 = 0.0;
+            for (int d = 0; d < D; ++d) {
+                const double v = ora_get(V, dtype, (size_t)i * D + d);
+                n2 += v * v;
+            }
+            imp[i] *= sqrt(n2);
+        }
     }
 
     /* Step 4. Anchors over all T keys: the centroid kbar (Eq. (1)) and the mean
@@ -290,6 +308,13 @@ int ora_score_unit(const void *K, const void *Q, size_t q_gstride, int dtype,
     return 0;
 }
 
+int ora_score_unit(const void *K, const void *Q, size_t q_gstride, int dtype,
+                   int T, int D, int G, int w, const ora_params *p,
+                   double *S, double *stats, const ora_trace *tr)
+{
+    return ora_score_unit_v(K, NULL, Q, q_gstride, dtype, T, D, G, w, p, S, stats, tr);
+}
+
 /* ---------------------------------------------------------------------------
  * Selection (Sec. 3): the k = b - w highest-scoring non-window tokens plus the
  * whole window.  Reading: equal scores rank the smaller position first; the
@@ -392,9 +417,9 @@ int ora_select_flat(const double *S, size_t hstride, int H, int T, int w, int b,
  *   S      [L][Hkv][Ptot]      Ptot = Ttot - B*w; sequence s at cu[s] - s*w
  *   stats  [L][Hkv][B][ORA_NSTATS]
  * ------------------------------------------------------------------------- */
-int ora_score(const void *K, const void *Q, int dtype, int L, int Hq, int Hkv, int B,
-              const int32_t *cu, int D, int w, const ora_params *p,
-              double *S, double *stats, int nthreads)
+int ora_score_v(const void *K, const void *V, const void *Q, int dtype, int L, int Hq, int Hkv, int B,
+                const int32_t *cu, int D, int w, const ora_params *p,
+                double *S, double *stats, int nthreads)
 {
     if (L < 0 || Hkv < 1 || Hq % Hkv != 0 || B < 1) return -1;
     const int G = Hq / Hkv;
@@ -411,14 +436,23 @@ int ora_score(const void *K, const void *Q, int dtype, int L, int Hq, int Hkv, i
         const int h = (int)((u / B) % Hkv);
         const int l = (int)(u / ((int64_t)B * Hkv));
         const int T = cu[s + 1] - cu[s];
-        const char *Ku = (const char *)K + (((size_t)l * Hkv + h) * (size_t)Ttot + (size_t)cu[s]) * (size_t)D * es;
+        const size_t krow = ((size_t)l * Hkv + h) * (size_t)Ttot + (size_t)cu[s];
+        const char *Ku = (const char *)K + krow * (size_t)D * es;
+        const char *Vu = V ? (const char *)V + krow * (size_t)D * es : NULL;
         const char *Qu = (const char *)Q + ((((size_t)l * Hq + (size_t)h * G) * B + s) * (size_t)w * D) * es;
         double *Su = S + ((size_t)l * Hkv + h) * (size_t)Ptot + (size_t)(cu[s] - s * w);
         double *st = stats ? stats + (size_t)u * ORA_NSTATS : NULL;
-        if (ora_score_unit(Ku, Qu, (size_t)B * w * D, dtype, T, D, G, w, p, Su, st, NULL) != 0) bad = 1;
+        if (ora_score_unit_v(Ku, Vu, Qu, (size_t)B * w * D, dtype, T, D, G, w, p, Su, st, NULL) != 0) bad = 1;
     }
     (void)nthreads;
     return bad ? -1 : 0;
+}
+
+int ora_score(const void *K, const void *Q, int dtype, int L, int Hq, int Hkv, int B,
+              const int32_t *cu, int D, int w, const ora_params *p,
+              double *S, double *stats, int nthreads)
+{
+    return ora_score_v(K, NULL, Q, dtype, L, Hq, Hkv, B, cu, D, w, p, S, stats, nthreads);
 }
 
 /* idx layout: PER_HEAD -- unit (l, h, s) owns min(b_s, T_s) entries, units in

@@ -79,6 +79,8 @@ int check_params(const ecokv_params *p)
         return fail(ECOKV_EINVAL, "pool_kernel %d must be odd and >= 1", p->pool_kernel);
     if (p->causal != 0 && p->causal != 1) return fail(ECOKV_EINVAL, "causal must be 0 or 1");
     if (isinf(p->lambda_override)) return fail(ECOKV_EINVAL, "lambda_override must be NaN or finite");
+    if (p->imp_mode != ECOKV_IMP_ATTN && p->imp_mode != ECOKV_IMP_ATTN_VNORM)
+        return fail(ECOKV_EINVAL, "imp_mode %d", p->imp_mode);
     return ECOKV_OK;
 }
 
@@ -245,6 +247,7 @@ int ecokv_default_params(ecokv_params *p)
     p->pool_kernel = 5;
     p->causal = 1;
     p->lambda_override = NAN;
+    p->imp_mode = ECOKV_IMP_ATTN;
     return ECOKV_OK;
 }
 
@@ -259,8 +262,9 @@ int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, s
         return fail(ECOKV_EUNSUPPORTED, "(H_q/H_kv)*window = %d exceeds %d", si.R, ECOKV_MAX_ROWS);
     *bytes = 0;  // the size depends on the element type; report the larger layout
     {
-        const size_t b0 = ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, true).total;
-        const size_t b1 = ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, false).total;
+        const bool vn = params->imp_mode == ECOKV_IMP_ATTN_VNORM;
+        const size_t b0 = ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, true, vn).total;
+        const size_t b1 = ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, false, vn).total;
         *bytes = b0 > b1 ? b0 : b1;
     }
     return ECOKV_OK;
@@ -268,6 +272,16 @@ int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, s
 
 int ecokv_score(const void *K, const void *Q_win, int dtype, const ecokv_shape *shape, const ecokv_params *params,
                 float *scores, float *lambda, float *stats, void *workspace, size_t workspace_bytes, void *stream)
+{
+    if (params && params->imp_mode != ECOKV_IMP_ATTN)
+        return fail(ECOKV_EINVAL, "imp_mode %d needs the values: use ecokv_score_v", params->imp_mode);
+    return ecokv_score_v(K, nullptr, Q_win, dtype, shape, params, scores, lambda, stats, workspace,
+                         workspace_bytes, stream);
+}
+
+int ecokv_score_v(const void *K, const void *V, const void *Q_win, int dtype, const ecokv_shape *shape,
+                  const ecokv_params *params, float *scores, float *lambda, float *stats, void *workspace,
+                  size_t workspace_bytes, void *stream)
 {
     ShapeInfo si;
     int rc = check_shape(shape, &si);
@@ -278,8 +292,10 @@ int ecokv_score(const void *K, const void *Q_win, int dtype, const ecokv_shape *
         return fail(ECOKV_EUNSUPPORTED, "(H_q/H_kv)*window = %d exceeds %d", si.R, ECOKV_MAX_ROWS);
     if (si.L == 0) return ECOKV_OK;
     if (!K || !Q_win || !scores) return fail(ECOKV_EINVAL, "K, Q_win and scores must be non-NULL");
+    const bool vnorm = params->imp_mode == ECOKV_IMP_ATTN_VNORM;
+    if (vnorm && !V) return fail(ECOKV_EINVAL, "imp_mode ECOKV_IMP_ATTN_VNORM needs V");
     const ecokv::WsLayout lay =
-        ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, dtype == ECOKV_BF16);
+        ecokv::score_ws_layout(si.L, si.Hkv, si.B, si.D, si.R, si.Ptot, si.maxT, dtype == ECOKV_BF16, vnorm);
     if (!workspace) return fail(ECOKV_EINVAL, "workspace is NULL");
     if (((uintptr_t)workspace & 255u) != 0) return fail(ECOKV_EINVAL, "workspace must be 256-byte aligned");
     if (workspace_bytes < lay.total)
@@ -288,6 +304,8 @@ int ecokv_score(const void *K, const void *Q_win, int dtype, const ecokv_shape *
     ecokv::ScoreArgs a;
     memset(&a, 0, sizeof a);
     a.K = K;
+    a.V = vnorm ? V : nullptr;
+    a.vnorm = vnorm ? 1 : 0;
     a.Q = Q_win;
     a.scores = scores;
     a.lambda = lambda;

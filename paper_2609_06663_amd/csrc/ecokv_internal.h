@@ -36,6 +36,7 @@ __device__ __forceinline__ Unit unit_of(int u, int Hkv, int B)
 
 struct ScoreArgs {
     const void *K;
+    const void *V;   // values, read only with the value-norm importance (vnorm)
     const void *Q;
     float *scores;
     float *lambda;
@@ -48,6 +49,7 @@ struct ScoreArgs {
     float *bufA;     // [L][Hkv][Ptot]      d_E
     float *bufB;     // [L][Hkv][Ptot]      khat.mu
     float *bufC;     // [L][Hkv][Ptot]      window-mean attention a
+    float *bufV;     // [L][Hkv][Ptot]      pool(a) * |v| (vnorm only)
     // single-read score path only: values published between blocks, each a
     // 64-bit word (launch tag << 32 | float bits) so that a reader can tell a
     // value of this launch from anything older without ordering fences
@@ -67,6 +69,7 @@ struct ScoreArgs {
     int rpb2;        // key rows per sweep-2 block
     float alpha, beta, eps, tau, inv_sqrt_d, lambda_override;
     int use_override, pool_half, causal;
+    int vnorm;       // S_imp = pool(a) * |v_i|_2
     SeqTab seq;
 };
 
@@ -123,10 +126,10 @@ struct CompactArgs {
 
 // Workspace layout, shared by the size query and the launcher.
 struct WsLayout {
-    size_t part1, anchors, part2, part3, bufA, bufB, bufC, partT, ancT, epiT, status, total;
+    size_t part1, anchors, part2, part3, bufA, bufB, bufC, bufV, partT, ancT, epiT, status, total;
 };
 
-WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16);
+WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16, bool vnorm);
 hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hipStream_t st, bool bf16);
 
 // Single-read score path (bf16, head_dim 128, G*w <= 28): eligibility for a

@@ -1652,7 +1652,77 @@ bool score_fast_path(int D, bool bf16) { return bf16 && D == fast::kD; }
 
 static int rows_per_block(int D, bool bf16) { return score_fast_path(D, bf16) ? fast::kRows : kCh; }
 
-WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16)
+// ---------------------------------------------------------------------------
+// Value-norm importance (ECOKV_IMP_ATTN_VNORM, Sec. 5.2): S_imp(i) =
+// pool(a)(i) * |v_i|_2 for the non-window keys, in one coalesced pass over V.
+// A wave takes 64 consecutive rows; its load instruction q covers the 16-byte
+// pieces 64q .. 64q+63 of those rows (SEGS pieces per row), so consecutive
+// lanes read consecutive bytes.  The SEGS partial sums of squares of a row
+// are combined by shuffles and parked in LDS; lane r then pools the window
+// attention around row r (zero padding, fixed divisor, as the epilogue) and
+// writes the product.  Rows at or past P read as zero (buffer range).
+// ---------------------------------------------------------------------------
+constexpr int kVnThreads = 256;
+
+template <bool BF16, int SEGS>
+__global__ __launch_bounds__(kVnThreads) void k_vnorm(ScoreArgs a)
+{
+    __shared__ float n2s[kVnThreads];
+    constexpr int kRowBytes = SEGS * 16;
+    const int u = blockIdx.y;
+    const Unit un = unit_of(u, a.Hkv, a.B);
+    const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
+    const int P = T - a.w;
+    const int row0 = blockIdx.x * kVnThreads;
+    if (row0 >= P) return;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int wrow = row0 + 64 * wv;                      // the wave's first row
+    const int nrows = max(0, min(64, P - wrow));          // rows of the wave below P
+    const char *vw = static_cast<const char *>(a.V) + (unit_row0(a, un) + wrow) * kRowBytes;
+    const __amdgpu_buffer_rsrc_t rv =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(vw), (short)0, nrows * kRowBytes, 0x00020000);
+    u32x4 x[SEGS];
+#pragma unroll
+    for (int q = 0; q < SEGS; ++q)
+        x[q] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, (64 * q + lane) * 16, 0, 0));
+#pragma unroll
+    for (int q = 0; q < SEGS; ++q) {
+        float s2 = 0.f;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            if (BF16) {
+                const float lo = __uint_as_float(x[q][c] << 16), hi = __uint_as_float(x[q][c] & 0xffff0000u);
+                s2 += lo * lo + hi * hi;
+            } else {
+                const float v = __uint_as_float(x[q][c]);
+                s2 += v * v;
+            }
+        }
+#pragma unroll
+        for (int m = 1; m < SEGS; m <<= 1) s2 += __shfl_xor(s2, m, kWave);
+        if (lane % SEGS == 0) n2s[64 * wv + (64 / SEGS) * q + lane / SEGS] = s2;
+    }
+    __syncthreads();
+    const int i = wrow + lane;
+    if (i < P) {
+        const int64_t ob = unit_out_base(a, un);
+        const float *att = a.bufC + ob;
+        float acc = 0.f;
+        for (int t = -a.pool_half; t <= a.pool_half; ++t)
+            if (i + t >= 0 && i + t < P) acc += att[i + t];
+        a.bufV[ob + i] = acc * (1.f / (float)(2 * a.pool_half + 1)) * sqrtf(n2s[threadIdx.x]);
+    }
+}
+
+static void launch_vnorm(const ScoreArgs &a, dim3 grid, hipStream_t st, bool bf16)
+{
+    if (bf16 && a.D == 64) hipLaunchKernelGGL((k_vnorm<true, 8>), grid, dim3(kVnThreads), 0, st, a);
+    else if (bf16) hipLaunchKernelGGL((k_vnorm<true, 16>), grid, dim3(kVnThreads), 0, st, a);
+    else if (a.D == 64) hipLaunchKernelGGL((k_vnorm<false, 16>), grid, dim3(kVnThreads), 0, st, a);
+    else hipLaunchKernelGGL((k_vnorm<false, 32>), grid, dim3(kVnThreads), 0, st, a);
+}
+
+WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16, bool vnorm)
 {
     WsLayout w{};
     const int64_t U = (int64_t)L * Hkv * B;
@@ -1672,6 +1742,7 @@ WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int 
     w.bufA = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
     w.bufB = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
     w.bufC = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
+    w.bufV = o; o = align256(o + (vnorm ? sizeof(float) * (int64_t)L * Hkv * Ptot : 0));
     w.partT = o; o = align256(o + sizeof(unsigned long long) * U * stride * nchf);
     w.ancT = o; o = align256(o + (single ? sizeof(unsigned long long) * U * stride : 0));
     w.epiT = o; o = align256(o + sizeof(unsigned long long) * U * 2 * 4);
@@ -1792,6 +1863,16 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
             ECOKV_TIMED("sweep2_block", st, launch_sweep(2, a, grid, st, bf16));
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (a.vnorm) {
+        // the importance with the value norm; the epilogue then reads it as
+        // its (already pooled) importance
+        a.bufV = reinterpret_cast<float *>(ws + lay.bufV);
+        const dim3 gv((maxT - a.w + kVnThreads - 1) / kVnThreads, U);
+        ECOKV_TIMED("vnorm", st, launch_vnorm(a, gv, st, bf16));
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        a.bufC = a.bufV;
+        a.pool_half = 0;
     }
     if (maxT - a.w <= kUKeys && a.pool_half <= kPoolHalfMax && (maxT + a.rpb2 - 1) / a.rpb2 <= kUThreads && a.D <= kUThreads) {
         // two blocks per unit when all of them can be resident at once (their

@@ -20,12 +20,13 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libecokv.s
 OK, EINVAL, EWORKSPACE, EUNSUPPORTED, EHIP = 0, -1, -2, -3, -4
 BF16, F32 = 0, 1
 PER_HEAD, LAYER_FLAT, HEAD_BUDGETS = 0, 1, 2
+IMP_ATTN, IMP_ATTN_VNORM = 0, 1
 MAX_SEQS, MAX_ROWS = 64, 64
 NSTATS = 12
 STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7, imp_mean=8, sbar_mean=9,
             mu_norm2=10, scale=11)
 
-EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_score", "ecokv_index_count",
+EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_score", "ecokv_score_v", "ecokv_index_count",
            "ecokv_index_count_mode", "ecokv_select", "ecokv_compact", "ecokv_pyramid_budgets",
            "ecokv_last_error", "ecokv_stage_times"]
 
@@ -51,11 +52,12 @@ class Params(ctypes.Structure):
     """ecokv_params; defaults are the paper's (Table 6)."""
     _fields_ = [("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("eps", ctypes.c_float),
                 ("tau", ctypes.c_float), ("pool_kernel", ctypes.c_int32), ("causal", ctypes.c_int32),
-                ("lambda_override", ctypes.c_float)]
+                ("lambda_override", ctypes.c_float), ("imp_mode", ctypes.c_int32)]
 
     def __init__(self, alpha=0.8, beta=0.6, eps=1e-6, tau=0.0, pool_kernel=5, causal=True,
-                 lambda_override=math.nan):
-        super().__init__(alpha, beta, eps, tau, int(pool_kernel), int(bool(causal)), lambda_override)
+                 lambda_override=math.nan, imp_mode=IMP_ATTN):
+        super().__init__(alpha, beta, eps, tau, int(pool_kernel), int(bool(causal)), lambda_override,
+                         int(imp_mode))
 
 
 class Shape:
@@ -81,6 +83,7 @@ def _load():
     lib.ecokv_default_params.argtypes = [pp]
     lib.ecokv_workspace_size.argtypes = [sp, pp, ctypes.POINTER(ctypes.c_size_t)]
     lib.ecokv_score.argtypes = [vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.ecokv_score_v.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_index_count.argtypes = [sp, i32p, ctypes.POINTER(ctypes.c_int64)]
     lib.ecokv_index_count_mode.argtypes = [sp, ctypes.c_int, i32p, ctypes.POINTER(ctypes.c_int64)]
     lib.ecokv_pyramid_budgets.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_int, i32p]
@@ -173,6 +176,21 @@ def ecokv_score(K: torch.Tensor, Q_win: torch.Tensor, shape: Shape, params: Opti
     _check(lib.ecokv_score(_ptr(K), _ptr(Q_win), _dtype_code(K), ctypes.byref(shape.c), ctypes.byref(p),
                            _ptr(scores), _ptr(lambda_), _ptr(stats), _ptr(workspace),
                            workspace.numel(), _stream(stream)))
+
+
+def ecokv_score_v(K: torch.Tensor, V: Optional[torch.Tensor], Q_win: torch.Tensor, shape: Shape,
+                  params: Optional[Params], scores: torch.Tensor, lambda_: Optional[torch.Tensor] = None,
+                  stats: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                  stream=None) -> None:
+    """Enqueue ecokv_score_v (V is read with imp_mode IMP_ATTN_VNORM)."""
+    p = params or Params()
+    if workspace is None:
+        workspace = torch.empty(ecokv_workspace_size(shape, p), dtype=torch.uint8, device=K.device)
+    if Q_win.dtype != K.dtype or (V is not None and V.dtype != K.dtype):
+        raise TypeError("K, V and Q_win must have the same element type")
+    _check(lib.ecokv_score_v(_ptr(K), _ptr(V), _ptr(Q_win), _dtype_code(K), ctypes.byref(shape.c),
+                             ctypes.byref(p), _ptr(scores), _ptr(lambda_), _ptr(stats), _ptr(workspace),
+                             workspace.numel(), _stream(stream)))
 
 
 def ecokv_index_count(shape: Shape, budget: Sequence[int]) -> int:

@@ -36,9 +36,13 @@ class EvictionPass:
         self.Kc = torch.empty((max(self.n_idx, 1), D), dtype=dtype, device=device)
         self.Vc = torch.empty((max(self.n_idx, 1), D), dtype=dtype, device=device)
 
-    def score(self, K: torch.Tensor, Q_win: torch.Tensor, stream=None):
-        E.ecokv_score(K, Q_win, self.shape, self.params, self.scores, self.lambda_, self.stats,
-                      self.workspace, stream)
+    def score(self, K: torch.Tensor, Q_win: torch.Tensor, stream=None, V: Optional[torch.Tensor] = None):
+        if self.params.imp_mode == E.IMP_ATTN_VNORM:
+            E.ecokv_score_v(K, V, Q_win, self.shape, self.params, self.scores, self.lambda_, self.stats,
+                            self.workspace, stream)
+        else:
+            E.ecokv_score(K, Q_win, self.shape, self.params, self.scores, self.lambda_, self.stats,
+                          self.workspace, stream)
 
     def select(self, stream=None):
         E.ecokv_select(self.scores, self.shape, self.mode, self.budget, self.idx, self.counts,
@@ -49,7 +53,7 @@ class EvictionPass:
                         self.Kc, self.Vc, stream)
 
     def run(self, K: torch.Tensor, V: torch.Tensor, Q_win: torch.Tensor, stream=None):
-        self.score(K, Q_win, stream)
+        self.score(K, Q_win, stream, V)
         self.select(stream)
         self.compact(K, V, stream)
         return self

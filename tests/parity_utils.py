@@ -74,7 +74,8 @@ def oracle_params(p=None):
     return oracle.Params(alpha=float(np.float32(p.alpha)), beta=float(np.float32(p.beta)),
                          eps=float(np.float32(p.eps)), tau=float(np.float32(p.tau)),
                          pool_kernel=int(p.pool_kernel), causal=bool(p.causal),
-                         lambda_override=lo if not math.isnan(lo) else math.nan)
+                         lambda_override=lo if not math.isnan(lo) else math.nan,
+                         imp_mode=int(p.imp_mode))
 
 
 def unit_slices(wl: W.Workload, s: int):
@@ -88,7 +89,8 @@ def oracle_unit(wl: W.Workload, l: int, h: int, s: int, params=None):
     cu = wl.cu_seqlens
     K = wl.K[l, h, cu[s]:cu[s + 1]]
     Q = wl.Q[l, h * wl.G:(h + 1) * wl.G, s]
-    return oracle.score_unit(K, Q, wl.w, oracle_params(params))
+    V = wl.V[l, h, cu[s]:cu[s + 1]] if params is not None and params.imp_mode else None
+    return oracle.score_unit(K, Q, wl.w, oracle_params(params), V=V)
 
 
 def check_scores(Sg: np.ndarray, So: np.ndarray, imp_mean: float, what: str = ""):

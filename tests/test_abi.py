@@ -182,3 +182,30 @@ def test_head_budget_calls_fail_before_device_work(P):
     assert lib.ecokv_compact(fake, None, 0, ctypes.byref(s.c), 2, bud, fake, None, None, fake, fake, None) == -1
     s0 = P.Shape(0, 4, 2, 128, 4, [0, 100])
     assert lib.ecokv_select(None, ctypes.byref(s0.c), 2, None, None, None, None, None) == 0   # nothing to do
+
+
+def test_value_norm_mode_checks(P):
+    from paper_2609_06663_amd import ecokv as E
+    s = P.Shape(2, 8, 2, 128, 4, [0, 1000])
+    p0, p1 = P.Params(), P.Params(imp_mode=P.IMP_ATTN_VNORM)
+    assert P.ecokv_default_params().imp_mode == P.IMP_ATTN
+    # one float per non-window key of the workspace holds the finished importance
+    assert P.ecokv_workspace_size(s, p1) >= P.ecokv_workspace_size(s, p0) + 4 * 2 * 2 * 996
+    bad = P.Params(imp_mode=5)
+    with pytest.raises(P.EcoKVError):
+        P.ecokv_workspace_size(s, bad)
+    fake = ctypes.c_void_p(256)
+    ws = P.ecokv_workspace_size(s, p1)
+    lib = E.lib
+    # ecokv_score has no V: the value-norm mode is refused there
+    rc = lib.ecokv_score(fake, fake, 0, ctypes.byref(s.c), ctypes.byref(p1), fake, None, None, fake, ws, None)
+    assert rc == -1 and "ecokv_score_v" in P.ecokv_last_error()
+    # ecokv_score_v needs V in that mode
+    rc = lib.ecokv_score_v(fake, None, fake, 0, ctypes.byref(s.c), ctypes.byref(p1), fake, None, None, fake, ws,
+                           None)
+    assert rc == -1
+    # the value-norm workspace is larger
+    ws0 = P.ecokv_workspace_size(s, p0)
+    rc = lib.ecokv_score_v(fake, fake, fake, 0, ctypes.byref(s.c), ctypes.byref(p1), fake, None, None, fake, ws0,
+                           None)
+    assert rc == -2

@@ -566,3 +566,73 @@ def test_pyramid_schedule_properties(ora, m, total, beta):
     # non-increasing for beta >= 1, the sum within m of the total, never above
     assert all(x >= y for x, y in zip(b, b[1:]))
     assert total - m < sum(b) <= total
+
+
+# --------------------------------------------------------------------------
+# Value-norm importance (imp_mode IMP_ATTN_VNORM; Sec. 5.2: the importance
+# combines |v_i|_2 with the window-mean attention; reading: the product,
+# taken after pooling)
+# --------------------------------------------------------------------------
+
+def vnorm_params(**kw):
+    import oracle
+    return oracle.Params(imp_mode=oracle.IMP_ATTN_VNORM, **kw)
+
+
+def test_vnorm_with_unit_values_is_attention_importance(ora):
+    K, Q = rand_unit(50, 60, 16, G=2, w=3)
+    V = np.random.default_rng(51).standard_normal((60, 16))
+    V = f32(V / np.linalg.norm(V, axis=1, keepdims=True))
+    r0 = ora.score_unit(K, Q, 3)
+    r1 = ora.score_unit(K, Q, 3, vnorm_params(), V=V)
+    np.testing.assert_allclose(r1["S"], r0["S"], rtol=1e-6)
+    np.testing.assert_allclose(r1["stats"], r0["stats"], rtol=1e-6)
+
+
+def test_vnorm_closed_form_with_identical_keys(ora):
+    # identical keys: a_i = mean_j 1 / (P + j + 1) for every i < P (pinned
+    # above); a width-5 zero-padded pool gives a_i * (number of in-range
+    # neighbours) / 5, which the value norm then multiplies
+    T, D, G, w = 41, 8, 2, 3
+    K = f32(np.tile(np.linspace(-1, 1, D), (T, 1)))
+    Q = f32(np.random.default_rng(52).standard_normal((G, w, D)))
+    V = f32(np.random.default_rng(53).standard_normal((T, D)) * 3.0)
+    P = T - w
+    r = ora.score_unit(K, Q, w, vnorm_params(), trace=True, V=V)
+    a = np.mean([1.0 / (P + j + 1) for j in range(w)])
+    inrange = np.array([sum(1 for t in range(-2, 3) if 0 <= i + t < P) for i in range(P)])
+    vn = np.sqrt(np.sum(V[:P].astype(np.float64) ** 2, axis=1))
+    np.testing.assert_allclose(r["imp"], a * inrange / 5.0 * vn, rtol=1e-12)
+    assert r["stats"][S_["imp_mean"]] == pytest.approx(np.mean(a * inrange / 5.0 * vn), rel=1e-12)
+
+
+def test_vnorm_scales_with_the_values_and_keeps_the_selection(ora):
+    # lambda does not depend on V; S_imp, the rescaled diversity and S all
+    # scale by c when V does (c = 2: exact in fp32)
+    K, Q = rand_unit(54, 80, 16, G=2, w=2, offset=0.4)
+    V = f32(np.random.default_rng(55).standard_normal((80, 16)))
+    r1 = ora.score_unit(K, Q, 2, vnorm_params(), V=V)
+    r2 = ora.score_unit(K, Q, 2, vnorm_params(), V=f32(2.0 * V))
+    np.testing.assert_allclose(r2["S"], 2.0 * r1["S"], rtol=1e-12)
+    for k in ("lambda_", "rC", "rE", "DE", "sbar_mean"):
+        assert r2["stats"][S_[k]] == pytest.approx(r1["stats"][S_[k]], rel=1e-12)
+    for k in ("imp_mean", "scale"):
+        assert r2["stats"][S_[k]] == pytest.approx(2.0 * r1["stats"][S_[k]], rel=1e-12)
+    np.testing.assert_array_equal(ora.select_unit(r1["S"], 80, 2, 20), ora.select_unit(r2["S"], 80, 2, 20))
+
+
+def test_vnorm_dominant_value_row_is_kept(ora):
+    # with lambda = 0 the score is S_imp; a value row 1000 times longer than
+    # the others makes its key the clear first choice
+    K, Q = rand_unit(56, 50, 16, G=1, w=2)
+    V = f32(np.random.default_rng(57).standard_normal((50, 16)) * 0.01)
+    V[17] *= 1e5
+    r = ora.score_unit(K, Q, 2, vnorm_params(lambda_override=0.0), V=V)
+    assert int(np.argmax(r["S"])) == 17
+    np.testing.assert_array_equal(ora.select_unit(r["S"], 50, 2, 3), [17, 48, 49])
+
+
+def test_vnorm_needs_values(ora):
+    K, Q = rand_unit(58, 20, 8)
+    with pytest.raises(ValueError):
+        ora.score_unit(K, Q, 2, vnorm_params())
