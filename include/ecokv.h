@@ -72,13 +72,27 @@ extern "C" {
 #define ECOKV_IMP_ATTN 0       /* S_imp: pooled window-mean attention (SnapKV)   */
 #define ECOKV_IMP_ATTN_VNORM 1 /* S_imp: that times |v_i|_2 (Sec. 5.2; VNorm)    */
 
+/* Normalisation of d_E into s_E (the Eq. (2) step; Sec. 6.3, Table 4). */
+#define ECOKV_NORM_MINMAX 0  /* (d - min) / (max - min + eps), Eq. (2)           */
+#define ECOKV_NORM_WINSOR 1  /* d clipped to its q and 1-q quantiles, then       */
+                             /* min-max between them                            */
+#define ECOKV_NORM_MAD 2     /* sigmoid((d - median) / (mad_tau * MAD + eps))    */
+
+/* Redundancy in lambda (Eq. (6)). */
+#define ECOKV_RED_EUCLID 0   /* r_E = 2 - 2 sigmoid(D_E / tau), Eq. (5)          */
+#define ECOKV_RED_STD 1      /* r_std = 1 - sigmoid(D_std / tau), Appendix D     */
+
+/* Keys averaged into the centroid kbar (Eq. (1)). */
+#define ECOKV_CENTROID_ALL 0    /* all T keys                                   */
+#define ECOKV_CENTROID_PREFIX 1 /* the P non-window keys (Appendix B.6)         */
+
 #define ECOKV_MAX_SEQS 64   /* sequences per call                              */
 #define ECOKV_MAX_ROWS 64   /* window rows per KV head, (H_q/H_kv)*w           */
 
 /* Per-unit statistics written by ecokv_score when `stats` is non-NULL. */
 #define ECOKV_STAT_LAMBDA 0    /* lambda = beta r_E + (1-beta) r_C, Eq. (6)      */
 #define ECOKV_STAT_RC 1        /* cosine redundancy (T|mu|^2-1)/(T-1), App. A.1  */
-#define ECOKV_STAT_RE 2        /* 2 - 2 sigmoid(D_E/tau), Eq. (5)                */
+#define ECOKV_STAT_RE 2        /* the redundancy in lambda: r_E, Eq. (5), or r_std */
 #define ECOKV_STAT_DE 3        /* mean distance to the centroid, Eq. (4)         */
 #define ECOKV_STAT_DMIN 4      /* min / max of d_E over the non-window keys      */
 #define ECOKV_STAT_DMAX 5
@@ -113,10 +127,23 @@ typedef struct ecokv_params {
     int32_t causal;         /* 1: window row j sees keys <= T-w+j; 0: all keys    */
     float lambda_override;  /* NaN: lambda from Eq. (6); else this fixed value    */
     int32_t imp_mode;       /* ECOKV_IMP_ATTN or ECOKV_IMP_ATTN_VNORM             */
+    int32_t norm_mode;      /* ECOKV_NORM_MINMAX / _WINSOR / _MAD                 */
+    float winsor_q;         /* ECOKV_NORM_WINSOR: lower quantile q in [0, 0.5)    */
+    float mad_tau;          /* ECOKV_NORM_MAD: temperature (> 0); 1               */
+    int32_t redundancy;     /* ECOKV_RED_EUCLID or ECOKV_RED_STD                  */
+    int32_t centroid_scope; /* ECOKV_CENTROID_ALL or ECOKV_CENTROID_PREFIX        */
 } ecokv_params;
 
 /* Fills *p with the paper's defaults: alpha 0.8, beta 0.6, eps 1e-6,
- * tau sqrt(D), pool 5, causal, no override, ECOKV_IMP_ATTN.  Returns ECOKV_OK. */
+ * tau sqrt(D), pool 5, causal, no override, ECOKV_IMP_ATTN, min-max
+ * normalisation (winsor_q 0.01 and mad_tau 1 for the alternatives), r_E, the
+ * centroid over all T keys.  Returns ECOKV_OK.
+ * Quantiles (ECOKV_NORM_WINSOR, ECOKV_NORM_MAD) are taken over the P
+ * non-window keys of a unit, interpolating linearly between the two nearest
+ * order statistics at rank q (P - 1); the median is the 0.5 quantile and MAD
+ * the median of |d_E - median|.  D_std = sqrt(mean over the T keys of
+ * |k - kbar|^2).  With ECOKV_CENTROID_PREFIX only kbar changes (mu, D_E and
+ * D_std still average over all T keys). */
 int ecokv_default_params(ecokv_params *p);
 
 /* Bytes of device workspace ecokv_score / ecokv_score_v need for this shape
@@ -141,7 +168,8 @@ int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, s
  * waits for its partner for seconds (the device taken by other work all that
  * time), that unit's lambda and scores come out NaN.
  * Paths: two sweeps over K (default), or, with the environment variable
- * ECOKV_SCORE_PATH=single (bf16, head_dim 128, (H_q/H_kv)*w <= 28), one
+ * ECOKV_SCORE_PATH=single (bf16, head_dim 128, (H_q/H_kv)*w <= 28, r_E and the
+ * centroid over all T keys), one
  * persistent kernel that reads K once and exchanges per-unit sums between its
  * blocks.  That kernel needs all of its blocks resident at once (two per
  * compute unit): it must not share the device with another running launch of

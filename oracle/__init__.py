@@ -30,6 +30,9 @@ STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7,
             imp_mean=8, sbar_mean=9, mu_norm2=10, scale=11)
 PER_HEAD, LAYER_FLAT, HEAD_BUDGETS = 0, 1, 2
 IMP_ATTN, IMP_ATTN_VNORM = 0, 1
+NORM_MINMAX, NORM_WINSOR, NORM_MAD = 0, 1, 2
+RED_EUCLID, RED_STD = 0, 1
+CENTROID_ALL, CENTROID_PREFIX = 0, 1
 BF16, F32 = 0, 1
 
 
@@ -46,7 +49,9 @@ def build(force: bool = True) -> str:
 class _Params(ctypes.Structure):
     _fields_ = [("alpha", ctypes.c_double), ("beta", ctypes.c_double), ("eps", ctypes.c_double),
                 ("tau", ctypes.c_double), ("pool_kernel", ctypes.c_int), ("causal", ctypes.c_int),
-                ("lambda_override", ctypes.c_double), ("imp_mode", ctypes.c_int)]
+                ("lambda_override", ctypes.c_double), ("imp_mode", ctypes.c_int), ("norm_mode", ctypes.c_int),
+                ("winsor_q", ctypes.c_double), ("mad_tau", ctypes.c_double), ("redundancy", ctypes.c_int),
+                ("centroid_scope", ctypes.c_int)]
 
 
 _TRACE_FIELDS = ["a", "imp", "dE", "cosmu", "sC", "sE", "sdiv", "sbar", "stilde", "kbar", "mu", "rowmass"]
@@ -66,10 +71,17 @@ class Params:
     causal: bool = True
     lambda_override: float = math.nan
     imp_mode: int = IMP_ATTN       # IMP_ATTN_VNORM: times the value norm (Sec. 5.2)
+    norm_mode: int = NORM_MINMAX   # s_E normalisation (Sec. 6.3, Table 4)
+    winsor_q: float = 0.01
+    mad_tau: float = 1.0
+    redundancy: int = RED_EUCLID   # RED_STD: r_std (Appendix D)
+    centroid_scope: int = CENTROID_ALL  # CENTROID_PREFIX: Appendix B.6
 
     def c(self) -> _Params:
         return _Params(self.alpha, self.beta, self.eps, self.tau, int(self.pool_kernel),
-                       int(bool(self.causal)), self.lambda_override, int(self.imp_mode))
+                       int(bool(self.causal)), self.lambda_override, int(self.imp_mode), int(self.norm_mode),
+                       float(self.winsor_q), float(self.mad_tau), int(self.redundancy),
+                       int(self.centroid_scope))
 
 
 _lib = None

@@ -62,6 +62,11 @@ typedef struct {
     int causal;              /* window query j sees keys <= P + j                 */
     double lambda_override;  /* NaN: use Eq. (6); else use this value (tests)     */
     int imp_mode;            /* 0: S_imp = pooled attention; 1: times |v_i|_2     */
+    int norm_mode;           /* s_E: 0 min-max (Eq. (2)), 1 winsorised, 2 MAD     */
+    double winsor_q;         /* winsorised min-max: clip at quantiles q, 1 - q    */
+    double mad_tau;          /* MAD scaling temperature                           */
+    int redundancy;          /* 0: r_E (Eq. (5)); 1: r_std (Appendix D)           */
+    int centroid_scope;      /* 0: kbar over all T keys; 1: over the P non-window */
 } ora_params;
 
 /* Optional per-unit intermediates (any pointer may be NULL). */
@@ -79,6 +84,28 @@ typedef struct {
     double *mu;      /* [D] mean of the normalised keys               */
     double *rowmass; /* [G*w] softmax mass of each window row         */
 } ora_trace;
+
+static int ora_dbl_cmp(const void *x, const void *y)
+{
+    const double a = *(const double *)x, b = *(const double *)y;
+    return a < b ? -1 : (a > b ? 1 : 0);
+}
+
+/* The q quantile of x[0..n) (n >= 1) by linear interpolation between the order
+ * statistics at ranks floor(h) and floor(h) + 1, h = q (n - 1) (the usual
+ * definition, as numpy's default).  Sorts a copy. */
+static double ora_quantile(const double *x, int n, double q)
+{
+    double *c = malloc((size_t)n * sizeof(double));
+    if (!c) return NAN;
+    memcpy(c, x, (size_t)n * sizeof(double));
+    qsort(c, (size_t)n, sizeof(double), ora_dbl_cmp);
+    const double h = q * (double)(n - 1);
+    const int j = (int)floor(h);
+    const double r = j + 1 < n ? c[j] + (h - j) * (c[j + 1] - c[j]) : c[j];
+    free(c);
+    return r;
+}
 
 static double ora_get(const void *base, int dtype, size_t i)
 {
@@ -107,6 +134,9 @@ int ora_score_unit_v(const void *K, const void *V, const void *Q, size_t q_gstri
     if (T < 2 || w < 1 || w >= T || D < 1 || G < 1 || p->pool_kernel < 1 || (p->pool_kernel % 2) == 0)
         return -1;
     if (p->imp_mode != 0 && (p->imp_mode != 1 || !V)) return -1;
+    if (p->norm_mode < 0 || p->norm_mode > 2 || p->redundancy < 0 || p->redundancy > 1 ||
+        p->centroid_scope < 0 || p->centroid_scope > 1)
+        return -1;
     const int P = T - w;
     const double inv_sqrt_d = 1.0 / sqrt((double)D);
 
@@ -200,6 +230,15 @@ int ora_score_unit_v(const void *K, const void *V, const void *Q, size_t q_gstri
         kbar[d] /= (double)T;
         mu[d] /= (double)T;
     }
+    /* Alternative (Appendix B.6): the centroid over the non-window keys only;
+     * mu keeps all T keys (the alternative concerns the Euclidean step). */
+    if (p->centroid_scope == 1) {
+        for (int d = 0; d < D; ++d) {
+            kbar[d] = 0.0;
+            for (int i = 0; i < P; ++i) kbar[d] += ora_get(K, dtype, (size_t)i * D + d);
+            kbar[d] /= (double)P;
+        }
+    }
 
     /* Step 5. Cosine diversity of each non-window key (Appendix A.1, MixKV:
      * negative similarity to mu).  Reading: mapped to [0, 1] as (1 - khat.mu)/2,
@@ -236,7 +275,26 @@ int ora_score_unit_v(const void *K, const void *V, const void *Q, size_t q_gstri
         if (dE[i] < dmin) dmin = dE[i];
         if (dE[i] > dmax) dmax = dE[i];
     }
-    for (int i = 0; i < P; ++i) sE[i] = (dE[i] - dmin) / (dmax - dmin + p->eps);
+    if (p->norm_mode == 0) {
+        for (int i = 0; i < P; ++i) sE[i] = (dE[i] - dmin) / (dmax - dmin + p->eps);
+    } else if (p->norm_mode == 1) {
+        /* Winsorised min-max (Sec. 6.3, Table 4): d_E clipped to its q and
+         * 1 - q quantiles over the non-window keys, then min-max between them. */
+        const double lo = ora_quantile(dE, P, p->winsor_q), hi = ora_quantile(dE, P, 1.0 - p->winsor_q);
+        for (int i = 0; i < P; ++i) {
+            const double c = dE[i] < lo ? lo : (dE[i] > hi ? hi : dE[i]);
+            sE[i] = (c - lo) / (hi - lo + p->eps);
+        }
+    } else {
+        /* Per-head MAD scaling (Sec. 6.3, Table 4), temperature mad_tau.
+         * Reading: the deviation from the median in units of the median
+         * absolute deviation, mapped to (0, 1) by a sigmoid so that it blends
+         * with s_C as the min-max value does. */
+        const double med = ora_quantile(dE, P, 0.5);
+        for (int i = 0; i < P; ++i) sE[i] = fabs(dE[i] - med);  /* the deviations, then s_E */
+        const double mad = ora_quantile(sE, P, 0.5);
+        for (int i = 0; i < P; ++i) sE[i] = 1.0 / (1.0 + exp(-(dE[i] - med) / (p->mad_tau * mad + p->eps)));
+    }
 
     /* Step 8. Mean distance over all T keys, Eq. (4), and the magnitude-aware
      * redundancy r_E = 2 - 2 sigmoid(D_E / tau), Eq. (5), tau = sqrt(d_k). */
@@ -244,7 +302,16 @@ int ora_score_unit_v(const void *K, const void *V, const void *Q, size_t q_gstri
     for (int i = 0; i < T; ++i) DE += dE[i];
     DE /= (double)T;
     const double tau = p->tau > 0.0 ? p->tau : sqrt((double)D);
-    const double rE = 2.0 - 2.0 / (1.0 + exp(-DE / tau));
+    double rE = 2.0 - 2.0 / (1.0 + exp(-DE / tau));
+    if (p->redundancy == 1) {
+        /* Alternative (Appendix D): the standard deviation of the keys,
+         * D_std = sqrt(mean_T |k_i - kbar|^2), and r_std = 1 - sigmoid(D_std / tau)
+         * in place of r_E. */
+        double ss = 0.0;
+        for (int i = 0; i < T; ++i) ss += dE[i] * dE[i];
+        const double Dstd = sqrt(ss / (double)T);
+        rE = 1.0 - 1.0 / (1.0 + exp(-Dstd / tau));
+    }
 
     /* Step 9. Head-adaptive weight, Eq. (6). */
     double lambda = p->beta * rE + (1.0 - p->beta) * rC;

@@ -636,3 +636,87 @@ def test_vnorm_needs_values(ora):
     K, Q = rand_unit(58, 20, 8)
     with pytest.raises(ValueError):
         ora.score_unit(K, Q, 2, vnorm_params())
+
+
+# --------------------------------------------------------------------------
+# Alternatives of Sec. 6.3 (Table 4: winsorised min-max, MAD scaling),
+# Appendix D (r_std) and Appendix B.6 (centroid over the non-window keys)
+# --------------------------------------------------------------------------
+
+def alt_params(**kw):
+    import oracle
+    return oracle.Params(**kw)
+
+
+def test_winsor_at_zero_is_minmax(ora):
+    K, Q = rand_unit(70, 90, 16, G=2, w=3, offset=0.3)
+    r0 = ora.score_unit(K, Q, 3, trace=True)
+    r1 = ora.score_unit(K, Q, 3, alt_params(norm_mode=ora.NORM_WINSOR, winsor_q=0.0), trace=True)
+    np.testing.assert_array_equal(r1["sE"], r0["sE"])
+    np.testing.assert_array_equal(r1["S"], r0["S"])
+
+
+@pytest.mark.parametrize("q,T", [(0.01, 300), (0.05, 300), (0.05, 41), (0.25, 12)])
+def test_winsor_matches_numpy_quantiles(ora, q, T):
+    K, Q = rand_unit(71, T, 16, G=2, w=2, offset=0.2)
+    P = T - 2
+    r = ora.score_unit(K, Q, 2, alt_params(norm_mode=ora.NORM_WINSOR, winsor_q=q), trace=True)
+    d = r["dE"][:P]
+    lo, hi = np.quantile(d, [q, 1 - q])
+    np.testing.assert_allclose(r["sE"], (np.clip(d, lo, hi) - lo) / (hi - lo + 1e-6), rtol=1e-12, atol=1e-15)
+    # the clipped extremes map to 0 and (almost) 1
+    assert r["sE"].min() == 0.0 and abs(r["sE"].max() - (hi - lo) / (hi - lo + 1e-6)) < 1e-12
+
+
+@pytest.mark.parametrize("T,tau", [(200, 1.0), (57, 1.0), (58, 2.5)])
+def test_mad_matches_numpy_median(ora, T, tau):
+    K, Q = rand_unit(72, T, 16, G=1, w=3, offset=0.5)
+    P = T - 3
+    r = ora.score_unit(K, Q, 3, alt_params(norm_mode=ora.NORM_MAD, mad_tau=tau), trace=True)
+    d = r["dE"][:P]
+    med = np.median(d)
+    mad = np.median(np.abs(d - med))
+    np.testing.assert_allclose(r["sE"], 1.0 / (1.0 + np.exp(-(d - med) / (tau * mad + 1e-6))), rtol=1e-12)
+    # half of the keys lie at or above the median: s_E >= 1/2 for them
+    assert np.sum(r["sE"] >= 0.5) >= P // 2
+
+
+def test_rstd_is_the_key_standard_deviation(ora):
+    # mean_T |k - kbar|^2 is the summed per-dimension variance of the keys
+    K, Q = rand_unit(73, 120, 16, G=2, w=2, scale=1.7, offset=0.8)
+    tau = 4.0
+    r = ora.score_unit(K, Q, 2, alt_params(redundancy=ora.RED_STD, tau=tau, beta=1.0))
+    Dstd = np.sqrt(np.var(K.astype(np.float64), axis=0).sum())
+    rstd = 1.0 - 1.0 / (1.0 + np.exp(-Dstd / tau))
+    assert r["stats"][S_["rE"]] == pytest.approx(rstd, rel=1e-12)
+    assert r["stats"][S_["lambda_"]] == pytest.approx(rstd, rel=1e-12)   # beta = 1
+    # r_std lies in (0, 1/2) and D_E <= D_std (Jensen)
+    assert 0.0 < rstd < 0.5 and r["stats"][S_["DE"]] <= Dstd * (1 + 1e-12)
+
+
+def test_rstd_two_antipodal_keys(ora):
+    # k and -k: kbar = 0, every distance is |k|, D_std = |k|
+    k = np.array([3.0, 4.0, 0.0, 0.0], np.float32)
+    K = np.stack([k, -k, k, -k]).astype(np.float32)
+    Q = np.ones((1, 1, 4), np.float32)
+    r = ora.score_unit(K, Q, 1, alt_params(redundancy=ora.RED_STD, tau=5.0))
+    assert r["stats"][S_["rE"]] == pytest.approx(1.0 - 1.0 / (1.0 + np.exp(-1.0)), rel=1e-12)
+
+
+def test_prefix_centroid_ignores_the_window_keys(ora):
+    T, w = 70, 4
+    K, Q = rand_unit(74, T, 16, G=2, w=w, offset=0.3)
+    P = T - w
+    pp = alt_params(centroid_scope=ora.CENTROID_PREFIX)
+    r1 = ora.score_unit(K, Q, w, pp, trace=True)
+    np.testing.assert_allclose(r1["kbar"], K[:P].astype(np.float64).mean(axis=0), rtol=1e-12, atol=1e-15)
+    K2 = K.copy()
+    K2[P:] += np.float32(5.0)        # move only the window keys
+    r2 = ora.score_unit(K2, Q, w, pp, trace=True)
+    np.testing.assert_array_equal(r2["kbar"], r1["kbar"])
+    np.testing.assert_array_equal(r2["dE"][:P], r1["dE"][:P])
+    np.testing.assert_array_equal(r2["sE"], r1["sE"])
+    # with the centroid over all T keys the same move changes the distances
+    a1 = ora.score_unit(K, Q, w, trace=True)
+    a2 = ora.score_unit(K2, Q, w, trace=True)
+    assert np.abs(a2["dE"][:P] - a1["dE"][:P]).max() > 1e-3
