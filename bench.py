@@ -54,6 +54,7 @@ STAGE_KERNELS = {
     "sweep2_stream": ["k_fs2s"], "sweep2_block": ["k_fs2", "k_pass2"], "epilogue": ["k_epi_unit"],
     "epilogue1": ["k_epi1"], "epilogue2": ["k_epi2"], "single_read": ["k_fused"],
     "select": ["k_select_reg", "k_select"], "compact": ["k_compact"], "vnorm": ["k_vnorm"],
+    "dquant": ["k_dquant"],
 }
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, vendor figure
 COPY_BYTES = 1 << 30  # size of the calibration copy in --counter-run
@@ -299,6 +300,42 @@ def main():
                   "vnorm_algorithmic_bytes": bytes_v + 2 * bytes_scores,
                   "vnorm_GBs": round((bytes_v + 2 * bytes_scores) / vn_s / 1e9, 1)}
 
+    # Alternatives of Sec. 6.3 / Appendix D / Appendix B.6: the score call with
+    # each option, and the quantile kernel of the winsorised / MAD forms.
+    log("normalisation / redundancy / centroid alternatives")
+    alternatives = {"score_ms_default": round(per_call_ms["score"], 4)}
+    alt_opts = {
+        "winsorised_1pct": P.Params(norm_mode=P.NORM_WINSOR, winsor_q=0.01),
+        "mad": P.Params(norm_mode=P.NORM_MAD),
+        "r_std": P.Params(redundancy=P.RED_STD),
+        "prefix_centroid": P.Params(centroid_scope=P.CENTROID_PREFIX),
+    }
+    for name, pa in alt_opts.items():
+        ws_a = torch.empty(P.ecokv_workspace_size(shape, pa), dtype=torch.uint8, device=dev)
+
+        def score_a():
+            P.ecokv_score(K, Q, shape, pa, ep.scores, ep.lambda_, ep.stats, ws_a)
+
+        score_a()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            score_a()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        alternatives[f"score_ms_{name}"] = round(e0.elapsed_time(e1) / args.steps, 4)
+        if name == "mad":
+            os.environ["ECOKV_STAGE_TIMING"] = "1"
+            P.ecokv_stage_times()
+            for _ in range(args.steps):
+                score_a()
+            torch.cuda.synchronize()
+            st_a = P.ecokv_stage_times()
+            os.environ["ECOKV_STAGE_TIMING"] = "0"
+            alternatives["dquant_mad_us"] = round(st_a["dquant"][0] / st_a["dquant"][1] * 1e3, 2)
+        del ws_a
+
     extras = {}
     if args.extras:
         for frac in (0.1, 0.4):
@@ -367,6 +404,7 @@ def main():
         "mfma_window_gemm": mfma,
         "head_budgets": head_budgets,
         "value_norm": value_norm,
+        "alternatives": alternatives,
     }
     if extras:
         out["extras"] = extras

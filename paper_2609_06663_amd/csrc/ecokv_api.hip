@@ -81,6 +81,15 @@ int check_params(const ecokv_params *p)
     if (isinf(p->lambda_override)) return fail(ECOKV_EINVAL, "lambda_override must be NaN or finite");
     if (p->imp_mode != ECOKV_IMP_ATTN && p->imp_mode != ECOKV_IMP_ATTN_VNORM)
         return fail(ECOKV_EINVAL, "imp_mode %d", p->imp_mode);
+    if (p->norm_mode < ECOKV_NORM_MINMAX || p->norm_mode > ECOKV_NORM_MAD)
+        return fail(ECOKV_EINVAL, "norm_mode %d", p->norm_mode);
+    if (!(p->winsor_q >= 0.f && p->winsor_q < 0.5f))
+        return fail(ECOKV_EINVAL, "winsor_q %g outside [0, 0.5)", (double)p->winsor_q);
+    if (!(isfinite(p->mad_tau) && p->mad_tau > 0.f)) return fail(ECOKV_EINVAL, "mad_tau %g", (double)p->mad_tau);
+    if (p->redundancy != ECOKV_RED_EUCLID && p->redundancy != ECOKV_RED_STD)
+        return fail(ECOKV_EINVAL, "redundancy %d", p->redundancy);
+    if (p->centroid_scope != ECOKV_CENTROID_ALL && p->centroid_scope != ECOKV_CENTROID_PREFIX)
+        return fail(ECOKV_EINVAL, "centroid_scope %d", p->centroid_scope);
     return ECOKV_OK;
 }
 
@@ -248,6 +257,11 @@ int ecokv_default_params(ecokv_params *p)
     p->causal = 1;
     p->lambda_override = NAN;
     p->imp_mode = ECOKV_IMP_ATTN;
+    p->norm_mode = ECOKV_NORM_MINMAX;
+    p->winsor_q = 0.01f;
+    p->mad_tau = 1.f;
+    p->redundancy = ECOKV_RED_EUCLID;
+    p->centroid_scope = ECOKV_CENTROID_ALL;
     return ECOKV_OK;
 }
 
@@ -329,6 +343,12 @@ int ecokv_score_v(const void *K, const void *V, const void *Q_win, int dtype, co
     a.lambda_override = a.use_override ? params->lambda_override : 0.f;
     a.pool_half = params->pool_kernel / 2;
     a.causal = params->causal;
+    a.kbf16 = dtype == ECOKV_BF16;
+    a.norm_mode = params->norm_mode;
+    a.mad_tau = params->mad_tau;
+    a.red_std = params->redundancy == ECOKV_RED_STD;
+    a.centroid_prefix = params->centroid_scope == ECOKV_CENTROID_PREFIX;
+    a.winsor_q = params->winsor_q;
     if ((rc = fill_seqtab(shape, nullptr, si.w, &a.seq, nullptr))) return rc;
     const hipError_t e = ecokv::score_launch(a, static_cast<char *>(workspace), lay, si.maxT,
                                              static_cast<hipStream_t>(stream), dtype == ECOKV_BF16);

@@ -44,7 +44,7 @@ struct ScoreArgs {
     // workspace regions
     float *part1;    // [U][nch1][2D + 2R]  column sums, row max / sum-exp per block
     float *anchors;  // [U][2D + 2R]        kbar, mu, row max, row normaliser
-    float *part2;    // [U][nch2][4]        sum d_E, min d_E, max d_E per block
+    float *part2;    // [U][nch2][4]        sum d_E, min d_E, max d_E, sum d_E^2 per block
     float *part3;    // [U][nch3][4]        sum S_div, sum S_imp, min/max S_div per block
     float *bufA;     // [L][Hkv][Ptot]      d_E
     float *bufB;     // [L][Hkv][Ptot]      khat.mu
@@ -70,6 +70,12 @@ struct ScoreArgs {
     float alpha, beta, eps, tau, inv_sqrt_d, lambda_override;
     int use_override, pool_half, causal;
     int vnorm;       // S_imp = pool(a) * |v_i|_2
+    int kbf16;       // K holds bf16 (else fp32)
+    int norm_mode;   // ECOKV_NORM_*: how d_E becomes s_E
+    float mad_tau, winsor_q;
+    const float *dq; // [U][2] quantile pair of d_E per unit (winsorised or MAD norm)
+    int red_std;     // lambda uses r_std (Appendix D) instead of r_E
+    int centroid_prefix;  // kbar over the non-window keys (Appendix B.6)
     SeqTab seq;
 };
 
@@ -126,8 +132,21 @@ struct CompactArgs {
 
 // Workspace layout, shared by the size query and the launcher.
 struct WsLayout {
-    size_t part1, anchors, part2, part3, bufA, bufB, bufC, bufV, partT, ancT, epiT, status, total;
+    size_t part1, anchors, part2, part3, bufA, bufB, bufC, bufV, dq, partT, ancT, epiT, status, total;
 };
+
+// Order statistics of d_E per unit for the winsorised and MAD normalisations:
+// out[u] = (quantile q, quantile 1 - q), or (median, median of |d - median|).
+struct DQuantArgs {
+    const float *d;  // [L][Hkv][Ptot] d_E of the non-window keys
+    float *out;      // [U][2]
+    int L, Hkv, B, w;
+    int64_t Ptot;
+    int mode;        // ECOKV_NORM_WINSOR or ECOKV_NORM_MAD
+    float q;
+    SeqTab seq;
+};
+hipError_t dquant_launch(const DQuantArgs &a, hipStream_t st);
 
 WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16, bool vnorm);
 hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hipStream_t st, bool bf16);

@@ -146,7 +146,7 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
     constexpr int ESZ = BF ? 2 : 4;
     __shared__ float q_lds[ECOKV_MAX_ROWS * D];
     __shared__ float kb[D], mu[D], rm[ECOKV_MAX_ROWS], rs_inv[ECOKV_MAX_ROWS];
-    __shared__ float wred[3][kThreads / kWave];
+    __shared__ float wred[4][kThreads / kWave];
 
     const int u = blockIdx.y;
     const Unit un = unit_of(u, a.Hkv, a.B);
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
     const char *k0 = static_cast<const char *>(a.K) + unit_row0(a, un) * D * ESZ;
     const int64_t obase = unit_out_base(a, un);
     const float inv_r = 1.f / (float)a.R;
-    float dsum = 0.f, dmin = INFINITY, dmax = -INFINITY;
+    float dsum = 0.f, dsq = 0.f, dmin = INFINITY, dmax = -INFINITY;
 
     for (int it = 0; it < kCh / 16; ++it) {
         const int i = row0 + it * 16 + wv * 4 + sub;
@@ -209,6 +209,7 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
         }
         if (valid) {
             dsum += (c == 0) ? dE : 0.f;
+            dsq += (c == 0) ? dE * dE : 0.f;
             if (i < P) {
                 dmin = fminf(dmin, dE);
                 dmax = fmaxf(dmax, dE);
@@ -221,26 +222,29 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
         }
     }
     dsum = wave_sum(dsum);
+    dsq = wave_sum(dsq);
     dmin = wave_min(dmin);
     dmax = wave_max(dmax);
     if (lane == 0) {
         wred[0][wv] = dsum;
         wred[1][wv] = dmin;
         wred[2][wv] = dmax;
+        wred[3][wv] = dsq;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        float s = 0.f, mn = INFINITY, mx = -INFINITY;
+        float s = 0.f, s2 = 0.f, mn = INFINITY, mx = -INFINITY;
         for (int k = 0; k < kThreads / kWave; ++k) {
             s += wred[0][k];
             mn = fminf(mn, wred[1][k]);
             mx = fmaxf(mx, wred[2][k]);
+            s2 += wred[3][k];
         }
         float *pp = a.part2 + ((int64_t)u * a.nch2 + blockIdx.x) * 4;
         pp[0] = s;
         pp[1] = mn;
         pp[2] = mx;
-        pp[3] = 0.f;
+        pp[3] = s2;
     }
 }
 
@@ -534,7 +538,7 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
     constexpr int kAnc = 32 * MT - 4;  // first anchor row of the A operand
     __shared__ u32x4 kt[kTile * kChunks];
     __shared__ float rowM[32 * MT], rowIS[32 * MT];
-    __shared__ float wred[3][4];
+    __shared__ float wred[4][4];
     __shared__ float kb2_lds;
 
     const int u = blockIdx.y;
@@ -606,7 +610,7 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
         rowIS[tid] = ok ? 1.f / anc[2 * kD + a.R + tid] : 0.f;
     }
 
-    float dsum = 0.f, dmn = INFINITY, dmx = -INFINITY;
+    float dsum = 0.f, dsq = 0.f, dmn = INFINITY, dmx = -INFINITY;
     const float inv_r = 1.f / (float)a.R;
     const int ntiles = min(kTilesPerBlock, (T - row_base + kTile - 1) / kTile);
     const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + kRows));
@@ -646,7 +650,10 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
         const float cm = kmu * __builtin_amdgcn_rsqf(fmaxf(n2, 1e-24f));
         const int gi = tr0 + 32 * wv + (lane & 31);
         if (h == 0) {
-            if (gi < T) dsum += dE;
+            if (gi < T) {
+                dsum += dE;
+                dsq += dE * dE;
+            }
             if (gi < P) {
                 dmn = fminf(dmn, dE);
                 dmx = fmaxf(dmx, dE);
@@ -658,26 +665,29 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
     });
 
     dsum = wave_sum(dsum);
+    dsq = wave_sum(dsq);
     dmn = wave_min(dmn);
     dmx = wave_max(dmx);
     if (lane == 0) {
         wred[0][wv] = dsum;
         wred[1][wv] = dmn;
         wred[2][wv] = dmx;
+        wred[3][wv] = dsq;
     }
     lds_barrier();
     if (tid == 0) {
-        float s = 0.f, mn = INFINITY, mx = -INFINITY;
+        float s = 0.f, s2 = 0.f, mn = INFINITY, mx = -INFINITY;
         for (int k = 0; k < 4; ++k) {
             s += wred[0][k];
             mn = fminf(mn, wred[1][k]);
             mx = fmaxf(mx, wred[2][k]);
+            s2 += wred[3][k];
         }
         float *pp = a.part2 + ((int64_t)u * a.nch2 + blockIdx.x) * 4;
         pp[0] = s;
         pp[1] = mn;
         pp[2] = mx;
-        pp[3] = 0.f;
+        pp[3] = s2;
     }
 }
 
@@ -704,7 +714,7 @@ __device__ __forceinline__ void group_load(u32x4 (&b)[8], __amdgpu_buffer_rsrc_t
 
 __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
 {
-    __shared__ float wred[3][kS2Waves];
+    __shared__ float wred[4][kS2Waves];
     __shared__ u32x4 stage[kS2Waves][32 * kChunks];  // per wave: 32 rows, swizzled 16-byte chunks
     // the block's per-key outputs (d_E, khat.mu, a), written out once at the end:
     // a few long stores instead of three 128-byte stores per 32 keys, which
@@ -787,7 +797,7 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
     const int wbase = row_base + wv * (32 * kS2Groups);
     const int wkeys = __builtin_amdgcn_readfirstlane(max(0, min(32 * kS2Groups, T - wbase)));
     const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0 + (int64_t)wbase * kD, wkeys);
-    float dsum = 0.f, dmn = INFINITY, dmx = -INFINITY;
+    float dsum = 0.f, dsq = 0.f, dmn = INFINITY, dmx = -INFINITY;
     const float inv_r = 1.f / (float)a.R;
 
     u32x4 *wst = stage[wv];
@@ -819,7 +829,10 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
         const float cm = kmu * __builtin_amdgcn_rsqf(fmaxf(n2, 1e-24f));
         const int gi = key0 + kl;
         if (valid && h == 0) {
-            if (gi < T) dsum += dE;
+            if (gi < T) {
+                dsum += dE;
+                dsq += dE * dE;
+            }
             if (gi < P) {
                 dmn = fminf(dmn, dE);
                 dmx = fmaxf(dmx, dE);
@@ -864,12 +877,14 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
     }
 
     dsum = wave_sum(dsum);
+    dsq = wave_sum(dsq);
     dmn = wave_min(dmn);
     dmx = wave_max(dmx);
     if (lane == 0) {
         wred[0][wv] = dsum;
         wred[1][wv] = dmn;
         wred[2][wv] = dmx;
+        wred[3][wv] = dsq;
     }
     __syncthreads();
     {
@@ -888,17 +903,18 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
         }
     }
     if (tid == 0) {
-        float s2 = 0.f, mn = INFINITY, mx = -INFINITY;
+        float s = 0.f, s2 = 0.f, mn = INFINITY, mx = -INFINITY;
         for (int k = 0; k < kS2Waves; ++k) {
-            s2 += wred[0][k];
+            s += wred[0][k];
             mn = fminf(mn, wred[1][k]);
             mx = fmaxf(mx, wred[2][k]);
+            s2 += wred[3][k];
         }
         float *pp = a.part2 + ((int64_t)u * a.nch2 + blockIdx.x) * 4;
-        pp[0] = s2;
+        pp[0] = s;
         pp[1] = mn;
         pp[2] = mx;
-        pp[3] = 0.f;
+        pp[3] = s2;
     }
 }
 
@@ -1107,7 +1123,22 @@ __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
             for (int b = q; b < nb; b += 4) s += p[(int64_t)b * stride + c];
             s += __shfl_xor(s, 1, 4);
             s += __shfl_xor(s, 2, 4);
-            if (q == 0) anc[c] = s / (float)T;
+            if (q == 0) {
+                float n = (float)T;
+                if (c < a.D && a.centroid_prefix) {
+                    // kbar over the P non-window keys: the window rows leave the sum
+                    const int64_t r0 = unit_row0(a, un) + (T - a.w);
+                    float ws = 0.f;
+                    for (int j = 0; j < a.w; ++j) {
+                        const int64_t off = (r0 + j) * a.D + c;
+                        ws += a.kbf16 ? __uint_as_float((uint32_t)static_cast<const uint16_t *>(a.K)[off] << 16)
+                                      : static_cast<const float *>(a.K)[off];
+                    }
+                    s -= ws;
+                    n = (float)(T - a.w);
+                }
+                anc[c] = s / n;
+            }
         } else {
             const int r = c - 2 * a.D;
             float m = -INFINITY, s = 0.f;
@@ -1240,11 +1271,48 @@ __device__ __forceinline__ void epi_keys(const ScoreArgs &a, const float *dbuf, 
     load_imp<kEpiPer>(a, abuf, P, i0, imp);
 }
 
-// The per-unit constants of Eq. (2)-(7) from the unit's reductions: d_E
-// (sum over T, min / max over P), S_div (sum, min, max over P) and S_imp
-// (sum over P), and |mu|^2.
+// s_E of a distance (the Eq. (2) step): min-max over the unit's non-window
+// keys; or, after clipping to the q and 1 - q quantiles, min-max between
+// them (winsorised); or a sigmoid of the deviation from the median in units
+// of the median absolute deviation (MAD) (Sec. 6.3, Table 4).  The quantile
+// pair of a unit comes from k_dquant.
+struct DNorm {
+    float lo, hi, g;
+    int sig;
+};
+
+__device__ __forceinline__ DNorm d_norm(const ScoreArgs &a, int u, const Red4 &dst)
+{
+    DNorm n;
+    n.sig = 0;
+    if (a.norm_mode == ECOKV_NORM_MINMAX) {
+        n.lo = dst.mn;
+        n.hi = dst.mx;
+        n.g = 1.f / (dst.mx - dst.mn + a.eps);
+    } else if (a.norm_mode == ECOKV_NORM_WINSOR) {
+        n.lo = a.dq[2 * (int64_t)u];
+        n.hi = a.dq[2 * (int64_t)u + 1];
+        n.g = 1.f / (n.hi - n.lo + a.eps);
+    } else {
+        n.lo = a.dq[2 * (int64_t)u];
+        n.hi = INFINITY;
+        n.g = 1.f / (a.mad_tau * a.dq[2 * (int64_t)u + 1] + a.eps);
+        n.sig = 1;
+    }
+    return n;
+}
+
+__device__ __forceinline__ float s_euclid(float d, const DNorm &n)
+{
+    if (n.sig) return 1.f / (1.f + expf(-(d - n.lo) * n.g));
+    return (fminf(fmaxf(d, n.lo), n.hi) - n.lo) * n.g;
+}
+
+// The per-unit constants of Eq. (3)-(7) from the unit's reductions: d_E
+// (sum and sum of squares over T, min / max over P), S_div (sum, min, max over
+// P) and S_imp (sum over P), and |mu|^2.
 struct EpiConsts {
-    float lam, rE, rC, DE, dmin, dden, smin, sden, impmean, sbarmean, scale;
+    float lam, rE, rC, DE, smin, sden, impmean, sbarmean, scale;
 };
 
 __device__ __forceinline__ EpiConsts epi_consts(const ScoreArgs &a, const Red4 &dst, const Red4 &sd, float mu2, int T,
@@ -1252,9 +1320,10 @@ __device__ __forceinline__ EpiConsts epi_consts(const ScoreArgs &a, const Red4 &
 {
     EpiConsts k;
     k.DE = dst.s0 / (float)T;
-    k.dmin = dst.mn;
-    k.dden = dst.mx - dst.mn + a.eps;
-    k.rE = 2.f - 2.f / (1.f + expf(-k.DE / a.tau));
+    if (a.red_std)  // r_std = 1 - sigmoid(D_std / tau), D_std = sqrt(mean_T d_E^2) (Appendix D)
+        k.rE = 1.f - 1.f / (1.f + expf(-sqrtf(dst.s1 / (float)T) / a.tau));
+    else
+        k.rE = 2.f - 2.f / (1.f + expf(-k.DE / a.tau));
     k.rC = ((float)T * mu2 - 1.f) / ((float)T - 1.f);
     k.lam = a.use_override ? a.lambda_override : a.beta * k.rE + (1.f - a.beta) * k.rC;
     if (a.status && *a.status == a.tag) k.lam = NAN;  // a publication wait of this launch timed out
@@ -1287,7 +1356,7 @@ __device__ __forceinline__ void epi_write_stats(const ScoreArgs &a, int u, const
     if (a.lambda) a.lambda[u] = k.lam;
 }
 
-// Sum, min and max of d_E over the unit, from the sweep-2 partials.
+// Sum, sum of squares, min and max of d_E over the unit, from the sweep-2 partials.
 __device__ Red4 unit_distance_stats(const ScoreArgs &a, int u, int T, Red4 *lds)
 {
     const int nb = (T + a.rpb2 - 1) / a.rpb2;
@@ -1295,6 +1364,7 @@ __device__ Red4 unit_distance_stats(const ScoreArgs &a, int u, int T, Red4 *lds)
     for (int b = threadIdx.x; b < nb; b += blockDim.x) {
         const float *pp = a.part2 + ((int64_t)u * a.nch2 + b) * 4;
         v.s0 += pp[0];
+        v.s1 += pp[3];
         v.mn = fminf(v.mn, pp[1]);
         v.mx = fmaxf(v.mx, pp[2]);
     }
@@ -1314,7 +1384,7 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi1(ScoreArgs a)
     const int64_t ob = unit_out_base(a, un);
     const float *dbuf = a.bufA + ob, *cbuf = a.bufB + ob, *abuf = a.bufC + ob;
     const Red4 dst = unit_distance_stats(a, u, T, lds);
-    const float dmin = dst.mn, dden = dst.mx - dst.mn + a.eps;
+    const DNorm dn = d_norm(a, u, dst);
 
     Red4 w{0.f, 0.f, INFINITY, -INFINITY};
     {
@@ -1324,7 +1394,7 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi1(ScoreArgs a)
 #pragma unroll
         for (int j = 0; j < kEpiPer; ++j)
             if (k0 + j < i1) {
-                const float sE = (d[j] - dmin) / dden;
+                const float sE = s_euclid(d[j], dn);
                 const float sC = (1.f - c[j]) * 0.5f;
                 const float sdiv = a.alpha * sE + (1.f - a.alpha) * sC;
                 w.s0 += sdiv;
@@ -1373,7 +1443,8 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
     for (int d = threadIdx.x; d < a.D; d += blockDim.x) m2.s0 += mu[d] * mu[d];
     const float mu2 = block_red4(m2, lds).s0;
     const EpiConsts k = epi_consts(a, dst, sd, mu2, T, P);
-    const float lam = k.lam, dmin = k.dmin, dden = k.dden, smin = k.smin, sden = k.sden, scale = k.scale;
+    const float lam = k.lam, smin = k.smin, sden = k.sden, scale = k.scale;
+    const DNorm dn = d_norm(a, u, dst);
 
     float *out = a.scores + ob;
     {
@@ -1382,7 +1453,7 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
         epi_keys(a, dbuf, cbuf, abuf, P, k0, d, c, imp);
 #pragma unroll
         for (int j = 0; j < kEpiPer; ++j) {
-            const float sE = (d[j] - dmin) / dden;
+            const float sE = s_euclid(d[j], dn);
             const float sC = (1.f - c[j]) * 0.5f;
             const float sdiv = a.alpha * sE + (1.f - a.alpha) * sC;
             sv[j] = lam * (((sdiv - smin) / sden) * scale) + (1.f - lam) * imp[j];
@@ -1502,12 +1573,14 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
     // attention just outside the block's range (a negative offset wraps past
     // the range and reads zero)
     Red4 v{0.f, 0.f, INFINITY, -INFINITY};
+    float dq2 = 0.f;  // this thread's partial sum of d_E^2
     const int nb2 = (T + a.rpb2 - 1) / a.rpb2;
     if ((int)threadIdx.x < nb2) {
         const float *pp = a.part2 + ((int64_t)u * a.nch2 + threadIdx.x) * 4;
         v.s0 = pp[0];
         v.mn = pp[1];
         v.mx = pp[2];
+        dq2 = pp[3];
     }
     const float mv = (int)threadIdx.x < a.D ? mu[threadIdx.x] : 0.f;
     const __amdgpu_buffer_rsrc_t rd = float_rsrc(a.bufA + ob, P), rc = float_rsrc(a.bufB + ob, P),
@@ -1530,11 +1603,12 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
 
     v.s1 = mv * mv;
     const Red4 dm = block_red4_lds(v, lds);
-    const Red4 dst{dm.s0, 0.f, dm.mn, dm.mx};
+    const float dsq = a.red_std ? block_red4_lds(Red4{dq2, 0.f, INFINITY, -INFINITY}, lds).s0 : 0.f;
+    const Red4 dst{dm.s0, dsq, dm.mn, dm.mx};
     const float mu2 = dm.s1;
 
     // S_div, kept in LDS (each thread reads back only its own values)
-    const float dmin = dst.mn, inv_dden = 1.f / (dst.mx - dst.mn + a.eps);
+    const DNorm dn = d_norm(a, u, dst);
     Red4 w{0.f, 0.f, INFINITY, -INFINITY};
 #pragma unroll
     for (int j = 0; j < kVec; ++j) {
@@ -1542,7 +1616,7 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
         f32x4 sv;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const float sE = (xd[j][e] - dmin) * inv_dden;
+            const float sE = s_euclid(xd[j][e], dn);
             const float sC = (1.f - xc[j][e]) * 0.5f;
             sv[e] = a.alpha * sE + (1.f - a.alpha) * sC;
             if (k4 + e < P) {
@@ -1743,6 +1817,7 @@ WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int 
     w.bufB = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
     w.bufC = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
     w.bufV = o; o = align256(o + (vnorm ? sizeof(float) * (int64_t)L * Hkv * Ptot : 0));
+    w.dq = o; o = align256(o + sizeof(float) * U * 2);
     w.partT = o; o = align256(o + sizeof(unsigned long long) * U * stride * nchf);
     w.ancT = o; o = align256(o + (single ? sizeof(unsigned long long) * U * stride : 0));
     w.epiT = o; o = align256(o + sizeof(unsigned long long) * U * 2 * 4);
@@ -1824,7 +1899,9 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     const char *path = getenv("ECOKV_SCORE_PATH");
     const bool want_single = path && strcmp(path, "single") == 0;
     int fgrid = 0;
-    if (want_single && fused_eligible(a.D, bf16, a.R, a.seq, a.L, a.Hkv, a.Hq, a.w, &fgrid)) {
+    // (its partials carry no sum of d_E^2 and its centroid spans all T keys)
+    if (want_single && !a.red_std && !a.centroid_prefix &&
+        fused_eligible(a.D, bf16, a.R, a.seq, a.L, a.Hkv, a.Hq, a.w, &fgrid)) {
         a.partT = reinterpret_cast<unsigned long long *>(ws + lay.partT);
         a.ancT = reinterpret_cast<unsigned long long *>(ws + lay.ancT);
         a.status = reinterpret_cast<unsigned *>(ws + lay.status);
@@ -1873,6 +1950,23 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         if ((e = hipGetLastError()) != hipSuccess) return e;
         a.bufC = a.bufV;
         a.pool_half = 0;
+    }
+    if (a.norm_mode != ECOKV_NORM_MINMAX) {
+        // quantiles of d_E for the winsorised or MAD normalisation
+        DQuantArgs qa;
+        memset(&qa, 0, sizeof qa);
+        qa.d = a.bufA;
+        qa.out = reinterpret_cast<float *>(ws + lay.dq);
+        qa.L = a.L;
+        qa.Hkv = a.Hkv;
+        qa.B = a.B;
+        qa.w = a.w;
+        qa.Ptot = a.Ptot;
+        qa.mode = a.norm_mode;
+        qa.q = a.winsor_q;
+        qa.seq = a.seq;
+        if ((e = dquant_launch(qa, st)) != hipSuccess) return e;
+        a.dq = qa.out;
     }
     if (maxT - a.w <= kUKeys && a.pool_half <= kPoolHalfMax && (maxT + a.rpb2 - 1) / a.rpb2 <= kUThreads && a.D <= kUThreads) {
         // two blocks per unit when all of them can be resident at once (their

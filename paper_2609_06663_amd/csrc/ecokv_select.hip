@@ -357,6 +357,119 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// Register-resident radix select: thread t holds keys kk[0..KPT) at positions
+// v0 .. v0+KPT-1 of n (positions >= n are not keys).
+// ---------------------------------------------------------------------------
+// Block-wide min and max of the keys (mm: LDS, 2 x kSelWaves).
+template <int KPT>
+__device__ __forceinline__ void reg_extremes(const uint32_t (&kk)[KPT], int v0, int n, uint32_t (*mm)[kSelWaves],
+                                             uint32_t *kmin_out, uint32_t *kmax_out)
+{
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+    for (int q = 0; q < KPT; ++q)
+        if (v0 + q < n) {
+            kmin = min(kmin, kk[q]);
+            kmax = max(kmax, kk[q]);
+        }
+    kmin = wave_min_u(kmin);
+    kmax = wave_max_u(kmax);
+    if (lane == 0) {
+        mm[0][wv] = kmin;
+        mm[1][wv] = kmax;
+    }
+    __syncthreads();
+    kmin = mm[0][0];
+    kmax = mm[1][0];
+    for (int q = 1; q < kSelWaves; ++q) {
+        kmin = min(kmin, mm[0][q]);
+        kmax = max(kmax, mm[1][q]);
+    }
+    *kmin_out = kmin;
+    *kmax_out = kmax;
+}
+
+// The k-th largest key (k >= 1): digits of up to 8 bits below the common
+// prefix of kmin and kmax, one LDS histogram per wave, three barriers per
+// pass (the histogram is cleared by the threads that fold it, and the chosen
+// digit alternates between two slots).  Returns the threshold and how many
+// keys equal to it are taken.
+template <int KPT>
+__device__ __forceinline__ void reg_radix_select(const uint32_t (&kk)[KPT], int v0, int n, int k, uint32_t kmin,
+                                                 uint32_t kmax, uint32_t (*hist)[256], uint32_t *hsum,
+                                                 uint32_t (*bc)[2], uint32_t *thr_out, int *need_eq_out)
+{
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const uint32_t diff = kmin ^ kmax;
+    if (diff == 0) {
+        *thr_out = kmin;
+        *need_eq_out = k;
+        return;
+    }
+    int hi = 31 - __clz(diff);
+    uint32_t mask = hi == 31 ? 0u : ~((2u << hi) - 1u);
+    uint32_t prefix = kmin & mask;
+    int rem = k;
+    for (int b = tid; b < kSelWaves * 256; b += blockDim.x) (&hist[0][0])[b] = 0;
+    __syncthreads();
+    int par = 0;
+    while (hi >= 0) {
+        const int lo = hi >= 7 ? hi - 7 : 0;
+        const uint32_t nb = 1u << (hi - lo + 1);
+#pragma unroll
+        for (int q = 0; q < KPT; ++q)
+            if (v0 + q < n && (kk[q] & mask) == prefix) atomicAdd(&hist[wv][(kk[q] >> lo) & (nb - 1u)], 1u);
+        __syncthreads();
+        if (tid < 256) {
+            uint32_t c = 0;
+#pragma unroll
+            for (int w2 = 0; w2 < kSelWaves; ++w2) {
+                c += hist[w2][tid];
+                hist[w2][tid] = 0;
+            }
+            hsum[tid] = c;
+        }
+        __syncthreads();
+        if (tid < kWave) {
+            // lane owns bins 255-4l .. 252-4l (descending digit order)
+            uint32_t c4[4], loc = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                c4[q] = hsum[255 - 4 * lane - q];
+                loc += c4[q];
+            }
+            uint32_t inc = loc;
+#pragma unroll
+            for (int d = 1; d < kWave; d <<= 1) {
+                const uint32_t y = __shfl_up(inc, d, kWave);
+                if (lane >= d) inc += y;
+            }
+            const uint32_t before = inc - loc;
+            if ((int)before < rem && rem <= (int)inc) {
+                uint32_t cum = before;
+                for (int q = 0; q < 4; ++q) {
+                    if ((int)(cum + c4[q]) >= rem) {
+                        bc[par][0] = 255u - 4u * lane - q;
+                        bc[par][1] = cum;
+                        break;
+                    }
+                    cum += c4[q];
+                }
+            }
+        }
+        __syncthreads();
+        prefix |= bc[par][0] << lo;
+        rem -= (int)bc[par][1];
+        mask |= (nb - 1u) << lo;
+        hi = lo - 1;
+        par ^= 1;
+    }
+    *thr_out = prefix;
+    *need_eq_out = rem;
+}
+
+// ---------------------------------------------------------------------------
 // Register-resident variant for groups of up to 64 Ki keys: thread t owns the
 // contiguous run [t*KPT, t*KPT + KPT) of the group's keys in registers
 // (16-byte loads in per-head mode), the radix passes histogram them into one
@@ -448,96 +561,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
     uint32_t thr = 0xffffffffu;
     int need_eq = 0;
     if (k > 0) {
-        uint32_t kmin = 0xffffffffu, kmax = 0u;
-#pragma unroll
-        for (int q = 0; q < KPT; ++q)
-            if (v0 + q < n) {
-                kmin = min(kmin, kk[q]);
-                kmax = max(kmax, kk[q]);
-            }
-        kmin = wave_min_u(kmin);
-        kmax = wave_max_u(kmax);
-        if (lane == 0) {
-            mm[0][wv] = kmin;
-            mm[1][wv] = kmax;
-        }
-        __syncthreads();
-        kmin = mm[0][0];
-        kmax = mm[1][0];
-        for (int q = 1; q < kSelWaves; ++q) {
-            kmin = min(kmin, mm[0][q]);
-            kmax = max(kmax, mm[1][q]);
-        }
-        // radix select of the k-th largest key, digits of up to 8 bits below
-        // the common prefix of kmin and kmax
-        const uint32_t diff = kmin ^ kmax;
-        if (diff == 0) {
-            thr = kmin;
-            need_eq = k;
-        } else {
-            int hi = 31 - __clz(diff);
-            uint32_t mask = hi == 31 ? 0u : ~((2u << hi) - 1u);
-            uint32_t prefix = kmin & mask;
-            int rem = k;
-            // Three barriers per pass: the histogram is cleared by the threads
-            // that fold it, and the chosen digit alternates between two slots.
-            for (int b = tid; b < kSelWaves * 256; b += blockDim.x) (&hist[0][0])[b] = 0;
-            __syncthreads();
-            int par = 0;
-            while (hi >= 0) {
-                const int lo = hi >= 7 ? hi - 7 : 0;
-                const uint32_t nb = 1u << (hi - lo + 1);
-#pragma unroll
-                for (int q = 0; q < KPT; ++q)
-                    if (v0 + q < n && (kk[q] & mask) == prefix) atomicAdd(&hist[wv][(kk[q] >> lo) & (nb - 1u)], 1u);
-                __syncthreads();
-                if (tid < 256) {
-                    uint32_t c = 0;
-#pragma unroll
-                    for (int w2 = 0; w2 < kSelWaves; ++w2) {
-                        c += hist[w2][tid];
-                        hist[w2][tid] = 0;
-                    }
-                    hsum[tid] = c;
-                }
-                __syncthreads();
-                if (tid < kWave) {
-                    // lane owns bins 255-4l .. 252-4l (descending digit order)
-                    uint32_t c4[4], loc = 0;
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        c4[q] = hsum[255 - 4 * lane - q];
-                        loc += c4[q];
-                    }
-                    uint32_t inc = loc;
-#pragma unroll
-                    for (int d = 1; d < kWave; d <<= 1) {
-                        const uint32_t y = __shfl_up(inc, d, kWave);
-                        if (lane >= d) inc += y;
-                    }
-                    const uint32_t before = inc - loc;
-                    if ((int)before < rem && rem <= (int)inc) {
-                        uint32_t cum = before;
-                        for (int q = 0; q < 4; ++q) {
-                            if ((int)(cum + c4[q]) >= rem) {
-                                bc[par][0] = 255u - 4u * lane - q;
-                                bc[par][1] = cum;
-                                break;
-                            }
-                            cum += c4[q];
-                        }
-                    }
-                }
-                __syncthreads();
-                prefix |= bc[par][0] << lo;
-                rem -= (int)bc[par][1];
-                mask |= (nb - 1u) << lo;
-                hi = lo - 1;
-                par ^= 1;
-            }
-            thr = prefix;
-            need_eq = rem;
-        }
+        uint32_t kmin, kmax;
+        reg_extremes<KPT>(kk, v0, n, mm, &kmin, &kmax);
+        // radix select of the k-th largest key
+        reg_radix_select<KPT>(kk, v0, n, k, kmin, kmax, hist, hsum, bc, &thr, &need_eq);
 
         // ordered emission from the registers
         uint32_t cg = 0, ce = 0;
@@ -594,6 +621,196 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
         if (a.counts) a.counts[u] = (int32_t)(through[hh] - prev + a.w);
         if (a.offsets) a.offsets[u] = (int32_t)(out_base + prev + (int64_t)hh * a.w);
     }
+}
+
+// ---------------------------------------------------------------------------
+// Order statistics of d_E for the winsorised and MAD normalisations (Sec. 6.3,
+// Table 4): per unit, its q and 1 - q quantiles, or its median and the median
+// of |d_E - median|, over the P non-window keys.  A quantile interpolates
+// linearly between the order statistics at ranks floor(h) and floor(h) + 1,
+// h = q (P - 1).  One block per unit; the lower order statistic is an exact
+// radix select (the unit's values are re-read from the cache in every pass),
+// the upper one either equals it (ties) or is the smallest key above it.
+// ---------------------------------------------------------------------------
+struct DistKey {
+    const float *d;
+    float c;   // with dev: the key of v is |d[v] - c|
+    bool dev;
+    __device__ __forceinline__ uint32_t operator()(int64_t v) const { return score_key(dev ? fabsf(d[v] - c) : d[v]); }
+};
+
+// The value of an order-preserving key (inverse of score_key for numbers).
+__device__ __forceinline__ float key_value(uint32_t k)
+{
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// Block-wide min and max of the keys.
+template <class Src>
+__device__ void key_extremes(const Src &key, int64_t n, uint32_t *red, uint32_t *kmin, uint32_t *kmax)
+{
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    uint32_t mn = 0xffffffffu, mx = 0u;
+    for_each_key(key, n, [&](int64_t, uint32_t kk) {
+        mn = min(mn, kk);
+        mx = max(mx, kk);
+    });
+    mn = wave_min_u(mn);
+    mx = wave_max_u(mx);
+    if (lane == 0) {
+        red[wv] = mn;
+        red[kSelWaves + wv] = mx;
+    }
+    __syncthreads();
+    mn = red[0];
+    mx = red[kSelWaves];
+    for (int q = 1; q < kSelWaves; ++q) {
+        mn = min(mn, red[q]);
+        mx = max(mx, red[kSelWaves + q]);
+    }
+    __syncthreads();
+    *kmin = mn;
+    *kmax = mx;
+}
+
+// The q quantile (linear interpolation) of n >= 1 keys with extremes kmin, kmax.
+template <class Src>
+__device__ float key_quantile(const Src &key, int64_t n, double q, uint32_t kmin, uint32_t kmax, uint32_t *hist,
+                              uint32_t *bc, uint32_t *red)
+{
+    const double h = q * (double)(n - 1);
+    const int64_t j = (int64_t)floor(h);
+    // x_(j), the (n - j)-th largest; need_eq counts its copies among the n - j largest
+    uint32_t thr;
+    int64_t need_eq;
+    radix_threshold(key, n, n - j, kmin, kmax, hist, bc, &thr, &need_eq);
+    __syncthreads();
+    const float x = key_value(thr);
+    if (j + 1 >= n || need_eq >= 2) return x;  // x_(j+1) = x_(j), or no x_(j+1)
+    uint32_t m = 0xffffffffu;
+    for_each_key(key, n, [&](int64_t, uint32_t kk) {
+        if (kk > thr) m = min(m, kk);
+    });
+    m = wave_min_u(m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    m = red[0];
+    for (int w2 = 1; w2 < kSelWaves; ++w2) m = min(m, red[w2]);
+    __syncthreads();
+    return x + (float)(h - (double)j) * (key_value(m) - x);
+}
+
+__global__ __launch_bounds__(kSelThreads) void k_dquant(DQuantArgs a)
+{
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t bc[2];
+    __shared__ uint32_t red[2 * kSelWaves];
+    const Unit un = unit_of(blockIdx.x, a.Hkv, a.B);
+    const int P = a.seq.cu[un.s + 1] - a.seq.cu[un.s] - a.w;
+    const float *d = a.d + ((int64_t)un.l * a.Hkv + un.h) * a.Ptot + (a.seq.cu[un.s] - (int64_t)un.s * a.w);
+    const DistKey key{d, 0.f, false};
+    uint32_t kmin, kmax;
+    key_extremes(key, P, red, &kmin, &kmax);
+    float o0, o1;
+    if (a.mode == ECOKV_NORM_WINSOR) {
+        o0 = key_quantile(key, P, (double)a.q, kmin, kmax, hist, bc, red);
+        o1 = key_quantile(key, P, 1.0 - (double)a.q, kmin, kmax, hist, bc, red);
+    } else {
+        o0 = key_quantile(key, P, 0.5, kmin, kmax, hist, bc, red);  // median
+        const DistKey dev{d, o0, true};
+        key_extremes(dev, P, red, &kmin, &kmax);
+        o1 = key_quantile(dev, P, 0.5, kmin, kmax, hist, bc, red);  // median absolute deviation
+    }
+    if (threadIdx.x == 0) {
+        a.out[2 * (int64_t)blockIdx.x] = o0;
+        a.out[2 * (int64_t)blockIdx.x + 1] = o1;
+    }
+}
+
+// The q quantile of the keys held in registers (extremes kmin, kmax; mm as
+// in reg_extremes).
+template <int KPT>
+__device__ float reg_quantile(const uint32_t (&kk)[KPT], int v0, int n, double q, uint32_t kmin, uint32_t kmax,
+                              uint32_t (*hist)[256], uint32_t *hsum, uint32_t (*bc)[2], uint32_t (*mm)[kSelWaves])
+{
+    const double h = q * (double)(n - 1);
+    const int j = (int)floor(h);
+    uint32_t thr;
+    int need_eq;
+    reg_radix_select<KPT>(kk, v0, n, n - j, kmin, kmax, hist, hsum, bc, &thr, &need_eq);
+    const float x = key_value(thr);
+    if (j + 1 >= n || need_eq >= 2) return x;  // x_(j+1) = x_(j), or no x_(j+1)
+    uint32_t m = 0xffffffffu;
+#pragma unroll
+    for (int k = 0; k < KPT; ++k)
+        if (v0 + k < n && kk[k] > thr) m = min(m, kk[k]);
+    m = wave_min_u(m);
+    if ((threadIdx.x & 63) == 0) mm[0][threadIdx.x >> 6] = m;
+    __syncthreads();
+    m = mm[0][0];
+    for (int w2 = 1; w2 < kSelWaves; ++w2) m = min(m, mm[0][w2]);
+    __syncthreads();
+    return x + (float)(h - (double)j) * (key_value(m) - x);
+}
+
+// Register-resident form for units of at most 32 Ki non-window keys: thread t
+// holds d_E of keys 32t .. 32t+31 for every pass.
+constexpr int kDqKeys = 32 * kSelThreads;
+
+__global__ __launch_bounds__(kSelThreads) void k_dquant_reg(DQuantArgs a)
+{
+    constexpr int KPT = 32;
+    __shared__ uint32_t hist[kSelWaves][256];
+    __shared__ uint32_t hsum[256];
+    __shared__ uint32_t bc[2][2];
+    __shared__ uint32_t mm[2][kSelWaves];
+    const Unit un = unit_of(blockIdx.x, a.Hkv, a.B);
+    const int P = a.seq.cu[un.s + 1] - a.seq.cu[un.s] - a.w;  // <= kDqKeys (checked on the host)
+    const float *d = a.d + ((int64_t)un.l * a.Hkv + un.h) * a.Ptot + (a.seq.cu[un.s] - (int64_t)un.s * a.w);
+    const int v0 = threadIdx.x * KPT;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(d), (short)0, P * 4, 0x00020000);
+    typedef float f32x4_t __attribute__((ext_vector_type(4)));
+    float dv[KPT];
+    uint32_t kk[KPT];
+#pragma unroll
+    for (int q = 0; q < KPT / 4; ++q) {
+        const f32x4_t x = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (v0 + 4 * q) * 4, 0, 0));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dv[4 * q + e] = x[e];
+    }
+#pragma unroll
+    for (int q = 0; q < KPT; ++q) kk[q] = score_key(dv[q]);
+    uint32_t kmin, kmax;
+    reg_extremes<KPT>(kk, v0, P, mm, &kmin, &kmax);
+    float o0, o1;
+    if (a.mode == ECOKV_NORM_WINSOR) {
+        o0 = reg_quantile<KPT>(kk, v0, P, (double)a.q, kmin, kmax, hist, hsum, bc, mm);
+        o1 = reg_quantile<KPT>(kk, v0, P, 1.0 - (double)a.q, kmin, kmax, hist, hsum, bc, mm);
+    } else {
+        o0 = reg_quantile<KPT>(kk, v0, P, 0.5, kmin, kmax, hist, hsum, bc, mm);  // median
+#pragma unroll
+        for (int q = 0; q < KPT; ++q) kk[q] = score_key(fabsf(dv[q] - o0));
+        reg_extremes<KPT>(kk, v0, P, mm, &kmin, &kmax);
+        o1 = reg_quantile<KPT>(kk, v0, P, 0.5, kmin, kmax, hist, hsum, bc, mm);  // median absolute deviation
+    }
+    if (threadIdx.x == 0) {
+        a.out[2 * (int64_t)blockIdx.x] = o0;
+        a.out[2 * (int64_t)blockIdx.x + 1] = o1;
+    }
+}
+
+hipError_t dquant_launch(const DQuantArgs &a, hipStream_t st)
+{
+    const unsigned units = (unsigned)(a.L * a.Hkv * a.B);
+    if (units == 0) return hipSuccess;
+    int maxP = 0;
+    for (int s = 0; s < a.B; ++s) maxP = max(maxP, a.seq.cu[s + 1] - a.seq.cu[s] - a.w);
+    if (maxP <= kDqKeys)
+        ECOKV_TIMED("dquant", st, hipLaunchKernelGGL(k_dquant_reg, dim3(units), dim3(kSelThreads), 0, st, a));
+    else
+        ECOKV_TIMED("dquant", st, hipLaunchKernelGGL(k_dquant, dim3(units), dim3(kSelThreads), 0, st, a));
+    return hipGetLastError();
 }
 
 hipError_t select_launch(const SelectArgs &a, hipStream_t st)

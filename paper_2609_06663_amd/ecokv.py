@@ -21,6 +21,9 @@ OK, EINVAL, EWORKSPACE, EUNSUPPORTED, EHIP = 0, -1, -2, -3, -4
 BF16, F32 = 0, 1
 PER_HEAD, LAYER_FLAT, HEAD_BUDGETS = 0, 1, 2
 IMP_ATTN, IMP_ATTN_VNORM = 0, 1
+NORM_MINMAX, NORM_WINSOR, NORM_MAD = 0, 1, 2
+RED_EUCLID, RED_STD = 0, 1
+CENTROID_ALL, CENTROID_PREFIX = 0, 1
 MAX_SEQS, MAX_ROWS = 64, 64
 NSTATS = 12
 STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7, imp_mean=8, sbar_mean=9,
@@ -52,12 +55,15 @@ class Params(ctypes.Structure):
     """ecokv_params; defaults are the paper's (Table 6)."""
     _fields_ = [("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("eps", ctypes.c_float),
                 ("tau", ctypes.c_float), ("pool_kernel", ctypes.c_int32), ("causal", ctypes.c_int32),
-                ("lambda_override", ctypes.c_float), ("imp_mode", ctypes.c_int32)]
+                ("lambda_override", ctypes.c_float), ("imp_mode", ctypes.c_int32),
+                ("norm_mode", ctypes.c_int32), ("winsor_q", ctypes.c_float), ("mad_tau", ctypes.c_float),
+                ("redundancy", ctypes.c_int32), ("centroid_scope", ctypes.c_int32)]
 
     def __init__(self, alpha=0.8, beta=0.6, eps=1e-6, tau=0.0, pool_kernel=5, causal=True,
-                 lambda_override=math.nan, imp_mode=IMP_ATTN):
+                 lambda_override=math.nan, imp_mode=IMP_ATTN, norm_mode=NORM_MINMAX, winsor_q=0.01,
+                 mad_tau=1.0, redundancy=RED_EUCLID, centroid_scope=CENTROID_ALL):
         super().__init__(alpha, beta, eps, tau, int(pool_kernel), int(bool(causal)), lambda_override,
-                         int(imp_mode))
+                         int(imp_mode), int(norm_mode), winsor_q, mad_tau, int(redundancy), int(centroid_scope))
 
 
 class Shape:

@@ -75,7 +75,9 @@ def oracle_params(p=None):
                          eps=float(np.float32(p.eps)), tau=float(np.float32(p.tau)),
                          pool_kernel=int(p.pool_kernel), causal=bool(p.causal),
                          lambda_override=lo if not math.isnan(lo) else math.nan,
-                         imp_mode=int(p.imp_mode))
+                         imp_mode=int(p.imp_mode), norm_mode=int(p.norm_mode),
+                         winsor_q=float(np.float32(p.winsor_q)), mad_tau=float(np.float32(p.mad_tau)),
+                         redundancy=int(p.redundancy), centroid_scope=int(p.centroid_scope))
 
 
 def unit_slices(wl: W.Workload, s: int):

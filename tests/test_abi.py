@@ -209,3 +209,18 @@ def test_value_norm_mode_checks(P):
     rc = lib.ecokv_score_v(fake, fake, fake, 0, ctypes.byref(s.c), ctypes.byref(p1), fake, None, None, fake, ws0,
                            None)
     assert rc == -2
+
+
+def test_alternative_options_defaults_and_checks(P):
+    d = P.ecokv_default_params()
+    assert (d.norm_mode, d.redundancy, d.centroid_scope) == (P.NORM_MINMAX, P.RED_EUCLID, P.CENTROID_ALL)
+    assert d.winsor_q == pytest.approx(0.01) and d.mad_tau == 1.0
+    s = P.Shape(1, 4, 2, 128, 4, [0, 100])
+    for kw in (dict(norm_mode=3), dict(norm_mode=-1), dict(winsor_q=0.5), dict(winsor_q=-0.1),
+               dict(mad_tau=0.0), dict(mad_tau=float("inf")), dict(redundancy=2), dict(centroid_scope=2)):
+        with pytest.raises(P.EcoKVError) as e:
+            P.ecokv_workspace_size(s, P.Params(**kw))
+        assert e.value.code == -1, kw
+    for kw in (dict(norm_mode=P.NORM_WINSOR, winsor_q=0.0), dict(norm_mode=P.NORM_MAD, mad_tau=2.0),
+               dict(redundancy=P.RED_STD), dict(centroid_scope=P.CENTROID_PREFIX)):
+        assert P.ecokv_workspace_size(s, P.Params(**kw)) > 0

@@ -1,0 +1,110 @@
+"""GPU parity of the alternatives the paper evaluates beside its main method:
+winsorised min-max and MAD normalisation of d_E (Sec. 6.3, Table 4), r_std in
+place of r_E (Appendix D) and the centroid over the non-window keys
+(Appendix B.6).  Each runs through the C ABI against the oracle with the same
+options, to the tolerances of parity_utils.
+"""
+import sys
+
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from parity_utils import gpu_pass
+from test_gpu_parity import check_all_selections_valid, check_compact, check_per_head
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_06663_amd  # noqa: F401  (fails loudly if the library is not built)
+    oracle.build(force=False)
+
+
+def say(msg):
+    print(f"[gpu-alternatives] {msg}", file=sys.stderr, flush=True)
+
+
+def opts(name):
+    import paper_2609_06663_amd as P
+    return {
+        "winsor1": P.Params(norm_mode=P.NORM_WINSOR, winsor_q=0.01),
+        "winsor5": P.Params(norm_mode=P.NORM_WINSOR, winsor_q=0.05),
+        "mad": P.Params(norm_mode=P.NORM_MAD, mad_tau=1.0),
+        "mad_tau3": P.Params(norm_mode=P.NORM_MAD, mad_tau=3.0),
+        "rstd": P.Params(redundancy=P.RED_STD),
+        "prefix": P.Params(centroid_scope=P.CENTROID_PREFIX),
+        "all": P.Params(norm_mode=P.NORM_MAD, redundancy=P.RED_STD, centroid_scope=P.CENTROID_PREFIX,
+                        imp_mode=P.IMP_ATTN_VNORM),
+    }[name]
+
+
+@pytest.mark.parametrize("name", ["winsor1", "winsor5", "mad", "mad_tau3", "rstd", "prefix", "all"])
+def test_alternative_bf16_d128(name):
+    wl = W.custom(81, L=2, Hq=8, Hkv=2, D=128, w=4, seqlens=[1500, 333, 70], dtype="bf16", budget=[300, 60, 9],
+                  group=64)
+    say(f"{name}: bf16 head_dim 128, ragged sequences")
+    p = opts(name)
+    g = gpu_pass(wl, params=p)
+    check_per_head(wl, g, params=p)
+    check_compact(wl, g)
+
+
+@pytest.mark.parametrize("name", ["winsor5", "mad", "rstd", "prefix"])
+def test_alternative_f32_d64(name):
+    # the block sweeps (fp32 keys, head_dim 64) carry the same partials
+    wl = W.custom(82, L=1, Hq=4, Hkv=2, D=64, w=8, seqlens=[900, 131], dtype="f32", budget=[200, 40], group=32)
+    say(f"{name}: fp32 head_dim 64")
+    p = opts(name)
+    g = gpu_pass(wl, params=p)
+    check_per_head(wl, g, params=p)
+
+
+def test_alternatives_long_sequence_split_epilogue():
+    import paper_2609_06663_amd as P
+    wl = W.custom(83, L=1, Hq=4, Hkv=1, D=128, w=4, seqlens=[40000], dtype="bf16", budget=[4000], group=256)
+    p = P.Params(norm_mode=P.NORM_WINSOR, winsor_q=0.05, redundancy=P.RED_STD, centroid_scope=P.CENTROID_PREFIX)
+    say("winsorised + r_std + prefix centroid on a 40000-token sequence (split epilogue)")
+    g = gpu_pass(wl, params=p)
+    check_per_head(wl, g, params=p)
+
+
+def test_alternatives_on_the_single_read_request(monkeypatch):
+    # the normalisations run after either score path; r_std and the prefix
+    # centroid make the request fall back to the two sweeps
+    monkeypatch.setenv("ECOKV_SCORE_PATH", "single")
+    wl = W.custom(84, L=2, Hq=28, Hkv=4, D=128, w=1, seqlens=[5003, 1200], dtype="bf16", budget=[700, 100],
+                  group=128)
+    for name in ("mad", "winsor1", "rstd", "prefix"):
+        say(f"{name} with the single-read path requested")
+        p = opts(name)
+        g = gpu_pass(wl, params=p)
+        check_per_head(wl, g, params=p)
+
+
+def test_identical_keys_with_quantile_norms():
+    import paper_2609_06663_amd as P
+    wl = W.custom(85, L=1, Hq=4, Hkv=2, D=128, w=4, seqlens=[600], dtype="bf16", budget=[100], group=32)
+    wl.K[0, 0, :] = wl.K[0, 0, 17]
+    for p in (P.Params(norm_mode=P.NORM_WINSOR, winsor_q=0.05), P.Params(norm_mode=P.NORM_MAD)):
+        say(f"identical keys in head 0, norm_mode {p.norm_mode}")
+        g = gpu_pass(wl, params=p)
+        # every distance is ~0: the quantile constants and s_E are rounding noise
+        check_per_head(wl, g, units=[(0, 1, 0)], params=p)
+        assr = g["scores"][0, 0]
+        assert (assr == assr).all()
+
+
+def test_stack28_mad_and_rstd_sampled():
+    import paper_2609_06663_amd as P
+    wl = W.stack28()
+    p = P.Params(norm_mode=P.NORM_MAD, redundancy=P.RED_STD)
+    say("stack28 with MAD normalisation and r_std (sampled oracle units)")
+    g = gpu_pass(wl, params=p)
+    check_all_selections_valid(wl, g)
+    check_compact(wl, g)
+    check_per_head(wl, g, units=[(0, 0, 0), (19, 1, 0), (27, 3, 0)], params=p)
