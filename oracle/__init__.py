@@ -107,6 +107,8 @@ def lib():
                                  ctypes.c_int, i32p, i32p, i32p, ctypes.c_int]
         L.ora_compact.argtypes = [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, i32p,
                                   ctypes.c_int, i32p, i32p, i32p, vp, vp]
+        L.ora_decode.argtypes = [vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                 ctypes.c_int, i32p, i32p, dp, dp]
         _lib = L
     return _lib
 
@@ -271,3 +273,23 @@ def compact(K, V, L, Hkv, cu_seqlens, D, idx, counts, offsets):
     if rc != 0:
         raise ValueError("index out of range")
     return Kc, Vc
+
+
+def decode(Q, Kc, Vc, L, Hq, Hkv, B, D, counts, offsets):
+    """Decode attention of one query per (layer, query head, sequence) over the
+    compressed cache.  Q [L][Hq][B][D] (uint16 bf16 bits or float32), Kc / Vc
+    [entries][D] as written by compact, counts / offsets [L][Hkv][B].
+    Returns O [L][Hq][B][D] and lse [L][Hq][B] (float64)."""
+    Q = np.ascontiguousarray(Q)
+    Kc = np.ascontiguousarray(Kc)
+    Vc = np.ascontiguousarray(Vc)
+    code = _dtype_code(Q)
+    assert _dtype_code(Kc) == code and _dtype_code(Vc) == code
+    O = np.zeros((L, Hq, B, D), np.float64)
+    lse = np.zeros((L, Hq, B), np.float64)
+    rc = lib().ora_decode(Q.ctypes.data, Kc.ctypes.data, Vc.ctypes.data, code, L, Hq, Hkv, B, D,
+                          _ip(np.ascontiguousarray(counts, np.int32)), _ip(np.ascontiguousarray(offsets, np.int32)),
+                          _dp(O), _dp(lse))
+    if rc != 0:
+        raise ValueError("invalid decode arguments")
+    return O, lse

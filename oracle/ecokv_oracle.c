@@ -14,7 +14,9 @@
  *   - rescaled diversity and final score S (Sec. 5.2, Eq. (7));
  *   - top-k over the non-window tokens plus the whole window (Sec. 3),
  *     per head or flattened across the heads of a layer (AdaKV, Appendix A.1);
- *   - gather of the kept K/V rows.
+ *   - gather of the kept K/V rows;
+ *   - decode attention of one new query per head over the kept rows (the
+ *     generation step that reads the compressed cache, Sec. 3).
  *
  * Who may use it: the test-suite, the package smoke check and the benchmark's
  * CPU-baseline leg.  The HIP library never links, loads or calls this file and
@@ -646,6 +648,55 @@ int ora_compact(const void *K, const void *V, int esize, int L, int Hkv, int B,
                     memcpy((char *)Kc + ((size_t)offsets[u] + j) * row, (const char *)K + (base + i) * row, row);
                     memcpy((char *)Vc + ((size_t)offsets[u] + j) * row, (const char *)V + (base + i) * row, row);
                 }
+            }
+    return 0;
+}
+
+/* Decode attention over the compressed cache (Sec. 3: generation attends to
+ * the kept rows).  For layer l, query head q (KV head h = q / G) and sequence
+ * s, unit u = (l, h, s) owns the n = counts[u] rows offsets[u] .. of Kc / Vc:
+ *   x_j = q . Kc[j] / sqrt(D),  O = sum_j softmax(x)_j Vc[j],
+ *   lse = log sum_j exp(x_j)  (max-subtracted).
+ * Q [L][Hq][B][D] (dtype), O [L][Hq][B][D], lse [L][Hq][B].  A unit with no
+ * rows gives O = 0 and lse = -inf. */
+int ora_decode(const void *Q, const void *Kc, const void *Vc, int dtype, int L, int Hq, int Hkv, int B, int D,
+               const int32_t *counts, const int32_t *offsets, double *O, double *lse)
+{
+    if (L < 0 || Hkv < 1 || Hq % Hkv != 0 || B < 1 || D < 1) return -1;
+    const int G = Hq / Hkv;
+    const double inv_sqrt_d = 1.0 / sqrt((double)D);
+    for (int l = 0; l < L; ++l)
+        for (int q = 0; q < Hq; ++q)
+            for (int s = 0; s < B; ++s) {
+                const int h = q / G;
+                const int64_t u = ((int64_t)l * Hkv + h) * B + s;
+                const int64_t r = ((int64_t)l * Hq + q) * B + s;
+                const int n = counts[u];
+                double *o = O + (size_t)r * D;
+                for (int d = 0; d < D; ++d) o[d] = 0.0;
+                if (n <= 0) {
+                    lse[r] = -INFINITY;
+                    continue;
+                }
+                double *x = malloc((size_t)n * sizeof(double));
+                if (!x) return -2;
+                double m = -INFINITY;
+                for (int j = 0; j < n; ++j) {
+                    double dot = 0.0;
+                    for (int d = 0; d < D; ++d)
+                        dot += ora_get(Q, dtype, (size_t)r * D + d) *
+                               ora_get(Kc, dtype, ((size_t)offsets[u] + j) * D + d);
+                    x[j] = dot * inv_sqrt_d;
+                    if (x[j] > m) m = x[j];
+                }
+                double z = 0.0;
+                for (int j = 0; j < n; ++j) z += exp(x[j] - m);
+                for (int j = 0; j < n; ++j) {
+                    const double pj = exp(x[j] - m) / z;
+                    for (int d = 0; d < D; ++d) o[d] += pj * ora_get(Vc, dtype, ((size_t)offsets[u] + j) * D + d);
+                }
+                lse[r] = m + log(z);
+                free(x);
             }
     return 0;
 }

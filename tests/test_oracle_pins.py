@@ -720,3 +720,55 @@ def test_prefix_centroid_ignores_the_window_keys(ora):
     a1 = ora.score_unit(K, Q, w, trace=True)
     a2 = ora.score_unit(K2, Q, w, trace=True)
     assert np.abs(a2["dE"][:P] - a1["dE"][:P]).max() > 1e-3
+
+
+# --------------------------------------------------------------------------
+# Decode attention over the compressed cache (the generation step, Sec. 3)
+# --------------------------------------------------------------------------
+
+def test_decode_one_row_returns_its_value(ora):
+    r = np.random.default_rng(90)
+    D = 16
+    Q = f32(r.standard_normal((1, 1, 1, D)))
+    Kc, Vc = f32(r.standard_normal((1, D))), f32(r.standard_normal((1, D)))
+    O, lse = ora.decode(Q, Kc, Vc, 1, 1, 1, 1, D, [[[1]]], [[[0]]])
+    np.testing.assert_allclose(O[0, 0, 0], Vc[0].astype(np.float64), rtol=1e-15)
+    x = float(np.dot(Q[0, 0, 0].astype(np.float64), Kc[0].astype(np.float64)) / 4.0)
+    assert lse[0, 0, 0] == pytest.approx(x, rel=1e-14)
+
+
+def test_decode_identical_keys_average_the_values(ora):
+    r = np.random.default_rng(91)
+    D, n = 8, 13
+    Kc = f32(np.tile(r.standard_normal(D), (n, 1)))
+    Vc = f32(r.standard_normal((n, D)))
+    Q = f32(r.standard_normal((1, 1, 1, D)))
+    O, lse = ora.decode(Q, Kc, Vc, 1, 1, 1, 1, D, [[[n]]], [[[0]]])
+    np.testing.assert_allclose(O[0, 0, 0], Vc.astype(np.float64).mean(axis=0), rtol=1e-13)
+    x = float(np.dot(Q[0, 0, 0].astype(np.float64), Kc[0].astype(np.float64)) / np.sqrt(D))
+    assert lse[0, 0, 0] == pytest.approx(x + np.log(n), rel=1e-13)
+
+
+def test_decode_matches_torch_attention_and_logsumexp(ora):
+    from scipy.special import logsumexp
+    r = np.random.default_rng(92)
+    L, Hq, Hkv, B, D = 2, 6, 2, 2, 32
+    G = Hq // Hkv
+    counts = r.integers(1, 40, size=(L, Hkv, B)).astype(np.int32)
+    offsets = np.concatenate([[0], np.cumsum(counts.reshape(-1))[:-1]]).reshape(L, Hkv, B).astype(np.int32)
+    n = int(counts.sum())
+    Kc, Vc = f32(r.standard_normal((n, D)) * 2), f32(r.standard_normal((n, D)))
+    Q = f32(r.standard_normal((L, Hq, B, D)))
+    O, lse = ora.decode(Q, Kc, Vc, L, Hq, Hkv, B, D, counts, offsets)
+    for l in range(L):
+        for q in range(Hq):
+            for s in range(B):
+                h = q // G
+                o, c = offsets[l, h, s], counts[l, h, s]
+                k = torch.from_numpy(Kc[o:o + c].astype(np.float64))
+                v = torch.from_numpy(Vc[o:o + c].astype(np.float64))
+                qq = torch.from_numpy(Q[l, q, s].astype(np.float64))
+                ref = torch.nn.functional.scaled_dot_product_attention(qq[None, None], k[None], v[None])[0, 0]
+                np.testing.assert_allclose(O[l, q, s], ref.numpy(), rtol=1e-12, atol=1e-14)
+                x = (k @ qq).numpy() / np.sqrt(D)
+                assert lse[l, q, s] == pytest.approx(logsumexp(x), rel=1e-13)
