@@ -54,7 +54,7 @@ STAGE_KERNELS = {
     "sweep2_stream": ["k_fs2s"], "sweep2_block": ["k_fs2", "k_pass2"], "epilogue": ["k_epi_unit"],
     "epilogue1": ["k_epi1"], "epilogue2": ["k_epi2"], "single_read": ["k_fused"],
     "select": ["k_select_reg", "k_select"], "compact": ["k_compact"], "vnorm": ["k_vnorm"],
-    "dquant": ["k_dquant"],
+    "dquant": ["k_dquant", "k_dquant_reg"], "decode": ["k_decode"], "decode_merge": ["k_decode_merge"],
 }
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, vendor figure
 COPY_BYTES = 1 << 30  # size of the calibration copy in --counter-run
@@ -336,6 +336,43 @@ def main():
             alternatives["dquant_mad_us"] = round(st_a["dquant"][0] / st_a["dquant"][1] * 1e3, 2)
         del ws_a
 
+    # Decode attention over the compressed cache the pass just wrote: one new
+    # query per (layer, query head), all kept rows of its KV head.
+    log("decode attention over the compressed cache")
+    gq = torch.Generator(device="cpu").manual_seed(5)
+    Qd = torch.randn((L, Hq, 1, D), generator=gq).to(torch.bfloat16).to(dev)
+    Od = torch.empty((L, Hq, 1, D), dtype=torch.float32, device=dev)
+    lsed = torch.empty((L, Hq, 1), dtype=torch.float32, device=dev)
+    ws_d = torch.empty(max(P.ecokv_decode_workspace_size(shape, b), 256), dtype=torch.uint8, device=dev)
+
+    def decode():
+        P.ecokv_decode(Qd, ep.Kc, ep.Vc, shape, ep.counts, ep.offsets, b, Od, lsed, ws_d)
+
+    decode()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        decode()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    os.environ["ECOKV_STAGE_TIMING"] = "1"
+    P.ecokv_stage_times()
+    for _ in range(args.steps):
+        decode()
+    torch.cuda.synchronize()
+    dstages = P.ecokv_stage_times()
+    os.environ["ECOKV_STAGE_TIMING"] = "0"
+    dk_s = dstages["decode"][0] / dstages["decode"][1] / 1e3
+    bytes_dec = 2 * n_idx * D * e + 2 * L * Hq * D * e  # Kc, Vc and the queries
+    decode_att = {"call_ms": round(e0.elapsed_time(e1) / args.steps, 4),
+                  "decode_kernel_us": round(dk_s * 1e6, 2),
+                  "merge_kernel_us": round(dstages["decode_merge"][0] / dstages["decode_merge"][1] * 1e3, 2),
+                  "algorithmic_bytes": bytes_dec,
+                  "decode_GBs": round(bytes_dec / dk_s / 1e9, 1),
+                  "frac_of_hbm_peak": round(bytes_dec / dk_s / 1e9 / HBM_PEAK_GBS, 4)}
+    del ws_d
+
     extras = {}
     if args.extras:
         for frac in (0.1, 0.4):
@@ -405,6 +442,7 @@ def main():
         "head_budgets": head_budgets,
         "value_norm": value_norm,
         "alternatives": alternatives,
+        "decode_attention": decode_att,
     }
     if extras:
         out["extras"] = extras

@@ -236,6 +236,30 @@ int ecokv_compact(const void *K, const void *V, int dtype, const ecokv_shape *sh
                   const int32_t *budget, const int32_t *idx, const int32_t *counts,
                   const int32_t *offsets, void *Kc, void *Vc, void *stream);
 
+/* Workspace bytes of ecokv_decode for this shape and max_count (>= 1). */
+int ecokv_decode_workspace_size(const ecokv_shape *shape, int32_t max_count, size_t *bytes);
+
+/* Decode attention over the compressed cache: the generation step that reads
+ * the kept rows (Sec. 3).  For layer l, query head q (KV head h = q / G, G =
+ * H_q / H_kv) and sequence s, unit u = (l, h, s) owns rows offsets[u] ..
+ * offsets[u] + counts[u] - 1 of Kc / Vc, and
+ *   O[l][q][s] = sum_j softmax_j(Q_dec[l][q][s] . Kc[j] / sqrt(D)) Vc[j],
+ *   lse[l][q][s] = log sum_j exp(Q_dec[l][q][s] . Kc[j] / sqrt(D)).
+ *   Q_dec   [L][H_q][B][D]  one new query per head and sequence (dtype)
+ *   Kc, Vc  [entries][D]    as written by ecokv_compact (dtype)
+ *   counts, offsets  DEVICE [L][H_kv][B], as written by ecokv_select (any mode)
+ *   max_count  an upper bound of every counts[u] (e.g. the largest budget);
+ *           the work is split into chunks of rows up to it.  A unit with more
+ *           rows gets NaN outputs.
+ *   O       [L][H_q][B][D] float32 output;  lse [L][H_q][B] float32, may be NULL
+ *   workspace of ecokv_decode_workspace_size bytes, 256-byte aligned.
+ * Q_dec, Kc and Vc must be 16-byte aligned.  Arithmetic: fp32 accumulation;
+ * the softmax is computed online per row chunk and the chunks are merged by
+ * their log-sum-exp. */
+int ecokv_decode(const void *Q_dec, const void *Kc, const void *Vc, int dtype, const ecokv_shape *shape,
+                 const int32_t *counts, const int32_t *offsets, int32_t max_count, float *O, float *lse,
+                 void *workspace, size_t workspace_bytes, void *stream);
+
 /* PyramidKV's layer schedule (Appendix A.1), host only: for m = num_layers
  * layers sharing `total` tokens per head, the last layer gets
  * b^{m-1} = total / (beta m), the first b^0 = 2 total / m - b^{m-1}, and the

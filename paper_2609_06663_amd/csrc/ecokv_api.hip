@@ -517,6 +517,61 @@ int ecokv_compact(const void *K, const void *V, int dtype, const ecokv_shape *sh
     return ECOKV_OK;
 }
 
+int ecokv_decode_workspace_size(const ecokv_shape *shape, int32_t max_count, size_t *bytes)
+{
+    ShapeInfo si;
+    int rc = check_shape(shape, &si);
+    if (rc) return rc;
+    if (!bytes) return fail(ECOKV_EINVAL, "bytes is NULL");
+    if (max_count < 1) return fail(ECOKV_EINVAL, "max_count %d < 1", max_count);
+    *bytes = sizeof(float) * (size_t)si.L * si.Hq * si.B * (size_t)ecokv::decode_parts(max_count) * (si.D + 2);
+    return ECOKV_OK;
+}
+
+int ecokv_decode(const void *Q_dec, const void *Kc, const void *Vc, int dtype, const ecokv_shape *shape,
+                 const int32_t *counts, const int32_t *offsets, int32_t max_count, float *O, float *lse,
+                 void *workspace, size_t workspace_bytes, void *stream)
+{
+    ShapeInfo si;
+    int rc = check_shape(shape, &si);
+    if (rc) return rc;
+    if (dtype != ECOKV_BF16 && dtype != ECOKV_F32) return fail(ECOKV_EUNSUPPORTED, "dtype %d", dtype);
+    if (max_count < 1) return fail(ECOKV_EINVAL, "max_count %d < 1", max_count);
+    size_t need = 0;
+    if ((rc = ecokv_decode_workspace_size(shape, max_count, &need))) return rc;
+    if (si.L == 0) return ECOKV_OK;
+    if (!Q_dec || !Kc || !Vc || !counts || !offsets || !O)
+        return fail(ECOKV_EINVAL, "Q_dec, Kc, Vc, counts, offsets and O must be non-NULL");
+    if (!workspace) return fail(ECOKV_EINVAL, "workspace is NULL");
+    if (((uintptr_t)workspace & 255u) != 0) return fail(ECOKV_EINVAL, "workspace must be 256-byte aligned");
+    if (((uintptr_t)Q_dec & 15u) != 0 || ((uintptr_t)Kc & 15u) != 0 || ((uintptr_t)Vc & 15u) != 0)
+        return fail(ECOKV_EINVAL, "Q_dec, Kc and Vc must be 16-byte aligned");
+    if (workspace_bytes < need)
+        return fail(ECOKV_EWORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+    ecokv::DecodeArgs a;
+    memset(&a, 0, sizeof a);
+    a.Q = Q_dec;
+    a.Kc = Kc;
+    a.Vc = Vc;
+    a.counts = counts;
+    a.offsets = offsets;
+    a.O = O;
+    a.lse = lse;
+    a.part = static_cast<float *>(workspace);
+    a.L = si.L;
+    a.Hq = si.Hq;
+    a.Hkv = si.Hkv;
+    a.G = si.G;
+    a.B = si.B;
+    a.D = si.D;
+    a.max_count = max_count;
+    a.nparts = ecokv::decode_parts(max_count);
+    a.qscale = 1.4426950408889634f / sqrtf((float)si.D);
+    const hipError_t e = ecokv::decode_launch(a, dtype == ECOKV_BF16, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "ecokv_decode launch");
+    return ECOKV_OK;
+}
+
 int ecokv_pyramid_budgets(int num_layers, double total, double beta, int window, int32_t *out)
 {
     if (num_layers < 1 || !out) return fail(ECOKV_EINVAL, "num_layers %d < 1 or out is NULL", num_layers);

@@ -1,0 +1,288 @@
+// ecokv_decode kernels (gfx950): attention of one new query per (layer, query
+// head, sequence) over the compressed cache written by ecokv_compact -- the
+// generation step that reads the kept rows (Sec. 3).
+//
+// Split over rows (flash-decoding): block (c, u, z) takes chunk c of unit u's
+// rows for query heads QG z .. QG z + QG - 1 of the unit's G.  Each wave takes
+// kWaveRows consecutive rows in batches of NR load instructions; S =
+// row_bytes / 16 lanes cover a row with 16-byte loads (64 / S rows per
+// instruction), so Kc and Vc stream in coalesced.  The S lanes of a row add
+// their partial dot products by DPP butterflies; the online softmax (base 2)
+// keeps wave-uniform maxima (read lane by lane across the row groups); P.V accumulates in fp32, each lane over its 16-byte
+// segment of the head dimension, the next batch's loads in flight meanwhile.
+// A block merges its waves in LDS and writes one (max, sum, acc[D]) per query
+// to the workspace; k_decode_merge combines a query row's chunks.
+#include "ecokv_internal.h"
+
+namespace ecokv {
+
+typedef unsigned int u32x4d __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2d __attribute__((ext_vector_type(2)));
+
+constexpr int kDecThreads = 256;
+constexpr int kDecWaves = kDecThreads / kWave;
+constexpr int kWaveRows = 128;  // rows per wave
+constexpr int kDecChunk = kDecWaves * kWaveRows;
+constexpr int kDecQG = 8;       // query heads per block at most
+
+// a.lo * b.lo + a.hi * b.hi + c for packed bf16 pairs, fp32 accumulation.
+// (The words are passed by value: a bit cast applied to a vector element
+// inside an unrolled loop has compiled to element 0 for every index.)
+__device__ __forceinline__ float dot2_bf16(unsigned a, unsigned b, float c)
+{
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2d, a), __builtin_bit_cast(bf16x2d, b), c, false);
+}
+
+// Max over the 64 / S row groups of a value that is uniform within each group.
+template <int S>
+__device__ __forceinline__ float groups_max(float v)
+{
+    float M = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+#pragma unroll
+    for (int r = 1; r < kWave / S; ++r) M = fmaxf(M, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), r * S)));
+    return M;
+}
+
+template <bool BF16>
+__device__ __forceinline__ void unpack(const u32x4d &x, float (&f)[BF16 ? 8 : 4])
+{
+    if constexpr (BF16) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            f[2 * c] = __uint_as_float(x[c] << 16);
+            f[2 * c + 1] = __uint_as_float(x[c] & 0xffff0000u);
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) f[c] = __uint_as_float(x[c]);
+    }
+}
+
+template <bool BF16, int D, int QG>
+__global__ __launch_bounds__(kDecThreads) void k_decode(DecodeArgs a)
+{
+    constexpr int E = BF16 ? 2 : 4;
+    constexpr int RB = D * E;       // row bytes
+    constexpr int S = RB / 16;      // lanes per row
+    constexpr int RPI = kWave / S;  // rows per load instruction
+    constexpr int EL = 16 / E;      // elements per lane
+    constexpr int NR = 4;           // load instructions per batch
+    constexpr int BR = NR * RPI;    // rows per batch
+    __shared__ float cm[kDecWaves][QG], cl[kDecWaves][QG];
+    __shared__ float cacc[kDecWaves][QG][D];
+    const int c = blockIdx.x, u = blockIdx.y, z = blockIdx.z;
+    const Unit un = unit_of(u, a.Hkv, a.B);
+    const int lane = threadIdx.x & 63, wv = uniform_i32(threadIdx.x >> 6);
+    const int seg = lane % S;
+    // (u is the block's: the unit's count and offset are the same in every lane)
+    const int n = uniform_i32(min(a.counts[u], a.max_count));  // more rows than max_count: the merge writes NaN
+    const int64_t off = uniform_i32(a.offsets[u]);
+    const int row0 = (c * kDecWaves + wv) * kWaveRows;
+    const int nrows = max(0, min(n - row0, kWaveRows));
+    const int nq = min(QG, a.G - z * QG);
+
+    // this lane's 16-byte segment of every query (the logit scale
+    // log2(e) / sqrt(D) is applied after the dot product)
+    u32x4d qw[QG];
+#pragma unroll
+    for (int g = 0; g < QG; ++g) {
+        qw[g] = (u32x4d){0u, 0u, 0u, 0u};
+        if (g < nq) {
+            const int64_t qrow = ((int64_t)un.l * a.Hq + un.h * a.G + z * QG + g) * a.B + un.s;
+            qw[g] = *reinterpret_cast<const u32x4d *>(static_cast<const char *>(a.Q) + qrow * RB + seg * 16);
+        }
+    }
+
+    const int64_t base = (off + row0) * RB;
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char *>(uniform_ptr(static_cast<const char *>(a.Kc) + base)), (short)0, uniform_i32(nrows * RB),
+        0x00020000);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char *>(uniform_ptr(static_cast<const char *>(a.Vc) + base)), (short)0, uniform_i32(nrows * RB),
+        0x00020000);
+
+    float m[QG], ls[QG], acc[QG][EL];
+#pragma unroll
+    for (int g = 0; g < QG; ++g) {
+        m[g] = -INFINITY;
+        ls[g] = 0.f;
+#pragma unroll
+        for (int e = 0; e < EL; ++e) acc[g][e] = 0.f;
+    }
+
+    // lane l covers row l / S of an instruction's rows, bytes 16 (l % S): offset 16 l
+    auto load = [&](u32x4d (&kx)[NR], u32x4d (&vx)[NR], int b0) {
+#pragma unroll
+        for (int i = 0; i < NR; ++i) {
+            const int o = (b0 + i * RPI) * RB + lane * 16;
+            kx[i] = __builtin_bit_cast(u32x4d, __builtin_amdgcn_raw_buffer_load_b128(rk, o, 0, 0));
+            vx[i] = __builtin_bit_cast(u32x4d, __builtin_amdgcn_raw_buffer_load_b128(rv, o, 0, 0));
+        }
+    };
+    u32x4d kx[NR], vx[NR];
+    load(kx, vx, 0);
+    for (int b0 = 0; b0 < nrows; b0 += BR) {
+        // the next batch is in flight while this one is used (past the rows:
+        // no memory access, zeros)
+        u32x4d kn[NR], vn[NR];
+        load(kn, vn, b0 + BR);
+        __builtin_amdgcn_sched_barrier(0);
+        float x[NR][QG];
+#pragma unroll
+        for (int i = 0; i < NR; ++i) {
+            const bool valid = b0 + i * RPI + lane / S < nrows;
+            float kf[EL];
+            if constexpr (!BF16) unpack<BF16>(kx[i], kf);
+#pragma unroll
+            for (int g = 0; g < QG; ++g) {
+                float pd = 0.f;
+                if constexpr (BF16) {
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) pd = dot2_bf16(qw[g][w], kx[i][w], pd);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < EL; ++e) pd += __uint_as_float(qw[g][e]) * kf[e];
+                }
+                pd = row_sum<S>(pd);
+                x[i][g] = valid ? pd * a.qscale : -INFINITY;
+            }
+        }
+#pragma unroll
+        for (int g = 0; g < QG; ++g) {
+            float mb = x[0][g];
+#pragma unroll
+            for (int i = 1; i < NR; ++i) mb = fmaxf(mb, x[i][g]);
+            mb = groups_max<S>(mb);
+            const float mn = fmaxf(m[g], mb);  // finite: row b0 of the batch is valid
+            const float sc = __builtin_amdgcn_exp2f(m[g] - mn);
+            m[g] = mn;
+            ls[g] *= sc;
+#pragma unroll
+            for (int e = 0; e < EL; ++e) acc[g][e] *= sc;
+        }
+#pragma unroll
+        for (int i = 0; i < NR; ++i) {
+            float vf[EL];
+            unpack<BF16>(vx[i], vf);
+#pragma unroll
+            for (int g = 0; g < QG; ++g) {
+                const float p = __builtin_amdgcn_exp2f(x[i][g] - m[g]);
+                ls[g] += p;
+#pragma unroll
+                for (int e = 0; e < EL; ++e) acc[g][e] += p * vf[e];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < NR; ++i) {
+            kx[i] = kn[i];
+            vx[i] = vn[i];
+        }
+    }
+
+    // the rows of a wave are spread over its 64 / S row groups: add them up,
+    // then merge the block's waves through LDS (fixed order)
+#pragma unroll
+    for (int g = 0; g < QG; ++g)
+#pragma unroll
+        for (int msk = S; msk < kWave; msk <<= 1) {
+            ls[g] += __shfl_xor(ls[g], msk, kWave);
+#pragma unroll
+            for (int e = 0; e < EL; ++e) acc[g][e] += __shfl_xor(acc[g][e], msk, kWave);
+        }
+    if (lane < S) {
+#pragma unroll
+        for (int g = 0; g < QG; ++g) {
+#pragma unroll
+            for (int e = 0; e < EL; ++e) cacc[wv][g][seg * EL + e] = acc[g][e];
+            if (lane == 0) {
+                cm[wv][g] = m[g];
+                cl[wv][g] = ls[g];
+            }
+        }
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < nq * D; t += kDecThreads) {
+        const int g = t / D, d = t - g * D;
+        float M = cm[0][g];
+        for (int w2 = 1; w2 < kDecWaves; ++w2) M = fmaxf(M, cm[w2][g]);
+        float L = 0.f, A = 0.f;
+        if (M != -INFINITY)
+            for (int w2 = 0; w2 < kDecWaves; ++w2) {
+                const float wt = exp2f(cm[w2][g] - M);
+                L += cl[w2][g] * wt;
+                A += cacc[w2][g][d] * wt;
+            }
+        const int64_t qrow = ((int64_t)un.l * a.Hq + un.h * a.G + z * QG + g) * a.B + un.s;
+        float *pp = a.part + (qrow * a.nparts + c) * (D + 2);
+        pp[2 + d] = A;
+        if (d == 0) {
+            pp[0] = M;
+            pp[1] = L;
+        }
+    }
+}
+
+// One block per query row (D threads): the log-sum-exp merge of its chunks.
+__global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a)
+{
+    const int64_t qrow = blockIdx.x;
+    const int t = threadIdx.x;
+    const int s = (int)(qrow % a.B), q = (int)((qrow / a.B) % a.Hq), l = (int)(qrow / ((int64_t)a.B * a.Hq));
+    const int64_t u = ((int64_t)l * a.Hkv + q / a.G) * a.B + s;
+    const int n = a.counts[u];
+    const float *pp = a.part + qrow * a.nparts * (a.D + 2);
+    const int used = min((min(n, a.max_count) + kDecChunk - 1) / kDecChunk, a.nparts);
+    // (unrolled so that the chunks' loads are in flight together)
+    float M = -INFINITY;
+#pragma unroll 8
+    for (int p = 0; p < used; ++p) M = fmaxf(M, pp[(int64_t)p * (a.D + 2)]);
+    float L = 0.f, o = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll 8
+        for (int p = 0; p < used; ++p) {
+            const float *r = pp + (int64_t)p * (a.D + 2);
+            const float w = exp2f(r[0] - M);
+            L += r[1] * w;
+            if (t < a.D) o += r[2 + t] * w;
+        }
+    }
+    const bool bad = n > a.max_count || n < 0;
+    if (t < a.D) a.O[qrow * a.D + t] = bad ? NAN : (M == -INFINITY ? 0.f : o / L);
+    if (t == 0 && a.lse)
+        a.lse[qrow] = bad ? NAN : (M == -INFINITY ? -INFINITY : (M + log2f(L)) * 0.69314718055994531f);
+}
+
+// Query heads per block: all of G up to 8 (so that Kc / Vc are read once),
+// rounded up to 1, 2, 4 or 8; larger G takes several blocks of 8.
+static int decode_qg(int G) { return G > 4 ? kDecQG : G > 2 ? 4 : G; }
+
+template <bool BF16, int D>
+static void launch_dec(const DecodeArgs &a, dim3 grid, hipStream_t st)
+{
+    const int qg = decode_qg(a.G);
+    if (qg == 8) hipLaunchKernelGGL((k_decode<BF16, D, 8>), grid, dim3(kDecThreads), 0, st, a);
+    else if (qg == 4) hipLaunchKernelGGL((k_decode<BF16, D, 4>), grid, dim3(kDecThreads), 0, st, a);
+    else if (qg == 2) hipLaunchKernelGGL((k_decode<BF16, D, 2>), grid, dim3(kDecThreads), 0, st, a);
+    else hipLaunchKernelGGL((k_decode<BF16, D, 1>), grid, dim3(kDecThreads), 0, st, a);
+}
+
+int decode_parts(int max_count) { return (max_count + kDecChunk - 1) / kDecChunk; }
+
+hipError_t decode_launch(DecodeArgs a, bool bf16, hipStream_t st)
+{
+    const int U = a.L * a.Hkv * a.B;
+    if (U == 0) return hipSuccess;
+    const int qg = decode_qg(a.G);
+    const dim3 grid(a.nparts, U, (a.G + qg - 1) / qg);
+    if (bf16 && a.D == 128) ECOKV_TIMED("decode", st, (launch_dec<true, 128>(a, grid, st)));
+    else if (bf16) ECOKV_TIMED("decode", st, (launch_dec<true, 64>(a, grid, st)));
+    else if (a.D == 128) ECOKV_TIMED("decode", st, (launch_dec<false, 128>(a, grid, st)));
+    else ECOKV_TIMED("decode", st, (launch_dec<false, 64>(a, grid, st)));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const unsigned rows = (unsigned)((int64_t)a.L * a.Hq * a.B);
+    ECOKV_TIMED("decode_merge", st, hipLaunchKernelGGL(k_decode_merge, dim3(rows), dim3(128), 0, st, a));
+    return hipGetLastError();
+}
+
+}  // namespace ecokv

@@ -148,6 +148,23 @@ struct DQuantArgs {
 };
 hipError_t dquant_launch(const DQuantArgs &a, hipStream_t st);
 
+// Decode attention over the compressed cache (one query per query head).
+struct DecodeArgs {
+    const void *Q;        // [L][Hq][B][D]
+    const void *Kc;       // [entries][D]
+    const void *Vc;
+    const int32_t *counts;   // [L][Hkv][B]
+    const int32_t *offsets;  // [L][Hkv][B]
+    float *O;             // [L][Hq][B][D]
+    float *lse;           // [L][Hq][B] or null
+    float *part;          // [L][Hq][B][nparts][D + 2]: max, sum, acc per row chunk
+    int L, Hq, Hkv, G, B, D;
+    int max_count, nparts;
+    float qscale;         // log2(e) / sqrt(D)
+};
+int decode_parts(int max_count);
+hipError_t decode_launch(DecodeArgs a, bool bf16, hipStream_t st);
+
 WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16, bool vnorm);
 hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hipStream_t st, bool bf16);
 
@@ -250,6 +267,44 @@ __device__ __forceinline__ void load_seg(const void *row, int c, float *v)
             v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
         }
     }
+}
+
+// A value the caller knows to be equal in every lane of the wave, made
+// visibly so to the compiler (read from the first active lane): buffer
+// descriptors built from it then live in scalar registers, instead of every
+// buffer access being repeated for each distinct descriptor value.
+__device__ __forceinline__ int uniform_i32(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ int64_t uniform_i64(int64_t v)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+template <class T>
+__device__ __forceinline__ T *uniform_ptr(T *p)
+{
+    return reinterpret_cast<T *>(uniform_i64(reinterpret_cast<int64_t>(p)));
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dppf(float x)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the S lanes of a row group (S = 8, 16 or 32), in every lane, by DPP
+// butterflies: lane ^ 1, lane ^ 2 (quad permutes), then the mirrored lane
+// within 8 and within 16 (each pairs a lane with the other half); the same
+// additions in every lane, so all lanes hold the same sum.
+template <int S>
+__device__ __forceinline__ float row_sum(float x)
+{
+    x += dppf<0xB1>(x);   // quad_perm [1, 0, 3, 2]
+    x += dppf<0x4E>(x);   // quad_perm [2, 3, 0, 1]
+    x += dppf<0x141>(x);  // row_half_mirror
+    if constexpr (S >= 16) x += dppf<0x140>(x);  // row_mirror
+    if constexpr (S == 32) x += __shfl_xor(x, 16, kWave);
+    return x;
 }
 
 // Order-preserving map of a float score to an unsigned radix key: larger

@@ -1732,7 +1732,7 @@ static int rows_per_block(int D, bool bf16) { return score_fast_path(D, bf16) ? 
 // A wave takes 64 consecutive rows; its load instruction q covers the 16-byte
 // pieces 64q .. 64q+63 of those rows (SEGS pieces per row), so consecutive
 // lanes read consecutive bytes.  The SEGS partial sums of squares of a row
-// are combined by shuffles and parked in LDS; lane r then pools the window
+// are combined by DPP butterflies and parked in LDS; lane r then pools the window
 // attention around row r (zero padding, fixed divisor, as the epilogue) and
 // writes the product.  Rows at or past P read as zero (buffer range).
 // ---------------------------------------------------------------------------
@@ -1749,12 +1749,12 @@ __global__ __launch_bounds__(kVnThreads) void k_vnorm(ScoreArgs a)
     const int P = T - a.w;
     const int row0 = blockIdx.x * kVnThreads;
     if (row0 >= P) return;
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wv = uniform_i32(threadIdx.x >> 6);
     const int wrow = row0 + 64 * wv;                      // the wave's first row
     const int nrows = max(0, min(64, P - wrow));          // rows of the wave below P
     const char *vw = static_cast<const char *>(a.V) + (unit_row0(a, un) + wrow) * kRowBytes;
-    const __amdgpu_buffer_rsrc_t rv =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(vw), (short)0, nrows * kRowBytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char *>(uniform_ptr(vw)), (short)0, uniform_i32(nrows * kRowBytes), 0x00020000);
     u32x4 x[SEGS];
 #pragma unroll
     for (int q = 0; q < SEGS; ++q)
@@ -1772,8 +1772,7 @@ __global__ __launch_bounds__(kVnThreads) void k_vnorm(ScoreArgs a)
                 s2 += v * v;
             }
         }
-#pragma unroll
-        for (int m = 1; m < SEGS; m <<= 1) s2 += __shfl_xor(s2, m, kWave);
+        s2 = row_sum<SEGS>(s2);
         if (lane % SEGS == 0) n2s[64 * wv + (64 / SEGS) * q + lane / SEGS] = s2;
     }
     __syncthreads();

@@ -525,8 +525,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
         // consecutive 16-byte pieces (1 KiB per wave instruction) into a
         // swizzled stage (piece g at g ^ ((g >> 3) & 7)), then each thread takes
         // its 32 consecutive scores from it.
-        const __amdgpu_buffer_rsrc_t rs =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(g.base), (short)0, n * 4, 0x00020000);
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(uniform_ptr(g.base)), (short)0, uniform_i32(n) * 4, 0x00020000);
         u32x4_t x[KPT / 4];
 #pragma unroll
         for (int q = 0; q < KPT / 4; ++q)
@@ -541,8 +541,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
             for (int e = 0; e < 4; ++e) kk[4 * q + e] = score_key(__uint_as_float(y[e]));
         }
     } else if (nh == 1) {
-        const __amdgpu_buffer_rsrc_t rs =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(g.base), (short)0, n * 4, 0x00020000);
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(uniform_ptr(g.base)), (short)0, uniform_i32(n) * 4, 0x00020000);
 #pragma unroll
         for (int q = 0; q < KPT / 4; ++q) {
             const u32x4_t x = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (v0 + 4 * q) * 4, 0, 0));
@@ -768,8 +768,8 @@ __global__ __launch_bounds__(kSelThreads) void k_dquant_reg(DQuantArgs a)
     const int P = a.seq.cu[un.s + 1] - a.seq.cu[un.s] - a.w;  // <= kDqKeys (checked on the host)
     const float *d = a.d + ((int64_t)un.l * a.Hkv + un.h) * a.Ptot + (a.seq.cu[un.s] - (int64_t)un.s * a.w);
     const int v0 = threadIdx.x * KPT;
-    const __amdgpu_buffer_rsrc_t rs =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(d), (short)0, P * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(uniform_ptr(d)), (short)0, uniform_i32(P) * 4, 0x00020000);
     typedef float f32x4_t __attribute__((ext_vector_type(4)));
     float dv[KPT];
     uint32_t kk[KPT];

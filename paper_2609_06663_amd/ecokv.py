@@ -31,6 +31,7 @@ STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7, imp_m
 
 EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_score", "ecokv_score_v", "ecokv_index_count",
            "ecokv_index_count_mode", "ecokv_select", "ecokv_compact", "ecokv_pyramid_budgets",
+           "ecokv_decode_workspace_size", "ecokv_decode",
            "ecokv_last_error", "ecokv_stage_times"]
 
 
@@ -92,6 +93,9 @@ def _load():
     lib.ecokv_score_v.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_index_count.argtypes = [sp, i32p, ctypes.POINTER(ctypes.c_int64)]
     lib.ecokv_index_count_mode.argtypes = [sp, ctypes.c_int, i32p, ctypes.POINTER(ctypes.c_int64)]
+    lib.ecokv_decode_workspace_size.argtypes = [sp, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
+    lib.ecokv_decode.argtypes = [vp, vp, vp, ctypes.c_int, sp, vp, vp, ctypes.c_int32, vp, vp, vp,
+                                 ctypes.c_size_t, vp]
     lib.ecokv_pyramid_budgets.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_int, i32p]
     lib.ecokv_select.argtypes = [vp, sp, ctypes.c_int, i32p, vp, vp, vp, vp]
     lib.ecokv_compact.argtypes = [vp, vp, ctypes.c_int, sp, ctypes.c_int, i32p, vp, vp, vp, vp, vp, vp]
@@ -233,6 +237,28 @@ def ecokv_compact(K: torch.Tensor, V: torch.Tensor, shape: Shape, mode: int, bud
     _check(lib.ecokv_compact(_ptr(K), _ptr(V), _dtype_code(K), ctypes.byref(shape.c), int(mode),
                              _budget(shape, budget, mode), _ptr(idx), _ptr(counts), _ptr(offsets), _ptr(Kc),
                              _ptr(Vc), _stream(stream)))
+
+
+def ecokv_decode_workspace_size(shape: Shape, max_count: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib.ecokv_decode_workspace_size(ctypes.byref(shape.c), int(max_count), ctypes.byref(n)))
+    return n.value
+
+
+def ecokv_decode(Q_dec: torch.Tensor, Kc: torch.Tensor, Vc: torch.Tensor, shape: Shape, counts: torch.Tensor,
+                 offsets: torch.Tensor, max_count: int, O: torch.Tensor, lse: Optional[torch.Tensor] = None,
+                 workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Enqueue ecokv_decode (attention of one query per head over the compressed cache)."""
+    if workspace is None:
+        workspace = torch.empty(max(ecokv_decode_workspace_size(shape, max_count), 256), dtype=torch.uint8,
+                                device=Q_dec.device)
+    if Kc.dtype != Q_dec.dtype or Vc.dtype != Q_dec.dtype:
+        raise TypeError("Q_dec, Kc and Vc must share one element type")
+    if counts.dtype != torch.int32 or offsets.dtype != torch.int32:
+        raise TypeError("counts and offsets are int32")
+    _check(lib.ecokv_decode(_ptr(Q_dec), _ptr(Kc), _ptr(Vc), _dtype_code(Q_dec), ctypes.byref(shape.c),
+                            _ptr(counts), _ptr(offsets), int(max_count), _ptr(O), _ptr(lse), _ptr(workspace),
+                            workspace.numel(), _stream(stream)))
 
 
 def ecokv_last_error() -> str:

@@ -224,3 +224,24 @@ def test_alternative_options_defaults_and_checks(P):
     for kw in (dict(norm_mode=P.NORM_WINSOR, winsor_q=0.0), dict(norm_mode=P.NORM_MAD, mad_tau=2.0),
                dict(redundancy=P.RED_STD), dict(centroid_scope=P.CENTROID_PREFIX)):
         assert P.ecokv_workspace_size(s, P.Params(**kw)) > 0
+
+
+def test_decode_checks_before_device_work(P):
+    from paper_2609_06663_amd import ecokv as E
+    s = P.Shape(2, 8, 2, 128, 4, [0, 100])
+    assert P.ecokv_decode_workspace_size(s, 512) == 4 * 2 * 8 * 1 * 1 * 130
+    assert P.ecokv_decode_workspace_size(s, 513) == 4 * 2 * 8 * 1 * 2 * 130
+    with pytest.raises(P.EcoKVError):
+        P.ecokv_decode_workspace_size(s, 0)
+    lib = E.lib
+    fake = ctypes.c_void_p(256)
+    ws = P.ecokv_decode_workspace_size(s, 100)
+    args = lambda **kw: [kw.get("Q", fake), fake, fake, kw.get("dtype", 0), ctypes.byref(s.c), fake, fake,
+                         kw.get("mc", 100), kw.get("O", fake), None, kw.get("ws", fake), kw.get("wsb", ws), None]
+    assert lib.ecokv_decode(*args(Q=None)) == -1
+    assert lib.ecokv_decode(*args(O=None)) == -1
+    assert lib.ecokv_decode(*args(dtype=5)) == -3
+    assert lib.ecokv_decode(*args(mc=0)) == -1
+    assert lib.ecokv_decode(*args(wsb=ws - 1)) == -2
+    assert lib.ecokv_decode(*args(ws=ctypes.c_void_p(260))) == -1
+    assert lib.ecokv_decode(*args(Q=ctypes.c_void_p(264))) == -1   # not 16-byte aligned
