@@ -192,6 +192,27 @@ int ecokv_score_v(const void *K, const void *V, const void *Q_win, int dtype, co
                   const ecokv_params *params, float *scores, float *lambda, float *stats,
                   void *workspace, size_t workspace_bytes, void *stream);
 
+/* ecokv_score_v with the results of the first sweep over K supplied by the
+ * caller, so that K is read only once.  A prefill that runs flash attention
+ * over the window queries has each window row's softmax max and sum as a
+ * by-product of its epilogue, and the pass that writes K into the cache can
+ * accumulate the two key sums; passing them here skips the first sweep
+ * (Sec. 3 window attention; Eq. (1) centroid; Appendix A.1 mu).
+ *   pre  DEVICE [L][H_kv][B][2D + 2R] float32, per unit u:
+ *          [0, D)          sum over its T keys of k_i
+ *          [D, 2D)         sum over its T keys of k_i / max(|k_i|, 1e-12)
+ *          [2D, 2D+R)      per window row r = g w + j (query head g of the
+ *                          group, window row j): the max over its visible
+ *                          keys of q.k / sqrt(D)
+ *          [2D+R, 2D+2R)   the sum over its visible keys of
+ *                          exp(q.k / sqrt(D) - that max)
+ *        (visible: keys <= T - w + j when causal, all T otherwise).
+ * Everything else as ecokv_score_v; the two-sweep path's second sweep and
+ * epilogue run as usual.  pre == NULL is ecokv_score_v. */
+int ecokv_score_pre(const void *K, const void *V, const void *Q_win, int dtype, const ecokv_shape *shape,
+                    const ecokv_params *params, const float *pre, float *scores, float *lambda, float *stats,
+                    void *workspace, size_t workspace_bytes, void *stream);
+
 /* Number of int32 entries ecokv_select writes to idx:
  * L * H_kv * sum_s min(budget[s], T_s) (ECOKV_PER_HEAD and ECOKV_LAYER_FLAT). */
 int ecokv_index_count(const ecokv_shape *shape, const int32_t *budget, int64_t *count);

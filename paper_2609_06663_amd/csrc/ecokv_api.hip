@@ -297,6 +297,14 @@ int ecokv_score_v(const void *K, const void *V, const void *Q_win, int dtype, co
                   const ecokv_params *params, float *scores, float *lambda, float *stats, void *workspace,
                   size_t workspace_bytes, void *stream)
 {
+    return ecokv_score_pre(K, V, Q_win, dtype, shape, params, nullptr, scores, lambda, stats, workspace,
+                           workspace_bytes, stream);
+}
+
+int ecokv_score_pre(const void *K, const void *V, const void *Q_win, int dtype, const ecokv_shape *shape,
+                    const ecokv_params *params, const float *pre, float *scores, float *lambda, float *stats,
+                    void *workspace, size_t workspace_bytes, void *stream)
+{
     ShapeInfo si;
     int rc = check_shape(shape, &si);
     if (rc) return rc;
@@ -349,6 +357,8 @@ int ecokv_score_v(const void *K, const void *V, const void *Q_win, int dtype, co
     a.red_std = params->redundancy == ECOKV_RED_STD;
     a.centroid_prefix = params->centroid_scope == ECOKV_CENTROID_PREFIX;
     a.winsor_q = params->winsor_q;
+    a.pre = pre;
+    if (pre && ((uintptr_t)pre & 3u) != 0) return fail(ECOKV_EINVAL, "pre must be 4-byte aligned");
     if ((rc = fill_seqtab(shape, nullptr, si.w, &a.seq, nullptr))) return rc;
     const hipError_t e = ecokv::score_launch(a, static_cast<char *>(workspace), lay, si.maxT,
                                              static_cast<hipStream_t>(stream), dtype == ECOKV_BF16);

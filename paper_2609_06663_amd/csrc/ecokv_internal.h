@@ -76,6 +76,7 @@ struct ScoreArgs {
     const float *dq; // [U][2] quantile pair of d_E per unit (winsorised or MAD norm)
     int red_std;     // lambda uses r_std (Appendix D) instead of r_E
     int centroid_prefix;  // kbar over the non-window keys (Appendix B.6)
+    const float *pre;     // [U][2D + 2R] caller-supplied first-sweep sums (ecokv_score_pre), or null
     SeqTab seq;
 };
 

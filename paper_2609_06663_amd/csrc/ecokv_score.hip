@@ -1106,6 +1106,43 @@ __global__ __launch_bounds__(256, 2) void k_fs1s(ScoreArgs a)
 // ends with the same value.
 constexpr int kReduceThreads = 1024;
 
+// Component c of kbar from the sum of the unit's T keys: divided by T, or,
+// with the centroid over the non-window keys, the w window rows taken out
+// and divided by P.
+__device__ __forceinline__ float centroid_component(const ScoreArgs &a, const Unit &un, int T, int c, float s)
+{
+    if (!a.centroid_prefix) return s / (float)T;
+    const int64_t r0 = unit_row0(a, un) + (T - a.w);
+    float ws = 0.f;
+    for (int j = 0; j < a.w; ++j) {
+        const int64_t off = (r0 + j) * a.D + c;
+        ws += a.kbf16 ? __uint_as_float((uint32_t)static_cast<const uint16_t *>(a.K)[off] << 16)
+                      : static_cast<const float *>(a.K)[off];
+    }
+    return (s - ws) / (float)(T - a.w);
+}
+
+// The anchors from sums a prefill supplied (ecokv_score_pre) instead of the
+// first sweep: sum k and sum k/|k| over the T keys, and per window row its
+// max logit (natural units) and sum of exp(logit - max).  The row maxima are
+// kept in base 2, as the first sweep produces them.
+__global__ __launch_bounds__(256) void k_pre_anchors(ScoreArgs a)
+{
+    const int u = blockIdx.x;
+    const Unit un = unit_of(u, a.Hkv, a.B);
+    const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
+    const int stride = 2 * a.D + 2 * a.R;
+    const float *p = a.pre + (int64_t)u * stride;
+    float *anc = a.anchors + (int64_t)u * stride;
+    for (int c = threadIdx.x; c < stride; c += blockDim.x) {
+        const float v = p[c];
+        if (c < a.D) anc[c] = centroid_component(a, un, T, c, v);
+        else if (c < 2 * a.D) anc[c] = v / (float)T;
+        else if (c < 2 * a.D + a.R) anc[c] = v * kLog2e;
+        else anc[c] = v;
+    }
+}
+
 __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
 {
     const int u = blockIdx.x;
@@ -1123,22 +1160,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
             for (int b = q; b < nb; b += 4) s += p[(int64_t)b * stride + c];
             s += __shfl_xor(s, 1, 4);
             s += __shfl_xor(s, 2, 4);
-            if (q == 0) {
-                float n = (float)T;
-                if (c < a.D && a.centroid_prefix) {
-                    // kbar over the P non-window keys: the window rows leave the sum
-                    const int64_t r0 = unit_row0(a, un) + (T - a.w);
-                    float ws = 0.f;
-                    for (int j = 0; j < a.w; ++j) {
-                        const int64_t off = (r0 + j) * a.D + c;
-                        ws += a.kbf16 ? __uint_as_float((uint32_t)static_cast<const uint16_t *>(a.K)[off] << 16)
-                                      : static_cast<const float *>(a.K)[off];
-                    }
-                    s -= ws;
-                    n = (float)(T - a.w);
-                }
-                anc[c] = s / n;
-            }
+            if (q == 0) anc[c] = c < a.D ? centroid_component(a, un, T, c, s) : s / (float)T;
         } else {
             const int r = c - 2 * a.D;
             float m = -INFINITY, s = 0.f;
@@ -1896,7 +1918,7 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     // The single-read path is selected with ECOKV_SCORE_PATH=single (read on
     // every call); the two-sweep path is the default.
     const char *path = getenv("ECOKV_SCORE_PATH");
-    const bool want_single = path && strcmp(path, "single") == 0;
+    const bool want_single = path && strcmp(path, "single") == 0 && !a.pre;
     int fgrid = 0;
     // (its partials carry no sum of d_E^2 and its centroid spans all T keys)
     if (want_single && !a.red_std && !a.centroid_prefix &&
@@ -1916,16 +1938,22 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         a.rpb1 = rows_per_block(a.D, bf16);
         a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
         const dim3 grid(a.nch1, U);
-        if (score_fast_path(a.D, bf16) && a.R <= 32) {
-            // streaming sweep 1: one 32-row window operand
-            a.rpb1 = fast::kS2Keys;
-            a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
-            ECOKV_TIMED("sweep1_stream", st, hipLaunchKernelGGL(fast::k_fs1s, dim3(a.nch1, U), dim3(256), 0, st, a));
+        if (a.pre) {
+            // the first sweep's sums come from the caller: K is read once
+            ECOKV_TIMED("pre_anchors", st, hipLaunchKernelGGL(k_pre_anchors, dim3(U), dim3(256), 0, st, a));
         } else {
-            ECOKV_TIMED("sweep1_block", st, launch_sweep(1, a, grid, st, bf16));
+            if (score_fast_path(a.D, bf16) && a.R <= 32) {
+                // streaming sweep 1: one 32-row window operand
+                a.rpb1 = fast::kS2Keys;
+                a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
+                ECOKV_TIMED("sweep1_stream", st,
+                            hipLaunchKernelGGL(fast::k_fs1s, dim3(a.nch1, U), dim3(256), 0, st, a));
+            } else {
+                ECOKV_TIMED("sweep1_block", st, launch_sweep(1, a, grid, st, bf16));
+            }
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            ECOKV_TIMED("reduce1", st, hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kReduceThreads), 0, st, a));
         }
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        ECOKV_TIMED("reduce1", st, hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kReduceThreads), 0, st, a));
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (score_fast_path(a.D, bf16) && a.R <= kFusedMaxRows) {
             // streaming sweep 2: window rows and the four anchor rows in one operand

@@ -29,7 +29,8 @@ NSTATS = 12
 STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7, imp_mean=8, sbar_mean=9,
             mu_norm2=10, scale=11)
 
-EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_score", "ecokv_score_v", "ecokv_index_count",
+EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_score", "ecokv_score_v", "ecokv_score_pre",
+           "ecokv_index_count",
            "ecokv_index_count_mode", "ecokv_select", "ecokv_compact", "ecokv_pyramid_budgets",
            "ecokv_decode_workspace_size", "ecokv_decode",
            "ecokv_last_error", "ecokv_stage_times"]
@@ -91,6 +92,7 @@ def _load():
     lib.ecokv_workspace_size.argtypes = [sp, pp, ctypes.POINTER(ctypes.c_size_t)]
     lib.ecokv_score.argtypes = [vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_score_v.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.ecokv_score_pre.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_index_count.argtypes = [sp, i32p, ctypes.POINTER(ctypes.c_int64)]
     lib.ecokv_index_count_mode.argtypes = [sp, ctypes.c_int, i32p, ctypes.POINTER(ctypes.c_int64)]
     lib.ecokv_decode_workspace_size.argtypes = [sp, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
@@ -201,6 +203,22 @@ def ecokv_score_v(K: torch.Tensor, V: Optional[torch.Tensor], Q_win: torch.Tenso
     _check(lib.ecokv_score_v(_ptr(K), _ptr(V), _ptr(Q_win), _dtype_code(K), ctypes.byref(shape.c),
                              ctypes.byref(p), _ptr(scores), _ptr(lambda_), _ptr(stats), _ptr(workspace),
                              workspace.numel(), _stream(stream)))
+
+
+def ecokv_score_pre(K: torch.Tensor, V: Optional[torch.Tensor], Q_win: torch.Tensor, shape: Shape,
+                    params: Optional[Params], pre: torch.Tensor, scores: torch.Tensor,
+                    lambda_: Optional[torch.Tensor] = None, stats: Optional[torch.Tensor] = None,
+                    workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Enqueue ecokv_score_pre: `pre` (float32 [L][Hkv][B][2D + 2R]) holds the
+    key sums and window softmax statistics a prefill produced."""
+    p = params or Params()
+    if workspace is None:
+        workspace = torch.empty(ecokv_workspace_size(shape, p), dtype=torch.uint8, device=K.device)
+    if pre.dtype != torch.float32:
+        raise TypeError("pre is float32")
+    _check(lib.ecokv_score_pre(_ptr(K), _ptr(V), _ptr(Q_win), _dtype_code(K), ctypes.byref(shape.c),
+                               ctypes.byref(p), _ptr(pre), _ptr(scores), _ptr(lambda_), _ptr(stats),
+                               _ptr(workspace), workspace.numel(), _stream(stream)))
 
 
 def ecokv_index_count(shape: Shape, budget: Sequence[int]) -> int:

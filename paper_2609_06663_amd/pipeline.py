@@ -36,8 +36,12 @@ class EvictionPass:
         self.Kc = torch.empty((max(self.n_idx, 1), D), dtype=dtype, device=device)
         self.Vc = torch.empty((max(self.n_idx, 1), D), dtype=dtype, device=device)
 
-    def score(self, K: torch.Tensor, Q_win: torch.Tensor, stream=None, V: Optional[torch.Tensor] = None):
-        if self.params.imp_mode == E.IMP_ATTN_VNORM:
+    def score(self, K: torch.Tensor, Q_win: torch.Tensor, stream=None, V: Optional[torch.Tensor] = None,
+              pre: Optional[torch.Tensor] = None):
+        if pre is not None:
+            E.ecokv_score_pre(K, V, Q_win, self.shape, self.params, pre, self.scores, self.lambda_, self.stats,
+                              self.workspace, stream)
+        elif self.params.imp_mode == E.IMP_ATTN_VNORM:
             E.ecokv_score_v(K, V, Q_win, self.shape, self.params, self.scores, self.lambda_, self.stats,
                             self.workspace, stream)
         else:
@@ -52,8 +56,9 @@ class EvictionPass:
         E.ecokv_compact(K, V, self.shape, self.mode, self.budget, self.idx, self.counts, self.offsets,
                         self.Kc, self.Vc, stream)
 
-    def run(self, K: torch.Tensor, V: torch.Tensor, Q_win: torch.Tensor, stream=None):
-        self.score(K, Q_win, stream, V)
+    def run(self, K: torch.Tensor, V: torch.Tensor, Q_win: torch.Tensor, stream=None,
+            pre: Optional[torch.Tensor] = None):
+        self.score(K, Q_win, stream, V, pre)
         self.select(stream)
         self.compact(K, V, stream)
         return self

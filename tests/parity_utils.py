@@ -39,7 +39,7 @@ def host_bits(t: torch.Tensor) -> np.ndarray:
     return t.numpy()
 
 
-def gpu_pass(wl: W.Workload, params=None, mode=None, budget=None):
+def gpu_pass(wl: W.Workload, params=None, mode=None, budget=None, pre=None):
     """Run score -> select -> compact through the C ABI; returns numpy outputs.
     `budget` overrides the workload's per-sequence budgets (e.g. [L][Hkv]
     budgets with mode HEAD_BUDGETS)."""
@@ -50,7 +50,7 @@ def gpu_pass(wl: W.Workload, params=None, mode=None, budget=None):
     tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     ep = EvictionPass(shape, wl.budget if budget is None else budget, m, params or P.Params(), tdt)
     K, V, Q = dev(wl.K, wl.dtype), dev(wl.V, wl.dtype), dev(wl.Q, wl.dtype)
-    ep.run(K, V, Q)
+    ep.run(K, V, Q, pre=None if pre is None else torch.from_numpy(np.ascontiguousarray(pre, np.float32)).cuda())
     torch.cuda.synchronize()
     U = wl.L * wl.Hkv * wl.B
     out = dict(
