@@ -9,7 +9,9 @@
 // instruction), so Kc and Vc stream in coalesced.  The S lanes of a row add
 // their partial dot products by DPP butterflies; the online softmax (base 2)
 // keeps wave-uniform maxima (read lane by lane across the row groups); P.V accumulates in fp32, each lane over its 16-byte
-// segment of the head dimension, the next batch's loads in flight meanwhile.
+// segment of the head dimension.  (Prefetching the next batch into registers,
+// or a third wave's worth of rows, measured slower: the occupancy it costs
+// outweighs the latency it hides.)
 // A block merges its waves in LDS and writes one (max, sum, acc[D]) per query
 // to the workspace; k_decode_merge combines a query row's chunks.
 #include "ecokv_internal.h"
@@ -21,7 +23,7 @@ typedef __bf16 bf16x2d __attribute__((ext_vector_type(2)));
 
 constexpr int kDecThreads = 256;
 constexpr int kDecWaves = kDecThreads / kWave;
-constexpr int kWaveRows = 128;  // rows per wave
+constexpr int kWaveRows = 192;  // rows per wave (128 and 256 measured slower)
 constexpr int kDecChunk = kDecWaves * kWaveRows;
 constexpr int kDecQG = 8;       // query heads per block at most
 
@@ -119,13 +121,9 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(DecodeArgs a)
             vx[i] = __builtin_bit_cast(u32x4d, __builtin_amdgcn_raw_buffer_load_b128(rv, o, 0, 0));
         }
     };
-    u32x4d kx[NR], vx[NR];
-    load(kx, vx, 0);
     for (int b0 = 0; b0 < nrows; b0 += BR) {
-        // the next batch is in flight while this one is used (past the rows:
-        // no memory access, zeros)
-        u32x4d kn[NR], vn[NR];
-        load(kn, vn, b0 + BR);
+        u32x4d kx[NR], vx[NR];
+        load(kx, vx, b0);
         __builtin_amdgcn_sched_barrier(0);
         float x[NR][QG];
 #pragma unroll
@@ -172,11 +170,7 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(DecodeArgs a)
                 for (int e = 0; e < EL; ++e) acc[g][e] += p * vf[e];
             }
         }
-#pragma unroll
-        for (int i = 0; i < NR; ++i) {
-            kx[i] = kn[i];
-            vx[i] = vn[i];
-        }
+
     }
 
     // the rows of a wave are spread over its 64 / S row groups: add them up,

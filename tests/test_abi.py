@@ -229,8 +229,8 @@ def test_alternative_options_defaults_and_checks(P):
 def test_decode_checks_before_device_work(P):
     from paper_2609_06663_amd import ecokv as E
     s = P.Shape(2, 8, 2, 128, 4, [0, 100])
-    assert P.ecokv_decode_workspace_size(s, 512) == 4 * 2 * 8 * 1 * 1 * 130
-    assert P.ecokv_decode_workspace_size(s, 513) == 4 * 2 * 8 * 1 * 2 * 130
+    assert P.ecokv_decode_workspace_size(s, 768) == 4 * 2 * 8 * 1 * 1 * 130
+    assert P.ecokv_decode_workspace_size(s, 769) == 4 * 2 * 8 * 1 * 2 * 130
     with pytest.raises(P.EcoKVError):
         P.ecokv_decode_workspace_size(s, 0)
     lib = E.lib
