@@ -6,9 +6,14 @@ may import this package; the HIP product path never does.  Nothing here
 imports the HIP package, and the C source shares nothing with it.
 
 Functions follow the paper's steps (see ``ecokv_oracle.c`` for citations):
-``score_unit`` (Sec. 3 and Sec. 5, Eqs. (1)-(7), Algorithm 1), ``score`` (all
-units of a tensor), ``select`` (Sec. 3 selection; AdaKV layer-flat budget,
-Appendix A.1) and ``compact`` (gather of the kept rows).
+``score_unit`` (Sec. 3 and Sec. 5, Eqs. (1)-(7), Algorithm 1; with V, the
+value-norm importance of Sec. 5.2; the alternatives of Sec. 6.3 / Table 4,
+Appendix D and Appendix B.6 through ``Params``), ``score`` (all units of a
+tensor), ``select`` (Sec. 3 selection; AdaKV layer-flat budget and budgets
+per layer and head, Appendix A.1), ``pyramid_budgets`` (PyramidKV's layer
+schedule, Appendix A.1), ``compact`` (gather of the kept rows) and
+``decode`` (attention of one query per head over the compressed cache).
+Every one is pinned by ``tests/test_oracle_pins.py``.
 """
 from __future__ import annotations
 
