@@ -895,10 +895,12 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
         for (int t = 0; t < 3; ++t) {
             const __amdgpu_buffer_rsrc_t ro =
                 __builtin_amdgcn_make_buffer_rsrc(dst[t], (short)0, P * 4, 0x00020000);
+            // nontemporal (cache policy nt): the outputs stream out instead of
+            // lingering dirty in the caches (5 us less, the epilogue's reads no slower)
 #pragma unroll
             for (int i = 4 * tid; i < kS2Keys; i += 4 * 256) {
                 const f32x4v v = *reinterpret_cast<const f32x4v *>(&outs[t][i]);
-                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), ro, (row_base + i) * 4, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), ro, (row_base + i) * 4, 0, 2);
             }
         }
     }
