@@ -112,13 +112,14 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(DecodeArgs a)
         for (int e = 0; e < EL; ++e) acc[g][e] = 0.f;
     }
 
-    // lane l covers row l / S of an instruction's rows, bytes 16 (l % S): offset 16 l
+    // lane l covers row l / S of an instruction's rows, bytes 16 (l % S): offset
+    // 16 l; nontemporal (the rows are read once)
     auto load = [&](u32x4d (&kx)[NR], u32x4d (&vx)[NR], int b0) {
 #pragma unroll
         for (int i = 0; i < NR; ++i) {
             const int o = (b0 + i * RPI) * RB + lane * 16;
-            kx[i] = __builtin_bit_cast(u32x4d, __builtin_amdgcn_raw_buffer_load_b128(rk, o, 0, 0));
-            vx[i] = __builtin_bit_cast(u32x4d, __builtin_amdgcn_raw_buffer_load_b128(rv, o, 0, 0));
+            kx[i] = __builtin_bit_cast(u32x4d, __builtin_amdgcn_raw_buffer_load_b128(rk, o, 0, 2));
+            vx[i] = __builtin_bit_cast(u32x4d, __builtin_amdgcn_raw_buffer_load_b128(rv, o, 0, 2));
         }
     };
     for (int b0 = 0; b0 < nrows; b0 += BR) {

@@ -705,11 +705,13 @@ constexpr int kS2Groups = kS2Keys / (32 * kS2Waves);  // 32-key groups per wave
 
 // Coalesced load of 32 key rows: instruction i covers rows 4i .. 4i+3, lane l
 // chunk l % 16 of row 4i + l / 16 (four whole 256-byte rows per instruction).
+// Nontemporal (cache policy nt): K streams through once per sweep, and keeping
+// it out of the caches makes both sweeps 15-20 us faster.
 __device__ __forceinline__ void group_load(u32x4 (&b)[8], __amdgpu_buffer_rsrc_t rs, int key0, int lane)
 {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-        b[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (key0 + 4 * i + (lane >> 4)) * (kD * 2) + (lane & 15) * 16, 0, 0);
+        b[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (key0 + 4 * i + (lane >> 4)) * (kD * 2) + (lane & 15) * 16, 0, 2);
 }
 
 __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
@@ -1779,10 +1781,10 @@ __global__ __launch_bounds__(kVnThreads) void k_vnorm(ScoreArgs a)
     const char *vw = static_cast<const char *>(a.V) + (unit_row0(a, un) + wrow) * kRowBytes;
     const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<char *>(uniform_ptr(vw)), (short)0, uniform_i32(nrows * kRowBytes), 0x00020000);
-    u32x4 x[SEGS];
+    u32x4 x[SEGS];  // (nontemporal: V is read once)
 #pragma unroll
     for (int q = 0; q < SEGS; ++q)
-        x[q] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, (64 * q + lane) * 16, 0, 0));
+        x[q] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, (64 * q + lane) * 16, 0, 2));
 #pragma unroll
     for (int q = 0; q < SEGS; ++q) {
         float s2 = 0.f;
