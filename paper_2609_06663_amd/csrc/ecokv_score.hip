@@ -266,7 +266,7 @@ __device__ __forceinline__ void tile_load(u32x4 (&pf)[8], __amdgpu_buffer_rsrc_t
 {
 #pragma unroll
     for (int j = 0; j < 8; ++j)
-        pf[j] = __builtin_amdgcn_raw_buffer_load_b128(rs, (tr0 + j * 16 + g) * (kD * 2) + c * 16, 0, 0);
+        pf[j] = __builtin_amdgcn_raw_buffer_load_b128(rs, (tr0 + j * 16 + g) * (kD * 2) + c * 16, 0, 2);  // nt: read once
 }
 
 __device__ __forceinline__ void tile_store(u32x4 *kt, const u32x4 (&pf)[8], int g, int c)
