@@ -697,11 +697,12 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
 // groups in flight), re-lays them out through a wave-private LDS stage into
 // MFMA B operands (lane l: key l % 32, 16-byte chunks 2s + l / 32).  The
 // attention of row m is 2^(x - M'_m) with M'_m = M_m + log2(S_m), the
-// normaliser folded into the shift.  2048-key blocks: 1024 and 4096 measured
-// no better.
+// normaliser folded into the shift.  2048-key blocks (1024 and 4096 measured
+// no better); 512-key blocks when a call has too few keys to fill the device
+// with 2048-key ones (a single layer, say).
 constexpr int kS2Waves = 4;
-constexpr int kS2Keys = 2048;                          // keys per block
-constexpr int kS2Groups = kS2Keys / (32 * kS2Waves);  // 32-key groups per wave
+constexpr int kS2Keys = 2048;       // keys per block
+constexpr int kS2KeysSmall = 512;   // keys per block for calls with few blocks
 
 // Coalesced load of 32 key rows: instruction i covers rows 4i .. 4i+3, lane l
 // chunk l % 16 of row 4i + l / 16 (four whole 256-byte rows per instruction).
@@ -714,19 +715,21 @@ __device__ __forceinline__ void group_load(u32x4 (&b)[8], __amdgpu_buffer_rsrc_t
         b[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (key0 + 4 * i + (lane >> 4)) * (kD * 2) + (lane & 15) * 16, 0, 2);
 }
 
+template <int KEYS>
 __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
 {
+    constexpr int kS2Groups = KEYS / (32 * kS2Waves);  // 32-key groups per wave
     __shared__ float wred[4][kS2Waves];
     __shared__ u32x4 stage[kS2Waves][32 * kChunks];  // per wave: 32 rows, swizzled 16-byte chunks
     // the block's per-key outputs (d_E, khat.mu, a), written out once at the end:
     // a few long stores instead of three 128-byte stores per 32 keys, which
     // interleave with the read stream at a high price
-    __shared__ __attribute__((aligned(16))) float outs[3][kS2Keys];
+    __shared__ __attribute__((aligned(16))) float outs[3][KEYS];
     const int u = blockIdx.y;
     const Unit un = unit_of(u, a.Hkv, a.B);
     const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
     const int P = T - a.w;
-    const int row_base = blockIdx.x * kS2Keys;
+    const int row_base = blockIdx.x * KEYS;
     if (row_base >= T) return;
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, kl = lane & 31;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -900,7 +903,7 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
             // nontemporal (cache policy nt): the outputs stream out instead of
             // lingering dirty in the caches (5 us less, the epilogue's reads no slower)
 #pragma unroll
-            for (int i = 4 * tid; i < kS2Keys; i += 4 * 256) {
+            for (int i = 4 * tid; i < KEYS; i += 4 * 256) {
                 const f32x4v v = *reinterpret_cast<const f32x4v *>(&outs[t][i]);
                 __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), ro, (row_base + i) * 4, 0, 2);
             }
@@ -936,8 +939,10 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
 //    as B.
 constexpr float kRebase1 = 16.f;  // log2 headroom of the lazily moved row reference
 
+template <int KEYS>
 __global__ __launch_bounds__(256, 2) void k_fs1s(ScoreArgs a)
 {
+    constexpr int kS2Groups = KEYS / (32 * kS2Waves);  // 32-key groups per wave
     __shared__ u32x4 stage[kS2Waves][32 * kChunks];
     __shared__ __attribute__((aligned(16))) uint16_t wts[kS2Waves][4][32];  // 1, 1/|k| hi, remainder, 0
     __shared__ float wcs[kS2Waves][2][kD];                                 // per-wave column sums
@@ -947,7 +952,7 @@ __global__ __launch_bounds__(256, 2) void k_fs1s(ScoreArgs a)
     const Unit un = unit_of(u, a.Hkv, a.B);
     const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
     const int P = T - a.w;
-    const int row_base = blockIdx.x * kS2Keys;
+    const int row_base = blockIdx.x * KEYS;
     if (row_base >= T) return;
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, kl = lane & 31;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1825,7 +1830,9 @@ WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int 
 {
     WsLayout w{};
     const int64_t U = (int64_t)L * Hkv * B;
-    const int rpb = rows_per_block(D, bf16);
+    // the smallest key block of any sweep: the block sweeps' rows, or the
+    // streaming sweeps' small blocks
+    const int rpb = min(rows_per_block(D, bf16), fast::kS2KeysSmall);
     const int64_t nch1 = (maxT + rpb - 1) / rpb;
     // the single-read path publishes per slice; size for it whenever it may run
     const bool single = bf16 && D == fast::kD && R <= kFusedMaxRows;
@@ -1923,6 +1930,10 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     // every call); the two-sweep path is the default.
     const char *path = getenv("ECOKV_SCORE_PATH");
     const bool want_single = path && strcmp(path, "single") == 0 && !a.pre;
+    // streaming sweeps: 2048-key blocks, or 512-key ones when those would be
+    // fewer than four per compute unit (1024 blocks)
+    const int sblock = (int64_t)U * ((maxT + fast::kS2Keys - 1) / fast::kS2Keys) >= 1024 ? fast::kS2Keys
+                                                                                       : fast::kS2KeysSmall;
     int fgrid = 0;
     // (its partials carry no sum of d_E^2 and its centroid spans all T keys)
     if (want_single && !a.red_std && !a.centroid_prefix &&
@@ -1948,10 +1959,14 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         } else {
             if (score_fast_path(a.D, bf16) && a.R <= 32) {
                 // streaming sweep 1: one 32-row window operand
-                a.rpb1 = fast::kS2Keys;
+                a.rpb1 = sblock;
                 a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
-                ECOKV_TIMED("sweep1_stream", st,
-                            hipLaunchKernelGGL(fast::k_fs1s, dim3(a.nch1, U), dim3(256), 0, st, a));
+                if (sblock == fast::kS2Keys)
+                    ECOKV_TIMED("sweep1_stream", st,
+                                hipLaunchKernelGGL(fast::k_fs1s<fast::kS2Keys>, dim3(a.nch1, U), dim3(256), 0, st, a));
+                else
+                    ECOKV_TIMED("sweep1_stream", st,
+                                hipLaunchKernelGGL(fast::k_fs1s<fast::kS2KeysSmall>, dim3(a.nch1, U), dim3(256), 0, st, a));
             } else {
                 ECOKV_TIMED("sweep1_block", st, launch_sweep(1, a, grid, st, bf16));
             }
@@ -1961,9 +1976,14 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (score_fast_path(a.D, bf16) && a.R <= kFusedMaxRows) {
             // streaming sweep 2: window rows and the four anchor rows in one operand
-            a.rpb2 = fast::kS2Keys;
+            a.rpb2 = sblock;
             a.nch2 = (maxT + a.rpb2 - 1) / a.rpb2;
-            ECOKV_TIMED("sweep2_stream", st, hipLaunchKernelGGL(fast::k_fs2s, dim3(a.nch2, U), dim3(256), 0, st, a));
+            if (sblock == fast::kS2Keys)
+                ECOKV_TIMED("sweep2_stream", st,
+                            hipLaunchKernelGGL(fast::k_fs2s<fast::kS2Keys>, dim3(a.nch2, U), dim3(256), 0, st, a));
+            else
+                ECOKV_TIMED("sweep2_stream", st,
+                            hipLaunchKernelGGL(fast::k_fs2s<fast::kS2KeysSmall>, dim3(a.nch2, U), dim3(256), 0, st, a));
         } else {
             // block sweep 2: the chunking of the block sweeps (grid)
             a.rpb2 = rows_per_block(a.D, bf16);
