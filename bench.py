@@ -54,7 +54,7 @@ STAGE_KERNELS = {
     "sweep2_stream": ["k_fs2s"], "sweep2_block": ["k_fs2", "k_pass2"], "epilogue": ["k_epi_unit"],
     "epilogue1": ["k_epi1"], "epilogue2": ["k_epi2"], "single_read": ["k_fused"],
     "select": ["k_select_reg", "k_select"], "compact": ["k_compact"], "vnorm": ["k_vnorm"],
-    "dquant": ["k_dquant", "k_dquant_reg"], "decode": ["k_decode"], "decode_merge": ["k_decode_merge"],
+    "dquant": ["k_dquant", "k_dquant_reg"], "decode": ["k_decode_mx", "k_decode"], "decode_merge": ["k_decode_merge"],
     "pre_anchors": ["k_pre_anchors"],
 }
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, vendor figure

@@ -160,10 +160,12 @@ struct DecodeArgs {
     float *lse;           // [L][Hq][B] or null
     float *part;          // [L][Hq][B][nparts][D + 2]: max, sum, acc per row chunk
     int L, Hq, Hkv, G, B, D;
-    int max_count, nparts;
+    int max_count, nparts;  // nparts: chunks per query row in part (decode_parts(max_count))
+    int wave_rows;        // rows per wave; a chunk is the rows of a block's waves
     float qscale;         // log2(e) / sqrt(D)
 };
 int decode_parts(int max_count);
+// Sets a.nparts and a.wave_rows, then launches the decode and merge kernels.
 hipError_t decode_launch(DecodeArgs a, bool bf16, hipStream_t st);
 
 WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16, bool vnorm);

@@ -119,3 +119,19 @@ def test_decode_stack28_sized_cache():
     say("28 layers x 4 KV heads x 6553 rows, 28 query heads")
     O, lse = run(c, L, Hq, Hkv, B, D, "bf16")
     check(c, O, lse, L, Hq, Hkv, B, D, "bf16")
+
+
+def test_decode_many_units_ragged():
+    # 224 units of up to 6000 rows (more blocks than the device holds at once);
+    # the counts are ragged, so chunks and 16-row tiles end inside and past units
+    L, Hq, Hkv, B, D = 28, 28, 4, 2, 128
+    r = np.random.default_rng(11)
+    counts = r.integers(1, 6000, size=(L, Hkv, B))
+    counts.reshape(-1)[3] = 6000
+    counts.reshape(-1)[4] = 1
+    counts.reshape(-1)[7] = 16
+    counts.reshape(-1)[8] = 17
+    c = make_cache(12, L, Hq, Hkv, B, D, counts, "bf16")
+    say(f"224 units, ragged counts up to 6000, {int(counts.sum())} rows")
+    O, lse = run(c, L, Hq, Hkv, B, D, "bf16", max_count=6000)
+    check(c, O, lse, L, Hq, Hkv, B, D, "bf16")
