@@ -3,19 +3,18 @@
 // generation step that reads the kept rows (Sec. 3).
 //
 // Split over rows (flash-decoding): block (c, u, z) takes chunk c of unit u's
-// rows for query heads QG z .. QG z + QG - 1 of the unit's G.  Each wave takes
-// kWaveRows consecutive rows in batches of NR load instructions; S =
-// row_bytes / 16 lanes cover a row with 16-byte loads (64 / S rows per
-// instruction), so Kc and Vc stream in coalesced.  The S lanes of a row add
-// their partial dot products by DPP butterflies; the online softmax (base 2)
-// keeps wave-uniform maxima (read lane by lane across the row groups); P.V accumulates in fp32, each lane over its 16-byte
-// segment of the head dimension.  (Prefetching the next batch into registers,
-// or a third wave's worth of rows, measured slower: the occupancy it costs
-// outweighs the latency it hides.)
-// A block merges its waves in LDS and writes one (max, sum, acc[D]) per query
-// to the workspace; k_decode_merge combines a query row's chunks.
+// rows for query heads QG z .. QG z + QG - 1 of the unit's G; each of its
+// waves takes kWaveRows consecutive rows.  Two forms of the wave's work:
+//  * k_decode_mx (bf16): q.k on the matrix cores, 16 rows per MFMA tile, P
+//    through LDS into the layout of the coalesced V loads, P.V by fp32 FMAs,
+//    the next tile's rows loading while one is used;
+//  * k_decode (fp32): S = row_bytes / 16 lanes cover a row with 16-byte
+//    loads (64 / S rows per instruction); the S lanes of a row add their
+//    partial dot products by DPP butterflies; P.V as above.
+// Both keep the online softmax in base 2.  A block merges its waves in LDS
+// and writes one (max, sum, acc[D]) per query to the workspace;
+// k_decode_merge combines a query row's chunks.
 #include "ecokv_internal.h"
-
 
 namespace ecokv {
 

@@ -391,16 +391,24 @@ __device__ __forceinline__ void reg_extremes(const uint32_t (&kk)[KPT], int v0, 
 }
 
 // The k-th largest key (k >= 1): digits of up to 8 bits below the common
-// prefix of kmin and kmax, one LDS histogram per wave, three barriers per
-// pass (the histogram is cleared by the threads that fold it, and the chosen
-// digit alternates between two slots).  Returns the threshold and how many
-// keys equal to it are taken.
-template <int KPT>
+// prefix of kmin and kmax, C LDS histograms per wave, three barriers per
+// pass (the histograms are cleared by the threads that fold them, and the
+// chosen digit alternates between two slots).  Returns the threshold and how
+// many keys equal to it are taken.
+// hist: kSelWaves * C histograms of 256 counters; lane l of wave w counts
+// into histogram w C + l % C.  The keys of a unit crowd into few digits near
+// its threshold, and the LDS serialises the lanes of one atomic instruction
+// that hit the same address; C > 1 spreads them over C addresses in
+// different banks (histograms 257 words apart).
+template <int KPT, int C>
 __device__ __forceinline__ void reg_radix_select(const uint32_t (&kk)[KPT], int v0, int n, int k, uint32_t kmin,
-                                                 uint32_t kmax, uint32_t (*hist)[256], uint32_t *hsum,
+                                                 uint32_t kmax, uint32_t *hist, uint32_t *hsum,
                                                  uint32_t (*bc)[2], uint32_t *thr_out, int *need_eq_out)
 {
+    constexpr int HS = C > 1 ? 257 : 256;
+    constexpr int NH = kSelWaves * C;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    uint32_t *const myh = hist + (wv * C + (lane & (C - 1))) * HS;
     const uint32_t diff = kmin ^ kmax;
     if (diff == 0) {
         *thr_out = kmin;
@@ -411,7 +419,7 @@ __device__ __forceinline__ void reg_radix_select(const uint32_t (&kk)[KPT], int 
     uint32_t mask = hi == 31 ? 0u : ~((2u << hi) - 1u);
     uint32_t prefix = kmin & mask;
     int rem = k;
-    for (int b = tid; b < kSelWaves * 256; b += blockDim.x) (&hist[0][0])[b] = 0;
+    for (int b = tid; b < NH * HS; b += blockDim.x) hist[b] = 0;
     __syncthreads();
     int par = 0;
     while (hi >= 0) {
@@ -419,14 +427,14 @@ __device__ __forceinline__ void reg_radix_select(const uint32_t (&kk)[KPT], int 
         const uint32_t nb = 1u << (hi - lo + 1);
 #pragma unroll
         for (int q = 0; q < KPT; ++q)
-            if (v0 + q < n && (kk[q] & mask) == prefix) atomicAdd(&hist[wv][(kk[q] >> lo) & (nb - 1u)], 1u);
+            if (v0 + q < n && (kk[q] & mask) == prefix) atomicAdd(&myh[(kk[q] >> lo) & (nb - 1u)], 1u);
         __syncthreads();
         if (tid < 256) {
             uint32_t c = 0;
 #pragma unroll
-            for (int w2 = 0; w2 < kSelWaves; ++w2) {
-                c += hist[w2][tid];
-                hist[w2][tid] = 0;
+            for (int w2 = 0; w2 < NH; ++w2) {
+                c += hist[w2 * HS + tid];
+                hist[w2 * HS + tid] = 0;
             }
             hsum[tid] = c;
         }
@@ -480,15 +488,20 @@ constexpr int kRegMaxKeys = 64 * kSelThreads;
 template <int KPT>
 __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
 {
-    __shared__ uint32_t hist[kSelWaves][256];
+    // KPT == 32: the radix histograms (four per wave) live in stg
+    constexpr int kHistCopies = KPT == 32 ? 4 : 1;
+    __shared__ uint32_t hist[KPT == 32 ? 1 : kSelWaves * 256];
     __shared__ uint32_t hsum[256];
     __shared__ uint32_t bc[2][2];
     __shared__ uint32_t wsum[2 * kSelWaves + 2];
     __shared__ uint32_t mm[2][kSelWaves];
     __shared__ int64_t through[kMaxFlatHeads];
     typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
-    // KPT == 32: the stage of the coalesced score load, then of the output
+    // KPT == 32: the stage of the coalesced score load, then of the radix
+    // histograms, then of the output (the barriers of reg_extremes and of the
+    // radix passes separate the three uses)
     __shared__ u32x4_t stg[KPT == 32 ? KPT / 4 * kSelThreads : 1];
+    static_assert(KPT != 32 || kSelWaves * kHistCopies * 257 <= KPT * kSelThreads, "histograms must fit the stage");
 
     const SelGroup grp = sel_group(a);
     const int l = grp.l, h0 = grp.h0, s = grp.s, nh = grp.nh;
@@ -564,7 +577,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
         uint32_t kmin, kmax;
         reg_extremes<KPT>(kk, v0, n, mm, &kmin, &kmax);
         // radix select of the k-th largest key
-        reg_radix_select<KPT>(kk, v0, n, k, kmin, kmax, hist, hsum, bc, &thr, &need_eq);
+        uint32_t *const hp = KPT == 32 ? reinterpret_cast<uint32_t *>(stg) : hist;
+        reg_radix_select<KPT, kHistCopies>(kk, v0, n, k, kmin, kmax, hp, hsum, bc, &thr, &need_eq);
 
         // ordered emission from the registers
         uint32_t cg = 0, ce = 0;
@@ -737,7 +751,7 @@ __device__ float reg_quantile(const uint32_t (&kk)[KPT], int v0, int n, double q
     const int j = (int)floor(h);
     uint32_t thr;
     int need_eq;
-    reg_radix_select<KPT>(kk, v0, n, n - j, kmin, kmax, hist, hsum, bc, &thr, &need_eq);
+    reg_radix_select<KPT, 1>(kk, v0, n, n - j, kmin, kmax, &hist[0][0], hsum, bc, &thr, &need_eq);
     const float x = key_value(thr);
     if (j + 1 >= n || need_eq >= 2) return x;  // x_(j+1) = x_(j), or no x_(j+1)
     uint32_t m = 0xffffffffu;
