@@ -477,6 +477,153 @@ __device__ __forceinline__ void reg_radix_select(const uint32_t (&kk)[KPT], int 
     *need_eq_out = rem;
 }
 
+// Wave 0 (all 64 lanes): the digit of the rem-th largest key from a 256-bin
+// histogram h, counts above it into slot[1]; with clear, the bins are zeroed.
+__device__ __forceinline__ void pick_digit(uint32_t *h, bool clear, int rem, uint32_t *slot)
+{
+    const int lane = threadIdx.x & 63;
+    // lane owns bins 255-4l .. 252-4l (descending digit order)
+    uint32_t c4[4], loc = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        c4[q] = h[255 - 4 * lane - q];
+        if (clear) h[255 - 4 * lane - q] = 0u;
+        loc += c4[q];
+    }
+    uint32_t inc = loc;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const uint32_t y = __shfl_up(inc, d, kWave);
+        if (lane >= d) inc += y;
+    }
+    const uint32_t before = inc - loc;
+    if ((int)before < rem && rem <= (int)inc) {
+        uint32_t cum = before;
+        for (int q = 0; q < 4; ++q) {
+            if ((int)(cum + c4[q]) >= rem) {
+                slot[0] = 255u - 4u * lane - q;
+                slot[1] = cum;
+                break;
+            }
+            cum += c4[q];
+        }
+    }
+}
+
+// The k-th largest key, as reg_radix_select, for a block whose 128 KiB
+// stage (lds) is free during the selection:
+//  * first digit: four histograms per wave (lane l of wave w counts into
+//    histogram 4 w + l % 4; 257 words apart, so lanes that share a digit hit
+//    different banks), folded by 256 threads;
+//  * then the keys that still carry the chosen prefix -- usually a small part
+//    of the group -- are gathered into the stage (a wave scan of the
+//    per-thread counts and one LDS atomic per wave place them), and the later
+//    digits count only them, into one shared histogram that the scanning wave
+//    reads and clears: two barriers per digit and no fold.  When they do not
+//    fit, the later digits count the registers into that histogram instead.
+constexpr int kStHistC = 4;
+constexpr int kStHistWords = kSelWaves * kStHistC * 257;
+constexpr int kStCandOff = kStHistWords + 256;
+constexpr int kStCandCap = 32 * kSelThreads - kStCandOff;
+
+template <int KPT>
+__device__ __forceinline__ void reg_radix_select_staged(const uint32_t (&kk)[KPT], int v0, int n, int k,
+                                                        uint32_t kmin, uint32_t kmax, uint32_t *lds,
+                                                        uint32_t *hsum, uint32_t (*bc)[2], uint32_t *ccount,
+                                                        uint32_t *thr_out, int *need_eq_out)
+{
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const uint32_t diff = kmin ^ kmax;
+    if (diff == 0) {
+        *thr_out = kmin;
+        *need_eq_out = k;
+        return;
+    }
+    int hi = 31 - __clz(diff);
+    uint32_t mask = hi == 31 ? 0u : ~((2u << hi) - 1u);
+    uint32_t prefix = kmin & mask;
+    int rem = k;
+    uint32_t *const h1 = lds + kStHistWords;
+    uint32_t *const cand = lds + kStCandOff;
+    for (int b = tid; b < kStHistWords + 256; b += blockDim.x) lds[b] = 0u;
+    if (tid == 0) *ccount = 0u;
+    __syncthreads();
+    {
+        // first digit (every key lies in [kmin, kmax], so all carry the prefix)
+        const int lo = hi >= 7 ? hi - 7 : 0;
+        const uint32_t nb = 1u << (hi - lo + 1);
+        uint32_t *const myh = lds + (wv * kStHistC + (lane & (kStHistC - 1))) * 257;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q)
+            if (v0 + q < n) atomicAdd(&myh[(kk[q] >> lo) & (nb - 1u)], 1u);
+        __syncthreads();
+        if (tid < 256) {
+            uint32_t c = 0;
+#pragma unroll 8
+            for (int w2 = 0; w2 < kSelWaves * kStHistC; ++w2) c += lds[w2 * 257 + tid];
+            hsum[tid] = c;
+        }
+        __syncthreads();
+        if (tid < kWave) pick_digit(hsum, false, rem, bc[0]);
+        __syncthreads();
+        prefix |= bc[0][0] << lo;
+        rem -= (int)bc[0][1];
+        mask |= (nb - 1u) << lo;
+        hi = lo - 1;
+    }
+    if (hi >= 0) {
+        // gather the keys that carry the prefix
+        uint32_t cnt = 0;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q) cnt += (v0 + q < n && (kk[q] & mask) == prefix) ? 1u : 0u;
+        uint32_t inc = cnt;
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) {
+            const uint32_t y = __shfl_up(inc, d, kWave);
+            if (lane >= d) inc += y;
+        }
+        const uint32_t wtot = __shfl(inc, kWave - 1, kWave);
+        uint32_t base = 0;
+        if (lane == kWave - 1 && wtot > 0) base = atomicAdd(ccount, wtot);
+        base = __shfl(base, kWave - 1, kWave);
+        uint32_t pos = base + inc - cnt;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q)
+            if (v0 + q < n && (kk[q] & mask) == prefix) {
+                if (pos < (uint32_t)kStCandCap) cand[pos] = kk[q];
+                ++pos;
+            }
+        __syncthreads();
+        const uint32_t ncand = *ccount;
+        const bool use_cand = ncand <= (uint32_t)kStCandCap;
+        int par = 1;
+        while (hi >= 0) {
+            const int lo = hi >= 7 ? hi - 7 : 0;
+            const uint32_t nb = 1u << (hi - lo + 1);
+            if (use_cand) {
+                for (uint32_t i = tid; i < ncand; i += kSelThreads) {
+                    const uint32_t key = cand[i];
+                    if ((key & mask) == prefix) atomicAdd(&h1[(key >> lo) & (nb - 1u)], 1u);
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < KPT; ++q)
+                    if (v0 + q < n && (kk[q] & mask) == prefix) atomicAdd(&h1[(kk[q] >> lo) & (nb - 1u)], 1u);
+            }
+            __syncthreads();
+            if (tid < kWave) pick_digit(h1, true, rem, bc[par]);
+            __syncthreads();
+            prefix |= bc[par][0] << lo;
+            rem -= (int)bc[par][1];
+            mask |= (nb - 1u) << lo;
+            hi = lo - 1;
+            par ^= 1;
+        }
+    }
+    *thr_out = prefix;
+    *need_eq_out = rem;
+}
+
 // ---------------------------------------------------------------------------
 // Register-resident variant for groups of up to 64 Ki keys: thread t owns the
 // contiguous run [t*KPT, t*KPT + KPT) of the group's keys in registers
@@ -488,20 +635,20 @@ constexpr int kRegMaxKeys = 64 * kSelThreads;
 template <int KPT>
 __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
 {
-    // KPT == 32: the radix histograms (four per wave) live in stg
-    constexpr int kHistCopies = KPT == 32 ? 4 : 1;
+    // KPT == 32: the radix histograms live in stg
     __shared__ uint32_t hist[KPT == 32 ? 1 : kSelWaves * 256];
     __shared__ uint32_t hsum[256];
     __shared__ uint32_t bc[2][2];
     __shared__ uint32_t wsum[2 * kSelWaves + 2];
     __shared__ uint32_t mm[2][kSelWaves];
+    __shared__ uint32_t ccount;
     __shared__ int64_t through[kMaxFlatHeads];
     typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
     // KPT == 32: the stage of the coalesced score load, then of the radix
-    // histograms, then of the output (the barriers of reg_extremes and of the
-    // radix passes separate the three uses)
+    // histograms and candidates, then of the output (the barriers of the
+    // extremes and of the radix passes separate the three uses)
     __shared__ u32x4_t stg[KPT == 32 ? KPT / 4 * kSelThreads : 1];
-    static_assert(KPT != 32 || kSelWaves * kHistCopies * 257 <= KPT * kSelThreads, "histograms must fit the stage");
+    static_assert(KPT != 32 || kStCandCap > 0, "histograms must fit the stage");
 
     const SelGroup grp = sel_group(a);
     const int l = grp.l, h0 = grp.h0, s = grp.s, nh = grp.nh;
@@ -533,6 +680,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
 
     for (int h = tid; h < nh; h += blockDim.x) through[h] = 0;
     uint32_t kk[KPT];
+    bool ext_done = false;  // the extremes are in mm (reduced with the load's barrier)
     if (nh == 1 && KPT == 32) {
         // Coalesced load through LDS: the block reads the group's scores as
         // consecutive 16-byte pieces (1 KiB per wave instruction) into a
@@ -544,9 +692,28 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
 #pragma unroll
         for (int q = 0; q < KPT / 4; ++q)
             x[q] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (q * kSelThreads + tid) * 16, 0, 0));
+        // the extremes of the loaded keys (the same set as the thread's run
+        // after the stage) ride on the stage's barrier
+        uint32_t lmin = 0xffffffffu, lmax = 0u;
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if ((q * kSelThreads + tid) * 4 + e < n) {
+                    const uint32_t kv = score_key(__uint_as_float(x[q][e]));
+                    lmin = min(lmin, kv);
+                    lmax = max(lmax, kv);
+                }
+        lmin = wave_min_u(lmin);
+        lmax = wave_max_u(lmax);
+        if (lane == 0) {
+            mm[0][wv] = lmin;
+            mm[1][wv] = lmax;
+        }
 #pragma unroll
         for (int q = 0; q < KPT / 4; ++q) stg[q * kSelThreads + (tid ^ ((tid >> 3) & 7))] = x[q];
         lds_barrier();
+        ext_done = true;
 #pragma unroll
         for (int q = 0; q < KPT / 4; ++q) {
             const u32x4_t y = stg[(KPT / 4) * tid + (q ^ (tid & 7))];
@@ -575,12 +742,59 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
     int need_eq = 0;
     if (k > 0) {
         uint32_t kmin, kmax;
-        reg_extremes<KPT>(kk, v0, n, mm, &kmin, &kmax);
+        if (ext_done) {
+            kmin = mm[0][0];
+            kmax = mm[1][0];
+            for (int q = 1; q < kSelWaves; ++q) {
+                kmin = min(kmin, mm[0][q]);
+                kmax = max(kmax, mm[1][q]);
+            }
+        } else {
+            reg_extremes<KPT>(kk, v0, n, mm, &kmin, &kmax);
+        }
         // radix select of the k-th largest key
-        uint32_t *const hp = KPT == 32 ? reinterpret_cast<uint32_t *>(stg) : hist;
-        reg_radix_select<KPT, kHistCopies>(kk, v0, n, k, kmin, kmax, hp, hsum, bc, &thr, &need_eq);
-
-        // ordered emission from the registers
+        if constexpr (KPT == 32)
+            reg_radix_select_staged<KPT>(kk, v0, n, k, kmin, kmax, reinterpret_cast<uint32_t *>(stg), hsum, bc,
+                                         &ccount, &thr, &need_eq);
+        else
+            reg_radix_select<KPT, 1>(kk, v0, n, k, kmin, kmax, hist, hsum, bc, &thr, &need_eq);
+    }
+    if (k > 0 && nh == 1 && KPT == 32) {
+        // ordered emission of one head: bit q of gtm / eqm marks key v0 + q
+        // above / equal to the threshold; the thread's taken keys go to
+        // consecutive slots from the number taken before its run
+        typedef uint32_t bits_t;
+        bits_t gtm = 0, eqm = 0;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q)
+            if (v0 + q < n) {
+                gtm |= kk[q] > thr ? (bits_t)1 << q : (bits_t)0;
+                eqm |= kk[q] == thr ? (bits_t)1 << q : (bits_t)0;
+            }
+        const uint32_t cg = (uint32_t)__builtin_popcount(gtm), ce = (uint32_t)__builtin_popcount(eqm);
+        uint32_t eg, ee, tg, te;
+        block_exscan2(cg, ce, wsum, eg, ee, tg, te);
+        (void)tg;
+        (void)te;
+        // equal keys are taken in position order while fewer than need_eq precede them
+        const int eq_take = min((int)ce, max(need_eq - (int)ee, 0));
+        bits_t take = gtm, em = eqm;
+        for (int r = 0; r < eq_take; ++r) {
+            const bits_t low = em & (~em + 1);
+            take |= low;
+            em ^= low;
+        }
+        int o = (int)eg + min((int)ee, need_eq);
+        while (take) {
+            const int q = __builtin_ctz(take);
+            take &= take - 1;
+            if (staged) ost[o] = (uint32_t)(v0 + q);
+            else out[o] = v0 + q;
+            ++o;
+        }
+        if (tid == 0) through[0] = k;
+    } else if (k > 0) {
+        // ordered emission from the registers (several heads, or 64 keys a thread)
         uint32_t cg = 0, ce = 0;
 #pragma unroll
         for (int q = 0; q < KPT; ++q)
@@ -608,13 +822,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
                 gt_before += gt;
                 eq_before += eq;
                 if (++pos == P) {
-                    if (nh > 1) through[h] = gt_before + min(eq_before, need_eq);
+                    through[h] = gt_before + min(eq_before, need_eq);
                     pos = 0;
                     ++h;
                 }
             }
         }
-        if (nh == 1 && tid == 0) through[0] = k;
     }
     __syncthreads();
     // windows, counts and offsets
