@@ -344,3 +344,54 @@ def test_select_bit_exact_with_ties(mode):
     np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
     np.testing.assert_array_equal(counts.cpu().numpy(), ref_c.reshape(-1))
     np.testing.assert_array_equal(offsets.cpu().numpy(), ref_o.reshape(-1))
+
+
+def _digit_case(case, rng):
+    """Scores of one 32000-key unit shaped for a path of the register radix select."""
+    P = 32000
+    spread = np.exp(rng.uniform(np.log(1e-3), np.log(100.0), size=P)).astype(np.float32)
+    if case == "prefix_overflow":
+        # 31000 keys in [1, 1.0001): one first digit (the exponent) holds more
+        # keys than the stage can gather, so the later digits count the registers
+        S = spread.copy()
+        S[:31000] = 1.0 + rng.uniform(0, 1e-4, size=31000).astype(np.float32)
+        k = 12000
+    elif case == "prefix_fits":
+        S = spread.copy()
+        S[:12000] = 1.0 + rng.uniform(0, 1e-4, size=12000).astype(np.float32)
+        k = 9000
+    elif case == "one_digit":
+        # keys that differ only in their low 8 bits: a single radix digit
+        S = (np.float32(1.0).view(np.uint32) + rng.integers(0, 200, size=P).astype(np.uint32)).view(np.float32)
+        k = 7000
+    else:  # "cluster_ties": 64 values inside the cluster, many equal to the threshold
+        S = spread.copy()
+        S[:13000] = 1.0 + rng.integers(0, 64, size=13000).astype(np.float32) * np.float32(1e-6)
+        k = 11000
+    rng.shuffle(S)
+    return S.astype(np.float32), k
+
+
+@pytest.mark.parametrize("case", ["prefix_overflow", "prefix_fits", "one_digit", "cluster_ties"])
+def test_select_register_digit_paths(case):
+    import paper_2609_06663_amd as P
+    rng = np.random.default_rng({"prefix_overflow": 61, "prefix_fits": 62, "one_digit": 63, "cluster_ties": 64}[case])
+    w = 4
+    S1, k = _digit_case(case, rng)
+    S2, _ = _digit_case(case, rng)
+    L, Hkv = 1, 2
+    cu = [0, len(S1) + w]
+    S = np.stack([S1, S2])[None]  # [L][Hkv][P]
+    budget = [k + w]
+    shape = P.Shape(L, Hkv, Hkv, 128, w, cu)
+    n = P.ecokv_index_count(shape, budget)
+    idx = torch.full((n,), -7, dtype=torch.int32, device="cuda")
+    counts = torch.full((L * Hkv,), -7, dtype=torch.int32, device="cuda")
+    offsets = torch.full_like(counts, -7)
+    say(f"select-only bit-exact, {case}: 32000 keys, k = {k}")
+    P.ecokv_select(torch.from_numpy(np.ascontiguousarray(S)).cuda(), shape, P.PER_HEAD, budget, idx, counts, offsets)
+    torch.cuda.synchronize()
+    ref_idx, ref_c, ref_o = oracle.select(S.astype(np.float64), L, Hkv, cu, w, budget, oracle.PER_HEAD)
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
+    np.testing.assert_array_equal(counts.cpu().numpy(), ref_c.reshape(-1))
+    np.testing.assert_array_equal(offsets.cpu().numpy(), ref_o.reshape(-1))
