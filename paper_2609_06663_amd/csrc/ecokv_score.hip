@@ -1109,11 +1109,17 @@ __global__ __launch_bounds__(256, 2) void k_fs1s(ScoreArgs a)
 // ---------------------------------------------------------------------------
 // Per-unit reduction of the sweep-1 partials.
 // ---------------------------------------------------------------------------
-// Four lanes per column, each over every fourth block partial, so that a
-// unit's partials are all requested at once; the four sums and the four
-// (max, normaliser) pairs are combined by commutative steps, so every lane
-// ends with the same value.
+// Columns of a unit's partial rows: sum k (D), sum k/|k| (D), the R window
+// rows' (max, normaliser) pairs.  `lanes` lanes per column, each over every
+// lanes-th block partial with its loads in flight together, then combined by
+// butterflies of commutative steps, so every lane ends with the same value.
+// Up to 16 partials per unit: 4 lanes, one block per unit looping over the
+// columns; more (64 for a 32 Ki-token unit in 512-key blocks): 16 lanes, grid
+// (unit, column group of 64), so that no lane waits on a chain of loads
+// (one layer: 9 -> 7 us; the 28-layer stack in 2048-key blocks is 0.7 us
+// faster with one block per unit).
 constexpr int kReduceThreads = 1024;
+inline int reduce1_lanes(int nch1) { return nch1 > 16 ? 16 : 4; }
 
 // Component c of kbar from the sum of the unit's T keys: divided by T, or,
 // with the centroid over the non-window keys, the w window rows taken out
@@ -1152,6 +1158,7 @@ __global__ __launch_bounds__(256) void k_pre_anchors(ScoreArgs a)
     }
 }
 
+template <int LANES>
 __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
 {
     const int u = blockIdx.x;
@@ -1161,24 +1168,27 @@ __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
     const int stride = 2 * a.D + 2 * a.R;
     const float *p = a.part1 + (int64_t)u * a.nch1 * stride;
     float *anc = a.anchors + (int64_t)u * stride;
-    const int q = threadIdx.x & 3;
-    for (int c = threadIdx.x >> 2; c < 2 * a.D + a.R; c += kReduceThreads / 4) {
+    constexpr int lanes = LANES;
+    constexpr int cpb = kReduceThreads / lanes;  // columns per block per step
+    const int q = threadIdx.x & (lanes - 1);
+    // (every lane of a column takes the same path: the butterflies stay within it)
+    for (int c = blockIdx.y * cpb + threadIdx.x / lanes; c < 2 * a.D + a.R; c += gridDim.y * cpb) {
         if (c < 2 * a.D) {
             float s = 0.f;
 #pragma unroll 4
-            for (int b = q; b < nb; b += 4) s += p[(int64_t)b * stride + c];
-            s += __shfl_xor(s, 1, 4);
-            s += __shfl_xor(s, 2, 4);
+            for (int b = q; b < nb; b += lanes) s += p[(int64_t)b * stride + c];
+#pragma unroll
+            for (int x = 1; x < lanes; x <<= 1) s += __shfl_xor(s, x, lanes);
             if (q == 0) anc[c] = c < a.D ? centroid_component(a, un, T, c, s) : s / (float)T;
         } else {
             const int r = c - 2 * a.D;
             float m = -INFINITY, s = 0.f;
 #pragma unroll 4
-            for (int b = q; b < nb; b += 4)
+            for (int b = q; b < nb; b += lanes)
                 softmax_merge2(m, s, p[(int64_t)b * stride + 2 * a.D + r], p[(int64_t)b * stride + 2 * a.D + a.R + r]);
 #pragma unroll
-            for (int x = 1; x <= 2; x <<= 1) {
-                const float m2 = __shfl_xor(m, x, 4), s2 = __shfl_xor(s, x, 4);
+            for (int x = 1; x < lanes; x <<= 1) {
+                const float m2 = __shfl_xor(m, x, lanes), s2 = __shfl_xor(s, x, lanes);
                 softmax_merge2(m, s, m2, s2);
             }
             if (q == 0) {
@@ -1971,7 +1981,12 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
                 ECOKV_TIMED("sweep1_block", st, launch_sweep(1, a, grid, st, bf16));
             }
             if ((e = hipGetLastError()) != hipSuccess) return e;
-            ECOKV_TIMED("reduce1", st, hipLaunchKernelGGL(k_reduce1, dim3(U), dim3(kReduceThreads), 0, st, a));
+            if (reduce1_lanes(a.nch1) == 4)
+                ECOKV_TIMED("reduce1", st, hipLaunchKernelGGL(k_reduce1<4>, dim3(U), dim3(kReduceThreads), 0, st, a));
+            else
+                ECOKV_TIMED("reduce1", st,
+                            hipLaunchKernelGGL(k_reduce1<16>, dim3(U, (2 * a.D + a.R + 63) / 64), dim3(kReduceThreads),
+                                               0, st, a));
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (score_fast_path(a.D, bf16) && a.R <= kFusedMaxRows) {
