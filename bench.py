@@ -28,14 +28,14 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, vendor figure
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--budget-frac", type=float, default=0.2)
     ap.add_argument("--tokens", type=int, default=32768)
     ap.add_argument("--layers", type=int, default=28)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-layers", type=int, default=28)
-    ap.add_argument("--extras", action="store_true", help="also time 10/40 % budgets and per-layer calls")
+    ap.add_argument("--extras", action="store_true", help="also time 10 % and 40 % budgets")
     ap.add_argument("--counter-run", action="store_true",
                     help="run a few passes and a 1 GiB copy for rocprofv3 --pmc, then exit")
     ap.add_argument("--traffic-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "COMMAND"),
@@ -148,14 +148,18 @@ def main():
     torch.cuda.synchronize()
 
     log(f"timing {args.steps} steps")
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # an event between consecutive steps as well, for the median step time
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    ev0.record(stream)
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for i in range(args.steps):
         ep.run(K, V, Q)
-    ev1.record(stream)
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
-    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    ms_per_step = evs[0].elapsed_time(evs[-1]) / args.steps
+    step_ms = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+    median_ms = step_ms[len(step_ms) // 2] if len(step_ms) % 2 else 0.5 * (step_ms[len(step_ms) // 2 - 1] +
+                                                                           step_ms[len(step_ms) // 2])
     t_layer_s = ms_per_step / 1e3 / L
     value = T / t_layer_s
 
@@ -428,22 +432,44 @@ def main():
             extras[f"budget_{int(frac * 100)}pct"] = {"budget": bb, "ms_per_step": round(ms, 4),
                                                       "tokens_per_s_per_layer": T / (ms / 1e3 / L)}
             del ep2
-        # 28 single-layer calls on one stream
-        shape1 = P.Shape(1, Hq, Hkv, D, w, wl.cu_seqlens)
-        ep1 = EvictionPass(shape1, [b], P.PER_HEAD, P.Params(), torch.bfloat16, "cuda")
-        Ks, Vs, Qs = [K[l:l + 1] for l in range(L)], [V[l:l + 1] for l in range(L)], [Q[l:l + 1] for l in range(L)]
+
+    # the same stack as L single-layer calls on one stream (one call per layer
+    # as its prefill finishes)
+    log(f"{L} single-layer calls")
+    shape1 = P.Shape(1, Hq, Hkv, D, w, wl.cu_seqlens)
+    ep1 = EvictionPass(shape1, [b], P.PER_HEAD, P.Params(), torch.bfloat16, "cuda")
+    Ks, Vs, Qs = [K[l:l + 1] for l in range(L)], [V[l:l + 1] for l in range(L)], [Q[l:l + 1] for l in range(L)]
+    for l in range(L):
+        ep1.run(Ks[l], Vs[l], Qs[l])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
         for l in range(L):
             ep1.run(Ks[l], Vs[l], Qs[l])
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(args.steps):
-            for l in range(L):
-                ep1.run(Ks[l], Vs[l], Qs[l])
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / args.steps
-        extras["per_layer_calls"] = {"ms_per_step": round(ms, 4), "tokens_per_s_per_layer": T / (ms / 1e3 / L)}
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms1 = e0.elapsed_time(e1) / args.steps
+    per_layer_calls = {"ms_per_step": round(ms1, 4), "us_per_layer": round(ms1 * 1e3 / L, 2),
+                       "tokens_per_s_per_layer": round(T / (ms1 / 1e3 / L), 1)}
+    del ep1, Ks, Vs, Qs
+
+    # a plain device copy of 1 GiB (torch's copy kernel), for the bandwidth the
+    # memory system gives an ordinary streaming kernel next to the 8 TB/s peak
+    log("copy bandwidth")
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(10):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    copy_ms = e0.elapsed_time(e1) / 10
+    copy_bw = {"bytes_per_copy": 2 * COPY_BYTES, "GBs": round(2 * COPY_BYTES / (copy_ms / 1e3) / 1e9, 1),
+               "frac_of_hbm_peak": round(2 * COPY_BYTES / (copy_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
+    del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -470,9 +496,12 @@ def main():
         },
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "median_ms_per_step": round(median_ms, 4),
         "pass": {"algorithmic_bytes": pass_bytes, "achieved_GBs": round(pass_gbs, 1),
                  "frac_of_hbm_peak": round(pass_gbs / HBM_PEAK_GBS, 4),
                  "t_layer_us": round(t_layer_s * 1e6, 3)},
+        "per_layer_calls": per_layer_calls,
+        "copy_bandwidth": copy_bw,
         "per_call_ms": {k: round(v, 4) for k, v in per_call_ms.items()},
         "per_call_algorithmic_bytes": algo,
         "kernels": kernels,
