@@ -471,9 +471,10 @@ def main():
                "frac_of_hbm_peak": round(2 * COPY_BYTES / (copy_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
     del src, dst
 
-    cpu = None
+    cpu = cpu1 = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, args.cpu_sample_layers)
+        cpu1 = cpu_baseline_one_thread()
 
     out = {
         "metric": "tokens scored+evicted/sec per layer (all heads) at N=32k; % of HBM roofline",
@@ -496,6 +497,7 @@ def main():
         },
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "cpu_baseline_one_thread": cpu1,
         "median_ms_per_step": round(median_ms, 4),
         "pass": {"algorithmic_bytes": pass_bytes, "achieved_GBs": round(pass_gbs, 1),
                  "frac_of_hbm_peak": round(pass_gbs / HBM_PEAK_GBS, 4),
@@ -610,6 +612,27 @@ def cpu_baseline(wl, sample_layers):
     return {"value": round(T * reps / (dt / Ls), 1), "unit": "tokens/s per layer", "cores": used, "kind": "oracle",
             "sample": f"first {Ls} of {wl.L} layers ({Ls * wl.Hkv} (layer, head) units of {T} tokens), "
                       f"score+select+compact, fp64, {reps} repetitions, {dt:.2f}s wall"}
+
+
+def cpu_baseline_one_thread():
+    """The CPU oracle on one thread, on one 8192-token layer of the same head shape (28q/4kv, D 128)."""
+    import workloads as W
+    import oracle
+    wl = W.layer7b()
+    T = wl.cu_seqlens[-1]
+    log(f"cpu baseline: oracle on one {T}-token layer with 1 thread, repeated for >= 3 s")
+    reps, dt = 0, 0.0
+    while dt < 3.0 and reps < 64:
+        t0 = time.perf_counter()
+        S, _ = oracle.score(wl.K, wl.Q, wl.L, wl.Hq, wl.Hkv, wl.cu_seqlens, wl.D, wl.w, nthreads=1)
+        idx, counts, offsets = oracle.select(S, wl.L, wl.Hkv, wl.cu_seqlens, wl.w, wl.budget, oracle.PER_HEAD,
+                                             nthreads=1)
+        oracle.compact(wl.K, wl.V, wl.L, wl.Hkv, wl.cu_seqlens, wl.D, idx, counts, offsets)
+        dt += time.perf_counter() - t0
+        reps += 1
+    return {"value": round(T * reps / (dt / wl.L), 1), "unit": "tokens/s per layer", "cores": 1, "kind": "oracle",
+            "sample": f"one layer of {wl.Hkv} KV heads x {T} tokens (28 query heads, window {wl.w}, budget "
+                      f"{wl.budget[0]}), score+select+compact, fp64, {reps} repetitions, {dt:.2f}s wall"}
 
 
 if __name__ == "__main__":
