@@ -391,24 +391,19 @@ __device__ __forceinline__ void reg_extremes(const uint32_t (&kk)[KPT], int v0, 
 }
 
 // The k-th largest key (k >= 1): digits of up to 8 bits below the common
-// prefix of kmin and kmax, C LDS histograms per wave, three barriers per
-// pass (the histograms are cleared by the threads that fold them, and the
-// chosen digit alternates between two slots).  Returns the threshold and how
-// many keys equal to it are taken.
-// hist: kSelWaves * C histograms of 256 counters; lane l of wave w counts
-// into histogram w C + l % C.  The keys of a unit crowd into few digits near
-// its threshold, and the LDS serialises the lanes of one atomic instruction
-// that hit the same address; C > 1 spreads them over C addresses in
-// different banks (histograms 257 words apart).
-template <int KPT, int C>
+// prefix of kmin and kmax, one LDS histogram of 256 counters per wave (hist:
+// kSelWaves of them), three barriers per pass (the histograms are cleared by
+// the threads that fold them, and the chosen digit alternates between two
+// slots).  Returns the threshold and how many keys equal to it are taken.
+template <int KPT>
 __device__ __forceinline__ void reg_radix_select(const uint32_t (&kk)[KPT], int v0, int n, int k, uint32_t kmin,
                                                  uint32_t kmax, uint32_t *hist, uint32_t *hsum,
                                                  uint32_t (*bc)[2], uint32_t *thr_out, int *need_eq_out)
 {
-    constexpr int HS = C > 1 ? 257 : 256;
-    constexpr int NH = kSelWaves * C;
+    constexpr int HS = 256;
+    constexpr int NH = kSelWaves;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    uint32_t *const myh = hist + (wv * C + (lane & (C - 1))) * HS;
+    uint32_t *const myh = hist + wv * HS;
     const uint32_t diff = kmin ^ kmax;
     if (diff == 0) {
         *thr_out = kmin;
@@ -757,7 +752,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
             reg_radix_select_staged<KPT>(kk, v0, n, k, kmin, kmax, reinterpret_cast<uint32_t *>(stg), hsum, bc,
                                          &ccount, &thr, &need_eq);
         else
-            reg_radix_select<KPT, 1>(kk, v0, n, k, kmin, kmax, hist, hsum, bc, &thr, &need_eq);
+            reg_radix_select<KPT>(kk, v0, n, k, kmin, kmax, hist, hsum, bc, &thr, &need_eq);
     }
     if (k > 0 && nh == 1 && KPT == 32) {
         // ordered emission of one head: bit q of gtm / eqm marks key v0 + q
@@ -964,7 +959,7 @@ __device__ float reg_quantile(const uint32_t (&kk)[KPT], int v0, int n, double q
     const int j = (int)floor(h);
     uint32_t thr;
     int need_eq;
-    reg_radix_select<KPT, 1>(kk, v0, n, n - j, kmin, kmax, &hist[0][0], hsum, bc, &thr, &need_eq);
+    reg_radix_select<KPT>(kk, v0, n, n - j, kmin, kmax, &hist[0][0], hsum, bc, &thr, &need_eq);
     const float x = key_value(thr);
     if (j + 1 >= n || need_eq >= 2) return x;  // x_(j+1) = x_(j), or no x_(j+1)
     uint32_t m = 0xffffffffu;
