@@ -90,14 +90,23 @@ class Params:
 
 
 _lib = None
+_lib_path = _LIB  # the build lib() loads
+
+
+def use_library(path: str) -> None:
+    """Load the routines from another build of this source from now on: the
+    planted-mistake test builds altered copies and checks that the pins
+    fail on each."""
+    global _lib, _lib_path
+    _lib, _lib_path = None, path
 
 
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB):
+        if _lib_path == _LIB and not os.path.exists(_LIB):
             build(force=False)
-        L = ctypes.CDLL(_LIB)
+        L = ctypes.CDLL(_lib_path)
         vp, i32p, dp = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)
         L.ora_score_unit_v.argtypes = [vp, vp, vp, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                        ctypes.c_int, ctypes.c_int, ctypes.POINTER(_Params), dp, dp,
