@@ -42,6 +42,9 @@ MUTANTS = [
     ("sE_reversed", "sE[i] = (dE[i] - dmin) / (dmax - dmin + p->eps);", "sE[i] = (dmax - dE[i]) / (dmax - dmin + p->eps);"),
     ("winsor_upper_quantile", "hi = ora_quantile(dE, P, 1.0 - p->winsor_q);", "hi = ora_quantile(dE, P, 1.0 - 2.0 * p->winsor_q);"),
     ("mad_sign", "exp(-(dE[i] - med) / (p->mad_tau * mad + p->eps))", "exp((dE[i] - med) / (p->mad_tau * mad + p->eps))"),
+    ("quantile_rank_n", "const double h = q * (double)(n - 1);", "const double h = q * (double)n;"),
+    ("quantile_no_interpolation", "c[j] + (h - j) * (c[j + 1] - c[j])", "c[j]"),
+    ("mad_deviation_signed", "sE[i] = fabs(dE[i] - med);", "sE[i] = dE[i] - med;"),
     # redundancy and weight (Eq. (4)-(6), App. D)
     ("DE_over_prefix", "    DE /= (double)T;", "    DE /= (double)P;"),
     ("rE_missing_complement", "double rE = 2.0 - 2.0 / (1.0 + exp(-DE / tau));", "double rE = 2.0 / (1.0 + exp(-DE / tau));"),
@@ -60,6 +63,9 @@ MUTANTS = [
     ("tie_larger_position_first", "return a->key < b->key ? -1 : (a->key > b->key ? 1 : 0);",
      "return a->key > b->key ? -1 : (a->key < b->key ? 1 : 0);"),
     ("window_shifted", "for (int j = 0; j < w; ++j) idx[k + j] = P + j;", "for (int j = 0; j < w; ++j) idx[k + j] = P + j - 1;"),
+    ("head_budget_of_layer", "const int32_t b = budget[u / B];", "const int32_t b = budget[(u / B) / Hkv];"),
+    ("head_budget_units_by_sequence", "const int n = ora_select_unit(S + lh * Ptot + (cu[s] - s * w), T, w, budget[lh], idx + start[u]);",
+     "const int n = ora_select_unit(S + lh * Ptot + (cu[s] - s * w), T, w, budget[s % Hkv], idx + start[u]);"),
     ("flat_tie_position_major", "it[(int64_t)h * P + i].key = (int64_t)h * P + i;", "it[(int64_t)h * P + i].key = (int64_t)i * H + h;"),
     ("compact_V_from_K", "(const char *)V + (base + i) * row, row);", "(const char *)K + (base + i) * row, row);"),
     ("decode_scale_dropped", "x[j] = dot * inv_sqrt_d;", "x[j] = dot;"),
