@@ -289,14 +289,19 @@ __global__ __launch_bounds__(kDecThreads, 3) void k_decode_mx(DecodeArgs a)
         for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
     float *ptw = &pt[wv][0][0];
 
-    // every load is unconditional: rows past nrows read zero
+    // every load is unconditional: rows past nrows read zero.  A Kc load
+    // instruction covers 64 of a row's bytes, so two instructions share each
+    // 128-byte line: those loads keep the default cache policy, and the
+    // second finds the line the first brought in (nontemporal Kc loads took
+    // 68 us instead of 62 on the 28-layer cache); the Vc loads cover whole
+    // lines and stream nontemporally.
     auto load = [&](u32x4d (&kx)[TB][KS], u32x4d (&vx)[TB][NV], int b0) {
 #pragma unroll
         for (int t = 0; t < TB; ++t) {
 #pragma unroll
             for (int st = 0; st < KS; ++st)
                 kx[t][st] = __builtin_bit_cast(
-                    u32x4d, __builtin_amdgcn_raw_buffer_load_b128(rk, (b0 + 16 * t + r16) * RB + 64 * st + 16 * kg, 0, 2));
+                    u32x4d, __builtin_amdgcn_raw_buffer_load_b128(rk, (b0 + 16 * t + r16) * RB + 64 * st + 16 * kg, 0, 0));
 #pragma unroll
             for (int i = 0; i < NV; ++i)
                 vx[t][i] = __builtin_bit_cast(
