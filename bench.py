@@ -433,6 +433,33 @@ def main():
                                                       "tokens_per_s_per_layer": T / (ms / 1e3 / L)}
             del ep2
 
+    # the head-adaptive batch: 8 packed sequences of 4k-32k tokens, one layer,
+    # layer-flat selection with H_kv * floor(0.15 T_s) places per sequence
+    log("layer-flat selection over 8 packed sequences")
+    wv_ = W.varlen()
+    Kv_, Vv_, Qv_ = to_dev(wv_.K), to_dev(wv_.V), to_dev(wv_.Q)
+    shape_v = P.Shape(wv_.L, wv_.Hq, wv_.Hkv, wv_.D, wv_.w, wv_.cu_seqlens)
+    ep_v = EvictionPass(shape_v, wv_.budget, P.LAYER_FLAT, P.Params(), torch.bfloat16, "cuda")
+    for _ in range(3):
+        ep_v.run(Kv_, Vv_, Qv_)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        ep_v.run(Kv_, Vv_, Qv_)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_v = e0.elapsed_time(e1) / args.steps
+    tot_v = wv_.cu_seqlens[-1]
+    bytes_v = (wv_.Hkv * tot_v * wv_.D * 2 + wv_.Hq * (len(wv_.cu_seqlens) - 1) * wv_.w * wv_.D * 2
+               + 4 * ep_v.n_idx * wv_.D * 2 + 4 * ep_v.n_idx)
+    layer_flat_varlen = {
+        "sequences": len(wv_.cu_seqlens) - 1, "tokens": tot_v, "entries": ep_v.n_idx,
+        "ms_per_pass": round(ms_v, 4), "tokens_per_s": round(tot_v / (ms_v / 1e3), 1),
+        "algorithmic_bytes": bytes_v, "achieved_GBs": round(bytes_v / (ms_v / 1e3) / 1e9, 1),
+        "frac_of_hbm_peak": round(bytes_v / (ms_v / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
+    del ep_v, Kv_, Vv_, Qv_, wv_
+
     # the same stack as L single-layer calls on one stream (one call per layer
     # as its prefill finishes)
     log(f"{L} single-layer calls")
@@ -513,6 +540,7 @@ def main():
         "alternatives": alternatives,
         "decode_attention": decode_att,
         "with_prefill_sums": with_pre,
+        "layer_flat_varlen": layer_flat_varlen,
     }
     if extras:
         out["extras"] = extras

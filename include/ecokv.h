@@ -244,7 +244,9 @@ int ecokv_index_count_mode(const ecokv_shape *shape, int mode, const int32_t *bu
  *           LAYER_FLAT)
  *   offsets [L][H_kv][B] output: start of each unit in idx (may be NULL,
  *           except in LAYER_FLAT)
- * NaN scores rank below every number; -0 ranks equal to +0. */
+ * NaN scores rank below every number; -0 ranks equal to +0.
+ * ECOKV_EUNSUPPORTED: LAYER_FLAT with more than 256 KV heads, or with
+ * H_kv * Ptot * 4 > 2^31 - 1 bytes of scores per layer. */
 int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const int32_t *budget,
                  int32_t *idx, int32_t *counts, int32_t *offsets, void *stream);
 

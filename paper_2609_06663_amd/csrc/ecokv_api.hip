@@ -439,6 +439,9 @@ int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const 
         if (!counts || !offsets) return fail(ECOKV_EINVAL, "LAYER_FLAT needs counts and offsets");
         if (si.Hkv > ecokv::select_max_flat_heads())
             return fail(ECOKV_EUNSUPPORTED, "LAYER_FLAT supports at most %d KV heads", ecokv::select_max_flat_heads());
+        // (a selection group's scores are read through one 32-bit-addressed buffer descriptor)
+        if ((int64_t)si.Hkv * si.Ptot * 4 > INT32_MAX)
+            return fail(ECOKV_EUNSUPPORTED, "LAYER_FLAT: H_kv x P_total scores of a layer exceed 2^31 bytes");
     }
     if (si.L == 0) return ECOKV_OK;
     if (!scores || !idx) return fail(ECOKV_EINVAL, "scores and idx must be non-NULL");

@@ -83,7 +83,6 @@ struct GroupView {
     }
 };
 
-constexpr int kLdsKeys = 38912;  // keys kept in LDS by the resident variant (152 KiB)
 
 // The selection group of this block: layer l, heads h0 .. h0+nh-1 of
 // sequence s, min(budget, T_s) entries per head, first entry at out_base.
@@ -157,6 +156,39 @@ __device__ __forceinline__ void for_each_key(const Src &key, int64_t n, F &&f)
     }
 }
 
+// The same over the scores in memory, head by head (v = h P + i): no index
+// division per key; lane l reads scores 4l .. 4l+3 of each 4096-score round
+// with one 16-byte buffer load, four rounds in flight (the head's descriptor
+// ends at P, so loads past it read zero).
+typedef float f32x4s __attribute__((ext_vector_type(4)));
+template <class F>
+__device__ __forceinline__ void for_each_key(const KeySource<false> &key, int64_t n, F &&f)
+{
+    const GroupView &g = key.g;
+    constexpr int U = 4;
+    const int step = 4 * blockDim.x;
+    for (int h = 0; h < g.nh; ++h) {
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(uniform_ptr(g.base + (int64_t)h * g.hstride)), (short)0, uniform_i32(g.P) * 4,
+            0x00020000);
+        const int64_t vh = (int64_t)h * g.P;
+        for (int base = 4 * (int)threadIdx.x; base < g.P; base += U * step) {
+            f32x4s x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                x[u] = __builtin_bit_cast(f32x4s, __builtin_amdgcn_raw_buffer_load_b128(rs, (base + u * step) * 4, 0, 0));
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int i = base + u * step + e;
+                    if (i < g.P) f(vh + i, score_key(x[u][e]));
+                }
+        }
+    }
+    (void)n;
+}
+
 __device__ __forceinline__ uint32_t wave_min_u(uint32_t x)
 {
     for (int m = 32; m >= 1; m >>= 1) x = min(x, (uint32_t)__shfl_xor(x, m, kWave));
@@ -189,11 +221,20 @@ __device__ void radix_threshold(const Src &key, int64_t n, int64_t k, uint32_t k
     while (hi >= 0) {
         const int lo = hi >= 7 ? hi - 7 : 0;
         const uint32_t nb = 1u << (hi - lo + 1);
-        for (int b = threadIdx.x; b < 256; b += blockDim.x) hist[b] = 0;
+        for (int b = threadIdx.x; b < kSelWaves * 256; b += blockDim.x) hist[b] = 0;
         __syncthreads();
+        uint32_t *const myh = hist + (threadIdx.x >> 6) * 256;
         for_each_key(key, n, [&](int64_t, uint32_t kk) {
-            if ((kk & mask) == prefix) atomicAdd(&hist[(kk >> lo) & (nb - 1u)], 1u);
+            if ((kk & mask) == prefix) atomicAdd(&myh[(kk >> lo) & (nb - 1u)], 1u);
         });
+        __syncthreads();
+        if (threadIdx.x < 256) {
+            // fold the wave histograms into the first (each thread its own bin)
+            uint32_t c = 0;
+#pragma unroll
+            for (int w2 = 0; w2 < kSelWaves; ++w2) c += hist[w2 * 256 + threadIdx.x];
+            hist[threadIdx.x] = c;
+        }
         __syncthreads();
         if (threadIdx.x < kWave) {
             // lane l owns bins 255-4l .. 252-4l (descending order of digit)
@@ -235,11 +276,122 @@ __device__ void radix_threshold(const Src &key, int64_t n, int64_t k, uint32_t k
     *need_eq_out = rem;
 }
 
-template <bool RESIDENT>
+// radix_threshold for the streaming select of large groups, with the later
+// digits over a gathered list: after the first digit, the keys that keep the
+// chosen prefix (usually a small part of the group) are written to cand (one
+// LDS atomic per wave and load, positions by mbcnt), and the later digits
+// count only them into the first histogram, which the scanning wave reads
+// directly.  If more than cap keys keep the prefix, every digit reads all
+// keys.  hist: kSelWaves x 256 counters.
+constexpr int kCandKeys = 32768;  // gathered keys (128 KiB of LDS)
+
+__device__ void radix_threshold_gather(const KeySource<false> &key, int64_t n, int64_t k, uint32_t kmin, uint32_t kmax,
+                                       uint32_t *hist, uint32_t *bc, uint32_t *cand, uint32_t *ccount,
+                                       uint32_t *thr_out, int64_t *need_eq_out)
+{
+    const uint32_t diff = kmin ^ kmax;
+    if (diff == 0) {
+        *thr_out = kmin;
+        *need_eq_out = k;
+        return;
+    }
+    const int lane = threadIdx.x & 63;
+    int hi = 31 - __clz(diff);
+    uint32_t mask = hi == 31 ? 0u : ~((2u << hi) - 1u);
+    uint32_t prefix = kmin & mask;
+    int64_t rem = k;
+    bool first = true, listed = false;
+    uint32_t ncand = 0;
+    while (hi >= 0) {
+        const int lo = hi >= 7 ? hi - 7 : 0;
+        const uint32_t nb = 1u << (hi - lo + 1);
+        for (int b = threadIdx.x; b < kSelWaves * 256; b += blockDim.x) hist[b] = 0;
+        __syncthreads();
+        if (listed) {
+            for (uint32_t i = threadIdx.x; i < ncand; i += blockDim.x) {
+                const uint32_t kk = cand[i];
+                if ((kk & mask) == prefix) atomicAdd(&hist[(kk >> lo) & (nb - 1u)], 1u);
+            }
+        } else {
+            uint32_t *const myh = hist + (threadIdx.x >> 6) * 256;
+            for_each_key(key, n, [&](int64_t, uint32_t kk) {
+                if ((kk & mask) == prefix) atomicAdd(&myh[(kk >> lo) & (nb - 1u)], 1u);
+            });
+        }
+        __syncthreads();
+        if (!listed && threadIdx.x < 256) {
+            // fold the wave histograms into the first (each thread its own bin)
+            uint32_t c = 0;
+#pragma unroll
+            for (int w2 = 0; w2 < kSelWaves; ++w2) c += hist[w2 * 256 + threadIdx.x];
+            hist[threadIdx.x] = c;
+        }
+        __syncthreads();
+        if (threadIdx.x < kWave) {
+            // lane l owns bins 255-4l .. 252-4l (descending order of digit)
+            uint32_t c4[4], loc = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                c4[q] = hist[255 - 4 * lane - q];
+                loc += c4[q];
+            }
+            uint32_t inc = loc;
+#pragma unroll
+            for (int d = 1; d < kWave; d <<= 1) {
+                const uint32_t y = __shfl_up(inc, d, kWave);
+                if (lane >= d) inc += y;
+            }
+            const uint32_t before = inc - loc;
+            if ((int64_t)before < rem && rem <= (int64_t)inc) {
+                uint32_t cum = before;
+                for (int q = 0; q < 4; ++q) {
+                    if ((int64_t)(cum + c4[q]) >= rem) {
+                        bc[0] = 255u - 4u * lane - q;
+                        bc[1] = cum;
+                        break;
+                    }
+                    cum += c4[q];
+                }
+            }
+        }
+        __syncthreads();
+        const uint32_t digit = bc[0];
+        rem -= bc[1];
+        prefix |= digit << lo;
+        mask |= (nb - 1u) << lo;
+        hi = lo - 1;
+        __syncthreads();
+        if (first && hi >= 0) {
+            // gather the keys that keep the prefix
+            first = false;
+            if (threadIdx.x == 0) *ccount = 0u;
+            __syncthreads();
+            for_each_key(key, n, [&](int64_t, uint32_t kk) {
+                const bool m = (kk & mask) == prefix;
+                const unsigned long long bal = __ballot(m);
+                if (bal) {
+                    const int leader = __ffsll((long long)bal) - 1;
+                    uint32_t base = 0;
+                    if (lane == leader) base = atomicAdd(ccount, (uint32_t)__popcll(bal));
+                    base = __shfl(base, leader, kWave);
+                    const uint32_t pos = base + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
+                    if (m && pos < (uint32_t)kCandKeys) cand[pos] = kk;
+                }
+            });
+            __syncthreads();
+            ncand = *ccount;
+            listed = ncand <= (uint32_t)kCandKeys;
+        }
+    }
+    *thr_out = prefix;
+    *need_eq_out = rem;
+}
+
 __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a)
 {
-    __shared__ uint32_t keys_lds[RESIDENT ? kLdsKeys : 1];
-    __shared__ uint32_t hist[256];
+    __shared__ uint32_t hist[kSelWaves * 256];  // one histogram per wave
+    __shared__ uint32_t cand[kCandKeys];
+    __shared__ uint32_t ccount;
     __shared__ uint32_t bc[2];
     __shared__ uint32_t wsum[2 * kSelWaves + 2];
     __shared__ uint32_t mm[2][kSelWaves];
@@ -270,18 +422,16 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a)
     g.nh = nh;
     const int64_t n = (int64_t)nh * P;
     const int64_t k = (int64_t)nh * (beff - a.w);
-    const KeySource<RESIDENT> key{g, keys_lds};
+    const KeySource<false> key{g, nullptr};
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
 
     for (int h = tid; h < nh; h += blockDim.x) through[h] = 0;
     uint32_t thr = 0xffffffffu;
     int64_t need_eq = 0;
     if (k > 0) {
-        // keys (kept in LDS by the resident variant) and their extremes
+        // the keys' extremes
         uint32_t kmin = 0xffffffffu, kmax = 0u;
-        const KeySource<false> from_scores{g, nullptr};
-        for_each_key(from_scores, n, [&](int64_t v, uint32_t kk) {
-            if constexpr (RESIDENT) keys_lds[v] = kk;
+        for_each_key(key, n, [&](int64_t, uint32_t kk) {
             kmin = min(kmin, kk);
             kmax = max(kmax, kk);
         });
@@ -298,45 +448,88 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a)
             kmin = min(kmin, mm[0][q]);
             kmax = max(kmax, mm[1][q]);
         }
-        radix_threshold(key, n, k, kmin, kmax, hist, bc, &thr, &need_eq);
+        radix_threshold_gather(key, n, k, kmin, kmax, hist, bc, cand, &ccount, &thr, &need_eq);
     }
     __syncthreads();
 
     if (k > 0) {
-        // ordered emission: thread t owns the contiguous run [v0, v1)
+        // ordered emission: thread t owns the contiguous run [v0, v1); its
+        // keys are read by (head, position), stepped along the run (one
+        // division per thread), sixteen at a time: four 16-byte loads while
+        // they lie in one head, else one load per key.  One descriptor spans
+        // the group's scores (head h at h hstride).
         const int64_t per = (n + blockDim.x - 1) / blockDim.x;
         const int64_t v0 = min((int64_t)tid * per, n), v1 = min(v0 + per, n);
-        uint32_t cg = 0, ce = 0;
-        for (int64_t b = v0; b < v1; b += 8) {
-            uint32_t kk[8];
+        const int h_0 = nh == 1 ? 0 : (int)(v0 / P);
+        const int pos_0 = (int)(v0 - (int64_t)h_0 * P);
+        const __amdgpu_buffer_rsrc_t rg = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(uniform_ptr(g.base)), (short)0,
+            uniform_i32((int)(((int64_t)(nh - 1) * g.hstride + P) * 4)), 0x00020000);
+        auto load16 = [&](int hh, int pp, int64_t b, uint32_t (&kk)[16]) {
+            const int off = (int)((int64_t)hh * g.hstride + pp);
+            if (pp + 16 <= P && b + 16 <= v1) {
 #pragma unroll
-            for (int q = 0; q < 8; ++q) kk[q] = b + q < v1 ? key(b + q) : 0u;
+                for (int u = 0; u < 4; ++u) {
+                    const f32x4s x = __builtin_bit_cast(f32x4s, __builtin_amdgcn_raw_buffer_load_b128(rg, (off + 4 * u) * 4, 0, 0));
 #pragma unroll
-            for (int q = 0; q < 8; ++q)
-                if (b + q < v1) {
-                    cg += kk[q] > thr;
-                    ce += kk[q] == thr;
+                    for (int e = 0; e < 4; ++e) kk[4 * u + e] = score_key(x[e]);
                 }
+            } else {
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    kk[q] = b + q < v1 ? score_key(__builtin_bit_cast(
+                                             float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                        rg, (int)((int64_t)hh * g.hstride + pp) * 4, 0, 0)))
+                                       : 0u;
+                    if (++pp == P) {
+                        pp = 0;
+                        ++hh;
+                    }
+                }
+            }
+        };
+        uint32_t cg = 0, ce = 0;
+        {
+            int hh = h_0, pp = pos_0;
+            for (int64_t b = v0; b < v1; b += 16) {
+                uint32_t kk[16];
+                load16(hh, pp, b, kk);
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    if (b + q < v1) {
+                        cg += kk[q] > thr;
+                        ce += kk[q] == thr;
+                    }
+                    if (++pp == P) {
+                        pp = 0;
+                        ++hh;
+                    }
+                }
+            }
         }
         uint32_t eg, ee, tg, te;
         block_exscan2(cg, ce, wsum, eg, ee, tg, te);
         (void)tg;
         (void)te;
         int64_t gt_before = eg, eq_before = ee;
-        // head and position of v0, then stepped along the run
-        int h = nh == 1 ? 0 : (int)(v0 / P);
-        int pos = (int)(v0 - (int64_t)h * P);
-        for (int64_t v = v0; v < v1; ++v) {
-            const uint32_t kk = key(v);  // second read of the run (LDS, or cache-resident scores)
-            const bool gt = kk > thr, eq = kk == thr;
-            const bool take = gt || (eq && eq_before < need_eq);
-            if (take) out[gt_before + min(eq_before, need_eq) + (int64_t)h * a.w] = (int32_t)pos;
-            gt_before += gt;
-            eq_before += eq;
-            if (++pos == P) {
-                if (nh > 1) through[h] = gt_before + min(eq_before, need_eq);
-                pos = 0;
-                ++h;
+        int h = h_0, pos = pos_0;
+        for (int64_t b = v0; b < v1; b += 16) {
+            // the run's next sixteen keys (second read of the cache-resident scores)
+            uint32_t kk[16];
+            load16(h, pos, b, kk);
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                if (b + q >= v1) break;
+                const bool gt = kk[q] > thr, eq = kk[q] == thr;
+                const bool take = gt || (eq && eq_before < need_eq);
+                if (take) out[gt_before + min(eq_before, need_eq) + (int64_t)h * a.w] = (int32_t)pos;
+                gt_before += gt;
+                eq_before += eq;
+                if (++pos == P) {
+                    if (nh > 1) through[h] = gt_before + min(eq_before, need_eq);
+                    pos = 0;
+                    ++h;
+                }
             }
         }
         if (nh == 1 && tid == 0) through[0] = k;
@@ -924,7 +1117,7 @@ __device__ float key_quantile(const Src &key, int64_t n, double q, uint32_t kmin
 
 __global__ __launch_bounds__(kSelThreads) void k_dquant(DQuantArgs a)
 {
-    __shared__ uint32_t hist[256];
+    __shared__ uint32_t hist[kSelWaves * 256];  // one histogram per wave
     __shared__ uint32_t bc[2];
     __shared__ uint32_t red[2 * kSelWaves];
     const Unit un = unit_of(blockIdx.x, a.Hkv, a.B);
@@ -1050,10 +1243,8 @@ hipError_t select_launch(const SelectArgs &a, hipStream_t st)
         ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select_reg<32>, dim3(groups), dim3(kSelThreads), 0, st, a));
     else if (maxn <= kRegMaxKeys)
         ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select_reg<64>, dim3(groups), dim3(kSelThreads), 0, st, a));
-    else if (maxn <= kLdsKeys)
-        ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select<true>, dim3(groups), dim3(kSelThreads), 0, st, a));
     else
-        ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select<false>, dim3(groups), dim3(kSelThreads), 0, st, a));
+        ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select, dim3(groups), dim3(kSelThreads), 0, st, a));
     return hipGetLastError();
 }
 

@@ -115,6 +115,11 @@ def test_calls_fail_before_device_work(P):
     assert rc == -1
     rc = lib.ecokv_select(fake, ctypes.byref(s.c), 5, bud, fake, None, None, None)   # bad mode
     assert rc == -1
+    # layer-flat scores of a layer beyond 2^31 bytes (8 heads x 67.1 M tokens)
+    big = P.Shape(1, 8, 8, 128, 4, [0, 1 << 26, (1 << 26) + 200000])
+    bud2 = (ctypes.c_int32 * 2)(10, 10)
+    rc = lib.ecokv_select(fake, ctypes.byref(big.c), 1, bud2, fake, fake, fake, None)
+    assert rc == -3 and b"2^31" in lib.ecokv_last_error()
     rc = lib.ecokv_compact(fake, None, 0, ctypes.byref(s.c), 0, bud, fake, None, None, fake, fake, None)
     assert rc == -1
     rc = lib.ecokv_compact(fake, fake, 0, ctypes.byref(s.c), 1, bud, fake, None, None, fake, fake, None)

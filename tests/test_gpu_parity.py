@@ -395,3 +395,36 @@ def test_select_register_digit_paths(case):
     np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
     np.testing.assert_array_equal(counts.cpu().numpy(), ref_c.reshape(-1))
     np.testing.assert_array_equal(offsets.cpu().numpy(), ref_o.reshape(-1))
+
+
+@pytest.mark.parametrize("case", ["list_fits", "list_overflows", "ties_in_list"])
+def test_select_flat_large_group_paths(case):
+    # layer-flat groups of 4 x 32000 keys: past the register select, so the
+    # streaming select runs; its later digits count a gathered list of the keys
+    # that keep the first digit's prefix (up to 32768 of them), or every key
+    import paper_2609_06663_amd as P
+    rng = np.random.default_rng({"list_fits": 71, "list_overflows": 72, "ties_in_list": 73}[case])
+    L, Hkv, w, Pn = 1, 4, 4, 32000
+    S = np.exp(rng.uniform(np.log(1e-3), np.log(100.0), size=(L, Hkv, Pn))).astype(np.float32)
+    if case == "list_fits":
+        S[..., :6000] = 1.0 + rng.uniform(0, 1e-4, size=(L, Hkv, 6000)).astype(np.float32)
+    elif case == "list_overflows":
+        S[..., :31000] = 1.0 + rng.uniform(0, 1e-4, size=(L, Hkv, 31000)).astype(np.float32)
+    else:
+        S[..., :6000] = 1.0 + rng.integers(0, 64, size=(L, Hkv, 6000)).astype(np.float32) * np.float32(1e-6)
+    for h in range(Hkv):
+        rng.shuffle(S[0, h])
+    cu = [0, Pn + w]
+    budget = [12000 + w]
+    shape = P.Shape(L, Hkv, Hkv, 128, w, cu)
+    n = P.ecokv_index_count(shape, budget)
+    idx = torch.full((n,), -7, dtype=torch.int32, device="cuda")
+    counts = torch.full((L * Hkv,), -7, dtype=torch.int32, device="cuda")
+    offsets = torch.full_like(counts, -7)
+    say(f"layer-flat select-only bit-exact, {case}: 4 x 32000 keys, {Hkv * 12000} places")
+    P.ecokv_select(torch.from_numpy(np.ascontiguousarray(S)).cuda(), shape, P.LAYER_FLAT, budget, idx, counts, offsets)
+    torch.cuda.synchronize()
+    ref_idx, ref_c, ref_o = oracle.select(S.astype(np.float64), L, Hkv, cu, w, budget, oracle.LAYER_FLAT)
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
+    np.testing.assert_array_equal(counts.cpu().numpy(), ref_c.reshape(-1))
+    np.testing.assert_array_equal(offsets.cpu().numpy(), ref_o.reshape(-1))
