@@ -259,6 +259,7 @@ constexpr int kTilesPerBlock = 8;  // tiles per block (1024 keys)
 constexpr int kSweep1Depth = 2;    // tiles in flight ahead of the one in use
 constexpr int kSweep2Depth = 2;
 constexpr int kRows = kTile * kTilesPerBlock;
+constexpr int kSmallRows = 2 * kTile;  // keys per block when 1024-key blocks would be too few to fill the device
 
 // One 128-key tile into registers: 16 lanes per 256-byte row, coalesced.
 // Rows outside the descriptor's range come back as zero.
@@ -329,7 +330,7 @@ __device__ __forceinline__ void load_query_operands(const ScoreArgs &a, const Un
     }
 }
 
-// Sweep 1, per block of kRows keys:
+// Sweep 1, per block of a.rpb1 keys (kRows, or kSmallRows for calls with few blocks):
 //  * window logits on the matrix cores (window rows x 32 keys per wave) with
 //    per-row online softmax statistics, x = log2(e) q.k / sqrt(d_k);
 //  * |k|^2 from v_dot2 on the same B registers, and 1/|k| per key;
@@ -349,7 +350,7 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
     const Unit un = unit_of(u, a.Hkv, a.B);
     const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
     const int P = T - a.w;
-    const int row_base = blockIdx.x * kRows;
+    const int row_base = blockIdx.x * a.rpb1;
     if (row_base >= T) return;
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -381,8 +382,8 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
         }
     f32x16 csum = (f32x16){};
 
-    const int ntiles = min(kTilesPerBlock, (T - row_base + kTile - 1) / kTile);
-    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + kRows));
+    const int ntiles = min(a.rpb1 / kTile, (T - row_base + kTile - 1) / kTile);
+    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + a.rpb1));
     tile_pipeline<kSweep1Depth>(kt, rs, row_base, ntiles, g, c, [&](int tr0) {
         // window logits and |k|^2 of this wave's 32 keys
         f32x16 acc[MT];
@@ -545,7 +546,7 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
     const Unit un = unit_of(u, a.Hkv, a.B);
     const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
     const int P = T - a.w;
-    const int row_base = blockIdx.x * kRows;
+    const int row_base = blockIdx.x * a.rpb2;
     if (row_base >= T) return;
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -612,8 +613,8 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
 
     float dsum = 0.f, dsq = 0.f, dmn = INFINITY, dmx = -INFINITY;
     const float inv_r = 1.f / (float)a.R;
-    const int ntiles = min(kTilesPerBlock, (T - row_base + kTile - 1) / kTile);
-    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + kRows));
+    const int ntiles = min(a.rpb2 / kTile, (T - row_base + kTile - 1) / kTile);
+    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + a.rpb2));
     tile_pipeline<kSweep2Depth>(kt, rs, row_base, ntiles, g, c, [&](int tr0) {
 
         f32x16 acc[MT];
@@ -1770,6 +1771,15 @@ bool score_fast_path(int D, bool bf16) { return bf16 && D == fast::kD; }
 
 static int rows_per_block(int D, bool bf16) { return score_fast_path(D, bf16) ? fast::kRows : kCh; }
 
+// Key rows per block of the block sweeps for a call: 256-key blocks when
+// 1024-key ones would be fewer than 1024 (one 8192-token layer: 32 blocks
+// on 256 compute units).
+static int block_sweep_rows(int D, bool bf16, int U, int maxT)
+{
+    if (!score_fast_path(D, bf16)) return kCh;
+    return (int64_t)U * ((maxT + fast::kRows - 1) / fast::kRows) >= 1024 ? fast::kRows : fast::kSmallRows;
+}
+
 // ---------------------------------------------------------------------------
 // Value-norm importance (ECOKV_IMP_ATTN_VNORM, Sec. 5.2): S_imp(i) =
 // pool(a)(i) * |v_i|_2 for the non-window keys, in one coalesced pass over V.
@@ -1843,9 +1853,9 @@ WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int 
 {
     WsLayout w{};
     const int64_t U = (int64_t)L * Hkv * B;
-    // the smallest key block of any sweep: the block sweeps' rows, or the
-    // streaming sweeps' small blocks
-    const int rpb = min(rows_per_block(D, bf16), fast::kS2KeysSmall);
+    // the smallest key block of any sweep: the block sweeps' small blocks
+    // (the streaming sweeps' are larger)
+    const int rpb = min(rows_per_block(D, bf16), fast::kSmallRows);
     const int64_t nch1 = (maxT + rpb - 1) / rpb;
     // the single-read path publishes per slice; size for it whenever it may run
     const bool single = bf16 && D == fast::kD && R <= kFusedMaxRows;
@@ -1963,7 +1973,7 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         ECOKV_TIMED("single_read", st, e = fused_launch(a, fgrid, st));
         if (e != hipSuccess) return e;
     } else {
-        a.rpb1 = rows_per_block(a.D, bf16);
+        a.rpb1 = block_sweep_rows(a.D, bf16, U, maxT);
         a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
         const dim3 grid(a.nch1, U);
         if (a.pre) {
@@ -2004,7 +2014,7 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
                             hipLaunchKernelGGL(fast::k_fs2s<fast::kS2KeysSmall>, dim3(a.nch2, U), dim3(256), 0, st, a));
         } else {
             // block sweep 2: the chunking of the block sweeps (grid)
-            a.rpb2 = rows_per_block(a.D, bf16);
+            a.rpb2 = block_sweep_rows(a.D, bf16, U, maxT);
             a.nch2 = (maxT + a.rpb2 - 1) / a.rpb2;
             ECOKV_TIMED("sweep2_block", st, launch_sweep(2, a, grid, st, bf16));
         }
