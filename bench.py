@@ -479,7 +479,37 @@ def main():
     ms1 = e0.elapsed_time(e1) / args.steps
     per_layer_calls = {"ms_per_step": round(ms1, 4), "us_per_layer": round(ms1 * 1e3 / L, 2),
                        "tokens_per_s_per_layer": round(T / (ms1 / 1e3 / L), 1)}
-    del ep1, Ks, Vs, Qs
+    # the same calls alternating over two streams (one workspace each): one
+    # layer's latency-bound kernels overlap the next layer's sweeps
+    log(f"{L} single-layer calls on two streams")
+    ep2s = [ep1, EvictionPass(shape1, [b], P.PER_HEAD, P.Params(), torch.bfloat16, "cuda")]
+    st2 = [torch.cuda.Stream(), torch.cuda.Stream()]
+
+    def two_streams():
+        ev = torch.cuda.Event()
+        ev.record(stream)
+        for s2 in st2:
+            s2.wait_event(ev)
+        for l in range(L):
+            with torch.cuda.stream(st2[l % 2]):
+                ep2s[l % 2].run(Ks[l], Vs[l], Qs[l], stream=st2[l % 2])
+        for s2 in st2:
+            e = torch.cuda.Event()
+            e.record(s2)
+            stream.wait_event(e)
+
+    for _ in range(3):
+        two_streams()
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        two_streams()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms2 = e0.elapsed_time(e1) / args.steps
+    per_layer_calls["two_streams_ms_per_step"] = round(ms2, 4)
+    per_layer_calls["two_streams_us_per_layer"] = round(ms2 * 1e3 / L, 2)
+    del ep1, ep2s, Ks, Vs, Qs
 
     # a plain device copy of 1 GiB (torch's copy kernel), for the bandwidth the
     # memory system gives an ordinary streaming kernel next to the 8 TB/s peak
