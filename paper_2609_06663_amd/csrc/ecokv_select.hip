@@ -823,8 +823,7 @@ constexpr int kRegMaxKeys = 64 * kSelThreads;
 template <int KPT>
 __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
 {
-    // KPT == 32: the radix histograms live in stg
-    __shared__ uint32_t hist[KPT == 32 ? 1 : kSelWaves * 256];
+    // the radix histograms and the gathered keys live in stg
     __shared__ uint32_t hsum[256];
     __shared__ uint32_t bc[2][2];
     __shared__ uint32_t wsum[2 * kSelWaves + 2];
@@ -832,11 +831,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
     __shared__ uint32_t ccount;
     __shared__ int64_t through[kMaxFlatHeads];
     typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
-    // KPT == 32: the stage of the coalesced score load, then of the radix
-    // histograms and candidates, then of the output (the barriers of the
-    // extremes and of the radix passes separate the three uses)
-    __shared__ u32x4_t stg[KPT == 32 ? KPT / 4 * kSelThreads : 1];
-    static_assert(KPT != 32 || kStCandCap > 0, "histograms must fit the stage");
+    // 128 KiB: with KPT == 32 the stage of the coalesced score load, then of
+    // the radix histograms and gathered keys, then of the output (the
+    // barriers of the extremes and of the radix passes separate the three
+    // uses); with KPT == 64 the radix scratch only
+    __shared__ u32x4_t stg[8 * kSelThreads];
+    static_assert(kStCandCap > 0, "histograms must fit the stage");
 
     const SelGroup grp = sel_group(a);
     const int l = grp.l, h0 = grp.h0, s = grp.s, nh = grp.nh;
@@ -941,11 +941,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
             reg_extremes<KPT>(kk, v0, n, mm, &kmin, &kmax);
         }
         // radix select of the k-th largest key
-        if constexpr (KPT == 32)
-            reg_radix_select_staged<KPT>(kk, v0, n, k, kmin, kmax, reinterpret_cast<uint32_t *>(stg), hsum, bc,
-                                         &ccount, &thr, &need_eq);
-        else
-            reg_radix_select<KPT>(kk, v0, n, k, kmin, kmax, hist, hsum, bc, &thr, &need_eq);
+        reg_radix_select_staged<KPT>(kk, v0, n, k, kmin, kmax, reinterpret_cast<uint32_t *>(stg), hsum, bc, &ccount,
+                                     &thr, &need_eq);
     }
     if (k > 0 && nh == 1 && KPT == 32) {
         // ordered emission of one head: bit q of gtm / eqm marks key v0 + q

@@ -428,3 +428,31 @@ def test_select_flat_large_group_paths(case):
     np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
     np.testing.assert_array_equal(counts.cpu().numpy(), ref_c.reshape(-1))
     np.testing.assert_array_equal(offsets.cpu().numpy(), ref_o.reshape(-1))
+
+
+@pytest.mark.parametrize("case", ["fits", "overflows"])
+def test_select_register_64_keys_per_thread(case):
+    # 60000-key units: 64 keys per thread; the later digits count the gathered
+    # keys that keep the first digit's prefix, or every key when they overflow
+    import paper_2609_06663_amd as P
+    rng = np.random.default_rng({"fits": 81, "overflows": 82}[case])
+    L, Hkv, w, Pn = 1, 2, 4, 60000
+    S = np.exp(rng.uniform(np.log(1e-3), np.log(100.0), size=(L, Hkv, Pn))).astype(np.float32)
+    nc = 10000 if case == "fits" else 55000
+    S[..., :nc] = 1.0 + rng.uniform(0, 1e-4, size=(L, Hkv, nc)).astype(np.float32)
+    for h in range(Hkv):
+        rng.shuffle(S[0, h])
+    cu = [0, Pn + w]
+    budget = [20000 + w]
+    shape = P.Shape(L, Hkv, Hkv, 128, w, cu)
+    n = P.ecokv_index_count(shape, budget)
+    idx = torch.full((n,), -7, dtype=torch.int32, device="cuda")
+    counts = torch.full((L * Hkv,), -7, dtype=torch.int32, device="cuda")
+    offsets = torch.full_like(counts, -7)
+    say(f"select-only bit-exact, 60000-key units, gathered list {case}")
+    P.ecokv_select(torch.from_numpy(np.ascontiguousarray(S)).cuda(), shape, P.PER_HEAD, budget, idx, counts, offsets)
+    torch.cuda.synchronize()
+    ref_idx, ref_c, ref_o = oracle.select(S.astype(np.float64), L, Hkv, cu, w, budget, oracle.PER_HEAD)
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
+    np.testing.assert_array_equal(counts.cpu().numpy(), ref_c.reshape(-1))
+    np.testing.assert_array_equal(offsets.cpu().numpy(), ref_o.reshape(-1))
