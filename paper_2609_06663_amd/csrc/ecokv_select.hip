@@ -944,42 +944,59 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
         reg_radix_select_staged<KPT>(kk, v0, n, k, kmin, kmax, reinterpret_cast<uint32_t *>(stg), hsum, bc, &ccount,
                                      &thr, &need_eq);
     }
-    if (k > 0 && nh == 1 && KPT == 32) {
-        // ordered emission of one head: bit q of gtm / eqm marks key v0 + q
-        // above / equal to the threshold; the thread's taken keys go to
-        // consecutive slots from the number taken before its run
-        typedef uint32_t bits_t;
-        bits_t gtm = 0, eqm = 0;
+    if (k > 0 && nh == 1) {
+        // ordered emission of one head: bit q of gtm[c] / eqm[c] marks key
+        // v0 + 32 c + q above / equal to the threshold; the thread's taken
+        // keys go to consecutive slots from the number taken before its run
+        constexpr int NC = KPT / 32;  // 32-key words per thread
+        uint32_t gtm[NC], eqm[NC];
+        uint32_t cg = 0, ce = 0;
 #pragma unroll
-        for (int q = 0; q < KPT; ++q)
-            if (v0 + q < n) {
-                gtm |= kk[q] > thr ? (bits_t)1 << q : (bits_t)0;
-                eqm |= kk[q] == thr ? (bits_t)1 << q : (bits_t)0;
-            }
-        const uint32_t cg = (uint32_t)__builtin_popcount(gtm), ce = (uint32_t)__builtin_popcount(eqm);
+        for (int c = 0; c < NC; ++c) {
+            gtm[c] = 0u;
+            eqm[c] = 0u;
+#pragma unroll
+            for (int q = 0; q < 32; ++q)
+                if (v0 + 32 * c + q < n) {
+                    gtm[c] |= kk[32 * c + q] > thr ? 1u << q : 0u;
+                    eqm[c] |= kk[32 * c + q] == thr ? 1u << q : 0u;
+                }
+            cg += (uint32_t)__builtin_popcount(gtm[c]);
+            ce += (uint32_t)__builtin_popcount(eqm[c]);
+        }
         uint32_t eg, ee, tg, te;
         block_exscan2(cg, ce, wsum, eg, ee, tg, te);
         (void)tg;
         (void)te;
         // equal keys are taken in position order while fewer than need_eq precede them
         const int eq_take = min((int)ce, max(need_eq - (int)ee, 0));
-        bits_t take = gtm, em = eqm;
+        uint32_t take[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) take[c] = gtm[c];
         for (int r = 0; r < eq_take; ++r) {
-            const bits_t low = em & (~em + 1);
-            take |= low;
-            em ^= low;
+            bool done = false;
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                if (!done && eqm[c]) {
+                    const uint32_t low = eqm[c] & (~eqm[c] + 1u);
+                    take[c] |= low;
+                    eqm[c] ^= low;
+                    done = true;
+                }
         }
         int o = (int)eg + min((int)ee, need_eq);
-        while (take) {
-            const int q = __builtin_ctz(take);
-            take &= take - 1;
-            if (staged) ost[o] = (uint32_t)(v0 + q);
-            else out[o] = v0 + q;
-            ++o;
-        }
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+            while (take[c]) {
+                const int q = 32 * c + __builtin_ctz(take[c]);
+                take[c] &= take[c] - 1u;
+                if (staged) ost[o] = (uint32_t)(v0 + q);
+                else out[o] = v0 + q;
+                ++o;
+            }
         if (tid == 0) through[0] = k;
     } else if (k > 0) {
-        // ordered emission from the registers (several heads, or 64 keys a thread)
+        // ordered emission from the registers (several heads)
         uint32_t cg = 0, ce = 0;
 #pragma unroll
         for (int q = 0; q < KPT; ++q)
