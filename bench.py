@@ -119,7 +119,7 @@ def main():
 
     import workloads as W
     import paper_2609_06663_amd as P
-    from paper_2609_06663_amd.pipeline import EvictionPass
+    from paper_2609_06663_amd.pipeline import EvictionPass, LayerwiseEviction
 
     T, L = args.tokens, args.layers
     log(f"generating stack: {L} layers x 4 KV heads x {T} tokens (bf16)")
@@ -482,21 +482,11 @@ def main():
     # the same calls alternating over two streams (one workspace each): one
     # layer's latency-bound kernels overlap the next layer's sweeps
     log(f"{L} single-layer calls on two streams")
-    ep2s = [ep1, EvictionPass(shape1, [b], P.PER_HEAD, P.Params(), torch.bfloat16, "cuda")]
-    st2 = [torch.cuda.Stream(), torch.cuda.Stream()]
+    lw = LayerwiseEviction(shape1, [b], L)
 
     def two_streams():
-        ev = torch.cuda.Event()
-        ev.record(stream)
-        for s2 in st2:
-            s2.wait_event(ev)
-        for l in range(L):
-            with torch.cuda.stream(st2[l % 2]):
-                ep2s[l % 2].run(Ks[l], Vs[l], Qs[l], stream=st2[l % 2])
-        for s2 in st2:
-            e = torch.cuda.Event()
-            e.record(s2)
-            stream.wait_event(e)
+        lw.run_layers(range(L), Ks, Vs, Qs)
+        lw.wait()
 
     for _ in range(3):
         two_streams()
@@ -509,7 +499,7 @@ def main():
     ms2 = e0.elapsed_time(e1) / args.steps
     per_layer_calls["two_streams_ms_per_step"] = round(ms2, 4)
     per_layer_calls["two_streams_us_per_layer"] = round(ms2 * 1e3 / L, 2)
-    del ep1, ep2s, Ks, Vs, Qs
+    del ep1, lw, Ks, Vs, Qs
 
     # a plain device copy of 1 GiB (torch's copy kernel), for the bandwidth the
     # memory system gives an ordinary streaming kernel next to the 8 TB/s peak

@@ -16,7 +16,7 @@ from . import ecokv as E
 class EvictionPass:
     def __init__(self, shape: E.Shape, budget, mode: int = E.PER_HEAD,
                  params: Optional[E.Params] = None, dtype: torch.dtype = torch.bfloat16,
-                 device: str = "cuda"):
+                 device: str = "cuda", workspace: Optional[torch.Tensor] = None):
         self.shape, self.budget, self.mode = shape, E._flat_ints(budget), mode
         self.params = params or E.Params()
         c = shape.c
@@ -28,7 +28,10 @@ class EvictionPass:
         self.lambda_ = torch.empty(U, dtype=torch.float32, device=device)
         self.stats = torch.empty(U * E.NSTATS, dtype=torch.float32, device=device)
         ws = E.ecokv_workspace_size(shape, self.params)
-        self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
+        if workspace is not None and workspace.numel() >= ws:
+            self.workspace = workspace  # (shared with passes that never run at the same time)
+        else:
+            self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
         self.n_idx = E.ecokv_index_count_mode(shape, mode, self.budget)
         self.idx = torch.empty(max(self.n_idx, 1), dtype=torch.int32, device=device)
         self.counts = torch.empty(max(U, 1), dtype=torch.int32, device=device)
@@ -62,3 +65,56 @@ class EvictionPass:
         self.select(stream)
         self.compact(K, V, stream)
         return self
+
+
+class LayerwiseEviction:
+    """The pass for one layer at a time, as a prefill finishes each layer.
+
+    Layer l runs on the l % 2-th of two side streams (default priority), with
+    its own outputs (`passes[l]`: scores, idx, counts, offsets, Kc, Vc) and the
+    workspace of its stream.  One layer's select and epilogue occupy only a few
+    compute units; on two streams they overlap the next layer's sweeps (28
+    layers of 28q/4kv at 32768 tokens: 77 -> 48 us per layer).  `run_layer`
+    orders the layer after the work already queued on the caller's stream;
+    `wait` makes the caller's stream wait for every layer queued so far.  The
+    caller keeps a layer's K, V and Q_win alive until `wait` (they are read on
+    a side stream, which torch's allocator does not track).  The per-layer
+    host work is one event record and wait plus the three library calls.
+    """
+
+    def __init__(self, shape: E.Shape, budget, num_layers: int, mode: int = E.PER_HEAD,
+                 params: Optional[E.Params] = None, dtype: torch.dtype = torch.bfloat16, device: str = "cuda"):
+        if shape.c.num_layers != 1:
+            raise ValueError("LayerwiseEviction takes the shape of one layer (num_layers = 1)")
+        params = params or E.Params()
+        ws = max(E.ecokv_workspace_size(shape, params), 256)
+        self.streams = [torch.cuda.Stream(device=device), torch.cuda.Stream(device=device)]
+        self.workspaces = [torch.empty(ws, dtype=torch.uint8, device=device) for _ in range(2)]
+        self.passes = [EvictionPass(shape, budget, mode, params, dtype, device, self.workspaces[l % 2])
+                       for l in range(num_layers)]
+        self._ready = [torch.cuda.Event(), torch.cuda.Event()]
+        self._done = [torch.cuda.Event(), torch.cuda.Event()]
+
+    def run_layer(self, layer: int, K: torch.Tensor, V: torch.Tensor, Q_win: torch.Tensor) -> EvictionPass:
+        i = layer % 2
+        s, ready = self.streams[i], self._ready[i]
+        ready.record(torch.cuda.current_stream(K.device))
+        s.wait_event(ready)
+        return self.passes[layer].run(K, V, Q_win, stream=s)
+
+    def run_layers(self, layers, K, V, Q_win):
+        """Several layers whose inputs are all ready: one ordering event for
+        all of them (per-layer events cost 48 -> 54 us per layer on the
+        28-layer stack).  K, V, Q_win: sequences indexed like `layers`."""
+        cur = torch.cuda.current_stream(self.workspaces[0].device)
+        for s, ready in zip(self.streams, self._ready):
+            ready.record(cur)
+            s.wait_event(ready)
+        for j, layer in enumerate(layers):
+            self.passes[layer].run(K[j], V[j], Q_win[j], stream=self.streams[layer % 2])
+
+    def wait(self):
+        cur = torch.cuda.current_stream(self.workspaces[0].device)
+        for s, done in zip(self.streams, self._done):
+            done.record(s)
+            cur.wait_event(done)
