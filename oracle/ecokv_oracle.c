@@ -23,6 +23,9 @@
  * the two share no source, header, table or helper.
  *
  * Readings of points the paper leaves open are marked "Reading:" below.
+ * Parity unpinned: the sigmoid that maps the MAD-scaled deviation to s_E
+ * (ECOKV_NORM_MAD, an alternative of Sec. 6.3); the paper gives no formula
+ * or value for it, so it rests on that reading alone.
  * Inputs are the exact bytes the GPU consumes (bf16 bit patterns or fp32),
  * decoded exactly to double; everything is accumulated in double with plain
  * loops, in the order the paper states the steps.
@@ -291,7 +294,9 @@ int ora_score_unit_v(const void *K, const void *V, const void *Q, size_t q_gstri
         /* Per-head MAD scaling (Sec. 6.3, Table 4), temperature mad_tau.
          * Reading: the deviation from the median in units of the median
          * absolute deviation, mapped to (0, 1) by a sigmoid so that it blends
-         * with s_C as the min-max value does. */
+         * with s_C as the min-max value does.  Parity unpinned: the paper
+         * names the method but not the mapping, so no pin can fix the sigmoid
+         * (the median and MAD themselves are pinned to numpy). */
         const double med = ora_quantile(dE, P, 0.5);
         for (int i = 0; i < P; ++i) sE[i] = fabs(dE[i] - med);  /* the deviations, then s_E */
         const double mad = ora_quantile(sE, P, 0.5);

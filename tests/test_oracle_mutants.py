@@ -19,6 +19,11 @@ PINS = os.path.join(ROOT, "tests", "test_oracle_pins.py")
 
 # (name, text in the source, replacement); each text occurs exactly once
 MUTANTS = [
+    # input decode: bf16 bit patterns are the upper half of a binary32
+    ("bf16_decode_shift", "uint32_t u = (uint32_t)((const uint16_t *)base)[i] << 16;",
+     "uint32_t u = (uint32_t)((const uint16_t *)base)[i] << 15;"),
+    ("bf16_decode_low_half", "uint32_t u = (uint32_t)((const uint16_t *)base)[i] << 16;",
+     "uint32_t u = (uint32_t)((const uint16_t *)base)[i];"),
     # window importance (Sec. 3, Sec. 5.2)
     ("logit_scale_dropped", "logit[i] = dot * inv_sqrt_d;", "logit[i] = dot;"),
     ("causal_row_short", "const int last = p->causal ? P + j : T - 1;", "const int last = p->causal ? P + j - 1 : T - 1;"),

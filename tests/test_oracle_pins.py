@@ -464,6 +464,51 @@ def test_compact_is_exact_gather(ora):
 
 
 # --------------------------------------------------------------------------
+# Input decode: every bf16 configuration reaches the oracle as bit patterns
+# --------------------------------------------------------------------------
+
+def test_bf16_keys_decode_to_their_values(ora):
+    # bf16 is the upper half of an IEEE binary32: 0x3f80 = 1, 0x4000 = 2,
+    # 0x4040 = 3, 0xbf80 = -1, 0x3f00 = 0.5, 0x4120 = 10 (exact values).  With
+    # identical window queries of zero the attention is uniform, so only the
+    # anchors depend on the keys: kbar is the exact column mean of the values.
+    bits = np.array([[0x3f80, 0x4000], [0x4040, 0xbf80], [0x3f00, 0x4120], [0x4000, 0x3f80]], np.uint16)
+    vals = np.array([[1.0, 2.0], [3.0, -1.0], [0.5, 10.0], [2.0, 1.0]])
+    Q = np.zeros((1, 1, 2), np.uint16)
+    r = ora.score_unit(bits, Q, 1, ora.Params(pool_kernel=1), trace=True)
+    np.testing.assert_array_equal(r["kbar"], vals.mean(axis=0))
+    np.testing.assert_allclose(r["dE"], np.linalg.norm(vals - vals.mean(axis=0), axis=1), rtol=1e-15)
+    # subnormal and negative-zero patterns decode exactly too
+    bits2 = np.array([[0x0001, 0x8000], [0x0080, 0x0000], [0x3f80, 0x3f80]], np.uint16)
+    vals2 = np.array([[2.0 ** -133, 0.0], [2.0 ** -126, 0.0], [1.0, 1.0]])
+    r2 = ora.score_unit(bits2, np.zeros((1, 1, 2), np.uint16), 1, ora.Params(pool_kernel=1), trace=True)
+    np.testing.assert_array_equal(r2["kbar"], vals2.mean(axis=0))
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_bf16_unit_equals_its_float32_values(ora, seed):
+    # the same unit given as bf16 bit patterns and as the float32 values those
+    # patterns encode (decoded here by numpy, not by the oracle) scores
+    # identically, bit for bit, with the value norm too
+    wl = W.custom(seed, L=1, Hq=6, Hkv=2, D=32, w=3, seqlens=[70], dtype="bf16", group=8, strength=2.0)
+    for h in range(2):
+        K, V, Q = wl.K[0, h], wl.V[0, h], wl.Q[0, 3 * h:3 * h + 3, 0]
+        p = ora.Params(imp_mode=ora.IMP_ATTN_VNORM)
+        rb = ora.score_unit(K, Q, wl.w, p, V=V)
+        rf = ora.score_unit(W.bf16_bits_to_f32(K), W.bf16_bits_to_f32(Q), wl.w, p, V=W.bf16_bits_to_f32(V))
+        np.testing.assert_array_equal(rb["S"], rf["S"])
+        np.testing.assert_array_equal(rb["stats"], rf["stats"])
+    Qd = wl.Q[0, :, 0, 0]
+    O, lse = ora.decode(Qd[None, :, None], wl.K[0, 0, :9], wl.V[0, 0, :9], 1, 6, 2, 1, 32,
+                        np.array([[[9], [0]]]), np.array([[[0], [9]]]))
+    O2, lse2 = ora.decode(W.bf16_bits_to_f32(Qd)[None, :, None], W.bf16_bits_to_f32(wl.K[0, 0, :9]),
+                          W.bf16_bits_to_f32(wl.V[0, 0, :9]), 1, 6, 2, 1, 32,
+                          np.array([[[9], [0]]]), np.array([[[0], [9]]]))
+    np.testing.assert_array_equal(O[0, :3], O2[0, :3])
+    np.testing.assert_array_equal(lse[0, :3], lse2[0, :3])
+
+
+# --------------------------------------------------------------------------
 # Generator sanity (statistics of the synthetic tiny workload)
 # --------------------------------------------------------------------------
 
