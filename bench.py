@@ -52,7 +52,7 @@ def log(msg):
 STAGE_KERNELS = {
     "sweep1_stream": ["k_fs1s"], "sweep1_block": ["k_fs1", "k_pass1"], "reduce1": ["k_reduce1"],
     "sweep2_stream": ["k_fs2s"], "sweep2_block": ["k_fs2", "k_pass2"], "epilogue": ["k_epi_unit"],
-    "epilogue1": ["k_epi1"], "epilogue2": ["k_epi2"], "single_read": ["k_fused"],
+    "epilogue1": ["k_epi1"], "epilogue2": ["k_epi2"],
     "select": ["k_select_reg", "k_select"], "compact": ["k_compact"], "vnorm": ["k_vnorm"],
     "dquant": ["k_dquant", "k_dquant_reg"], "decode": ["k_decode_mx", "k_decode"], "decode_merge": ["k_decode_merge"],
     "pre_anchors": ["k_pre_anchors"],
@@ -208,7 +208,7 @@ def main():
     stage_algo = {
         "sweep1_stream": bytes_k + bytes_q, "sweep1_block": bytes_k + bytes_q,
         "sweep2_stream": bytes_k + bytes_q, "sweep2_block": bytes_k + bytes_q,
-        "single_read": bytes_k + bytes_q + bytes_scores, "reduce1": 0, "epilogue": bytes_scores,
+        "reduce1": 0, "epilogue": bytes_scores,
         "epilogue1": 0, "epilogue2": bytes_scores, "select": bytes_scores + bytes_idx,
         "compact": bytes_gather + bytes_idx,
     }
@@ -238,7 +238,7 @@ def main():
     }
     pass_gbs = pass_bytes / (ms_per_step / 1e3) / 1e9
     mfma = {}
-    for name in ("sweep1_stream", "sweep2_stream", "single_read"):
+    for name in ("sweep1_stream", "sweep2_stream"):
         if name in kernels:
             tf = window_flops / (kernels[name]["avg_us"] / 1e6) / 1e12
             mfma[name] = {"window_flops": window_flops, "achieved_tflops": round(tf, 1),
@@ -642,7 +642,10 @@ def cpu_baseline(wl, sample_layers):
         ncpu = len(os.sched_getaffinity(0))
     except AttributeError:
         ncpu = os.cpu_count() or 1
-    threads = max(1, min(16, ncpu))
+    # the host cores this process may use: its CPU affinity, or the thread
+    # count the machine assigns it (OMP_NUM_THREADS) when that is smaller
+    omp = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    threads = max(1, min(ncpu, omp) if omp > 0 else ncpu)
     Ls = min(sample_layers, wl.L)
     K, V, Q = wl.K[:Ls], wl.V[:Ls], wl.Q[:Ls]
     log(f"cpu baseline: oracle on {Ls} layers x {wl.Hkv} heads with {threads} threads, repeated for >= 10 s")
@@ -659,7 +662,8 @@ def cpu_baseline(wl, sample_layers):
     used = min(threads, Ls * wl.Hkv)
     return {"value": round(T * reps / (dt / Ls), 1), "unit": "tokens/s per layer", "cores": used, "kind": "oracle",
             "sample": f"first {Ls} of {wl.L} layers ({Ls * wl.Hkv} (layer, head) units of {T} tokens), "
-                      f"score+select+compact, fp64, {reps} repetitions, {dt:.2f}s wall"}
+                      f"score+select+compact, fp64, {reps} repetitions, {dt:.2f}s wall",
+            "host_cpus": {"affinity": ncpu, "os_cpu_count": os.cpu_count(), "OMP_NUM_THREADS": omp or None}}
 
 
 def cpu_baseline_one_thread():

@@ -20,10 +20,11 @@
  *  - All tensor pointers are DEVICE pointers unless stated; the caller
  *    allocates and owns every buffer (inputs, outputs, workspace).  The library
  *    never allocates or frees device memory and never synchronises outside
- *    ecokv_stage_times().  Its only process-wide state is a launch counter, a
- *    per-device cache of the compute-unit count and the optional stage timer;
- *    calls on different streams with different workspaces may run
- *    concurrently (see ecokv_score for the single-read path).
+ *    ecokv_stage_times() and ecokv_workspace_status().  Its only process-wide
+ *    state is an atomic launch counter (tags that tell one launch's values from
+ *    an older one's), a per-device cache of the number of blocks the device
+ *    holds at once and the optional stage timer; calls on different streams
+ *    with different workspaces may run concurrently.
  *  - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *    Work is enqueued asynchronously; results are valid once the stream has
  *    been synchronised.
@@ -56,6 +57,8 @@ extern "C" {
 #define ECOKV_EWORKSPACE (-2)   /* workspace smaller than ecokv_workspace_size   */
 #define ECOKV_EUNSUPPORTED (-3) /* valid request this build does not implement   */
 #define ECOKV_EHIP (-4)         /* the HIP runtime refused a launch              */
+#define ECOKV_ETIMEOUT (-5)     /* a bounded wait between blocks gave up (see    */
+                                /* ecokv_workspace_status)                        */
 
 #define ECOKV_BF16 0 /* bfloat16 elements (2 bytes) */
 #define ECOKV_F32 1  /* float32 elements  (4 bytes) */
@@ -148,10 +151,21 @@ int ecokv_default_params(ecokv_params *p);
 
 /* Bytes of device workspace ecokv_score / ecokv_score_v need for this shape
  * and these parameters (select and compact need none; ECOKV_IMP_ATTN_VNORM
- * adds one float per non-window key).  The workspace is scratch: its contents
- * are undefined between calls and it must not be shared by calls that may
+ * adds one float per non-window key).  The workspace is scratch, except for
+ * its first 4 bytes, a status word (see ecokv_workspace_status) that must be
+ * zero before the workspace's first use: allocate it zero-filled, or call
+ * ecokv_workspace_status once.  It must not be shared by calls that may
  * overlap. */
 int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, size_t *bytes);
+
+/* Status of the score calls enqueued on `workspace` since the last query.
+ * The only failure a score call can meet after its launch is a bounded wait
+ * between two blocks of its final step that gives up (see ecokv_score); it
+ * then writes NaN lambda and scores for the units concerned and sets the
+ * workspace's status word.  This query synchronises `stream` (which must be
+ * the stream of those calls, or ordered after them), reads the word, clears
+ * it and returns ECOKV_ETIMEOUT if it was set, else ECOKV_OK. */
+int ecokv_workspace_status(void *workspace, void *stream);
 
 /* Score every unit (Sec. 3 and Sec. 5, Eqs. (1)-(7)).
  *   K      [L][H_kv][Ttot][D]  keys, element type `dtype`
@@ -166,15 +180,11 @@ int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, s
  * blocks (two per (layer, KV head, sequence)) that exchange sums once and wait
  * for each other, when the device can hold all of them at once; if one ever
  * waits for its partner for seconds (the device taken by other work all that
- * time), that unit's lambda and scores come out NaN.
- * Paths: two sweeps over K (default), or, with the environment variable
- * ECOKV_SCORE_PATH=single (bf16, head_dim 128, (H_q/H_kv)*w <= 28, r_E and the
- * centroid over all T keys), one
- * persistent kernel that reads K once and exchanges per-unit sums between its
- * blocks.  That kernel needs all of its blocks resident at once (two per
- * compute unit): it must not share the device with another running launch of
- * it.  If a wait between its blocks ever times out, lambda and the scores of
- * the launch come out NaN.
+ * time), that unit's lambda and scores come out NaN and the workspace's status
+ * word records it: check with ecokv_workspace_status.  (The environment
+ * variable ECOKV_SPIN_LIMIT, read at each call, sets how many times such a
+ * wait polls before it gives up; values <= 0 give up at once.  It exists for
+ * tests.)
  * params->imp_mode must be ECOKV_IMP_ATTN here (the value norm needs V:
  * ecokv_score_v). */
 int ecokv_score(const void *K, const void *Q_win, int dtype, const ecokv_shape *shape,

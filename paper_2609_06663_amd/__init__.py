@@ -9,4 +9,5 @@ from .ecokv import (  # noqa: F401
     RED_EUCLID, RED_STD, CENTROID_ALL, CENTROID_PREFIX, NSTATS, STAT, EcoKVError, Params, Shape,
     ecokv_compact, ecokv_decode, ecokv_decode_workspace_size, ecokv_default_params, ecokv_index_count, ecokv_index_count_mode, ecokv_last_error,
     ecokv_pyramid_budgets, ecokv_score, ecokv_score_pre, ecokv_score_v, ecokv_select, ecokv_stage_times, ecokv_workspace_size,
+    ecokv_workspace_status, ETIMEOUT,
 )

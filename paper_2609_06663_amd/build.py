@@ -16,8 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libecokv.so")
-SOURCES = ["ecokv_api.hip", "ecokv_score.hip", "ecokv_fused.hip", "ecokv_select.hip", "ecokv_compact.hip",
-           "ecokv_decode.hip"]
+SOURCES = ["ecokv_api.hip", "ecokv_score.hip", "ecokv_select.hip", "ecokv_compact.hip", "ecokv_decode.hip"]
 ARCH = "gfx950"
 
 # Packed-fp32 instructions are disabled for every HIP translation unit.

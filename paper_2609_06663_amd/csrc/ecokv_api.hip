@@ -359,11 +359,32 @@ int ecokv_score_pre(const void *K, const void *V, const void *Q_win, int dtype, 
     a.winsor_q = params->winsor_q;
     a.pre = pre;
     if (pre && ((uintptr_t)pre & 3u) != 0) return fail(ECOKV_EINVAL, "pre must be 4-byte aligned");
+    // bounded waits between blocks poll up to this many times; ECOKV_SPIN_LIMIT
+    // lowers it so that tests can make a wait give up (every kernel still ends)
+    a.spin_limit = 1 << 20;
+    if (const char *sl = getenv("ECOKV_SPIN_LIMIT")) a.spin_limit = atoi(sl);
     if ((rc = fill_seqtab(shape, nullptr, si.w, &a.seq, nullptr))) return rc;
     const hipError_t e = ecokv::score_launch(a, static_cast<char *>(workspace), lay, si.maxT,
                                              static_cast<hipStream_t>(stream), dtype == ECOKV_BF16);
     if (e != hipSuccess) return hip_fail(e, "ecokv_score launch");
     return ECOKV_OK;
+}
+
+int ecokv_workspace_status(void *workspace, void *stream)
+{
+    if (!workspace) return fail(ECOKV_EINVAL, "workspace is NULL");
+    if (((uintptr_t)workspace & 255u) != 0) return fail(ECOKV_EINVAL, "workspace must be 256-byte aligned");
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    unsigned word = 0u;
+    hipError_t e = hipMemcpyAsync(&word, workspace, sizeof word, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "ecokv_workspace_status");
+    if (word == 0u) return ECOKV_OK;
+    if ((e = ecokv::status_clear(static_cast<unsigned *>(workspace), st)) != hipSuccess)
+        return hip_fail(e, "ecokv_workspace_status");
+    return fail(ECOKV_ETIMEOUT,
+                "a wait between the blocks of an ecokv_score call on this workspace gave up: that call's lambda "
+                "and scores of the affected units are NaN");
 }
 
 int ecokv_index_count(const ecokv_shape *shape, const int32_t *budget, int64_t *count)

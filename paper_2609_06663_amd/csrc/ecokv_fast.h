@@ -104,5 +104,63 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t key_rows_rsrc(const uint16_t *
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(krow0), (short)0, rows * (kD * 2), 0x00020000);
 }
 
+// Lane layout of a 32-key B operand of v_mfma_f32_32x32x16_bf16 (and of the
+// window-row A operands): lane l holds, for k-step s = 0..7, the 16-byte chunk
+// 2s + l/32 of its row, i.e. dimensions 8(2s + h) .. +7 with h = l/32.
+
+// MFMA operand row `which` (0: bf16 high part, 1: bf16 remainder) of the
+// fp32 vector v [kD] in that layout.
+__device__ __forceinline__ void mu_operand(const float *v, int which, int h, bf16x8 (&op)[8])
+{
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+        const float4 *src = reinterpret_cast<const float4 *>(v + 8 * (2 * s + h));
+        const float4 x = src[0], y = src[1];
+        const float f8[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+        u32x4 q;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            unsigned half2[2];
+#pragma unroll
+            for (int z = 0; z < 2; ++z) {
+                const float f = f8[2 * e + z];
+                const unsigned hb = bf16_rne(f);
+                half2[z] = which ? bf16_rne(f - __uint_as_float(hb << 16)) : hb;
+            }
+            q[e] = half2[0] | (half2[1] << 16);
+        }
+        op[s] = __builtin_bit_cast(bf16x8, q);
+    }
+}
+
+// The centroid's components at the 64 dimensions a lane holds in that layout.
+__device__ __forceinline__ void centroid_lane(const float *kbar, int h, float (&kb)[8][8])
+{
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+        const float4 *src = reinterpret_cast<const float4 *>(kbar + 8 * (2 * s + h));
+        const float4 x = src[0], y = src[1];
+        kb[s][0] = x.x; kb[s][1] = x.y; kb[s][2] = x.z; kb[s][3] = x.w;
+        kb[s][4] = y.x; kb[s][5] = y.y; kb[s][6] = y.z; kb[s][7] = y.w;
+    }
+}
+
+// Sum over the lane's 64 dimensions of (k_d - kbar_d)^2, the differences
+// formed in fp32 (exact for bf16 keys near the centroid); two partial sums.
+__device__ __forceinline__ float dist2_lane(const u32x4 (&b)[8], const float (&kb)[8][8])
+{
+    float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float d0 = __uint_as_float(b[s][e] << 16) - kb[s][2 * e];
+            const float d1 = __uint_as_float(b[s][e] & 0xffff0000u) - kb[s][2 * e + 1];
+            s0 = fmaf(d0, d0, s0);
+            s1 = fmaf(d1, d1, s1);
+        }
+    return s0 + s1;
+}
+
 }  // namespace fast
 }  // namespace ecokv

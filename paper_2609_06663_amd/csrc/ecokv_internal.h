@@ -17,7 +17,6 @@ struct SeqTab {
     int cu[ECOKV_MAX_SEQS + 1];    // token offsets (prefix of T_s)
     int beff[ECOKV_MAX_SEQS];      // min(b_s, T_s)
     int boff[ECOKV_MAX_SEQS + 1];  // prefix of beff
-    int spre[ECOKV_MAX_SEQS + 1];  // prefix of the work items per sequence (single-read score path)
 };
 
 // Decode unit u = (l*Hkv + h)*B + s.
@@ -50,16 +49,13 @@ struct ScoreArgs {
     float *bufB;     // [L][Hkv][Ptot]      khat.mu
     float *bufC;     // [L][Hkv][Ptot]      window-mean attention a
     float *bufV;     // [L][Hkv][Ptot]      pool(a) * |v| (vnorm only)
-    // single-read score path only: values published between blocks, each a
-    // 64-bit word (launch tag << 32 | float bits) so that a reader can tell a
-    // value of this launch from anything older without ordering fences
-    unsigned long long *partT;  // [U][2D + 2R][nch1]  per-item column sums and softmax partials
-    unsigned long long *ancT;   // [U][2D + 2R]        per-unit kbar, mu, row max, row normaliser
-    unsigned long long *epiT;   // [U][2][4]           the one-launch epilogue's half-unit S_div / S_imp sums
-    unsigned *status;           // set to the launch tag if a wait ran out of time
+    // values the two blocks of a unit's split epilogue exchange, each a 64-bit
+    // word (launch tag << 32 | float bits) so that a reader can tell a value of
+    // this launch from anything older without ordering fences
+    unsigned long long *epiT;   // [U][2][4]           half-unit S_div / S_imp sums and extrema
+    unsigned *status;           // workspace status word: set to the launch tag if a wait ran out of time
     unsigned tag;               // launch tag (never 0)
-    int items;                  // work items of the launch
-    int slices_per_lh;          // work items of one (layer, head) over all sequences
+    int spin_limit;             // polls of a bounded wait before it gives up (<= 0: give up at once)
     int L, Hq, Hkv, G, D, w, R, B;
     int64_t Ttot, Ptot;
     int nch1;        // sweep blocks per unit (for the longest sequence)
@@ -133,7 +129,7 @@ struct CompactArgs {
 
 // Workspace layout, shared by the size query and the launcher.
 struct WsLayout {
-    size_t part1, anchors, part2, part3, bufA, bufB, bufC, bufV, dq, partT, ancT, epiT, status, total;
+    size_t status, part1, anchors, part2, part3, bufA, bufB, bufC, bufV, dq, epiT, total;
 };
 
 // Order statistics of d_E per unit for the winsorised and MAD normalisations:
@@ -171,16 +167,12 @@ hipError_t decode_launch(DecodeArgs a, bool bf16, hipStream_t st);
 WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int maxT, bool bf16, bool vnorm);
 hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hipStream_t st, bool bf16);
 
-// Single-read score path (bf16, head_dim 128, G*w <= 28): eligibility for a
-// shape on the current device, and its launch.  The launcher fills the
-// fused-path fields of ScoreArgs.
-bool fused_eligible(int D, bool bf16, int R, const SeqTab &seq, int L, int Hkv, int Hq, int w, int *grid);
-hipError_t fused_launch(ScoreArgs &a, int grid, hipStream_t st);
 // A launch tag (never 0), distinct for every launch of the process: values a
 // launch publishes between its blocks carry it.
 unsigned launch_tag();
-constexpr int kFusedItem = 224;        // keys per work item (slice) of the single-read path
-constexpr int kFusedMaxRows = 28;      // window rows; 4 more rows carry kbar and mu
+// Clears the workspace status word (stream-ordered, by a one-thread kernel).
+hipError_t status_clear(unsigned *status, hipStream_t st);
+constexpr int kStreamMaxRows = 30;     // window rows of the streaming sweep 2; 2 more rows carry mu
 hipError_t select_launch(const SelectArgs &a, hipStream_t st);
 int select_max_flat_heads();
 hipError_t compact_launch(const CompactArgs &a, hipStream_t st);

@@ -27,6 +27,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
+
 #include "ecokv_fast.h"
 
 namespace ecokv {
@@ -528,19 +530,21 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
     }
 }
 
-// Sweep 2.  The A operand carries the window rows and, in its last four rows,
-// mu and kbar each split into a bf16 high part and a bf16 remainder, so that
-// one MFMA chain gives q.k for the window rows together with k.mu and k.kbar
-// to about 2^-17 relative.  |k|^2 comes from v_dot2 on the same B registers;
-// d_E = sqrt(|k|^2 - 2 k.kbar + |kbar|^2), khat.mu = k.mu / |k|.
+// Sweep 2.  The A operand carries the window rows and, in its last two rows,
+// mu split into a bf16 high part and a bf16 remainder, so that one MFMA chain
+// gives q.k for the window rows together with k.mu to about 2^-17 relative.
+// |k|^2 comes from v_dot2 on the same B registers; khat.mu = k.mu / |k|.
+// d_E = |k - kbar| is summed directly from the differences in fp32 (each lane
+// over the 64 dimensions it holds): the expansion |k|^2 - 2 k.kbar + |kbar|^2
+// would lose the distance to cancellation when the keys share a large common
+// offset (mean cosine near 1, Sec. 4).
 template <int MT>
 __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
 {
-    constexpr int kAnc = 32 * MT - 4;  // first anchor row of the A operand
+    constexpr int kAnc = 32 * MT - 2;  // first anchor row of the A operand
     __shared__ u32x4 kt[kTile * kChunks];
     __shared__ float rowM[32 * MT], rowIS[32 * MT];
     __shared__ float wred[4][4];
-    __shared__ float kb2_lds;
 
     const int u = blockIdx.y;
     const Unit un = unit_of(u, a.Hkv, a.B);
@@ -560,51 +564,12 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
     bf16x8 aq[MT][8];
     load_query_operands<MT>(a, un, lane, aq);
     {
-        // anchor rows: kAnc + 0: mu high, +1: mu remainder, +2: kbar high, +3: kbar remainder
+        // anchor rows: kAnc + 0: mu high, +1: mu remainder
         const int rr = 32 * (MT - 1) + (lane & 31);
-        if (rr >= kAnc) {
-            const int which = rr - kAnc;
-            const float4 *src = reinterpret_cast<const float4 *>((which < 2) ? anc + kD : anc);
-            float4 fv[16];
-#pragma unroll
-            for (int s = 0; s < 8; ++s) {
-                fv[2 * s] = src[2 * (2 * s + h)];
-                fv[2 * s + 1] = src[2 * (2 * s + h) + 1];
-            }
-#pragma unroll
-            for (int s = 0; s < 8; ++s) {
-                const float f8[8] = {fv[2 * s].x, fv[2 * s].y, fv[2 * s].z, fv[2 * s].w,
-                                     fv[2 * s + 1].x, fv[2 * s + 1].y, fv[2 * s + 1].z, fv[2 * s + 1].w};
-                u32x4 q;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    unsigned half2[2];
-#pragma unroll
-                    for (int z = 0; z < 2; ++z) {
-                        const float f = f8[2 * e + z];
-                        const unsigned hi = bf16_rne(f);
-                        half2[z] = (which & 1) ? bf16_rne(f - __uint_as_float(hi << 16)) : hi;
-                    }
-                    q[e] = half2[0] | (half2[1] << 16);
-                }
-                aq[MT - 1][s] = __builtin_bit_cast(bf16x8, q);
-            }
-        }
+        if (rr >= kAnc) mu_operand(anc + kD, rr - kAnc, h, aq[MT - 1]);
     }
-    if (tid < 64) {
-        // |kbar'|^2 of the centroid as represented (high + remainder)
-        float acc2 = 0.f;
-#pragma unroll
-        for (int z = 0; z < 2; ++z) {
-            const float f = anc[2 * tid + z];
-            const float hi = __uint_as_float(bf16_rne(f) << 16);
-            const float lo = __uint_as_float(bf16_rne(f - hi) << 16);
-            const float kb = hi + lo;
-            acc2 = fmaf(kb, kb, acc2);
-        }
-        acc2 = wave_sum(acc2);
-        if (tid == 0) kb2_lds = acc2;
-    }
+    float kbv[8][8];  // kbar at the 64 dimensions this lane holds
+    centroid_lane(anc, h, kbv);
     if (tid < 32 * MT) {
         const bool ok = tid < a.R;
         rowM[tid] = ok ? anc[2 * kD + tid] : 0.f;
@@ -641,13 +606,20 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
                 const int m = 32 * t + 8 * (i >> 2) + 4 * h + (i & 3);
                 if (m < a.R) att = fmaf(fast_exp2(fmaf(acc[t][i], sc, -rowM[m])), rowIS[m], att);
             }
-        float kmu = h ? acc[MT - 1][12] + acc[MT - 1][13] : 0.f;
-        float kk = h ? acc[MT - 1][14] + acc[MT - 1][15] : 0.f;
+        float kmu = h ? acc[MT - 1][14] + acc[MT - 1][15] : 0.f;
+        float d2;
+        {
+            const int r = 32 * wv + (lane & 31);
+            u32x4 bq[8];
+#pragma unroll
+            for (int s = 0; s < 8; ++s) bq[s] = kt[sw(r, 2 * s + h)];
+            d2 = dist2_lane(bq, kbv);
+        }
         n2 += __shfl_xor(n2, 32, kWave);
         att += __shfl_xor(att, 32, kWave);
         kmu += __shfl_xor(kmu, 32, kWave);
-        kk += __shfl_xor(kk, 32, kWave);
-        const float dE = __builtin_amdgcn_sqrtf(fmaxf(n2 - 2.f * kk + kb2_lds, 0.f));
+        d2 += __shfl_xor(d2, 32, kWave);
+        const float dE = __builtin_amdgcn_sqrtf(d2);
         const float cm = kmu * __builtin_amdgcn_rsqf(fmaxf(n2, 1e-24f));
         const int gi = tr0 + 32 * wv + (lane & 31);
         if (h == 0) {
@@ -692,8 +664,8 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
     }
 }
 
-// Sweep 2, streaming form (window rows + 4 anchor rows in one 32-row operand,
-// i.e. G*w <= 28): no LDS tile and no barrier in the key loop.  Each wave
+// Sweep 2, streaming form (window rows + 2 rows of mu in one 32-row operand,
+// i.e. G*w <= 30): no LDS tile and no barrier in the key loop.  Each wave
 // streams its own 512 keys in groups of 32 from HBM into registers (three
 // groups in flight), re-lays them out through a wave-private LDS stage into
 // MFMA B operands (lane l: key l % 32, 16-byte chunks 2s + l / 32).  The
@@ -722,6 +694,7 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
     constexpr int kS2Groups = KEYS / (32 * kS2Waves);  // 32-key groups per wave
     __shared__ float wred[4][kS2Waves];
     __shared__ u32x4 stage[kS2Waves][32 * kChunks];  // per wave: 32 rows, swizzled 16-byte chunks
+    __shared__ float wd2[kS2Waves][32];               // per wave: |k - kbar|^2 of its 32 rows
     // the block's per-key outputs (d_E, khat.mu, a), written out once at the end:
     // a few long stores instead of three 128-byte stores per 32 keys, which
     // interleave with the read stream at a high price
@@ -739,49 +712,20 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
     const int stride = 2 * kD + 2 * a.R;
     const float *anc = a.anchors + (int64_t)u * stride;
     const float sc = a.inv_sqrt_d * kLog2e;
-    constexpr int kAnc = 28;
+    constexpr int kAnc = 32 - 2;
 
-    // A operand: window rows (zero beyond R), rows 28..31 mu high/remainder, kbar high/remainder
+    // A operand: window rows (zero beyond R), rows 30, 31 mu high / remainder
     bf16x8 aq[1][8];
     load_query_operands<1>(a, un, lane, aq);
-    if (kl >= kAnc) {
-        const int which = kl - kAnc;
-        const float4 *src = reinterpret_cast<const float4 *>((which < 2) ? anc + kD : anc);
-        float4 fv[16];
-#pragma unroll
-        for (int st = 0; st < 8; ++st) {
-            fv[2 * st] = src[2 * (2 * st + h)];
-            fv[2 * st + 1] = src[2 * (2 * st + h) + 1];
-        }
-#pragma unroll
-        for (int st = 0; st < 8; ++st) {
-            const float f8[8] = {fv[2 * st].x,     fv[2 * st].y,     fv[2 * st].z,     fv[2 * st].w,
-                                 fv[2 * st + 1].x, fv[2 * st + 1].y, fv[2 * st + 1].z, fv[2 * st + 1].w};
-            u32x4 q;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                unsigned half2[2];
-#pragma unroll
-                for (int z = 0; z < 2; ++z) {
-                    const float f = f8[2 * e + z];
-                    const unsigned hb = bf16_rne(f);
-                    half2[z] = (which & 1) ? bf16_rne(f - __uint_as_float(hb << 16)) : hb;
-                }
-                q[e] = half2[0] | (half2[1] << 16);
-            }
-            aq[0][st] = __builtin_bit_cast(bf16x8, q);
-        }
+    if (kl >= kAnc) mu_operand(anc + kD, kl - kAnc, h, aq[0]);
+    // kbar at the 8 dimensions of chunk lane % 16, the chunk this lane loads
+    float kbc[8];
+    {
+        const float4 *src = reinterpret_cast<const float4 *>(anc + 8 * (lane & 15));
+        const float4 x = src[0], y = src[1];
+        kbc[0] = x.x; kbc[1] = x.y; kbc[2] = x.z; kbc[3] = x.w;
+        kbc[4] = y.x; kbc[5] = y.y; kbc[6] = y.z; kbc[7] = y.w;
     }
-    // |kbar'|^2 (each wave on its own)
-    float kb2 = 0.f;
-#pragma unroll
-    for (int z = 0; z < 2; ++z) {
-        const float f = anc[2 * lane + z];
-        const float fh = __uint_as_float(bf16_rne(f) << 16);
-        const float fl = __uint_as_float(bf16_rne(f - fh) << 16);
-        kb2 = fmaf(fh + fl, fh + fl, kb2);
-    }
-    kb2 = wave_sum(kb2);
     // per-lane row shifts M'_m for the rows m = 8(r/4) + 4h + r%4 of accumulator r
     float rsh[16];
     {
@@ -807,7 +751,30 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
     const float inv_r = 1.f / (float)a.R;
 
     u32x4 *wst = stage[wv];
+    float *wd = wd2[wv];
     auto group = [&](const u32x4 (&ld)[8], int key0, bool valid) {
+        // |k - kbar|^2 in the load layout (lane l: chunk l % 16 of rows 4i + l / 16):
+        // the differences in fp32, summed over the lane's 8 dimensions, then
+        // over the 16 lanes of a row by DPP; one lane per row parks the sum
+        {
+            float dp[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float d0 = __uint_as_float(ld[i][e] << 16) - kbc[2 * e];
+                    const float d1 = __uint_as_float(ld[i][e] & 0xffff0000u) - kbc[2 * e + 1];
+                    s0 = fmaf(d0, d0, s0);
+                    s1 = fmaf(d1, d1, s1);
+                }
+                dp[i] = row_sum<16>(s0 + s1);
+            }
+            if ((lane & 15) == 0) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) wd[4 * i + (lane >> 4)] = dp[i];
+            }
+        }
         // through this wave's LDS stage into the B-operand layout (lane l: key
         // l % 32, chunks 2s + l / 32); a wave's own LDS accesses are ordered
 #pragma unroll
@@ -825,13 +792,11 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
         float att = 0.f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) att += fast_exp2(fmaf(acc[r], sc, -rsh[r]));
-        float kmu = h ? acc[12] + acc[13] : 0.f;
-        float kk = h ? acc[14] + acc[15] : 0.f;
+        float kmu = h ? acc[14] + acc[15] : 0.f;
         n2 += __shfl_xor(n2, 32, kWave);
         att += __shfl_xor(att, 32, kWave);
         kmu += __shfl_xor(kmu, 32, kWave);
-        kk += __shfl_xor(kk, 32, kWave);
-        const float dE = __builtin_amdgcn_sqrtf(fmaxf(n2 - 2.f * kk + kb2, 0.f));
+        const float dE = __builtin_amdgcn_sqrtf(wd[kl]);
         const float cm = kmu * __builtin_amdgcn_rsqf(fmaxf(n2, 1e-24f));
         const int gi = key0 + kl;
         if (valid && h == 0) {
@@ -1370,7 +1335,7 @@ __device__ __forceinline__ EpiConsts epi_consts(const ScoreArgs &a, const Red4 &
         k.rE = 2.f - 2.f / (1.f + expf(-k.DE / a.tau));
     k.rC = ((float)T * mu2 - 1.f) / ((float)T - 1.f);
     k.lam = a.use_override ? a.lambda_override : a.beta * k.rE + (1.f - a.beta) * k.rC;
-    if (a.status && *a.status == a.tag) k.lam = NAN;  // a publication wait of this launch timed out
+    if (sd.s0 != sd.s0) k.lam = NAN;  // the split epilogue's wait gave up (or NaN inputs)
     k.smin = sd.mn;
     k.sden = sd.mx - sd.mn + a.eps;
     k.impmean = sd.s1 / (float)P;
@@ -1522,8 +1487,10 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
 // (SPLIT = 1) or two (SPLIT = 2, each with half of the keys).  Every per-unit
 // reduction is block-local, except that with SPLIT = 2 the two halves of a
 // unit exchange their S_div / S_imp sums and extrema once (tagged 64-bit
-// relaxed atomics, as in the single-read path; the halves are combined in a
-// fixed order, so both compute the same constants).  Each key's d_E,
+// relaxed atomics; the halves are combined in a fixed order, so both compute
+// the same constants).  The wait for the other half is bounded: if it gives
+// up, the unit's lambda and scores come out NaN and the workspace status word
+// records the launch.  Each key's d_E,
 // khat.mu and attention is read once.  Wave w holds 8/SPLIT chunks of 256
 // consecutive keys; lane l of chunk j holds keys 256 j + 4 l .. +3 of the
 // wave's range, so each load instruction covers 1 KiB of consecutive keys.
@@ -1534,7 +1501,7 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
 constexpr int kUThreads = 1024;
 constexpr int kUW = kUThreads / kWave;
 constexpr int kUKeys = kUThreads * 32;  // 32768 keys per unit
-constexpr int kUSpinLimit = 1 << 20;  // a few seconds: the partner block only has to be scheduled
+constexpr int kUSpinLimit = 1 << 20;  // polls (a few seconds): the partner block only has to be scheduled
 
 // Block sum / min / max whose barriers order LDS only, so that global loads
 // issued before it stay in flight.
@@ -1716,10 +1683,10 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
             epi_tag_store(mine + 2, sd.mn, a.tag);
             epi_tag_store(mine + 3, sd.mx, a.tag);
             const unsigned long long *other = a.epiT + ((int64_t)u * 2 + (part ^ 1)) * 4;
-            unsigned long long o[4];
-            int tries = 0;
-            bool ok;
-            do {
+            unsigned long long o[4] = {0ull, 0ull, 0ull, 0ull};
+            bool ok = false;
+            // a spin limit <= 0 (set by the host to exercise this path) gives up at once
+            for (int tries = 0; tries < a.spin_limit && !ok; ++tries) {
                 ok = true;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
@@ -1727,7 +1694,7 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
                     ok = ok && (unsigned)(o[q] >> 32) == a.tag;
                 }
                 if (!ok) __builtin_amdgcn_s_sleep(2);
-            } while (!ok && ++tries < kUSpinLimit);
+            }
             if (!ok) __hip_atomic_store(a.status, a.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             const Red4 so{__uint_as_float((unsigned)o[0]), __uint_as_float((unsigned)o[1]),
                           __uint_as_float((unsigned)o[2]), __uint_as_float((unsigned)o[3])};
@@ -1762,10 +1729,29 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
     if (part == 0 && threadIdx.x == 0) epi_write_stats(a, u, k, dst, sd, mu2);
 }
 
+// Clears the workspace status word (a one-thread kernel rather than a memset,
+// so that a captured graph holds no memset node).
+__global__ void k_status_clear(unsigned *status) { *status = 0u; }
+
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static std::atomic<unsigned> g_tag{0u};
+
+unsigned launch_tag()
+{
+    unsigned t = ++g_tag;
+    if (t == 0) t = ++g_tag;
+    return t;
+}
+
+hipError_t status_clear(unsigned *status, hipStream_t st)
+{
+    hipLaunchKernelGGL(k_status_clear, dim3(1), dim3(1), 0, st, status);
+    return hipGetLastError();
+}
 
 bool score_fast_path(int D, bool bf16) { return bf16 && D == fast::kD; }
 
@@ -1857,13 +1843,11 @@ WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int 
     // (the streaming sweeps' are larger)
     const int rpb = min(rows_per_block(D, bf16), fast::kSmallRows);
     const int64_t nch1 = (maxT + rpb - 1) / rpb;
-    // the single-read path publishes per slice; size for it whenever it may run
-    const bool single = bf16 && D == fast::kD && R <= kFusedMaxRows;
-    const int64_t nchf = single ? (maxT + kFusedItem - 1) / kFusedItem : 0;
-    const int64_t nch2 = nch1 > nchf ? nch1 : nchf;
+    const int64_t nch2 = nch1;
     const int64_t nch3 = (maxT + kEpiKeys - 1) / kEpiKeys;
     const int64_t stride = 2 * D + 2 * R;
     size_t o = 0;
+    w.status = o; o = align256(o + sizeof(unsigned));  // first: a fixed offset for the status query
     w.part1 = o; o = align256(o + sizeof(float) * U * nch1 * stride);
     w.anchors = o; o = align256(o + sizeof(float) * U * stride);
     w.part2 = o; o = align256(o + sizeof(float) * U * nch2 * 4);
@@ -1873,10 +1857,7 @@ WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int 
     w.bufC = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
     w.bufV = o; o = align256(o + (vnorm ? sizeof(float) * (int64_t)L * Hkv * Ptot : 0));
     w.dq = o; o = align256(o + sizeof(float) * U * 2);
-    w.partT = o; o = align256(o + sizeof(unsigned long long) * U * stride * nchf);
-    w.ancT = o; o = align256(o + (single ? sizeof(unsigned long long) * U * stride : 0));
     w.epiT = o; o = align256(o + sizeof(unsigned long long) * U * 2 * 4);
-    w.status = o; o = align256(o + sizeof(unsigned));
     w.total = o;
     return w;
 }
@@ -1893,8 +1874,8 @@ static void launch_fast_sweep(int pass, const ScoreArgs &a, dim3 grid, hipStream
 static void launch_sweep(int pass, const ScoreArgs &a, dim3 grid, hipStream_t st, bool bf16)
 {
     if (score_fast_path(a.D, bf16)) {
-        // MT1 = ceil(R / 32) tiles of window rows; MT2 also holds 4 anchor rows.
-        const int mt1 = (a.R + 31) / 32, mt2 = (a.R + 4 + 31) / 32;
+        // MT1 = ceil(R / 32) tiles of window rows; MT2 also holds the 2 rows of mu.
+        const int mt1 = (a.R + 31) / 32, mt2 = (a.R + 2 + 31) / 32;
         if (pass == 1) {
             if (mt1 == 1) launch_fast_sweep<1, 1>(1, a, grid, st);
             else launch_fast_sweep<2, 1>(1, a, grid, st);
@@ -1942,37 +1923,15 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     a.bufB = reinterpret_cast<float *>(ws + lay.bufB);
     a.bufC = reinterpret_cast<float *>(ws + lay.bufC);
     a.nch3 = (maxT + kEpiKeys - 1) / kEpiKeys;
+    a.status = reinterpret_cast<unsigned *>(ws + lay.status);
     const dim3 grid_e(a.nch3, U);
     hipError_t e;
 
-    // work items of the single-read path: 256-key slices of every sequence
-    a.seq.spre[0] = 0;
-    for (int s = 0; s < a.seq.nseq; ++s)
-        a.seq.spre[s + 1] = a.seq.spre[s] + (a.seq.cu[s + 1] - a.seq.cu[s] + kFusedItem - 1) / kFusedItem;
-    // The single-read path is selected with ECOKV_SCORE_PATH=single (read on
-    // every call); the two-sweep path is the default.
-    const char *path = getenv("ECOKV_SCORE_PATH");
-    const bool want_single = path && strcmp(path, "single") == 0 && !a.pre;
     // streaming sweeps: 2048-key blocks, or 512-key ones when those would be
     // fewer than four per compute unit (1024 blocks)
     const int sblock = (int64_t)U * ((maxT + fast::kS2Keys - 1) / fast::kS2Keys) >= 1024 ? fast::kS2Keys
                                                                                        : fast::kS2KeysSmall;
-    int fgrid = 0;
-    // (its partials carry no sum of d_E^2 and its centroid spans all T keys)
-    if (want_single && !a.red_std && !a.centroid_prefix &&
-        fused_eligible(a.D, bf16, a.R, a.seq, a.L, a.Hkv, a.Hq, a.w, &fgrid)) {
-        a.partT = reinterpret_cast<unsigned long long *>(ws + lay.partT);
-        a.ancT = reinterpret_cast<unsigned long long *>(ws + lay.ancT);
-        a.status = reinterpret_cast<unsigned *>(ws + lay.status);
-        a.rpb1 = kFusedItem;
-        a.nch1 = (maxT + kFusedItem - 1) / kFusedItem;
-        a.rpb2 = a.rpb1;
-        a.nch2 = a.nch1;
-        a.slices_per_lh = a.seq.spre[a.seq.nseq];
-        a.items = a.L * a.Hkv * a.slices_per_lh;
-        ECOKV_TIMED("single_read", st, e = fused_launch(a, fgrid, st));
-        if (e != hipSuccess) return e;
-    } else {
+    {
         a.rpb1 = block_sweep_rows(a.D, bf16, U, maxT);
         a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
         const dim3 grid(a.nch1, U);
@@ -2002,7 +1961,7 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
                                                0, st, a));
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        if (score_fast_path(a.D, bf16) && a.R <= kFusedMaxRows) {
+        if (score_fast_path(a.D, bf16) && a.R <= kStreamMaxRows) {
             // streaming sweep 2: window rows and the four anchor rows in one operand
             a.rpb2 = sblock;
             a.nch2 = (maxT + a.rpb2 - 1) / a.rpb2;
@@ -2052,8 +2011,7 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         // exchange waits for each other; four per unit measured no faster), else one
         if (2 * (int64_t)U <= epi_split_capacity()) {
             a.epiT = reinterpret_cast<unsigned long long *>(ws + lay.epiT);
-            a.status = reinterpret_cast<unsigned *>(ws + lay.status);
-            if (a.tag == 0) a.tag = launch_tag();  // (the single-read path's tag, if it ran)
+            a.tag = launch_tag();
             ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL(k_epi_unit<2>, dim3(2 * U), dim3(kUThreads), 0, st, a));
         } else {
             ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL(k_epi_unit<1>, dim3(U), dim3(kUThreads), 0, st, a));

@@ -17,7 +17,7 @@ import torch
 
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libecokv.so")
 
-OK, EINVAL, EWORKSPACE, EUNSUPPORTED, EHIP = 0, -1, -2, -3, -4
+OK, EINVAL, EWORKSPACE, EUNSUPPORTED, EHIP, ETIMEOUT = 0, -1, -2, -3, -4, -5
 BF16, F32 = 0, 1
 PER_HEAD, LAYER_FLAT, HEAD_BUDGETS = 0, 1, 2
 IMP_ATTN, IMP_ATTN_VNORM = 0, 1
@@ -29,7 +29,8 @@ NSTATS = 12
 STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7, imp_mean=8, sbar_mean=9,
             mu_norm2=10, scale=11)
 
-EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_score", "ecokv_score_v", "ecokv_score_pre",
+EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_workspace_status", "ecokv_score", "ecokv_score_v",
+           "ecokv_score_pre",
            "ecokv_index_count",
            "ecokv_index_count_mode", "ecokv_select", "ecokv_compact", "ecokv_pyramid_budgets",
            "ecokv_decode_workspace_size", "ecokv_decode",
@@ -81,6 +82,31 @@ class Shape:
     def cu_seqlens(self):
         return list(self.cu)
 
+    # element counts of the tensors of a call, for the binding's checks
+    @property
+    def units(self) -> int:
+        c = self.c
+        return c.num_layers * c.num_kv_heads * c.num_seqs
+
+    @property
+    def ttot(self) -> int:
+        return int(self.cu[self.c.num_seqs])
+
+    @property
+    def ptot(self) -> int:
+        return self.ttot - self.c.num_seqs * self.c.window
+
+    def kv_numel(self) -> int:
+        c = self.c
+        return c.num_layers * c.num_kv_heads * self.ttot * c.head_dim
+
+    def q_numel(self) -> int:
+        c = self.c
+        return c.num_layers * c.num_q_heads * c.num_seqs * c.window * c.head_dim
+
+    def score_numel(self) -> int:
+        return self.c.num_layers * self.c.num_kv_heads * self.ptot
+
 
 def _load():
     if not os.path.exists(_LIB_PATH):
@@ -90,6 +116,7 @@ def _load():
     i32p = ctypes.POINTER(ctypes.c_int32)
     lib.ecokv_default_params.argtypes = [pp]
     lib.ecokv_workspace_size.argtypes = [sp, pp, ctypes.POINTER(ctypes.c_size_t)]
+    lib.ecokv_workspace_status.argtypes = [vp, vp]
     lib.ecokv_score.argtypes = [vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_score_v.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_score_pre.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
@@ -123,6 +150,49 @@ def _ptr(t: Optional[torch.Tensor]):
     if not t.is_contiguous():
         raise ValueError("tensors passed to libecokv must be contiguous")
     return ctypes.c_void_p(t.data_ptr())
+
+
+_ELEM = {torch.bfloat16: "bf16", torch.float32: "float32", torch.int32: "int32", torch.uint8: "uint8"}
+
+
+def _arg(t: Optional[torch.Tensor], name: str, dtypes, numel: int, device, optional: bool = False):
+    """Device pointer of `t` after checking that it is a contiguous tensor on
+    `device` with an allowed element type and at least `numel` elements: the
+    kernels trust these sizes, so a mismatch is refused here rather than read
+    or written out of bounds on the GPU."""
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (got {t.device})")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the call's tensors on {device}")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} must be {' or '.join(_ELEM.get(d, str(d)) for d in dtypes)} (got {t.dtype})")
+    if t.numel() < numel:
+        raise ValueError(f"{name} has {t.numel()} elements, the call needs {numel}")
+    return _ptr(t)
+
+
+_KV_TYPES = (torch.bfloat16, torch.float32)
+_F32 = (torch.float32,)
+_I32 = (torch.int32,)
+_U8 = (torch.uint8,)
+
+
+def _workspace(workspace: Optional[torch.Tensor], nbytes: int, device, stream):
+    """The caller's workspace, or a zero-filled one allocated here; a tensor
+    allocated here is recorded on `stream`, so that torch's allocator does not
+    hand its memory out again before the work queued there has used it."""
+    if workspace is not None:
+        return workspace
+    ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=device)
+    if stream is not None:
+        ws.record_stream(stream)
+    return ws
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -174,20 +244,41 @@ def ecokv_workspace_size(shape: Shape, params: Optional[Params] = None) -> int:
     return n.value
 
 
+def _score_args(K, V, Q_win, shape: Shape, p: Params, scores, lambda_, stats, workspace, stream, pre=None):
+    """Checked pointers of a score call, in the order of ecokv_score_pre."""
+    L = shape.c.num_layers
+    if L == 0:  # nothing is read or written
+        return [_ptr(K), _ptr(V), _ptr(Q_win), _dtype_code(K) if K is not None else BF16, ctypes.byref(shape.c),
+                ctypes.byref(p), _ptr(pre), _ptr(scores), _ptr(lambda_), _ptr(stats), _ptr(workspace),
+                0 if workspace is None else workspace.numel(), _stream(stream)]
+    dev = K.device if isinstance(K, torch.Tensor) else None
+    kp = _arg(K, "K", _KV_TYPES, shape.kv_numel(), dev)
+    if Q_win.dtype != K.dtype or (V is not None and V.dtype != K.dtype):
+        raise TypeError("K, V and Q_win must have the same element type")
+    vp = _arg(V, "V", _KV_TYPES, shape.kv_numel(), dev, optional=p.imp_mode != IMP_ATTN_VNORM)
+    qp = _arg(Q_win, "Q_win", _KV_TYPES, shape.q_numel(), dev)
+    R = shape.c.num_q_heads // shape.c.num_kv_heads * shape.c.window
+    pp = _arg(pre, "pre", _F32, shape.units * (2 * shape.c.head_dim + 2 * R), dev, optional=True)
+    sp_ = _arg(scores, "scores", _F32, shape.score_numel(), dev)
+    lp = _arg(lambda_, "lambda", _F32, shape.units, dev, optional=True)
+    stp = _arg(stats, "stats", _F32, shape.units * NSTATS, dev, optional=True)
+    need = ecokv_workspace_size(shape, p)
+    workspace = _workspace(workspace, need, dev, stream)
+    wp = _arg(workspace, "workspace", _U8, need, dev)
+    return [kp, vp, qp, _dtype_code(K), ctypes.byref(shape.c), ctypes.byref(p), pp, sp_, lp, stp, wp,
+            workspace.numel(), _stream(stream)]
+
+
 def ecokv_score(K: torch.Tensor, Q_win: torch.Tensor, shape: Shape, params: Optional[Params],
                 scores: torch.Tensor, lambda_: Optional[torch.Tensor] = None,
                 stats: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
                 stream=None) -> None:
-    """Enqueue ecokv_score.  `workspace` (uint8, >= ecokv_workspace_size bytes) is
-    allocated here with torch when not given."""
+    """Enqueue ecokv_score.  `workspace` (uint8, >= ecokv_workspace_size bytes,
+    zero-filled before its first use) is allocated here when not given."""
     p = params or Params()
-    if workspace is None:
-        workspace = torch.empty(ecokv_workspace_size(shape, p), dtype=torch.uint8, device=K.device)
-    if Q_win.dtype != K.dtype:
-        raise TypeError("K and Q_win must have the same element type")
-    _check(lib.ecokv_score(_ptr(K), _ptr(Q_win), _dtype_code(K), ctypes.byref(shape.c), ctypes.byref(p),
-                           _ptr(scores), _ptr(lambda_), _ptr(stats), _ptr(workspace),
-                           workspace.numel(), _stream(stream)))
+    a = _score_args(K, None, Q_win, shape, p, scores, lambda_, stats, workspace, stream)
+    del a[1], a[5]  # no V, no pre
+    _check(lib.ecokv_score(*a))
 
 
 def ecokv_score_v(K: torch.Tensor, V: Optional[torch.Tensor], Q_win: torch.Tensor, shape: Shape,
@@ -196,13 +287,9 @@ def ecokv_score_v(K: torch.Tensor, V: Optional[torch.Tensor], Q_win: torch.Tenso
                   stream=None) -> None:
     """Enqueue ecokv_score_v (V is read with imp_mode IMP_ATTN_VNORM)."""
     p = params or Params()
-    if workspace is None:
-        workspace = torch.empty(ecokv_workspace_size(shape, p), dtype=torch.uint8, device=K.device)
-    if Q_win.dtype != K.dtype or (V is not None and V.dtype != K.dtype):
-        raise TypeError("K, V and Q_win must have the same element type")
-    _check(lib.ecokv_score_v(_ptr(K), _ptr(V), _ptr(Q_win), _dtype_code(K), ctypes.byref(shape.c),
-                             ctypes.byref(p), _ptr(scores), _ptr(lambda_), _ptr(stats), _ptr(workspace),
-                             workspace.numel(), _stream(stream)))
+    a = _score_args(K, V, Q_win, shape, p, scores, lambda_, stats, workspace, stream)
+    del a[6]  # no pre
+    _check(lib.ecokv_score_v(*a))
 
 
 def ecokv_score_pre(K: torch.Tensor, V: Optional[torch.Tensor], Q_win: torch.Tensor, shape: Shape,
@@ -212,13 +299,17 @@ def ecokv_score_pre(K: torch.Tensor, V: Optional[torch.Tensor], Q_win: torch.Ten
     """Enqueue ecokv_score_pre: `pre` (float32 [L][Hkv][B][2D + 2R]) holds the
     key sums and window softmax statistics a prefill produced."""
     p = params or Params()
-    if workspace is None:
-        workspace = torch.empty(ecokv_workspace_size(shape, p), dtype=torch.uint8, device=K.device)
-    if pre.dtype != torch.float32:
+    if pre is not None and pre.dtype != torch.float32:
         raise TypeError("pre is float32")
-    _check(lib.ecokv_score_pre(_ptr(K), _ptr(V), _ptr(Q_win), _dtype_code(K), ctypes.byref(shape.c),
-                               ctypes.byref(p), _ptr(pre), _ptr(scores), _ptr(lambda_), _ptr(stats),
-                               _ptr(workspace), workspace.numel(), _stream(stream)))
+    a = _score_args(K, V, Q_win, shape, p, scores, lambda_, stats, workspace, stream, pre=pre)
+    _check(lib.ecokv_score_pre(*a))
+
+
+def ecokv_workspace_status(workspace: torch.Tensor, stream=None) -> None:
+    """Synchronise `stream` and raise EcoKVError (code ETIMEOUT) if a score call
+    on `workspace` since the last query had a wait between blocks give up (its
+    lambda and scores of the affected units are then NaN); clears the record."""
+    _check(lib.ecokv_workspace_status(_arg(workspace, "workspace", _U8, 4, None), _stream(stream)))
 
 
 def ecokv_index_count(shape: Shape, budget: Sequence[int]) -> int:
@@ -243,8 +334,19 @@ def ecokv_pyramid_budgets(num_layers: int, total: float, beta: float, window: in
 def ecokv_select(scores: torch.Tensor, shape: Shape, mode: int, budget, idx: torch.Tensor,
                  counts: Optional[torch.Tensor] = None, offsets: Optional[torch.Tensor] = None,
                  stream=None) -> None:
-    _check(lib.ecokv_select(_ptr(scores), ctypes.byref(shape.c), int(mode), _budget(shape, budget, mode),
-                            _ptr(idx), _ptr(counts), _ptr(offsets), _stream(stream)))
+    bud = _budget(shape, budget, mode)
+    if shape.c.num_layers == 0:
+        _check(lib.ecokv_select(_ptr(scores), ctypes.byref(shape.c), int(mode), bud, _ptr(idx), _ptr(counts),
+                                _ptr(offsets), _stream(stream)))
+        return
+    n = ecokv_index_count_mode(shape, mode, budget)
+    dev = scores.device if isinstance(scores, torch.Tensor) else None
+    flat = int(mode) == LAYER_FLAT
+    _check(lib.ecokv_select(_arg(scores, "scores", _F32, shape.score_numel(), dev), ctypes.byref(shape.c),
+                            int(mode), bud, _arg(idx, "idx", _I32, n, dev),
+                            _arg(counts, "counts", _I32, shape.units, dev, optional=not flat),
+                            _arg(offsets, "offsets", _I32, shape.units, dev, optional=not flat),
+                            _stream(stream)))
 
 
 def ecokv_compact(K: torch.Tensor, V: torch.Tensor, shape: Shape, mode: int, budget,
@@ -252,9 +354,22 @@ def ecokv_compact(K: torch.Tensor, V: torch.Tensor, shape: Shape, mode: int, bud
                   Kc: torch.Tensor, Vc: torch.Tensor, stream=None) -> None:
     if V.dtype != K.dtype or Kc.dtype != K.dtype or Vc.dtype != K.dtype:
         raise TypeError("K, V, Kc and Vc must share one element type")
-    _check(lib.ecokv_compact(_ptr(K), _ptr(V), _dtype_code(K), ctypes.byref(shape.c), int(mode),
-                             _budget(shape, budget, mode), _ptr(idx), _ptr(counts), _ptr(offsets), _ptr(Kc),
-                             _ptr(Vc), _stream(stream)))
+    bud = _budget(shape, budget, mode)
+    if shape.c.num_layers == 0:
+        _check(lib.ecokv_compact(_ptr(K), _ptr(V), _dtype_code(K), ctypes.byref(shape.c), int(mode), bud,
+                                 _ptr(idx), _ptr(counts), _ptr(offsets), _ptr(Kc), _ptr(Vc), _stream(stream)))
+        return
+    n = ecokv_index_count_mode(shape, mode, budget)
+    dev = K.device
+    flat = int(mode) == LAYER_FLAT
+    D = shape.c.head_dim
+    _check(lib.ecokv_compact(_arg(K, "K", _KV_TYPES, shape.kv_numel(), dev),
+                             _arg(V, "V", _KV_TYPES, shape.kv_numel(), dev), _dtype_code(K), ctypes.byref(shape.c),
+                             int(mode), bud, _arg(idx, "idx", _I32, n, dev),
+                             _arg(counts, "counts", _I32, shape.units, dev, optional=True),
+                             _arg(offsets, "offsets", _I32, shape.units, dev, optional=not flat),
+                             _arg(Kc, "Kc", _KV_TYPES, n * D, dev), _arg(Vc, "Vc", _KV_TYPES, n * D, dev),
+                             _stream(stream)))
 
 
 def ecokv_decode_workspace_size(shape: Shape, max_count: int) -> int:
@@ -266,17 +381,28 @@ def ecokv_decode_workspace_size(shape: Shape, max_count: int) -> int:
 def ecokv_decode(Q_dec: torch.Tensor, Kc: torch.Tensor, Vc: torch.Tensor, shape: Shape, counts: torch.Tensor,
                  offsets: torch.Tensor, max_count: int, O: torch.Tensor, lse: Optional[torch.Tensor] = None,
                  workspace: Optional[torch.Tensor] = None, stream=None) -> None:
-    """Enqueue ecokv_decode (attention of one query per head over the compressed cache)."""
-    if workspace is None:
-        workspace = torch.empty(max(ecokv_decode_workspace_size(shape, max_count), 256), dtype=torch.uint8,
-                                device=Q_dec.device)
+    """Enqueue ecokv_decode (attention of one query per head over the compressed cache).
+    The rows each unit reads (offsets[u] .. + counts[u]) are device values the
+    binding cannot see; the caller guarantees they lie inside Kc and Vc, as
+    ecokv_select writes them for a cache that ecokv_compact filled."""
     if Kc.dtype != Q_dec.dtype or Vc.dtype != Q_dec.dtype:
         raise TypeError("Q_dec, Kc and Vc must share one element type")
-    if counts.dtype != torch.int32 or offsets.dtype != torch.int32:
-        raise TypeError("counts and offsets are int32")
-    _check(lib.ecokv_decode(_ptr(Q_dec), _ptr(Kc), _ptr(Vc), _dtype_code(Q_dec), ctypes.byref(shape.c),
-                            _ptr(counts), _ptr(offsets), int(max_count), _ptr(O), _ptr(lse), _ptr(workspace),
-                            workspace.numel(), _stream(stream)))
+    c = shape.c
+    need = ecokv_decode_workspace_size(shape, max_count)
+    if c.num_layers == 0:
+        return
+    dev = Q_dec.device
+    D = c.head_dim
+    nq = c.num_layers * c.num_q_heads * c.num_seqs
+    if Kc.numel() % D or Vc.numel() != Kc.numel():
+        raise ValueError("Kc and Vc must hold the same whole number of rows of head_dim elements")
+    workspace = _workspace(workspace, need, dev, stream)
+    _check(lib.ecokv_decode(_arg(Q_dec, "Q_dec", _KV_TYPES, nq * D, dev), _arg(Kc, "Kc", _KV_TYPES, D, dev),
+                            _arg(Vc, "Vc", _KV_TYPES, D, dev), _dtype_code(Q_dec), ctypes.byref(shape.c),
+                            _arg(counts, "counts", _I32, shape.units, dev),
+                            _arg(offsets, "offsets", _I32, shape.units, dev), int(max_count),
+                            _arg(O, "O", _F32, nq * D, dev), _arg(lse, "lse", _F32, nq, dev, optional=True),
+                            _arg(workspace, "workspace", _U8, need, dev), workspace.numel(), _stream(stream)))
 
 
 def ecokv_last_error() -> str:

@@ -31,7 +31,8 @@ class EvictionPass:
         if workspace is not None and workspace.numel() >= ws:
             self.workspace = workspace  # (shared with passes that never run at the same time)
         else:
-            self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
+            # zero-filled: its first word is the status that ecokv_workspace_status reads
+            self.workspace = torch.zeros(max(ws, 256), dtype=torch.uint8, device=device)
         self.n_idx = E.ecokv_index_count_mode(shape, mode, self.budget)
         self.idx = torch.empty(max(self.n_idx, 1), dtype=torch.int32, device=device)
         self.counts = torch.empty(max(U, 1), dtype=torch.int32, device=device)
@@ -66,6 +67,11 @@ class EvictionPass:
         self.compact(K, V, stream)
         return self
 
+    def check(self, stream=None):
+        """Synchronise `stream` and raise if a score call since the last check
+        had a wait between blocks give up (see ecokv_workspace_status)."""
+        E.ecokv_workspace_status(self.workspace, stream)
+
 
 class LayerwiseEviction:
     """The pass for one layer at a time, as a prefill finishes each layer.
@@ -89,7 +95,7 @@ class LayerwiseEviction:
         params = params or E.Params()
         ws = max(E.ecokv_workspace_size(shape, params), 256)
         self.streams = [torch.cuda.Stream(device=device), torch.cuda.Stream(device=device)]
-        self.workspaces = [torch.empty(ws, dtype=torch.uint8, device=device) for _ in range(2)]
+        self.workspaces = [torch.zeros(ws, dtype=torch.uint8, device=device) for _ in range(2)]
         self.passes = [EvictionPass(shape, budget, mode, params, dtype, device, self.workspaces[l % 2])
                        for l in range(num_layers)]
         self._ready = [torch.cuda.Event(), torch.cuda.Event()]
@@ -118,3 +124,9 @@ class LayerwiseEviction:
         for s, done in zip(self.streams, self._done):
             done.record(s)
             cur.wait_event(done)
+
+    def check(self):
+        """Synchronise both side streams and raise if a layer's score call had a
+        wait between blocks give up (see ecokv_workspace_status)."""
+        for s, ws in zip(self.streams, self.workspaces):
+            E.ecokv_workspace_status(ws, s)

@@ -209,9 +209,9 @@ def test_value_norm_mode_checks(P):
     rc = lib.ecokv_score_v(fake, None, fake, 0, ctypes.byref(s.c), ctypes.byref(p1), fake, None, None, fake, ws,
                            None)
     assert rc == -1
-    # the value-norm workspace is larger
+    # the value-norm workspace is larger (fp32 keys: the larger of the two layouts)
     ws0 = P.ecokv_workspace_size(s, p0)
-    rc = lib.ecokv_score_v(fake, fake, fake, 0, ctypes.byref(s.c), ctypes.byref(p1), fake, None, None, fake, ws0,
+    rc = lib.ecokv_score_v(fake, fake, fake, 1, ctypes.byref(s.c), ctypes.byref(p1), fake, None, None, fake, ws0,
                            None)
     assert rc == -2
 
@@ -250,3 +250,24 @@ def test_decode_checks_before_device_work(P):
     assert lib.ecokv_decode(*args(wsb=ws - 1)) == -2
     assert lib.ecokv_decode(*args(ws=ctypes.c_void_p(260))) == -1
     assert lib.ecokv_decode(*args(Q=ctypes.c_void_p(264))) == -1   # not 16-byte aligned
+
+
+def test_workspace_status_checks_before_device_work(P):
+    from paper_2609_06663_amd import ecokv as E
+    assert E.lib.ecokv_workspace_status(None, None) == -1
+    assert E.lib.ecokv_workspace_status(ctypes.c_void_p(260), None) == -1
+    assert P.ETIMEOUT == -5
+
+
+def test_binding_refuses_host_tensors(P):
+    # the binding checks device, element type and size before calling the
+    # library: a host tensor never reaches a kernel
+    import torch
+    s = P.Shape(1, 4, 2, 128, 4, [0, 100])
+    K = torch.zeros(2 * 100 * 128, dtype=torch.bfloat16)
+    Q = torch.zeros(4 * 4 * 128, dtype=torch.bfloat16)
+    out = torch.zeros(2 * 96)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        P.ecokv_score(K, Q, s, None, out, workspace=torch.zeros(1 << 20, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="GPU tensor"):
+        P.ecokv_select(out, s, P.PER_HEAD, [10], torch.zeros(20, dtype=torch.int32))
