@@ -252,8 +252,10 @@ def main():
     hbud = [bl for bl in per_layer for _ in range(Hkv)]
     n_h = P.ecokv_index_count_mode(shape, P.HEAD_BUDGETS, hbud)
     assert n_h <= ep.n_idx
+    ws_h = torch.zeros(P.ecokv_select_workspace_size(shape, P.HEAD_BUDGETS), dtype=torch.uint8, device=dev)
     h_calls = {
-        "select": lambda: P.ecokv_select(ep.scores, shape, P.HEAD_BUDGETS, hbud, ep.idx, ep.counts, ep.offsets),
+        "select": lambda: P.ecokv_select(ep.scores, shape, P.HEAD_BUDGETS, hbud, ep.idx, ep.counts, ep.offsets,
+                                         ws_h),
         "compact": lambda: P.ecokv_compact(K, V, shape, P.HEAD_BUDGETS, hbud, ep.idx, None, None, ep.Kc, ep.Vc),
     }
     head_budgets = {"schedule": "PyramidKV, beta 20", "budget_first_layer": per_layer[0],

@@ -232,6 +232,12 @@ int ecokv_index_count(const ecokv_shape *shape, const int32_t *budget, int64_t *
  * sum over (l, h, s) of min(budget[l][h], T_s)). */
 int ecokv_index_count_mode(const ecokv_shape *shape, int mode, const int32_t *budget, int64_t *count);
 
+/* Bytes of device workspace ecokv_select needs for this shape and mode (the
+ * budgets do not change it).  Like the score workspace it must be zero-filled
+ * before its first use; ecokv_select leaves it zero-filled, so one workspace
+ * serves any number of calls of this or a smaller shape, one at a time. */
+int ecokv_select_workspace_size(const ecokv_shape *shape, int mode, size_t *bytes);
+
 /* Select the kept positions (Sec. 3; AdaKV, PyramidKV and SparseMM budgets,
  * Appendix A.1).
  *   scores  [L][H_kv][Ptot] float32, as written by ecokv_score
@@ -254,11 +260,19 @@ int ecokv_index_count_mode(const ecokv_shape *shape, int mode, const int32_t *bu
  *           LAYER_FLAT)
  *   offsets [L][H_kv][B] output: start of each unit in idx (may be NULL,
  *           except in LAYER_FLAT)
+ *   workspace, workspace_bytes: device scratch of at least
+ *           ecokv_select_workspace_size bytes, 256-byte aligned, zero-filled
+ *           before its first use (left so); not shared by calls that may
+ *           overlap.  Each selection group (a unit, or the heads of a
+ *           (layer, sequence) in LAYER_FLAT) is split over many blocks: its
+ *           radix-select histograms and per-slice counts live there.
  * NaN scores rank below every number; -0 ranks equal to +0.
  * ECOKV_EUNSUPPORTED: LAYER_FLAT with more than 256 KV heads, or with
- * H_kv * Ptot * 4 > 2^31 - 1 bytes of scores per layer. */
+ * H_kv * Ptot * 4 > 2^31 - 1 bytes of scores per layer; a sequence with
+ * (T_s - w) * 4 > 2^31 - 1 bytes of scores. */
 int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const int32_t *budget,
-                 int32_t *idx, int32_t *counts, int32_t *offsets, void *stream);
+                 int32_t *idx, int32_t *counts, int32_t *offsets, void *workspace, size_t workspace_bytes,
+                 void *stream);
 
 /* Gather Kc[e] = K[row of entry e], Vc[e] = V[row of entry e] for every idx
  * entry e, bit-exact (Sec. 3).  `mode` and `budget` as given to ecokv_select;

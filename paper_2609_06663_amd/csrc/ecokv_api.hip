@@ -171,6 +171,50 @@ std::vector<StageRec> g_stages;
 thread_local const char *g_stage_name = nullptr;
 thread_local hipEvent_t g_stage_start = nullptr;
 
+// Groups of the largest select launch and keys of the largest group, which
+// size the select workspace.
+void select_dims(const ShapeInfo &si, const ecokv_shape *sh, int mode, int64_t *groups, int64_t *maxn)
+{
+    const int64_t pairs = (int64_t)si.L * si.Hkv;
+    *groups = mode == ECOKV_HEAD_BUDGETS ? (pairs < ecokv::kLhChunk ? pairs : ecokv::kLhChunk) * si.B
+              : mode == ECOKV_LAYER_FLAT ? (int64_t)si.L * si.B
+                                         : pairs * si.B;
+    *maxn = (int64_t)si.maxP * (mode == ECOKV_LAYER_FLAT ? si.Hkv : 1);
+    (void)sh;
+}
+
+int check_select_mode(const ShapeInfo &si, int mode)
+{
+    if (mode != ECOKV_PER_HEAD && mode != ECOKV_LAYER_FLAT && mode != ECOKV_HEAD_BUDGETS)
+        return fail(ECOKV_EINVAL, "mode %d", mode);
+    if (mode == ECOKV_LAYER_FLAT) {
+        if (si.Hkv > ecokv::select_max_flat_heads())
+            return fail(ECOKV_EUNSUPPORTED, "LAYER_FLAT supports at most %d KV heads", ecokv::select_max_flat_heads());
+        // (a selection group's scores are read through one 32-bit-addressed buffer descriptor)
+        if ((int64_t)si.Hkv * si.Ptot * 4 > INT32_MAX)
+            return fail(ECOKV_EUNSUPPORTED, "LAYER_FLAT: H_kv x P_total scores of a layer exceed 2^31 bytes");
+    }
+    if ((int64_t)si.maxP * 4 > INT32_MAX)
+        return fail(ECOKV_EUNSUPPORTED, "a sequence's scores exceed 2^31 bytes");
+    return ECOKV_OK;
+}
+
+// Checks the caller's select workspace and points the launch at it.
+int select_workspace(const ShapeInfo &si, const ecokv_shape *shape, int mode, void *workspace, size_t workspace_bytes,
+                     ecokv::SelectArgs *a)
+{
+    int64_t groups = 0, maxn = 0;
+    select_dims(si, shape, mode, &groups, &maxn);
+    const size_t need = ecokv::select_ws_layout(groups, maxn).total;
+    if (!workspace) return fail(ECOKV_EINVAL, "workspace is NULL");
+    if (((uintptr_t)workspace & 255u) != 0) return fail(ECOKV_EINVAL, "workspace must be 256-byte aligned");
+    if (workspace_bytes < need)
+        return fail(ECOKV_EWORKSPACE, "select workspace has %zu bytes, needs %zu", workspace_bytes, need);
+    a->mb_groups = groups;
+    a->mb_maxn = maxn;
+    return ECOKV_OK;
+}
+
 }  // namespace
 
 namespace ecokv {
@@ -414,14 +458,27 @@ int ecokv_index_count_mode(const ecokv_shape *shape, int mode, const int32_t *bu
     return ECOKV_OK;
 }
 
-int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const int32_t *budget, int32_t *idx,
-                 int32_t *counts, int32_t *offsets, void *stream)
+int ecokv_select_workspace_size(const ecokv_shape *shape, int mode, size_t *bytes)
 {
     ShapeInfo si;
     int rc = check_shape(shape, &si);
     if (rc) return rc;
-    if (mode != ECOKV_PER_HEAD && mode != ECOKV_LAYER_FLAT && mode != ECOKV_HEAD_BUDGETS)
-        return fail(ECOKV_EINVAL, "mode %d", mode);
+    if ((rc = check_select_mode(si, mode))) return rc;
+    if (!bytes) return fail(ECOKV_EINVAL, "bytes is NULL");
+    int64_t groups = 0, maxn = 0;
+    select_dims(si, shape, mode, &groups, &maxn);
+    *bytes = ecokv::select_ws_layout(groups, maxn).total;
+    return ECOKV_OK;
+}
+
+int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const int32_t *budget,
+                            int32_t *idx, int32_t *counts, int32_t *offsets, void *workspace,
+                            size_t workspace_bytes, void *stream)
+{
+    ShapeInfo si;
+    int rc = check_shape(shape, &si);
+    if (rc) return rc;
+    if ((rc = check_select_mode(si, mode))) return rc;
     if (!budget && (mode != ECOKV_HEAD_BUDGETS || (int64_t)si.L * si.Hkv > 0))
         return fail(ECOKV_EINVAL, "budget is NULL");
     ecokv::SelectArgs a;
@@ -433,6 +490,7 @@ int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const 
         if ((rc = fill_seqtab(shape, nullptr, si.w, &a.seq, &per_lh))) return rc;
         if (si.L == 0) return ECOKV_OK;
         if (!scores || !idx) return fail(ECOKV_EINVAL, "scores and idx must be non-NULL");
+        if ((rc = select_workspace(si, shape, mode, workspace, workspace_bytes, &a))) return rc;
         a.scores = scores;
         a.idx = idx;
         a.counts = counts;
@@ -449,23 +507,19 @@ int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const 
         for (int64_t lh0 = 0; lh0 < npairs; lh0 += ecokv::kLhChunk) {
             const int n = (int)(npairs - lh0 < ecokv::kLhChunk ? npairs - lh0 : ecokv::kLhChunk);
             e0 = fill_lhtab(shape, si.B, budget, lh0, n, e0, &a.lht);
-            const hipError_t e = ecokv::select_launch(a, static_cast<hipStream_t>(stream));
+            const hipError_t e = ecokv::select_launch(a, static_cast<char *>(workspace),
+                                                      static_cast<hipStream_t>(stream));
             if (e != hipSuccess) return hip_fail(e, "ecokv_select launch");
         }
         return ECOKV_OK;
     }
     if ((rc = fill_seqtab(shape, budget, si.w, &a.seq, &per_lh))) return rc;
     if ((int64_t)si.L * si.Hkv * per_lh > INT32_MAX) return fail(ECOKV_EINVAL, "index count overflows int32");
-    if (mode == ECOKV_LAYER_FLAT) {
-        if (!counts || !offsets) return fail(ECOKV_EINVAL, "LAYER_FLAT needs counts and offsets");
-        if (si.Hkv > ecokv::select_max_flat_heads())
-            return fail(ECOKV_EUNSUPPORTED, "LAYER_FLAT supports at most %d KV heads", ecokv::select_max_flat_heads());
-        // (a selection group's scores are read through one 32-bit-addressed buffer descriptor)
-        if ((int64_t)si.Hkv * si.Ptot * 4 > INT32_MAX)
-            return fail(ECOKV_EUNSUPPORTED, "LAYER_FLAT: H_kv x P_total scores of a layer exceed 2^31 bytes");
-    }
+    if (mode == ECOKV_LAYER_FLAT && (!counts || !offsets))
+        return fail(ECOKV_EINVAL, "LAYER_FLAT needs counts and offsets");
     if (si.L == 0) return ECOKV_OK;
     if (!scores || !idx) return fail(ECOKV_EINVAL, "scores and idx must be non-NULL");
+    if ((rc = select_workspace(si, shape, mode, workspace, workspace_bytes, &a))) return rc;
     a.scores = scores;
     a.idx = idx;
     a.counts = counts;
@@ -477,7 +531,7 @@ int ecokv_select(const float *scores, const ecokv_shape *shape, int mode, const 
     a.Ptot = si.Ptot;
     a.per_lh = per_lh;
     a.flat = mode == ECOKV_LAYER_FLAT;
-    const hipError_t e = ecokv::select_launch(a, static_cast<hipStream_t>(stream));
+    const hipError_t e = ecokv::select_launch(a, static_cast<char *>(workspace), static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "ecokv_select launch");
     return ECOKV_OK;
 }

@@ -104,9 +104,23 @@ struct SelectArgs {
     int64_t per_lh;  // sum over s of min(b_s, T_s) (not ECOKV_HEAD_BUDGETS)
     int flat;
     int heads;       // ECOKV_HEAD_BUDGETS: budgets and starts from lht
+    // the caller's workspace (select_ws_layout(mb_groups, mb_maxn)), filled by select_launch
+    uint4 *mb_state;     // [3][mb_groups]           selection state after each digit
+    uint32_t *mb_hist;   // [mb_groups][5120]        global digit histograms
+    uint32_t *mb_head;   // [mb_groups][256][2]      per-head keys above / equal to the threshold
+    uint32_t *mb_cnt;    // [mb_groups][slices][2]   per-slice keys above / equal to the threshold
+    int64_t mb_groups;   // groups of the largest launch of the call
+    int64_t mb_maxn;     // keys of the largest group of the call
+    int mb_slices;       // slices per group of this launch
     SeqTab seq;
     LhTab lht;
 };
+
+// Workspace of ecokv_select.
+struct SelWsLayout {
+    size_t state, hist, head, cnt, total;
+};
+SelWsLayout select_ws_layout(int64_t groups, int64_t maxn);
 
 struct CompactArgs {
     const char *K;
@@ -173,7 +187,7 @@ unsigned launch_tag();
 // Clears the workspace status word (stream-ordered, by a one-thread kernel).
 hipError_t status_clear(unsigned *status, hipStream_t st);
 constexpr int kStreamMaxRows = 30;     // window rows of the streaming sweep 2; 2 more rows carry mu
-hipError_t select_launch(const SelectArgs &a, hipStream_t st);
+hipError_t select_launch(SelectArgs a, char *ws, hipStream_t st);
 int select_max_flat_heads();
 hipError_t compact_launch(const CompactArgs &a, hipStream_t st);
 

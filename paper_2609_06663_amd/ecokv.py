@@ -32,7 +32,8 @@ STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7, imp_m
 EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_workspace_status", "ecokv_score", "ecokv_score_v",
            "ecokv_score_pre",
            "ecokv_index_count",
-           "ecokv_index_count_mode", "ecokv_select", "ecokv_compact", "ecokv_pyramid_budgets",
+           "ecokv_index_count_mode", "ecokv_select_workspace_size", "ecokv_select", "ecokv_compact",
+           "ecokv_pyramid_budgets",
            "ecokv_decode_workspace_size", "ecokv_decode",
            "ecokv_last_error", "ecokv_stage_times"]
 
@@ -126,7 +127,8 @@ def _load():
     lib.ecokv_decode.argtypes = [vp, vp, vp, ctypes.c_int, sp, vp, vp, ctypes.c_int32, vp, vp, vp,
                                  ctypes.c_size_t, vp]
     lib.ecokv_pyramid_budgets.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_int, i32p]
-    lib.ecokv_select.argtypes = [vp, sp, ctypes.c_int, i32p, vp, vp, vp, vp]
+    lib.ecokv_select_workspace_size.argtypes = [sp, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
+    lib.ecokv_select.argtypes = [vp, sp, ctypes.c_int, i32p, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_compact.argtypes = [vp, vp, ctypes.c_int, sp, ctypes.c_int, i32p, vp, vp, vp, vp, vp, vp]
     lib.ecokv_last_error.restype = ctypes.c_char_p
     lib.ecokv_stage_times.argtypes = [ctypes.POINTER(_StageTime), ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
@@ -331,22 +333,34 @@ def ecokv_pyramid_budgets(num_layers: int, total: float, beta: float, window: in
     return [int(v) for v in out[:num_layers]]
 
 
+def ecokv_select_workspace_size(shape: Shape, mode: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib.ecokv_select_workspace_size(ctypes.byref(shape.c), int(mode), ctypes.byref(n)))
+    return n.value
+
+
 def ecokv_select(scores: torch.Tensor, shape: Shape, mode: int, budget, idx: torch.Tensor,
                  counts: Optional[torch.Tensor] = None, offsets: Optional[torch.Tensor] = None,
-                 stream=None) -> None:
+                 workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Enqueue ecokv_select.  `workspace` (uint8, >= ecokv_select_workspace_size
+    bytes, zero-filled before its first use) is allocated here when not given."""
     bud = _budget(shape, budget, mode)
     if shape.c.num_layers == 0:
         _check(lib.ecokv_select(_ptr(scores), ctypes.byref(shape.c), int(mode), bud, _ptr(idx), _ptr(counts),
-                                _ptr(offsets), _stream(stream)))
+                                _ptr(offsets), _ptr(workspace), 0 if workspace is None else workspace.numel(),
+                                _stream(stream)))
         return
     n = ecokv_index_count_mode(shape, mode, budget)
     dev = scores.device if isinstance(scores, torch.Tensor) else None
     flat = int(mode) == LAYER_FLAT
-    _check(lib.ecokv_select(_arg(scores, "scores", _F32, shape.score_numel(), dev), ctypes.byref(shape.c),
-                            int(mode), bud, _arg(idx, "idx", _I32, n, dev),
-                            _arg(counts, "counts", _I32, shape.units, dev, optional=not flat),
-                            _arg(offsets, "offsets", _I32, shape.units, dev, optional=not flat),
-                            _stream(stream)))
+    sp_ = _arg(scores, "scores", _F32, shape.score_numel(), dev)
+    ip = _arg(idx, "idx", _I32, n, dev)
+    cp = _arg(counts, "counts", _I32, shape.units, dev, optional=not flat)
+    op = _arg(offsets, "offsets", _I32, shape.units, dev, optional=not flat)
+    need = ecokv_select_workspace_size(shape, mode)
+    workspace = _workspace(workspace, need, dev, stream)
+    _check(lib.ecokv_select(sp_, ctypes.byref(shape.c), int(mode), bud, ip, cp, op,
+                            _arg(workspace, "workspace", _U8, need, dev), workspace.numel(), _stream(stream)))
 
 
 def ecokv_compact(K: torch.Tensor, V: torch.Tensor, shape: Shape, mode: int, budget,

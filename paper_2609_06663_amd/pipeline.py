@@ -33,6 +33,9 @@ class EvictionPass:
         else:
             # zero-filled: its first word is the status that ecokv_workspace_status reads
             self.workspace = torch.zeros(max(ws, 256), dtype=torch.uint8, device=device)
+        # zero-filled, as ecokv_select leaves it
+        self.sel_workspace = torch.zeros(max(E.ecokv_select_workspace_size(shape, mode), 256), dtype=torch.uint8,
+                                         device=device)
         self.n_idx = E.ecokv_index_count_mode(shape, mode, self.budget)
         self.idx = torch.empty(max(self.n_idx, 1), dtype=torch.int32, device=device)
         self.counts = torch.empty(max(U, 1), dtype=torch.int32, device=device)
@@ -54,7 +57,7 @@ class EvictionPass:
 
     def select(self, stream=None):
         E.ecokv_select(self.scores, self.shape, self.mode, self.budget, self.idx, self.counts,
-                       self.offsets, stream)
+                       self.offsets, self.sel_workspace, stream)
 
     def compact(self, K: torch.Tensor, V: torch.Tensor, stream=None):
         E.ecokv_compact(K, V, self.shape, self.mode, self.budget, self.idx, self.counts, self.offsets,

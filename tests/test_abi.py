@@ -108,17 +108,17 @@ def test_calls_fail_before_device_work(P):
     rc = lib.ecokv_score(fake, fake, 7, ctypes.byref(s.c), ctypes.byref(p), fake, None, None, fake, ws, None)
     assert rc == -3
     bud = (ctypes.c_int32 * 1)(3)   # below the window
-    rc = lib.ecokv_select(fake, ctypes.byref(s.c), 0, bud, fake, None, None, None)
+    rc = lib.ecokv_select(fake, ctypes.byref(s.c), 0, bud, fake, None, None, fake, 1 << 30, None)
     assert rc == -1
     bud = (ctypes.c_int32 * 1)(10)
-    rc = lib.ecokv_select(fake, ctypes.byref(s.c), 1, bud, fake, None, None, None)   # flat without counts
+    rc = lib.ecokv_select(fake, ctypes.byref(s.c), 1, bud, fake, None, None, fake, 1 << 30, None)   # flat without counts
     assert rc == -1
-    rc = lib.ecokv_select(fake, ctypes.byref(s.c), 5, bud, fake, None, None, None)   # bad mode
+    rc = lib.ecokv_select(fake, ctypes.byref(s.c), 5, bud, fake, None, None, fake, 1 << 30, None)   # bad mode
     assert rc == -1
     # layer-flat scores of a layer beyond 2^31 bytes (8 heads x 67.1 M tokens)
     big = P.Shape(1, 8, 8, 128, 4, [0, 1 << 26, (1 << 26) + 200000])
     bud2 = (ctypes.c_int32 * 2)(10, 10)
-    rc = lib.ecokv_select(fake, ctypes.byref(big.c), 1, bud2, fake, fake, fake, None)
+    rc = lib.ecokv_select(fake, ctypes.byref(big.c), 1, bud2, fake, fake, fake, fake, 1 << 30, None)
     assert rc == -3 and b"2^31" in lib.ecokv_last_error()
     rc = lib.ecokv_compact(fake, None, 0, ctypes.byref(s.c), 0, bud, fake, None, None, fake, fake, None)
     assert rc == -1
@@ -179,14 +179,14 @@ def test_head_budget_calls_fail_before_device_work(P):
     lib = E.lib
     fake = ctypes.c_void_p(256)
     bud = (ctypes.c_int32 * 4)(10, 20, 3, 50)   # pair (1, 0) below the window
-    assert lib.ecokv_select(fake, ctypes.byref(s.c), 2, bud, fake, None, None, None) == -1
+    assert lib.ecokv_select(fake, ctypes.byref(s.c), 2, bud, fake, None, None, fake, 1 << 30, None) == -1
     assert "below the window" in P.ecokv_last_error()
     assert lib.ecokv_compact(fake, fake, 0, ctypes.byref(s.c), 2, bud, fake, None, None, fake, fake, None) == -1
     bud = (ctypes.c_int32 * 4)(10, 20, 30, 50)
-    assert lib.ecokv_select(None, ctypes.byref(s.c), 2, bud, fake, None, None, None) == -1   # NULL scores
+    assert lib.ecokv_select(None, ctypes.byref(s.c), 2, bud, fake, None, None, fake, 1 << 30, None) == -1   # NULL scores
     assert lib.ecokv_compact(fake, None, 0, ctypes.byref(s.c), 2, bud, fake, None, None, fake, fake, None) == -1
     s0 = P.Shape(0, 4, 2, 128, 4, [0, 100])
-    assert lib.ecokv_select(None, ctypes.byref(s0.c), 2, None, None, None, None, None) == 0   # nothing to do
+    assert lib.ecokv_select(None, ctypes.byref(s0.c), 2, None, None, None, None, None, 0, None) == 0   # nothing to do
 
 
 def test_value_norm_mode_checks(P):
@@ -271,3 +271,21 @@ def test_binding_refuses_host_tensors(P):
         P.ecokv_score(K, Q, s, None, out, workspace=torch.zeros(1 << 20, dtype=torch.uint8))
     with pytest.raises(ValueError, match="GPU tensor"):
         P.ecokv_select(out, s, P.PER_HEAD, [10], torch.zeros(20, dtype=torch.int32))
+
+
+def test_select_workspace_checks(P):
+    from paper_2609_06663_amd import ecokv as E
+    s = P.Shape(2, 8, 2, 128, 4, [0, 1000, 5000])
+    fake = ctypes.c_void_p(256)
+    bud = (ctypes.c_int32 * 2)(100, 200)
+    for mode in (P.PER_HEAD, P.LAYER_FLAT, P.HEAD_BUDGETS):
+        assert P.ecokv_select_workspace_size(s, mode) > 0
+    need = P.ecokv_select_workspace_size(s, P.PER_HEAD)
+    lib = E.lib
+    assert lib.ecokv_select(fake, ctypes.byref(s.c), 0, bud, fake, None, None, None, need, None) == -1   # NULL
+    assert lib.ecokv_select(fake, ctypes.byref(s.c), 0, bud, fake, None, None, ctypes.c_void_p(260), need,
+                            None) == -1   # misaligned
+    assert lib.ecokv_select(fake, ctypes.byref(s.c), 0, bud, fake, None, None, fake, need - 1, None) == -2
+    # a layer-flat group holds every head's keys of a (layer, sequence): more slices per group
+    assert P.ecokv_select_workspace_size(P.Shape(1, 8, 8, 128, 4, [0, 32768]), P.LAYER_FLAT) > \
+        P.ecokv_select_workspace_size(P.Shape(1, 8, 8, 128, 4, [0, 32768]), P.PER_HEAD) // 8

@@ -485,3 +485,73 @@ def test_select_register_64_keys_per_thread(case):
     np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
     np.testing.assert_array_equal(counts.cpu().numpy(), ref_c.reshape(-1))
     np.testing.assert_array_equal(offsets.cpu().numpy(), ref_o.reshape(-1))
+
+
+# ---------------------------------------------------------------------------
+# multi-block selection: shapes for each path, bit-exact against the oracle
+# ---------------------------------------------------------------------------
+
+def _select_case(name, rng):
+    """(L, Hkv, w, seqlens, budget, mode, scores[L][Hkv][Ptot] float32) for one case."""
+    if name == "ties_across_slices":
+        # 3 values over 40000 keys: the threshold class spans many slices
+        L, Hkv, w, lens, bud = 1, 2, 4, [40004], [15004]
+        S = rng.integers(0, 3, size=(L, Hkv, 40000)).astype(np.float32)
+    elif name == "bin_taken_whole":
+        # the k largest are exactly the keys of one top-digit bin and above
+        L, Hkv, w, lens, bud = 1, 2, 4, [20004], [5004]
+        S = rng.uniform(0.0, 0.5, size=(L, Hkv, 20000)).astype(np.float32)
+        for h in range(Hkv):
+            top = rng.choice(20000, 5000, replace=False)
+            S[0, h, top] = rng.uniform(4.0, 8.0, size=5000).astype(np.float32)
+    elif name == "flat_tiny_heads":
+        # layer-flat groups whose slices span many heads (P = 5 and 9)
+        L, Hkv, w, lens, bud = 2, 200, 3, [8, 12], [5, 7]
+        S = rng.integers(0, 5, size=(L, Hkv, 5 + 9)).astype(np.float32) * np.float32(0.5)
+    elif name == "flat_long":
+        L, Hkv, w, lens, bud = 1, 4, 4, [70004, 9000], [10504, 1350]
+        S = rng.standard_normal((L, Hkv, 70000 + 8996)).astype(np.float32)
+    elif name == "many_groups_16_per_thread":
+        # 160 groups of 4 slices each: the 16-keys-per-thread form
+        L, Hkv, w, lens, bud = 40, 4, 4, [16004], [3204]
+        S = np.exp(rng.uniform(-8, 2, size=(L, Hkv, 16000))).astype(np.float32)
+    elif name == "nan_and_signed_zero":
+        L, Hkv, w, lens, bud = 1, 3, 2, [3002, 500], [1500, 300]
+        S = rng.integers(-3, 3, size=(L, Hkv, 3000 + 498)).astype(np.float32) * np.float32(0.0) + \
+            rng.integers(0, 4, size=(L, Hkv, 3498)).astype(np.float32)
+        S[0, 0, :400] = np.nan
+        S[0, 1, 100:900] = -0.0
+        S[0, 2, 50:70] = np.inf
+        S[0, 2, 70:90] = -np.inf
+    else:
+        raise ValueError(name)
+    return L, Hkv, w, lens, bud, S
+
+
+@pytest.mark.parametrize("mode", ["per_head", "layer_flat"])
+@pytest.mark.parametrize("name", ["ties_across_slices", "bin_taken_whole", "flat_tiny_heads", "flat_long",
+                                  "many_groups_16_per_thread", "nan_and_signed_zero"])
+def test_select_multiblock_bit_exact(name, mode):
+    import paper_2609_06663_amd as P
+    import zlib
+    rng = np.random.default_rng(zlib.crc32(f"{name}/{mode}".encode()))
+    L, Hkv, w, lens, bud, S = _select_case(name, rng)
+    cu = np.concatenate([[0], np.cumsum(lens)]).tolist()
+    m = P.PER_HEAD if mode == "per_head" else P.LAYER_FLAT
+    shape = P.Shape(L, Hkv, Hkv, 128, w, cu)
+    n = P.ecokv_index_count(shape, bud)
+    idx = torch.full((n,), -7, dtype=torch.int32, device="cuda")
+    counts = torch.full((L * Hkv * len(lens),), -7, dtype=torch.int32, device="cuda")
+    offsets = torch.full_like(counts, -7)
+    ws = torch.zeros(P.ecokv_select_workspace_size(shape, m), dtype=torch.uint8, device="cuda")
+    say(f"multi-block select {name} ({mode}): {L} layers x {Hkv} heads, sequences {lens}")
+    Sd = torch.from_numpy(np.ascontiguousarray(S)).cuda()
+    ref_idx, ref_c, ref_o = oracle.select(S.astype(np.float64), L, Hkv, cu, w, bud,
+                                          oracle.PER_HEAD if m == P.PER_HEAD else oracle.LAYER_FLAT)
+    for rep in range(2):  # the same workspace twice: the calls leave it as they found it
+        P.ecokv_select(Sd, shape, m, bud, idx, counts, offsets, ws)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
+        np.testing.assert_array_equal(counts.cpu().numpy(), ref_c.reshape(-1))
+        np.testing.assert_array_equal(offsets.cpu().numpy(), ref_o.reshape(-1))
+        idx.fill_(-7)
