@@ -477,6 +477,466 @@ hipError_t dquant_launch(const DQuantArgs &a, hipStream_t st)
     return hipGetLastError();
 }
 
+
+// Exclusive block-wide scan of two uint32 per thread (independent sums);
+// returns the exclusive prefixes and the block totals.
+__device__ __forceinline__ void block_exscan2(uint32_t x0, uint32_t x1, uint32_t *wsum, uint32_t &e0, uint32_t &e1,
+                                              uint32_t &t0, uint32_t &t1)
+{
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    uint32_t i0 = x0, i1 = x1;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const uint32_t y0 = __shfl_up(i0, d, kWave), y1 = __shfl_up(i1, d, kWave);
+        if (lane >= d) {
+            i0 += y0;
+            i1 += y1;
+        }
+    }
+    if (lane == kWave - 1) {
+        wsum[wv] = i0;
+        wsum[kSelWaves + 1 + wv] = i1;
+    }
+    __syncthreads();
+    if (wv == 0) {
+        uint32_t a0 = lane < kSelWaves ? wsum[lane] : 0u;
+        uint32_t a1 = lane < kSelWaves ? wsum[kSelWaves + 1 + lane] : 0u;
+        uint32_t c0 = a0, c1 = a1;
+#pragma unroll
+        for (int d = 1; d < kSelWaves; d <<= 1) {
+            const uint32_t y0 = __shfl_up(c0, d, kWave), y1 = __shfl_up(c1, d, kWave);
+            if (lane >= d) {
+                c0 += y0;
+                c1 += y1;
+            }
+        }
+        if (lane < kSelWaves) {
+            wsum[lane] = c0 - a0;
+            wsum[kSelWaves + 1 + lane] = c1 - a1;
+        }
+        if (lane == kSelWaves - 1) {
+            wsum[kSelWaves] = c0;
+            wsum[2 * kSelWaves + 1] = c1;
+        }
+    }
+    __syncthreads();
+    e0 = wsum[wv] + i0 - x0;
+    e1 = wsum[kSelWaves + 1 + wv] + i1 - x1;
+    t0 = wsum[kSelWaves];
+    t1 = wsum[2 * kSelWaves + 1];
+    __syncthreads();
+}
+
+// Scores of one selection group: head h's non-window scores at base + h * hstride
+
+// (a single head in per-head mode: no division on that path; a group has at
+// most kMaxFlatHeads * 2^31 keys, so the head index fits 32 bits).
+struct GroupView {
+    const float *base;
+    int64_t hstride;
+    int P;
+    int nh;
+    __device__ __forceinline__ float get(int64_t v) const
+    {
+        if (nh == 1) return base[v];
+        const int h = v < 0x7fffffff ? (int)((uint32_t)v / (uint32_t)P) : (int)(v / P);
+        return base[(int64_t)h * hstride + (v - (int64_t)h * P)];
+    }
+};
+
+
+// The selection group of this block: layer l, heads h0 .. h0+nh-1 of
+
+
+// Wave 0 (all 64 lanes): the digit of the rem-th largest key from a 256-bin
+// histogram h, counts above it into slot[1]; with clear, the bins are zeroed.
+__device__ __forceinline__ void pick_digit(uint32_t *h, bool clear, int rem, uint32_t *slot)
+{
+    const int lane = threadIdx.x & 63;
+    // lane owns bins 255-4l .. 252-4l (descending digit order)
+    uint32_t c4[4], loc = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        c4[q] = h[255 - 4 * lane - q];
+        if (clear) h[255 - 4 * lane - q] = 0u;
+        loc += c4[q];
+    }
+    uint32_t inc = loc;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const uint32_t y = __shfl_up(inc, d, kWave);
+        if (lane >= d) inc += y;
+    }
+    const uint32_t before = inc - loc;
+    if ((int)before < rem && rem <= (int)inc) {
+        uint32_t cum = before;
+        for (int q = 0; q < 4; ++q) {
+            if ((int)(cum + c4[q]) >= rem) {
+                slot[0] = 255u - 4u * lane - q;
+                slot[1] = cum;
+                break;
+            }
+            cum += c4[q];
+        }
+    }
+}
+
+// The k-th largest key, as reg_radix_select, for a block whose 128 KiB
+// stage (lds) is free during the selection:
+//  * first digit: four histograms per wave (lane l of wave w counts into
+//    histogram 4 w + l % 4; 257 words apart, so lanes that share a digit hit
+//    different banks), folded by 256 threads;
+//  * then the keys that still carry the chosen prefix -- usually a small part
+//    of the group -- are gathered into the stage (a wave scan of the
+//    per-thread counts and one LDS atomic per wave place them), and the later
+//    digits count only them, into one shared histogram that the scanning wave
+//    reads and clears: two barriers per digit and no fold.  When they do not
+//    fit, the later digits count the registers into that histogram instead.
+constexpr int kStHistC = 4;
+constexpr int kStHistWords = kSelWaves * kStHistC * 257;
+constexpr int kStCandOff = kStHistWords + 256;
+constexpr int kStCandCap = 32 * kSelThreads - kStCandOff;
+
+template <int KPT>
+__device__ __forceinline__ void reg_radix_select_staged(const uint32_t (&kk)[KPT], int v0, int n, int k,
+                                                        uint32_t kmin, uint32_t kmax, uint32_t *lds,
+                                                        uint32_t *hsum, uint32_t (*bc)[2], uint32_t *ccount,
+                                                        uint32_t *thr_out, int *need_eq_out)
+{
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const uint32_t diff = kmin ^ kmax;
+    if (diff == 0) {
+        *thr_out = kmin;
+        *need_eq_out = k;
+        return;
+    }
+    int hi = 31 - __clz(diff);
+    uint32_t mask = hi == 31 ? 0u : ~((2u << hi) - 1u);
+    uint32_t prefix = kmin & mask;
+    int rem = k;
+    uint32_t *const h1 = lds + kStHistWords;
+    uint32_t *const cand = lds + kStCandOff;
+    for (int b = tid; b < kStHistWords + 256; b += blockDim.x) lds[b] = 0u;
+    if (tid == 0) *ccount = 0u;
+    __syncthreads();
+    {
+        // first digit (every key lies in [kmin, kmax], so all carry the prefix)
+        const int lo = hi >= 7 ? hi - 7 : 0;
+        const uint32_t nb = 1u << (hi - lo + 1);
+        uint32_t *const myh = lds + (wv * kStHistC + (lane & (kStHistC - 1))) * 257;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q)
+            if (v0 + q < n) atomicAdd(&myh[(kk[q] >> lo) & (nb - 1u)], 1u);
+        __syncthreads();
+        if (tid < 256) {
+            uint32_t c = 0;
+#pragma unroll 8
+            for (int w2 = 0; w2 < kSelWaves * kStHistC; ++w2) c += lds[w2 * 257 + tid];
+            hsum[tid] = c;
+        }
+        __syncthreads();
+        if (tid < kWave) pick_digit(hsum, false, rem, bc[0]);
+        __syncthreads();
+        prefix |= bc[0][0] << lo;
+        rem -= (int)bc[0][1];
+        mask |= (nb - 1u) << lo;
+        hi = lo - 1;
+    }
+    if (hi >= 0) {
+        // gather the keys that carry the prefix
+        uint32_t cnt = 0;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q) cnt += (v0 + q < n && (kk[q] & mask) == prefix) ? 1u : 0u;
+        uint32_t inc = cnt;
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) {
+            const uint32_t y = __shfl_up(inc, d, kWave);
+            if (lane >= d) inc += y;
+        }
+        const uint32_t wtot = __shfl(inc, kWave - 1, kWave);
+        uint32_t base = 0;
+        if (lane == kWave - 1 && wtot > 0) base = atomicAdd(ccount, wtot);
+        base = __shfl(base, kWave - 1, kWave);
+        uint32_t pos = base + inc - cnt;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q)
+            if (v0 + q < n && (kk[q] & mask) == prefix) {
+                if (pos < (uint32_t)kStCandCap) cand[pos] = kk[q];
+                ++pos;
+            }
+        __syncthreads();
+        const uint32_t ncand = *ccount;
+        const bool use_cand = ncand <= (uint32_t)kStCandCap;
+        int par = 1;
+        while (hi >= 0) {
+            const int lo = hi >= 7 ? hi - 7 : 0;
+            const uint32_t nb = 1u << (hi - lo + 1);
+            if (use_cand) {
+                for (uint32_t i = tid; i < ncand; i += kSelThreads) {
+                    const uint32_t key = cand[i];
+                    if ((key & mask) == prefix) atomicAdd(&h1[(key >> lo) & (nb - 1u)], 1u);
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < KPT; ++q)
+                    if (v0 + q < n && (kk[q] & mask) == prefix) atomicAdd(&h1[(kk[q] >> lo) & (nb - 1u)], 1u);
+            }
+            __syncthreads();
+            if (tid < kWave) pick_digit(h1, true, rem, bc[par]);
+            __syncthreads();
+            prefix |= bc[par][0] << lo;
+            rem -= (int)bc[par][1];
+            mask |= (nb - 1u) << lo;
+            hi = lo - 1;
+            par ^= 1;
+        }
+    }
+    *thr_out = prefix;
+    *need_eq_out = rem;
+}
+
+
+// ---------------------------------------------------------------------------
+// One block per group, for groups of up to 32 Ki keys (each a handful of
+// launches' worth of work for the multi-block form below): thread t owns the
+// contiguous run [t*KPT, t*KPT + KPT) of the group's keys in registers
+// (16-byte loads in per-head mode), the radix passes histogram them into one
+// LDS copy per wave, and the ordered emission walks the registers.
+// ---------------------------------------------------------------------------
+constexpr int kRegMaxKeys = 64 * kSelThreads;
+
+template <int KPT>
+__global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
+{
+    // the radix histograms and the gathered keys live in stg
+    __shared__ uint32_t hsum[256];
+    __shared__ uint32_t bc[2][2];
+    __shared__ uint32_t wsum[2 * kSelWaves + 2];
+    __shared__ uint32_t mm[2][kSelWaves];
+    __shared__ uint32_t ccount;
+    __shared__ int64_t through[kMaxFlatHeads];
+    typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+    // 128 KiB: with KPT == 32 the stage of the coalesced score load, then of
+    // the radix histograms and gathered keys, then of the output (the
+    // barriers of the extremes and of the radix passes separate the three
+    // uses); with KPT == 64 the radix scratch only
+    __shared__ u32x4_t stg[8 * kSelThreads];
+    static_assert(kStCandCap > 0, "histograms must fit the stage");
+
+    const SelGroup grp = sel_group(a, blockIdx.x);
+    const int l = grp.l, h0 = grp.h0, s = grp.s, nh = grp.nh;
+    const int T = a.seq.cu[s + 1] - a.seq.cu[s];
+    const int P = T - a.w;
+    const int beff = grp.beff;
+    const int64_t out_base = grp.out_base;
+    int32_t *out = a.idx + out_base;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+
+    if (beff >= T) {  // keep every token
+        for (int64_t e = tid; e < (int64_t)nh * T; e += blockDim.x) out[e] = (int32_t)(e % T);
+        if (tid < nh && (a.counts || a.offsets)) {
+            const int64_t u = ((int64_t)l * a.Hkv + h0 + tid) * a.B + s;
+            if (a.counts) a.counts[u] = T;
+            if (a.offsets) a.offsets[u] = (int32_t)(out_base + (int64_t)tid * T);
+        }
+        return;
+    }
+
+    GroupView g;
+    g.base = a.scores + ((int64_t)l * a.Hkv + h0) * a.Ptot + (a.seq.cu[s] - s * a.w);
+    g.hstride = a.Ptot;
+    g.P = P;
+    g.nh = nh;
+    const int n = nh * P;  // <= KPT * kSelThreads (chosen on the host)
+    const int k = nh * (beff - a.w);
+    const int v0 = tid * KPT;
+
+    for (int h = tid; h < nh; h += blockDim.x) through[h] = 0;
+    uint32_t kk[KPT];
+    bool ext_done = false;  // the extremes are in mm (reduced with the load's barrier)
+    if (nh == 1 && KPT == 32) {
+        // Coalesced load through LDS: the block reads the group's scores as
+        // consecutive 16-byte pieces (1 KiB per wave instruction) into a
+        // swizzled stage (piece g at g ^ ((g >> 3) & 7)), then each thread takes
+        // its 32 consecutive scores from it.
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(uniform_ptr(g.base)), (short)0, uniform_i32(n) * 4, 0x00020000);
+        u32x4_t x[KPT / 4];
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q)
+            x[q] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (q * kSelThreads + tid) * 16, 0, 0));
+        // the extremes of the loaded keys (the same set as the thread's run
+        // after the stage) ride on the stage's barrier
+        uint32_t lmin = 0xffffffffu, lmax = 0u;
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if ((q * kSelThreads + tid) * 4 + e < n) {
+                    const uint32_t kv = score_key(__uint_as_float(x[q][e]));
+                    lmin = min(lmin, kv);
+                    lmax = max(lmax, kv);
+                }
+        lmin = wave_min_u(lmin);
+        lmax = wave_max_u(lmax);
+        if (lane == 0) {
+            mm[0][wv] = lmin;
+            mm[1][wv] = lmax;
+        }
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q) stg[q * kSelThreads + (tid ^ ((tid >> 3) & 7))] = x[q];
+        lds_barrier();
+        ext_done = true;
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q) {
+            const u32x4_t y = stg[(KPT / 4) * tid + (q ^ (tid & 7))];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) kk[4 * q + e] = score_key(__uint_as_float(y[e]));
+        }
+    } else if (nh == 1) {
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(uniform_ptr(g.base)), (short)0, uniform_i32(n) * 4, 0x00020000);
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q) {
+            const u32x4_t x = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (v0 + 4 * q) * 4, 0, 0));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) kk[4 * q + e] = score_key(__uint_as_float(x[e]));
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < KPT; ++q) kk[q] = v0 + q < n ? score_key(g.get(v0 + q)) : 0u;
+    }
+
+    // KPT == 32: the ordered output is assembled in LDS and written out in
+    // consecutive 4-byte pieces (instead of each thread's scattered stores)
+    uint32_t *ost = reinterpret_cast<uint32_t *>(stg);
+    const bool staged = KPT == 32 && k + nh * a.w <= KPT * kSelThreads;
+    uint32_t thr = 0xffffffffu;
+    int need_eq = 0;
+    if (k > 0) {
+        uint32_t kmin, kmax;
+        if (ext_done) {
+            kmin = mm[0][0];
+            kmax = mm[1][0];
+            for (int q = 1; q < kSelWaves; ++q) {
+                kmin = min(kmin, mm[0][q]);
+                kmax = max(kmax, mm[1][q]);
+            }
+        } else {
+            reg_extremes<KPT>(kk, v0, n, mm, &kmin, &kmax);
+        }
+        // radix select of the k-th largest key
+        reg_radix_select_staged<KPT>(kk, v0, n, k, kmin, kmax, reinterpret_cast<uint32_t *>(stg), hsum, bc, &ccount,
+                                     &thr, &need_eq);
+    }
+    if (k > 0 && nh == 1) {
+        // ordered emission of one head: bit q of gtm[c] / eqm[c] marks key
+        // v0 + 32 c + q above / equal to the threshold; the thread's taken
+        // keys go to consecutive slots from the number taken before its run
+        constexpr int NC = KPT / 32;  // 32-key words per thread
+        uint32_t gtm[NC], eqm[NC];
+        uint32_t cg = 0, ce = 0;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            gtm[c] = 0u;
+            eqm[c] = 0u;
+#pragma unroll
+            for (int q = 0; q < 32; ++q)
+                if (v0 + 32 * c + q < n) {
+                    gtm[c] |= kk[32 * c + q] > thr ? 1u << q : 0u;
+                    eqm[c] |= kk[32 * c + q] == thr ? 1u << q : 0u;
+                }
+            cg += (uint32_t)__builtin_popcount(gtm[c]);
+            ce += (uint32_t)__builtin_popcount(eqm[c]);
+        }
+        uint32_t eg, ee, tg, te;
+        block_exscan2(cg, ce, wsum, eg, ee, tg, te);
+        (void)tg;
+        (void)te;
+        // equal keys are taken in position order while fewer than need_eq precede them
+        const int eq_take = min((int)ce, max(need_eq - (int)ee, 0));
+        uint32_t take[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) take[c] = gtm[c];
+        for (int r = 0; r < eq_take; ++r) {
+            bool done = false;
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                if (!done && eqm[c]) {
+                    const uint32_t low = eqm[c] & (~eqm[c] + 1u);
+                    take[c] |= low;
+                    eqm[c] ^= low;
+                    done = true;
+                }
+        }
+        int o = (int)eg + min((int)ee, need_eq);
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+            while (take[c]) {
+                const int q = 32 * c + __builtin_ctz(take[c]);
+                take[c] &= take[c] - 1u;
+                if (staged) ost[o] = (uint32_t)(v0 + q);
+                else out[o] = v0 + q;
+                ++o;
+            }
+        if (tid == 0) through[0] = k;
+    } else if (k > 0) {
+        // ordered emission from the registers (several heads)
+        uint32_t cg = 0, ce = 0;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q)
+            if (v0 + q < n) {
+                cg += kk[q] > thr;
+                ce += kk[q] == thr;
+            }
+        uint32_t eg, ee, tg, te;
+        block_exscan2(cg, ce, wsum, eg, ee, tg, te);
+        (void)tg;
+        (void)te;
+        int gt_before = (int)eg, eq_before = (int)ee;
+        int h = nh == 1 ? 0 : (v0 < n ? v0 / P : nh);
+        int pos = v0 - h * P;
+#pragma unroll
+        for (int q = 0; q < KPT; ++q) {
+            if (v0 + q < n) {
+                const bool gt = kk[q] > thr, eq = kk[q] == thr;
+                const bool take = gt || (eq && eq_before < need_eq);
+                if (take) {
+                    const int64_t o = gt_before + min(eq_before, need_eq) + (int64_t)h * a.w;
+                    if (staged) ost[o] = (uint32_t)pos;
+                    else out[o] = pos;
+                }
+                gt_before += gt;
+                eq_before += eq;
+                if (++pos == P) {
+                    through[h] = gt_before + min(eq_before, need_eq);
+                    pos = 0;
+                    ++h;
+                }
+            }
+        }
+    }
+    __syncthreads();
+    // windows, counts and offsets
+    for (int e = tid; e < nh * a.w; e += blockDim.x) {
+        const int hh = e / a.w, j = e % a.w;
+        const int64_t o = through[hh] + (int64_t)hh * a.w + j;
+        if (staged) ost[o] = (uint32_t)(P + j);
+        else out[o] = P + j;
+    }
+    if (staged) {
+        __syncthreads();
+        for (int e = tid; e < k + nh * a.w; e += blockDim.x) out[e] = (int32_t)ost[e];
+    }
+    if (tid < nh && (a.counts || a.offsets)) {
+        const int hh = tid;
+        const int64_t prev = hh > 0 ? through[hh - 1] : 0;
+        const int64_t u = ((int64_t)l * a.Hkv + h0 + hh) * a.B + s;
+        if (a.counts) a.counts[u] = (int32_t)(through[hh] - prev + a.w);
+        if (a.offsets) a.offsets[u] = (int32_t)(out_base + prev + (int64_t)hh * a.w);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Selection over many blocks per group.  A group's n keys, in (head,
 // position) order, are cut into slices of kMbThreads * KPT keys, one block
@@ -606,13 +1066,18 @@ __device__ uint4 mb_advance(uint4 st, const uint32_t *gh, int d, uint32_t *sh)
     if (st.w) return st;
     const int nb = mb_bins(d), per = nb / kMbThreads;
     const int t = threadIdx.x;
-    // thread t: bins nb-1-per*t .. nb-per*(t+1), in descending digit order
-    uint32_t c[8], loc = 0;
+    // thread t: bins nb-1-per*t .. nb-per*(t+1), in descending digit order,
+    // read as 16-byte pieces (the histogram was completed by an earlier launch)
+    typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+    const u32x4_t *src = reinterpret_cast<const u32x4_t *>(gh + nb - per * (t + 1));
+    u32x4_t v0 = src[0], v1 = per == 8 ? src[1] : (u32x4_t){0u, 0u, 0u, 0u};
+    // descending order: the last bin of the piece first
+    uint32_t c[8] = {per == 8 ? v1[3] : v0[3], per == 8 ? v1[2] : v0[2], per == 8 ? v1[1] : v0[1],
+                     per == 8 ? v1[0] : v0[0], v0[3], v0[2], v0[1], v0[0]};
+    if (per == 4) c[4] = c[5] = c[6] = c[7] = 0u;
+    uint32_t loc = 0;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        c[q] = q < per ? __hip_atomic_load(&gh[nb - 1 - per * t - q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
-        loc += c[q];
-    }
+    for (int q = 0; q < 8; ++q) loc += c[q];
     uint32_t total;
     const uint32_t before = mb_exscan(loc, sh, &total);
     const uint32_t rem = st.z;
@@ -679,16 +1144,17 @@ __global__ __launch_bounds__(kMbThreads) void k_sel_digit(SelectArgs a)
     if (g.sg.beff >= g.T || g.k <= 0) return;
     const int ns = mb_slices<KPT>(g);
     if (j >= ns) return;
-    const uint4 st = mb_state<DIG>(a, gi, j, g.k, sh);
-    if (DIG == 2) mb_clear(a, gi, j, ns, 0);  // digit 0's histogram: its last reader was the previous launch
-    if (st.w) return;
-    const int nb = mb_bins(DIG), lo = mb_lo(DIG);
     const int t = threadIdx.x, wv = t >> 6;
-    for (int b = t; b < kMbWaves * 2048; b += kMbThreads) (&hist[0][0])[b] = 0u;
+    // the keys first, so that their loads overlap those of the state and histogram
     const int64_t r0 = (int64_t)j * kMbThreads * KPT + (int64_t)t * KPT;
     uint32_t kk[KPT];
     int hh, ii;
     if (r0 < g.n) mb_load<KPT>(g, r0, kk, hh, ii);
+    const uint4 st = mb_state<DIG>(a, gi, j, g.k, sh);
+    if (DIG == 2) mb_clear(a, gi, j, ns, 0);  // digit 0's histogram: its last reader was the previous launch
+    if (st.w) return;
+    const int nb = mb_bins(DIG), lo = mb_lo(DIG);
+    for (int b = t; b < kMbWaves * 2048; b += kMbThreads) (&hist[0][0])[b] = 0u;
     __syncthreads();
     if (r0 < g.n) {
 #pragma unroll
@@ -717,16 +1183,16 @@ __global__ __launch_bounds__(kMbThreads) void k_sel_count(SelectArgs a)
     if (g.sg.beff >= g.T || g.k <= 0) return;
     const int ns = mb_slices<KPT>(g);
     if (j >= ns) return;
-    const uint4 st = mb_state<3>(a, gi, j, g.k, sh);
-    mb_clear(a, gi, j, ns, 1);  // digit 1's histogram: last read by the previous launch
     const int t = threadIdx.x;
-    const bool flat = g.sg.nh > 1;
-    if (flat)
-        for (int h = t; h < g.sg.nh; h += kMbThreads) hc[h][0] = hc[h][1] = 0u;
     const int64_t r0 = (int64_t)j * kMbThreads * KPT + (int64_t)t * KPT;
     uint32_t kk[KPT];
     int h = 0, i = 0;
-    if (r0 < g.n) mb_load<KPT>(g, r0, kk, h, i);
+    if (r0 < g.n) mb_load<KPT>(g, r0, kk, h, i);  // (overlaps the state's loads)
+    const uint4 st = mb_state<3>(a, gi, j, g.k, sh);
+    mb_clear(a, gi, j, ns, 1);  // digit 1's histogram: last read by the previous launch
+    const bool flat = g.sg.nh > 1;
+    if (flat)
+        for (int hh = t; hh < g.sg.nh; hh += kMbThreads) hc[hh][0] = hc[hh][1] = 0u;
     __syncthreads();
     uint32_t cg = 0, ce = 0, hg = 0, he = 0;
     if (r0 < g.n) {
@@ -866,9 +1332,9 @@ __global__ __launch_bounds__(kMbThreads) void k_sel_emit(SelectArgs a)
         const uint4 st = g.k > 0 ? a.mb_state[2 * (int64_t)a.mb_groups + gi] : uint4{0u, 0u, 0u, 0u};
         uint32_t *gc = a.mb_head + (int64_t)gi * kMaxFlatHeads * 2;
         uint32_t hgt = 0, heq = 0;
-        if (t < nh && g.k > 0) {
-            hgt = __hip_atomic_load(&gc[2 * t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            heq = __hip_atomic_load(&gc[2 * t + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (t < nh && g.k > 0) {  // (completed by the count launch)
+            hgt = gc[2 * t];
+            heq = gc[2 * t + 1];
         }
         uint32_t tot;
         const int64_t g_incl = (int64_t)mb_exscan(hgt, sh, &tot) + hgt;
@@ -934,6 +1400,14 @@ hipError_t select_launch(SelectArgs a, char *ws, hipStream_t st)
     for (int s = 0; s < a.B; ++s) {
         const int64_t P = (int64_t)(a.seq.cu[s + 1] - a.seq.cu[s]) - a.w;
         maxn = max(maxn, P * (a.flat ? a.Hkv : 1));
+    }
+    if (maxn <= 32 * kSelThreads) {
+        // one block per group: for groups this small, one launch beats five
+        // short ones (28-layer stack, 112 groups of 32764 keys: 29 against 46 us;
+        // one layer, 4 groups: 25 against 33 us)
+        ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select_reg<32>, dim3((unsigned)groups), dim3(kSelThreads), 0,
+                                                     st, a));
+        return hipGetLastError();
     }
     const SelWsLayout lay = select_ws_layout(a.mb_groups, a.mb_maxn);
     a.mb_state = reinterpret_cast<uint4 *>(ws + lay.state);

@@ -122,7 +122,7 @@ def _mllm_unit_keys(rng, T, D, n_visual, group, sigmas, offset):
 
 
 def _gqa_generate(name, seed, L, Hq, Hkv, D, w, seqlens, dtype, budget, mode,
-                  visual_frac, group, sigma_fn, strength_fn, meta):
+                  visual_frac, group, sigma_fn, strength_fn, meta, query_offset=True):
     """Generic generator for the MLLM-shaped configurations."""
     B = len(seqlens)
     cu = [0]
@@ -149,7 +149,9 @@ def _gqa_generate(name, seed, L, Hq, Hkv, D, w, seqlens, dtype, budget, mode,
         rv = _rng(seed, _TAG_V, l, h, s)
         V[l, h, cu[s]:cu[s + 1]] = _encode(rv.standard_normal((T, D), dtype=np.float32), dtype)
         rq = _rng(seed, _TAG_Q, l, h, s)
-        Qg = rq.standard_normal((G, w, D), dtype=np.float32) + off[None, None, :]
+        Qg = rq.standard_normal((G, w, D), dtype=np.float32)
+        if query_offset:
+            Qg += off[None, None, :]
         Q[l, h * G:(h + 1) * G, s] = _encode(Qg, dtype)
 
     units = [(l, h, s) for l in range(L) for h in range(Hkv) for s in range(B)]
@@ -265,14 +267,17 @@ def varlen(seed: int = 4, nseq: int = 8, tmin: int = 4096, tmax: int = 32768,
 def custom(seed: int, L: int, Hq: int, Hkv: int, D: int, w: int, seqlens: List[int],
            dtype: str = "bf16", budget: Optional[List[int]] = None, mode: str = "per_head",
            visual_frac: float = 0.75, group: int = 256, sigma: float = 0.1,
-           strength: float = 1.5) -> Workload:
-    """Any shape with the MLLM recipe (used for ragged / edge-case parity tests)."""
+           strength: float = 1.5, query_offset: bool = True) -> Workload:
+    """Any shape with the MLLM recipe (used for ragged / edge-case parity tests).
+    With query_offset False the window queries are plain N(0, I) draws instead
+    of sharing the keys' offset: with a strong offset the keys then share a
+    common direction while the window logits stay of ordinary size."""
     if budget is None:
         budget = [max(w, int(0.2 * t)) for t in seqlens]
     return _gqa_generate("custom", seed, L, Hq, Hkv, D, w, list(seqlens), dtype, budget, mode,
                          visual_frac, group, lambda r, n: np.full(n, sigma), lambda r: strength,
                          {"visual_frac": visual_frac, "group": group, "sigma": sigma,
-                          "strength": strength})
+                          "strength": strength, "query_offset": query_offset}, query_offset=query_offset)
 
 
 CONFIG_BUILDERS = {
