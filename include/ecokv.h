@@ -223,6 +223,21 @@ int ecokv_score_pre(const void *K, const void *V, const void *Q_win, int dtype, 
                     const ecokv_params *params, const float *pre, float *scores, float *lambda, float *stats,
                     void *workspace, size_t workspace_bytes, void *stream);
 
+/* ecokv_score_pre for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops, harnesses that forbid it): no
+ * workspace argument.  Its scratch is a 96 MiB device array that the library
+ * holds on every device it runs on until the process ends, shared by all
+ * calls on that device: calls that may overlap on one device race.  A call
+ * whose scratch (ecokv_workspace_size for its shape) would exceed 96 MiB is
+ * refused with ECOKV_EWORKSPACE before anything is enqueued (the 28-layer,
+ * 4-KV-head, 32768-token stack needs 77 MiB).  The final step runs one block
+ * per (layer, KV head, sequence), so no block waits for another and there is
+ * no status to query.  The current device must be the stream's device.  No
+ * allocation, no memset, no synchronisation. */
+int ecokv_score_noalloc(const void *K, const void *V, const void *Q_win, int dtype, const ecokv_shape *shape,
+                        const ecokv_params *params, const float *pre, float *scores, float *lambda, float *stats,
+                        void *stream);
+
 /* Number of int32 entries ecokv_select writes to idx:
  * L * H_kv * sum_s min(budget[s], T_s) (ECOKV_PER_HEAD and ECOKV_LAYER_FLAT). */
 int ecokv_index_count(const ecokv_shape *shape, const int32_t *budget, int64_t *count);

@@ -215,6 +215,54 @@ int select_workspace(const ShapeInfo &si, const ecokv_shape *shape, int mode, vo
     return ECOKV_OK;
 }
 
+int score_impl(const void *K, const void *V, const void *Q_win, int dtype, const ecokv_shape *shape,
+               const ecokv_params *params, const float *pre, float *scores, float *lambda, float *stats,
+               void *workspace, size_t workspace_bytes, void *stream, bool noalloc);
+
+// Scratch of ecokv_score_noalloc: a file-scope device array, one copy on
+// every device the library runs on, kept until the process ends.  In host
+// code `scratch` names a host-side stand-in, not device memory: its device
+// address comes from hipGetSymbolAddress, taken once per device (with that
+// device current) on the entry point's first call there and kept here.
+constexpr size_t kNoAllocBytes = (size_t)96 << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices];
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+namespace {
+
+// The scratch's device address on the current device, which must be the
+// stream's device.
+int noalloc_scratch(hipStream_t stream, void **out)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "ecokv_score_noalloc: hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(ECOKV_EUNSUPPORTED, "ecokv_score_noalloc: device %d", dev);
+    if (stream) {
+        hipDevice_t sdev = -1;
+        if ((e = hipStreamGetDevice(stream, &sdev)) != hipSuccess)
+            return hip_fail(e, "ecokv_score_noalloc: hipStreamGetDevice");
+        if ((int)sdev != dev)
+            return fail(ECOKV_EINVAL, "ecokv_score_noalloc: the stream belongs to device %d, device %d is current",
+                        (int)sdev, dev);
+    }
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess)
+            return hip_fail(e, "ecokv_score_noalloc: hipGetSymbolAddress");
+        if (!p || ((uintptr_t)p & 255u) != 0) return fail(ECOKV_EHIP, "ecokv_score_noalloc: bad scratch address");
+        g_scratch[dev] = p;
+    }
+    *out = g_scratch[dev];
+    return ECOKV_OK;
+}
+
 }  // namespace
 
 namespace ecokv {
@@ -349,6 +397,29 @@ int ecokv_score_pre(const void *K, const void *V, const void *Q_win, int dtype, 
                     const ecokv_params *params, const float *pre, float *scores, float *lambda, float *stats,
                     void *workspace, size_t workspace_bytes, void *stream)
 {
+    return score_impl(K, V, Q_win, dtype, shape, params, pre, scores, lambda, stats, workspace, workspace_bytes,
+                      stream, false);
+}
+
+int ecokv_score_noalloc(const void *K, const void *V, const void *Q_win, int dtype, const ecokv_shape *shape,
+                        const ecokv_params *params, const float *pre, float *scores, float *lambda, float *stats,
+                        void *stream)
+{
+    void *ws = nullptr;
+    const int rc = noalloc_scratch(static_cast<hipStream_t>(stream), &ws);
+    if (rc) return rc;
+    return score_impl(K, V, Q_win, dtype, shape, params, pre, scores, lambda, stats, ws, kNoAllocBytes, stream,
+                      true);
+}
+
+}  // extern "C"
+
+namespace {
+
+int score_impl(const void *K, const void *V, const void *Q_win, int dtype, const ecokv_shape *shape,
+               const ecokv_params *params, const float *pre, float *scores, float *lambda, float *stats,
+               void *workspace, size_t workspace_bytes, void *stream, bool noalloc)
+{
     ShapeInfo si;
     int rc = check_shape(shape, &si);
     if (rc) return rc;
@@ -365,7 +436,10 @@ int ecokv_score_pre(const void *K, const void *V, const void *Q_win, int dtype, 
     if (!workspace) return fail(ECOKV_EINVAL, "workspace is NULL");
     if (((uintptr_t)workspace & 255u) != 0) return fail(ECOKV_EINVAL, "workspace must be 256-byte aligned");
     if (workspace_bytes < lay.total)
-        return fail(ECOKV_EWORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
+        return noalloc ? fail(ECOKV_EWORKSPACE,
+                              "ecokv_score_noalloc: this call needs %zu bytes of scratch, the library holds %zu "
+                              "per device; split it (fewer layers per call)", lay.total, workspace_bytes)
+                       : fail(ECOKV_EWORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
 
     ecokv::ScoreArgs a;
     memset(&a, 0, sizeof a);
@@ -407,12 +481,17 @@ int ecokv_score_pre(const void *K, const void *V, const void *Q_win, int dtype, 
     // lowers it so that tests can make a wait give up (every kernel still ends)
     a.spin_limit = 1 << 20;
     if (const char *sl = getenv("ECOKV_SPIN_LIMIT")) a.spin_limit = atoi(sl);
+    a.no_wait = noalloc ? 1 : 0;  // (its final step runs one block per unit: no waits, no status word)
     if ((rc = fill_seqtab(shape, nullptr, si.w, &a.seq, nullptr))) return rc;
     const hipError_t e = ecokv::score_launch(a, static_cast<char *>(workspace), lay, si.maxT,
                                              static_cast<hipStream_t>(stream), dtype == ECOKV_BF16);
     if (e != hipSuccess) return hip_fail(e, "ecokv_score launch");
     return ECOKV_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 int ecokv_workspace_status(void *workspace, void *stream)
 {

@@ -56,6 +56,7 @@ struct ScoreArgs {
     unsigned *status;           // workspace status word: set to the launch tag if a wait ran out of time
     unsigned tag;               // launch tag (never 0)
     int spin_limit;             // polls of a bounded wait before it gives up (<= 0: give up at once)
+    int no_wait;                // no waits between blocks (the final step one block per unit)
     int L, Hq, Hkv, G, D, w, R, B;
     int64_t Ttot, Ptot;
     int nch1;        // sweep blocks per unit (for the longest sequence)

@@ -2009,7 +2009,7 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     if (maxT - a.w <= kUKeys && a.pool_half <= kPoolHalfMax && (maxT + a.rpb2 - 1) / a.rpb2 <= kUThreads && a.D <= kUThreads) {
         // two blocks per unit when all of them can be resident at once (their
         // exchange waits for each other; four per unit measured no faster), else one
-        if (2 * (int64_t)U <= epi_split_capacity()) {
+        if (!a.no_wait && 2 * (int64_t)U <= epi_split_capacity()) {
             a.epiT = reinterpret_cast<unsigned long long *>(ws + lay.epiT);
             a.tag = launch_tag();
             ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL(k_epi_unit<2>, dim3(2 * U), dim3(kUThreads), 0, st, a));

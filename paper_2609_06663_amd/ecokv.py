@@ -30,7 +30,7 @@ STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7, imp_m
             mu_norm2=10, scale=11)
 
 EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_workspace_status", "ecokv_score", "ecokv_score_v",
-           "ecokv_score_pre",
+           "ecokv_score_pre", "ecokv_score_noalloc",
            "ecokv_index_count",
            "ecokv_index_count_mode", "ecokv_select_workspace_size", "ecokv_select", "ecokv_compact",
            "ecokv_pyramid_budgets",
@@ -121,6 +121,7 @@ def _load():
     lib.ecokv_score.argtypes = [vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_score_v.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_score_pre.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.ecokv_score_noalloc.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, vp]
     lib.ecokv_index_count.argtypes = [sp, i32p, ctypes.POINTER(ctypes.c_int64)]
     lib.ecokv_index_count_mode.argtypes = [sp, ctypes.c_int, i32p, ctypes.POINTER(ctypes.c_int64)]
     lib.ecokv_decode_workspace_size.argtypes = [sp, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
@@ -305,6 +306,32 @@ def ecokv_score_pre(K: torch.Tensor, V: Optional[torch.Tensor], Q_win: torch.Ten
         raise TypeError("pre is float32")
     a = _score_args(K, V, Q_win, shape, p, scores, lambda_, stats, workspace, stream, pre=pre)
     _check(lib.ecokv_score_pre(*a))
+
+
+def ecokv_score_noalloc(K: torch.Tensor, V: Optional[torch.Tensor], Q_win: torch.Tensor, shape: Shape,
+                        params: Optional[Params], pre: Optional[torch.Tensor], scores: torch.Tensor,
+                        lambda_: Optional[torch.Tensor] = None, stats: Optional[torch.Tensor] = None,
+                        stream=None) -> None:
+    """Enqueue ecokv_score_noalloc: ecokv_score_pre (pre may be None) with the
+    library's own per-device scratch; nothing is allocated here either."""
+    p = params or Params()
+    if pre is not None and pre.dtype != torch.float32:
+        raise TypeError("pre is float32")
+    if shape.c.num_layers == 0:
+        return
+    dev = K.device
+    kp = _arg(K, "K", _KV_TYPES, shape.kv_numel(), dev)
+    if Q_win.dtype != K.dtype or (V is not None and V.dtype != K.dtype):
+        raise TypeError("K, V and Q_win must have the same element type")
+    vp = _arg(V, "V", _KV_TYPES, shape.kv_numel(), dev, optional=p.imp_mode != IMP_ATTN_VNORM)
+    qp = _arg(Q_win, "Q_win", _KV_TYPES, shape.q_numel(), dev)
+    R = shape.c.num_q_heads // shape.c.num_kv_heads * shape.c.window
+    prp = _arg(pre, "pre", _F32, shape.units * (2 * shape.c.head_dim + 2 * R), dev, optional=True)
+    _check(lib.ecokv_score_noalloc(kp, vp, qp, _dtype_code(K), ctypes.byref(shape.c), ctypes.byref(p), prp,
+                                   _arg(scores, "scores", _F32, shape.score_numel(), dev),
+                                   _arg(lambda_, "lambda", _F32, shape.units, dev, optional=True),
+                                   _arg(stats, "stats", _F32, shape.units * NSTATS, dev, optional=True),
+                                   _stream(stream)))
 
 
 def ecokv_workspace_status(workspace: torch.Tensor, stream=None) -> None:
