@@ -121,6 +121,10 @@ def lib():
                                  ctypes.c_int, i32p, i32p, i32p, ctypes.c_int]
         L.ora_compact.argtypes = [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, i32p,
                                   ctypes.c_int, i32p, i32p, i32p, vp, vp]
+        L.ora_prefill_unit.argtypes = [vp, vp, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                       ctypes.c_int, ctypes.c_int, ctypes.c_int, dp]
+        L.ora_prefill_sums.argtypes = [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                       ctypes.c_int, i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, dp, ctypes.c_int]
         L.ora_decode.argtypes = [vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                  ctypes.c_int, i32p, i32p, dp, dp]
         _lib = L
@@ -206,6 +210,40 @@ def score(K, Q, L, Hq, Hkv, cu_seqlens, D, w, params: Optional[Params] = None, n
     if rc != 0:
         raise ValueError(f"oracle rejected the shape (rc={rc})")
     return S, stats
+
+
+def prefill_unit(K: np.ndarray, Q: np.ndarray, w: int, causal: bool = True) -> np.ndarray:
+    """The first sweep's results of one unit as a prefill hands them to the
+    pass: [2D + 2R] = sum k, sum k/|k|, per window row r = g w + j the largest
+    visible logit q.k/sqrt(D) and the sum of exp(logit - largest).
+    K: [T, D], Q: [G, w, D] (uint16 bf16 bits or float32)."""
+    K = np.ascontiguousarray(K)
+    Q = np.ascontiguousarray(Q)
+    code = _dtype_code(K)
+    assert _dtype_code(Q) == code and K.ndim == 2 and Q.ndim == 3 and Q.shape[1] == w
+    T, D = K.shape
+    G = Q.shape[0]
+    out = np.zeros(2 * D + 2 * G * w, np.float64)
+    rc = lib().ora_prefill_unit(K.ctypes.data, Q.ctypes.data, w * D, code, T, D, G, w, int(bool(causal)), _dp(out))
+    if rc != 0:
+        raise ValueError(f"oracle rejected the unit (rc={rc})")
+    return out
+
+
+def prefill_sums(K, Q, L, Hq, Hkv, cu_seqlens, D, w, causal: bool = True, nthreads: int = 1) -> np.ndarray:
+    """prefill_unit over every unit: K [L][Hkv][Ttot][D], Q [L][Hq][B][w][D];
+    returns [L][Hkv][B][2D + 2R] (float64)."""
+    K = np.ascontiguousarray(K)
+    Q = np.ascontiguousarray(Q)
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    B = len(cu) - 1
+    R = (Hq // Hkv) * w
+    out = np.zeros((L, Hkv, B, 2 * D + 2 * R), np.float64)
+    rc = lib().ora_prefill_sums(K.ctypes.data, Q.ctypes.data, _dtype_code(K), L, Hq, Hkv, B, _ip(cu), D, w,
+                                int(bool(causal)), _dp(out), nthreads)
+    if rc != 0:
+        raise ValueError(f"oracle rejected the shape (rc={rc})")
+    return out
 
 
 def select_unit(S: np.ndarray, T: int, w: int, b: int) -> np.ndarray:

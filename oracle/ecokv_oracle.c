@@ -14,6 +14,8 @@
  *   - rescaled diversity and final score S (Sec. 5.2, Eq. (7));
  *   - top-k over the non-window tokens plus the whole window (Sec. 3),
  *     per head or flattened across the heads of a layer (AdaKV, Appendix A.1);
+ *   - the first sweep's key sums and window softmax statistics in the form a
+ *     prefill can hand them over (ora_prefill_unit);
  *   - gather of the kept K/V rows;
  *   - decode attention of one new query per head over the kept rows (the
  *     generation step that reads the compressed cache, Sec. 3).
@@ -527,6 +529,95 @@ int ora_score(const void *K, const void *Q, int dtype, int L, int Hq, int Hkv, i
               double *S, double *stats, int nthreads)
 {
     return ora_score_v(K, NULL, Q, dtype, L, Hq, Hkv, B, cu, D, w, p, S, stats, nthreads);
+}
+
+/* ---------------------------------------------------------------------------
+ * The first sweep's results for one unit, in the form a prefill hands them
+ * to the pass (what the KV-cache write and the window rows of the prefill's
+ * attention can produce as it runs), pre[2D + 2R]:
+ *   [0, D)          sum over the T keys of k_i (the centroid of Eq. (1)
+ *                   before its division by T);
+ *   [D, 2D)         sum over the T keys of k_i / |k_i| (the mean normalised
+ *                   key mu of the cosine term, Appendix A.1, before its
+ *                   division by T; a zero key counts as zero, as above);
+ *   [2D + r]        for window row r = g w + j (query head g of the group,
+ *                   window position j): the largest q.k / sqrt(D) over the
+ *                   keys that row sees (Sec. 3 attention; keys 0 .. P + j
+ *                   when causal, all T otherwise);
+ *   [2D + R + r]    the sum over those keys of exp(q.k / sqrt(D) - largest).
+ * Returns 0, or -1 on invalid sizes.
+ * ------------------------------------------------------------------------- */
+int ora_prefill_unit(const void *K, const void *Q, size_t q_gstride, int dtype, int T, int D, int G, int w,
+                     int causal, double *pre)
+{
+    if (T < 2 || w < 1 || w >= T || D < 1 || G < 1) return -1;
+    const int R = G * w, P = T - w;
+    const double inv_sqrt_d = 1.0 / sqrt((double)D);
+    for (int c = 0; c < 2 * D + 2 * R; ++c) pre[c] = 0.0;
+    for (int i = 0; i < T; ++i) {
+        double n2 = 0.0;
+        for (int d = 0; d < D; ++d) {
+            const double x = ora_get(K, dtype, (size_t)i * D + d);
+            n2 += x * x;
+        }
+        const double nrm = fmax(sqrt(n2), 1e-12);
+        for (int d = 0; d < D; ++d) {
+            const double x = ora_get(K, dtype, (size_t)i * D + d);
+            pre[d] += x;
+            pre[D + d] += x / nrm;
+        }
+    }
+    double *lg = malloc((size_t)T * sizeof(double));
+    if (!lg) return -2;
+    for (int g = 0; g < G; ++g) {
+        for (int j = 0; j < w; ++j) {
+            const size_t qoff = (size_t)g * q_gstride + (size_t)j * D;
+            const int seen = causal ? P + j : T - 1;  /* last key the row sees */
+            double m = -INFINITY;
+            for (int i = 0; i <= seen; ++i) {
+                double dot = 0.0;
+                for (int d = 0; d < D; ++d) dot += ora_get(Q, dtype, qoff + d) * ora_get(K, dtype, (size_t)i * D + d);
+                lg[i] = dot * inv_sqrt_d;
+                m = fmax(m, lg[i]);
+            }
+            double z = 0.0;
+            for (int i = 0; i <= seen; ++i) z += exp(lg[i] - m);
+            pre[2 * D + g * w + j] = m;
+            pre[2 * D + R + g * w + j] = z;
+        }
+    }
+    free(lg);
+    return 0;
+}
+
+/* ora_prefill_unit over every unit; K, Q laid out as for ora_score_v,
+ * pre [L][Hkv][B][2D + 2R]. */
+int ora_prefill_sums(const void *K, const void *Q, int dtype, int L, int Hq, int Hkv, int B, const int32_t *cu,
+                     int D, int w, int causal, double *pre, int nthreads)
+{
+    if (L < 0 || Hkv < 1 || Hq % Hkv != 0 || B < 1) return -1;
+    const int G = Hq / Hkv;
+    const int64_t Ttot = cu[B];
+    const size_t es = dtype == ORA_BF16 ? 2 : 4;
+    const size_t width = (size_t)2 * D + (size_t)2 * G * w;
+    const int64_t U = (int64_t)L * Hkv * B;
+    int bad = 0;
+#ifdef _OPENMP
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads > 0 ? nthreads : 1) reduction(|| : bad)
+#endif
+    for (int64_t u = 0; u < U; ++u) {
+        const int s = (int)(u % B);
+        const int h = (int)((u / B) % Hkv);
+        const int l = (int)(u / ((int64_t)B * Hkv));
+        const int T = cu[s + 1] - cu[s];
+        const size_t krow = ((size_t)l * Hkv + h) * (size_t)Ttot + (size_t)cu[s];
+        const char *Ku = (const char *)K + krow * (size_t)D * es;
+        const char *Qu = (const char *)Q + ((((size_t)l * Hq + (size_t)h * G) * B + s) * (size_t)w * D) * es;
+        if (ora_prefill_unit(Ku, Qu, (size_t)B * w * D, dtype, T, D, G, w, causal, pre + (size_t)u * width) != 0)
+            bad = 1;
+    }
+    (void)nthreads;
+    return bad ? -1 : 0;
 }
 
 /* idx layout: PER_HEAD -- unit (l, h, s) owns min(b_s, T_s) entries, units in

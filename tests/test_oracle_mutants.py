@@ -33,6 +33,12 @@ MUTANTS = [
      "for (int t = -half; t <= half; ++t)\n            if (i + t >= 0 && i + t < P) acc += a[i + t];",
      "for (int t = -half; t < half; ++t)\n            if (i + t >= 0 && i + t < P) acc += a[i + t];"),
     ("value_norm_squared", "imp[i] *= sqrt(n2);", "imp[i] *= n2;"),
+    # first-sweep results handed over by a prefill (Eq. (1), App. A.1, Sec. 3)
+    ("prefill_logit_scale_dropped", "lg[i] = dot * inv_sqrt_d;", "lg[i] = dot;"),
+    ("prefill_causal_row_short", "const int seen = causal ? P + j : T - 1;", "const int seen = causal ? P + j - 1 : T - 1;"),
+    ("prefill_khat_unnormalised", "pre[D + d] += x / nrm;", "pre[D + d] += x;"),
+    ("prefill_sum_not_shifted", "z += exp(lg[i] - m);", "z += exp(lg[i]);"),
+    ("prefill_rows_transposed", "pre[2 * D + g * w + j] = m;", "pre[2 * D + j * G + g] = m;"),
     # anchors and geometry (Eq. (1), App. A.1)
     ("kbar_over_prefix_count", "        kbar[d] /= (double)T;\n        mu[d] /= (double)T;",
      "        kbar[d] /= (double)(T - 1);\n        mu[d] /= (double)T;"),

@@ -817,3 +817,87 @@ def test_decode_matches_torch_attention_and_logsumexp(ora):
                 np.testing.assert_allclose(O[l, q, s], ref.numpy(), rtol=1e-12, atol=1e-14)
                 x = (k @ qq).numpy() / np.sqrt(D)
                 assert lse[l, q, s] == pytest.approx(logsumexp(x), rel=1e-13)
+
+
+# --------------------------------------------------------------------------
+# the first sweep's results as a prefill hands them over: key sums (Eq. (1);
+# Appendix A.1 mu) and window softmax statistics (Sec. 3 attention)
+# --------------------------------------------------------------------------
+
+def test_prefill_sums_of_identical_keys(ora):
+    # every key is v: sum k = T v and sum k/|k| = T v/|v|; every logit of a
+    # row is q.v/sqrt(D), so that is its max, and the sum of exp(logit - max)
+    # counts the keys the row sees (P + j + 1 causal, all T otherwise)
+    T, D, G, w = 29, 16, 3, 4
+    K = f32(np.tile(np.linspace(-1.5, 2.0, D), (T, 1)))
+    Q = f32(np.random.default_rng(3).standard_normal((G, w, D)))
+    v = K[0].astype(np.float64)
+    P, R = T - w, G * w
+    for causal in (True, False):
+        pre = ora.prefill_unit(K, Q, w, causal)
+        assert pre.shape == (2 * D + 2 * R,)
+        np.testing.assert_allclose(pre[:D], T * v, rtol=1e-13)
+        np.testing.assert_allclose(pre[D:2 * D], T * v / math.sqrt(float(v @ v)), rtol=1e-13)
+        for g in range(G):
+            for j in range(w):
+                r = g * w + j
+                qv = float(Q[g, j].astype(np.float64) @ v) / math.sqrt(D)
+                assert pre[2 * D + r] == pytest.approx(qv, rel=1e-12, abs=1e-12)
+                assert pre[2 * D + R + r] == pytest.approx(P + j + 1 if causal else T, rel=1e-12)
+
+
+def test_prefill_zero_key_adds_no_direction(ora):
+    # a zero key counts as zero in sum k/|k| (its norm is floored, not divided by)
+    T, D, w = 12, 8, 2
+    K = f32(np.tile(np.arange(1, D + 1, dtype=np.float64), (T, 1)))
+    K[5] = 0.0
+    Q = f32(np.zeros((1, w, D)))
+    pre = ora.prefill_unit(K, Q, w)
+    v = K[0].astype(np.float64)
+    np.testing.assert_allclose(pre[D:2 * D], (T - 1) * v / np.linalg.norm(v), rtol=1e-13)
+    np.testing.assert_allclose(pre[:D], (T - 1) * v, rtol=1e-13)
+    # zero queries: every visible logit is 0
+    np.testing.assert_array_equal(pre[2 * D:2 * D + w], 0.0)
+    np.testing.assert_allclose(pre[2 * D + w:], [T - w + j + 1 for j in range(w)], rtol=1e-13)
+
+
+def test_prefill_window_statistics_are_a_logsumexp(ora):
+    # max + log(sum) is the log-sum-exp of the row's visible logits (scipy's
+    # routine), and the max term alone contributes 1 to the sum
+    from scipy.special import logsumexp
+    T, D, G, w = 45, 32, 2, 5
+    K, Q = rand_unit(4, T, D, G, w, scale=2.0)
+    P, R = T - w, G * w
+    Kd = K.astype(np.float64)
+    for causal in (True, False):
+        pre = ora.prefill_unit(K, Q, w, causal)
+        for g in range(G):
+            for j in range(w):
+                r = g * w + j
+                x = Kd[:(P + j + 1) if causal else T] @ Q[g, j].astype(np.float64) / math.sqrt(D)
+                assert pre[2 * D + r] + math.log(pre[2 * D + R + r]) == pytest.approx(logsumexp(x), rel=1e-12)
+                assert 1.0 <= pre[2 * D + R + r] <= len(x)
+
+
+def test_prefill_sums_are_the_score_anchors_times_T(ora):
+    # the score's own centroid and mu (its trace) are these sums over T
+    T, D, G, w = 60, 16, 2, 3
+    K, Q = rand_unit(5, T, D, G, w, offset=0.7)
+    pre = ora.prefill_unit(K, Q, w)
+    tr = ora.score_unit(K, Q, w, trace=True)
+    np.testing.assert_allclose(pre[:D] / T, tr["kbar"], rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(pre[D:2 * D] / T, tr["mu"], rtol=1e-12, atol=1e-15)
+    mu = pre[D:2 * D] / T
+    assert float(mu @ mu) == pytest.approx(tr["stats"][S_["mu_norm2"]], rel=1e-12)
+
+
+def test_prefill_sums_driver_layout(ora):
+    # the whole-tensor form takes unit (l, h, s) from the same places as the score
+    wl = W.custom(6, 2, 4, 2, 16, 3, [20, 33], dtype="f32")
+    pre = ora.prefill_sums(wl.K, wl.Q, wl.L, wl.Hq, wl.Hkv, wl.cu_seqlens, wl.D, wl.w)
+    cu, G = wl.cu_seqlens, wl.Hq // wl.Hkv
+    for l in range(wl.L):
+        for h in range(wl.Hkv):
+            for s in range(len(cu) - 1):
+                want = ora.prefill_unit(wl.K[l, h, cu[s]:cu[s + 1]], wl.Q[l, h * G:(h + 1) * G, s], wl.w)
+                np.testing.assert_array_equal(pre[l, h, s], want)
