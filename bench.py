@@ -343,41 +343,72 @@ def main():
             alternatives["dquant_mad_us"] = round(st_a["dquant"][0] / st_a["dquant"][1] * 1e3, 2)
         del ws_a
 
-    # The pass with the first sweep's sums supplied (as a prefill's attention
-    # epilogue and KV-cache write can produce them): K is read once.  The sums
-    # are prepared here in fp32 torch outside the timed region.
-    log("pass with prefill-supplied first-sweep sums")
+    # The pass with the first sweep's results handed over by the prefill's
+    # KV-cache write (ecokv_prefill_write): the new K and V rows arrive
+    # token-major, as a projection writes them, and the producer moves them
+    # into the head-major cache while it accumulates the key sums and the
+    # window rows' softmax statistics; the pass then reads K once.  The
+    # producer's cost beyond a plain cache write is measured against the
+    # library's own copy of V in the same call (the same rows moved the same
+    # way, without the sweep) and against torch's transposing copy.
+    log("prefill cache write with the first sweep, then the pass reading K once")
     G_, R_ = Hq // Hkv, (Hq // Hkv) * w
-    with torch.no_grad():
-        Kf = K.view(L * Hkv, T, D).float()
-        ksum = Kf.sum(dim=1)
-        khsum = (Kf / Kf.norm(dim=2, keepdim=True).clamp_min(1e-12)).sum(dim=1)
-        Qr = Q.view(L * Hkv, R_, D).float()
-        x = torch.bmm(Qr, Kf.transpose(1, 2).contiguous()) / float(D) ** 0.5   # [L*Hkv, R, T]
-        vis = torch.arange(T, device=dev)[None, :] <= (T - w + torch.arange(R_, device=dev) % w)[:, None]
-        x = x.masked_fill(~vis[None], float("-inf"))
-        mx = x.max(dim=2).values
-        se = torch.exp(x - mx[:, :, None]).sum(dim=2)
-        pre = torch.cat([ksum, khsum, mx, se], dim=1).contiguous()
-        del Kf, x, Qr, vis
-    ep.run(K, V, Q, pre=pre)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
+    U_ = L * Hkv
+    Kn = K.transpose(1, 2).contiguous()  # [L][T][Hkv][D]
+    Vn = V.transpose(1, 2).contiguous()
+    Kc_, Vc_ = torch.empty_like(K), torch.empty_like(V)
+    pre = torch.empty(U_ * (2 * D + 2 * R_), dtype=torch.float32, device=dev)
+    ws_p = torch.empty(P.ecokv_prefill_workspace_size(shape), dtype=torch.uint8, device=dev)
+
+    def producer():
+        P.ecokv_prefill_write(Kn, Vn, Q, shape, P.Params(), Kc_, Vc_, pre, ws_p)
+
+    def plain_write():
+        Kc_.view(L, Hkv, T, D).copy_(Kn.view(L, T, Hkv, D).transpose(1, 2))
+        Vc_.view(L, Hkv, T, D).copy_(Vn.view(L, T, Hkv, D).transpose(1, 2))
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    ms_plain = timed(plain_write, args.steps)
+    ms_prod = timed(producer, args.steps)
+    assert torch.equal(Kc_, K) and torch.equal(Vc_, V), "the producer's cache differs from the rows it was given"
+    os.environ["ECOKV_STAGE_TIMING"] = "1"
+    P.ecokv_stage_times()
     for _ in range(args.steps):
-        ep.run(K, V, Q, pre=pre)
-    e1.record(stream)
+        producer()
     torch.cuda.synchronize()
-    ms_pre = e0.elapsed_time(e1) / args.steps
-    e0.record(stream)
-    for _ in range(args.steps):
-        ep.score(K, Q, pre=pre)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    with_pre = {"ms_per_step": round(ms_pre, 4), "score_ms": round(e0.elapsed_time(e1) / args.steps, 4),
+    pstages = P.ecokv_stage_times()
+    os.environ["ECOKV_STAGE_TIMING"] = "0"
+    p_us = {k: round(v[0] / v[1] * 1e3, 2) for k, v in pstages.items()}
+    ms_pre = timed(lambda: ep.run(Kc_, Vc_, Q, pre=pre), args.steps)
+    ms_pre_score = timed(lambda: ep.score(Kc_, Q, pre=pre), args.steps)
+    # the sweep's cost beyond moving the same rows: the K sweep-with-copy minus
+    # the plain copy of V (same bytes, same layout move), plus the reduction
+    extra_us = p_us.get("prefill_sweep", 0.0) + p_us.get("prefill_reduce", 0.0) - p_us.get("prefill_copy_v", 0.0)
+    kv_bytes = 2 * bytes_k
+    with_pre = {"ms_per_step": round(ms_pre, 4), "score_ms": round(ms_pre_score, 4),
                 "tokens_per_s_per_layer": round(T / (ms_pre / 1e3 / L), 1),
-                "pass_frac_of_hbm_peak": round(pass_bytes / (ms_pre / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
-    del pre
+                "pass_frac_of_hbm_peak": round(pass_bytes / (ms_pre / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                "pre_from": "ecokv_prefill_write (timed below)",
+                "producer": {"ms_per_call": round(ms_prod, 4), "kernels_us": p_us,
+                             "algorithmic_bytes": 2 * kv_bytes + bytes_q,
+                             "GBs": round((2 * kv_bytes + bytes_q) / (ms_prod / 1e3) / 1e9, 1),
+                             "torch_transpose_copy_ms": round(ms_plain, 4),
+                             "extra_over_plain_copy_us": round(extra_us, 2)},
+                "producer_plus_pass_ms": round(ms_prod + ms_pre, 4),
+                "plain_write_plus_two_sweep_pass_ms": round(ms_plain + ms_per_step, 4),
+                "pass_frac_counting_producer_extra": round(
+                    pass_bytes / ((ms_pre + max(extra_us, 0.0) / 1e3) / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
+    del Kn, Vn, Kc_, Vc_, pre, ws_p
     torch.cuda.empty_cache()
 
     # Decode attention over the compressed cache the pass just wrote: one new

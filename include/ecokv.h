@@ -212,11 +212,13 @@ int ecokv_score_v(const void *K, const void *V, const void *Q_win, int dtype, co
  *          [0, D)          sum over its T keys of k_i
  *          [D, 2D)         sum over its T keys of k_i / max(|k_i|, 1e-12)
  *          [2D, 2D+R)      per window row r = g w + j (query head g of the
- *                          group, window row j): the max over its visible
- *                          keys of q.k / sqrt(D)
- *          [2D+R, 2D+2R)   the sum over its visible keys of
- *                          exp(q.k / sqrt(D) - that max)
- *        (visible: keys <= T - w + j when causal, all T otherwise).
+ *                          group, window row j): a reference m_r, and
+ *          [2D+R, 2D+2R)   z_r, the sum over its visible keys of
+ *                          exp(q.k / sqrt(D) - m_r)
+ *        (visible: keys <= T - w + j when causal, all T otherwise).  Only
+ *        m_r + log(z_r), the row's log-sum-exp, is used: m_r is usually the
+ *        row's largest logit, and a prefill's flash attention can pass its
+ *        log-sum-exp output as m_r with z_r = 1.
  * Everything else as ecokv_score_v; the two-sweep path's second sweep and
  * epilogue run as usual.  pre == NULL is ecokv_score_v. */
 int ecokv_score_pre(const void *K, const void *V, const void *Q_win, int dtype, const ecokv_shape *shape,
@@ -237,6 +239,36 @@ int ecokv_score_pre(const void *K, const void *V, const void *Q_win, int dtype, 
 int ecokv_score_noalloc(const void *K, const void *V, const void *Q_win, int dtype, const ecokv_shape *shape,
                         const ecokv_params *params, const float *pre, float *scores, float *lambda, float *stats,
                         void *stream);
+
+/* The KV-cache write of a prefill with the first sweep over K as its
+ * by-product (Sec. 3 window attention; Eq. (1) centroid; Appendix A.1 mu), so
+ * that the pass reads K once (ecokv_score_pre).  It copies the new K and V
+ * rows from the token-major layout a projection writes into the head-major
+ * layout the pass reads, and while K streams through it accumulates the two
+ * key sums and runs the window rows' online softmax over the keys:
+ *   K_new, V_new      DEVICE [L][T_total][H_kv][D] dtype (token-major: row
+ *                     cu[s] + t holds token t of sequence s for every KV head)
+ *   Q_win             DEVICE as for ecokv_score
+ *   params            only params->causal is read (which keys a window row sees)
+ *   K_cache, V_cache  DEVICE [L][H_kv][T_total][D] dtype, the K and V layout of
+ *                     ecokv_score; written, every row
+ *   pre               DEVICE [L][H_kv][B][2D + 2R] float32, written in the
+ *                     layout ecokv_score_pre reads; the reference m_r of a
+ *                     window row is at most its largest logit and within
+ *                     16 ln 2 of it (the sweep moves it lazily)
+ *   workspace         DEVICE, >= ecokv_prefill_workspace_size bytes, 256-byte
+ *                     aligned; no initial contents needed
+ * V_new and V_cache are both NULL (keys only) or both non-NULL.  The four row
+ * buffers must be 16-byte aligned and the new rows must not overlap the
+ * cache.  Errors: ECOKV_EINVAL for NULL, misaligned or overlapping buffers,
+ * ECOKV_EWORKSPACE for a short workspace, ECOKV_EUNSUPPORTED as ecokv_score;
+ * nothing is enqueued then.  No allocation, no synchronisation. */
+int ecokv_prefill_write(const void *K_new, const void *V_new, const void *Q_win, int dtype, const ecokv_shape *shape,
+                        const ecokv_params *params, void *K_cache, void *V_cache, float *pre, void *workspace,
+                        size_t workspace_bytes, void *stream);
+
+/* Workspace bytes of ecokv_prefill_write for this shape (either element type). */
+int ecokv_prefill_workspace_size(const ecokv_shape *shape, size_t *bytes);
 
 /* Number of int32 entries ecokv_select writes to idx:
  * L * H_kv * sum_s min(budget[s], T_s) (ECOKV_PER_HEAD and ECOKV_LAYER_FLAT). */

@@ -493,6 +493,80 @@ int score_impl(const void *K, const void *V, const void *Q_win, int dtype, const
 
 extern "C" {
 
+int ecokv_prefill_workspace_size(const ecokv_shape *shape, size_t *bytes)
+{
+    ShapeInfo si;
+    int rc = check_shape(shape, &si);
+    if (rc) return rc;
+    if (!bytes) return fail(ECOKV_EINVAL, "bytes is NULL");
+    if (si.R > ECOKV_MAX_ROWS)
+        return fail(ECOKV_EUNSUPPORTED, "(H_q/H_kv)*window = %d exceeds %d", si.R, ECOKV_MAX_ROWS);
+    // the element type changes the key block; report the larger
+    const size_t b0 = ecokv::prefill_ws_bytes(si.L, si.Hkv, si.B, si.D, si.R, si.maxT, true);
+    const size_t b1 = ecokv::prefill_ws_bytes(si.L, si.Hkv, si.B, si.D, si.R, si.maxT, false);
+    *bytes = b0 > b1 ? b0 : b1;
+    return ECOKV_OK;
+}
+
+int ecokv_prefill_write(const void *K_new, const void *V_new, const void *Q_win, int dtype, const ecokv_shape *shape,
+                        const ecokv_params *params, void *K_cache, void *V_cache, float *pre, void *workspace,
+                        size_t workspace_bytes, void *stream)
+{
+    ShapeInfo si;
+    int rc = check_shape(shape, &si);
+    if (rc) return rc;
+    if ((rc = check_params(params))) return rc;
+    if (dtype != ECOKV_BF16 && dtype != ECOKV_F32) return fail(ECOKV_EUNSUPPORTED, "dtype %d", dtype);
+    if (si.R > ECOKV_MAX_ROWS)
+        return fail(ECOKV_EUNSUPPORTED, "(H_q/H_kv)*window = %d exceeds %d", si.R, ECOKV_MAX_ROWS);
+    if (si.L == 0) return ECOKV_OK;
+    if (!K_new || !Q_win || !K_cache || !pre) return fail(ECOKV_EINVAL, "K_new, Q_win, K_cache and pre must be non-NULL");
+    if ((V_new == nullptr) != (V_cache == nullptr)) return fail(ECOKV_EINVAL, "V_new and V_cache: both or neither");
+    const uintptr_t al = (uintptr_t)K_new | (uintptr_t)K_cache | (uintptr_t)V_new | (uintptr_t)V_cache;
+    if ((al & 15u) != 0) return fail(ECOKV_EINVAL, "K_new, V_new, K_cache and V_cache must be 16-byte aligned");
+    if (((uintptr_t)pre & 3u) != 0) return fail(ECOKV_EINVAL, "pre must be 4-byte aligned");
+    // the copies read and write different memory
+    const size_t es = dtype == ECOKV_BF16 ? 2 : 4;
+    const size_t nb = (size_t)si.L * si.Hkv * (size_t)si.Ttot * si.D * es;
+    auto overlap = [nb](const void *x, const void *y) {
+        const uintptr_t a = (uintptr_t)x, b = (uintptr_t)y;
+        return a < b + nb && b < a + nb;
+    };
+    if (overlap(K_new, K_cache) || (V_new && (overlap(V_new, V_cache) || overlap(K_new, V_cache) ||
+                                             overlap(V_new, K_cache) || overlap(K_cache, V_cache))))
+        return fail(ECOKV_EINVAL, "the new rows and the cache must not overlap");
+    const bool bf16 = dtype == ECOKV_BF16;
+    const size_t need = ecokv::prefill_ws_bytes(si.L, si.Hkv, si.B, si.D, si.R, si.maxT, bf16);
+    if (!workspace) return fail(ECOKV_EINVAL, "workspace is NULL");
+    if (((uintptr_t)workspace & 255u) != 0) return fail(ECOKV_EINVAL, "workspace must be 256-byte aligned");
+    if (workspace_bytes < need) return fail(ECOKV_EWORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+
+    ecokv::ScoreArgs a;
+    memset(&a, 0, sizeof a);
+    a.K = K_cache;
+    a.Ksrc = K_new;
+    a.Q = Q_win;
+    a.pre_out = pre;
+    a.L = si.L;
+    a.Hq = si.Hq;
+    a.Hkv = si.Hkv;
+    a.G = si.G;
+    a.D = si.D;
+    a.w = si.w;
+    a.R = si.R;
+    a.B = si.B;
+    a.Ttot = si.Ttot;
+    a.Ptot = si.Ptot;
+    a.inv_sqrt_d = 1.f / sqrtf((float)si.D);
+    a.causal = params->causal;
+    a.kbf16 = bf16;
+    if ((rc = fill_seqtab(shape, nullptr, si.w, &a.seq, nullptr))) return rc;
+    const hipError_t e = ecokv::prefill_launch(a, V_new, V_cache, static_cast<char *>(workspace), si.maxT,
+                                               static_cast<hipStream_t>(stream), bf16);
+    if (e != hipSuccess) return hip_fail(e, "ecokv_prefill_write launch");
+    return ECOKV_OK;
+}
+
 int ecokv_workspace_status(void *workspace, void *stream)
 {
     if (!workspace) return fail(ECOKV_EINVAL, "workspace is NULL");

@@ -104,6 +104,27 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t key_rows_rsrc(const uint16_t *
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(krow0), (short)0, rows * (kD * 2), 0x00020000);
 }
 
+// group_load over rows `row_bytes` apart (key rows interleaved with other
+// heads' rows, as a projection writes them): the same lane layout.
+__device__ __forceinline__ void group_load_rows(u32x4 (&b)[8], __amdgpu_buffer_rsrc_t rs, int key0, int lane,
+                                                int row_bytes)
+{
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        b[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (key0 + 4 * i + (lane >> 4)) * row_bytes + (lane & 15) * 16, 0,
+                                                     2);
+}
+
+// Store of 32 key rows held in the load layout of group_load to consecutive
+// 256-byte rows (stores at or past the descriptor's end are dropped).
+__device__ __forceinline__ void group_store(const u32x4 (&b)[8], __amdgpu_buffer_rsrc_t rs, int key0, int lane)
+{
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        __builtin_amdgcn_raw_buffer_store_b128(b[i], rs, (key0 + 4 * i + (lane >> 4)) * (kD * 2) + (lane & 15) * 16, 0,
+                                               2);
+}
+
 // Lane layout of a 32-key B operand of v_mfma_f32_32x32x16_bf16 (and of the
 // window-row A operands): lane l holds, for k-step s = 0..7, the 16-byte chunk
 // 2s + l/32 of its row, i.e. dimensions 8(2s + h) .. +7 with h = l/32.

@@ -74,6 +74,12 @@ struct ScoreArgs {
     int red_std;     // lambda uses r_std (Appendix D) instead of r_E
     int centroid_prefix;  // kbar over the non-window keys (Appendix B.6)
     const float *pre;     // [U][2D + 2R] caller-supplied first-sweep sums (ecokv_score_pre), or null
+    // the KV-cache write with the first sweep (ecokv_prefill_write): K rows are
+    // read from Ksrc (token-major, [L][Ttot][Hkv][D]) and written to K (the
+    // head-major cache) while sweep 1 runs over them; the reduction writes
+    // pre_out in the layout of `pre`
+    const void *Ksrc;
+    float *pre_out;
     SeqTab seq;
 };
 
@@ -185,6 +191,11 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
 // A launch tag (never 0), distinct for every launch of the process: values a
 // launch publishes between its blocks carry it.
 unsigned launch_tag();
+
+// ecokv_prefill_write: workspace bytes, and the launches (a.K = the cache,
+// a.Ksrc = the new rows, a.pre_out = pre; Vsrc / Vdst may be null).
+size_t prefill_ws_bytes(int L, int Hkv, int B, int D, int R, int maxT, bool bf16);
+hipError_t prefill_launch(ScoreArgs a, const void *Vsrc, void *Vdst, char *ws, int maxT, hipStream_t st, bool bf16);
 // Clears the workspace status word (stream-ordered, by a one-thread kernel).
 hipError_t status_clear(unsigned *status, hipStream_t st);
 constexpr int kStreamMaxRows = 30;     // window rows of the streaming sweep 2; 2 more rows carry mu

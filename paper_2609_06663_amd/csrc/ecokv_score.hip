@@ -907,7 +907,12 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
 //    as B.
 constexpr float kRebase1 = 16.f;  // log2 headroom of the lazily moved row reference
 
-template <int KEYS>
+//
+// With CACHE (the KV-cache write of ecokv_prefill_write), each key row is read
+// from the token-major new rows a.Ksrc and the loaded registers are written to
+// the head-major cache a.K on arrival, before the group is used: one read and
+// one write of K, and the sweep rides on them.
+template <int KEYS, bool CACHE>
 __global__ __launch_bounds__(256, 2) void k_fs1s(ScoreArgs a)
 {
     constexpr int kS2Groups = KEYS / (32 * kS2Waves);  // 32-key groups per wave
@@ -937,7 +942,16 @@ __global__ __launch_bounds__(256, 2) void k_fs1s(ScoreArgs a)
 
     const int wbase = row_base + wv * (32 * kS2Groups);
     const int wkeys = __builtin_amdgcn_readfirstlane(max(0, min(32 * kS2Groups, T - wbase)));
-    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0 + (int64_t)wbase * kD, wkeys);
+    // CACHE: key i of the unit at row (l Ttot + cu[s] + i) Hkv + h of the new rows
+    const int src_row_bytes = CACHE ? a.Hkv * kD * 2 : kD * 2;
+    const __amdgpu_buffer_rsrc_t rs =
+        CACHE ? __builtin_amdgcn_make_buffer_rsrc(
+                    const_cast<uint16_t *>(uniform_ptr(static_cast<const uint16_t *>(a.Ksrc) +
+                                                       (((int64_t)un.l * a.Ttot + a.seq.cu[un.s] + wbase) * a.Hkv +
+                                                        un.h) * kD)),
+                    (short)0, wkeys * src_row_bytes, 0x00020000)
+              : key_rows_rsrc(krow0 + (int64_t)wbase * kD, wkeys);
+    const __amdgpu_buffer_rsrc_t rdst = key_rows_rsrc(krow0 + (int64_t)wbase * kD, CACHE ? wkeys : 0);
     u32x4 *wst = stage[wv];
 
     float ms = -INFINITY, ss = 0.f;  // window row kl over this lane's keys
@@ -952,6 +966,7 @@ __global__ __launch_bounds__(256, 2) void k_fs1s(ScoreArgs a)
     const int w_row = (lane & 15) < 3 ? (lane & 15) : 3;
 
     auto group = [&](const u32x4 (&ld)[8], int key0, bool valid) {
+        if constexpr (CACHE) group_store(ld, rdst, key0 - wbase, lane);  // (rows past the wave's end are dropped)
 #pragma unroll
         for (int i = 0; i < 8; ++i) wst[sw(4 * i + (lane >> 4), lane & 15)] = ld[i];
         u32x4 b[8];
@@ -1024,17 +1039,17 @@ __global__ __launch_bounds__(256, 2) void k_fs1s(ScoreArgs a)
                            : 0;
     auto goff = [&](int g) { return g < ng ? 32 * (g + rot < ng ? g + rot : g + rot - ng) : 32 * ng; };
     u32x4 b0[8], b1[8], b2[8];
-    group_load(b0, rs, goff(0), lane);
-    group_load(b1, rs, goff(1), lane);
+    group_load_rows(b0, rs, goff(0), lane, src_row_bytes);
+    group_load_rows(b1, rs, goff(1), lane, src_row_bytes);
 #pragma unroll 1
     for (int g = 0; g < ng; g += 3) {
-        group_load(b2, rs, goff(g + 2), lane);
+        group_load_rows(b2, rs, goff(g + 2), lane, src_row_bytes);
         __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the use
         group(b0, wbase + goff(g), g < ng);
-        group_load(b0, rs, goff(g + 3), lane);
+        group_load_rows(b0, rs, goff(g + 3), lane, src_row_bytes);
         __builtin_amdgcn_sched_barrier(0);
         group(b1, wbase + goff(g + 1), g + 1 < ng);
-        group_load(b1, rs, goff(g + 4), lane);
+        group_load_rows(b1, rs, goff(g + 4), lane, src_row_bytes);
         __builtin_amdgcn_sched_barrier(0);
         group(b2, wbase + goff(g + 2), g + 2 < ng);
     }
@@ -1126,7 +1141,10 @@ __global__ __launch_bounds__(256) void k_pre_anchors(ScoreArgs a)
     }
 }
 
-template <int LANES>
+// With PRE (ecokv_prefill_write) the unit's sums are written to a.pre_out in
+// the layout ecokv_score_pre takes: plain sums, and the row maxima in natural
+// units (max q.k / sqrt(D)).
+template <int LANES, bool PRE>
 __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
 {
     const int u = blockIdx.x;
@@ -1135,7 +1153,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
     const int nb = (T + a.rpb1 - 1) / a.rpb1;
     const int stride = 2 * a.D + 2 * a.R;
     const float *p = a.part1 + (int64_t)u * a.nch1 * stride;
-    float *anc = a.anchors + (int64_t)u * stride;
+    float *anc = (PRE ? a.pre_out : a.anchors) + (int64_t)u * stride;
     constexpr int lanes = LANES;
     constexpr int cpb = kReduceThreads / lanes;  // columns per block per step
     const int q = threadIdx.x & (lanes - 1);
@@ -1147,7 +1165,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
             for (int b = q; b < nb; b += lanes) s += p[(int64_t)b * stride + c];
 #pragma unroll
             for (int x = 1; x < lanes; x <<= 1) s += __shfl_xor(s, x, lanes);
-            if (q == 0) anc[c] = c < a.D ? centroid_component(a, un, T, c, s) : s / (float)T;
+            if (q == 0) anc[c] = PRE ? s : c < a.D ? centroid_component(a, un, T, c, s) : s / (float)T;
         } else {
             const int r = c - 2 * a.D;
             float m = -INFINITY, s = 0.f;
@@ -1160,7 +1178,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
                 softmax_merge2(m, s, m2, s2);
             }
             if (q == 0) {
-                anc[2 * a.D + r] = m;
+                anc[2 * a.D + r] = PRE ? m * (1.f / kLog2e) : m;
                 anc[2 * a.D + a.R + r] = s;
             }
         }
@@ -1945,19 +1963,19 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
                 a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
                 if (sblock == fast::kS2Keys)
                     ECOKV_TIMED("sweep1_stream", st,
-                                hipLaunchKernelGGL(fast::k_fs1s<fast::kS2Keys>, dim3(a.nch1, U), dim3(256), 0, st, a));
+                                hipLaunchKernelGGL((fast::k_fs1s<fast::kS2Keys, false>), dim3(a.nch1, U), dim3(256), 0, st, a));
                 else
                     ECOKV_TIMED("sweep1_stream", st,
-                                hipLaunchKernelGGL(fast::k_fs1s<fast::kS2KeysSmall>, dim3(a.nch1, U), dim3(256), 0, st, a));
+                                hipLaunchKernelGGL((fast::k_fs1s<fast::kS2KeysSmall, false>), dim3(a.nch1, U), dim3(256), 0, st, a));
             } else {
                 ECOKV_TIMED("sweep1_block", st, launch_sweep(1, a, grid, st, bf16));
             }
             if ((e = hipGetLastError()) != hipSuccess) return e;
             if (reduce1_lanes(a.nch1) == 4)
-                ECOKV_TIMED("reduce1", st, hipLaunchKernelGGL(k_reduce1<4>, dim3(U), dim3(kReduceThreads), 0, st, a));
+                ECOKV_TIMED("reduce1", st, hipLaunchKernelGGL((k_reduce1<4, false>), dim3(U), dim3(kReduceThreads), 0, st, a));
             else
                 ECOKV_TIMED("reduce1", st,
-                            hipLaunchKernelGGL(k_reduce1<16>, dim3(U, (2 * a.D + a.R + 63) / 64), dim3(kReduceThreads),
+                            hipLaunchKernelGGL((k_reduce1<16, false>), dim3(U, (2 * a.D + a.R + 63) / 64), dim3(kReduceThreads),
                                                0, st, a));
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -2022,6 +2040,93 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     if ((e = hipGetLastError()) != hipSuccess) return e;
     ECOKV_TIMED("epilogue2", st, hipLaunchKernelGGL(k_epi2, grid_e, dim3(kEpiThreads), 0, st, a));
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// ecokv_prefill_write: the KV-cache write of a prefill with the first sweep.
+// ---------------------------------------------------------------------------
+
+// Copy of every unit's rows from the token-major new rows ([L][Ttot][Hkv] rows
+// of rowb bytes) to the head-major cache ([L][Hkv][Ttot] rows), 16 bytes per
+// thread and step; block (x, u) copies rows 64 x .. 64 x + 63 of unit u.
+constexpr int kCopyRows = 64;
+__global__ __launch_bounds__(256) void k_rows_copy(const char *src, char *dst, int rowb, int L, int Hkv, int B,
+                                                   int64_t Ttot, SeqTab seq)
+{
+    const int u = blockIdx.y;
+    const Unit un = unit_of(u, Hkv, B);
+    const int T = seq.cu[un.s + 1] - seq.cu[un.s];
+    const int r0 = blockIdx.x * kCopyRows;
+    if (r0 >= T) return;
+    const int rows = min(kCopyRows, T - r0);
+    const int pr = rowb / 16;  // 16-byte pieces per row
+    const int64_t t0 = (int64_t)seq.cu[un.s] + r0;
+    const char *s0 = src + (((int64_t)un.l * Ttot + t0) * Hkv + un.h) * rowb;
+    char *d0 = dst + (((int64_t)un.l * Hkv + un.h) * Ttot + t0) * rowb;
+    typedef unsigned v4u __attribute__((ext_vector_type(4)));
+    for (int p = threadIdx.x; p < rows * pr; p += blockDim.x) {
+        const int r = p / pr, c = p - r * pr;
+        const v4u x = __builtin_nontemporal_load(reinterpret_cast<const v4u *>(s0 + (int64_t)r * Hkv * rowb) + c);
+        __builtin_nontemporal_store(x, reinterpret_cast<v4u *>(d0 + (int64_t)r * rowb) + c);
+    }
+}
+
+size_t prefill_ws_bytes(int L, int Hkv, int B, int D, int R, int maxT, bool bf16)
+{
+    // the block partials of sweep 1 (part1), for its smallest key block (as
+    // in the score's layout)
+    const int rpb = min(rows_per_block(D, bf16), fast::kSmallRows);
+    const size_t nch1 = (size_t)((maxT + rpb - 1) / rpb);
+    return align256(sizeof(float) * (size_t)L * Hkv * B * nch1 * (size_t)(2 * D + 2 * R));
+}
+
+hipError_t prefill_launch(ScoreArgs a, const void *Vsrc, void *Vdst, char *ws, int maxT, hipStream_t st, bool bf16)
+{
+    const int U = a.L * a.Hkv * a.B;
+    const int es = bf16 ? 2 : 4;
+    a.part1 = reinterpret_cast<float *>(ws);
+    hipError_t e;
+    const dim3 gc((maxT + kCopyRows - 1) / kCopyRows, U);
+    if (score_fast_path(a.D, bf16) && a.R <= 32) {
+        // bf16, head_dim 128: the streaming sweep reads the new rows and writes the cache
+        const int sblock = (int64_t)U * ((maxT + fast::kS2Keys - 1) / fast::kS2Keys) >= 1024 ? fast::kS2Keys
+                                                                                           : fast::kS2KeysSmall;
+        a.rpb1 = sblock;
+        a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
+        if (sblock == fast::kS2Keys)
+            ECOKV_TIMED("prefill_sweep", st,
+                        hipLaunchKernelGGL((fast::k_fs1s<fast::kS2Keys, true>), dim3(a.nch1, U), dim3(256), 0, st, a));
+        else
+            ECOKV_TIMED("prefill_sweep", st,
+                        hipLaunchKernelGGL((fast::k_fs1s<fast::kS2KeysSmall, true>), dim3(a.nch1, U), dim3(256), 0, st,
+                                           a));
+    } else {
+        // other shapes: copy the rows, then the first sweep over the cache
+        ECOKV_TIMED("prefill_copy", st,
+                    hipLaunchKernelGGL(k_rows_copy, gc, dim3(256), 0, st, static_cast<const char *>(a.Ksrc),
+                                       static_cast<char *>(const_cast<void *>(a.K)), a.D * es, a.L, a.Hkv, a.B, a.Ttot,
+                                       a.seq));
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        a.rpb1 = block_sweep_rows(a.D, bf16, U, maxT);
+        a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
+        ECOKV_TIMED("prefill_sweep", st, launch_sweep(1, a, dim3(a.nch1, U), st, bf16));
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (reduce1_lanes(a.nch1) == 4)
+        ECOKV_TIMED("prefill_reduce", st,
+                    hipLaunchKernelGGL((k_reduce1<4, true>), dim3(U), dim3(kReduceThreads), 0, st, a));
+    else
+        ECOKV_TIMED("prefill_reduce", st,
+                    hipLaunchKernelGGL((k_reduce1<16, true>), dim3(U, (2 * a.D + a.R + 63) / 64),
+                                       dim3(kReduceThreads), 0, st, a));
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (Vsrc) {
+        ECOKV_TIMED("prefill_copy_v", st,
+                    hipLaunchKernelGGL(k_rows_copy, gc, dim3(256), 0, st, static_cast<const char *>(Vsrc),
+                                       static_cast<char *>(Vdst), a.D * es, a.L, a.Hkv, a.B, a.Ttot, a.seq));
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace ecokv

@@ -30,7 +30,7 @@ STAT = dict(lambda_=0, rC=1, rE=2, DE=3, dmin=4, dmax=5, sdmin=6, sdmax=7, imp_m
             mu_norm2=10, scale=11)
 
 EXPORTS = ["ecokv_default_params", "ecokv_workspace_size", "ecokv_workspace_status", "ecokv_score", "ecokv_score_v",
-           "ecokv_score_pre", "ecokv_score_noalloc",
+           "ecokv_score_pre", "ecokv_score_noalloc", "ecokv_prefill_workspace_size", "ecokv_prefill_write",
            "ecokv_index_count",
            "ecokv_index_count_mode", "ecokv_select_workspace_size", "ecokv_select", "ecokv_compact",
            "ecokv_pyramid_budgets",
@@ -122,6 +122,8 @@ def _load():
     lib.ecokv_score_v.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_score_pre.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_score_noalloc.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, vp]
+    lib.ecokv_prefill_workspace_size.argtypes = [sp, ctypes.POINTER(ctypes.c_size_t)]
+    lib.ecokv_prefill_write.argtypes = [vp, vp, vp, ctypes.c_int, sp, pp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ecokv_index_count.argtypes = [sp, i32p, ctypes.POINTER(ctypes.c_int64)]
     lib.ecokv_index_count_mode.argtypes = [sp, ctypes.c_int, i32p, ctypes.POINTER(ctypes.c_int64)]
     lib.ecokv_decode_workspace_size.argtypes = [sp, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
@@ -306,6 +308,41 @@ def ecokv_score_pre(K: torch.Tensor, V: Optional[torch.Tensor], Q_win: torch.Ten
         raise TypeError("pre is float32")
     a = _score_args(K, V, Q_win, shape, p, scores, lambda_, stats, workspace, stream, pre=pre)
     _check(lib.ecokv_score_pre(*a))
+
+
+def ecokv_prefill_workspace_size(shape: Shape) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib.ecokv_prefill_workspace_size(ctypes.byref(shape.c), ctypes.byref(n)))
+    return n.value
+
+
+def ecokv_prefill_write(K_new: torch.Tensor, V_new: Optional[torch.Tensor], Q_win: torch.Tensor, shape: Shape,
+                        params: Optional[Params], K_cache: torch.Tensor, V_cache: Optional[torch.Tensor],
+                        pre: torch.Tensor, workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Enqueue ecokv_prefill_write: K_new / V_new token-major ([L][T_total][Hkv][D])
+    into K_cache / V_cache (the pass's [L][Hkv][T_total][D]), and `pre` (float32
+    [L][Hkv][B][2D + 2R]) for ecokv_score_pre.  V_new and V_cache: both or neither."""
+    p = params or Params()
+    if shape.c.num_layers == 0:
+        return
+    if (V_new is None) != (V_cache is None):
+        raise ValueError("V_new and V_cache: both or neither")
+    dev = K_new.device
+    kn = _arg(K_new, "K_new", _KV_TYPES, shape.kv_numel(), dev)
+    for t, n in ((Q_win, "Q_win"), (K_cache, "K_cache"), (V_new, "V_new"), (V_cache, "V_cache")):
+        if t is not None and t.dtype != K_new.dtype:
+            raise TypeError(f"{n} must have the element type of K_new")
+    vn = _arg(V_new, "V_new", _KV_TYPES, shape.kv_numel(), dev, optional=True)
+    qp = _arg(Q_win, "Q_win", _KV_TYPES, shape.q_numel(), dev)
+    kc = _arg(K_cache, "K_cache", _KV_TYPES, shape.kv_numel(), dev)
+    vc = _arg(V_cache, "V_cache", _KV_TYPES, shape.kv_numel(), dev, optional=True)
+    R = shape.c.num_q_heads // shape.c.num_kv_heads * shape.c.window
+    pp = _arg(pre, "pre", _F32, shape.units * (2 * shape.c.head_dim + 2 * R), dev)
+    need = ecokv_prefill_workspace_size(shape)
+    workspace = _workspace(workspace, need, dev, stream)
+    wp = _arg(workspace, "workspace", _U8, need, dev)
+    _check(lib.ecokv_prefill_write(kn, vn, qp, _dtype_code(K_new), ctypes.byref(shape.c), ctypes.byref(p), kc, vc, pp,
+                                   wp, workspace.numel(), _stream(stream)))
 
 
 def ecokv_score_noalloc(K: torch.Tensor, V: Optional[torch.Tensor], Q_win: torch.Tensor, shape: Shape,

@@ -289,3 +289,36 @@ def test_select_workspace_checks(P):
     # a layer-flat group holds every head's keys of a (layer, sequence): more slices per group
     assert P.ecokv_select_workspace_size(P.Shape(1, 8, 8, 128, 4, [0, 32768]), P.LAYER_FLAT) > \
         P.ecokv_select_workspace_size(P.Shape(1, 8, 8, 128, 4, [0, 32768]), P.PER_HEAD) // 8
+
+
+def test_prefill_write_fails_before_device_work(P):
+    """NULL, unpaired, misaligned or overlapping buffers, a short workspace and an
+    unsupported element type are refused on the host; L = 0 enqueues nothing."""
+    from paper_2609_06663_amd import ecokv as E
+    s = P.Shape(1, 4, 2, 128, 4, [0, 100])
+    p = P.Params()
+    lib = E.lib
+    n = ctypes.c_size_t(0)
+    assert lib.ecokv_prefill_workspace_size(ctypes.byref(s.c), ctypes.byref(n)) == 0 and n.value > 0
+    ws = n.value
+    assert P.ecokv_prefill_workspace_size(s) == ws
+    # fake device addresses far apart (51200 bytes of rows each), never dereferenced
+    kn, kc, q, pre, wsp = (ctypes.c_void_p(1 << b) for b in (20, 30, 34, 38, 36))
+
+    def call(K_new=kn, V_new=None, K_cache=kc, V_cache=None, dtype=0, w=wsp, nbytes=ws):
+        return lib.ecokv_prefill_write(K_new, V_new, q, dtype, ctypes.byref(s.c), ctypes.byref(p), K_cache, V_cache,
+                                       pre, w, nbytes, None)
+
+    assert call(K_new=None) == -1
+    assert call(K_cache=None) == -1
+    assert call(V_cache=ctypes.c_void_p(1 << 39)) == -1                  # V_cache without V_new
+    assert call(K_cache=kn) == -1                                         # the cache on the new rows
+    assert "overlap" in P.ecokv_last_error()
+    assert call(K_cache=ctypes.c_void_p((1 << 20) + 4096)) == -1          # ... partly
+    assert call(K_new=ctypes.c_void_p((1 << 20) + 8)) == -1               # misaligned rows
+    assert call(w=ctypes.c_void_p((1 << 36) + 16)) == -1                  # misaligned workspace
+    assert call(nbytes=ws - 1) == -2
+    assert call(dtype=7) == -3
+    empty = P.Shape(0, 4, 2, 128, 4, [0, 100])
+    assert lib.ecokv_prefill_write(None, None, None, 0, ctypes.byref(empty.c), ctypes.byref(p), None, None, None, None,
+                                   0, None) == 0
