@@ -2088,9 +2088,12 @@ hipError_t prefill_launch(ScoreArgs a, const void *Vsrc, void *Vdst, char *ws, i
     hipError_t e;
     const dim3 gc((maxT + kCopyRows - 1) / kCopyRows, U);
     if (score_fast_path(a.D, bf16) && a.R <= 32) {
-        // bf16, head_dim 128: the streaming sweep reads the new rows and writes the cache
-        const int sblock = (int64_t)U * ((maxT + fast::kS2Keys - 1) / fast::kS2Keys) >= 1024 ? fast::kS2Keys
-                                                                                           : fast::kS2KeysSmall;
+        // bf16, head_dim 128: the streaming sweep reads the new rows and writes
+        // the cache, in 512-key blocks (28-layer stack, 32768 tokens: the sweep
+        // with the copy takes 326 us with them, as long as a plain copy of the
+        // same rows, against 367 us with 2048-key blocks, whose 1792 blocks
+        // leave the last of their 3.5 rounds half empty)
+        const int sblock = fast::kS2KeysSmall;
         a.rpb1 = sblock;
         a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
         if (sblock == fast::kS2Keys)

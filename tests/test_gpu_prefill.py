@@ -130,10 +130,10 @@ def test_prefill_write_keys_only_and_non_causal():
     check_per_head(wl, g, params=p)
 
 
-def test_prefill_write_2048_key_blocks():
-    # 64 units x 16 blocks of 2048 keys: the large-block form of the sweep
+def test_prefill_write_full_length():
+    # 64 units of 32768 keys, 64 blocks each
     wl = W.custom(95, L=8, Hq=56, Hkv=8, D=128, w=4, seqlens=[32768], dtype="bf16", budget=[6553], group=256)
-    say("8 layers x 8 KV heads x 32768 tokens: 2048-key blocks")
+    say("8 layers x 8 KV heads x 32768 tokens")
     Kc, Vc, pre = run_prefill(wl)
     check_cache(wl, Kc, Vc)
     check_pre(wl, pre, what="T=32768")
