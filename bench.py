@@ -35,7 +35,10 @@ def parse():
     ap.add_argument("--layers", type=int, default=28)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-layers", type=int, default=28)
-    ap.add_argument("--extras", action="store_true", help="also time 10 % and 40 % budgets")
+    ap.add_argument("--extras", action="store_true", help="also time 10 %% and 40 %% budgets")
+    ap.add_argument("--config", choices=sorted(CONFIGS),
+                    help="time only this configuration's pass (one JSON line; with --counter-run: its counter "
+                         "workload) -- for profiling one configuration at a time")
     ap.add_argument("--counter-run", action="store_true",
                     help="run a few passes and a 1 GiB copy for rocprofv3 --pmc, then exit")
     ap.add_argument("--traffic-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "COMMAND"),
@@ -53,7 +56,7 @@ STAGE_KERNELS = {
     "sweep1_stream": ["k_fs1s"], "sweep1_block": ["k_fs1", "k_pass1"], "reduce1": ["k_reduce1"],
     "sweep2_stream": ["k_fs2s"], "sweep2_block": ["k_fs2", "k_pass2"], "epilogue": ["k_epi_unit"],
     "epilogue1": ["k_epi1"], "epilogue2": ["k_epi2"],
-    "select": ["k_select_reg", "k_select"], "compact": ["k_compact"], "vnorm": ["k_vnorm"],
+    "select": ["k_select_reg", "k_select", "k_sel_digit", "k_sel_count", "k_sel_emit"], "compact": ["k_compact"], "vnorm": ["k_vnorm"],
     "dquant": ["k_dquant", "k_dquant_reg"], "decode": ["k_decode_mx", "k_decode"], "decode_merge": ["k_decode_merge"],
     "pre_anchors": ["k_pre_anchors"],
 }
@@ -104,10 +107,91 @@ def stored_traffic(stage):
     return val
 
 
+# The configurations of the benchmark: workload builder, selection mode, label.
+CONFIGS = {
+    "stack28": ("stack28", "per_head", "28-layer GQA stack (28q/4kv, head_dim 128, bf16), N=32768, window 4, "
+                                       "budget 20 % per head"),
+    "layer7b": ("layer7b", "per_head", "one 7B-MLLM layer (28q/4kv, head_dim 128, bf16), N=8192, window 8, "
+                                       "budget 20 % per head"),
+    "mha64k": ("mha64k", "per_head", "one 32-head MHA layer (head_dim 128, bf16), N=65536, window 8, "
+                                     "budget 2048 per head"),
+    "varlen": ("varlen", "layer_flat", "one layer over 8 packed sequences of 4k-32k tokens (28q/4kv, head_dim "
+                                       "128, bf16), window 4, layer-flat budget 15 % of each sequence"),
+}
+
+
+def timed(fn, reps, stream):
+    """Average milliseconds of fn() over reps calls, bracketed by events on `stream`."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def stage_us(fn, reps):
+    """Microseconds per call of fn() in every library stage (all its launches in
+    the call together; "launches" gives how many per call)."""
+    import torch
+    import paper_2609_06663_amd as P
+    os.environ["ECOKV_STAGE_TIMING"] = "1"
+    P.ecokv_stage_times()
+    for _ in range(reps):
+        fn()
+    torch.cuda.synchronize()
+    st = P.ecokv_stage_times()
+    os.environ["ECOKV_STAGE_TIMING"] = "0"
+    out = {k: round(v[0] / reps * 1e3, 2) for k, v in st.items()}
+    for k, v in st.items():
+        if v[1] != reps:
+            out[f"{k}_launches"] = round(v[1] / reps, 2)
+    return out
+
+
+def pass_leg(name, steps, to_dev, wl=None):
+    """One configuration's pass (score, select, compact): per-pass time, per-kernel
+    times, algorithmic bytes and the fraction of the HBM peak."""
+    import torch
+    import workloads as W
+    import paper_2609_06663_amd as P
+    from paper_2609_06663_amd.pipeline import EvictionPass
+    builder, mode, label = CONFIGS[name]
+    if wl is None:
+        t0 = time.time()
+        wl = W.CONFIG_BUILDERS[builder]()
+        log(f"{name}: generated in {time.time() - t0:.1f}s")
+    Kx, Vx, Qx = to_dev(wl.K), to_dev(wl.V), to_dev(wl.Q)
+    sh = P.Shape(wl.L, wl.Hq, wl.Hkv, wl.D, wl.w, wl.cu_seqlens)
+    epx = EvictionPass(sh, wl.budget, P.LAYER_FLAT if mode == "layer_flat" else P.PER_HEAD, P.Params(),
+                       torch.bfloat16, "cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        epx.run(Kx, Vx, Qx)
+    ms = timed(lambda: epx.run(Kx, Vx, Qx), steps, stream)
+    kern = stage_us(lambda: epx.run(Kx, Vx, Qx), steps)
+    epx.check()
+    tot, B = wl.cu_seqlens[-1], len(wl.cu_seqlens) - 1
+    nbytes = (wl.L * wl.Hkv * tot * wl.D * 2 + wl.L * wl.Hq * B * wl.w * wl.D * 2
+              + 4 * epx.n_idx * wl.D * 2 + 4 * epx.n_idx)
+    out = {"workload": label, "layers": wl.L, "q_heads": wl.Hq, "kv_heads": wl.Hkv, "sequences": B,
+           "tokens": tot, "entries": epx.n_idx, "ms_per_pass": round(ms, 4),
+           "tokens_per_s_per_layer": round(tot / (ms / 1e3 / wl.L), 1),
+           "algorithmic_bytes": nbytes, "achieved_GBs": round(nbytes / (ms / 1e3) / 1e9, 1),
+           "frac_of_hbm_peak": round(nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4), "kernels_us": kern}
+    del epx, Kx, Vx, Qx
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.traffic_summary:
-        traffic_summary(*args.traffic_summary)
+        traffic_summary(*args.traffic_summary, label=CONFIGS[args.config or "stack28"][2])
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the eviction pass is per (layer, KV head) and this "
@@ -121,16 +205,27 @@ def main():
     import paper_2609_06663_amd as P
     from paper_2609_06663_amd.pipeline import EvictionPass, LayerwiseEviction
 
+    dev = torch.device("cuda:0")
+
+    def to_dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    if args.config and args.config != "stack28":
+        if args.counter_run:
+            wl_c = W.CONFIG_BUILDERS[CONFIGS[args.config][0]]()
+            sh = P.Shape(wl_c.L, wl_c.Hq, wl_c.Hkv, wl_c.D, wl_c.w, wl_c.cu_seqlens)
+            mode_c = P.LAYER_FLAT if CONFIGS[args.config][1] == "layer_flat" else P.PER_HEAD
+            ep_c = EvictionPass(sh, wl_c.budget, mode_c, P.Params(), torch.bfloat16, "cuda")
+            counter_run(ep_c, to_dev(wl_c.K), to_dev(wl_c.V), to_dev(wl_c.Q))
+            return
+        print(json.dumps({"config": args.config, **pass_leg(args.config, args.steps, to_dev)}), flush=True)
+        return
+
     T, L = args.tokens, args.layers
     log(f"generating stack: {L} layers x 4 KV heads x {T} tokens (bf16)")
     t0 = time.time()
     wl = W.stack28(T=T, budget_frac=args.budget_frac, L=L)
     log(f"generated in {time.time() - t0:.1f}s")
-
-    dev = torch.device("cuda:0")
-
-    def to_dev(a):
-        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
 
     K, V, Q = to_dev(wl.K), to_dev(wl.V), to_dev(wl.Q)
     shape = P.Shape(wl.L, wl.Hq, wl.Hkv, wl.D, wl.w, wl.cu_seqlens)
@@ -146,6 +241,10 @@ def main():
     for _ in range(args.warmup):
         ep.run(K, V, Q)
     torch.cuda.synchronize()
+
+    if args.config == "stack28":
+        print(json.dumps({"config": "stack28", **pass_leg("stack28", args.steps, to_dev, wl=wl)}), flush=True)
+        return
 
     log(f"timing {args.steps} steps")
     # an event between consecutive steps as well, for the median step time
@@ -367,19 +466,8 @@ def main():
         Kc_.view(L, Hkv, T, D).copy_(Kn.view(L, T, Hkv, D).transpose(1, 2))
         Vc_.view(L, Hkv, T, D).copy_(Vn.view(L, T, Hkv, D).transpose(1, 2))
 
-    def timed(fn, reps):
-        fn()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(reps):
-            fn()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / reps
-
-    ms_plain = timed(plain_write, args.steps)
-    ms_prod = timed(producer, args.steps)
+    ms_plain = timed(plain_write, args.steps, stream)
+    ms_prod = timed(producer, args.steps, stream)
     assert torch.equal(Kc_, K) and torch.equal(Vc_, V), "the producer's cache differs from the rows it was given"
     os.environ["ECOKV_STAGE_TIMING"] = "1"
     P.ecokv_stage_times()
@@ -389,8 +477,8 @@ def main():
     pstages = P.ecokv_stage_times()
     os.environ["ECOKV_STAGE_TIMING"] = "0"
     p_us = {k: round(v[0] / v[1] * 1e3, 2) for k, v in pstages.items()}
-    ms_pre = timed(lambda: ep.run(Kc_, Vc_, Q, pre=pre), args.steps)
-    ms_pre_score = timed(lambda: ep.score(Kc_, Q, pre=pre), args.steps)
+    ms_pre = timed(lambda: ep.run(Kc_, Vc_, Q, pre=pre), args.steps, stream)
+    ms_pre_score = timed(lambda: ep.score(Kc_, Q, pre=pre), args.steps, stream)
     # the sweep's cost beyond moving the same rows: the K sweep-with-copy minus
     # the plain copy of V (same bytes, same layout move), plus the reduction
     extra_us = p_us.get("prefill_sweep", 0.0) + p_us.get("prefill_reduce", 0.0) - p_us.get("prefill_copy_v", 0.0)
@@ -466,32 +554,16 @@ def main():
                                                       "tokens_per_s_per_layer": T / (ms / 1e3 / L)}
             del ep2
 
-    # the head-adaptive batch: 8 packed sequences of 4k-32k tokens, one layer,
-    # layer-flat selection with H_kv * floor(0.15 T_s) places per sequence
+    # the other configurations, each as its own pass: one 8192-token layer, one
+    # 32-head 65536-token layer, and the head-adaptive batch (8 packed
+    # sequences of 4k-32k tokens, layer-flat selection with H_kv floor(0.15 T_s)
+    # places per sequence)
+    log("one 8192-token layer")
+    layer_8k = pass_leg("layer7b", args.steps, to_dev)
+    log("one 32-head 65536-token layer")
+    mha_64k = pass_leg("mha64k", args.steps, to_dev)
     log("layer-flat selection over 8 packed sequences")
-    wv_ = W.varlen()
-    Kv_, Vv_, Qv_ = to_dev(wv_.K), to_dev(wv_.V), to_dev(wv_.Q)
-    shape_v = P.Shape(wv_.L, wv_.Hq, wv_.Hkv, wv_.D, wv_.w, wv_.cu_seqlens)
-    ep_v = EvictionPass(shape_v, wv_.budget, P.LAYER_FLAT, P.Params(), torch.bfloat16, "cuda")
-    for _ in range(3):
-        ep_v.run(Kv_, Vv_, Qv_)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(args.steps):
-        ep_v.run(Kv_, Vv_, Qv_)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms_v = e0.elapsed_time(e1) / args.steps
-    tot_v = wv_.cu_seqlens[-1]
-    bytes_v = (wv_.Hkv * tot_v * wv_.D * 2 + wv_.Hq * (len(wv_.cu_seqlens) - 1) * wv_.w * wv_.D * 2
-               + 4 * ep_v.n_idx * wv_.D * 2 + 4 * ep_v.n_idx)
-    layer_flat_varlen = {
-        "sequences": len(wv_.cu_seqlens) - 1, "tokens": tot_v, "entries": ep_v.n_idx,
-        "ms_per_pass": round(ms_v, 4), "tokens_per_s": round(tot_v / (ms_v / 1e3), 1),
-        "algorithmic_bytes": bytes_v, "achieved_GBs": round(bytes_v / (ms_v / 1e3) / 1e9, 1),
-        "frac_of_hbm_peak": round(bytes_v / (ms_v / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
-    del ep_v, Kv_, Vv_, Qv_, wv_
+    layer_flat_varlen = pass_leg("varlen", args.steps, to_dev)
 
     # the same stack as L single-layer calls on one stream (one call per layer
     # as its prefill finishes)
@@ -593,6 +665,8 @@ def main():
         "alternatives": alternatives,
         "decode_attention": decode_att,
         "with_prefill_sums": with_pre,
+        "layer_8k": layer_8k,
+        "mha_64k": mha_64k,
         "layer_flat_varlen": layer_flat_varlen,
     }
     if extras:
@@ -627,7 +701,7 @@ def _counter_rows(d):
     return rows
 
 
-def traffic_summary(fetch_dir, write_dir, command):
+def traffic_summary(fetch_dir, write_dir, command, label):
     """FETCH_SIZE and WRITE_SIZE (KiB per dispatch) per stage, scaled by the same counters
     on a plain copy of COPY_BYTES, into the text that stored_traffic() reads."""
     per = {}
@@ -643,26 +717,30 @@ def traffic_summary(fetch_dir, write_dir, command):
                 continue
             st = stage_of_kernel(kname)
             if st:
-                per.setdefault(st, {}).setdefault(ctr, []).append(val)
+                per.setdefault(st, {}).setdefault(ctr, {}).setdefault(kname, []).append(val)
         if not copies:
             raise SystemExit(f"{ctr}: copy kernel not found")
         per.setdefault("_copy", {})[ctr] = copies
     cf = COPY_BYTES / (sum(per["_copy"]["FETCH_SIZE"]) / len(per["_copy"]["FETCH_SIZE"]))
     cw = COPY_BYTES / (sum(per["_copy"]["WRITE_SIZE"]) / len(per["_copy"]["WRITE_SIZE"]))
-    print("HBM traffic per launch from rocprofv3 counters: 28-layer stack, 28 query / 4 KV heads, "
-          "head_dim 128, bf16, N=32768, window 4, budget 6553 per head (20 %)")
+    print(f"HBM traffic per launch from rocprofv3 counters: {label}")
     print(f"command: {command}")
     print("FETCH_SIZE and WRITE_SIZE are KiB per dispatch; each is scaled by copy_bytes / counter "
           f"on torch.neg over {COPY_BYTES} bytes (reads and writes that many bytes)")
     print(f"copy_factor_fetch: {cf:.4f}")
     print(f"copy_factor_write: {cw:.4f}")
     print(f"source_digest: {source_digest()}")
-    print("# stage: name  fetch_bytes  write_bytes  =  scaled_total_bytes  (averages over dispatches)")
+    print("# stage: name  fetch_bytes  write_bytes  =  scaled_total_bytes  (per call: each kernel's average "
+          "over its dispatches, summed over the stage's kernels)")
+
+    def per_call(d):
+        return sum(sum(v) / len(v) for v in d.values())
+
     for st in STAGE_KERNELS:
         if st not in per or "FETCH_SIZE" not in per[st] or "WRITE_SIZE" not in per[st]:
             continue
-        f = sum(per[st]["FETCH_SIZE"]) / len(per[st]["FETCH_SIZE"]) * cf
-        w = sum(per[st]["WRITE_SIZE"]) / len(per[st]["WRITE_SIZE"]) * cw
+        f = per_call(per[st]["FETCH_SIZE"]) * cf
+        w = per_call(per[st]["WRITE_SIZE"]) * cw
         print(f"stage: {st} {f:.0f} {w:.0f} = {f + w:.0f}")
 
 
