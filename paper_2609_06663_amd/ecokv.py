@@ -15,7 +15,9 @@ from typing import Optional, Sequence
 
 import torch
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libecokv.so")
+# ECOKV_LIBRARY names another build of the library to load instead of the
+# in-tree one (for instance one whose host code is built with sanitizers).
+_LIB_PATH = os.environ.get("ECOKV_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libecokv.so")
 
 OK, EINVAL, EWORKSPACE, EUNSUPPORTED, EHIP, ETIMEOUT = 0, -1, -2, -3, -4, -5
 BF16, F32 = 0, 1
