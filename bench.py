@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--config", choices=sorted(CONFIGS),
                     help="time only this configuration's pass (one JSON line; with --counter-run: its counter "
                          "workload) -- for profiling one configuration at a time")
+    ap.add_argument("--prefill", action="store_true",
+                    help="with --config stack28: the prefill's cache write (ecokv_prefill_write) from token-major "
+                         "rows, then the pass with the handed-over sums (score_pre, select, compact)")
     ap.add_argument("--counter-run", action="store_true",
                     help="run a few passes and a 1 GiB copy for rocprofv3 --pmc, then exit")
     ap.add_argument("--traffic-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "COMMAND"),
@@ -58,7 +61,7 @@ STAGE_KERNELS = {
     "epilogue1": ["k_epi1"], "epilogue2": ["k_epi2"],
     "select": ["k_select_reg", "k_select", "k_sel_digit", "k_sel_count", "k_sel_emit"], "compact": ["k_compact"], "vnorm": ["k_vnorm"],
     "dquant": ["k_dquant", "k_dquant_reg"], "decode": ["k_decode_mx", "k_decode"], "decode_merge": ["k_decode_merge"],
-    "pre_anchors": ["k_pre_anchors"],
+    "pre_anchors": ["k_pre_anchors"], "prefill_sweep": [], "prefill_reduce": [], "prefill_copy": [],
 }
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, vendor figure
 COPY_BYTES = 1 << 30  # size of the calibration copy in --counter-run
@@ -70,6 +73,11 @@ def stage_of_kernel(kname):
     m = re.search(r"::(k_\w+?)(<|\()", kname)
     if not m:
         return None
+    # the prefill cache write's forms of sweep 1 and its reduction, and its copies
+    if m.group(1) in ("k_fs1s", "k_reduce1") and ", true>" in kname:
+        return "prefill_sweep" if m.group(1) == "k_fs1s" else "prefill_reduce"
+    if m.group(1) == "k_rows_copy":
+        return "prefill_copy"
     for st, ks in STAGE_KERNELS.items():
         if m.group(1) in ks:
             return st
@@ -191,7 +199,11 @@ def pass_leg(name, steps, to_dev, wl=None):
 def main():
     args = parse()
     if args.traffic_summary:
-        traffic_summary(*args.traffic_summary, label=CONFIGS[args.config or "stack28"][2])
+        label = CONFIGS[args.config or "stack28"][2]
+        if args.prefill:
+            label += "; the prefill's cache write from token-major rows (ecokv_prefill_write), then the pass " \
+                     "with its sums (ecokv_score_pre, select, compact)"
+        traffic_summary(*args.traffic_summary, label=label)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the eviction pass is per (layer, KV head) and this "
@@ -234,7 +246,7 @@ def main():
     stream = torch.cuda.current_stream()
 
     if args.counter_run:
-        counter_run(ep, K, V, Q)
+        counter_run(ep, K, V, Q, prefill=args.prefill)
         return
 
     log(f"warmup {args.warmup}")
@@ -243,6 +255,14 @@ def main():
     torch.cuda.synchronize()
 
     if args.config == "stack28":
+        if args.prefill:
+            pre, producer = prefill_inputs(ep, K, V, Q)
+            ms_prod = timed(producer, args.steps, stream)
+            ms = timed(lambda: ep.run(K, V, Q, pre=pre), args.steps, stream)
+            kern = stage_us(lambda: (producer(), ep.run(K, V, Q, pre=pre)), args.steps)
+            print(json.dumps({"config": "stack28", "prefill": True, "producer_ms": round(ms_prod, 4),
+                              "ms_per_pass": round(ms, 4), "kernels_us": kern}), flush=True)
+            return
         print(json.dumps({"config": "stack28", **pass_leg("stack28", args.steps, to_dev, wl=wl)}), flush=True)
         return
 
@@ -674,11 +694,44 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def counter_run(ep, K, V, Q):
-    """Workload for rocprofv3 --pmc: three passes, then three copies of COPY_BYTES."""
+def prefill_inputs(ep, K, V, Q):
+    """Token-major copies of K and V, a cache to write, `pre`, and the producer call
+    (ecokv_prefill_write) that fills the cache and `pre` from them."""
     import torch
-    for _ in range(3):
-        ep.run(K, V, Q)
+    import paper_2609_06663_amd as P
+    c = ep.shape.c
+    L, Hkv, D, w, Hq = c.num_layers, c.num_kv_heads, c.head_dim, c.window, c.num_q_heads
+    R = Hq // Hkv * w
+    Kn = K.view(L, Hkv, -1, D).transpose(1, 2).contiguous()
+    Vn = V.view(L, Hkv, -1, D).transpose(1, 2).contiguous()
+    Kc, Vc = torch.empty_like(K), torch.empty_like(V)
+    pre = torch.empty(L * Hkv * c.num_seqs * (2 * D + 2 * R), dtype=torch.float32, device=K.device)
+    ws = torch.empty(P.ecokv_prefill_workspace_size(ep.shape), dtype=torch.uint8, device=K.device)
+
+    def producer():
+        P.ecokv_prefill_write(Kn, Vn, Q, ep.shape, P.Params(), Kc, Vc, pre, ws)
+
+    producer()
+    torch.cuda.synchronize()
+    return pre, producer
+
+
+def counter_run(ep, K, V, Q, prefill=False):
+    """Workload for rocprofv3 --pmc: three passes (with prefill: three cache writes
+    from token-major rows, then three passes with the handed-over sums), then three
+    copies of COPY_BYTES."""
+    import torch
+    if prefill:
+        pre, producer = prefill_inputs(ep, K, V, Q)
+        for _ in range(3):
+            producer()
+        torch.cuda.synchronize()
+        for _ in range(3):
+            ep.run(K, V, Q, pre=pre)
+        del producer
+    else:
+        for _ in range(3):
+            ep.run(K, V, Q)
     torch.cuda.synchronize()
     src = torch.ones(COPY_BYTES // 2, dtype=torch.bfloat16, device=K.device)
     dst = torch.empty_like(src)
