@@ -833,7 +833,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
         // ordered emission of one head: bit q of gtm[c] / eqm[c] marks key
         // v0 + 32 c + q above / equal to the threshold; the thread's taken
         // keys go to consecutive slots from the number taken before its run
-        constexpr int NC = KPT / 32;  // 32-key words per thread
+        constexpr int NC = (KPT + 31) / 32;   // 32-key words per thread
+        constexpr int QW = KPT < 32 ? KPT : 32;  // keys per word
         uint32_t gtm[NC], eqm[NC];
         uint32_t cg = 0, ce = 0;
 #pragma unroll
@@ -841,7 +842,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
             gtm[c] = 0u;
             eqm[c] = 0u;
 #pragma unroll
-            for (int q = 0; q < 32; ++q)
+            for (int q = 0; q < QW; ++q)
                 if (v0 + 32 * c + q < n) {
                     gtm[c] |= kk[32 * c + q] > thr ? 1u << q : 0u;
                     eqm[c] |= kk[32 * c + q] == thr ? 1u << q : 0u;
@@ -1404,9 +1405,17 @@ hipError_t select_launch(SelectArgs a, char *ws, hipStream_t st)
     if (maxn <= 32 * kSelThreads) {
         // one block per group: for groups this small, one launch beats five
         // short ones (28-layer stack, 112 groups of 32764 keys: 29 against 46 us;
-        // one layer, 4 groups: 25 against 33 us)
-        ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select_reg<32>, dim3((unsigned)groups), dim3(kSelThreads), 0,
-                                                     st, a));
+        // one layer, 4 groups: 25 against 33 us).  Keys per thread by group
+        // size, so that a small group's per-key work spreads over every wave
+        if (maxn <= 8 * kSelThreads)
+            ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select_reg<8>, dim3((unsigned)groups), dim3(kSelThreads),
+                                                         0, st, a));
+        else if (maxn <= 16 * kSelThreads)
+            ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select_reg<16>, dim3((unsigned)groups), dim3(kSelThreads),
+                                                         0, st, a));
+        else
+            ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_select_reg<32>, dim3((unsigned)groups), dim3(kSelThreads),
+                                                         0, st, a));
         return hipGetLastError();
     }
     const SelWsLayout lay = select_ws_layout(a.mb_groups, a.mb_maxn);

@@ -2,9 +2,9 @@
 
 Every case draws seeded synthetic inputs (workloads/), runs score -> select ->
 compact on the GPU and compares with the oracle on the same bytes, to the
-tolerances stated in parity_utils.  Small and medium shapes are checked in
-full; the full-size shapes (28 layers x 32k tokens, 32 heads x 64k tokens)
-are checked on sampled units plus properties that hold everywhere.
+tolerances stated in parity_utils.  Every unit of every shape is compared,
+the full-size ones (28 layers x 32k tokens, 32 heads x 64k tokens) included,
+with the oracle on all host threads.
 """
 import sys
 
@@ -378,39 +378,46 @@ def test_select_bit_exact_with_ties(mode):
     np.testing.assert_array_equal(offsets.cpu().numpy(), ref_o.reshape(-1))
 
 
-def _digit_case(case, rng):
-    """Scores of one 32000-key unit shaped for a path of the register radix select."""
-    P = 32000
+def _digit_case(case, rng, P=32000):
+    """Scores of one P-key unit shaped for a path of the register radix select
+    (counts scaled from the 32000-key form)."""
+    f = P / 32000
     spread = np.exp(rng.uniform(np.log(1e-3), np.log(100.0), size=P)).astype(np.float32)
     if case == "prefix_overflow":
-        # 31000 keys in [1, 1.0001): one first digit (the exponent) holds more
-        # keys than the stage can gather, so the later digits count the registers
+        # 31000 of 32000 keys in [1, 1.0001): one first digit (the exponent)
+        # holds more keys than the stage can gather, so the later digits count
+        # the registers (at smaller sizes the cluster fits the stage)
         S = spread.copy()
-        S[:31000] = 1.0 + rng.uniform(0, 1e-4, size=31000).astype(np.float32)
-        k = 12000
+        nc = int(31000 * f)
+        S[:nc] = 1.0 + rng.uniform(0, 1e-4, size=nc).astype(np.float32)
+        k = int(12000 * f)
     elif case == "prefix_fits":
         S = spread.copy()
-        S[:12000] = 1.0 + rng.uniform(0, 1e-4, size=12000).astype(np.float32)
-        k = 9000
+        nc = int(12000 * f)
+        S[:nc] = 1.0 + rng.uniform(0, 1e-4, size=nc).astype(np.float32)
+        k = int(9000 * f)
     elif case == "one_digit":
         # keys that differ only in their low 8 bits: a single radix digit
         S = (np.float32(1.0).view(np.uint32) + rng.integers(0, 200, size=P).astype(np.uint32)).view(np.float32)
-        k = 7000
+        k = int(7000 * f)
     else:  # "cluster_ties": 64 values inside the cluster, many equal to the threshold
         S = spread.copy()
-        S[:13000] = 1.0 + rng.integers(0, 64, size=13000).astype(np.float32) * np.float32(1e-6)
-        k = 11000
+        nc = int(13000 * f)
+        S[:nc] = 1.0 + rng.integers(0, 64, size=nc).astype(np.float32) * np.float32(1e-6)
+        k = int(11000 * f)
     rng.shuffle(S)
     return S.astype(np.float32), k
 
 
+@pytest.mark.parametrize("keys", [32000, 16000, 8000])  # 32, 16 and 8 keys per thread
 @pytest.mark.parametrize("case", ["prefix_overflow", "prefix_fits", "one_digit", "cluster_ties"])
-def test_select_register_digit_paths(case):
+def test_select_register_digit_paths(case, keys):
     import paper_2609_06663_amd as P
-    rng = np.random.default_rng({"prefix_overflow": 61, "prefix_fits": 62, "one_digit": 63, "cluster_ties": 64}[case])
+    rng = np.random.default_rng({"prefix_overflow": 61, "prefix_fits": 62, "one_digit": 63, "cluster_ties": 64}[case]
+                                + keys)
     w = 4
-    S1, k = _digit_case(case, rng)
-    S2, _ = _digit_case(case, rng)
+    S1, k = _digit_case(case, rng, keys)
+    S2, _ = _digit_case(case, rng, keys)
     L, Hkv = 1, 2
     cu = [0, len(S1) + w]
     S = np.stack([S1, S2])[None]  # [L][Hkv][P]
@@ -420,7 +427,7 @@ def test_select_register_digit_paths(case):
     idx = torch.full((n,), -7, dtype=torch.int32, device="cuda")
     counts = torch.full((L * Hkv,), -7, dtype=torch.int32, device="cuda")
     offsets = torch.full_like(counts, -7)
-    say(f"select-only bit-exact, {case}: 32000 keys, k = {k}")
+    say(f"select-only bit-exact, {case}: {keys} keys, k = {k}")
     P.ecokv_select(torch.from_numpy(np.ascontiguousarray(S)).cuda(), shape, P.PER_HEAD, budget, idx, counts, offsets)
     torch.cuda.synchronize()
     ref_idx, ref_c, ref_o = oracle.select(S.astype(np.float64), L, Hkv, cu, w, budget, oracle.PER_HEAD)
