@@ -54,22 +54,6 @@ constexpr int kTile = 128;            // keys per LDS tile (4 waves x 32 keys)
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-template <int CTRL>
-__device__ __forceinline__ float dpp(float x)
-{
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-
-// Sum over an aligned 16-lane row; every lane of the row gets the total.
-__device__ __forceinline__ float row16_sum(float x)
-{
-    x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
-    x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
-    x += dpp<0x141>(x);  // row_half_mirror
-    x += dpp<0x140>(x);  // row_mirror
-    return x;
-}
-
 __device__ __forceinline__ void unpack8(u32x4 q, float *v)
 {
 #pragma unroll

@@ -228,31 +228,92 @@ __device__ __forceinline__ void lds_barrier()
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t x) { return __uint_as_float((uint32_t)x << 16); }
 
-// Sum over the 16 lanes of an aligned 16-lane segment; every lane gets the total.
-__device__ __forceinline__ float seg16_sum(float x)
+// Lane moves within 16-lane rows (DPP, no LDS round trip): quad permutes, the
+// mirrored lane within each 8 and within each 16.
+template <int CTRL>
+__device__ __forceinline__ float dpp_row(float x)
 {
-    x += __shfl_xor(x, 8, 16);
-    x += __shfl_xor(x, 4, 16);
-    x += __shfl_xor(x, 2, 16);
-    x += __shfl_xor(x, 1, 16);
-    return x;
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
 }
 
-__device__ __forceinline__ float wave_sum(float x)
+// op over the S lanes of an aligned group (S = 16, 32 or 64), every lane
+// getting the result: butterflies by DPP within each 16-lane row (lane ^ 1,
+// lane ^ 2 by quad permutes, then the mirrored lane within 8 and within 16,
+// each pairing a lane with the other half), and one cross-lane move for each
+// further doubling (lane ^ 16, lane ^ 32).  The same operations in every lane,
+// so all hold the same value.
+template <int S, class Op>
+__device__ __forceinline__ float row_reduce(float x, Op op)
 {
-    for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, kWave);
+    static_assert(S == 16 || S == 32 || S == 64, "group of 16, 32 or 64 lanes");
+    x = op(x, dpp_row<0xB1>(x));   // quad_perm [1, 0, 3, 2]
+    x = op(x, dpp_row<0x4E>(x));   // quad_perm [2, 3, 0, 1]
+    x = op(x, dpp_row<0x141>(x));  // row_half_mirror
+    x = op(x, dpp_row<0x140>(x));  // row_mirror
+    if constexpr (S >= 32) x = op(x, __shfl_xor(x, 16, kWave));
+    if constexpr (S == 64) x = op(x, __shfl_xor(x, 32, kWave));
     return x;
 }
-__device__ __forceinline__ float wave_min(float x)
+struct OpAdd {
+    __device__ float operator()(float x, float y) const { return x + y; }
+};
+struct OpMin {
+    __device__ float operator()(float x, float y) const { return fminf(x, y); }
+};
+struct OpMax {
+    __device__ float operator()(float x, float y) const { return fmaxf(x, y); }
+};
+
+// The same on 32-bit unsigned values, and a DPP move with row / bank masks
+// (lanes outside them, or without a source lane, take 0).
+template <int CTRL, int ROWS = 0xF, int BANKS = 0xF>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x)
 {
-    for (int m = 32; m >= 1; m >>= 1) x = fminf(x, __shfl_xor(x, m, kWave));
-    return x;
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, BANKS, false);
 }
-__device__ __forceinline__ float wave_max(float x)
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x)
 {
-    for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m, kWave));
-    return x;
+    x = min(x, dpp_u32<0xB1>(x));
+    x = min(x, dpp_u32<0x4E>(x));
+    x = min(x, dpp_u32<0x141>(x));
+    x = min(x, dpp_u32<0x140>(x));
+    x = min(x, (uint32_t)__shfl_xor(x, 16, kWave));
+    return min(x, (uint32_t)__shfl_xor(x, 32, kWave));
 }
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x)
+{
+    x = max(x, dpp_u32<0xB1>(x));
+    x = max(x, dpp_u32<0x4E>(x));
+    x = max(x, dpp_u32<0x141>(x));
+    x = max(x, dpp_u32<0x140>(x));
+    x = max(x, (uint32_t)__shfl_xor(x, 16, kWave));
+    return max(x, (uint32_t)__shfl_xor(x, 32, kWave));
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave (lane i: x_0 + ... + x_i)
+// by DPP, with no LDS round trip: within each 16-lane row the inputs shifted
+// by 1, 2 and 3 lanes give sums of 4, the partial sums shifted by 4 (lanes
+// 4..15) and by 8 (lanes 8..15) sums of 8 and 16; then rows 1 and 3 add the
+// last lane of rows 0 and 2 (row broadcast 15) and rows 2 and 3 the last lane
+// of row 1 (row broadcast 31).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
+{
+    uint32_t v = x + dpp_u32<0x111>(x);  // row_shr:1
+    v += dpp_u32<0x112>(x);              // row_shr:2
+    v += dpp_u32<0x113>(x);              // row_shr:3
+    v += dpp_u32<0x114, 0xF, 0xE>(v);    // row_shr:4, banks 1-3
+    v += dpp_u32<0x118, 0xF, 0xC>(v);    // row_shr:8, banks 2-3
+    v += dpp_u32<0x142, 0xA, 0xF>(v);    // row_bcast:15 into rows 1, 3
+    v += dpp_u32<0x143, 0xC, 0xF>(v);    // row_bcast:31 into rows 2, 3
+    return v;
+}
+
+// Sum over the 16 lanes of an aligned 16-lane segment; every lane gets the total.
+__device__ __forceinline__ float seg16_sum(float x) { return row_reduce<16>(x, OpAdd{}); }
+
+__device__ __forceinline__ float wave_sum(float x) { return row_reduce<64>(x, OpAdd{}); }
+__device__ __forceinline__ float wave_min(float x) { return row_reduce<64>(x, OpMin{}); }
+__device__ __forceinline__ float wave_max(float x) { return row_reduce<64>(x, OpMax{}); }
 
 // Load the VEC = D/16 elements of segment c of a key row as float.
 template <int D, bool BF>
@@ -307,25 +368,19 @@ __device__ __forceinline__ T *uniform_ptr(T *p)
     return reinterpret_cast<T *>(uniform_i64(reinterpret_cast<int64_t>(p)));
 }
 
-template <int CTRL>
-__device__ __forceinline__ float dppf(float x)
-{
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-
-// Sum over the S lanes of a row group (S = 8, 16 or 32), in every lane, by DPP
-// butterflies: lane ^ 1, lane ^ 2 (quad permutes), then the mirrored lane
-// within 8 and within 16 (each pairs a lane with the other half); the same
-// additions in every lane, so all lanes hold the same sum.
+// Sum over the S lanes of a row group (S = 8, 16 or 32), in every lane: the
+// butterflies of row_reduce (S = 8 stops within each 8 lanes).
 template <int S>
 __device__ __forceinline__ float row_sum(float x)
 {
-    x += dppf<0xB1>(x);   // quad_perm [1, 0, 3, 2]
-    x += dppf<0x4E>(x);   // quad_perm [2, 3, 0, 1]
-    x += dppf<0x141>(x);  // row_half_mirror
-    if constexpr (S >= 16) x += dppf<0x140>(x);  // row_mirror
-    if constexpr (S == 32) x += __shfl_xor(x, 16, kWave);
-    return x;
+    if constexpr (S == 8) {
+        x += dpp_row<0xB1>(x);   // quad_perm [1, 0, 3, 2]
+        x += dpp_row<0x4E>(x);   // quad_perm [2, 3, 0, 1]
+        x += dpp_row<0x141>(x);  // row_half_mirror
+        return x;
+    } else {
+        return row_reduce<S>(x, OpAdd{});
+    }
 }
 
 // Order-preserving map of a float score to an unsigned radix key: larger

@@ -503,18 +503,18 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
         part[32 * wv + lane] = csum[0];              // sum of k
         part[kD + 32 * wv + lane] = csum[1] + csum[2];  // sum of k / |k|
     }
-    // per-row softmax partials: merge over the 32 lanes that hold the row
+    // per-row softmax partials over the 32 lanes that hold the row: the row's
+    // largest reference by a max butterfly, each lane's sum moved onto it (one
+    // exponential), then a sum butterfly, both by DPP within 16-lane rows (a
+    // pairwise merge per level by LDS shuffles took 10.8 of this block's 18 us
+    // on one 8192-token layer: dependent LDS round trips)
 #pragma unroll
     for (int t = 0; t < MT; ++t)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            float m = ms[t][i], s = ss[t][i];
-#pragma unroll
-            for (int mask = 1; mask < 32; mask <<= 1) {
-                const float m2 = __shfl_xor(m, mask, kWave);
-                const float s2 = __shfl_xor(s, mask, kWave);
-                softmax_merge2(m, s, m2, s2);
-            }
+            const float m = row_reduce<32>(ms[t][i], OpMax{});
+            float s = ms[t][i] == -INFINITY ? 0.f : ss[t][i] * fast_exp2(ms[t][i] - m);
+            s = row_reduce<32>(s, OpAdd{});
             if ((lane & 31) == 0) {
                 const int row = 32 * t + 8 * (i >> 2) + 4 * h + (i & 3);
                 wm[wv][row] = m;

@@ -77,16 +77,8 @@ __device__ __forceinline__ void for_each_key(const Src &key, int64_t n, F &&f)
     }
 }
 
-__device__ __forceinline__ uint32_t wave_min_u(uint32_t x)
-{
-    for (int m = 32; m >= 1; m >>= 1) x = min(x, (uint32_t)__shfl_xor(x, m, kWave));
-    return x;
-}
-__device__ __forceinline__ uint32_t wave_max_u(uint32_t x)
-{
-    for (int m = 32; m >= 1; m >>= 1) x = max(x, (uint32_t)__shfl_xor(x, m, kWave));
-    return x;
-}
+__device__ __forceinline__ uint32_t wave_min_u(uint32_t x) { return wave_min_u32(x); }
+__device__ __forceinline__ uint32_t wave_max_u(uint32_t x) { return wave_max_u32(x); }
 
 // Exact radix select of the k-th largest key (k >= 1) among n keys whose
 // extremes are kmin, kmax: digits of up to 8 bits, starting just below the
@@ -133,12 +125,7 @@ __device__ void radix_threshold(const Src &key, int64_t n, int64_t k, uint32_t k
                 c4[q] = hist[255 - 4 * lane - q];
                 loc += c4[q];
             }
-            uint32_t inc = loc;
-#pragma unroll
-            for (int d = 1; d < kWave; d <<= 1) {
-                const uint32_t y = __shfl_up(inc, d, kWave);
-                if (lane >= d) inc += y;
-            }
+            uint32_t inc = wave_incl_scan(loc);
             const uint32_t before = inc - loc;
             if ((int64_t)before < rem && rem <= (int64_t)inc) {
                 uint32_t cum = before;
@@ -257,12 +244,7 @@ __device__ __forceinline__ void reg_radix_select(const uint32_t (&kk)[KPT], int 
                 c4[q] = hsum[255 - 4 * lane - q];
                 loc += c4[q];
             }
-            uint32_t inc = loc;
-#pragma unroll
-            for (int d = 1; d < kWave; d <<= 1) {
-                const uint32_t y = __shfl_up(inc, d, kWave);
-                if (lane >= d) inc += y;
-            }
+            uint32_t inc = wave_incl_scan(loc);
             const uint32_t before = inc - loc;
             if ((int)before < rem && rem <= (int)inc) {
                 uint32_t cum = before;
@@ -484,15 +466,7 @@ __device__ __forceinline__ void block_exscan2(uint32_t x0, uint32_t x1, uint32_t
                                               uint32_t &t0, uint32_t &t1)
 {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    uint32_t i0 = x0, i1 = x1;
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        const uint32_t y0 = __shfl_up(i0, d, kWave), y1 = __shfl_up(i1, d, kWave);
-        if (lane >= d) {
-            i0 += y0;
-            i1 += y1;
-        }
-    }
+    const uint32_t i0 = wave_incl_scan(x0), i1 = wave_incl_scan(x1);
     if (lane == kWave - 1) {
         wsum[wv] = i0;
         wsum[kSelWaves + 1 + wv] = i1;
@@ -501,15 +475,7 @@ __device__ __forceinline__ void block_exscan2(uint32_t x0, uint32_t x1, uint32_t
     if (wv == 0) {
         uint32_t a0 = lane < kSelWaves ? wsum[lane] : 0u;
         uint32_t a1 = lane < kSelWaves ? wsum[kSelWaves + 1 + lane] : 0u;
-        uint32_t c0 = a0, c1 = a1;
-#pragma unroll
-        for (int d = 1; d < kSelWaves; d <<= 1) {
-            const uint32_t y0 = __shfl_up(c0, d, kWave), y1 = __shfl_up(c1, d, kWave);
-            if (lane >= d) {
-                c0 += y0;
-                c1 += y1;
-            }
-        }
+        const uint32_t c0 = wave_incl_scan(a0), c1 = wave_incl_scan(a1);  // (lanes past the waves add 0)
         if (lane < kSelWaves) {
             wsum[lane] = c0 - a0;
             wsum[kSelWaves + 1 + lane] = c1 - a1;
@@ -561,12 +527,7 @@ __device__ __forceinline__ void pick_digit(uint32_t *h, bool clear, int rem, uin
         if (clear) h[255 - 4 * lane - q] = 0u;
         loc += c4[q];
     }
-    uint32_t inc = loc;
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        const uint32_t y = __shfl_up(inc, d, kWave);
-        if (lane >= d) inc += y;
-    }
+    uint32_t inc = wave_incl_scan(loc);
     const uint32_t before = inc - loc;
     if ((int)before < rem && rem <= (int)inc) {
         uint32_t cum = before;
@@ -647,16 +608,11 @@ __device__ __forceinline__ void reg_radix_select_staged(const uint32_t (&kk)[KPT
         uint32_t cnt = 0;
 #pragma unroll
         for (int q = 0; q < KPT; ++q) cnt += (v0 + q < n && (kk[q] & mask) == prefix) ? 1u : 0u;
-        uint32_t inc = cnt;
-#pragma unroll
-        for (int d = 1; d < kWave; d <<= 1) {
-            const uint32_t y = __shfl_up(inc, d, kWave);
-            if (lane >= d) inc += y;
-        }
-        const uint32_t wtot = __shfl(inc, kWave - 1, kWave);
+        uint32_t inc = wave_incl_scan(cnt);
+        const uint32_t wtot = (uint32_t)__builtin_amdgcn_readlane((int)inc, kWave - 1);
         uint32_t base = 0;
         if (lane == kWave - 1 && wtot > 0) base = atomicAdd(ccount, wtot);
-        base = __shfl(base, kWave - 1, kWave);
+        base = (uint32_t)__builtin_amdgcn_readlane((int)base, kWave - 1);
         uint32_t pos = base + inc - cnt;
 #pragma unroll
         for (int q = 0; q < KPT; ++q)
@@ -703,7 +659,6 @@ __device__ __forceinline__ void reg_radix_select_staged(const uint32_t (&kk)[KPT
 // (16-byte loads in per-head mode), the radix passes histogram them into one
 // LDS copy per wave, and the ordered emission walks the registers.
 // ---------------------------------------------------------------------------
-constexpr int kRegMaxKeys = 64 * kSelThreads;
 
 template <int KPT>
 __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
@@ -1037,12 +992,7 @@ __device__ __forceinline__ void mb_load(const MbGroup &g, int64_t r0, uint32_t (
 __device__ __forceinline__ uint32_t mb_exscan(uint32_t x, uint32_t *ws, uint32_t *total)
 {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    uint32_t inc = x;
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        const uint32_t y = __shfl_up(inc, d, kWave);
-        if (lane >= d) inc += y;
-    }
+    uint32_t inc = wave_incl_scan(x);
     if (lane == kWave - 1) ws[wv] = inc;
     __syncthreads();
     uint32_t before = 0, tot = 0;
