@@ -1144,6 +1144,17 @@ __global__ __launch_bounds__(256) void k_pre_anchors(ScoreArgs a)
 // With PRE (ecokv_prefill_write) the unit's sums are written to a.pre_out in
 // the layout ecokv_score_pre takes: plain sums, and the row maxima in natural
 // units (max q.k / sqrt(D)).
+// op over an aligned group of 4 or 16 lanes (a quad, a DPP row), every lane
+// getting the result.
+template <int LANES, class Op>
+__device__ __forceinline__ float lane_group_reduce(float x, Op op)
+{
+    static_assert(LANES == 4 || LANES == 16, "a quad or a 16-lane row");
+    if constexpr (LANES == 16) return row_reduce<16>(x, op);
+    x = op(x, dpp_row<0xB1>(x));  // quad_perm [1, 0, 3, 2]
+    return op(x, dpp_row<0x4E>(x));  // quad_perm [2, 3, 0, 1]
+}
+
 template <int LANES, bool PRE>
 __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
 {
@@ -1163,8 +1174,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
             float s = 0.f;
 #pragma unroll 4
             for (int b = q; b < nb; b += lanes) s += p[(int64_t)b * stride + c];
-#pragma unroll
-            for (int x = 1; x < lanes; x <<= 1) s += __shfl_xor(s, x, lanes);
+            s = lane_group_reduce<lanes>(s, OpAdd{});
             if (q == 0) anc[c] = PRE ? s : c < a.D ? centroid_component(a, un, T, c, s) : s / (float)T;
         } else {
             const int r = c - 2 * a.D;
@@ -1172,11 +1182,10 @@ __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
 #pragma unroll 4
             for (int b = q; b < nb; b += lanes)
                 softmax_merge2(m, s, p[(int64_t)b * stride + 2 * a.D + r], p[(int64_t)b * stride + 2 * a.D + a.R + r]);
-#pragma unroll
-            for (int x = 1; x < lanes; x <<= 1) {
-                const float m2 = __shfl_xor(m, x, lanes), s2 = __shfl_xor(s, x, lanes);
-                softmax_merge2(m, s, m2, s2);
-            }
+            // the group's largest reference, each lane's sum moved onto it, summed
+            const float mg = lane_group_reduce<lanes>(m, OpMax{});
+            s = lane_group_reduce<lanes>(m == -INFINITY ? 0.f : s * __builtin_amdgcn_exp2f(m - mg), OpAdd{});
+            m = mg;
             if (q == 0) {
                 anc[2 * a.D + r] = PRE ? m * (1.f / kLog2e) : m;
                 anc[2 * a.D + a.R + r] = s;
