@@ -625,6 +625,26 @@ def main():
     per_layer_calls["two_streams_ms_per_step"] = round(ms2, 4)
     per_layer_calls["two_streams_us_per_layer"] = round(ms2 * 1e3 / L, 2)
     del ep1, lw, Ks, Vs, Qs
+    # a call per group of consecutive layers (as a prefill can issue every few
+    # layers), alternating over two streams
+    for k in (2, 4):
+        if L % k:
+            continue
+        log(f"{L // k} calls of {k} layers on two streams")
+        shapek = P.Shape(k, Hq, Hkv, D, w, wl.cu_seqlens)
+        lwk = LayerwiseEviction(shapek, [b], L)
+        Kg = [K[c * k:(c + 1) * k] for c in range(L // k)]
+        Vg = [V[c * k:(c + 1) * k] for c in range(L // k)]
+        Qg = [Q[c * k:(c + 1) * k] for c in range(L // k)]
+
+        def groups():
+            lwk.run_layers(range(L // k), Kg, Vg, Qg)
+            lwk.wait()
+
+        msk = timed(groups, args.steps, stream)
+        lwk.check()
+        per_layer_calls[f"groups_of_{k}_two_streams_us_per_layer"] = round(msk * 1e3 / L, 2)
+        del lwk, Kg, Vg, Qg
 
     # a plain device copy of 1 GiB (torch's copy kernel), for the bandwidth the
     # memory system gives an ordinary streaming kernel next to the 8 TB/s peak

@@ -77,50 +77,66 @@ class EvictionPass:
 
 
 class LayerwiseEviction:
-    """The pass for one layer at a time, as a prefill finishes each layer.
+    """The pass layer by layer as a prefill finishes the layers, one call per
+    layer or per group of consecutive layers.
 
-    Layer l runs on the l % 2-th of two side streams (default priority), with
-    its own outputs (`passes[l]`: scores, idx, counts, offsets, Kc, Vc) and the
-    workspace of its stream.  One layer's select and epilogue occupy only a few
-    compute units; on two streams they overlap the next layer's sweeps (28
-    layers of 28q/4kv at 32768 tokens: 77 -> 48 us per layer).  `run_layer`
-    orders the layer after the work already queued on the caller's stream;
-    `wait` makes the caller's stream wait for every layer queued so far.  The
-    caller keeps a layer's K, V and Q_win alive until `wait` (they are read on
-    a side stream, which torch's allocator does not track).  The per-layer
-    host work is one event record and wait plus the three library calls.
+    `shape` is the shape of one call: num_layers = 1 for a call per layer, or
+    k > 1 for a call per group of k consecutive layers (whose K, V and Q_win
+    the caller passes as [k][...] tensors, e.g. views of a cache laid out layer
+    by layer).  Call c runs on the c % 2-th of two side streams (default
+    priority), with its own outputs (`passes[c]`: scores, idx, counts, offsets,
+    Kc, Vc) and the workspace of its stream.  One call's select and epilogue
+    occupy only a few compute units; on two streams they overlap the next
+    call's sweeps (28 layers of 28q/4kv at 32768 tokens: 77 -> 48 us per layer
+    with a call per layer); a group of layers per call fills more of the chip
+    per launch.  `run_layer` / `run_group` order the call after the work
+    already queued on the caller's stream; `wait` makes the caller's stream
+    wait for every call queued so far.  The caller keeps a call's K, V and
+    Q_win alive until `wait` (they are read on a side stream, which torch's
+    allocator does not track).  The host work per call is one event record
+    and wait plus the three library calls.
     """
 
     def __init__(self, shape: E.Shape, budget, num_layers: int, mode: int = E.PER_HEAD,
                  params: Optional[E.Params] = None, dtype: torch.dtype = torch.bfloat16, device: str = "cuda"):
-        if shape.c.num_layers != 1:
-            raise ValueError("LayerwiseEviction takes the shape of one layer (num_layers = 1)")
+        k = shape.c.num_layers
+        if k < 1 or num_layers % k != 0:
+            raise ValueError(f"the call shape's {k} layers must divide the {num_layers} layers")
+        self.layers_per_call = k
         params = params or E.Params()
         ws = max(E.ecokv_workspace_size(shape, params), 256)
         self.streams = [torch.cuda.Stream(device=device), torch.cuda.Stream(device=device)]
         self.workspaces = [torch.zeros(ws, dtype=torch.uint8, device=device) for _ in range(2)]
-        self.passes = [EvictionPass(shape, budget, mode, params, dtype, device, self.workspaces[l % 2])
-                       for l in range(num_layers)]
+        self.passes = [EvictionPass(shape, budget, mode, params, dtype, device, self.workspaces[c % 2])
+                       for c in range(num_layers // k)]
         self._ready = [torch.cuda.Event(), torch.cuda.Event()]
         self._done = [torch.cuda.Event(), torch.cuda.Event()]
 
-    def run_layer(self, layer: int, K: torch.Tensor, V: torch.Tensor, Q_win: torch.Tensor) -> EvictionPass:
-        i = layer % 2
+    def run_group(self, call: int, K: torch.Tensor, V: torch.Tensor, Q_win: torch.Tensor) -> EvictionPass:
+        """Call `call`: layers call * k .. call * k + k - 1 (K, V, Q_win over them)."""
+        i = call % 2
         s, ready = self.streams[i], self._ready[i]
         ready.record(torch.cuda.current_stream(K.device))
         s.wait_event(ready)
-        return self.passes[layer].run(K, V, Q_win, stream=s)
+        return self.passes[call].run(K, V, Q_win, stream=s)
 
-    def run_layers(self, layers, K, V, Q_win):
-        """Several layers whose inputs are all ready: one ordering event for
-        all of them (per-layer events cost 48 -> 54 us per layer on the
-        28-layer stack).  K, V, Q_win: sequences indexed like `layers`."""
+    def run_layer(self, layer: int, K: torch.Tensor, V: torch.Tensor, Q_win: torch.Tensor) -> EvictionPass:
+        """One layer per call (the call shape's num_layers = 1)."""
+        if self.layers_per_call != 1:
+            raise ValueError("this instance takes groups of layers: use run_group")
+        return self.run_group(layer, K, V, Q_win)
+
+    def run_layers(self, calls, K, V, Q_win):
+        """Several calls whose inputs are all ready: one ordering event for
+        all of them (per-call events cost 48 -> 54 us per layer on the
+        28-layer stack with a call per layer).  K, V, Q_win: sequences indexed
+        like `calls`."""
         cur = torch.cuda.current_stream(self.workspaces[0].device)
         for s, ready in zip(self.streams, self._ready):
             ready.record(cur)
             s.wait_event(ready)
-        for j, layer in enumerate(layers):
-            self.passes[layer].run(K[j], V[j], Q_win[j], stream=self.streams[layer % 2])
+        for j, c in enumerate(calls):
+            self.passes[c].run(K[j], V[j], Q_win[j], stream=self.streams[c % 2])
 
     def wait(self):
         cur = torch.cuda.current_stream(self.workspaces[0].device)
