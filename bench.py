@@ -61,7 +61,7 @@ STAGE_KERNELS = {
     "epilogue1": ["k_epi1"], "epilogue2": ["k_epi2"],
     "select": ["k_select_reg", "k_select", "k_sel_digit", "k_sel_count", "k_sel_emit"], "compact": ["k_compact"], "vnorm": ["k_vnorm"],
     "dquant": ["k_dquant", "k_dquant_reg"], "decode": ["k_decode_mx", "k_decode"], "decode_merge": ["k_decode_merge"],
-    "pre_anchors": ["k_pre_anchors"], "prefill_sweep": [], "prefill_reduce": [], "prefill_copy": [],
+    "prefill_sweep": [], "prefill_reduce": [], "prefill_copy": [],
 }
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, vendor figure
 COPY_BYTES = 1 << 30  # size of the calibration copy in --counter-run

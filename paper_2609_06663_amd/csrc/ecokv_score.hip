@@ -36,6 +36,48 @@ namespace ecokv {
 constexpr int kThreads = 256;
 constexpr int kCh = 128;        // key rows per block, generic sweeps
 
+// Component c of kbar from the sum of the unit's T keys: divided by T, or,
+// with the centroid over the non-window keys, the w window rows taken out
+// and divided by P.
+__device__ __forceinline__ float centroid_component(const ScoreArgs &a, const Unit &un, int T, int c, float s)
+{
+    if (!a.centroid_prefix) return s / (float)T;
+    const int64_t r0 = unit_row0(a, un) + (T - a.w);
+    float ws = 0.f;
+    for (int j = 0; j < a.w; ++j) {
+        const int64_t off = (r0 + j) * a.D + c;
+        ws += a.kbf16 ? __uint_as_float((uint32_t)static_cast<const uint16_t *>(a.K)[off] << 16)
+                      : static_cast<const float *>(a.K)[off];
+    }
+    return (s - ws) / (float)(T - a.w);
+}
+
+// Anchor column c of unit u (the layout of a.anchors: kbar, mu, the window
+// rows' base-2 references and sums): from the workspace after the first sweep,
+// or converted from the sums a prefill handed over (ecokv_score_pre: plain
+// sums over the T keys, references in natural units).
+__device__ __forceinline__ float anchor_value(const ScoreArgs &a, const Unit &un, int u, int T, int c)
+{
+    const int64_t at = (int64_t)u * (2 * a.D + 2 * a.R) + c;
+    if (!a.pre) return a.anchors[at];
+    const float v = a.pre[at];
+    if (c < a.D) return centroid_component(a, un, T, c, v);
+    if (c < 2 * a.D) return v / (float)T;
+    if (c < 2 * a.D + a.R) return v * kLog2e;
+    return v;
+}
+
+// The unit's anchors for a sweep-2 block: the workspace row after the first
+// sweep, or, with handed-over sums, the converted row staged in `lds` (every
+// thread of the block calls it; a.pre is the same for the whole launch).
+__device__ __forceinline__ const float *unit_anchors(const ScoreArgs &a, const Unit &un, int u, int T, float *lds)
+{
+    if (!a.pre) return a.anchors + (int64_t)u * (2 * a.D + 2 * a.R);
+    for (int c = threadIdx.x; c < 2 * a.D + 2 * a.R; c += blockDim.x) lds[c] = anchor_value(a, un, u, T, c);
+    __syncthreads();
+    return lds;
+}
+
 // ---------------------------------------------------------------------------
 // Generic sweeps (fp32 or head_dim 64): 16 lanes per key row.
 // ---------------------------------------------------------------------------
@@ -156,17 +198,14 @@ __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
     const int P = T - a.w;
     const int row0 = blockIdx.x * kCh;
     if (row0 >= T) return;
-    const int stride = 2 * D + 2 * a.R;
-    const float *anc = a.anchors + (int64_t)u * stride;
-
     load_window_rows<D, BF>(a, un, q_lds);
     for (int d = threadIdx.x; d < D; d += blockDim.x) {
-        kb[d] = anc[d];
-        mu[d] = anc[D + d];
+        kb[d] = anchor_value(a, un, u, T, d);
+        mu[d] = anchor_value(a, un, u, T, D + d);
     }
     for (int r = threadIdx.x; r < a.R; r += blockDim.x) {
-        rm[r] = anc[2 * D + r];
-        rs_inv[r] = 1.f / anc[2 * D + a.R + r];
+        rm[r] = anchor_value(a, un, u, T, 2 * D + r);
+        rs_inv[r] = 1.f / anchor_value(a, un, u, T, 2 * D + a.R + r);
     }
     __syncthreads();
 
@@ -557,8 +596,8 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
     const int c = tid & 15, g = tid >> 4, h = lane >> 5;
     const uint16_t *krow0 = static_cast<const uint16_t *>(a.K) + unit_row0(a, un) * kD;
     const int64_t obase = unit_out_base(a, un);
-    const int stride = 2 * kD + 2 * a.R;
-    const float *anc = a.anchors + (int64_t)u * stride;
+    __shared__ __attribute__((aligned(16))) float sanc[2 * kD + 2 * ECOKV_MAX_ROWS];
+    const float *anc = unit_anchors(a, un, u, T, sanc);
     const float sc = a.inv_sqrt_d * kLog2e;
 
     bf16x8 aq[MT][8];
@@ -709,8 +748,8 @@ __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint16_t *krow0 = static_cast<const uint16_t *>(a.K) + unit_row0(a, un) * kD;
     const int64_t obase = unit_out_base(a, un);
-    const int stride = 2 * kD + 2 * a.R;
-    const float *anc = a.anchors + (int64_t)u * stride;
+    __shared__ __attribute__((aligned(16))) float sanc[2 * kD + 2 * ECOKV_MAX_ROWS];
+    const float *anc = unit_anchors(a, un, u, T, sanc);
     const float sc = a.inv_sqrt_d * kLog2e;
     constexpr int kAnc = 32 - 2;
 
@@ -1104,43 +1143,6 @@ __global__ __launch_bounds__(256, 2) void k_fs1s(ScoreArgs a)
 constexpr int kReduceThreads = 1024;
 inline int reduce1_lanes(int nch1) { return nch1 > 16 ? 16 : 4; }
 
-// Component c of kbar from the sum of the unit's T keys: divided by T, or,
-// with the centroid over the non-window keys, the w window rows taken out
-// and divided by P.
-__device__ __forceinline__ float centroid_component(const ScoreArgs &a, const Unit &un, int T, int c, float s)
-{
-    if (!a.centroid_prefix) return s / (float)T;
-    const int64_t r0 = unit_row0(a, un) + (T - a.w);
-    float ws = 0.f;
-    for (int j = 0; j < a.w; ++j) {
-        const int64_t off = (r0 + j) * a.D + c;
-        ws += a.kbf16 ? __uint_as_float((uint32_t)static_cast<const uint16_t *>(a.K)[off] << 16)
-                      : static_cast<const float *>(a.K)[off];
-    }
-    return (s - ws) / (float)(T - a.w);
-}
-
-// The anchors from sums a prefill supplied (ecokv_score_pre) instead of the
-// first sweep: sum k and sum k/|k| over the T keys, and per window row its
-// max logit (natural units) and sum of exp(logit - max).  The row maxima are
-// kept in base 2, as the first sweep produces them.
-__global__ __launch_bounds__(256) void k_pre_anchors(ScoreArgs a)
-{
-    const int u = blockIdx.x;
-    const Unit un = unit_of(u, a.Hkv, a.B);
-    const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
-    const int stride = 2 * a.D + 2 * a.R;
-    const float *p = a.pre + (int64_t)u * stride;
-    float *anc = a.anchors + (int64_t)u * stride;
-    for (int c = threadIdx.x; c < stride; c += blockDim.x) {
-        const float v = p[c];
-        if (c < a.D) anc[c] = centroid_component(a, un, T, c, v);
-        else if (c < 2 * a.D) anc[c] = v / (float)T;
-        else if (c < 2 * a.D + a.R) anc[c] = v * kLog2e;
-        else anc[c] = v;
-    }
-}
-
 // With PRE (ecokv_prefill_write) the unit's sums are written to a.pre_out in
 // the layout ecokv_score_pre takes: plain sums, and the row maxima in natural
 // units (max q.k / sqrt(D)).
@@ -1461,8 +1463,7 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
     const int i1 = min(i0 + kEpiKeys, P);
     const int64_t ob = unit_out_base(a, un);
     const float *dbuf = a.bufA + ob, *cbuf = a.bufB + ob, *abuf = a.bufC + ob;
-    const int stride = 2 * a.D + 2 * a.R;
-    const float *mu = a.anchors + (int64_t)u * stride + a.D;
+
 
     const Red4 dst = unit_distance_stats(a, u, T, lds);
     Red4 v{0.f, 0.f, INFINITY, -INFINITY};
@@ -1476,7 +1477,10 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
     }
     const Red4 sd = block_red4(v, lds);
     Red4 m2{0.f, 0.f, 0.f, 0.f};
-    for (int d = threadIdx.x; d < a.D; d += blockDim.x) m2.s0 += mu[d] * mu[d];
+    for (int d = threadIdx.x; d < a.D; d += blockDim.x) {
+        const float mv = anchor_value(a, un, u, T, a.D + d);
+        m2.s0 += mv * mv;
+    }
     const float mu2 = block_red4(m2, lds).s0;
     const EpiConsts k = epi_consts(a, dst, sd, mu2, T, P);
     const float lam = k.lam, smin = k.smin, sden = k.sden, scale = k.scale;
@@ -1528,7 +1532,6 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
 constexpr int kUThreads = 1024;
 constexpr int kUW = kUThreads / kWave;
 constexpr int kUKeys = kUThreads * 32;  // 32768 keys per unit
-constexpr int kUSpinLimit = 1 << 20;  // polls (a few seconds): the partner block only has to be scheduled
 
 // Block sum / min / max whose barriers order LDS only, so that global loads
 // issued before it stay in flight.
@@ -1597,8 +1600,7 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
     const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
     const int P = T - a.w;
     const int64_t ob = unit_out_base(a, un);
-    const int stride = 2 * a.D + 2 * a.R;
-    const float *mu = a.anchors + (int64_t)u * stride + a.D;
+
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int half = a.pool_half;  // <= kPoolHalfMax (checked on the host)
     const int kw = kPartKeys * part + kWaveKeys * wv;
@@ -1620,7 +1622,7 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
         v.mx = pp[2];
         dq2 = pp[3];
     }
-    const float mv = (int)threadIdx.x < a.D ? mu[threadIdx.x] : 0.f;
+    const float mv = (int)threadIdx.x < a.D ? anchor_value(a, un, u, T, a.D + (int)threadIdx.x) : 0.f;
     const __amdgpu_buffer_rsrc_t rd = float_rsrc(a.bufA + ob, P), rc = float_rsrc(a.bufB + ob, P),
                                  ra = float_rsrc(a.bufC + ob, P);
     f32x4 xd[kVec], xc[kVec], xa[kVec];
@@ -1963,8 +1965,8 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
         const dim3 grid(a.nch1, U);
         if (a.pre) {
-            // the first sweep's sums come from the caller: K is read once
-            ECOKV_TIMED("pre_anchors", st, hipLaunchKernelGGL(k_pre_anchors, dim3(U), dim3(256), 0, st, a));
+            // the first sweep's sums come from the caller: K is read once (the
+            // sweep-2 blocks and the epilogue convert them as they read them)
         } else {
             if (score_fast_path(a.D, bf16) && a.R <= 32) {
                 // streaming sweep 1: one 32-row window operand
