@@ -1157,10 +1157,11 @@ __device__ __forceinline__ float lane_group_reduce(float x, Op op)
     return op(x, dpp_row<0x4E>(x));  // quad_perm [2, 3, 0, 1]
 }
 
+// Columns cg, cg + ncg, ... (in groups of blockDim.x / LANES) of unit u's
+// partials, LANES lanes per column; the calling block's threads all take part.
 template <int LANES, bool PRE>
-__global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
+__device__ __forceinline__ void reduce1_columns(const ScoreArgs &a, int u, int cg, int ncg)
 {
-    const int u = blockIdx.x;
     const Unit un = unit_of(u, a.Hkv, a.B);
     const int T = a.seq.cu[un.s + 1] - a.seq.cu[un.s];
     const int nb = (T + a.rpb1 - 1) / a.rpb1;
@@ -1168,10 +1169,10 @@ __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
     const float *p = a.part1 + (int64_t)u * a.nch1 * stride;
     float *anc = (PRE ? a.pre_out : a.anchors) + (int64_t)u * stride;
     constexpr int lanes = LANES;
-    constexpr int cpb = kReduceThreads / lanes;  // columns per block per step
+    const int cpb = blockDim.x / lanes;  // columns per block per step
     const int q = threadIdx.x & (lanes - 1);
     // (every lane of a column takes the same path: the butterflies stay within it)
-    for (int c = blockIdx.y * cpb + threadIdx.x / lanes; c < 2 * a.D + a.R; c += gridDim.y * cpb) {
+    for (int c = cg * cpb + threadIdx.x / lanes; c < 2 * a.D + a.R; c += ncg * cpb) {
         if (c < 2 * a.D) {
             float s = 0.f;
 #pragma unroll 4
@@ -1194,6 +1195,12 @@ __global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
             }
         }
     }
+}
+
+template <int LANES, bool PRE>
+__global__ __launch_bounds__(kReduceThreads) void k_reduce1(ScoreArgs a)
+{
+    reduce1_columns<LANES, PRE>(a, blockIdx.x, blockIdx.y, gridDim.y);
 }
 
 // ---------------------------------------------------------------------------
@@ -2057,17 +2064,17 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
 // ecokv_prefill_write: the KV-cache write of a prefill with the first sweep.
 // ---------------------------------------------------------------------------
 
-// Copy of every unit's rows from the token-major new rows ([L][Ttot][Hkv] rows
-// of rowb bytes) to the head-major cache ([L][Hkv][Ttot] rows), 16 bytes per
-// thread and step; block (x, u) copies rows 64 x .. 64 x + 63 of unit u.
+// Copy of unit u's rows x * kCopyRows .. x * kCopyRows + 63 from the
+// token-major new rows ([L][Ttot][Hkv] rows of rowb bytes) to the head-major
+// cache ([L][Hkv][Ttot] rows), 16 bytes per thread and step, streamed past
+// the caches.
 constexpr int kCopyRows = 64;
-__global__ __launch_bounds__(256) void k_rows_copy(const char *src, char *dst, int rowb, int L, int Hkv, int B,
-                                                   int64_t Ttot, SeqTab seq)
+__device__ __forceinline__ void copy_unit_rows(const char *src, char *dst, int rowb, int Hkv, int B, int64_t Ttot,
+                                               const SeqTab &seq, int u, int x)
 {
-    const int u = blockIdx.y;
     const Unit un = unit_of(u, Hkv, B);
     const int T = seq.cu[un.s + 1] - seq.cu[un.s];
-    const int r0 = blockIdx.x * kCopyRows;
+    const int r0 = x * kCopyRows;
     if (r0 >= T) return;
     const int rows = min(kCopyRows, T - r0);
     const int pr = rowb / 16;  // 16-byte pieces per row
@@ -2077,9 +2084,32 @@ __global__ __launch_bounds__(256) void k_rows_copy(const char *src, char *dst, i
     typedef unsigned v4u __attribute__((ext_vector_type(4)));
     for (int p = threadIdx.x; p < rows * pr; p += blockDim.x) {
         const int r = p / pr, c = p - r * pr;
-        const v4u x = __builtin_nontemporal_load(reinterpret_cast<const v4u *>(s0 + (int64_t)r * Hkv * rowb) + c);
-        __builtin_nontemporal_store(x, reinterpret_cast<v4u *>(d0 + (int64_t)r * rowb) + c);
+        const v4u v = __builtin_nontemporal_load(reinterpret_cast<const v4u *>(s0 + (int64_t)r * Hkv * rowb) + c);
+        __builtin_nontemporal_store(v, reinterpret_cast<v4u *>(d0 + (int64_t)r * rowb) + c);
     }
+}
+
+__global__ __launch_bounds__(256) void k_rows_copy(const char *src, char *dst, int rowb, int L, int Hkv, int B,
+                                                   int64_t Ttot, SeqTab seq)
+{
+    copy_unit_rows(src, dst, rowb, Hkv, B, Ttot, seq, blockIdx.y, blockIdx.x);  // block (x, u)
+}
+
+// The V rows' copy and the reduction of the K sweep's block partials into
+// `pre` in one launch: blocks [0, nred) reduce (unit, group of 16 columns),
+// 16 lanes per column, and the rest copy V rows as k_rows_copy does, ncx
+// blocks per unit; the reduction's few loads then hide under the copy's
+// stream instead of taking a launch of their own.
+__global__ __launch_bounds__(256) void k_copy_reduce_pre(ScoreArgs a, const char *src, char *dst, int rowb, int ncg,
+                                                         int ncx)
+{
+    const int nred = a.L * a.Hkv * a.B * ncg;
+    if ((int)blockIdx.x < nred) {
+        reduce1_columns<16, true>(a, blockIdx.x / ncg, blockIdx.x % ncg, ncg);
+        return;
+    }
+    const int cb = blockIdx.x - nred;
+    copy_unit_rows(src, dst, rowb, a.Hkv, a.B, a.Ttot, a.seq, cb / ncx, cb % ncx);
 }
 
 size_t prefill_ws_bytes(int L, int Hkv, int B, int D, int R, int maxT, bool bf16)
@@ -2126,21 +2156,24 @@ hipError_t prefill_launch(ScoreArgs a, const void *Vsrc, void *Vdst, char *ws, i
         ECOKV_TIMED("prefill_sweep", st, launch_sweep(1, a, dim3(a.nch1, U), st, bf16));
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (reduce1_lanes(a.nch1) == 4)
+    if (Vsrc) {
+        // V's copy with the reduction into pre riding on it
+        const int ncg = (2 * a.D + a.R + 15) / 16;
+        const int64_t blocks = (int64_t)U * ncg + (int64_t)gc.x * U;
+        if (blocks > INT32_MAX) return hipErrorInvalidConfiguration;
+        ECOKV_TIMED("prefill_copy_v", st,
+                    hipLaunchKernelGGL(k_copy_reduce_pre, dim3((unsigned)blocks), dim3(256), 0, st, a,
+                                       static_cast<const char *>(Vsrc), static_cast<char *>(Vdst), a.D * es, ncg,
+                                       (int)gc.x));
+    } else if (reduce1_lanes(a.nch1) == 4) {
         ECOKV_TIMED("prefill_reduce", st,
                     hipLaunchKernelGGL((k_reduce1<4, true>), dim3(U), dim3(kReduceThreads), 0, st, a));
-    else
+    } else {
         ECOKV_TIMED("prefill_reduce", st,
                     hipLaunchKernelGGL((k_reduce1<16, true>), dim3(U, (2 * a.D + a.R + 63) / 64),
                                        dim3(kReduceThreads), 0, st, a));
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (Vsrc) {
-        ECOKV_TIMED("prefill_copy_v", st,
-                    hipLaunchKernelGGL(k_rows_copy, gc, dim3(256), 0, st, static_cast<const char *>(Vsrc),
-                                       static_cast<char *>(Vdst), a.D * es, a.L, a.Hkv, a.B, a.Ttot, a.seq));
-        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    return hipSuccess;
+    return hipGetLastError();
 }
 
 }  // namespace ecokv
