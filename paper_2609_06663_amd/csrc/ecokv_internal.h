@@ -238,18 +238,18 @@ __device__ __forceinline__ float dpp_row(float x)
 
 // op over the S lanes of an aligned group (S = 16, 32 or 64), every lane
 // getting the result: butterflies by DPP within each 16-lane row (lane ^ 1,
-// lane ^ 2 by quad permutes, then the mirrored lane within 8 and within 16,
-// each pairing a lane with the other half), and one cross-lane move for each
-// further doubling (lane ^ 16, lane ^ 32).  The same operations in every lane,
+// lane ^ 2 by quad permutes, then the mirrored lane within 8 and, for groups
+// of 16 or more, within 16, each pairing a lane with the other half), and one
+// cross-lane move for each further doubling (lane ^ 16, lane ^ 32).  The same operations in every lane,
 // so all hold the same value.
 template <int S, class Op>
 __device__ __forceinline__ float row_reduce(float x, Op op)
 {
-    static_assert(S == 16 || S == 32 || S == 64, "group of 16, 32 or 64 lanes");
+    static_assert(S == 8 || S == 16 || S == 32 || S == 64, "group of 8, 16, 32 or 64 lanes");
     x = op(x, dpp_row<0xB1>(x));   // quad_perm [1, 0, 3, 2]
     x = op(x, dpp_row<0x4E>(x));   // quad_perm [2, 3, 0, 1]
     x = op(x, dpp_row<0x141>(x));  // row_half_mirror
-    x = op(x, dpp_row<0x140>(x));  // row_mirror
+    if constexpr (S >= 16) x = op(x, dpp_row<0x140>(x));  // row_mirror
     if constexpr (S >= 32) x = op(x, __shfl_xor(x, 16, kWave));
     if constexpr (S == 64) x = op(x, __shfl_xor(x, 32, kWave));
     return x;
@@ -368,19 +368,11 @@ __device__ __forceinline__ T *uniform_ptr(T *p)
     return reinterpret_cast<T *>(uniform_i64(reinterpret_cast<int64_t>(p)));
 }
 
-// Sum over the S lanes of a row group (S = 8, 16 or 32), in every lane: the
-// butterflies of row_reduce (S = 8 stops within each 8 lanes).
+// Sum over the S lanes of a row group (S = 8, 16 or 32), in every lane.
 template <int S>
 __device__ __forceinline__ float row_sum(float x)
 {
-    if constexpr (S == 8) {
-        x += dpp_row<0xB1>(x);   // quad_perm [1, 0, 3, 2]
-        x += dpp_row<0x4E>(x);   // quad_perm [2, 3, 0, 1]
-        x += dpp_row<0x141>(x);  // row_half_mirror
-        return x;
-    } else {
-        return row_reduce<S>(x, OpAdd{});
-    }
+    return row_reduce<S>(x, OpAdd{});
 }
 
 // Order-preserving map of a float score to an unsigned radix key: larger

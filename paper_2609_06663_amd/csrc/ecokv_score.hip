@@ -317,20 +317,28 @@ __device__ __forceinline__ void tile_store(u32x4 *kt, const u32x4 (&pf)[8], int 
     for (int j = 0; j < 8; ++j) kt[sw(j * 16 + g, c)] = pf[j];
 }
 
+// The first DEPTH 128-key tiles of a block into registers: issued before the
+// block's set-up loads (window rows, anchors), so that their latencies overlap.
+template <int DEPTH>
+__device__ __forceinline__ void tile_prefetch(u32x4 (&pf)[DEPTH][8], __amdgpu_buffer_rsrc_t rs, int row_base, int g,
+                                              int c)
+{
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) tile_load(pf[d], rs, row_base + d * kTile, g, c);
+}
+
 // Calls body(tr0) for each of the block's `ntiles` 128-key tiles with the tile
-// in kt.  DEPTH tiles are in flight in registers while one is processed.  The
-// prefetch is unconditional (the descriptor ends at the block's last row), so
-// every barrier waits only for LDS and the oldest tile.
+// in kt, the first DEPTH of them already in pf (tile_prefetch).  DEPTH tiles
+// are in flight in registers while one is processed.  The prefetch is
+// unconditional (the descriptor ends at the block's last row), so every
+// barrier waits only for LDS and the oldest tile.
 template <int DEPTH, class F>
-__device__ __forceinline__ void tile_pipeline(u32x4 *kt, __amdgpu_buffer_rsrc_t rs, int row_base, int ntiles, int g,
-                                              int c, F &&body)
+__device__ __forceinline__ void tile_pipeline(u32x4 (&pf)[DEPTH][8], u32x4 *kt, __amdgpu_buffer_rsrc_t rs,
+                                              int row_base, int ntiles, int g, int c, F &&body)
 {
     // The loop over groups of DEPTH tiles is kept rolled (code size); the
     // loads are unconditional, so the outstanding-load count is the same on
     // every path and each barrier waits only for the oldest tile.
-    u32x4 pf[DEPTH][8];
-#pragma unroll
-    for (int d = 0; d < DEPTH; ++d) tile_load(pf[d], rs, row_base + d * kTile, g, c);
     // Whole groups only: a tile past the block's range reads as zeros from the
     // descriptor and adds nothing (callers mask keys at or past T), so every
     // iteration is identical and no path re-enters the loop with fewer loads
@@ -385,7 +393,6 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
 {
     __shared__ u32x4 kt[kTile * kChunks];                   // 32 KiB key tile
     __shared__ __attribute__((aligned(16))) uint16_t aw[4][kTile];  // ones, 1/|k| high, remainder, zeros
-    __shared__ float wm[4][32 * MT], wsm[4][32 * MT];
 
     const int u = blockIdx.y;
     const Unit un = unit_of(u, a.Hkv, a.B);
@@ -398,6 +405,9 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
     const int c = tid & 15, g = tid >> 4, h = lane >> 5;
     const uint16_t *krow0 = static_cast<const uint16_t *>(a.K) + unit_row0(a, un) * kD;
     const float sc = a.inv_sqrt_d * kLog2e;
+    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + a.rpb1));
+    u32x4 pf[kSweep1Depth][8];
+    tile_prefetch(pf, rs, row_base, g, c);
 
     bf16x8 aq[MT][8];
     load_query_operands<MT>(a, un, lane, aq);
@@ -424,8 +434,7 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
     f32x16 csum = (f32x16){};
 
     const int ntiles = min(a.rpb1 / kTile, (T - row_base + kTile - 1) / kTile);
-    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + a.rpb1));
-    tile_pipeline<kSweep1Depth>(kt, rs, row_base, ntiles, g, c, [&](int tr0) {
+    tile_pipeline(pf, kt, rs, row_base, ntiles, g, c, [&](int tr0) {
         // window logits and |k|^2 of this wave's 32 keys
         f32x16 acc[MT];
 #pragma unroll
@@ -542,30 +551,39 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
         part[32 * wv + lane] = csum[0];              // sum of k
         part[kD + 32 * wv + lane] = csum[1] + csum[2];  // sum of k / |k|
     }
-    // per-row softmax partials over the 32 lanes that hold the row: the row's
-    // largest reference by a max butterfly, each lane's sum moved onto it (one
-    // exponential), then a sum butterfly, both by DPP within 16-lane rows (a
-    // pairwise merge per level by LDS shuffles took 10.8 of this block's 18 us
-    // on one 8192-token layer: dependent LDS round trips)
+    // per-row softmax partials: a row's 128 (reference, sum) pairs (32 lanes
+    // of each of the 4 waves) go through the key tile, free now, and 8 threads
+    // per row merge 16 of them each, then by a 3-step DPP butterfly: the
+    // row's largest reference, each sum moved onto it, summed.  (Butterflies
+    // over the 32 lanes that hold a row, one row at a time, took 5 of this
+    // block's 12 us on one 8192-token layer: 64 dependent chains in 4 waves.)
+    // (pair p of row r at r * 128 + (p ^ 8 (r % 8)): the 8 rows a wave reads at
+    // once fall on different banks)
+    float2 *scr = reinterpret_cast<float2 *>(kt);  // [32 rows][4 waves x 32 lanes]
 #pragma unroll
-    for (int t = 0; t < MT; ++t)
+    for (int t = 0; t < MT; ++t) {
+        if (t) lds_barrier();  // the previous rows' readers are done
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            const float m = row_reduce<32>(ms[t][i], OpMax{});
-            float s = ms[t][i] == -INFINITY ? 0.f : ss[t][i] * fast_exp2(ms[t][i] - m);
-            s = row_reduce<32>(s, OpAdd{});
-            if ((lane & 31) == 0) {
-                const int row = 32 * t + 8 * (i >> 2) + 4 * h + (i & 3);
-                wm[wv][row] = m;
-                wsm[wv][row] = s;
-            }
+            const int r = 8 * (i >> 2) + 4 * h + (i & 3);
+            scr[r * 128 + ((32 * wv + (lane & 31)) ^ (8 * (r & 7)))] = make_float2(ms[t][i], ss[t][i]);
         }
-    lds_barrier();
-    if (tid < a.R) {
-        float m = wm[0][tid], s = wsm[0][tid];
-        for (int w2 = 1; w2 < 4; ++w2) softmax_merge2(m, s, wm[w2][tid], wsm[w2][tid]);
-        part[2 * kD + tid] = m;
-        part[2 * kD + a.R + tid] = s;
+        lds_barrier();
+        const int row = tid >> 3, q = tid & 7;
+        float2 v[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) v[j] = scr[row * 128 + ((8 * j + q) ^ (8 * (row & 7)))];
+        float m = -INFINITY, s = 0.f;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) m = fmaxf(m, v[j].x);
+#pragma unroll
+        for (int j = 0; j < 16; ++j) s += v[j].x == -INFINITY ? 0.f : v[j].y * fast_exp2(v[j].x - m);
+        const float mg = row_reduce<8>(m, OpMax{});
+        s = row_reduce<8>(m == -INFINITY ? 0.f : s * fast_exp2(m - mg), OpAdd{});
+        if (q == 0 && 32 * t + row < a.R) {
+            part[2 * kD + 32 * t + row] = mg;
+            part[2 * kD + a.R + 32 * t + row] = s;
+        }
     }
 }
 
@@ -596,6 +614,9 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
     const int c = tid & 15, g = tid >> 4, h = lane >> 5;
     const uint16_t *krow0 = static_cast<const uint16_t *>(a.K) + unit_row0(a, un) * kD;
     const int64_t obase = unit_out_base(a, un);
+    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + a.rpb2));
+    u32x4 pf[kSweep2Depth][8];
+    tile_prefetch(pf, rs, row_base, g, c);
     __shared__ __attribute__((aligned(16))) float sanc[2 * kD + 2 * ECOKV_MAX_ROWS];
     const float *anc = unit_anchors(a, un, u, T, sanc);
     const float sc = a.inv_sqrt_d * kLog2e;
@@ -618,8 +639,7 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
     float dsum = 0.f, dsq = 0.f, dmn = INFINITY, dmx = -INFINITY;
     const float inv_r = 1.f / (float)a.R;
     const int ntiles = min(a.rpb2 / kTile, (T - row_base + kTile - 1) / kTile);
-    const __amdgpu_buffer_rsrc_t rs = key_rows_rsrc(krow0, min(T, row_base + a.rpb2));
-    tile_pipeline<kSweep2Depth>(kt, rs, row_base, ntiles, g, c, [&](int tr0) {
+    tile_pipeline(pf, kt, rs, row_base, ntiles, g, c, [&](int tr0) {
 
         f32x16 acc[MT];
 #pragma unroll
