@@ -308,6 +308,12 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
     return v;
 }
 
+// Sum over the wave (the last lane of the inclusive scan, read as a scalar).
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x)
+{
+    return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(x), kWave - 1);
+}
+
 // Sum over the 16 lanes of an aligned 16-lane segment; every lane gets the total.
 __device__ __forceinline__ float seg16_sum(float x) { return row_reduce<16>(x, OpAdd{}); }
 

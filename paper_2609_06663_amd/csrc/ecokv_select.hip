@@ -1014,14 +1014,15 @@ __device__ __forceinline__ uint32_t mb_exscan(uint32_t x, uint32_t *ws, uint32_t
 // chosen bin is taken whole (the later digits are then skipped).
 __device__ uint4 mb_advance(uint4 st, const uint32_t *gh, int d, uint32_t *sh)
 {
-    if (st.w) return st;
     const int nb = mb_bins(d), per = nb / kMbThreads;
     const int t = threadIdx.x;
     // thread t: bins nb-1-per*t .. nb-per*(t+1), in descending digit order,
-    // read as 16-byte pieces (the histogram was completed by an earlier launch)
+    // read as 16-byte pieces (the histogram was completed by an earlier launch;
+    // read before st is looked at, so that these loads overlap the state's)
     typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
     const u32x4_t *src = reinterpret_cast<const u32x4_t *>(gh + nb - per * (t + 1));
     u32x4_t v0 = src[0], v1 = per == 8 ? src[1] : (u32x4_t){0u, 0u, 0u, 0u};
+    if (st.w) return st;
     // descending order: the last bin of the piece first
     uint32_t c[8] = {per == 8 ? v1[3] : v0[3], per == 8 ? v1[2] : v0[2], per == 8 ? v1[1] : v0[1],
                      per == 8 ? v1[0] : v0[0], v0[3], v0[2], v0[1], v0[0]};
@@ -1088,7 +1089,7 @@ __device__ __forceinline__ int mb_slices(const MbGroup &g)
 template <int KPT, int DIG>
 __global__ __launch_bounds__(kMbThreads) void k_sel_digit(SelectArgs a)
 {
-    __shared__ uint32_t hist[kMbWaves][2048];
+    __shared__ __attribute__((aligned(16))) uint32_t hist[kMbWaves][2048];
     __shared__ uint32_t sh[kMbWaves + 4];
     const int gi = blockIdx.x / a.mb_slices, j = blockIdx.x - gi * a.mb_slices;
     const MbGroup g = mb_group(a, gi);
@@ -1101,12 +1102,18 @@ __global__ __launch_bounds__(kMbThreads) void k_sel_digit(SelectArgs a)
     uint32_t kk[KPT];
     int hh, ii;
     if (r0 < g.n) mb_load<KPT>(g, r0, kk, hh, ii);
+    // the LDS histograms are cleared while the keys and the state are in
+    // flight (the state's block scan orders the clear before the counts)
+    {
+        typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+        u32x4_t *h4 = reinterpret_cast<u32x4_t *>(&hist[0][0]);
+        for (int b = t; b < kMbWaves * 2048 / 4; b += kMbThreads) h4[b] = (u32x4_t){0u, 0u, 0u, 0u};
+    }
     const uint4 st = mb_state<DIG>(a, gi, j, g.k, sh);
     if (DIG == 2) mb_clear(a, gi, j, ns, 0);  // digit 0's histogram: its last reader was the previous launch
     if (st.w) return;
     const int nb = mb_bins(DIG), lo = mb_lo(DIG);
-    for (int b = t; b < kMbWaves * 2048; b += kMbThreads) (&hist[0][0])[b] = 0u;
-    __syncthreads();
+    if (DIG == 0) __syncthreads();
     if (r0 < g.n) {
 #pragma unroll
         for (int q = 0; q < KPT; ++q)
@@ -1223,10 +1230,8 @@ __global__ __launch_bounds__(kMbThreads) void k_sel_emit(SelectArgs a)
             pg += c[0];
             pe += c[1];
         }
-        for (int m = 32; m >= 1; m >>= 1) {
-            pg += __shfl_xor(pg, m, kWave);
-            pe += __shfl_xor(pe, m, kWave);
-        }
+        pg = wave_sum_u32(pg);
+        pe = wave_sum_u32(pe);
         if (lane == 0) {
             red[0][wv] = pg;
             red[1][wv] = pe;
