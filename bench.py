@@ -627,7 +627,7 @@ def main():
     del ep1, lw, Ks, Vs, Qs
     # a call per group of consecutive layers (as a prefill can issue every few
     # layers), alternating over two streams
-    for k in (2, 4):
+    for k in (2, 4, 7):
         if L % k:
             continue
         log(f"{L // k} calls of {k} layers on two streams")
