@@ -205,7 +205,7 @@ int select_workspace(const ShapeInfo &si, const ecokv_shape *shape, int mode, vo
 {
     int64_t groups = 0, maxn = 0;
     select_dims(si, shape, mode, &groups, &maxn);
-    const size_t need = ecokv::select_ws_layout(groups, maxn).total;
+    const size_t need = ecokv::select_ws_layout(groups, maxn, mode != ECOKV_LAYER_FLAT).total;
     if (!workspace) return fail(ECOKV_EINVAL, "workspace is NULL");
     if (((uintptr_t)workspace & 255u) != 0) return fail(ECOKV_EINVAL, "workspace must be 256-byte aligned");
     if (workspace_bytes < need)
@@ -620,7 +620,7 @@ int ecokv_select_workspace_size(const ecokv_shape *shape, int mode, size_t *byte
     if (!bytes) return fail(ECOKV_EINVAL, "bytes is NULL");
     int64_t groups = 0, maxn = 0;
     select_dims(si, shape, mode, &groups, &maxn);
-    *bytes = ecokv::select_ws_layout(groups, maxn).total;
+    *bytes = ecokv::select_ws_layout(groups, maxn, mode != ECOKV_LAYER_FLAT).total;
     return ECOKV_OK;
 }
 

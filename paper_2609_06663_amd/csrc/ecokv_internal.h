@@ -119,15 +119,21 @@ struct SelectArgs {
     int64_t mb_groups;   // groups of the largest launch of the call
     int64_t mb_maxn;     // keys of the largest group of the call
     int mb_slices;       // slices per group of this launch
+    // two-stage selection of long single-head groups with small budgets:
+    // each slice's own top keys, then the group's among them
+    int32_t *c_pos;      // [mb_groups][c_slices][slice keys] candidate positions, ascending per slice
+    uint32_t *c_key;     // the same layout: their order-preserving keys
+    int c_slices;        // slices per group of this launch
     SeqTab seq;
     LhTab lht;
 };
 
 // Workspace of ecokv_select.
 struct SelWsLayout {
-    size_t state, hist, head, cnt, total;
+    size_t state, hist, head, cnt, cand, total;
 };
-SelWsLayout select_ws_layout(int64_t groups, int64_t maxn);
+// per_head: every group is a single head (ECOKV_PER_HEAD, ECOKV_HEAD_BUDGETS)
+SelWsLayout select_ws_layout(int64_t groups, int64_t maxn, bool per_head);
 
 struct CompactArgs {
     const char *K;

@@ -652,6 +652,63 @@ __device__ __forceinline__ void reg_radix_select_staged(const uint32_t (&kk)[KPT
 }
 
 
+// Ordered emission of one head's chosen keys from the registers (thread t
+// holds keys v0 .. v0+KPT-1 of n): bit q of gtm[c] / eqm[c] marks key
+// v0 + 32 c + q above / equal to the threshold; the thread's taken keys go to
+// consecutive slots from the number taken before its run, put(slot, key
+// index); equal keys are taken in key order while fewer than need_eq precede
+// them.
+template <int KPT, class F>
+__device__ __forceinline__ void emit_ordered(const uint32_t (&kk)[KPT], int v0, int n, uint32_t thr, int need_eq,
+                                             uint32_t *wsum, F &&put)
+{
+    constexpr int NC = (KPT + 31) / 32;      // 32-key words per thread
+    constexpr int QW = KPT < 32 ? KPT : 32;  // keys per word
+    uint32_t gtm[NC], eqm[NC];
+    uint32_t cg = 0, ce = 0;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        gtm[c] = 0u;
+        eqm[c] = 0u;
+#pragma unroll
+        for (int q = 0; q < QW; ++q)
+            if (v0 + 32 * c + q < n) {
+                gtm[c] |= kk[32 * c + q] > thr ? 1u << q : 0u;
+                eqm[c] |= kk[32 * c + q] == thr ? 1u << q : 0u;
+            }
+        cg += (uint32_t)__builtin_popcount(gtm[c]);
+        ce += (uint32_t)__builtin_popcount(eqm[c]);
+    }
+    uint32_t eg, ee, tg, te;
+    block_exscan2(cg, ce, wsum, eg, ee, tg, te);
+    (void)tg;
+    (void)te;
+    const int eq_take = min((int)ce, max(need_eq - (int)ee, 0));
+    uint32_t take[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) take[c] = gtm[c];
+    for (int r = 0; r < eq_take; ++r) {
+        bool done = false;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+            if (!done && eqm[c]) {
+                const uint32_t low = eqm[c] & (~eqm[c] + 1u);
+                take[c] |= low;
+                eqm[c] ^= low;
+                done = true;
+            }
+    }
+    int o = (int)eg + min((int)ee, need_eq);
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+        while (take[c]) {
+            const int q = 32 * c + __builtin_ctz(take[c]);
+            take[c] &= take[c] - 1u;
+            put(o, v0 + q);
+            ++o;
+        }
+}
+
 // ---------------------------------------------------------------------------
 // One block per group, for groups of up to 32 Ki keys (each a handful of
 // launches' worth of work for the multi-block form below): thread t owns the
@@ -785,56 +842,11 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
                                      &thr, &need_eq);
     }
     if (k > 0 && nh == 1) {
-        // ordered emission of one head: bit q of gtm[c] / eqm[c] marks key
-        // v0 + 32 c + q above / equal to the threshold; the thread's taken
-        // keys go to consecutive slots from the number taken before its run
-        constexpr int NC = (KPT + 31) / 32;   // 32-key words per thread
-        constexpr int QW = KPT < 32 ? KPT : 32;  // keys per word
-        uint32_t gtm[NC], eqm[NC];
-        uint32_t cg = 0, ce = 0;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            gtm[c] = 0u;
-            eqm[c] = 0u;
-#pragma unroll
-            for (int q = 0; q < QW; ++q)
-                if (v0 + 32 * c + q < n) {
-                    gtm[c] |= kk[32 * c + q] > thr ? 1u << q : 0u;
-                    eqm[c] |= kk[32 * c + q] == thr ? 1u << q : 0u;
-                }
-            cg += (uint32_t)__builtin_popcount(gtm[c]);
-            ce += (uint32_t)__builtin_popcount(eqm[c]);
-        }
-        uint32_t eg, ee, tg, te;
-        block_exscan2(cg, ce, wsum, eg, ee, tg, te);
-        (void)tg;
-        (void)te;
-        // equal keys are taken in position order while fewer than need_eq precede them
-        const int eq_take = min((int)ce, max(need_eq - (int)ee, 0));
-        uint32_t take[NC];
-#pragma unroll
-        for (int c = 0; c < NC; ++c) take[c] = gtm[c];
-        for (int r = 0; r < eq_take; ++r) {
-            bool done = false;
-#pragma unroll
-            for (int c = 0; c < NC; ++c)
-                if (!done && eqm[c]) {
-                    const uint32_t low = eqm[c] & (~eqm[c] + 1u);
-                    take[c] |= low;
-                    eqm[c] ^= low;
-                    done = true;
-                }
-        }
-        int o = (int)eg + min((int)ee, need_eq);
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-            while (take[c]) {
-                const int q = 32 * c + __builtin_ctz(take[c]);
-                take[c] &= take[c] - 1u;
-                if (staged) ost[o] = (uint32_t)(v0 + q);
-                else out[o] = v0 + q;
-                ++o;
-            }
+        // ordered emission of one head
+        emit_ordered<KPT>(kk, v0, n, thr, need_eq, wsum, [&](int o, int v) {
+            if (staged) ost[o] = (uint32_t)v;
+            else out[o] = v;
+        });
         if (tid == 0) through[0] = k;
     } else if (k > 0) {
         // ordered emission from the registers (several heads)
@@ -890,6 +902,137 @@ __global__ __launch_bounds__(kSelThreads) void k_select_reg(SelectArgs a)
         const int64_t u = ((int64_t)l * a.Hkv + h0 + hh) * a.B + s;
         if (a.counts) a.counts[u] = (int32_t)(through[hh] - prev + a.w);
         if (a.offsets) a.offsets[u] = (int32_t)(out_base + prev + (int64_t)hh * a.w);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Two-stage selection of single-head groups longer than one block's registers
+// when their budget is small.  The group's k chosen keys are the k largest
+// under the order (key descending, position ascending); restricted to one
+// slice they are that slice's largest, at most min(k, slice) of them.  So:
+//   stage 1  one block per slice of kCandSlice keys selects the slice's own
+//            min(k, n_slice) largest (the radix select and tie rule of the
+//            one-block form) and writes their keys and positions, ascending;
+//   stage 2  one block per group reads its slices' candidates in slice
+//            order -- ascending position, so equal keys still favour the
+//            smaller position -- selects the k largest among them and writes
+//            their positions.
+// Used when the candidates of every group fit one block's registers (32-head
+// layer of 65536 tokens, budget 2048: 8 slices of 2040 candidates).
+// ---------------------------------------------------------------------------
+constexpr int kCandKPT = 8;
+constexpr int kCandSlice = kCandKPT * kSelThreads;  // 8192 keys
+
+// The scores of single-head group grp.
+__device__ __forceinline__ const float *head_scores(const SelectArgs &a, const SelGroup &grp)
+{
+    return a.scores + ((int64_t)grp.l * a.Hkv + grp.h0) * a.Ptot + (a.seq.cu[grp.s] - grp.s * a.w);
+}
+
+__global__ __launch_bounds__(kSelThreads) void k_sel_cand(SelectArgs a)
+{
+    __shared__ uint32_t hsum[256];
+    __shared__ uint32_t bc[2][2];
+    __shared__ uint32_t wsum[2 * kSelWaves + 2];
+    __shared__ uint32_t mm[2][kSelWaves];
+    __shared__ uint32_t ccount;
+    typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+    __shared__ u32x4_t stg[8 * kSelThreads];  // the radix scratch
+    const int gi = blockIdx.x / a.c_slices, j = blockIdx.x - gi * a.c_slices;
+    const SelGroup grp = sel_group(a, gi);
+    const int T = a.seq.cu[grp.s + 1] - a.seq.cu[grp.s];
+    const int P = T - a.w;
+    const int k = grp.beff - a.w;
+    const int s0 = j * kCandSlice;
+    if (grp.beff >= T || k <= 0 || s0 >= P) return;  // (stage 2 writes those groups)
+    const int n = min(kCandSlice, P - s0);
+    const int tid = threadIdx.x, v0 = tid * kCandKPT;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(uniform_ptr(head_scores(a, grp) + s0)), (short)0, uniform_i32(n) * 4, 0x00020000);
+    uint32_t kk[kCandKPT];
+#pragma unroll
+    for (int q = 0; q < kCandKPT / 4; ++q) {
+        const u32x4_t x = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (v0 + 4 * q) * 4, 0, 0));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) kk[4 * q + e] = score_key(__uint_as_float(x[e]));
+    }
+    uint32_t kmin, kmax, thr;
+    int need_eq;
+    reg_extremes<kCandKPT>(kk, v0, n, mm, &kmin, &kmax);
+    reg_radix_select_staged<kCandKPT>(kk, v0, n, min(k, n), kmin, kmax, reinterpret_cast<uint32_t *>(stg), hsum, bc,
+                                      &ccount, &thr, &need_eq);
+    // the keys through LDS (free again after the selection), so that the
+    // emission can write each chosen key beside its position
+    uint32_t *kst = reinterpret_cast<uint32_t *>(stg);
+#pragma unroll
+    for (int q = 0; q < kCandKPT; ++q) kst[v0 + q] = kk[q];
+    __syncthreads();
+    // slice j's candidates follow those of the slices before it (each but
+    // the last has min(k, kCandSlice) of them)
+    const int64_t cb = (int64_t)gi * a.c_slices * kCandSlice + (int64_t)j * min(k, kCandSlice);
+    int32_t *cp = a.c_pos + cb;
+    uint32_t *ck = a.c_key + cb;
+    emit_ordered<kCandKPT>(kk, v0, n, thr, need_eq, wsum, [&](int o, int v) {
+        cp[o] = s0 + v;
+        ck[o] = kst[v];
+    });
+}
+
+template <int KPT>
+__global__ __launch_bounds__(kSelThreads) void k_sel_final(SelectArgs a)
+{
+    __shared__ uint32_t hsum[256];
+    __shared__ uint32_t bc[2][2];
+    __shared__ uint32_t wsum[2 * kSelWaves + 2];
+    __shared__ uint32_t mm[2][kSelWaves];
+    __shared__ uint32_t ccount;
+    typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+    __shared__ u32x4_t stg[8 * kSelThreads];  // the radix scratch
+    const int gi = blockIdx.x;
+    const SelGroup grp = sel_group(a, gi);
+    const int T = a.seq.cu[grp.s + 1] - a.seq.cu[grp.s];
+    const int P = T - a.w;
+    int32_t *out = a.idx + grp.out_base;
+    const int tid = threadIdx.x;
+    const int64_t u = ((int64_t)grp.l * a.Hkv + grp.h0) * a.B + grp.s;
+    if (grp.beff >= T) {  // keep every token
+        for (int e = tid; e < T; e += blockDim.x) out[e] = e;
+        if (tid == 0) {
+            if (a.counts) a.counts[u] = T;
+            if (a.offsets) a.offsets[u] = (int32_t)grp.out_base;
+        }
+        return;
+    }
+    const int k = grp.beff - a.w;
+    if (k > 0) {
+        const int ns = (P + kCandSlice - 1) / kCandSlice;
+        const int kfull = min(k, kCandSlice);                        // candidates of each slice but the last
+        const int nc = (ns - 1) * kfull + min(k, P - (ns - 1) * kCandSlice);  // <= KPT * kSelThreads (host)
+        // the candidates lie contiguously, in slice order: thread t takes
+        // candidates KPT t .. KPT t + KPT - 1 with 16-byte loads
+        const int64_t cb = (int64_t)gi * a.c_slices * kCandSlice;
+        const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+            uniform_ptr(a.c_key + cb), (short)0, uniform_i32(nc) * 4, 0x00020000);
+        const int v0 = tid * KPT;
+        uint32_t kk[KPT];
+#pragma unroll
+        for (int q = 0; q < KPT / 4; ++q) {
+            const u32x4_t x = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rk, (v0 + 4 * q) * 4, 0, 0));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) kk[4 * q + e] = x[e];
+        }
+        uint32_t kmin, kmax, thr;
+        int need_eq;
+        reg_extremes<KPT>(kk, v0, nc, mm, &kmin, &kmax);
+        reg_radix_select_staged<KPT>(kk, v0, nc, k, kmin, kmax, reinterpret_cast<uint32_t *>(stg), hsum, bc, &ccount,
+                                     &thr, &need_eq);
+        emit_ordered<KPT>(kk, v0, nc, thr, need_eq, wsum, [&](int o, int v) { out[o] = a.c_pos[cb + v]; });
+    }
+    // the window, count and offset
+    for (int e = tid; e < a.w; e += blockDim.x) out[max(k, 0) + e] = P + e;
+    if (tid == 0) {
+        if (a.counts) a.counts[u] = max(k, 0) + a.w;
+        if (a.offsets) a.offsets[u] = (int32_t)grp.out_base;
     }
 }
 
@@ -1323,16 +1466,19 @@ static int mb_kpt(int64_t groups, int64_t maxn)
     return blocks16 >= 512 ? 16 : 4;
 }
 
-SelWsLayout select_ws_layout(int64_t groups, int64_t maxn)
+SelWsLayout select_ws_layout(int64_t groups, int64_t maxn, bool per_head)
 {
     SelWsLayout w{};
     const int64_t slices = max((int64_t)1, (maxn + kMbThreads * 4 - 1) / (kMbThreads * 4));
+    // the two-stage form's candidate positions (single-head groups past one block)
+    const int64_t cand = per_head && maxn > 32 * kSelThreads ? (maxn + kCandSlice - 1) / kCandSlice * kCandSlice : 0;
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     size_t o = 0;
     w.state = o; o = al(o + sizeof(uint4) * 3 * groups);
     w.hist = o; o = al(o + sizeof(uint32_t) * kMbHistWords * groups);
     w.head = o; o = al(o + sizeof(uint32_t) * 2 * kMaxFlatHeads * groups);
     w.cnt = o; o = al(o + sizeof(uint32_t) * 2 * slices * groups);
+    w.cand = o; o = al(o + (sizeof(int32_t) + sizeof(uint32_t)) * cand * groups);
     w.total = o;
     return w;
 }
@@ -1373,7 +1519,42 @@ hipError_t select_launch(SelectArgs a, char *ws, hipStream_t st)
                                                          0, st, a));
         return hipGetLastError();
     }
-    const SelWsLayout lay = select_ws_layout(a.mb_groups, a.mb_maxn);
+    const SelWsLayout lay = select_ws_layout(a.mb_groups, a.mb_maxn, !a.flat);
+    if (!a.flat) {
+        // single-head groups: two stages when every group's candidates (the
+        // largest min(k, slice) keys of each slice) fit one block's registers
+        // (groups kept whole need none)
+        int kmax = 0;
+        for (int s = 0; s < a.B; ++s) {
+            const int Ts = a.seq.cu[s + 1] - a.seq.cu[s];
+            if (a.heads) {
+                for (int j = 0; j < a.lht.n; ++j)
+                    if (a.lht.b[j] < Ts) kmax = max(kmax, a.lht.b[j] - a.w);
+            } else if (a.seq.beff[s] < Ts) {
+                kmax = max(kmax, a.seq.beff[s] - a.w);
+            }
+        }
+        const int ns = (int)((maxn + kCandSlice - 1) / kCandSlice);
+        const int64_t ncmax = (int64_t)ns * min(kmax, kCandSlice);
+        if (ncmax <= 32 * kSelThreads) {
+            a.c_slices = ns;
+            const int64_t nslots = (a.mb_maxn + kCandSlice - 1) / kCandSlice * kCandSlice * a.mb_groups;
+            a.c_pos = reinterpret_cast<int32_t *>(ws + lay.cand);
+            a.c_key = reinterpret_cast<uint32_t *>(ws + lay.cand + sizeof(int32_t) * nslots);
+            ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_sel_cand, dim3((unsigned)(groups * ns)), dim3(kSelThreads), 0,
+                                                         st, a));
+            if (ncmax <= 8 * kSelThreads)
+                ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_sel_final<8>, dim3((unsigned)groups), dim3(kSelThreads),
+                                                             0, st, a));
+            else if (ncmax <= 16 * kSelThreads)
+                ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_sel_final<16>, dim3((unsigned)groups),
+                                                             dim3(kSelThreads), 0, st, a));
+            else
+                ECOKV_TIMED("select", st, hipLaunchKernelGGL(k_sel_final<32>, dim3((unsigned)groups),
+                                                             dim3(kSelThreads), 0, st, a));
+            return hipGetLastError();
+        }
+    }
     a.mb_state = reinterpret_cast<uint4 *>(ws + lay.state);
     a.mb_hist = reinterpret_cast<uint32_t *>(ws + lay.hist);
     a.mb_head = reinterpret_cast<uint32_t *>(ws + lay.head);

@@ -90,6 +90,27 @@ def test_select_bit_exact_with_ties_and_edges():
     check_against_oracle(S, L, Hkv, w, cu, bud, g)
 
 
+def test_long_sequences_two_stage_and_multi_block():
+    # sequences past 32768 keys: small per-head budgets take the two-stage
+    # selection (every head's candidates fit one block), one large budget in
+    # the second call sends the whole call to the multi-block form
+    rng = np.random.default_rng(43)
+    seqlens = [50004, 2000]
+    cu = np.concatenate([[0], np.cumsum(seqlens)]).tolist()
+    L, Hkv, w = 2, 3, 4
+    Ptot = cu[-1] - len(seqlens) * w
+    S = rng.integers(0, 300, size=(L, Hkv, Ptot)).astype(np.float32) * np.float32(0.125)
+    S[0, 1, 9000:9100] = np.nan
+    bud = rng.integers(w, 3000, size=(L, Hkv)).astype(np.int32)
+    bud[1, 2] = w          # the window only
+    bud[0, 2] = 60000      # every token
+    say(f"two-stage: budgets {bud.tolist()}")
+    check_against_oracle(S, L, Hkv, w, cu, bud, select_and_compact(S, L, Hkv, 128, w, cu, bud))
+    bud[1, 0] = 30000
+    say(f"multi-block: budgets {bud.tolist()}")
+    check_against_oracle(S, L, Hkv, w, cu, bud, select_and_compact(S, L, Hkv, 128, w, cu, bud))
+
+
 def test_more_pairs_than_one_table():
     # 40 layers x 8 KV heads = 320 (layer, head) pairs: two launches of the table
     rng = np.random.default_rng(42)

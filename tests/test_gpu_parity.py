@@ -498,7 +498,8 @@ def test_select_register_64_keys_per_thread(case):
 
 
 # ---------------------------------------------------------------------------
-# multi-block selection (groups past 32768 keys): shapes for each path,
+# selection of groups past 32768 keys: shapes for each path of the
+# multi-block form, and (per head, small budgets) of the two-stage form,
 # bit-exact against the oracle
 # ---------------------------------------------------------------------------
 
@@ -534,6 +535,26 @@ def _select_case(name, rng):
         S[0, 1, 100:900] = -0.0
         S[0, 2, 50:70] = np.inf
         S[0, 2, 70:90] = -np.inf
+    elif name == "two_stage_normal":
+        # per head: 8 slices of 8192 keys, k = 2048 (the two-stage form)
+        L, Hkv, w, lens, bud = 1, 4, 4, [65540], [2052]
+        S = rng.standard_normal((L, Hkv, 65536)).astype(np.float32)
+    elif name == "two_stage_ties":
+        # 7 values over 50000 keys, k = 1000: the threshold class spans every slice
+        L, Hkv, w, lens, bud = 1, 2, 4, [50004], [1004]
+        S = rng.integers(0, 7, size=(L, Hkv, 50000)).astype(np.float32)
+    elif name == "two_stage_nan_inf_zero":
+        L, Hkv, w, lens, bud = 1, 3, 2, [40002], [802]
+        S = rng.integers(0, 5, size=(L, Hkv, 40000)).astype(np.float32)
+        S[0, 0, 8000:8500] = np.nan
+        S[0, 1, 100:20000] = -0.0
+        S[0, 1, 30000:30010] = 0.0
+        S[0, 2, 16380:16390] = np.inf
+        S[0, 2, 70:90] = -np.inf
+    elif name == "two_stage_ragged":
+        # sequences of 70000, 9000 and 40000 keys (9, 2 and 5 slices), one kept whole
+        L, Hkv, w, lens, bud = 2, 2, 4, [70004, 9004, 40004, 300], [3004, 504, 3004, 400]
+        S = np.exp(rng.uniform(-6, 3, size=(L, Hkv, 70000 + 9000 + 40000 + 296))).astype(np.float32)
     else:
         raise ValueError(name)
     return L, Hkv, w, lens, bud, S
@@ -541,7 +562,8 @@ def _select_case(name, rng):
 
 @pytest.mark.parametrize("mode", ["per_head", "layer_flat"])
 @pytest.mark.parametrize("name", ["ties_across_slices", "bin_taken_whole", "flat_tiny_heads", "flat_long",
-                                  "many_groups_16_per_thread", "nan_and_signed_zero"])
+                                  "many_groups_16_per_thread", "nan_and_signed_zero", "two_stage_normal",
+                                  "two_stage_ties", "two_stage_nan_inf_zero", "two_stage_ragged"])
 def test_select_multiblock_bit_exact(name, mode):
     import paper_2609_06663_amd as P
     import zlib
