@@ -730,10 +730,11 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
 // MFMA B operands (lane l: key l % 32, 16-byte chunks 2s + l / 32).  The
 // attention of row m is 2^(x - M'_m) with M'_m = M_m + log2(S_m), the
 // normaliser folded into the shift.  2048-key blocks (1024 and 4096 measured
-// no better); 512-key blocks when a call has too few keys to fill the device
-// with 2048-key ones (a single layer, say).
+// no better); 1024- or 512-key blocks when a call has too few keys to fill
+// the device with 2048-key ones (one layer, say).
 constexpr int kS2Waves = 4;
 constexpr int kS2Keys = 2048;       // keys per block
+constexpr int kS2KeysMid = 1024;    // keys per block for calls with fewer blocks
 constexpr int kS2KeysSmall = 512;   // keys per block for calls with few blocks
 
 // Coalesced load of 32 key rows: instruction i covers rows 4i .. 4i+3, lane l
@@ -1983,10 +1984,18 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     const dim3 grid_e(a.nch3, U);
     hipError_t e;
 
-    // streaming sweeps: 2048-key blocks, or 512-key ones when those would be
-    // fewer than four per compute unit (1024 blocks)
-    const int sblock = (int64_t)U * ((maxT + fast::kS2Keys - 1) / fast::kS2Keys) >= 1024 ? fast::kS2Keys
-                                                                                       : fast::kS2KeysSmall;
+    // streaming sweeps: 2048-key blocks; 1024-key ones when those would be
+    // fewer than four per compute unit (1024 blocks) and the 1024-key ones at
+    // least two (one layer over 8 sequences of 4k-32k tokens: the pass
+    // 186 -> 174 us against 512-key blocks); else 512-key ones
+    auto work_blocks = [&](int keys) {
+        int64_t nb = 0;
+        for (int s = 0; s < a.B; ++s) nb += (a.seq.cu[s + 1] - a.seq.cu[s] + keys - 1) / keys;
+        return nb * a.L * a.Hkv;
+    };
+    const int sblock = work_blocks(fast::kS2Keys) >= 1024  ? fast::kS2Keys
+                       : work_blocks(fast::kS2KeysMid) >= 512 ? fast::kS2KeysMid
+                                                              : fast::kS2KeysSmall;
     {
         a.rpb1 = block_sweep_rows(a.D, bf16, U, maxT);
         a.nch1 = (maxT + a.rpb1 - 1) / a.rpb1;
@@ -2002,6 +2011,9 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
                 if (sblock == fast::kS2Keys)
                     ECOKV_TIMED("sweep1_stream", st,
                                 hipLaunchKernelGGL((fast::k_fs1s<fast::kS2Keys, false>), dim3(a.nch1, U), dim3(256), 0, st, a));
+                else if (sblock == fast::kS2KeysMid)
+                    ECOKV_TIMED("sweep1_stream", st,
+                                hipLaunchKernelGGL((fast::k_fs1s<fast::kS2KeysMid, false>), dim3(a.nch1, U), dim3(256), 0, st, a));
                 else
                     ECOKV_TIMED("sweep1_stream", st,
                                 hipLaunchKernelGGL((fast::k_fs1s<fast::kS2KeysSmall, false>), dim3(a.nch1, U), dim3(256), 0, st, a));
@@ -2024,6 +2036,9 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
             if (sblock == fast::kS2Keys)
                 ECOKV_TIMED("sweep2_stream", st,
                             hipLaunchKernelGGL(fast::k_fs2s<fast::kS2Keys>, dim3(a.nch2, U), dim3(256), 0, st, a));
+            else if (sblock == fast::kS2KeysMid)
+                ECOKV_TIMED("sweep2_stream", st,
+                            hipLaunchKernelGGL(fast::k_fs2s<fast::kS2KeysMid>, dim3(a.nch2, U), dim3(256), 0, st, a));
             else
                 ECOKV_TIMED("sweep2_stream", st,
                             hipLaunchKernelGGL(fast::k_fs2s<fast::kS2KeysSmall>, dim3(a.nch2, U), dim3(256), 0, st, a));
