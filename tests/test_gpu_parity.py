@@ -551,6 +551,10 @@ def _select_case(name, rng):
         S[0, 1, 30000:30010] = 0.0
         S[0, 2, 16380:16390] = np.inf
         S[0, 2, 70:90] = -np.inf
+    elif name == "two_stage_short_tail":
+        # 33000 keys: the fifth slice has 232, fewer than k = 1000 (all of them candidates)
+        L, Hkv, w, lens, bud = 1, 2, 4, [33004], [1004]
+        S = rng.standard_normal((L, Hkv, 33000)).astype(np.float32)
     elif name == "two_stage_ragged":
         # sequences of 70000, 9000 and 40000 keys (9, 2 and 5 slices), one kept whole
         L, Hkv, w, lens, bud = 2, 2, 4, [70004, 9004, 40004, 300], [3004, 504, 3004, 400]
@@ -563,7 +567,8 @@ def _select_case(name, rng):
 @pytest.mark.parametrize("mode", ["per_head", "layer_flat"])
 @pytest.mark.parametrize("name", ["ties_across_slices", "bin_taken_whole", "flat_tiny_heads", "flat_long",
                                   "many_groups_16_per_thread", "nan_and_signed_zero", "two_stage_normal",
-                                  "two_stage_ties", "two_stage_nan_inf_zero", "two_stage_ragged"])
+                                  "two_stage_ties", "two_stage_nan_inf_zero", "two_stage_short_tail",
+                                  "two_stage_ragged"])
 def test_select_multiblock_bit_exact(name, mode):
     import paper_2609_06663_amd as P
     import zlib
