@@ -55,7 +55,7 @@ extern "C" {
 #define ECOKV_OK 0
 #define ECOKV_EINVAL (-1)       /* bad shape, parameter or NULL pointer          */
 #define ECOKV_EWORKSPACE (-2)   /* workspace smaller than ecokv_workspace_size   */
-#define ECOKV_EUNSUPPORTED (-3) /* valid request this build does not implement   */
+#define ECOKV_EUNSUPPORTED (-3) /* valid request the library does not implement  */
 #define ECOKV_EHIP (-4)         /* the HIP runtime refused a launch              */
 #define ECOKV_ETIMEOUT (-5)     /* a bounded wait between blocks gave up (see    */
                                 /* ecokv_workspace_status)                        */

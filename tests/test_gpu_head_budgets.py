@@ -178,7 +178,7 @@ def test_stack28_pyramid_schedule():
 def test_layer7b_sparsemm_like_head_budgets():
     # SparseMM assigns each head the window, a uniform share and a head-specific
     # share; here the head-specific share is random (the visual-head scores
-    # come from a benchmark run that is not part of this build)
+    # come from a benchmark run outside this library)
     import paper_2609_06663_amd as P
     wl = W.custom(43, L=2, Hq=28, Hkv=4, D=128, w=8, seqlens=[4096, 1500], dtype="bf16", group=128)
     rng = np.random.default_rng(43)
