@@ -310,9 +310,11 @@ int ecokv_select_workspace_size(const ecokv_shape *shape, int mode, size_t *byte
  *   workspace, workspace_bytes: device scratch of at least
  *           ecokv_select_workspace_size bytes, 256-byte aligned, zero-filled
  *           before its first use (left so); not shared by calls that may
- *           overlap.  Each selection group (a unit, or the heads of a
- *           (layer, sequence) in LAYER_FLAT) is split over many blocks: its
- *           radix-select histograms and per-slice counts live there.
+ *           overlap.  A selection group (a unit, or the heads of a (layer,
+ *           sequence) in LAYER_FLAT) of more than 32768 keys is split over
+ *           many blocks: its radix-select histograms and per-slice counts
+ *           live there, or, for single-head groups whose budget is small,
+ *           each 8192-key slice's own largest keys and their positions.
  * NaN scores rank below every number; -0 ranks equal to +0.
  * ECOKV_EUNSUPPORTED: LAYER_FLAT with more than 256 KV heads, or with
  * H_kv * Ptot * 4 > 2^31 - 1 bytes of scores per layer; a sequence with
