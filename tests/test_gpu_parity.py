@@ -148,6 +148,31 @@ def test_high_anisotropy(strength, form):
     check_compact(wl, g)
 
 
+@pytest.mark.parametrize("case", ["rows28_short_keys", "rows29", "rows30"])
+def test_stream_key_norms(case):
+    # The streaming sweep 2 at the edges of its 32-row operand (window rows
+    # G w = 29 and 30 beside the two rows of mu), and with keys far shorter
+    # than the centroid among strongly aligned ones, where k.mu / |k| and
+    # |k - kbar| are each computed from a short key.
+    if case == "rows28_short_keys":
+        wl = W.custom(34, L=1, Hq=28, Hkv=4, D=128, w=4, seqlens=[3000, 1100], dtype="bf16",
+                      strength=10.0, query_offset=False)
+        rng = np.random.default_rng(35)
+        K = W.bf16_bits_to_f32(wl.K)
+        for h in range(wl.Hkv):
+            rows = rng.choice(wl.cu_seqlens[-1], size=150, replace=False)
+            K[0, h, rows] *= rng.uniform(0.0, 0.2, size=(150, 1)).astype(np.float32)
+        wl.K[...] = W.to_bf16_bits(K)
+    elif case == "rows29":
+        wl = W.custom(36, L=1, Hq=29, Hkv=1, D=128, w=1, seqlens=[2500, 700], dtype="bf16")
+    else:
+        wl = W.custom(37, L=1, Hq=10, Hkv=2, D=128, w=6, seqlens=[4100], dtype="bf16")
+    say(f"streaming sweep 2 key norms: {case}, G*w = {wl.Hq // wl.Hkv * wl.w}, sequences {wl.seqlens}")
+    g = gpu_pass(wl)
+    check_per_head(wl, g)
+    check_compact(wl, g)
+
+
 def check_layer_flat(wl, g, params=None):
     cu = wl.cu_seqlens
     for l in range(wl.L):
