@@ -30,8 +30,9 @@ def say(msg):
     print(f"[gpu-score-pre] {msg}", file=sys.stderr, flush=True)
 
 
-def prefill_sums(wl, causal=True):
-    """[L][Hkv][B][2D + 2R]: sum k, sum k/|k|, per window row max logit and sum exp(logit - max)."""
+def prefill_sums(wl, causal=True, lse=False):
+    """[L][Hkv][B][2D + 2R]: sum k, sum k/|k|, per window row max logit and sum exp(logit - max)
+    (with lse, each row's log-sum-exp and 1, the pair a flash-attention epilogue has)."""
     G, w, D = wl.G, wl.w, wl.D
     R = G * w
     out = np.zeros((wl.L, wl.Hkv, wl.B, 2 * D + 2 * R), np.float64)
@@ -51,8 +52,9 @@ def prefill_sums(wl, causal=True):
                     last = T - w + j if causal else T - 1
                     xr = x[r, :last + 1]
                     m = xr.max()
-                    out[l, h, s, 2 * D + r] = m
-                    out[l, h, s, 2 * D + R + r] = np.exp(xr - m).sum()
+                    z = np.exp(xr - m).sum()
+                    out[l, h, s, 2 * D + r] = m + np.log(z) if lse else m
+                    out[l, h, s, 2 * D + R + r] = 1.0 if lse else z
     return out
 
 
@@ -63,6 +65,17 @@ def test_score_pre_matches_oracle(dtype, D, Hq, Hkv, w):
                   group=64)
     say(f"{dtype} D={D} Hq={Hq} Hkv={Hkv} w={w}: first-sweep sums supplied")
     g = gpu_pass(wl, pre=prefill_sums(wl))
+    check_per_head(wl, g)
+    check_compact(wl, g)
+
+
+def test_score_pre_log_sum_exp_pairs():
+    # each window row handed over as (log-sum-exp, 1): the form a prefill's
+    # flash attention produces, above the row's largest logit by up to log T
+    wl = W.custom(93, L=2, Hq=28, Hkv=4, D=128, w=4, seqlens=[3000, 640], dtype="bf16", budget=[600, 128],
+                  group=64)
+    say("window rows handed over as (log-sum-exp, 1)")
+    g = gpu_pass(wl, pre=prefill_sums(wl, lse=True))
     check_per_head(wl, g)
     check_compact(wl, g)
 
