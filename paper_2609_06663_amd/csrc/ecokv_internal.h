@@ -52,7 +52,7 @@ struct ScoreArgs {
     // values the two blocks of a unit's split epilogue exchange, each a 64-bit
     // word (launch tag << 32 | float bits) so that a reader can tell a value of
     // this launch from anything older without ordering fences
-    unsigned long long *epiT;   // [U][2][4]           half-unit S_div / S_imp sums and extrema
+    unsigned long long *epiT;   // [U][4][4]           per-part S_div / S_imp sums and extrema
     unsigned *status;           // workspace status word: set to the launch tag if a wait ran out of time
     unsigned tag;               // launch tag (never 0)
     int spin_limit;             // polls of a bounded wait before it gives up (<= 0: give up at once)

@@ -1543,14 +1543,15 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
 }
 
 // Epilogue in one launch when a unit's P non-window keys fit one block
-// (SPLIT = 1) or two (SPLIT = 2, each with half of the keys).  Every per-unit
-// reduction is block-local, except that with SPLIT = 2 the two halves of a
-// unit exchange their S_div / S_imp sums and extrema once (tagged 64-bit
-// relaxed atomics; the halves are combined in a fixed order, so both compute
-// the same constants).  The wait for the other half is bounded: if it gives
-// up, the unit's lambda and scores come out NaN and the workspace status word
+// (SPLIT = 1), two (SPLIT = 2, each with half of the keys; units of up to
+// 32768 keys) or four (SPLIT = 4, units of up to 65536).  Every per-unit
+// reduction is block-local, except that with SPLIT > 1 the parts of a unit
+// exchange their S_div / S_imp sums and extrema once (tagged 64-bit relaxed
+// atomics; the parts are combined in a fixed order, so all compute the same
+// constants).  The wait for the other parts is bounded: if it gives up, the
+// unit's lambda and scores come out NaN and the workspace status word
 // records the launch.  Each key's d_E,
-// khat.mu and attention is read once.  Wave w holds 8/SPLIT chunks of 256
+// khat.mu and attention is read once.  Wave w holds KVEC chunks of 256
 // consecutive keys; lane l of chunk j holds keys 256 j + 4 l .. +3 of the
 // wave's range, so each load instruction covers 1 KiB of consecutive keys.
 // The pooling window (up to 4 keys on each side) comes from the neighbouring
@@ -1559,7 +1560,8 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
 // the ends of a block's range from memory.
 constexpr int kUThreads = 1024;
 constexpr int kUW = kUThreads / kWave;
-constexpr int kUKeys = kUThreads * 32;  // 32768 keys per unit
+constexpr int kUKeys = kUThreads * 32;  // 32768 keys per unit (one or two blocks)
+constexpr int kEpiSplitMax = 4;         // blocks per unit at most (65536 keys)
 
 // Block sum / min / max whose barriers order LDS only, so that global loads
 // issued before it stay in flight.
@@ -1613,11 +1615,12 @@ __device__ __forceinline__ void epi_tag_store(unsigned long long *p, float v, un
                        __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <int SPLIT>
+template <int SPLIT, int KVEC>
 __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
 {
-    static_assert(SPLIT == 1 || SPLIT == 2, "one or two blocks per unit");
-    constexpr int kVec = 8 / SPLIT;          // chunks (float4 per thread and array)
+    static_assert((SPLIT == 1 && KVEC == 8) || (SPLIT == 2 && KVEC == 4) || (SPLIT == 4 && KVEC == 4),
+                  "32768 keys in one or two blocks, 65536 in four");
+    constexpr int kVec = KVEC;               // chunks (float4 per thread and array)
     constexpr int kWaveKeys = 256 * kVec;    // keys per wave
     constexpr int kPartKeys = kUW * kWaveKeys;
     __shared__ Red4 lds[kUW + 1];
@@ -1635,8 +1638,8 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
 
     // every global load first, so that their latencies overlap: the sweep-2
     // partials and mu (d_E sum / extrema and |mu|^2 in one block reduction;
-    // one partial and one mu component per thread at most: a unit of at most
-    // 32768 + w keys has at most 257 sweep-2 blocks, and D <= 128), then
+    // one partial and one mu component per thread at most: the host checks
+    // that a unit has at most kUThreads sweep-2 blocks, and D <= 128), then
     // d_E, khat.mu and attention of the thread's keys (zero past P), and the
     // attention just outside the block's range (a negative offset wraps past
     // the range and reads zero)
@@ -1732,32 +1735,41 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
     }
     Red4 sd = block_red4_lds(w, lds);
     if (SPLIT > 1) {
-        // exchange with the other half of the unit: publish, then wait (bounded)
+        // exchange with the other parts of the unit: publish, then wait for each (bounded)
         if (threadIdx.x == 0) {
-            unsigned long long *mine = a.epiT + ((int64_t)u * 2 + part) * 4;
+            unsigned long long *mine = a.epiT + ((int64_t)u * SPLIT + part) * 4;
             epi_tag_store(mine + 0, sd.s0, a.tag);
             epi_tag_store(mine + 1, sd.s1, a.tag);
             epi_tag_store(mine + 2, sd.mn, a.tag);
             epi_tag_store(mine + 3, sd.mx, a.tag);
-            const unsigned long long *other = a.epiT + ((int64_t)u * 2 + (part ^ 1)) * 4;
-            unsigned long long o[4] = {0ull, 0ull, 0ull, 0ull};
-            bool ok = false;
-            // a spin limit <= 0 (set by the host to exercise this path) gives up at once
-            for (int tries = 0; tries < a.spin_limit && !ok; ++tries) {
-                ok = true;
+            Red4 c{0.f, 0.f, INFINITY, -INFINITY};
+            bool all_ok = true;
+            for (int pp = 0; pp < SPLIT; ++pp) {  // in part order, so every part adds in the same order
+                Red4 r = sd;
+                if (pp != part) {
+                    const unsigned long long *other = a.epiT + ((int64_t)u * SPLIT + pp) * 4;
+                    unsigned long long o[4] = {0ull, 0ull, 0ull, 0ull};
+                    bool ok = false;
+                    // a spin limit <= 0 (set by the host to exercise this path) gives up at once
+                    for (int tries = 0; tries < a.spin_limit && !ok; ++tries) {
+                        ok = true;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    o[q] = __hip_atomic_load(other + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    ok = ok && (unsigned)(o[q] >> 32) == a.tag;
+                        for (int q = 0; q < 4; ++q) {
+                            o[q] = __hip_atomic_load(other + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            ok = ok && (unsigned)(o[q] >> 32) == a.tag;
+                        }
+                        if (!ok) __builtin_amdgcn_s_sleep(2);
+                    }
+                    all_ok = all_ok && ok;
+                    r = Red4{__uint_as_float((unsigned)o[0]), __uint_as_float((unsigned)o[1]),
+                             __uint_as_float((unsigned)o[2]), __uint_as_float((unsigned)o[3])};
                 }
-                if (!ok) __builtin_amdgcn_s_sleep(2);
+                c = pp == 0 ? r : Red4{c.s0 + r.s0, c.s1 + r.s1, fminf(c.mn, r.mn), fmaxf(c.mx, r.mx)};
             }
-            if (!ok) __hip_atomic_store(a.status, a.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            const Red4 so{__uint_as_float((unsigned)o[0]), __uint_as_float((unsigned)o[1]),
-                          __uint_as_float((unsigned)o[2]), __uint_as_float((unsigned)o[3])};
-            const Red4 h0 = part == 0 ? sd : so, h1 = part == 0 ? so : sd;  // the same order in both halves
-            Red4 c{h0.s0 + h1.s0, h0.s1 + h1.s1, fminf(h0.mn, h1.mn), fmaxf(h0.mx, h1.mx)};
-            if (!ok) c.s0 = NAN;
+            if (!all_ok) {
+                __hip_atomic_store(a.status, a.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                c.s0 = NAN;
+            }
             lds[kUW] = c;
         }
         lds_barrier();
@@ -1914,7 +1926,7 @@ WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int 
     w.bufC = o; o = align256(o + sizeof(float) * (int64_t)L * Hkv * Ptot);
     w.bufV = o; o = align256(o + (vnorm ? sizeof(float) * (int64_t)L * Hkv * Ptot : 0));
     w.dq = o; o = align256(o + sizeof(float) * U * 2);
-    w.epiT = o; o = align256(o + sizeof(unsigned long long) * U * 2 * 4);
+    w.epiT = o; o = align256(o + sizeof(unsigned long long) * U * kEpiSplitMax * 4);
     w.total = o;
     return w;
 }
@@ -1954,7 +1966,8 @@ static void launch_sweep(int pass, const ScoreArgs &a, dim3 grid, hipStream_t st
     }
 }
 
-// Blocks of k_epi_unit<2> that the current device holds at once (cached per device).
+// Blocks of k_epi_unit<SPLIT, 4> that the current device holds at once (cached per device).
+template <int SPLIT>
 static int64_t epi_split_capacity()
 {
     static int64_t cache[64];
@@ -1963,7 +1976,7 @@ static int64_t epi_split_capacity()
     if (cache[dev] == 0) {
         int ncu = 0, nb = 0;
         if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_epi_unit<2>, kUThreads, 0) != hipSuccess) return 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_epi_unit<SPLIT, 4>, kUThreads, 0) != hipSuccess) return 0;
         cache[dev] = (int64_t)ncu * nb;
     }
     return cache[dev];
@@ -2077,16 +2090,26 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         if ((e = dquant_launch(qa, st)) != hipSuccess) return e;
         a.dq = qa.out;
     }
-    if (maxT - a.w <= kUKeys && a.pool_half <= kPoolHalfMax && (maxT + a.rpb2 - 1) / a.rpb2 <= kUThreads && a.D <= kUThreads) {
+    const bool epi_one = a.pool_half <= kPoolHalfMax && (maxT + a.rpb2 - 1) / a.rpb2 <= kUThreads && a.D <= kUThreads;
+    if (maxT - a.w <= kUKeys && epi_one) {
         // two blocks per unit when all of them can be resident at once (their
         // exchange waits for each other; four per unit measured no faster), else one
-        if (!a.no_wait && 2 * (int64_t)U <= epi_split_capacity()) {
+        if (!a.no_wait && 2 * (int64_t)U <= epi_split_capacity<2>()) {
             a.epiT = reinterpret_cast<unsigned long long *>(ws + lay.epiT);
             a.tag = launch_tag();
-            ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL(k_epi_unit<2>, dim3(2 * U), dim3(kUThreads), 0, st, a));
+            ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL((k_epi_unit<2, 4>), dim3(2 * U), dim3(kUThreads), 0, st, a));
         } else {
-            ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL(k_epi_unit<1>, dim3(U), dim3(kUThreads), 0, st, a));
+            ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL((k_epi_unit<1, 8>), dim3(U), dim3(kUThreads), 0, st, a));
         }
+        return hipGetLastError();
+    }
+    if (maxT - a.w <= kEpiSplitMax / 2 * kUKeys && epi_one && !a.no_wait &&
+        kEpiSplitMax * (int64_t)U <= epi_split_capacity<kEpiSplitMax>()) {
+        // units of up to 65536 keys: four blocks per unit, all resident at once
+        a.epiT = reinterpret_cast<unsigned long long *>(ws + lay.epiT);
+        a.tag = launch_tag();
+        ECOKV_TIMED("epilogue", st,
+                    hipLaunchKernelGGL((k_epi_unit<kEpiSplitMax, 4>), dim3(kEpiSplitMax * U), dim3(kUThreads), 0, st, a));
         return hipGetLastError();
     }
     ECOKV_TIMED("epilogue1", st, hipLaunchKernelGGL(k_epi1, grid_e, dim3(kEpiThreads), 0, st, a));

@@ -76,3 +76,24 @@ def test_forced_wait_timeout_is_reported(monkeypatch):
     ep.score(K, Q)
     ep.check()
     assert np.isfinite(ep.lambda_.cpu().numpy()).all() and np.isfinite(ep.scores.cpu().numpy()).all()
+
+
+def test_forced_wait_timeout_four_block_epilogue(monkeypatch):
+    # units of 32769 to 65536 non-window keys: four blocks per unit exchange sums
+    import paper_2609_06663_amd as P
+    from paper_2609_06663_amd.pipeline import EvictionPass
+    wl = W.custom(42, L=1, Hq=4, Hkv=1, D=128, w=4, seqlens=[40000], dtype="bf16", budget=[4000])
+    shape = P.Shape(wl.L, wl.Hq, wl.Hkv, wl.D, wl.w, wl.cu_seqlens)
+    ep = EvictionPass(shape, wl.budget, P.PER_HEAD, P.Params(), torch.bfloat16)
+    K, Q = dev(wl.K, "bf16"), dev(wl.Q, "bf16")
+    say("four-block epilogue with a spin limit of 0: its waits give up at once")
+    monkeypatch.setenv("ECOKV_SPIN_LIMIT", "0")
+    ep.score(K, Q)
+    with pytest.raises(P.EcoKVError) as e:
+        ep.check()
+    assert e.value.code == P.ETIMEOUT
+    assert np.isnan(ep.lambda_.cpu().numpy()).all() and np.isnan(ep.scores.cpu().numpy()).all()
+    monkeypatch.delenv("ECOKV_SPIN_LIMIT")
+    ep.score(K, Q)
+    ep.check()
+    assert np.isfinite(ep.lambda_.cpu().numpy()).all() and np.isfinite(ep.scores.cpu().numpy()).all()

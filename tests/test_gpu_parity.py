@@ -325,11 +325,12 @@ def test_parameter_variants(variant):
     check_per_head(wl, g, params=p)
 
 
-@pytest.mark.parametrize("seqlens", [[32772], [32773], [100, 32772], [2052, 255]])
+@pytest.mark.parametrize("seqlens", [[32772], [32773], [100, 32772], [2052, 255], [65540], [65541], [32773, 40000, 700]])
 def test_epilogue_unit_bounds(seqlens):
-    # P = 32768 non-window keys is the largest unit the one-launch epilogue takes
-    # (one block, 32 keys per thread); one more key selects the two-launch
-    # epilogue; short units leave most of the block's keys past P
+    # P = 32768 non-window keys is the largest unit the one-launch epilogue
+    # takes in one or two blocks; one more key takes four blocks per unit,
+    # up to P = 65536; one more again selects the two-launch epilogue; short
+    # units leave most of a block's keys past P
     wl = W.custom(24, L=1, Hq=8, Hkv=2, D=128, w=4, seqlens=seqlens, dtype="bf16", group=128)
     say(f"epilogue bounds: sequences {seqlens}")
     g = gpu_pass(wl)
