@@ -115,6 +115,17 @@ def test_stack28_full_size():
     assert np.all(g["lambda_"] <= 1.0 + 1e-6) and np.all(g["lambda_"] > -1e-3)
 
 
+@pytest.mark.parametrize("frac", [0.1, 0.4])
+def test_stack_other_budgets(frac):
+    # the stack's other two per-head budgets, on its first two layers
+    wl = W.stack28(L=2, budget_frac=frac)
+    say(f"stack, 2 layers, budget {frac:.0%} per head ({wl.budget[0]} tokens)")
+    g = gpu_pass(wl)
+    check_all_selections_valid(wl, g)
+    check_compact(wl, g)
+    check_per_head(wl, g)
+
+
 def test_mha64k_full_size():
     wl = W.mha64k()
     say("mha64k: 32 MHA heads, T=65536, bf16, w=8, b=2048 (every unit against the oracle)")
