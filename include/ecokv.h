@@ -22,8 +22,8 @@
  *    never allocates or frees device memory and never synchronises outside
  *    ecokv_stage_times() and ecokv_workspace_status().  Its only process-wide
  *    state is an atomic launch counter (tags that tell one launch's values from
- *    an older one's), a per-device cache of the number of blocks the device
- *    holds at once and the optional stage timer; calls on different streams
+ *    an older one's), per-device caches of the number of blocks of the split
+ *    epilogues the device holds at once and the optional stage timer; calls on different streams
  *    with different workspaces may run concurrently.
  *  - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *    Work is enqueued asynchronously; results are valid once the stream has
