@@ -23,8 +23,8 @@
  *    ecokv_stage_times() and ecokv_workspace_status().  Its only process-wide
  *    state is an atomic launch counter (tags that tell one launch's values from
  *    an older one's), per-device caches of the number of blocks of the split
- *    epilogues the device holds at once and the optional stage timer; calls on different streams
- *    with different workspaces may run concurrently.
+ *    epilogues the device holds at once and the optional stage timer; calls
+ *    on different streams with different workspaces may run concurrently.
  *  - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *    Work is enqueued asynchronously; results are valid once the stream has
  *    been synchronised.
