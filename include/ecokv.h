@@ -176,10 +176,12 @@ int ecokv_workspace_status(void *workspace, void *stream);
  *   workspace, workspace_bytes: device scratch of ecokv_workspace_size bytes,
  *   256-byte aligned.
  * Arithmetic: fp32 accumulation of bf16/fp32 inputs.
- * For sequences of at most 32768 + w tokens the final step runs as pairs of
- * blocks (two per (layer, KV head, sequence)), for sequences of at most
- * 65536 + w tokens as groups of four, that exchange sums once and wait for
- * each other, when the device can hold all of them at once; if one ever
+ * For sequences of at most 65536 + w tokens the final step runs as groups
+ * of 2 to 8 blocks per (layer, KV head, sequence) that exchange sums once and
+ * wait for each other, when the device can hold all of them at once (no
+ * waits when a unit has at most 4096 non-window keys, nor when the device
+ * cannot hold the groups: one block per unit then, or two launches past 32768
+ * keys); if one ever
  * waits for another for seconds (the device taken by other work all that
  * time), that unit's lambda and scores come out NaN and the workspace's status
  * word records it: check with ecokv_workspace_status.  (The environment

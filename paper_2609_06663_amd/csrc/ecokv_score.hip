@@ -1542,9 +1542,10 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
     if (blockIdx.x == 0 && threadIdx.x == 0) epi_write_stats(a, u, k, dst, sd, mu2);
 }
 
-// Epilogue in one launch when a unit's P non-window keys fit one block
-// (SPLIT = 1), two (SPLIT = 2, each with half of the keys; units of up to
-// 32768 keys) or four (SPLIT = 4, units of up to 65536).  Every per-unit
+// Epilogue in one launch: each unit's P non-window keys in SPLIT blocks
+// (1, 2, 4 or 8) of 4096 KVEC keys (KVEC 1, 2, 4 or 8; at most 65536 keys per
+// unit), the host choosing the most blocks the device holds at once (one
+// block of 32768 keys when the caller allows no waits).  Every per-unit
 // reduction is block-local, except that with SPLIT > 1 the parts of a unit
 // exchange their S_div / S_imp sums and extrema once (tagged 64-bit relaxed
 // atomics; the parts are combined in a fixed order, so all compute the same
@@ -1560,8 +1561,9 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
 // the ends of a block's range from memory.
 constexpr int kUThreads = 1024;
 constexpr int kUW = kUThreads / kWave;
-constexpr int kUKeys = kUThreads * 32;  // 32768 keys per unit (one or two blocks)
-constexpr int kEpiSplitMax = 4;         // blocks per unit at most (65536 keys)
+constexpr int kUKeys = kUThreads * 32;  // 32768 keys: one block of the one-launch epilogue at most
+constexpr int kEpiSplitMax = 8;         // blocks per unit at most
+constexpr int kEpiUnitMax = 2 * kUKeys; // keys per unit at most (65536)
 
 // Block sum / min / max whose barriers order LDS only, so that global loads
 // issued before it stay in flight.
@@ -1618,8 +1620,9 @@ __device__ __forceinline__ void epi_tag_store(unsigned long long *p, float v, un
 template <int SPLIT, int KVEC>
 __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
 {
-    static_assert((SPLIT == 1 && KVEC == 8) || (SPLIT == 2 && KVEC == 4) || (SPLIT == 4 && KVEC == 4),
-                  "32768 keys in one or two blocks, 65536 in four");
+    static_assert((SPLIT == 1 || SPLIT == 2 || SPLIT == 4 || SPLIT == 8) &&
+                      (KVEC == 1 || KVEC == 2 || KVEC == 4 || KVEC == 8) && SPLIT * KVEC * 4096 <= kEpiUnitMax,
+                  "1 to 8 blocks of 4096 KVEC keys, at most 65536 keys per unit");
     constexpr int kVec = KVEC;               // chunks (float4 per thread and array)
     constexpr int kWaveKeys = 256 * kVec;    // keys per wave
     constexpr int kPartKeys = kUW * kWaveKeys;
@@ -1966,8 +1969,8 @@ static void launch_sweep(int pass, const ScoreArgs &a, dim3 grid, hipStream_t st
     }
 }
 
-// Blocks of k_epi_unit<SPLIT, 4> that the current device holds at once (cached per device).
-template <int SPLIT>
+// Blocks of k_epi_unit<SPLIT, KVEC> that the current device holds at once (cached per device).
+template <int SPLIT, int KVEC>
 static int64_t epi_split_capacity()
 {
     static int64_t cache[64];
@@ -1976,10 +1979,23 @@ static int64_t epi_split_capacity()
     if (cache[dev] == 0) {
         int ncu = 0, nb = 0;
         if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_epi_unit<SPLIT, 4>, kUThreads, 0) != hipSuccess) return 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_epi_unit<SPLIT, KVEC>, kUThreads, 0) != hipSuccess)
+            return 0;
         cache[dev] = (int64_t)ncu * nb;
     }
     return cache[dev];
+}
+
+// Launches k_epi_unit<SPLIT, KVEC> over U units if its SPLIT U blocks fit the
+// device at once; returns false (nothing launched) otherwise.
+template <int SPLIT, int KVEC>
+static bool try_epi_unit(ScoreArgs &a, char *ws, const WsLayout &lay, int U, hipStream_t st)
+{
+    if ((int64_t)SPLIT * U > epi_split_capacity<SPLIT, KVEC>()) return false;
+    a.epiT = reinterpret_cast<unsigned long long *>(ws + lay.epiT);
+    a.tag = launch_tag();
+    ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL((k_epi_unit<SPLIT, KVEC>), dim3(SPLIT * U), dim3(kUThreads), 0, st, a));
+    return true;
 }
 
 hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hipStream_t st, bool bf16)
@@ -2091,25 +2107,37 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
         a.dq = qa.out;
     }
     const bool epi_one = a.pool_half <= kPoolHalfMax && (maxT + a.rpb2 - 1) / a.rpb2 <= kUThreads && a.D <= kUThreads;
-    if (maxT - a.w <= kUKeys && epi_one) {
-        // two blocks per unit when all of them can be resident at once (their
-        // exchange waits for each other; four per unit measured no faster), else one
-        if (!a.no_wait && 2 * (int64_t)U <= epi_split_capacity<2>()) {
-            a.epiT = reinterpret_cast<unsigned long long *>(ws + lay.epiT);
-            a.tag = launch_tag();
-            ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL((k_epi_unit<2, 4>), dim3(2 * U), dim3(kUThreads), 0, st, a));
-        } else {
-            ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL((k_epi_unit<1, 8>), dim3(U), dim3(kUThreads), 0, st, a));
+    const int64_t maxP = maxT - a.w;
+    if (epi_one && !a.no_wait && maxP <= kEpiUnitMax) {
+        // the one-launch epilogue with the most blocks per unit (each with
+        // 4096, 8192, ... keys) whose blocks can all be resident at once: the
+        // parts exchange sums and wait for each other
+        bool done = false;
+        auto fits = [&](int kvec, int split) { return maxP <= (int64_t)4096 * kvec * split; };
+        if (!done && fits(1, 8)) {
+            if (fits(1, 1)) {
+                ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL((k_epi_unit<1, 1>), dim3(U), dim3(kUThreads), 0, st, a));
+                done = true;
+            } else if (fits(1, 2)) {
+                done = try_epi_unit<2, 1>(a, ws, lay, U, st);
+            }
+            else if (fits(1, 4)) {
+                done = try_epi_unit<4, 1>(a, ws, lay, U, st);
+            } else {
+                done = try_epi_unit<8, 1>(a, ws, lay, U, st);
+            }
         }
-        return hipGetLastError();
+        if (!done && fits(2, 8)) {
+            if (fits(2, 2)) done = try_epi_unit<2, 2>(a, ws, lay, U, st);
+            else if (fits(2, 4)) done = try_epi_unit<4, 2>(a, ws, lay, U, st);
+            else done = try_epi_unit<8, 2>(a, ws, lay, U, st);
+        }
+        if (!done && fits(4, 4)) done = fits(4, 2) ? try_epi_unit<2, 4>(a, ws, lay, U, st) : try_epi_unit<4, 4>(a, ws, lay, U, st);
+        if (done) return hipGetLastError();
     }
-    if (maxT - a.w <= kEpiSplitMax / 2 * kUKeys && epi_one && !a.no_wait &&
-        kEpiSplitMax * (int64_t)U <= epi_split_capacity<kEpiSplitMax>()) {
-        // units of up to 65536 keys: four blocks per unit, all resident at once
-        a.epiT = reinterpret_cast<unsigned long long *>(ws + lay.epiT);
-        a.tag = launch_tag();
-        ECOKV_TIMED("epilogue", st,
-                    hipLaunchKernelGGL((k_epi_unit<kEpiSplitMax, 4>), dim3(kEpiSplitMax * U), dim3(kUThreads), 0, st, a));
+    if (epi_one && maxP <= kUKeys) {
+        // one block per unit, no waits
+        ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL((k_epi_unit<1, 8>), dim3(U), dim3(kUThreads), 0, st, a));
         return hipGetLastError();
     }
     ECOKV_TIMED("epilogue1", st, hipLaunchKernelGGL(k_epi1, grid_e, dim3(kEpiThreads), 0, st, a));

@@ -58,7 +58,8 @@ def test_wrong_types_and_sizes_are_refused():
 def test_forced_wait_timeout_is_reported(monkeypatch):
     import paper_2609_06663_amd as P
     from paper_2609_06663_amd.pipeline import EvictionPass
-    wl = W.custom(41, L=1, Hq=8, Hkv=2, D=128, w=4, seqlens=[3000], dtype="bf16", budget=[300])
+    # 8996 non-window keys: four blocks of 4096 keys per unit, which exchange sums
+    wl = W.custom(41, L=1, Hq=8, Hkv=2, D=128, w=4, seqlens=[9000], dtype="bf16", budget=[900])
     shape = P.Shape(wl.L, wl.Hq, wl.Hkv, wl.D, wl.w, wl.cu_seqlens)
     ep = EvictionPass(shape, wl.budget, P.PER_HEAD, P.Params(), torch.bfloat16)
     K, V, Q = dev(wl.K, "bf16"), dev(wl.V, "bf16"), dev(wl.Q, "bf16")
@@ -78,15 +79,15 @@ def test_forced_wait_timeout_is_reported(monkeypatch):
     assert np.isfinite(ep.lambda_.cpu().numpy()).all() and np.isfinite(ep.scores.cpu().numpy()).all()
 
 
-def test_forced_wait_timeout_four_block_epilogue(monkeypatch):
-    # units of 32769 to 65536 non-window keys: four blocks per unit exchange sums
+def test_forced_wait_timeout_long_units(monkeypatch):
+    # units of 32769 to 65536 non-window keys: eight blocks of 8192 keys per unit exchange sums
     import paper_2609_06663_amd as P
     from paper_2609_06663_amd.pipeline import EvictionPass
     wl = W.custom(42, L=1, Hq=4, Hkv=1, D=128, w=4, seqlens=[40000], dtype="bf16", budget=[4000])
     shape = P.Shape(wl.L, wl.Hq, wl.Hkv, wl.D, wl.w, wl.cu_seqlens)
     ep = EvictionPass(shape, wl.budget, P.PER_HEAD, P.Params(), torch.bfloat16)
     K, Q = dev(wl.K, "bf16"), dev(wl.Q, "bf16")
-    say("four-block epilogue with a spin limit of 0: its waits give up at once")
+    say("eight-block epilogue with a spin limit of 0: its waits give up at once")
     monkeypatch.setenv("ECOKV_SPIN_LIMIT", "0")
     ep.score(K, Q)
     with pytest.raises(P.EcoKVError) as e:

@@ -336,12 +336,14 @@ def test_parameter_variants(variant):
     check_per_head(wl, g, params=p)
 
 
-@pytest.mark.parametrize("seqlens", [[32772], [32773], [100, 32772], [2052, 255], [65540], [65541], [32773, 40000, 700]])
+@pytest.mark.parametrize("seqlens", [[4100], [4101, 4100], [8196, 8197, 30], [16388, 16389], [32772], [32773],
+                                     [100, 32772], [2052, 255], [65540], [65541], [32773, 40000, 700]])
 def test_epilogue_unit_bounds(seqlens):
-    # P = 32768 non-window keys is the largest unit the one-launch epilogue
-    # takes in one or two blocks; one more key takes four blocks per unit,
-    # up to P = 65536; one more again selects the two-launch epilogue; short
-    # units leave most of a block's keys past P
+    # The one-launch epilogue spreads a unit's P non-window keys over 1, 2, 4
+    # or 8 blocks of 4096 keys up to P = 32768, over 8 blocks of 8192 up to
+    # P = 65536, and past that the two-launch epilogue takes over: P at each
+    # boundary and one past it (window w = 4); short units leave most of a
+    # block's keys, or whole blocks, past P
     wl = W.custom(24, L=1, Hq=8, Hkv=2, D=128, w=4, seqlens=seqlens, dtype="bf16", group=128)
     say(f"epilogue bounds: sequences {seqlens}")
     g = gpu_pass(wl)
