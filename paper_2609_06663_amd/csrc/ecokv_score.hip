@@ -1986,12 +1986,14 @@ static int64_t epi_split_capacity()
     return cache[dev];
 }
 
-// Launches k_epi_unit<SPLIT, KVEC> over U units if its SPLIT U blocks fit the
-// device at once; returns false (nothing launched) otherwise.
+// Launches k_epi_unit<SPLIT, KVEC> over U units if its SPLIT U blocks fit
+// the device at once (with half: half of it); returns false (nothing
+// launched) otherwise.
 template <int SPLIT, int KVEC>
-static bool try_epi_unit(ScoreArgs &a, char *ws, const WsLayout &lay, int U, hipStream_t st)
+static bool try_epi_unit(ScoreArgs &a, char *ws, const WsLayout &lay, int U, hipStream_t st, bool half)
 {
-    if ((int64_t)SPLIT * U > epi_split_capacity<SPLIT, KVEC>()) return false;
+    const int64_t cap = epi_split_capacity<SPLIT, KVEC>();
+    if ((int64_t)SPLIT * U > (half ? cap / 2 : cap)) return false;
     a.epiT = reinterpret_cast<unsigned long long *>(ws + lay.epiT);
     a.tag = launch_tag();
     ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL((k_epi_unit<SPLIT, KVEC>), dim3(SPLIT * U), dim3(kUThreads), 0, st, a));
@@ -2109,30 +2111,32 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     const bool epi_one = a.pool_half <= kPoolHalfMax && (maxT + a.rpb2 - 1) / a.rpb2 <= kUThreads && a.D <= kUThreads;
     const int64_t maxP = maxT - a.w;
     if (epi_one && !a.no_wait && maxP <= kEpiUnitMax) {
-        // the one-launch epilogue with the most blocks per unit (each with
-        // 4096, 8192, ... keys) whose blocks can all be resident at once: the
-        // parts exchange sums and wait for each other
+        // The one-launch epilogue with the most blocks per unit (4096 KVEC
+        // keys each, KVEC = 1, 2, 4) whose blocks fill at most half the
+        // device: the parts of a unit wait for each other, and half the
+        // device leaves room for a concurrent call on another stream to be
+        // resident at once too.  Past that, two blocks per unit when the
+        // device holds all of them (a wait across calls is still bounded).
         bool done = false;
         auto fits = [&](int kvec, int split) { return maxP <= (int64_t)4096 * kvec * split; };
+        if (fits(1, 1)) {
+            ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL((k_epi_unit<1, 1>), dim3(U), dim3(kUThreads), 0, st, a));
+            done = true;
+        }
         if (!done && fits(1, 8)) {
-            if (fits(1, 1)) {
-                ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL((k_epi_unit<1, 1>), dim3(U), dim3(kUThreads), 0, st, a));
-                done = true;
-            } else if (fits(1, 2)) {
-                done = try_epi_unit<2, 1>(a, ws, lay, U, st);
-            }
-            else if (fits(1, 4)) {
-                done = try_epi_unit<4, 1>(a, ws, lay, U, st);
-            } else {
-                done = try_epi_unit<8, 1>(a, ws, lay, U, st);
-            }
+            if (fits(1, 2)) done = try_epi_unit<2, 1>(a, ws, lay, U, st, true);
+            else if (fits(1, 4)) done = try_epi_unit<4, 1>(a, ws, lay, U, st, true);
+            else done = try_epi_unit<8, 1>(a, ws, lay, U, st, true);
         }
         if (!done && fits(2, 8)) {
-            if (fits(2, 2)) done = try_epi_unit<2, 2>(a, ws, lay, U, st);
-            else if (fits(2, 4)) done = try_epi_unit<4, 2>(a, ws, lay, U, st);
-            else done = try_epi_unit<8, 2>(a, ws, lay, U, st);
+            if (fits(2, 2)) done = try_epi_unit<2, 2>(a, ws, lay, U, st, true);
+            else if (fits(2, 4)) done = try_epi_unit<4, 2>(a, ws, lay, U, st, true);
+            else done = try_epi_unit<8, 2>(a, ws, lay, U, st, true);
         }
-        if (!done && fits(4, 4)) done = fits(4, 2) ? try_epi_unit<2, 4>(a, ws, lay, U, st) : try_epi_unit<4, 4>(a, ws, lay, U, st);
+        if (!done && fits(4, 4)) {
+            if (fits(4, 2)) done = try_epi_unit<2, 4>(a, ws, lay, U, st, true) || try_epi_unit<2, 4>(a, ws, lay, U, st, false);
+            else done = try_epi_unit<4, 4>(a, ws, lay, U, st, true);
+        }
         if (done) return hipGetLastError();
     }
     if (epi_one && maxP <= kUKeys) {
