@@ -1544,15 +1544,15 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
 
 // Epilogue in one launch: each unit's P non-window keys in SPLIT blocks
 // (1, 2, 4 or 8) of 4096 KVEC keys (KVEC 1, 2, 4 or 8; at most 65536 keys per
-// unit), the host choosing the most blocks the device holds at once (one
-// block of 32768 keys when the caller allows no waits).  Every per-unit
-// reduction is block-local, except that with SPLIT > 1 the parts of a unit
-// exchange their S_div / S_imp sums and extrema once (tagged 64-bit relaxed
-// atomics; the parts are combined in a fixed order, so all compute the same
-// constants).  The wait for the other parts is bounded: if it gives up, the
-// unit's lambda and scores come out NaN and the workspace status word
-// records the launch.  Each key's d_E,
-// khat.mu and attention is read once.  Wave w holds KVEC chunks of 256
+// unit), the host choosing the most blocks per unit that fill at most half
+// the device (else two per unit if it holds them; one block of 32768 keys
+// when the caller allows no waits).  Every per-unit reduction is
+// block-local, except that with SPLIT > 1 the parts of a unit exchange their
+// S_div / S_imp sums and extrema once (tagged 64-bit relaxed atomics; the
+// parts are combined in a fixed order, so all compute the same constants).
+// The wait for the other parts is bounded: if it gives up, the unit's lambda
+// and scores come out NaN and the workspace status word records the launch.
+// Each key's d_E, khat.mu and attention is read once.  Wave w holds KVEC chunks of 256
 // consecutive keys; lane l of chunk j holds keys 256 j + 4 l .. +3 of the
 // wave's range, so each load instruction covers 1 KiB of consecutive keys.
 // The pooling window (up to 4 keys on each side) comes from the neighbouring
