@@ -21,10 +21,10 @@
  *    allocates and owns every buffer (inputs, outputs, workspace).  The library
  *    never allocates or frees device memory and never synchronises outside
  *    ecokv_stage_times() and ecokv_workspace_status().  Its only process-wide
- *    state is an atomic launch counter (tags that tell one launch's values from
- *    an older one's), per-device caches of the number of blocks of the split
+ *    state is per-device caches of the number of blocks of the split
  *    epilogues the device holds at once and the optional stage timer; calls
- *    on different streams with different workspaces may run concurrently.
+ *    on different streams with different workspaces may run concurrently,
+ *    and a call captured in a HIP graph may be replayed.
  *  - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *    Work is enqueued asynchronously; results are valid once the stream has
  *    been synchronised.
@@ -154,7 +154,8 @@ int ecokv_default_params(ecokv_params *p);
  * adds one float per non-window key).  The workspace is scratch, except for
  * its first 4 bytes, a status word (see ecokv_workspace_status) that must be
  * zero before the workspace's first use: allocate it zero-filled, or call
- * ecokv_workspace_status once.  It must not be shared by calls that may
+ * ecokv_workspace_status once; the next 4 bytes count the calls made on it
+ * (any initial value will do).  It must not be shared by calls that may
  * overlap. */
 int ecokv_workspace_size(const ecokv_shape *shape, const ecokv_params *params, size_t *bytes);
 

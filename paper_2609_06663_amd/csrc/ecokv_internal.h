@@ -53,8 +53,8 @@ struct ScoreArgs {
     // word (launch tag << 32 | float bits) so that a reader can tell a value of
     // this launch from anything older without ordering fences
     unsigned long long *epiT;   // [U][4][4]           per-part S_div / S_imp sums and extrema
-    unsigned *status;           // workspace status word: set to the launch tag if a wait ran out of time
-    unsigned tag;               // launch tag (never 0)
+    unsigned *status;           // workspace status word: set to the call's tag if a wait ran out of time
+    unsigned *tagw;             // workspace word: the call's tag (bumped by the second sweep, never 0)
     int spin_limit;             // polls of a bounded wait before it gives up (<= 0: give up at once)
     int no_wait;                // no waits between blocks (the final step one block per unit)
     int L, Hq, Hkv, G, D, w, R, B;
@@ -156,7 +156,7 @@ struct CompactArgs {
 
 // Workspace layout, shared by the size query and the launcher.
 struct WsLayout {
-    size_t status, part1, anchors, part2, part3, bufA, bufB, bufC, bufV, dq, epiT, total;
+    size_t status, tagw, part1, anchors, part2, part3, bufA, bufB, bufC, bufV, dq, epiT, total;
 };
 
 // Order statistics of d_E per unit for the winsorised and MAD normalisations:
@@ -196,7 +196,6 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
 
 // A launch tag (never 0), distinct for every launch of the process: values a
 // launch publishes between its blocks carry it.
-unsigned launch_tag();
 
 // ecokv_prefill_write: workspace bytes, and the launches (a.K = the cache,
 // a.Ksrc = the new rows, a.pre_out = pre; Vsrc / Vdst may be null).

@@ -27,8 +27,6 @@
 #include <stdlib.h>
 #include <string.h>
 
-#include <atomic>
-
 #include "ecokv_fast.h"
 
 namespace ecokv {
@@ -183,9 +181,23 @@ __global__ __launch_bounds__(kThreads) void k_pass1(ScoreArgs a)
     }
 }
 
+// The workspace's exchange tag, bumped once per score call by the second
+// sweep's first block and read by the split epilogue after it, so that every
+// call (every replay of a captured call included) tags its exchanges afresh
+// and never reads an older call's words (0 is skipped: the status word
+// records the tag of a call whose wait gave up).
+__device__ __forceinline__ void bump_call_tag(const ScoreArgs &a)
+{
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+        const unsigned t = *a.tagw + 1u;
+        *a.tagw = t ? t : 1u;
+    }
+}
+
 template <int D, bool BF>
 __global__ __launch_bounds__(kThreads) void k_pass2(ScoreArgs a)
 {
+    bump_call_tag(a);
     constexpr int VEC = D / 16;
     constexpr int ESZ = BF ? 2 : 4;
     __shared__ float q_lds[ECOKV_MAX_ROWS * D];
@@ -598,6 +610,7 @@ __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs1(ScoreArgs a)
 template <int MT>
 __global__ __launch_bounds__(256, MT == 1 ? 2 : 1) void k_fs2(ScoreArgs a)
 {
+    bump_call_tag(a);
     constexpr int kAnc = 32 * MT - 2;  // first anchor row of the A operand
     __shared__ u32x4 kt[kTile * kChunks];
     __shared__ float rowM[32 * MT], rowIS[32 * MT];
@@ -751,6 +764,7 @@ __device__ __forceinline__ void group_load(u32x4 (&b)[8], __amdgpu_buffer_rsrc_t
 template <int KEYS>
 __global__ __launch_bounds__(256, 2) void k_fs2s(ScoreArgs a)
 {
+    bump_call_tag(a);
     constexpr int kS2Groups = KEYS / (32 * kS2Waves);  // 32-key groups per wave
     __shared__ float wred[4][kS2Waves];
     __shared__ u32x4 stage[kS2Waves][32 * kChunks];  // per wave: 32 rows, swizzled 16-byte chunks
@@ -1740,11 +1754,12 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
     if (SPLIT > 1) {
         // exchange with the other parts of the unit: publish, then wait for each (bounded)
         if (threadIdx.x == 0) {
+            const unsigned tag = *a.tagw;  // this call's (bumped by the second sweep)
             unsigned long long *mine = a.epiT + ((int64_t)u * SPLIT + part) * 4;
-            epi_tag_store(mine + 0, sd.s0, a.tag);
-            epi_tag_store(mine + 1, sd.s1, a.tag);
-            epi_tag_store(mine + 2, sd.mn, a.tag);
-            epi_tag_store(mine + 3, sd.mx, a.tag);
+            epi_tag_store(mine + 0, sd.s0, tag);
+            epi_tag_store(mine + 1, sd.s1, tag);
+            epi_tag_store(mine + 2, sd.mn, tag);
+            epi_tag_store(mine + 3, sd.mx, tag);
             Red4 c{0.f, 0.f, INFINITY, -INFINITY};
             bool all_ok = true;
             for (int pp = 0; pp < SPLIT; ++pp) {  // in part order, so every part adds in the same order
@@ -1759,7 +1774,7 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
 #pragma unroll
                         for (int q = 0; q < 4; ++q) {
                             o[q] = __hip_atomic_load(other + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                            ok = ok && (unsigned)(o[q] >> 32) == a.tag;
+                            ok = ok && (unsigned)(o[q] >> 32) == tag;
                         }
                         if (!ok) __builtin_amdgcn_s_sleep(2);
                     }
@@ -1770,7 +1785,7 @@ __global__ __launch_bounds__(kUThreads) void k_epi_unit(ScoreArgs a)
                 c = pp == 0 ? r : Red4{c.s0 + r.s0, c.s1 + r.s1, fminf(c.mn, r.mn), fmaxf(c.mx, r.mx)};
             }
             if (!all_ok) {
-                __hip_atomic_store(a.status, a.tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(a.status, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 c.s0 = NAN;
             }
             lds[kUW] = c;
@@ -1809,15 +1824,6 @@ __global__ void k_status_clear(unsigned *status) { *status = 0u; }
 // Host side
 // ---------------------------------------------------------------------------
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
-
-static std::atomic<unsigned> g_tag{0u};
-
-unsigned launch_tag()
-{
-    unsigned t = ++g_tag;
-    if (t == 0) t = ++g_tag;
-    return t;
-}
 
 hipError_t status_clear(unsigned *status, hipStream_t st)
 {
@@ -1919,7 +1925,9 @@ WsLayout score_ws_layout(int L, int Hkv, int B, int D, int R, int64_t Ptot, int 
     const int64_t nch3 = (maxT + kEpiKeys - 1) / kEpiKeys;
     const int64_t stride = 2 * D + 2 * R;
     size_t o = 0;
-    w.status = o; o = align256(o + sizeof(unsigned));  // first: a fixed offset for the status query
+    w.status = o;  // first: a fixed offset for the status query
+    w.tagw = o + sizeof(unsigned);  // then the call tag (any initial value)
+    o = align256(o + 2 * sizeof(unsigned));
     w.part1 = o; o = align256(o + sizeof(float) * U * nch1 * stride);
     w.anchors = o; o = align256(o + sizeof(float) * U * stride);
     w.part2 = o; o = align256(o + sizeof(float) * U * nch2 * 4);
@@ -1995,7 +2003,6 @@ static bool try_epi_unit(ScoreArgs &a, char *ws, const WsLayout &lay, int U, hip
     const int64_t cap = epi_split_capacity<SPLIT, KVEC>();
     if ((int64_t)SPLIT * U > (half ? cap / 2 : cap)) return false;
     a.epiT = reinterpret_cast<unsigned long long *>(ws + lay.epiT);
-    a.tag = launch_tag();
     ECOKV_TIMED("epilogue", st, hipLaunchKernelGGL((k_epi_unit<SPLIT, KVEC>), dim3(SPLIT * U), dim3(kUThreads), 0, st, a));
     return true;
 }
@@ -2012,6 +2019,7 @@ hipError_t score_launch(ScoreArgs a, char *ws, const WsLayout &lay, int maxT, hi
     a.bufC = reinterpret_cast<float *>(ws + lay.bufC);
     a.nch3 = (maxT + kEpiKeys - 1) / kEpiKeys;
     a.status = reinterpret_cast<unsigned *>(ws + lay.status);
+    a.tagw = reinterpret_cast<unsigned *>(ws + lay.tagw);
     const dim3 grid_e(a.nch3, U);
     hipError_t e;
 

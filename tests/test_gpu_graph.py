@@ -1,0 +1,100 @@
+"""The pass captured in a HIP graph (torch.cuda.CUDAGraph) and replayed on
+changing inputs: every replay must reproduce, bit for bit, the eager pass on
+the same inputs.  The shape makes the epilogue split each unit over several
+blocks that exchange sums, and the selection take its one-block form; the
+no-alloc entry point is captured too.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from parity_utils import dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_06663_amd  # noqa: F401  (fails loudly if the library is not built)
+
+
+def say(msg):
+    print(f"[gpu-graph] {msg}", file=sys.stderr, flush=True)
+
+
+OUTS = ("scores", "lambda_", "stats", "idx", "counts", "offsets")
+
+
+def _inputs(seed):
+    wl = W.custom(seed, L=1, Hq=8, Hkv=2, D=128, w=4, seqlens=[9000, 3000], dtype="bf16", budget=[900, 300])
+    return wl, (dev(wl.K, "bf16"), dev(wl.V, "bf16"), dev(wl.Q, "bf16"))
+
+
+def _snapshot(ep):
+    out = {n: getattr(ep, n).clone() for n in OUTS}
+    out["Kc"] = ep.Kc.view(torch.int16).clone()
+    out["Vc"] = ep.Vc.view(torch.int16).clone()
+    return out
+
+
+def _same(a, b, what):
+    for n in a:
+        assert torch.equal(a[n], b[n]), f"{what}: {n} differs"
+
+
+@pytest.mark.parametrize("noalloc", [False, True])
+def test_graph_replays_match_eager(noalloc):
+    import paper_2609_06663_amd as P
+    from paper_2609_06663_amd.pipeline import EvictionPass
+    wl1, in1 = _inputs(61)
+    wl2, in2 = _inputs(62)
+    shape = P.Shape(wl1.L, wl1.Hq, wl1.Hkv, wl1.D, wl1.w, wl1.cu_seqlens)
+
+    def run(ep, K, V, Q, stream=None):
+        if noalloc:
+            P.ecokv_score_noalloc(K, V, Q, ep.shape, ep.params, None, ep.scores, ep.lambda_, ep.stats, stream)
+            ep.select(stream)
+            ep.compact(K, V, stream)
+        else:
+            ep.run(K, V, Q, stream)
+
+    say(f"eager passes on two inputs (noalloc={noalloc})")
+    ep_e = EvictionPass(shape, wl1.budget, P.PER_HEAD, P.Params(), torch.bfloat16)
+    eager = []
+    for K, V, Q in (in1, in2):
+        run(ep_e, K, V, Q)
+        torch.cuda.synchronize()
+        eager.append(_snapshot(ep_e))
+
+    ep_g = EvictionPass(shape, wl1.budget, P.PER_HEAD, P.Params(), torch.bfloat16)
+    Ks, Vs, Qs = (t.clone() for t in in1)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(2):
+            run(ep_g, Ks, Vs, Qs)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    say("capture")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run(ep_g, Ks, Vs, Qs)
+    torch.cuda.synchronize()
+    for rep, which in enumerate([0, 1, 1, 0, 1, 0]):
+        src = (in1, in2)[which]
+        for dst, s in zip((Ks, Vs, Qs), src):
+            dst.copy_(s)
+        # eager work of the program's own between replays
+        run(ep_e, *src)
+        g.replay()
+        torch.cuda.synchronize()
+        say(f"replay {rep} on input {which + 1}")
+        _same(_snapshot(ep_g), eager[which], f"replay {rep} (input {which + 1})")
+        _same(_snapshot(ep_e), eager[which], f"eager pass beside replay {rep}")
+    if not noalloc:
+        ep_g.check()
