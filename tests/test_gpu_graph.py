@@ -1,8 +1,7 @@
 """The pass captured in a HIP graph (torch.cuda.CUDAGraph) and replayed on
 changing inputs: every replay must reproduce, bit for bit, the eager pass on
-the same inputs.  The shape makes the epilogue split each unit over several
-blocks that exchange sums, and the selection take its one-block form; the
-no-alloc entry point is captured too.
+the same inputs, over shapes that take each selection form and the split
+epilogue; the no-alloc entry point is captured too.
 """
 import sys
 
@@ -30,8 +29,21 @@ def say(msg):
 OUTS = ("scores", "lambda_", "stats", "idx", "counts", "offsets")
 
 
-def _inputs(seed):
-    wl = W.custom(seed, L=1, Hq=8, Hkv=2, D=128, w=4, seqlens=[9000, 3000], dtype="bf16", budget=[900, 300])
+# shape cases: the epilogue split over blocks that exchange sums with a
+# one-block selection; layer-flat groups past 32 Ki keys (the five-launch
+# multi-block selection, whose workspace must end zero-filled after every
+# replay); a long single head with a small budget (the two-stage selection)
+CASES = {
+    "per_head": dict(L=1, Hq=8, Hkv=2, seqlens=[9000, 3000], budget=[900, 300], mode="per_head"),
+    "flat_multiblock": dict(L=1, Hq=8, Hkv=4, seqlens=[12000, 9500], budget=[1800, 1400], mode="layer_flat"),
+    "two_stage": dict(L=1, Hq=4, Hkv=1, seqlens=[40000], budget=[1024], mode="per_head"),
+}
+
+
+def _inputs(seed, case):
+    c = CASES[case]
+    wl = W.custom(seed, L=c["L"], Hq=c["Hq"], Hkv=c["Hkv"], D=128, w=4, seqlens=c["seqlens"], dtype="bf16",
+                  budget=c["budget"], mode=c["mode"])
     return wl, (dev(wl.K, "bf16"), dev(wl.V, "bf16"), dev(wl.Q, "bf16"))
 
 
@@ -47,13 +59,15 @@ def _same(a, b, what):
         assert torch.equal(a[n], b[n]), f"{what}: {n} differs"
 
 
-@pytest.mark.parametrize("noalloc", [False, True])
-def test_graph_replays_match_eager(noalloc):
+@pytest.mark.parametrize("case,noalloc", [("per_head", False), ("per_head", True), ("flat_multiblock", False),
+                                          ("two_stage", False)])
+def test_graph_replays_match_eager(case, noalloc):
     import paper_2609_06663_amd as P
     from paper_2609_06663_amd.pipeline import EvictionPass
-    wl1, in1 = _inputs(61)
-    wl2, in2 = _inputs(62)
+    wl1, in1 = _inputs(61, case)
+    wl2, in2 = _inputs(62, case)
     shape = P.Shape(wl1.L, wl1.Hq, wl1.Hkv, wl1.D, wl1.w, wl1.cu_seqlens)
+    mode = P.LAYER_FLAT if wl1.mode == "layer_flat" else P.PER_HEAD
 
     def run(ep, K, V, Q, stream=None):
         if noalloc:
@@ -63,15 +77,15 @@ def test_graph_replays_match_eager(noalloc):
         else:
             ep.run(K, V, Q, stream)
 
-    say(f"eager passes on two inputs (noalloc={noalloc})")
-    ep_e = EvictionPass(shape, wl1.budget, P.PER_HEAD, P.Params(), torch.bfloat16)
+    say(f"{case}: eager passes on two inputs (noalloc={noalloc})")
+    ep_e = EvictionPass(shape, wl1.budget, mode, P.Params(), torch.bfloat16)
     eager = []
     for K, V, Q in (in1, in2):
         run(ep_e, K, V, Q)
         torch.cuda.synchronize()
         eager.append(_snapshot(ep_e))
 
-    ep_g = EvictionPass(shape, wl1.budget, P.PER_HEAD, P.Params(), torch.bfloat16)
+    ep_g = EvictionPass(shape, wl1.budget, mode, P.Params(), torch.bfloat16)
     Ks, Vs, Qs = (t.clone() for t in in1)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
