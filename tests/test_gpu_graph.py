@@ -112,3 +112,78 @@ def test_graph_replays_match_eager(case, noalloc):
         _same(_snapshot(ep_e), eager[which], f"eager pass beside replay {rep}")
     if not noalloc:
         ep_g.check()
+
+
+def test_graph_replays_read_once_flow():
+    # the prefill's cache write with the first sweep's sums, the pass on them,
+    # then decode attention over the compressed cache: all captured in one graph
+    import paper_2609_06663_amd as P
+    from paper_2609_06663_amd.pipeline import EvictionPass
+    wl1, in1 = _inputs(63, "per_head")
+    wl2, in2 = _inputs(64, "per_head")
+    shape = P.Shape(wl1.L, wl1.Hq, wl1.Hkv, wl1.D, wl1.w, wl1.cu_seqlens)
+    L, Hq, Hkv, D, B, w = wl1.L, wl1.Hq, wl1.Hkv, wl1.D, wl1.B, wl1.w
+    R = Hq // Hkv * w
+    max_count = max(wl1.budget)
+    gen = torch.Generator(device="cuda").manual_seed(65)
+    inputs = []
+    for K, V, Q in (in1, in2):
+        Kn, Vn = K.transpose(1, 2).contiguous(), V.transpose(1, 2).contiguous()  # token-major new rows
+        Qd = torch.randn((L, Hq, B, D), generator=gen, device="cuda").to(torch.bfloat16)
+        inputs.append((Kn, Vn, Q, Qd))
+
+    class Flow:
+        def __init__(self):
+            self.ep = EvictionPass(shape, wl1.budget, P.PER_HEAD, P.Params(), torch.bfloat16)
+            self.Kcache = torch.empty_like(in1[0])
+            self.Vcache = torch.empty_like(in1[1])
+            self.pre = torch.empty(L * Hkv * B * (2 * D + 2 * R), dtype=torch.float32, device="cuda")
+            self.ws_p = torch.zeros(P.ecokv_prefill_workspace_size(shape), dtype=torch.uint8, device="cuda")
+            self.ws_d = torch.zeros(max(P.ecokv_decode_workspace_size(shape, max_count), 256), dtype=torch.uint8,
+                                    device="cuda")
+            self.O = torch.empty((L, Hq, B, D), dtype=torch.float32, device="cuda")
+            self.lse = torch.empty((L, Hq, B), dtype=torch.float32, device="cuda")
+
+        def __call__(self, Kn, Vn, Q, Qd):
+            P.ecokv_prefill_write(Kn, Vn, Q, shape, P.Params(), self.Kcache, self.Vcache, self.pre, self.ws_p)
+            self.ep.run(self.Kcache, self.Vcache, Q, pre=self.pre)
+            P.ecokv_decode(Qd, self.ep.Kc, self.ep.Vc, shape, self.ep.counts, self.ep.offsets, max_count, self.O,
+                           self.lse, self.ws_d)
+
+        def snapshot(self):
+            out = _snapshot(self.ep)
+            out.update(pre=self.pre.clone(), Kcache=self.Kcache.view(torch.int16).clone(),
+                       Vcache=self.Vcache.view(torch.int16).clone(), O=self.O.clone(), lse=self.lse.clone())
+            return out
+
+    say("read-once flow: eager on two inputs")
+    fe = Flow()
+    eager = []
+    for x in inputs:
+        fe(*x)
+        torch.cuda.synchronize()
+        eager.append(fe.snapshot())
+    fg = Flow()
+    static = [t.clone() for t in inputs[0]]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(2):
+            fg(*static)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    say("read-once flow: capture")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fg(*static)
+    torch.cuda.synchronize()
+    for rep, which in enumerate([0, 1, 1, 0, 1]):
+        for dst, s in zip(static, inputs[which]):
+            dst.copy_(s)
+        fe(*inputs[which])
+        g.replay()
+        torch.cuda.synchronize()
+        say(f"read-once flow: replay {rep} on input {which + 1}")
+        _same(fg.snapshot(), eager[which], f"replay {rep} (input {which + 1})")
+        _same(fe.snapshot(), eager[which], f"eager flow beside replay {rep}")
+    fg.ep.check()
