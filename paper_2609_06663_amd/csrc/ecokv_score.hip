@@ -1565,10 +1565,11 @@ __global__ __launch_bounds__(kEpiThreads) void k_epi2(ScoreArgs a)
 // S_div / S_imp sums and extrema once (tagged 64-bit relaxed atomics; the
 // parts are combined in a fixed order, so all compute the same constants).
 // The wait for the other parts is bounded: if it gives up, the unit's lambda
-// and scores come out NaN and the workspace status word records the launch.
-// Each key's d_E, khat.mu and attention is read once.  Wave w holds KVEC chunks of 256
-// consecutive keys; lane l of chunk j holds keys 256 j + 4 l .. +3 of the
-// wave's range, so each load instruction covers 1 KiB of consecutive keys.
+// and scores come out NaN and the workspace status word records the call's
+// tag.  Each key's d_E, khat.mu and attention is read once.  Wave w holds
+// KVEC chunks of 256 consecutive keys; lane l of chunk j holds keys
+// 256 j + 4 l .. +3 of the wave's range, so each load instruction covers
+// 1 KiB of consecutive keys.
 // The pooling window (up to 4 keys on each side) comes from the neighbouring
 // lanes' registers (or the neighbouring chunk's end lane); the wave's
 // outermost neighbours come from the neighbouring waves through LDS, and at
